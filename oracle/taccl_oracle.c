@@ -1,0 +1,867 @@
+/*
+ * CPU oracle for batched evaluation of candidate collective schedules
+ * (TACCL, arXiv 2111.04867).
+ *
+ * TEST INFRASTRUCTURE ONLY. This file is the plain, slow, sequential
+ * definition against which the GPU evaluator is checked. Only the tests,
+ * the smoke check and the CPU-baseline leg of the benchmark may load it.
+ * It shares no code, header, table or constant with the GPU library.
+ *
+ * What it computes, per candidate (a route choice per (chunk, destination)
+ * pair plus one 32-bit priority per send slot):
+ *   1. link cost under the alpha-beta model of Sec. 4.1 (Table 1), in
+ *      integer ns: alpha + ceil(beta_ps_per_byte * chunk_bytes / 1000);
+ *   2. the send set: Allgather chunks are multicast, so the routed paths of
+ *      one chunk are merged into a tree by first reach (destinations in
+ *      ascending rank order); this gives one is_sent per (chunk, link) as in
+ *      the routing encoding of App. B.1. Alltoall chunks follow their path;
+ *   3. the Step-2 ordering heuristic of Sec. 5.1 / App. B.2 as a static
+ *      per-link total order: longest remaining path first, then shortest
+ *      path already travelled, then the candidate's priority, then chunk id;
+ *   4. the exact schedule of App. B.3 with no contiguity (every send carries
+ *      one chunk): send >= start at the source, start = send + lat, and the
+ *      strict per-link order. The least solution of these difference
+ *      constraints is found by a topological sweep (Kahn's algorithm);
+ *   5. the postcondition of App. B (every (chunk, rank) pair it lists holds)
+ *      and the makespan, the objective of App. B.1 (latest finishing send).
+ *
+ * Paths: the sketch of Sec. 3.1 restricts links; routes are limited to
+ * shortest paths in the logical topology (Sec. 5.1, Step 1). Paths are found
+ * here by exhaustive depth-first search with cost pruning and sorted by
+ * (cost, hops, lexicographic vertex sequence).
+ */
+#include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+enum { ORC_ALLGATHER = 0, ORC_ALLTOALL = 1, ORC_EXPLICIT = 2 };
+enum { ORC_SHORTEST_ONLY = 0, ORC_KSHORTEST = 1, ORC_RELAY1 = 2, ORC_HIER_RELAY = 3 };
+
+#define ORC_OK 0
+#define ORC_EINVAL 1
+#define ORC_ELIMIT 2
+#define ORC_ENOMEM 3
+
+typedef struct {
+  int hops;
+  int *link; /* [hops] */
+  int *vert; /* [hops+1] */
+  uint64_t cost;
+} opath;
+
+typedef struct {
+  int n;
+  opath *p;
+} oplist;
+
+typedef struct orc_plan {
+  /* topology (CSR, link id = CSR edge index) */
+  int V, P, E;
+  int *row_ptr, *col, *lsrc, *node;
+  uint32_t *alpha, *beta;
+  /* collective */
+  int kind, cpr, C;
+  uint64_t S;
+  int *owner;    /* [C] */
+  int *post_ptr; /* [C+1] */
+  int *post;     /* ranks that must hold the chunk at the end */
+  /* sketch */
+  uint8_t *allowed, *relay;
+  int max_cross, mode, k;
+  /* derived */
+  uint64_t *cost; /* [E] */
+  oplist *paths;  /* [P*P], by (source rank, destination rank) */
+  int H;          /* longest path in hops */
+  int route_stride, prio_stride;
+  int max_sends;
+  char err[256];
+} orc_plan;
+
+/* ------------------------------------------------------------------ */
+/* paths                                                               */
+/* ------------------------------------------------------------------ */
+
+/* Order of Sec. 5.1's shortest-path restriction, made total:
+ * cost, then hop count, then vertex sequence. */
+static int path_cmp(const opath *a, const opath *b) {
+  if (a->cost != b->cost) return a->cost < b->cost ? -1 : 1;
+  if (a->hops != b->hops) return a->hops < b->hops ? -1 : 1;
+  for (int i = 0; i <= a->hops; i++)
+    if (a->vert[i] != b->vert[i]) return a->vert[i] < b->vert[i] ? -1 : 1;
+  return 0;
+}
+
+static opath path_make(int hops, const int *link, const int *vert, uint64_t cost) {
+  opath p;
+  p.hops = hops;
+  p.cost = cost;
+  p.link = (int *)malloc(sizeof(int) * (hops > 0 ? hops : 1));
+  p.vert = (int *)malloc(sizeof(int) * (hops + 1));
+  if (hops > 0) memcpy(p.link, link, sizeof(int) * hops);
+  memcpy(p.vert, vert, sizeof(int) * (hops + 1));
+  return p;
+}
+
+static void path_free(opath *p) {
+  free(p->link);
+  free(p->vert);
+}
+
+/* k best complete paths found so far, kept sorted */
+typedef struct {
+  int k, n;
+  opath *p;
+} kbest;
+
+static void kbest_offer(kbest *kb, int hops, const int *link, const int *vert, uint64_t cost) {
+  opath cand;
+  cand.hops = hops;
+  cand.cost = cost;
+  cand.link = (int *)link;
+  cand.vert = (int *)vert;
+  if (kb->n == kb->k && path_cmp(&cand, &kb->p[kb->n - 1]) >= 0) return;
+  opath keep = path_make(hops, link, vert, cost);
+  if (kb->n == kb->k) {
+    path_free(&kb->p[kb->n - 1]);
+    kb->n--;
+  }
+  int i = kb->n;
+  while (i > 0 && path_cmp(&keep, &kb->p[i - 1]) < 0) {
+    kb->p[i] = kb->p[i - 1];
+    i--;
+  }
+  kb->p[i] = keep;
+  kb->n++;
+}
+
+typedef struct {
+  const orc_plan *pl;
+  int dst;
+  int max_cross;
+  int *vs, *ls;
+  uint8_t *seen;
+  kbest *kb;
+} dfs_ctx;
+
+/* A link may be used if the sketch allows it; a link between two nodes
+ * counts as a crossing and, when relays are named, must join two relays
+ * (Sec. 3.1, Example 2; App. A internode sketch). */
+static void dfs(dfs_ctx *x, int u, int depth, uint64_t cost, int cross) {
+  const orc_plan *p = x->pl;
+  if (u == x->dst) {
+    kbest_offer(x->kb, depth, x->ls, x->vs, cost);
+    return;
+  }
+  /* every extension adds at least one link of positive cost */
+  if (x->kb->n == x->kb->k && cost >= x->kb->p[x->kb->n - 1].cost) return;
+  for (int e = p->row_ptr[u]; e < p->row_ptr[u + 1]; e++) {
+    if (p->allowed && !p->allowed[e]) continue;
+    int v = p->col[e];
+    if (x->seen[v]) continue;
+    int c2 = cross;
+    if (p->node[u] != p->node[v]) {
+      c2++;
+      if (x->max_cross >= 0 && c2 > x->max_cross) continue;
+      if (p->relay && !(p->relay[u] && p->relay[v])) continue;
+    }
+    x->seen[v] = 1;
+    x->vs[depth + 1] = v;
+    x->ls[depth] = e;
+    dfs(x, v, depth + 1, cost + p->cost[e], c2);
+    x->seen[v] = 0;
+  }
+}
+
+/* the k best simple paths s -> d (fills kb, caller frees) */
+static void k_best_paths(const orc_plan *p, int s, int d, int k, int max_cross, kbest *kb) {
+  kb->k = k;
+  kb->n = 0;
+  kb->p = (opath *)calloc((size_t)k + 1, sizeof(opath));
+  dfs_ctx x;
+  x.pl = p;
+  x.dst = d;
+  x.max_cross = max_cross;
+  x.vs = (int *)calloc((size_t)p->V + 1, sizeof(int));
+  x.ls = (int *)calloc((size_t)p->V + 1, sizeof(int));
+  x.seen = (uint8_t *)calloc((size_t)p->V, 1);
+  x.kb = kb;
+  x.vs[0] = s;
+  x.seen[s] = 1;
+  dfs(&x, s, 0, 0, 0);
+  free(x.vs);
+  free(x.ls);
+  free(x.seen);
+}
+
+/* Join a, one optional link, and b into one path. */
+static int join3(const orc_plan *p, const opath *a, int mid_link, const opath *b, opath *out) {
+  int h = a->hops + (mid_link >= 0 ? 1 : 0) + b->hops;
+  int *ls = (int *)malloc(sizeof(int) * (h > 0 ? h : 1));
+  int *vs = (int *)malloc(sizeof(int) * (h + 1));
+  int n = 0;
+  uint64_t cost = 0;
+  vs[0] = a->vert[0];
+  for (int i = 0; i < a->hops; i++) {
+    ls[n] = a->link[i];
+    vs[n + 1] = a->vert[i + 1];
+    cost += p->cost[a->link[i]];
+    n++;
+  }
+  if (mid_link >= 0) {
+    ls[n] = mid_link;
+    vs[n + 1] = p->col[mid_link];
+    cost += p->cost[mid_link];
+    n++;
+  }
+  for (int i = 0; i < b->hops; i++) {
+    ls[n] = b->link[i];
+    vs[n + 1] = b->vert[i + 1];
+    cost += p->cost[b->link[i]];
+    n++;
+  }
+  *out = path_make(n, ls, vs, cost);
+  free(ls);
+  free(vs);
+  return 0;
+}
+
+static int find_link(const orc_plan *p, int u, int v) {
+  for (int e = p->row_ptr[u]; e < p->row_ptr[u + 1]; e++)
+    if (p->col[e] == v && (!p->allowed || p->allowed[e])) return e;
+  return -1;
+}
+
+static void push_path(oplist *L, opath q) {
+  L->p = (opath *)realloc(L->p, sizeof(opath) * (size_t)(L->n + 1));
+  L->p[L->n++] = q;
+}
+
+/* the single best path s -> d under a crossing limit; 0 if none */
+static int best_path(const orc_plan *p, int s, int d, int max_cross, opath *out) {
+  if (s == d) {
+    int v = s;
+    *out = path_make(0, NULL, &v, 0);
+    return 1;
+  }
+  kbest kb;
+  k_best_paths(p, s, d, 1, max_cross, &kb);
+  int ok = kb.n == 1;
+  if (ok) *out = kb.p[0];
+  free(kb.p);
+  return ok;
+}
+
+static int build_paths(orc_plan *p) {
+  int P = p->P;
+  p->paths = (oplist *)calloc((size_t)P * P, sizeof(oplist));
+  for (int s = 0; s < P; s++) {
+    for (int d = 0; d < P; d++) {
+      if (s == d) continue;
+      oplist *L = &p->paths[s * P + d];
+      if (p->mode == ORC_SHORTEST_ONLY || p->mode == ORC_KSHORTEST) {
+        kbest kb;
+        k_best_paths(p, s, d, p->k, p->max_cross, &kb);
+        for (int i = 0; i < kb.n; i++) {
+          /* "the <=k shortest" keeps only minimal-cost paths */
+          if (p->mode == ORC_SHORTEST_ONLY && kb.p[i].cost != kb.p[0].cost) {
+            path_free(&kb.p[i]);
+            continue;
+          }
+          push_path(L, kb.p[i]);
+        }
+        free(kb.p);
+      } else if (p->mode == ORC_RELAY1) {
+        /* option 0: the best direct path; then one relay rank m, ascending */
+        opath q;
+        if (best_path(p, s, d, p->max_cross, &q)) push_path(L, q);
+        for (int m = 0; m < P; m++) {
+          if (m == s || m == d) continue;
+          if (p->relay && !p->relay[m]) continue;
+          opath a, b, j;
+          if (!best_path(p, s, m, p->max_cross, &a)) continue;
+          if (!best_path(p, m, d, p->max_cross, &b)) {
+            path_free(&a);
+            continue;
+          }
+          join3(p, &a, -1, &b, &j);
+          path_free(&a);
+          path_free(&b);
+          push_path(L, j);
+        }
+      } else if (p->mode == ORC_HIER_RELAY) {
+        if (p->node[s] == p->node[d]) {
+          opath q;
+          if (best_path(p, s, d, 0, &q)) push_path(L, q);
+        } else {
+          /* i-th relay of the source node -> i-th relay of the destination node */
+          int rs[4096], rd[4096], ns = 0, nd = 0;
+          for (int r = 0; r < P; r++) {
+            if (!p->relay || !p->relay[r]) continue;
+            if (p->node[r] == p->node[s] && ns < 4096) rs[ns++] = r;
+            if (p->node[r] == p->node[d] && nd < 4096) rd[nd++] = r;
+          }
+          int nr = ns < nd ? ns : nd;
+          for (int i = 0; i < nr; i++) {
+            int mid = find_link(p, rs[i], rd[i]);
+            if (mid < 0) continue;
+            opath a, b, j;
+            if (!best_path(p, s, rs[i], 0, &a)) continue;
+            if (!best_path(p, rd[i], d, 0, &b)) {
+              path_free(&a);
+              continue;
+            }
+            join3(p, &a, mid, &b, &j);
+            path_free(&a);
+            path_free(&b);
+            push_path(L, j);
+          }
+        }
+      }
+      if (L->n > 255) {
+        snprintf(p->err, sizeof p->err, "more than 255 paths for pair (%d,%d)", s, d);
+        return ORC_ELIMIT;
+      }
+      for (int i = 0; i < L->n; i++) {
+        if (L->p[i].hops > p->H) p->H = L->p[i].hops;
+        /* a path never uses a link twice, so a chunk crosses a link once */
+        for (int a = 0; a < L->p[i].hops; a++)
+          for (int b = a + 1; b < L->p[i].hops; b++)
+            if (L->p[i].link[a] == L->p[i].link[b]) {
+              snprintf(p->err, sizeof p->err, "path reuses a link (pair %d,%d)", s, d);
+              return ORC_EINVAL;
+            }
+      }
+    }
+  }
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------ */
+/* plan                                                                */
+/* ------------------------------------------------------------------ */
+
+void orc_destroy(orc_plan *p) {
+  if (!p) return;
+  if (p->paths) {
+    for (int i = 0; i < p->P * p->P; i++) {
+      for (int j = 0; j < p->paths[i].n; j++) path_free(&p->paths[i].p[j]);
+      free(p->paths[i].p);
+    }
+    free(p->paths);
+  }
+  free(p->row_ptr);
+  free(p->col);
+  free(p->lsrc);
+  free(p->node);
+  free(p->alpha);
+  free(p->beta);
+  free(p->owner);
+  free(p->post_ptr);
+  free(p->post);
+  free(p->allowed);
+  free(p->relay);
+  free(p->cost);
+  free(p);
+}
+
+const char *orc_error(const orc_plan *p) { return p ? p->err : "null plan"; }
+
+/*
+ * Build a plan.
+ *   V, P, row_ptr[V+1], col[E], alpha_ns[E], beta_ps_per_byte[E]: topology,
+ *     vertices [0,P) are ranks, the rest are switch vertices;
+ *   node_of[V] or NULL;
+ *   kind, cpr, chunk_bytes: collective; for ORC_EXPLICIT, C, owner[C],
+ *     post_ptr[C+1], post[] give the pre/postcondition (one owner per chunk);
+ *   allowed[E] or NULL, relay[V] or NULL, max_cross (-1 = no limit),
+ *     mode, k: sketch.
+ */
+int orc_create(int V, int P, const int *row_ptr, const int *col, const uint32_t *alpha,
+               const uint32_t *beta, const int *node_of, int kind, int cpr, uint64_t chunk_bytes,
+               int C_explicit, const int *owner_explicit, const int *post_ptr_explicit,
+               const int *post_explicit, const uint8_t *allowed, const uint8_t *relay,
+               int max_cross, int mode, int k, orc_plan **out) {
+  *out = NULL;
+  orc_plan *p = (orc_plan *)calloc(1, sizeof(orc_plan));
+  if (!p) return ORC_ENOMEM;
+  *out = p;
+  if (V <= 0 || P <= 0 || P > V || !row_ptr || !col || !alpha || !beta) {
+    snprintf(p->err, sizeof p->err, "bad topology arguments");
+    return ORC_EINVAL;
+  }
+  p->V = V;
+  p->P = P;
+  p->E = row_ptr[V];
+  p->row_ptr = (int *)malloc(sizeof(int) * (V + 1));
+  memcpy(p->row_ptr, row_ptr, sizeof(int) * (V + 1));
+  p->col = (int *)malloc(sizeof(int) * (p->E > 0 ? p->E : 1));
+  p->lsrc = (int *)malloc(sizeof(int) * (p->E > 0 ? p->E : 1));
+  p->alpha = (uint32_t *)malloc(sizeof(uint32_t) * (p->E > 0 ? p->E : 1));
+  p->beta = (uint32_t *)malloc(sizeof(uint32_t) * (p->E > 0 ? p->E : 1));
+  p->cost = (uint64_t *)malloc(sizeof(uint64_t) * (p->E > 0 ? p->E : 1));
+  p->node = (int *)calloc((size_t)V, sizeof(int));
+  for (int u = 0; u < V; u++) {
+    if (row_ptr[u + 1] < row_ptr[u]) {
+      snprintf(p->err, sizeof p->err, "row_ptr not monotone");
+      return ORC_EINVAL;
+    }
+    for (int e = row_ptr[u]; e < row_ptr[u + 1]; e++) {
+      if (col[e] < 0 || col[e] >= V || col[e] == u) {
+        snprintf(p->err, sizeof p->err, "bad link %d", e);
+        return ORC_EINVAL;
+      }
+      p->col[e] = col[e];
+      p->lsrc[e] = u;
+    }
+  }
+  memcpy(p->alpha, alpha, sizeof(uint32_t) * p->E);
+  memcpy(p->beta, beta, sizeof(uint32_t) * p->E);
+  if (node_of) memcpy(p->node, node_of, sizeof(int) * V);
+  p->S = chunk_bytes;
+  /* alpha-beta cost of one chunk on one link (Sec. 4.1), integer ns */
+  for (int e = 0; e < p->E; e++) {
+    uint64_t c = (uint64_t)alpha[e] + ((uint64_t)beta[e] * chunk_bytes + 999u) / 1000u;
+    if (c == 0 || c >= (1ull << 32)) {
+      snprintf(p->err, sizeof p->err, "link %d cost out of range", e);
+      return ORC_ELIMIT;
+    }
+    p->cost[e] = c;
+  }
+  /* collective */
+  p->kind = kind;
+  p->cpr = cpr;
+  if (kind == ORC_ALLGATHER) {
+    if (cpr <= 0) return ORC_EINVAL;
+    p->C = P * cpr;
+    p->owner = (int *)malloc(sizeof(int) * p->C);
+    p->post_ptr = (int *)malloc(sizeof(int) * (p->C + 1));
+    p->post = (int *)malloc(sizeof(int) * p->C * P);
+    for (int c = 0; c < p->C; c++) {
+      p->owner[c] = c / cpr;
+      p->post_ptr[c] = c * P;
+      for (int r = 0; r < P; r++) p->post[c * P + r] = r;
+    }
+    p->post_ptr[p->C] = p->C * P;
+  } else if (kind == ORC_ALLTOALL) {
+    if (cpr <= 0) return ORC_EINVAL;
+    p->C = P * P * cpr;
+    p->owner = (int *)malloc(sizeof(int) * p->C);
+    p->post_ptr = (int *)malloc(sizeof(int) * (p->C + 1));
+    p->post = (int *)malloc(sizeof(int) * p->C);
+    for (int c = 0; c < p->C; c++) {
+      int pair = c / cpr;
+      p->owner[c] = pair / P;
+      p->post_ptr[c] = c;
+      p->post[c] = pair % P;
+    }
+    p->post_ptr[p->C] = p->C;
+  } else if (kind == ORC_EXPLICIT) {
+    if (C_explicit <= 0 || !owner_explicit || !post_ptr_explicit || !post_explicit)
+      return ORC_EINVAL;
+    p->C = C_explicit;
+    p->owner = (int *)malloc(sizeof(int) * p->C);
+    p->post_ptr = (int *)malloc(sizeof(int) * (p->C + 1));
+    int np = post_ptr_explicit[p->C];
+    p->post = (int *)malloc(sizeof(int) * (np > 0 ? np : 1));
+    memcpy(p->owner, owner_explicit, sizeof(int) * p->C);
+    memcpy(p->post_ptr, post_ptr_explicit, sizeof(int) * (p->C + 1));
+    memcpy(p->post, post_explicit, sizeof(int) * (np > 0 ? np : 0));
+    for (int c = 0; c < p->C; c++) {
+      if (p->owner[c] < 0 || p->owner[c] >= P) return ORC_EINVAL;
+      for (int j = p->post_ptr[c]; j < p->post_ptr[c + 1]; j++)
+        if (p->post[j] < 0 || p->post[j] >= P) return ORC_EINVAL;
+    }
+  } else {
+    snprintf(p->err, sizeof p->err, "bad collective kind");
+    return ORC_EINVAL;
+  }
+  /* sketch */
+  if (allowed) {
+    p->allowed = (uint8_t *)malloc(p->E > 0 ? p->E : 1);
+    memcpy(p->allowed, allowed, p->E);
+  }
+  if (relay) {
+    p->relay = (uint8_t *)malloc(V);
+    memcpy(p->relay, relay, V);
+  }
+  p->max_cross = max_cross;
+  p->mode = mode;
+  p->k = k;
+  if (mode < 0 || mode > 3 || ((mode == ORC_SHORTEST_ONLY || mode == ORC_KSHORTEST) && k <= 0)) {
+    snprintf(p->err, sizeof p->err, "bad route mode");
+    return ORC_EINVAL;
+  }
+  int rc = build_paths(p);
+  if (rc) return rc;
+  /* layouts: Allgather-like (tree) chunks read route c*P+d and priority
+   * c*V+v; Alltoall chunks read route c and priority c*H+h */
+  if (kind == ORC_ALLTOALL) {
+    p->route_stride = p->C;
+    p->prio_stride = p->C * (p->H > 0 ? p->H : 1);
+    p->max_sends = p->C * p->H;
+  } else {
+    p->route_stride = p->C * P;
+    p->prio_stride = p->C * V;
+    p->max_sends = p->C * (V - 1);
+  }
+  return ORC_OK;
+}
+
+int orc_route_stride(const orc_plan *p) { return p->route_stride; }
+int orc_prio_stride(const orc_plan *p) { return p->prio_stride; }
+int orc_max_hops(const orc_plan *p) { return p->H; }
+int orc_num_chunks(const orc_plan *p) { return p->C; }
+int orc_max_sends(const orc_plan *p) { return p->max_sends; }
+uint64_t orc_link_cost(const orc_plan *p, int e) { return (e >= 0 && e < p->E) ? p->cost[e] : 0; }
+int orc_npaths(const orc_plan *p, int s, int d) {
+  if (s < 0 || d < 0 || s >= p->P || d >= p->P) return 0;
+  return p->paths[s * p->P + d].n;
+}
+/* copies the links of path (s,d,i) into out; returns hop count or -1 */
+int orc_path(const orc_plan *p, int s, int d, int i, int *out_links, int cap) {
+  if (s < 0 || d < 0 || s >= p->P || d >= p->P) return -1;
+  const oplist *L = &p->paths[s * p->P + d];
+  if (i < 0 || i >= L->n) return -1;
+  if (L->p[i].hops > cap) return -1;
+  for (int j = 0; j < L->p[i].hops; j++) out_links[j] = L->p[i].link[j];
+  return L->p[i].hops;
+}
+
+/* number of route options of route entry e (0 for entries no pair uses) */
+int orc_route_options(const orc_plan *p, int e) {
+  if (e < 0 || e >= p->route_stride) return 0;
+  if (p->kind == ORC_ALLTOALL) {
+    int s = p->owner[e], d = p->post[p->post_ptr[e]];
+    return s == d ? 0 : p->paths[s * p->P + d].n;
+  }
+  int c = e / p->P, d = e % p->P, s = p->owner[c];
+  if (d == s) return 0;
+  for (int j = p->post_ptr[c]; j < p->post_ptr[c + 1]; j++)
+    if (p->post[j] == d) return p->paths[s * p->P + d].n;
+  return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* evaluation of one candidate                                         */
+/* ------------------------------------------------------------------ */
+
+typedef struct {
+  int chunk, link, from, to, hop;
+  uint64_t rem, trav;
+  uint32_t prio;
+  int cpred;   /* send that brings the chunk to `from`, or -1 */
+  int lpred;   /* previous send on the same link, or -1 */
+  int pos;     /* position in the link's order */
+  uint64_t start, finish;
+} osend;
+
+static const osend *g_sort_base;
+
+/* Step-2 order (Sec. 5.1): longer remaining path first, then shorter
+ * travelled path, then the priority, then the chunk id. */
+static int send_order_cmp(const void *a, const void *b) {
+  const osend *x = &g_sort_base[*(const int *)a];
+  const osend *y = &g_sort_base[*(const int *)b];
+  if (x->rem != y->rem) return x->rem > y->rem ? -1 : 1;
+  if (x->trav != y->trav) return x->trav < y->trav ? -1 : 1;
+  if (x->prio != y->prio) return x->prio < y->prio ? -1 : 1;
+  if (x->chunk != y->chunk) return x->chunk < y->chunk ? -1 : 1;
+  return 0;
+}
+
+typedef struct {
+  osend *s;
+  int n;
+  int *tree_parent; /* [C*V] link into (c,v), -1 if none */
+  int *send_of;     /* [C*V] send index that brings c into v */
+  uint8_t *present; /* [C*V] */
+  int *idx, *succ_ptr, *succ, *indeg, *queue;
+  uint64_t *dist, *height;
+} oscratch;
+
+static void scratch_init(const orc_plan *p, oscratch *w) {
+  size_t cv = (size_t)p->C * p->V;
+  size_t ms = (size_t)(p->max_sends > 0 ? p->max_sends : 1);
+  w->s = (osend *)malloc(sizeof(osend) * ms);
+  w->tree_parent = (int *)malloc(sizeof(int) * cv);
+  w->send_of = (int *)malloc(sizeof(int) * cv);
+  w->present = (uint8_t *)malloc(cv);
+  w->idx = (int *)malloc(sizeof(int) * ms);
+  w->succ_ptr = (int *)malloc(sizeof(int) * (ms + 1));
+  w->succ = (int *)malloc(sizeof(int) * 2 * ms);
+  w->indeg = (int *)malloc(sizeof(int) * ms);
+  w->queue = (int *)malloc(sizeof(int) * ms);
+  w->dist = (uint64_t *)malloc(sizeof(uint64_t) * p->V);
+  w->height = (uint64_t *)malloc(sizeof(uint64_t) * p->V);
+}
+
+static void scratch_free(oscratch *w) {
+  free(w->s);
+  free(w->tree_parent);
+  free(w->send_of);
+  free(w->present);
+  free(w->idx);
+  free(w->succ_ptr);
+  free(w->succ);
+  free(w->indeg);
+  free(w->queue);
+  free(w->dist);
+  free(w->height);
+}
+
+/* is d one of the ranks chunk c must reach? */
+static int in_post(const orc_plan *p, int c, int d) {
+  for (int j = p->post_ptr[c]; j < p->post_ptr[c + 1]; j++)
+    if (p->post[j] == d) return 1;
+  return 0;
+}
+
+/* Multicast sends of one chunk: walk the routed path of every destination
+ * in ascending rank order and keep the first link that reaches each vertex
+ * (one is_sent per chunk and link, App. B.1; a GPU may forward a chunk it
+ * received once over several links, Sec. 8). Keys follow the resulting tree. */
+static void build_tree_sends(const orc_plan *p, const uint8_t *rt, const uint32_t *pr,
+                             oscratch *w) {
+  int V = p->V, P = p->P;
+  for (int c = 0; c < p->C; c++) {
+    int o = p->owner[c];
+    int *par = &w->tree_parent[(size_t)c * V];
+    uint8_t *pres = &w->present[(size_t)c * V];
+    for (int v = 0; v < V; v++) {
+      par[v] = -1;
+      pres[v] = 0;
+    }
+    pres[o] = 1;
+    for (int d = 0; d < P; d++) {
+      if (d == o || !in_post(p, c, d)) continue;
+      int ch = rt[(size_t)c * P + d];
+      const oplist *L = &p->paths[o * P + d];
+      if (ch >= L->n) continue; /* this pair is left unrouted */
+      const opath *q = &L->p[ch];
+      for (int j = 0; j < q->hops; j++) {
+        int v = q->vert[j + 1];
+        if (!pres[v]) {
+          pres[v] = 1;
+          par[v] = q->link[j];
+        }
+      }
+    }
+    /* distance from the owner along the tree (the path travelled so far) */
+    for (int v = 0; v < V; v++) {
+      uint64_t t = 0;
+      int x = v;
+      if (!pres[v]) {
+        w->dist[v] = 0;
+        continue;
+      }
+      while (x != o) {
+        int l = par[x];
+        t += p->cost[l];
+        x = p->lsrc[l];
+      }
+      w->dist[v] = t;
+    }
+    /* height: longest tree distance from v down to any vertex below it */
+    for (int v = 0; v < V; v++) w->height[v] = 0;
+    for (int v = 0; v < V; v++) {
+      if (!pres[v]) continue;
+      int x = v;
+      while (x != o) {
+        int a = p->lsrc[par[x]];
+        uint64_t h = w->dist[v] - w->dist[a];
+        if (h > w->height[a]) w->height[a] = h;
+        x = a;
+      }
+    }
+    for (int v = 0; v < V; v++) {
+      w->send_of[(size_t)c * V + v] = -1;
+      if (par[v] < 0) continue;
+      osend *s = &w->s[w->n];
+      s->chunk = c;
+      s->link = par[v];
+      s->from = p->lsrc[par[v]];
+      s->to = v;
+      s->hop = -1;
+      s->trav = w->dist[s->from];
+      s->rem = p->cost[par[v]] + w->height[v];
+      s->prio = pr[(size_t)c * V + v];
+      w->send_of[(size_t)c * V + v] = w->n;
+      w->n++;
+    }
+  }
+  for (int i = 0; i < w->n; i++) {
+    osend *s = &w->s[i];
+    s->cpred = (s->from == p->owner[s->chunk]) ? -1 : w->send_of[(size_t)s->chunk * V + s->from];
+  }
+}
+
+/* Alltoall sends: each hop of the chunk's routed path. */
+static void build_path_sends(const orc_plan *p, const uint8_t *rt, const uint32_t *pr,
+                             oscratch *w) {
+  int V = p->V, P = p->P, H = p->H;
+  for (int c = 0; c < p->C; c++) {
+    uint8_t *pres = &w->present[(size_t)c * V];
+    for (int v = 0; v < V; v++) pres[v] = 0;
+    int s0 = p->owner[c], d = p->post[p->post_ptr[c]];
+    pres[s0] = 1;
+    if (s0 == d) continue;
+    int ch = rt[c];
+    const oplist *L = &p->paths[s0 * P + d];
+    if (ch >= L->n) continue; /* unrouted */
+    const opath *q = &L->p[ch];
+    uint64_t total = q->cost, before = 0;
+    for (int j = 0; j < q->hops; j++) {
+      osend *s = &w->s[w->n];
+      s->chunk = c;
+      s->link = q->link[j];
+      s->from = q->vert[j];
+      s->to = q->vert[j + 1];
+      s->hop = j;
+      s->trav = before;
+      s->rem = total - before;
+      s->prio = pr[(size_t)c * H + j];
+      s->cpred = j == 0 ? -1 : w->n - 1;
+      before += p->cost[q->link[j]];
+      w->n++;
+    }
+    pres[d] = 1;
+  }
+}
+
+/* Evaluate one candidate. If detail is non-NULL the sends are copied there
+ * (at most cap of them) and *nsends is set. Returns ORC_OK. */
+static int eval_one(const orc_plan *p, const uint8_t *rt, const uint32_t *pr, oscratch *w,
+                    uint32_t *makespan, uint8_t *valid) {
+  w->n = 0;
+  if (p->kind == ORC_ALLTOALL)
+    build_path_sends(p, rt, pr, w);
+  else
+    build_tree_sends(p, rt, pr, w);
+  int n = w->n;
+  /* per-link total order chunk_order(l) (App. B.2) */
+  for (int i = 0; i < n; i++) w->idx[i] = i;
+  g_sort_base = w->s;
+  /* sort by link first, then by the Step-2 key inside each link */
+  for (int i = 0; i < n; i++) w->s[i].lpred = -1;
+  {
+    /* bucket the send indices by link */
+    int E = p->E;
+    int *cnt = (int *)calloc((size_t)E + 1, sizeof(int));
+    for (int i = 0; i < n; i++) cnt[w->s[i].link + 1]++;
+    for (int e = 0; e < E; e++) cnt[e + 1] += cnt[e];
+    int *fill = (int *)malloc(sizeof(int) * (E > 0 ? E : 1));
+    for (int e = 0; e < E; e++) fill[e] = cnt[e];
+    for (int i = 0; i < n; i++) w->idx[fill[w->s[i].link]++] = i;
+    for (int e = 0; e < E; e++) {
+      int a = cnt[e], b = cnt[e + 1];
+      if (b - a > 1) qsort(&w->idx[a], (size_t)(b - a), sizeof(int), send_order_cmp);
+      for (int j = a; j < b; j++) {
+        w->s[w->idx[j]].pos = j - a;
+        w->s[w->idx[j]].lpred = j > a ? w->idx[j - 1] : -1;
+        if (j > a && send_order_cmp(&w->idx[j - 1], &w->idx[j]) == 0) {
+          free(cnt);
+          free(fill);
+          return ORC_EINVAL; /* two sends of one chunk on one link */
+        }
+      }
+    }
+    free(cnt);
+    free(fill);
+  }
+  /* the difference constraints of App. B.3 without contiguity form a DAG
+   * (chunk edges and link-order edges); sweep it in topological order */
+  for (int i = 0; i <= n; i++) w->succ_ptr[i] = 0;
+  for (int i = 0; i < n; i++) {
+    w->indeg[i] = 0;
+    if (w->s[i].cpred >= 0) {
+      w->succ_ptr[w->s[i].cpred + 1]++;
+      w->indeg[i]++;
+    }
+    if (w->s[i].lpred >= 0) {
+      w->succ_ptr[w->s[i].lpred + 1]++;
+      w->indeg[i]++;
+    }
+  }
+  for (int i = 0; i < n; i++) w->succ_ptr[i + 1] += w->succ_ptr[i];
+  {
+    int *fill = w->queue; /* reuse as a cursor array before the sweep */
+    for (int i = 0; i < n; i++) fill[i] = w->succ_ptr[i];
+    for (int i = 0; i < n; i++) {
+      if (w->s[i].cpred >= 0) w->succ[fill[w->s[i].cpred]++] = i;
+      if (w->s[i].lpred >= 0) w->succ[fill[w->s[i].lpred]++] = i;
+    }
+  }
+  int head = 0, tail = 0;
+  for (int i = 0; i < n; i++)
+    if (w->indeg[i] == 0) w->queue[tail++] = i;
+  uint64_t span = 0;
+  while (head < tail) {
+    int i = w->queue[head++];
+    osend *s = &w->s[i];
+    uint64_t ready = s->cpred >= 0 ? w->s[s->cpred].finish : 0;
+    uint64_t busy = s->lpred >= 0 ? w->s[s->lpred].finish : 0;
+    s->start = ready > busy ? ready : busy;
+    s->finish = s->start + p->cost[s->link];
+    if (s->finish > span) span = s->finish;
+    for (int j = w->succ_ptr[i]; j < w->succ_ptr[i + 1]; j++)
+      if (--w->indeg[w->succ[j]] == 0) w->queue[tail++] = w->succ[j];
+  }
+  if (tail != n) return ORC_EINVAL; /* a cycle: cannot happen under this order */
+  if (span >= (1ull << 32)) return ORC_ELIMIT;
+  /* postcondition: every listed (chunk, rank) pair holds the chunk */
+  int ok = 1;
+  for (int c = 0; c < p->C && ok; c++)
+    for (int j = p->post_ptr[c]; j < p->post_ptr[c + 1]; j++)
+      if (!w->present[(size_t)c * p->V + p->post[j]]) {
+        ok = 0;
+        break;
+      }
+  *makespan = (uint32_t)span;
+  *valid = (uint8_t)ok;
+  return ORC_OK;
+}
+
+/* Evaluate n candidates; routes row stride route_stride bytes, priorities
+ * row stride prio_stride words. */
+int orc_eval(const orc_plan *p, int64_t n, const uint8_t *routes, const uint32_t *prio,
+             uint32_t *makespan, uint8_t *valid) {
+  oscratch w;
+  scratch_init(p, &w);
+  int rc = ORC_OK;
+  for (int64_t i = 0; i < n && rc == ORC_OK; i++)
+    rc = eval_one(p, routes + (size_t)i * p->route_stride, prio + (size_t)i * p->prio_stride, &w,
+                  &makespan[i], &valid[i]);
+  scratch_free(&w);
+  return rc;
+}
+
+/* One candidate with every send reported: chunk, link, from, to, hop,
+ * rem, trav, prio, position in its link's order, start, finish. */
+int orc_eval_detail(const orc_plan *p, const uint8_t *routes, const uint32_t *prio, int cap,
+                    int *nsends, int *chunk, int *link, int *from, int *to, int *hop,
+                    uint64_t *rem, uint64_t *trav, uint32_t *pr, int *pos, uint64_t *start,
+                    uint64_t *finish, uint32_t *makespan, uint8_t *valid) {
+  oscratch w;
+  scratch_init(p, &w);
+  int rc = eval_one(p, routes, prio, &w, makespan, valid);
+  if (rc == ORC_OK) {
+    *nsends = w.n;
+    if (w.n > cap) rc = ORC_ELIMIT;
+    for (int i = 0; i < w.n && i < cap; i++) {
+      chunk[i] = w.s[i].chunk;
+      link[i] = w.s[i].link;
+      from[i] = w.s[i].from;
+      to[i] = w.s[i].to;
+      hop[i] = w.s[i].hop;
+      rem[i] = w.s[i].rem;
+      trav[i] = w.s[i].trav;
+      pr[i] = w.s[i].prio;
+      pos[i] = w.s[i].pos;
+      start[i] = w.s[i].start;
+      finish[i] = w.s[i].finish;
+    }
+  }
+  scratch_free(&w);
+  return rc;
+}

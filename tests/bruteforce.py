@@ -1,0 +1,281 @@
+"""Pure-Python brute force for tiny inputs, independent of the oracle.
+
+Used only to pin the oracle. Each piece is a different formulation of what
+the paper defines, so that a slip in the oracle (a dropped term, a wrong
+index, a reversed order) shows up as a disagreement:
+
+* paths: every sketch-valid simple path up to a hop limit, enumerated
+  without pruning, then sorted by (cost, hops, vertex sequence);
+* multicast tree: the link that first brings chunk c to vertex v is taken
+  from the routed path of the smallest destination whose path contains v
+  (a closed characterisation of the first-reach merge, no sequential walk);
+* keys: the remaining path of a send is the longest root-to-leaf tree path
+  below it, found by enumerating those paths explicitly;
+* times: the least solution of the difference constraints of App. B.3
+  (send >= start at the source, start = send + lat, and for every pair of
+  sends on a link, the later one in the order starts no earlier than the
+  earlier one finishes), by Bellman-Ford style relaxation to a fixpoint;
+* optimum: the best makespan over every permutation of every link's sends.
+"""
+import itertools
+
+
+def link_cost(alpha, beta, chunk_bytes):
+    return int(alpha) + -(-int(beta) * int(chunk_bytes) // 1000)
+
+
+def costs_of(w):
+    return [link_cost(w.alpha_ns[e], w.beta_ps_per_byte[e], w.chunk_bytes) for e in range(w.E)]
+
+
+def out_links(w, u):
+    return [(e, int(w.col[e])) for e in range(int(w.row_ptr[u]), int(w.row_ptr[u + 1]))]
+
+
+def node(w, v):
+    return 0 if w.node_of is None else int(w.node_of[v])
+
+
+def all_simple_paths(w, s, d, hop_limit, max_cross=None):
+    """Every simple path s -> d with at most hop_limit links that respects the
+    sketch (allowed links, crossing limit, relay-only crossings)."""
+    mc = w.max_cross if max_cross is None else max_cross
+    out = []
+
+    def rec(u, verts, links, cross):
+        if u == d:
+            out.append((list(verts), list(links)))
+            return
+        if len(links) == hop_limit:
+            return
+        for e, v in out_links(w, u):
+            if w.allowed is not None and not w.allowed[e]:
+                continue
+            if v in verts:
+                continue
+            c2 = cross
+            if node(w, u) != node(w, v):
+                c2 += 1
+                if mc >= 0 and c2 > mc:
+                    continue
+                if w.relay is not None and not (w.relay[u] and w.relay[v]):
+                    continue
+            verts.append(v)
+            links.append(e)
+            rec(v, verts, links, c2)
+            verts.pop()
+            links.pop()
+
+    rec(s, [s], [], 0)
+    return out
+
+
+def sorted_paths(w, s, d, hop_limit, max_cross=None):
+    cost = costs_of(w)
+    ps = all_simple_paths(w, s, d, hop_limit, max_cross)
+    ps.sort(key=lambda p: (sum(cost[e] for e in p[1]), len(p[1]), p[0]))
+    return ps, cost
+
+
+def path_vertices(w, links, start):
+    vs = [start]
+    for e in links:
+        vs.append(int(w.col[e]))
+    return vs
+
+
+# ----------------------------------------------------------------------------
+# sends of one candidate
+# ----------------------------------------------------------------------------
+
+def tree_sends(w, cost, table, routes, prio, owner, posts):
+    """Multicast chunks. table[(s, d)] = list of link lists."""
+    P, V = w.P, w.V
+    sends = []
+    present = {}
+    for c, o in enumerate(owner):
+        routed = {}
+        for d in sorted(posts[c]):
+            if d == o:
+                continue
+            opts = table.get((o, d), [])
+            ch = int(routes[c * P + d])
+            if ch < len(opts):
+                routed[d] = opts[ch]
+        parent = {}
+        for v in range(V):
+            if v == o:
+                continue
+            holders = [d for d in sorted(routed) if v in path_vertices(w, routed[d], o)[1:]]
+            if holders:
+                dstar = holders[0]
+                links = routed[dstar]
+                vs = path_vertices(w, links, o)
+                parent[v] = links[vs.index(v) - 1]
+        # tree distances by walking to the root
+        src = {v: _src(w, parent[v]) for v in parent}
+
+        def dist(x):
+            t = 0
+            while x != o:
+                t += cost[parent[x]]
+                x = src[x]
+            return t
+
+        children = {}
+        for v in parent:
+            children.setdefault(src[v], []).append(v)
+
+        def leaf_paths(x):
+            """all downward tree paths from x, as lists of links"""
+            res = [[]]
+            for ch in children.get(x, []):
+                for tail in leaf_paths(ch):
+                    res.append([parent[ch]] + tail)
+            return res
+
+        for v in sorted(parent):
+            l = parent[v]
+            u = src[v]
+            longest_below = max(sum(cost[e] for e in p) for p in leaf_paths(v))
+            sends.append(dict(chunk=c, link=l, frm=u, to=v, rem=cost[l] + longest_below,
+                              trav=dist(u), prio=int(prio[c * V + v])))
+        present[c] = {o} | set(parent)
+    return sends, present
+
+
+def _src(w, e):
+    u = 0
+    while not (int(w.row_ptr[u]) <= e < int(w.row_ptr[u + 1])):
+        u += 1
+    return u
+
+
+def path_sends(w, cost, table, routes, prio, owner, dest, H):
+    sends = []
+    present = {}
+    for c, (s, d) in enumerate(zip(owner, dest)):
+        present[c] = {s}
+        if s == d:
+            continue
+        opts = table.get((s, d), [])
+        ch = int(routes[c])
+        if ch >= len(opts):
+            continue
+        links = opts[ch]
+        vs = path_vertices(w, links, s)
+        for h, l in enumerate(links):
+            sends.append(dict(chunk=c, link=l, frm=vs[h], to=vs[h + 1], hop=h,
+                              rem=sum(cost[e] for e in links[h:]),
+                              trav=sum(cost[e] for e in links[:h]),
+                              prio=int(prio[c * H + h])))
+        present[c].add(d)
+    return sends, present
+
+
+def link_orders(sends):
+    """chunk_order per link: the Step-2 heuristic (longest remaining path
+    first, then shortest travelled path) with priority and chunk id last."""
+    by_link = {}
+    for i, s in enumerate(sends):
+        by_link.setdefault(s["link"], []).append(i)
+    for l in by_link:
+        by_link[l].sort(key=lambda i: (-sends[i]["rem"], sends[i]["trav"], sends[i]["prio"],
+                                       sends[i]["chunk"]))
+    return by_link
+
+
+def chunk_pred(sends):
+    """index of the send that delivers the chunk to each send's source."""
+    into = {}
+    for i, s in enumerate(sends):
+        if "hop" in s:
+            into[(s["chunk"], s["hop"] + 1)] = i
+        else:
+            into[(s["chunk"], s["to"])] = i
+    pred = []
+    for s in sends:
+        if "hop" in s:
+            pred.append(into.get((s["chunk"], s["hop"])) if s["hop"] > 0 else None)
+        else:
+            pred.append(into.get((s["chunk"], s["frm"])))
+    return pred
+
+
+def least_schedule(sends, cost, orders):
+    """Least send times satisfying the App. B.3 constraints (no contiguity):
+    send >= arrival at the source; for any two sends a before b on one link,
+    send[b] >= send[a] + lat. Relaxed to a fixpoint."""
+    pred = chunk_pred(sends)
+    t = [0] * len(sends)
+    changed = True
+    rounds = 0
+    while changed:
+        changed = False
+        rounds += 1
+        if rounds > len(sends) + 2:
+            raise RuntimeError("constraint graph has a positive cycle")
+        for i, s in enumerate(sends):
+            lo = 0
+            if pred[i] is not None:
+                p = pred[i]
+                lo = max(lo, t[p] + cost[sends[p]["link"]])
+            if lo > t[i]:
+                t[i] = lo
+                changed = True
+        for l, order in orders.items():
+            for a_pos in range(len(order)):
+                for b_pos in range(a_pos + 1, len(order)):
+                    a, b = order[a_pos], order[b_pos]
+                    need = t[a] + cost[l]
+                    if need > t[b]:
+                        t[b] = need
+                        changed = True
+    finish = [t[i] + cost[s["link"]] for i, s in enumerate(sends)]
+    return t, finish
+
+
+def evaluate(w, table, routes, prio, H=None):
+    """Makespan, valid and per-send detail of one candidate."""
+    cost = costs_of(w)
+    P = w.P
+    if w.kind == 1:  # Alltoall
+        C = P * P * w.chunks_per_rank
+        owner = [(c // w.chunks_per_rank) // P for c in range(C)]
+        dest = [(c // w.chunks_per_rank) % P for c in range(C)]
+        sends, present = path_sends(w, cost, table, routes, prio, owner, dest, H)
+        posts = [[d] for d in dest]
+    else:
+        if w.kind == 0:
+            C = P * w.chunks_per_rank
+            owner = [c // w.chunks_per_rank for c in range(C)]
+            posts = [list(range(P)) for _ in range(C)]
+        else:
+            owner = [int(x) for x in w.owner]
+            posts = [[int(r) for r in w.post[w.post_ptr[c]:w.post_ptr[c + 1]]]
+                     for c in range(len(owner))]
+        sends, present = tree_sends(w, cost, table, routes, prio, owner, posts)
+    orders = link_orders(sends)
+    start, finish = least_schedule(sends, cost, orders)
+    valid = all(r in present[c] for c in range(len(posts)) for r in posts[c])
+    makespan = max(finish) if finish else 0
+    return makespan, int(valid), sends, start, finish, orders
+
+
+def optimum_over_orders(w, sends):
+    """Smallest makespan over every permutation of every link's sends."""
+    cost = costs_of(w)
+    by_link = {}
+    for i, s in enumerate(sends):
+        by_link.setdefault(s["link"], []).append(i)
+    links = sorted(by_link)
+    best = None
+    for perms in itertools.product(*[itertools.permutations(by_link[l]) for l in links]):
+        orders = {l: list(p) for l, p in zip(links, perms)}
+        try:
+            _, finish = least_schedule(sends, cost, orders)
+        except RuntimeError:
+            continue  # an order that contradicts the chunk dependencies
+        m = max(finish) if finish else 0
+        best = m if best is None else min(best, m)
+    return best
