@@ -1,0 +1,157 @@
+"""Benchmark: candidate schedules evaluated per second on one MI355X.
+
+One step = one taccl_eval_batch over the whole batch of the chosen workload
+(route decode, send set, Step-2 keys, per-link order, contention timing,
+postcondition and makespan for every candidate), inputs already resident in
+HBM. Prints one JSON line (rank 0).
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
+DEFAULT_WORKLOAD = "twonode16_ag"
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def time_launches(plan, d_r, d_p, d_m, d_v, steps, warmup):
+    """Per-launch durations (ms) from HIP events on the launch stream, plus
+    the wall time of the whole timed region."""
+    import torch
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        plan.eval_tensors(d_r, d_p, d_m, d_v, stream=stream)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    t0 = time.perf_counter()
+    ev[0].record(stream)
+    for k in range(steps):
+        plan.eval_tensors(d_r, d_p, d_m, d_v, stream=stream)
+        ev[k + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(steps)])
+    return per, wall
+
+
+def setup(name):
+    import torch
+    from paper_2111_04867_amd.binding import Plan
+    from workloads import generate, named
+    w = named(name)
+    plan = Plan.from_workload(w)
+    opts = plan.route_options()
+    t = time.perf_counter()
+    routes, prio = generate(w.seed, 0, w.n_candidates, opts, plan.prio_stride)
+    log(f"[bench] {name}: generated {w.n_candidates} candidates in "
+        f"{time.perf_counter() - t:.2f}s")
+    d_r = torch.from_numpy(routes).cuda()
+    d_p = torch.from_numpy(prio.view(np.int32)).cuda()
+    d_m = torch.empty(w.n_candidates, dtype=torch.int32, device="cuda")
+    d_v = torch.empty(w.n_candidates, dtype=torch.uint8, device="cuda")
+    return w, plan, routes, prio, (d_r, d_p, d_m, d_v)
+
+
+def cpu_baseline(w, routes, prio, budget_s):
+    """The oracle, single-threaded, on a bounded prefix of the same batch."""
+    from oracle import OraclePlan
+    ref = OraclePlan.from_workload(w)
+    n_done, t_used, step = 0, 0.0, 1
+    while n_done < w.n_candidates and t_used < budget_s:
+        n = min(step, w.n_candidates - n_done)
+        t = time.perf_counter()
+        ref.eval(routes[n_done:n_done + n], prio[n_done:n_done + n])
+        t_used += time.perf_counter() - t
+        n_done += n
+        step = min(step * 2, 4096)
+    return {"value": n_done / t_used, "unit": "candidates/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {n_done} of {w.n_candidates} {w.name} candidates "
+                      f"({t_used:.1f} s, one thread)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-all", action="store_true", help="skip the per-workload table")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("this evaluator runs on one GPU; candidates shard trivially across GPUs but no "
+              "multi-GPU run is implemented (use --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    from workloads import ORDER
+
+    w, plan, routes, prio, bufs = setup(args.workload)
+    per, wall = time_launches(plan, *bufs, args.steps, args.warmup)
+    n = w.n_candidates
+    total_s = per.sum() / 1e3
+    value = n * args.steps / total_s
+    bytes_launch = n * plan.bytes_per_candidate
+    avg_s = per.mean() / 1e3
+    achieved = bytes_launch / avg_s / 1e9
+    rec = {
+        "metric": "candidate schedules evaluated/sec (alpha-beta timing + postcondition)",
+        "value": value,
+        "unit": "candidates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": per.mean(),
+        "ms_per_step_p10_p50_p90": [float(np.percentile(per, q)) for q in (10, 50, 90)],
+        "wall_s_timed_region": wall,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32",
+        "data": "synthetic (seeded SplitMix64 routes and priorities)",
+        "config": {"workload": w.name, "candidates": n, "ranks": w.P, "vertices": w.V,
+                   "links": w.E, "chunks": plan.num_chunks,
+                   "collective": ["allgather", "alltoall", "explicit"][w.kind],
+                   "chunk_bytes": w.chunk_bytes, "bytes_per_candidate":
+                       plan.bytes_per_candidate, "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None},
+    }
+    if not args.no_all:
+        table = {}
+        for name in ORDER:
+            if name == args.workload:
+                wl, pl, pr_ = w, plan, per
+            else:
+                wl, pl, _, _, b2 = setup(name)
+                pr_, _ = time_launches(pl, *b2, max(10, args.steps // 2), args.warmup)
+                del b2
+            a_s = pr_.mean() / 1e3
+            gbs = wl.n_candidates * pl.bytes_per_candidate / a_s / 1e9
+            table[name] = {"candidates": wl.n_candidates, "ms_per_launch": pr_.mean(),
+                           "candidates_per_s": wl.n_candidates / a_s, "achieved_GBs": gbs,
+                           "hbm_roofline_frac": gbs / HBM_PEAK_GBS}
+            log(f"[bench] {name}: {table[name]['candidates_per_s']:.3e} cand/s, "
+                f"{gbs:.1f} GB/s ({100 * gbs / HBM_PEAK_GBS:.2f}% of HBM)")
+        rec["all_workloads"] = table
+    if not args.no_cpu:
+        rec["cpu_baseline"] = cpu_baseline(w, routes, prio, args.cpu_seconds)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,218 @@
+/*
+ * taccl.h - C ABI of the MI355X evaluator of candidate collective schedules
+ * (TACCL: Guiding Collective Algorithm Synthesis using Communication
+ * Sketches, arXiv 2111.04867).
+ *
+ * The library evaluates, for many candidates at once, the part of TACCL's
+ * synthesizer that follows routing: given one route per (chunk, destination)
+ * pair through a sketch-restricted topology, it
+ *   - orders the sends on every link with the Step-2 heuristic (Sec. 5.1,
+ *     App. B.2): longest remaining path first, then shortest path already
+ *     travelled, then a per-send 32-bit priority, then chunk id;
+ *   - times every send under the alpha-beta model (Sec. 4.1) with strict
+ *     per-link bandwidth and no contiguity (App. B.3 with every send carrying
+ *     one chunk), in integer nanoseconds;
+ *   - checks the collective's postcondition (App. B) and returns the
+ *     makespan (the objective of App. B.1).
+ *
+ * Conventions
+ *   - All functions return a taccl_status_t; on failure a message is kept per
+ *     thread and returned by taccl_last_error().
+ *   - Handles are opaque. create/apply deep-copy every host array they are
+ *     given; the caller may free its arrays when the call returns.
+ *   - Handles are immutable once built and may be used from several threads
+ *     and streams at once. Each destroy function accepts NULL.
+ *   - Device arrays passed to taccl_eval_batch belong to the caller.
+ *   - Nothing here allocates device memory except the first evaluation of a
+ *     plan on a device (or taccl_plan_upload), which uploads the plan's
+ *     read-only tables to that device once; they are freed by
+ *     taccl_plan_destroy.
+ */
+#ifndef TACCL_H
+#define TACCL_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TACCL_OK = 0,
+  TACCL_ERR_INVALID_ARGUMENT = 1, /* null/negative/out-of-range argument */
+  TACCL_ERR_UNSUPPORTED = 2,      /* valid input the evaluator cannot handle */
+  TACCL_ERR_LIMIT = 3,            /* an integer width would overflow */
+  TACCL_ERR_NO_MEMORY = 4,        /* host or device allocation failed */
+  TACCL_ERR_HIP = 5               /* a HIP runtime call failed */
+} taccl_status_t;
+
+/* Collectives (App. B: pre- and postcondition as (chunk, rank) pairs). */
+typedef enum {
+  /* chunk c = r*chunks_per_rank + j starts at rank r, must reach every rank */
+  TACCL_ALLGATHER = 0,
+  /* chunk c = (s*P + d)*chunks_per_rank + j starts at s, must reach d */
+  TACCL_ALLTOALL = 1,
+  /* one owner per chunk and an explicit list of ranks to reach (multicast) */
+  TACCL_EXPLICIT = 2
+} taccl_kind_t;
+
+/* How the candidate route options of a (source, destination) pair are
+ * built from the logical topology (Sec. 3.1, Sec. 5.1 Step 1). Paths are
+ * ordered by (cost, hops, lexicographic vertex sequence). */
+typedef enum {
+  TACCL_ROUTE_SHORTEST_ONLY = 0, /* minimal-cost simple paths, at most k */
+  TACCL_ROUTE_KSHORTEST = 1,     /* the first k simple paths */
+  TACCL_ROUTE_RELAY1 = 2,        /* best path, then best(s,m)+best(m,d) for
+                                    relay ranks m (ascending, m != s,d) */
+  TACCL_ROUTE_HIER_RELAY = 3     /* same node: best path; other node: for the
+                                    i-th relay R_i of each node,
+                                    best(s,R_i) + link(R_i,R'_i) + best(R'_i,d) */
+} taccl_route_mode_t;
+
+typedef struct taccl_topology *taccl_topology_t;
+typedef struct taccl_collective *taccl_collective_t;
+typedef struct taccl_plan *taccl_plan_t;
+
+/* A hipStream_t, passed as an opaque pointer (NULL = the null stream). */
+typedef void *taccl_stream_t;
+
+/*
+ * Physical topology (Sec. 4; alpha and beta per link, Table 1).
+ *   num_vertices V: vertices [0, num_ranks) are GPU ranks, the rest are
+ *     switch vertices (a store-and-forward switch with one link per port);
+ *   row_ptr[V+1], col[E]: directed links in CSR form; link id = CSR index;
+ *     no self loops, no duplicate (u, v);
+ *   alpha_ns[E]: latency in ns; beta_ps_per_byte[E]: inverse bandwidth in
+ *     ps per byte (= us per MB with MB = 10^6 B);
+ *   node_of_vertex[V]: machine of every vertex, or NULL (all on one node).
+ * Errors: INVALID_ARGUMENT for malformed CSR, LIMIT for more than 65535
+ * links or vertices.
+ */
+taccl_status_t taccl_topology_create(int32_t num_vertices, int32_t num_ranks,
+                                     const int32_t *row_ptr, const int32_t *col,
+                                     const uint32_t *alpha_ns, const uint32_t *beta_ps_per_byte,
+                                     const int32_t *node_of_vertex, taccl_topology_t *out);
+void taccl_topology_destroy(taccl_topology_t topo);
+
+/*
+ * Allgather or Alltoall over num_ranks ranks with chunks_per_rank chunks
+ * per rank (Allgather) or per ordered rank pair (Alltoall), each
+ * chunk_bytes long (Sec. 5.2, buffer size and chunk partitioning).
+ */
+taccl_status_t taccl_collective_create(taccl_kind_t kind, int32_t num_ranks,
+                                       int32_t chunks_per_rank, uint64_t chunk_bytes,
+                                       taccl_collective_t *out);
+
+/*
+ * Explicit multicast collective: chunk c starts at owner[c] and must reach
+ * every rank in post[post_ptr[c] .. post_ptr[c+1]) (App. B). Evaluated like
+ * Allgather (routes merge into one tree per chunk).
+ */
+taccl_status_t taccl_collective_create_explicit(int32_t num_chunks, int32_t num_ranks,
+                                                uint64_t chunk_bytes, const int32_t *owner,
+                                                const int32_t *post_ptr, const int32_t *post,
+                                                taccl_collective_t *out);
+void taccl_collective_destroy(taccl_collective_t coll);
+
+/*
+ * Communication sketch (Sec. 3, App. A) reduced to what routing needs.
+ *   allowed_link[E]: 1 = the link is in the logical topology, or NULL;
+ *   is_relay[V]: ranks allowed to send or receive across nodes (and the
+ *     relay set of RELAY1 / HIER_RELAY), or NULL (every rank);
+ *   max_node_crossings: node-boundary crossings allowed per path, -1 = any.
+ *     With 1, a path between nodes crosses exactly once and a path inside a
+ *     node never leaves it (App. B.1, inter-node constraint);
+ *   route_mode, k: see taccl_route_mode_t.
+ */
+typedef struct {
+  const uint8_t *allowed_link;
+  const uint8_t *is_relay;
+  int32_t max_node_crossings;
+  int32_t route_mode;
+  int32_t k;
+} taccl_sketch_desc_t;
+
+/*
+ * Build an evaluation plan: link costs alpha + ceil(beta*chunk_bytes/1000)
+ * ns, route options per pair, layouts and the per-level tables the kernels
+ * read. Host only; device tables are uploaded on first use.
+ * Errors: INVALID_ARGUMENT (mismatched ranks, bad mode), LIMIT (a link cost
+ * or the worst-case makespan does not fit 32 bits, more than 255 options
+ * per pair), UNSUPPORTED (sizes beyond what the kernels hold on chip).
+ */
+taccl_status_t taccl_sketch_apply(taccl_topology_t topo, taccl_collective_t coll,
+                                  const taccl_sketch_desc_t *sketch, taccl_plan_t *out);
+void taccl_plan_destroy(taccl_plan_t plan);
+
+typedef struct {
+  int32_t num_vertices, num_ranks, num_links, num_chunks;
+  int32_t kind;         /* taccl_kind_t */
+  int32_t route_stride; /* bytes of routes per candidate */
+  int32_t prio_stride;  /* uint32 priorities per candidate */
+  int32_t max_hops;     /* longest route option, in links */
+  int32_t max_paths;    /* most route options of any pair */
+  int32_t num_pairs;    /* route entries that carry a choice */
+  int32_t num_levels;   /* Alltoall: distinct remaining-path costs */
+  int64_t max_sends;    /* most sends one candidate can have */
+  uint64_t bytes_per_candidate; /* routes + priorities + 5 output bytes */
+  int32_t num_classes;  /* Alltoall: (level, link, travelled) send classes */
+  int32_t lds_bytes;    /* on-chip memory one evaluating block needs */
+} taccl_plan_info_t;
+
+/*
+ * Candidate layout, per candidate i (rows are contiguous):
+ *   routes[i*route_stride + e], uint8: route option chosen for entry e.
+ *     Allgather/explicit: e = c*P + d (chunk c to rank d); Alltoall: e = c.
+ *     A value >= the entry's option count leaves the pair unrouted, which
+ *     is not an error (the candidate may then fail its postcondition).
+ *   prio[i*prio_stride + q], uint32: tie-break priority of send slot q.
+ *     Allgather/explicit: q = c*V + v (the send that brings c into v);
+ *     Alltoall: q = c*max_hops + h (hop h of chunk c's path).
+ */
+taccl_status_t taccl_plan_info(taccl_plan_t plan, taccl_plan_info_t *out);
+
+/* options[route_stride]: number of route options of every route entry
+ * (0 for entries no pair uses). */
+taccl_status_t taccl_plan_route_options(taccl_plan_t plan, int32_t *options);
+
+/* Links of option `index` of pair (src, dst), hop order, into links[cap];
+ * *hops = its length. INVALID_ARGUMENT if the option does not exist. */
+taccl_status_t taccl_plan_path(taccl_plan_t plan, int32_t src, int32_t dst, int32_t index,
+                               int32_t *links, int32_t cap, int32_t *hops);
+
+/* cost_ns[num_links]: integer alpha-beta cost of one chunk on every link. */
+taccl_status_t taccl_plan_link_costs(taccl_plan_t plan, uint32_t *cost_ns);
+
+/* Upload the plan's read-only tables to the current device now (otherwise
+ * done by the first taccl_eval_batch on that device). Allocates. */
+taccl_status_t taccl_plan_upload(taccl_plan_t plan);
+
+/*
+ * Evaluate n candidates on the current device, asynchronously on `stream`.
+ *   d_routes: device, n*route_stride bytes;
+ *   d_prio: device, n*prio_stride uint32, 4-byte aligned;
+ *   d_makespan: device, n uint32: latest finish over all sends in ns (0 if
+ *     the candidate sends nothing);
+ *   d_valid: device, n uint8: 1 if every (chunk, rank) pair of the
+ *     postcondition holds at the end, else 0.
+ * Each candidate is evaluated independently; results are exact (integer).
+ * Errors (synchronous): INVALID_ARGUMENT for null pointers with n > 0,
+ * n < 0 or a misaligned d_prio; HIP if the plan upload or the launch fails.
+ * Faults inside the kernel surface at the caller's next synchronisation.
+ * n == 0 is a no-op.
+ */
+taccl_status_t taccl_eval_batch(taccl_plan_t plan, int64_t n, const uint8_t *d_routes,
+                                const uint32_t *d_prio, uint32_t *d_makespan, uint8_t *d_valid,
+                                taccl_stream_t stream);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char *taccl_last_error(void);
+
+/* Library version: major*10000 + minor*100 + patch. */
+int32_t taccl_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TACCL_H */

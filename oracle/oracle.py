@@ -154,6 +154,22 @@ class OraclePlan:
             raise OracleError(f"orc_eval failed ({rc})")
         return mk, ok
 
+    def eval_threads(self, routes, prio, threads=None):
+        """eval() split over threads on disjoint candidate ranges (the C call
+        releases the GIL; each call has its own scratch)."""
+        from concurrent.futures import ThreadPoolExecutor
+        routes = np.ascontiguousarray(routes, dtype=np.uint8).reshape(-1, self.route_stride)
+        prio = np.ascontiguousarray(prio, dtype=np.uint32).reshape(-1, self.prio_stride)
+        n = routes.shape[0]
+        threads = threads or min(16, os.cpu_count() or 1)
+        if n < 2 * threads:
+            return self.eval(routes, prio)
+        bounds = np.linspace(0, n, threads + 1).astype(int)
+        with ThreadPoolExecutor(threads) as ex:
+            parts = list(ex.map(lambda ab: self.eval(routes[ab[0]:ab[1]], prio[ab[0]:ab[1]]),
+                                zip(bounds[:-1], bounds[1:])))
+        return np.concatenate([p[0] for p in parts]), np.concatenate([p[1] for p in parts])
+
     def eval_detail(self, routes, prio):
         """One candidate; returns (makespan, valid, sends) where sends is a
         dict of per-send arrays."""

@@ -556,7 +556,7 @@ typedef struct {
   uint64_t start, finish;
 } osend;
 
-static const osend *g_sort_base;
+static _Thread_local const osend *g_sort_base;
 
 /* Step-2 order (Sec. 5.1): longer remaining path first, then shorter
  * travelled path, then the priority, then the chunk id. */

@@ -1,0 +1,179 @@
+// C ABI: plan upload and batched evaluation.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <vector>
+
+#include "kernels.h"
+#include "plan.h"
+
+namespace taccl {
+namespace {
+
+struct Packer {
+  std::vector<unsigned char> bytes;
+  template <class T>
+  size_t add(const std::vector<T> &v) {
+    size_t off = (bytes.size() + 255) & ~size_t(255);
+    bytes.resize(off + std::max<size_t>(v.size() * sizeof(T), 1), 0);
+    if (!v.empty()) std::memcpy(bytes.data() + off, v.data(), v.size() * sizeof(T));
+    return off;
+  }
+};
+
+taccl_status_t hip_fail(hipError_t e, const char *what) {
+  return fail(TACCL_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// Upload the read-only tables of `p` to the current device (once).
+taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  std::lock_guard<std::mutex> lock(p->mu);
+  auto it = p->dev.find(dev);
+  if (it != p->dev.end()) {
+    *out = &it->second;
+    return TACCL_OK;
+  }
+  hipDeviceProp_t prop;
+  e = hipGetDeviceProperties(&prop, dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
+  Packer pk;
+  size_t o_cost = pk.add(p->cost), o_lsrc = pk.add(p->lsrc), o_ldst = pk.add(p->ldst),
+         o_pb = pk.add(p->pair_base), o_np = pk.add(p->npaths), o_po = pk.add(p->path_off),
+         o_pl = pk.add(p->path_links), o_own = pk.add(p->coll.owner),
+         o_pm = pk.add(p->post_mask), o_hc = pk.add(p->hop_class),
+         o_plh = pk.add(p->path_lvl_hop), o_lcb = pk.add(p->lvl_cls_begin),
+         o_llc = pk.add(p->llc);
+  void *blk = nullptr;
+  e = hipMalloc(&blk, pk.bytes.size());
+  if (e != hipSuccess) return fail(TACCL_ERR_NO_MEMORY, "hipMalloc of plan tables failed");
+  e = hipMemcpy(blk, pk.bytes.data(), pk.bytes.size(), hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(blk);
+    return hip_fail(e, "hipMemcpy of plan tables");
+  }
+  DeviceTables t;
+  auto at = [&](size_t off) { return (const unsigned char *)blk + off; };
+  t.block = blk;
+  t.cost = (const uint32_t *)at(o_cost);
+  t.lsrc = (const uint16_t *)at(o_lsrc);
+  t.ldst = (const uint16_t *)at(o_ldst);
+  t.pair_base = (const uint32_t *)at(o_pb);
+  t.npaths = (const uint8_t *)at(o_np);
+  t.path_off = (const uint32_t *)at(o_po);
+  t.path_links = (const uint16_t *)at(o_pl);
+  t.owner = (const int32_t *)at(o_own);
+  t.post_mask = (const uint64_t *)at(o_pm);
+  t.hop_class = (const uint16_t *)at(o_hc);
+  t.path_lvl_hop = (const int8_t *)at(o_plh);
+  t.lvl_cls_begin = (const uint32_t *)at(o_lcb);
+  t.llc = (const uint32_t *)at(o_llc);
+  t.max_lds = (int)prop.sharedMemPerBlock;
+  t.num_cus = prop.multiProcessorCount;
+  *out = &(p->dev[dev] = t);
+  return TACCL_OK;
+}
+
+}  // namespace
+}  // namespace taccl
+
+using namespace taccl;
+
+extern "C" {
+
+void taccl_plan_destroy(taccl_plan_t p) {
+  if (!p) return;
+  int cur = -1;
+  (void)hipGetDevice(&cur);
+  for (auto &kv : p->dev) {
+    if (hipSetDevice(kv.first) == hipSuccess) (void)hipFree(kv.second.block);
+  }
+  if (cur >= 0) (void)hipSetDevice(cur);
+  delete p;
+}
+
+taccl_status_t taccl_plan_upload(taccl_plan_t p) {
+  if (!p) return fail(TACCL_ERR_INVALID_ARGUMENT, "null plan");
+  DeviceTables *t = nullptr;
+  return ensure_device(p, &t);
+}
+
+taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_routes,
+                                const uint32_t *d_prio, uint32_t *d_makespan, uint8_t *d_valid,
+                                taccl_stream_t stream) {
+  if (!p) return fail(TACCL_ERR_INVALID_ARGUMENT, "null plan");
+  if (n < 0) return fail(TACCL_ERR_INVALID_ARGUMENT, "negative candidate count");
+  if (n == 0) return TACCL_OK;
+  if (!d_routes || !d_prio || !d_makespan || !d_valid)
+    return fail(TACCL_ERR_INVALID_ARGUMENT, "null device pointer");
+  if (((uintptr_t)d_prio & 3) || ((uintptr_t)d_makespan & 3))
+    return fail(TACCL_ERR_INVALID_ARGUMENT, "d_prio and d_makespan must be 4-byte aligned");
+  DeviceTables *t = nullptr;
+  taccl_status_t st = ensure_device(p, &t);
+  if (st) return st;
+  hipStream_t s = (hipStream_t)stream;
+  // enough blocks to fill every CU several times over; each block loops
+  const int64_t cap = (int64_t)std::max(t->num_cus, 1) * 64;
+  const int grid = (int)std::min<int64_t>(n, cap);
+  hipError_t e;
+  if (p->coll.kind == TACCL_ALLTOALL) {
+    PathArgs a{};
+    a.C = p->coll.C;
+    a.P = p->topo.P;
+    a.E = p->topo.E;
+    a.H = std::max(p->H, 1);
+    a.cpr = p->coll.cpr;
+    a.nlev = p->nlev;
+    a.route_stride = p->route_stride;
+    a.prio_stride = p->prio_stride;
+    a.cost = t->cost;
+    a.pair_base = t->pair_base;
+    a.npaths = t->npaths;
+    a.path_off = t->path_off;
+    a.hop_class = t->hop_class;
+    a.path_lvl_hop = t->path_lvl_hop;
+    a.lvl_cls_begin = t->lvl_cls_begin;
+    a.llc = t->llc;
+    a.routes = d_routes;
+    a.prio = d_prio;
+    a.makespan = d_makespan;
+    a.valid = d_valid;
+    a.n = n;
+    if (path_layout(*p, a) > t->max_lds)
+      return fail(TACCL_ERR_UNSUPPORTED, "Alltoall plan needs more LDS than a block has");
+    e = launch_path(a, grid, s);
+  } else {
+    TreeArgs a{};
+    a.C = p->coll.C;
+    a.P = p->topo.P;
+    a.V = p->topo.V;
+    a.E = p->topo.E;
+    a.cpr = p->coll.kind == TACCL_ALLGATHER ? p->coll.cpr : 0;
+    a.route_stride = p->route_stride;
+    a.prio_stride = p->prio_stride;
+    a.cost = t->cost;
+    a.lsrc = t->lsrc;
+    a.ldst = t->ldst;
+    a.pair_base = t->pair_base;
+    a.npaths = t->npaths;
+    a.path_off = t->path_off;
+    a.path_links = t->path_links;
+    a.owner = t->owner;
+    a.post_mask = t->post_mask;
+    a.routes = d_routes;
+    a.prio = d_prio;
+    a.makespan = d_makespan;
+    a.valid = d_valid;
+    a.n = n;
+    if (tree_layout(*p, a) > t->max_lds)
+      return fail(TACCL_ERR_UNSUPPORTED, "multicast plan needs more LDS than a block has");
+    e = launch_tree(a, grid, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "kernel launch");
+  return TACCL_OK;
+}
+
+}  // extern "C"

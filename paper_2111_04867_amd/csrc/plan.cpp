@@ -1,0 +1,602 @@
+// Host-side plan builder: topology, collective, sketch -> evaluation plan.
+//
+// Route options follow the sketch (Sec. 3.1) and the shortest-path
+// restriction of routing (Sec. 5.1, Step 1). Paths are produced by a
+// best-first search over partial paths ordered by (cost, hops, vertex
+// sequence); with positive link costs the complete paths leave the queue in
+// exactly that order, so the first k popped are the k best.
+#include <algorithm>
+#include <cstring>
+#include <memory>
+#include <queue>
+#include <set>
+#include <tuple>
+
+#include "kernels.h"
+#include "plan.h"
+
+namespace taccl {
+
+static thread_local std::string g_err;
+
+taccl_status_t fail(taccl_status_t st, const std::string &msg) {
+  g_err = msg;
+  return st;
+}
+
+const char *last_error() { return g_err.c_str(); }
+void clear_error() { g_err.clear(); }
+
+namespace {
+
+struct Path {
+  std::vector<int32_t> verts;  // hops+1 vertices
+  std::vector<int32_t> links;  // hops links
+  uint64_t cost = 0;
+};
+
+struct Partial {
+  uint64_t cost;
+  int32_t cross;
+  std::vector<int32_t> verts;
+  std::vector<int32_t> links;
+};
+
+// priority_queue keeps the largest on top; invert (cost, hops, verts)
+struct PartialAfter {
+  bool operator()(const Partial &a, const Partial &b) const {
+    if (a.cost != b.cost) return a.cost > b.cost;
+    if (a.links.size() != b.links.size()) return a.links.size() > b.links.size();
+    return a.verts > b.verts;
+  }
+};
+
+class Router {
+ public:
+  Router(const taccl_topology &t, const std::vector<uint32_t> &cost, const uint8_t *allowed,
+         const uint8_t *relay)
+      : t_(t), cost_(cost), allowed_(allowed), relay_(relay) {}
+
+  // Up to k best simple paths s -> d with at most max_cross node crossings.
+  // only_min keeps just the minimal-cost ones. Returns false if the search
+  // exceeded its expansion budget.
+  bool k_best(int32_t s, int32_t d, int32_t k, int32_t max_cross, bool only_min,
+              std::vector<Path> &out) const {
+    out.clear();
+    std::priority_queue<Partial, std::vector<Partial>, PartialAfter> q;
+    q.push(Partial{0, 0, {s}, {}});
+    int64_t budget = 20000000;
+    while (!q.empty() && (int32_t)out.size() < k) {
+      Partial cur = q.top();
+      q.pop();
+      if (--budget < 0) return false;
+      int32_t u = cur.verts.back();
+      if (u == d) {
+        if (only_min && !out.empty() && cur.cost != out[0].cost) break;
+        out.push_back(Path{cur.verts, cur.links, cur.cost});
+        continue;
+      }
+      for (int32_t e = t_.row_ptr[u]; e < t_.row_ptr[u + 1]; e++) {
+        if (allowed_ && !allowed_[e]) continue;
+        int32_t v = t_.col[e];
+        if (std::find(cur.verts.begin(), cur.verts.end(), v) != cur.verts.end()) continue;
+        int32_t cross = cur.cross;
+        if (t_.node[u] != t_.node[v]) {
+          cross++;
+          if (max_cross >= 0 && cross > max_cross) continue;
+          if (relay_ && !(relay_[u] && relay_[v])) continue;
+        }
+        Partial nxt{cur.cost + cost_[e], cross, cur.verts, cur.links};
+        nxt.verts.push_back(v);
+        nxt.links.push_back(e);
+        q.push(std::move(nxt));
+      }
+    }
+    return true;
+  }
+
+  // Best single path (empty path when s == d); false if none exists.
+  bool best(int32_t s, int32_t d, int32_t max_cross, Path &out, bool &budget_ok) const {
+    if (s == d) {
+      out = Path{{s}, {}, 0};
+      return true;
+    }
+    std::vector<Path> v;
+    budget_ok = k_best(s, d, 1, max_cross, false, v) && budget_ok;
+    if (v.empty()) return false;
+    out = v[0];
+    return true;
+  }
+
+  Path join(const Path &a, int32_t mid, const Path &b) const {
+    Path p = a;
+    if (mid >= 0) {
+      p.links.push_back(mid);
+      p.verts.push_back(t_.col[mid]);
+      p.cost += cost_[mid];
+    }
+    for (size_t i = 0; i < b.links.size(); i++) {
+      p.links.push_back(b.links[i]);
+      p.verts.push_back(b.verts[i + 1]);
+      p.cost += cost_[b.links[i]];
+    }
+    return p;
+  }
+
+  int32_t link(int32_t u, int32_t v) const {
+    for (int32_t e = t_.row_ptr[u]; e < t_.row_ptr[u + 1]; e++)
+      if (t_.col[e] == v && (!allowed_ || allowed_[e])) return e;
+    return -1;
+  }
+
+ private:
+  const taccl_topology &t_;
+  const std::vector<uint32_t> &cost_;
+  const uint8_t *allowed_;
+  const uint8_t *relay_;
+};
+
+}  // namespace
+
+// -------------------------------------------------------------------------
+// route options, layouts and kernel tables
+// -------------------------------------------------------------------------
+
+static taccl_status_t build_routes(taccl_plan *p, const uint8_t *allowed, const uint8_t *relay) {
+  const taccl_topology &t = p->topo;
+  const int32_t P = t.P;
+  Router R(t, p->cost, allowed, relay);
+  p->pair_base.assign((size_t)P * P, 0);
+  p->npaths.assign((size_t)P * P, 0);
+  p->path_off.assign(1, 0);
+  bool budget_ok = true;
+  std::vector<std::vector<int32_t>> relays_of_node;
+  if (p->mode == TACCL_ROUTE_HIER_RELAY) {
+    int32_t nn = 0;
+    for (int32_t v = 0; v < t.V; v++) nn = std::max(nn, t.node[v] + 1);
+    relays_of_node.assign(nn, {});
+    for (int32_t r = 0; r < P; r++)
+      if (relay && relay[r]) relays_of_node[t.node[r]].push_back(r);
+  }
+  for (int32_t s = 0; s < P; s++) {
+    for (int32_t d = 0; d < P; d++) {
+      std::vector<Path> opts;
+      if (s != d) {
+        switch (p->mode) {
+          case TACCL_ROUTE_SHORTEST_ONLY:
+          case TACCL_ROUTE_KSHORTEST:
+            budget_ok = R.k_best(s, d, p->k, p->max_cross, p->mode == TACCL_ROUTE_SHORTEST_ONLY,
+                                 opts) && budget_ok;
+            break;
+          case TACCL_ROUTE_RELAY1: {
+            Path q;
+            if (R.best(s, d, p->max_cross, q, budget_ok)) opts.push_back(q);
+            for (int32_t m = 0; m < P; m++) {
+              if (m == s || m == d || (relay && !relay[m])) continue;
+              Path a, b;
+              if (!R.best(s, m, p->max_cross, a, budget_ok)) continue;
+              if (!R.best(m, d, p->max_cross, b, budget_ok)) continue;
+              opts.push_back(R.join(a, -1, b));
+            }
+            break;
+          }
+          case TACCL_ROUTE_HIER_RELAY: {
+            if (t.node[s] == t.node[d]) {
+              Path q;
+              if (R.best(s, d, 0, q, budget_ok)) opts.push_back(q);
+            } else {
+              const auto &rs = relays_of_node[t.node[s]];
+              const auto &rd = relays_of_node[t.node[d]];
+              size_t nr = std::min(rs.size(), rd.size());
+              for (size_t i = 0; i < nr; i++) {
+                int32_t mid = R.link(rs[i], rd[i]);
+                if (mid < 0) continue;
+                Path a, b;
+                if (!R.best(s, rs[i], 0, a, budget_ok)) continue;
+                if (!R.best(rd[i], d, 0, b, budget_ok)) continue;
+                opts.push_back(R.join(a, mid, b));
+              }
+            }
+            break;
+          }
+          default:
+            return fail(TACCL_ERR_INVALID_ARGUMENT, "unknown route mode");
+        }
+      }
+      if (!budget_ok)
+        return fail(TACCL_ERR_UNSUPPORTED, "path search exceeded its expansion budget");
+      if (opts.size() > 255)
+        return fail(TACCL_ERR_LIMIT, "more than 255 route options for one pair");
+      size_t pp = (size_t)s * P + d;
+      p->pair_base[pp] = (uint32_t)(p->path_off.size() - 1);
+      p->npaths[pp] = (uint8_t)opts.size();
+      p->max_paths = std::max<int32_t>(p->max_paths, (int32_t)opts.size());
+      for (const Path &q : opts) {
+        std::set<int32_t> uniq(q.links.begin(), q.links.end());
+        if (uniq.size() != q.links.size())
+          return fail(TACCL_ERR_UNSUPPORTED, "a route option uses one link twice");
+        for (int32_t l : q.links) p->path_links.push_back((uint16_t)l);
+        p->path_off.push_back((uint32_t)p->path_links.size());
+        p->path_cost.push_back(q.cost);
+        p->H = std::max<int32_t>(p->H, (int32_t)q.links.size());
+      }
+    }
+  }
+  return TACCL_OK;
+}
+
+// Remaining-cost levels and (level, link, travelled) classes of every hop of
+// every Alltoall route option. A chunk's remaining cost strictly decreases
+// along its path, so a path has at most one hop per level and, within one
+// level, no send depends on another send of the same level.
+static taccl_status_t build_levels(taccl_plan *p) {
+  const int32_t P = p->topo.P, E = p->topo.E;
+  const size_t npath = p->path_cost.size();
+  std::vector<uint8_t> used_path(npath, 0);
+  for (int32_t s = 0; s < P; s++)
+    for (int32_t d = 0; d < P; d++) {
+      if (s == d) continue;
+      size_t pp = (size_t)s * P + d;
+      for (int32_t k = 0; k < p->npaths[pp]; k++) used_path[p->pair_base[pp] + k] = 1;
+    }
+  std::set<uint64_t, std::greater<uint64_t>> rems;
+  for (size_t q = 0; q < npath; q++) {
+    if (!used_path[q]) continue;
+    uint64_t rem = p->path_cost[q];
+    for (uint32_t j = p->path_off[q]; j < p->path_off[q + 1]; j++) {
+      rems.insert(rem);
+      rem -= p->cost[p->path_links[j]];
+    }
+  }
+  std::vector<uint64_t> lv(rems.begin(), rems.end());  // descending
+  p->nlev = (int32_t)lv.size();
+  if (p->nlev > 127) return fail(TACCL_ERR_UNSUPPORTED, "more than 127 remaining-cost levels");
+  auto level_of = [&](uint64_t rem) {
+    return (int32_t)(std::lower_bound(lv.begin(), lv.end(), rem, std::greater<uint64_t>()) -
+                     lv.begin());
+  };
+  // classes sorted by (level, link, travelled)
+  std::set<std::tuple<int32_t, int32_t, uint64_t>> cls;
+  for (size_t q = 0; q < npath; q++) {
+    if (!used_path[q]) continue;
+    uint64_t rem = p->path_cost[q], trav = 0;
+    for (uint32_t j = p->path_off[q]; j < p->path_off[q + 1]; j++) {
+      cls.insert({level_of(rem), (int32_t)p->path_links[j], trav});
+      rem -= p->cost[p->path_links[j]];
+      trav += p->cost[p->path_links[j]];
+    }
+  }
+  if (cls.size() > 65535) return fail(TACCL_ERR_UNSUPPORTED, "more than 65535 send classes");
+  std::vector<std::tuple<int32_t, int32_t, uint64_t>> cv(cls.begin(), cls.end());
+  p->ncls = (int32_t)cv.size();
+  p->cls_link.resize(cv.size());
+  p->lvl_cls_begin.assign((size_t)p->nlev + 1, 0);
+  p->llc.assign((size_t)p->nlev * E * 2, 0);
+  for (size_t i = 0; i < cv.size(); i++) {
+    int32_t L = std::get<0>(cv[i]), l = std::get<1>(cv[i]);
+    p->cls_link[i] = (uint16_t)l;
+    p->lvl_cls_begin[L + 1] = (uint32_t)(i + 1);
+    uint32_t *r = &p->llc[((size_t)L * E + l) * 2];
+    if (r[0] == r[1]) r[0] = (uint32_t)i;
+    r[1] = (uint32_t)(i + 1);
+  }
+  for (int32_t L = 0; L < p->nlev; L++) {
+    p->lvl_cls_begin[L + 1] = std::max(p->lvl_cls_begin[L + 1], p->lvl_cls_begin[L]);
+    p->max_lvl_cls = std::max<int32_t>(p->max_lvl_cls,
+                                       (int32_t)(p->lvl_cls_begin[L + 1] - p->lvl_cls_begin[L]));
+  }
+  p->hop_class.assign(p->path_links.size(), 0);
+  p->path_lvl_hop.assign(npath * (size_t)std::max(p->nlev, 1), (int8_t)-1);
+  for (size_t q = 0; q < npath; q++) {
+    if (!used_path[q]) continue;
+    uint64_t rem = p->path_cost[q], trav = 0;
+    int32_t h = 0;
+    for (uint32_t j = p->path_off[q]; j < p->path_off[q + 1]; j++, h++) {
+      int32_t L = level_of(rem);
+      auto it = std::lower_bound(cv.begin(), cv.end(),
+                                 std::make_tuple(L, (int32_t)p->path_links[j], trav));
+      p->hop_class[j] = (uint16_t)(it - cv.begin());
+      p->path_lvl_hop[q * p->nlev + L] = (int8_t)h;
+      rem -= p->cost[p->path_links[j]];
+      trav += p->cost[p->path_links[j]];
+    }
+  }
+  // sends a level can hold: pairs with some option having a hop there
+  std::vector<int64_t> per_level(p->nlev, 0);
+  for (int32_t s = 0; s < P; s++)
+    for (int32_t d = 0; d < P; d++) {
+      if (s == d) continue;
+      size_t pp = (size_t)s * P + d;
+      std::vector<uint8_t> has(p->nlev, 0);
+      for (int32_t k = 0; k < p->npaths[pp]; k++)
+        for (int32_t L = 0; L < p->nlev; L++)
+          if (p->path_lvl_hop[(size_t)(p->pair_base[pp] + k) * p->nlev + L] >= 0) has[L] = 1;
+      // an ordered rank pair stands for chunks_per_rank chunks
+      for (int32_t L = 0; L < p->nlev; L++) per_level[L] += has[L] ? p->coll.cpr : 0;
+    }
+  for (int32_t L = 0; L < p->nlev; L++)
+    p->max_lvl_sends = std::max<int32_t>(p->max_lvl_sends, (int32_t)per_level[L]);
+  return TACCL_OK;
+}
+
+static taccl_status_t build_layout(taccl_plan *p) {
+  const taccl_topology &t = p->topo;
+  const taccl_collective &c = p->coll;
+  const int32_t P = t.P, V = t.V, C = c.C;
+  if (c.kind == TACCL_ALLTOALL) {
+    p->route_stride = C;
+    p->prio_stride = C * std::max(p->H, 1);
+    p->route_options.assign(C, 0);
+    int64_t sends = 0;
+    for (int32_t ch = 0; ch < C; ch++) {
+      int32_t s = c.owner[ch], d = c.post[c.post_ptr[ch]];
+      if (s == d) continue;
+      size_t pp = (size_t)s * P + d;
+      p->route_options[ch] = p->npaths[pp];
+      p->num_pairs++;
+      int32_t longest = 0;
+      for (int32_t k = 0; k < p->npaths[pp]; k++) {
+        uint32_t q = p->pair_base[pp] + k;
+        longest = std::max<int32_t>(longest, (int32_t)(p->path_off[q + 1] - p->path_off[q]));
+      }
+      sends += longest;
+    }
+    p->max_sends = sends;
+  } else {
+    p->route_stride = C * P;
+    p->prio_stride = C * V;
+    p->route_options.assign((size_t)C * P, 0);
+    p->post_mask.assign(C, 0);
+    std::vector<uint8_t> used((size_t)C * P, 0);
+    for (int32_t ch = 0; ch < C; ch++) {
+      for (int32_t j = c.post_ptr[ch]; j < c.post_ptr[ch + 1]; j++) {
+        int32_t d = c.post[j];
+        if (P <= 64) p->post_mask[ch] |= 1ull << d;
+        if (d == c.owner[ch] || used[(size_t)ch * P + d]) continue;
+        used[(size_t)ch * P + d] = 1;
+        p->num_pairs++;
+        p->route_options[(size_t)ch * P + d] = p->npaths[(size_t)c.owner[ch] * P + d];
+      }
+    }
+    p->max_sends = (int64_t)C * (V - 1);
+  }
+  return TACCL_OK;
+}
+
+}  // namespace taccl
+
+using namespace taccl;
+
+extern "C" {
+
+taccl_status_t taccl_topology_create(int32_t V, int32_t P, const int32_t *row_ptr,
+                                     const int32_t *col, const uint32_t *alpha_ns,
+                                     const uint32_t *beta_ps_per_byte,
+                                     const int32_t *node_of_vertex, taccl_topology_t *out) {
+  if (!out) return fail(TACCL_ERR_INVALID_ARGUMENT, "out is null");
+  *out = nullptr;
+  if (V <= 0 || P <= 0 || P > V || !row_ptr)
+    return fail(TACCL_ERR_INVALID_ARGUMENT, "need 0 < num_ranks <= num_vertices and row_ptr");
+  if (V > 65535) return fail(TACCL_ERR_LIMIT, "more than 65535 vertices");
+  if (row_ptr[0] != 0) return fail(TACCL_ERR_INVALID_ARGUMENT, "row_ptr[0] must be 0");
+  for (int32_t u = 0; u < V; u++)
+    if (row_ptr[u + 1] < row_ptr[u]) return fail(TACCL_ERR_INVALID_ARGUMENT, "row_ptr decreases");
+  const int32_t E = row_ptr[V];
+  if (E > 65535) return fail(TACCL_ERR_LIMIT, "more than 65535 links");
+  if (E > 0 && (!col || !alpha_ns || !beta_ps_per_byte))
+    return fail(TACCL_ERR_INVALID_ARGUMENT, "col, alpha_ns and beta_ps_per_byte are required");
+  auto *t = new (std::nothrow) taccl_topology();
+  if (!t) return fail(TACCL_ERR_NO_MEMORY, "topology allocation failed");
+  t->V = V;
+  t->P = P;
+  t->E = E;
+  t->row_ptr.assign(row_ptr, row_ptr + V + 1);
+  t->col.assign(col, col + E);
+  t->alpha.assign(alpha_ns, alpha_ns + E);
+  t->beta.assign(beta_ps_per_byte, beta_ps_per_byte + E);
+  t->src.resize(E);
+  t->node.assign(V, 0);
+  if (node_of_vertex) t->node.assign(node_of_vertex, node_of_vertex + V);
+  std::set<std::pair<int32_t, int32_t>> seen;
+  for (int32_t u = 0; u < V; u++)
+    for (int32_t e = row_ptr[u]; e < row_ptr[u + 1]; e++) {
+      int32_t v = col[e];
+      if (v < 0 || v >= V || v == u || !seen.insert({u, v}).second) {
+        delete t;
+        return fail(TACCL_ERR_INVALID_ARGUMENT,
+                    "link " + std::to_string(e) + " is a self loop, duplicate or out of range");
+      }
+      t->src[e] = u;
+    }
+  *out = t;
+  return TACCL_OK;
+}
+
+void taccl_topology_destroy(taccl_topology_t t) { delete t; }
+
+taccl_status_t taccl_collective_create(taccl_kind_t kind, int32_t P, int32_t cpr,
+                                       uint64_t chunk_bytes, taccl_collective_t *out) {
+  if (!out) return fail(TACCL_ERR_INVALID_ARGUMENT, "out is null");
+  *out = nullptr;
+  if (P <= 0 || cpr <= 0 || chunk_bytes == 0)
+    return fail(TACCL_ERR_INVALID_ARGUMENT, "need num_ranks, chunks_per_rank, chunk_bytes > 0");
+  int64_t C = kind == TACCL_ALLGATHER ? (int64_t)P * cpr
+            : kind == TACCL_ALLTOALL  ? (int64_t)P * P * cpr
+                                      : -1;
+  if (C < 0) return fail(TACCL_ERR_INVALID_ARGUMENT, "kind must be ALLGATHER or ALLTOALL");
+  if (C > 65536) return fail(TACCL_ERR_LIMIT, "more than 65536 chunks");
+  auto *c = new (std::nothrow) taccl_collective();
+  if (!c) return fail(TACCL_ERR_NO_MEMORY, "collective allocation failed");
+  c->kind = kind;
+  c->P = P;
+  c->cpr = cpr;
+  c->C = (int32_t)C;
+  c->S = chunk_bytes;
+  c->owner.resize(C);
+  c->post_ptr.resize(C + 1);
+  for (int32_t ch = 0; ch < C; ch++) {
+    c->post_ptr[ch] = (int32_t)c->post.size();
+    if (kind == TACCL_ALLGATHER) {
+      c->owner[ch] = ch / cpr;
+      for (int32_t r = 0; r < P; r++) c->post.push_back(r);
+    } else {
+      int32_t pair = ch / cpr;
+      c->owner[ch] = pair / P;
+      c->post.push_back(pair % P);
+    }
+  }
+  c->post_ptr[C] = (int32_t)c->post.size();
+  *out = c;
+  return TACCL_OK;
+}
+
+taccl_status_t taccl_collective_create_explicit(int32_t C, int32_t P, uint64_t chunk_bytes,
+                                                const int32_t *owner, const int32_t *post_ptr,
+                                                const int32_t *post, taccl_collective_t *out) {
+  if (!out) return fail(TACCL_ERR_INVALID_ARGUMENT, "out is null");
+  *out = nullptr;
+  if (C <= 0 || P <= 0 || chunk_bytes == 0 || !owner || !post_ptr || (post_ptr[C] > 0 && !post))
+    return fail(TACCL_ERR_INVALID_ARGUMENT, "bad explicit collective arguments");
+  if (C > 65536) return fail(TACCL_ERR_LIMIT, "more than 65536 chunks");
+  if (post_ptr[0] != 0) return fail(TACCL_ERR_INVALID_ARGUMENT, "post_ptr[0] must be 0");
+  for (int32_t ch = 0; ch < C; ch++) {
+    if (owner[ch] < 0 || owner[ch] >= P || post_ptr[ch + 1] < post_ptr[ch])
+      return fail(TACCL_ERR_INVALID_ARGUMENT, "bad owner or post_ptr");
+    for (int32_t j = post_ptr[ch]; j < post_ptr[ch + 1]; j++)
+      if (post[j] < 0 || post[j] >= P) return fail(TACCL_ERR_INVALID_ARGUMENT, "bad post rank");
+  }
+  auto *c = new (std::nothrow) taccl_collective();
+  if (!c) return fail(TACCL_ERR_NO_MEMORY, "collective allocation failed");
+  c->kind = TACCL_EXPLICIT;
+  c->P = P;
+  c->cpr = 0;
+  c->C = C;
+  c->S = chunk_bytes;
+  c->owner.assign(owner, owner + C);
+  c->post_ptr.assign(post_ptr, post_ptr + C + 1);
+  c->post.assign(post, post + post_ptr[C]);
+  *out = c;
+  return TACCL_OK;
+}
+
+void taccl_collective_destroy(taccl_collective_t c) { delete c; }
+
+taccl_status_t taccl_sketch_apply(taccl_topology_t topo, taccl_collective_t coll,
+                                  const taccl_sketch_desc_t *sk, taccl_plan_t *out) {
+  if (!out) return fail(TACCL_ERR_INVALID_ARGUMENT, "out is null");
+  *out = nullptr;
+  if (!topo || !coll || !sk) return fail(TACCL_ERR_INVALID_ARGUMENT, "null handle or sketch");
+  if (coll->P != topo->P)
+    return fail(TACCL_ERR_INVALID_ARGUMENT, "collective and topology disagree on rank count");
+  if (sk->route_mode < 0 || sk->route_mode > 3)
+    return fail(TACCL_ERR_INVALID_ARGUMENT, "unknown route mode");
+  if ((sk->route_mode == TACCL_ROUTE_SHORTEST_ONLY || sk->route_mode == TACCL_ROUTE_KSHORTEST) &&
+      (sk->k <= 0 || sk->k > 255))
+    return fail(TACCL_ERR_INVALID_ARGUMENT, "k must be in [1, 255]");
+  auto *p = new (std::nothrow) taccl_plan();
+  if (!p) return fail(TACCL_ERR_NO_MEMORY, "plan allocation failed");
+  std::unique_ptr<taccl_plan> guard(p);
+  p->topo = *topo;
+  p->coll = *coll;
+  p->mode = sk->route_mode;
+  p->k = sk->k;
+  p->max_cross = sk->max_node_crossings;
+  const int32_t E = topo->E;
+  // integer alpha-beta cost of one chunk on every link (Sec. 4.1)
+  p->cost.resize(E);
+  p->lsrc.resize(E);
+  p->ldst.resize(E);
+  uint64_t max_cost = 0;
+  for (int32_t e = 0; e < E; e++) {
+    uint64_t bs = (uint64_t)topo->beta[e] * coll->S;
+    if (topo->beta[e] != 0 && bs / topo->beta[e] != coll->S)
+      return fail(TACCL_ERR_LIMIT, "beta * chunk_bytes overflows 64 bits");
+    uint64_t c = (uint64_t)topo->alpha[e] + bs / 1000 + (bs % 1000 != 0);
+    if (c == 0) return fail(TACCL_ERR_INVALID_ARGUMENT, "a link has zero cost");
+    if (c > 0xFFFFFFFFull) return fail(TACCL_ERR_LIMIT, "a link cost does not fit 32 bits");
+    p->cost[e] = (uint32_t)c;
+    max_cost = std::max(max_cost, c);
+    p->lsrc[e] = (uint16_t)topo->src[e];
+    p->ldst[e] = (uint16_t)topo->col[e];
+  }
+  taccl_status_t st = build_routes(p, sk->allowed_link, sk->is_relay);
+  if (st) return st;
+  st = build_layout(p);
+  if (st) return st;
+  // every time is at most the sum of all send costs
+  if ((unsigned __int128)p->max_sends * max_cost >= ((unsigned __int128)1 << 32))
+    return fail(TACCL_ERR_LIMIT, "worst-case makespan does not fit 32 bits");
+  if (coll->kind == TACCL_ALLTOALL) {
+    st = build_levels(p);
+    if (st) return st;
+  } else {
+    if (topo->V > 64)
+      return fail(TACCL_ERR_UNSUPPORTED, "multicast evaluation holds at most 64 vertices");
+    if ((int64_t)coll->C * topo->V > 65535)
+      return fail(TACCL_ERR_UNSUPPORTED, "multicast evaluation holds at most 65535 send slots");
+  }
+  if (coll->kind == TACCL_ALLTOALL) {
+    PathArgs a{};
+    p->path_lds = path_layout(*p, a);
+  } else {
+    TreeArgs a{};
+    p->tree_lds = tree_layout(*p, a);
+  }
+  *out = guard.release();
+  clear_error();
+  return TACCL_OK;
+}
+
+taccl_status_t taccl_plan_info(taccl_plan_t p, taccl_plan_info_t *o) {
+  if (!p || !o) return fail(TACCL_ERR_INVALID_ARGUMENT, "null plan or out");
+  std::memset(o, 0, sizeof *o);
+  o->num_vertices = p->topo.V;
+  o->num_ranks = p->topo.P;
+  o->num_links = p->topo.E;
+  o->num_chunks = p->coll.C;
+  o->kind = p->coll.kind;
+  o->route_stride = p->route_stride;
+  o->prio_stride = p->prio_stride;
+  o->max_hops = p->H;
+  o->max_paths = p->max_paths;
+  o->num_pairs = p->num_pairs;
+  o->num_levels = p->nlev;
+  o->max_sends = p->max_sends;
+  o->bytes_per_candidate = (uint64_t)p->route_stride + 4ull * p->prio_stride + 5ull;
+  o->num_classes = p->ncls;
+  o->lds_bytes = p->coll.kind == TACCL_ALLTOALL ? p->path_lds : p->tree_lds;
+  return TACCL_OK;
+}
+
+taccl_status_t taccl_plan_route_options(taccl_plan_t p, int32_t *options) {
+  if (!p || !options) return fail(TACCL_ERR_INVALID_ARGUMENT, "null plan or options");
+  std::memcpy(options, p->route_options.data(), sizeof(int32_t) * p->route_options.size());
+  return TACCL_OK;
+}
+
+taccl_status_t taccl_plan_path(taccl_plan_t p, int32_t s, int32_t d, int32_t i, int32_t *links,
+                               int32_t cap, int32_t *hops) {
+  if (!p || !hops || (cap > 0 && !links)) return fail(TACCL_ERR_INVALID_ARGUMENT, "null argument");
+  const int32_t P = p->topo.P;
+  if (s < 0 || d < 0 || s >= P || d >= P) return fail(TACCL_ERR_INVALID_ARGUMENT, "bad pair");
+  size_t pp = (size_t)s * P + d;
+  if (i < 0 || i >= p->npaths[pp]) return fail(TACCL_ERR_INVALID_ARGUMENT, "no such option");
+  uint32_t q = p->pair_base[pp] + i;
+  int32_t n = (int32_t)(p->path_off[q + 1] - p->path_off[q]);
+  *hops = n;
+  if (n > cap) return fail(TACCL_ERR_INVALID_ARGUMENT, "links buffer too small");
+  for (int32_t j = 0; j < n; j++) links[j] = p->path_links[p->path_off[q] + j];
+  return TACCL_OK;
+}
+
+taccl_status_t taccl_plan_link_costs(taccl_plan_t p, uint32_t *cost_ns) {
+  if (!p || !cost_ns) return fail(TACCL_ERR_INVALID_ARGUMENT, "null argument");
+  std::memcpy(cost_ns, p->cost.data(), sizeof(uint32_t) * p->cost.size());
+  return TACCL_OK;
+}
+
+const char *taccl_last_error(void) { return taccl::last_error(); }
+
+int32_t taccl_version(void) { return 100; }
+
+}  // extern "C"

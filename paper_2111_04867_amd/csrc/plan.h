@@ -1,0 +1,93 @@
+// Internal plan structures of the evaluator library (not part of the ABI).
+#pragma once
+
+#include <cstdint>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "taccl.h"
+
+namespace taccl {
+
+// Set the thread-local error message and return the status.
+taccl_status_t fail(taccl_status_t st, const std::string &msg);
+
+}  // namespace taccl
+
+struct taccl_topology {
+  int32_t V = 0, P = 0, E = 0;
+  std::vector<int32_t> row_ptr, col, src, node;
+  std::vector<uint32_t> alpha, beta;
+};
+
+struct taccl_collective {
+  int32_t kind = 0, P = 0, cpr = 0, C = 0;
+  uint64_t S = 0;
+  std::vector<int32_t> owner;     // [C]
+  std::vector<int32_t> post_ptr;  // [C+1]
+  std::vector<int32_t> post;      // ranks to reach
+};
+
+namespace taccl {
+
+// Device copies of the read-only plan tables (one set per device).
+struct DeviceTables {
+  void *block = nullptr;  // one allocation holding every table
+  const uint32_t *cost = nullptr;
+  const uint16_t *lsrc = nullptr, *ldst = nullptr;
+  const uint32_t *pair_base = nullptr;
+  const uint8_t *npaths = nullptr;
+  const uint32_t *path_off = nullptr;
+  const uint16_t *path_links = nullptr;
+  const int32_t *owner = nullptr;
+  const uint64_t *post_mask = nullptr;
+  const uint16_t *hop_class = nullptr;
+  const int8_t *path_lvl_hop = nullptr;
+  const uint32_t *lvl_cls_begin = nullptr;
+  const uint32_t *llc = nullptr;
+  int max_lds = 0;  // bytes of LDS a block may use on this device
+  int num_cus = 0;
+};
+
+}  // namespace taccl
+
+struct taccl_plan {
+  taccl_topology topo;
+  taccl_collective coll;
+  int32_t mode = 0, k = 0, max_cross = -1;
+
+  // link tables
+  std::vector<uint32_t> cost;  // [E] integer alpha-beta cost in ns
+  std::vector<uint16_t> lsrc, ldst;
+
+  // route options per ordered rank pair (s, d), pair index s*P + d
+  std::vector<uint32_t> pair_base;  // [P*P] first option's global path index
+  std::vector<uint8_t> npaths;      // [P*P]
+  std::vector<uint32_t> path_off;   // [NPATH+1] into path_links
+  std::vector<uint16_t> path_links;
+  std::vector<uint64_t> path_cost;  // [NPATH]
+
+  int32_t H = 0, max_paths = 0, num_pairs = 0;
+  int32_t route_stride = 0, prio_stride = 0;
+  int64_t max_sends = 0;
+  std::vector<int32_t> route_options;  // [route_stride]
+
+  // multicast (tree) evaluation
+  std::vector<uint64_t> post_mask;  // [C], ranks a chunk must reach
+
+  // Alltoall (path) evaluation: levels of equal remaining cost
+  int32_t nlev = 0, ncls = 0, max_lvl_cls = 0, max_lvl_sends = 0;
+  std::vector<uint16_t> hop_class;     // [path_links.size()] class of each hop
+  std::vector<int8_t> path_lvl_hop;    // [NPATH*nlev] hop at each level or -1
+  std::vector<uint32_t> lvl_cls_begin; // [nlev+1]
+  std::vector<uint32_t> llc;           // [nlev*E*2] class range of a link at a level
+  std::vector<uint16_t> cls_link;      // [ncls]
+
+  // launch shape
+  int32_t tree_lds = 0, path_lds = 0;
+
+  std::mutex mu;
+  std::map<int, taccl::DeviceTables> dev;
+};
