@@ -58,6 +58,10 @@ def lib():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() or "
                           "python paper_2111_04867_amd/build.py")
+    # torch carries its own HIP runtime (soname libamdhip64.so.7); loading it
+    # first makes the library bind to that same runtime instead of starting
+    # a second one that would compete for the device
+    import torch  # noqa: F401
     L = ct.CDLL(LIB_PATH)
     P = ct.c_void_p
     st = ct.c_int

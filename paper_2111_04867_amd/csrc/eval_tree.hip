@@ -26,6 +26,16 @@ namespace {
 
 constexpr uint32_t kNotYet = 0xFFFFFFFFu;
 
+// Arrival times are written by one lane and read by others of the same wave
+// while links advance; relaxed workgroup-scope atomics keep these accesses
+// plain LDS instructions (a volatile pointer would turn them into FLAT ones).
+__device__ __forceinline__ uint32_t lds_get(uint32_t *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ void lds_put(uint32_t *p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
 __device__ __forceinline__ uint32_t wave_max(uint32_t v) {
   for (int o = 32; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o));
   return v;
@@ -46,7 +56,7 @@ __global__ __launch_bounds__(kTreeThreads) void tree_eval_kernel(TreeArgs a) {
   uint16_t *par = (uint16_t *)(lds + a.o_par);  // link+1 into (c,v), 0 = none
   uint32_t *dist = (uint32_t *)(lds + a.o_dist);
   uint32_t *hgt = (uint32_t *)(lds + a.o_hgt);
-  volatile uint32_t *fin = (volatile uint32_t *)(lds + a.o_fin);
+  uint32_t *fin = (uint32_t *)(lds + a.o_fin);
   uint16_t *ord = (uint16_t *)(lds + a.o_ord);
   uint16_t *sidx = (uint16_t *)(lds + a.o_sidx);
   uint16_t *tmp = (uint16_t *)(lds + a.o_tmp);
@@ -70,7 +80,7 @@ __global__ __launch_bounds__(kTreeThreads) void tree_eval_kernel(TreeArgs a) {
     for (int j = lane; j < CV; j += 64) {
       pr[j] = gpr[j];
       par[j] = 0;
-      fin[j] = kNotYet;
+      lds_put(&fin[j], kNotYet);
     }
     for (int l = lane; l <= E; l += 64) lcnt[l] = 0;
     __syncthreads();
@@ -101,10 +111,10 @@ __global__ __launch_bounds__(kTreeThreads) void tree_eval_kernel(TreeArgs a) {
       }
       reach[c] = reached;
       hgt[base + o] = 0;
-      for (int j = 0; j < cnt; j++) hgt[base + ord[j]] = 0;
+      for (int j = 0; j < cnt; j++) hgt[base + ord[base + j]] = 0;
       // children are discovered after their parents: sweep backwards
       for (int j = cnt - 1; j >= 0; j--) {
-        const int v = ord[j];
+        const int v = ord[base + j];
         const int l = par[base + v] - 1;
         const int u = a.lsrc[l];
         const uint32_t h = a.cost[l] + hgt[base + v];
@@ -184,10 +194,10 @@ __global__ __launch_bounds__(kTreeThreads) void tree_eval_kernel(TreeArgs a) {
           const int s = chain[h];
           const int c = s / V;
           const int o = a.cpr > 0 ? c / a.cpr : a.owner[c];
-          const uint32_t ready = (u == o) ? 0u : fin[c * V + u];
+          const uint32_t ready = (u == o) ? 0u : lds_get(&fin[c * V + u]);
           if (ready == kNotYet) break;
           f = max(ready, f) + cl;
-          fin[s] = f;
+          lds_put(&fin[s], f);
           h++;
         }
         lhead[l] = h;
