@@ -46,7 +46,7 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
          o_pl = pk.add(p->path_links), o_own = pk.add(p->coll.owner),
          o_pm = pk.add(p->post_mask), o_hc = pk.add(p->hop_class),
          o_plh = pk.add(p->path_lvl_hop), o_lcb = pk.add(p->lvl_cls_begin),
-         o_llc = pk.add(p->llc);
+         o_llc = pk.add(p->llc), o_trec = pk.add(p->tree_rec), o_own8 = pk.add(p->owner8);
   void *blk = nullptr;
   e = hipMalloc(&blk, pk.bytes.size());
   if (e != hipSuccess) return fail(TACCL_ERR_NO_MEMORY, "hipMalloc of plan tables failed");
@@ -71,7 +71,10 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
   t.path_lvl_hop = (const int8_t *)at(o_plh);
   t.lvl_cls_begin = (const uint32_t *)at(o_lcb);
   t.llc = (const uint32_t *)at(o_llc);
+  t.tree_rec = (const uint32_t *)at(o_trec);
+  t.owner8 = (const uint8_t *)at(o_own8);
   t.max_lds = (int)prop.sharedMemPerBlock;
+  t.lds_per_cu = (int)std::max<size_t>(prop.maxSharedMemoryPerMultiProcessor, prop.sharedMemPerBlock);
   t.num_cus = prop.multiProcessorCount;
   *out = &(p->dev[dev] = t);
   return TACCL_OK;
@@ -151,17 +154,15 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     a.P = p->topo.P;
     a.V = p->topo.V;
     a.E = p->topo.E;
-    a.cpr = p->coll.kind == TACCL_ALLGATHER ? p->coll.cpr : 0;
     a.route_stride = p->route_stride;
     a.prio_stride = p->prio_stride;
+    a.routes_word_aligned = (p->route_stride % 4 == 0) && (((uintptr_t)d_routes & 3) == 0);
     a.cost = t->cost;
     a.lsrc = t->lsrc;
     a.ldst = t->ldst;
-    a.pair_base = t->pair_base;
+    a.rec = t->tree_rec;
     a.npaths = t->npaths;
-    a.path_off = t->path_off;
-    a.path_links = t->path_links;
-    a.owner = t->owner;
+    a.owner8 = t->owner8;
     a.post_mask = t->post_mask;
     a.routes = d_routes;
     a.prio = d_prio;
@@ -170,7 +171,23 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     a.n = n;
     if (tree_layout(*p, a) > t->max_lds)
       return fail(TACCL_ERR_UNSUPPORTED, "multicast plan needs more LDS than a block has");
-    e = launch_tree(a, grid, s);
+    // wavefronts per block: most resident wavefronts per CU within the LDS
+    int best_w = 1, best_res = 0, best_bpc = 1;
+    for (int w = 1; w <= kTreeMaxThreads / 64; w++) {
+      const int bytes = tree_block_bytes(a, w);
+      if (bytes > t->max_lds) break;
+      const int bpc = std::min(t->lds_per_cu / bytes, 32 / w);
+      const int res = std::min(bpc * w, 32);
+      if (res > best_res) {
+        best_res = res;
+        best_w = w;
+        best_bpc = bpc;
+      }
+    }
+    a.waves_per_block = best_w;
+    const int64_t want = (n + best_w - 1) / best_w;
+    const int tgrid = (int)std::min<int64_t>(want, (int64_t)std::max(t->num_cus, 1) * best_bpc);
+    e = launch_tree(a, tgrid, s);
   }
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
   return TACCL_OK;

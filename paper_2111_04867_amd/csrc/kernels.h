@@ -9,27 +9,30 @@
 
 namespace taccl {
 
-// Multicast (Allgather / explicit) evaluation: one wavefront per candidate.
+// Multicast (Allgather / explicit) evaluation: persistent blocks of
+// wavefronts, one candidate per wavefront at a time.
 struct TreeArgs {
-  int32_t C, P, V, E, cpr;  // cpr > 0: owner = c / cpr; else owner table
-  int32_t route_stride, prio_stride;
+  int32_t C, P, V, E, K, H, mask_words;
+  int32_t route_stride, prio_stride, routes_word_aligned;
+  uint32_t vmagic;  // floor(2^32 / V) + 1
   const uint32_t *cost;
   const uint16_t *lsrc, *ldst;
-  const uint32_t *pair_base;
+  const uint32_t *rec;  // fixed-stride route records (one word per hop)
+  int32_t rec_len, rec_in_lds;
   const uint8_t *npaths;
-  const uint32_t *path_off;
-  const uint16_t *path_links;
-  const int32_t *owner;
+  const uint8_t *owner8;
   const uint64_t *post_mask;
   const uint8_t *routes;
   const uint32_t *prio;
   uint32_t *makespan;
   uint8_t *valid;
   int64_t n;
-  // LDS carve-up (byte offsets)
-  int32_t o_rt, o_pr, o_par, o_dist, o_hgt, o_fin, o_ord, o_sidx, o_tmp, o_chain, o_krem,
-      o_ktrav, o_lcnt, o_lhead, o_lfree, o_reach;
-  int32_t lds_bytes;
+  int32_t waves_per_block;
+  // LDS carve-up: shared tables (byte offsets from the block's base)
+  int32_t o_cost, o_src, o_dst, o_rec, o_np, o_own, o_post, o_wave;
+  // per-wavefront state (byte offsets from the wavefront's base)
+  int32_t w_rt, w_key, w_prio, w_chain, w_par, w_mask, w_base, w_head, w_free;
+  int32_t wave_bytes;
 };
 
 // Alltoall evaluation: one block per candidate, level by level.
@@ -54,11 +57,13 @@ struct PathArgs {
   int32_t lds_bytes;
 };
 
-constexpr int kTreeThreads = 64;
+constexpr int kTreeMaxThreads = 512;  // up to 8 wavefronts per block
+constexpr int kTreeRecLdsMax = 32768;  // route records kept in LDS up to this size
 constexpr int kPathThreads = 256;
 
-// Fill the LDS layout; returns the bytes needed per block.
+// Fill the LDS layout; returns the bytes needed by a one-wavefront block.
 int32_t tree_layout(const taccl_plan &p, TreeArgs &a);
+int32_t tree_block_bytes(const TreeArgs &a, int waves);
 int32_t path_layout(const taccl_plan &p, PathArgs &a);
 
 hipError_t launch_tree(const TreeArgs &a, int grid, hipStream_t stream);

@@ -359,6 +359,22 @@ static taccl_status_t build_layout(taccl_plan *p) {
       }
     }
     p->max_sends = (int64_t)C * (V - 1);
+    // fixed-stride copy of the route options for on-chip lookup
+    const int32_t K = std::max(p->max_paths, 1), H = std::max(p->H, 1);
+    p->tree_rec.assign((size_t)P * P * K * H, 0);
+    for (int32_t pp = 0; pp < P * P; pp++)
+      for (int32_t k = 0; k < p->npaths[pp]; k++) {
+        uint32_t q = p->pair_base[pp] + k;
+        uint32_t *r = &p->tree_rec[((size_t)pp * K + k) * H];
+        const uint32_t hops = p->path_off[q + 1] - p->path_off[q];
+        for (uint32_t j = 0; j < hops; j++) {
+          const uint32_t l = p->path_links[p->path_off[q] + j];
+          r[j] = l | ((uint32_t)p->ldst[l] << 16);
+        }
+        r[0] |= hops << 24;
+      }
+    p->owner8.resize(C);
+    for (int32_t ch = 0; ch < C; ch++) p->owner8[ch] = (uint8_t)c.owner[ch];
   }
   return TACCL_OK;
 }
@@ -534,6 +550,10 @@ taccl_status_t taccl_sketch_apply(taccl_topology_t topo, taccl_collective_t coll
       return fail(TACCL_ERR_UNSUPPORTED, "multicast evaluation holds at most 64 vertices");
     if ((int64_t)coll->C * topo->V > 65535)
       return fail(TACCL_ERR_UNSUPPORTED, "multicast evaluation holds at most 65535 send slots");
+    if (topo->E > 65534)
+      return fail(TACCL_ERR_UNSUPPORTED, "multicast evaluation holds at most 65534 links");
+    if (p->H > 255)
+      return fail(TACCL_ERR_UNSUPPORTED, "multicast evaluation holds paths of at most 255 hops");
   }
   if (coll->kind == TACCL_ALLTOALL) {
     PathArgs a{};

@@ -43,11 +43,14 @@ struct DeviceTables {
   const uint16_t *path_links = nullptr;
   const int32_t *owner = nullptr;
   const uint64_t *post_mask = nullptr;
+  const uint32_t *tree_rec = nullptr;
+  const uint8_t *owner8 = nullptr;
   const uint16_t *hop_class = nullptr;
   const int8_t *path_lvl_hop = nullptr;
   const uint32_t *lvl_cls_begin = nullptr;
   const uint32_t *llc = nullptr;
   int max_lds = 0;  // bytes of LDS a block may use on this device
+  int lds_per_cu = 0;
   int num_cus = 0;
 };
 
@@ -76,6 +79,11 @@ struct taccl_plan {
 
   // multicast (tree) evaluation
   std::vector<uint64_t> post_mask;  // [C], ranks a chunk must reach
+  // fixed-stride route records, one word per hop of option k of pair (s,d)
+  // at [((s*P+d)*max_paths + k)*H + j]: link | dst << 16 | (hops << 24 on
+  // the first word); options a pair does not have are all zero (no hops)
+  std::vector<uint32_t> tree_rec;
+  std::vector<uint8_t> owner8;      // [C] owner rank of every chunk
 
   // Alltoall (path) evaluation: levels of equal remaining cost
   int32_t nlev = 0, ncls = 0, max_lvl_cls = 0, max_lvl_sends = 0;
