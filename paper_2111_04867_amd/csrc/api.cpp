@@ -46,7 +46,9 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
          o_pl = pk.add(p->path_links), o_own = pk.add(p->coll.owner),
          o_pm = pk.add(p->post_mask), o_hc = pk.add(p->hop_class),
          o_plh = pk.add(p->path_lvl_hop), o_lcb = pk.add(p->lvl_cls_begin),
-         o_llc = pk.add(p->llc), o_trec = pk.add(p->tree_rec), o_own8 = pk.add(p->owner8);
+         o_llc = pk.add(p->llc), o_trec = pk.add(p->tree_rec), o_own8 = pk.add(p->owner8),
+         o_arec = pk.add(p->arec), o_cpath = pk.add(p->cpath), o_cinfo = pk.add(p->cinfo),
+         o_cbkt = pk.add(p->cbkt);
   void *blk = nullptr;
   e = hipMalloc(&blk, pk.bytes.size());
   if (e != hipSuccess) return fail(TACCL_ERR_NO_MEMORY, "hipMalloc of plan tables failed");
@@ -73,6 +75,10 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
   t.llc = (const uint32_t *)at(o_llc);
   t.tree_rec = (const uint32_t *)at(o_trec);
   t.owner8 = (const uint8_t *)at(o_own8);
+  t.arec = (const uint32_t *)at(o_arec);
+  t.cpath = (const uint32_t *)at(o_cpath);
+  t.cinfo = (const uint32_t *)at(o_cinfo);
+  t.cbkt = (const uint32_t *)at(o_cbkt);
   t.max_lds = (int)prop.sharedMemPerBlock;
   t.lds_per_cu = (int)std::max<size_t>(prop.maxSharedMemoryPerMultiProcessor, prop.sharedMemPerBlock);
   t.num_cus = prop.multiProcessorCount;
@@ -145,9 +151,20 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     a.makespan = d_makespan;
     a.valid = d_valid;
     a.n = n;
-    if (path_layout(*p, a) > t->max_lds)
-      return fail(TACCL_ERR_UNSUPPORTED, "Alltoall plan needs more LDS than a block has");
-    e = launch_path(a, grid, s);
+    a.arec = t->arec;
+    a.cpath = t->cpath;
+    a.cinfo = t->cinfo;
+    a.cbkt = t->cbkt;
+    const int cpt = p->path_fast ? path_fast_cpt(*p) : 0;
+    if (cpt && path_fast_layout(*p, a) <= t->max_lds) {
+      const int bpc = std::max(1, std::min(t->lds_per_cu / a.lds_bytes, 4));
+      const int fgrid = (int)std::min<int64_t>(n, (int64_t)std::max(t->num_cus, 1) * bpc);
+      e = launch_path_fast(a, cpt, fgrid, s);
+    } else {
+      if (path_layout(*p, a) > t->max_lds)
+        return fail(TACCL_ERR_UNSUPPORTED, "Alltoall plan needs more LDS than a block has");
+      e = launch_path(a, grid, s);
+    }
   } else {
     TreeArgs a{};
     a.C = p->coll.C;

@@ -208,3 +208,336 @@ hipError_t launch_path(const PathArgs &a, int grid, hipStream_t stream) {
 }
 
 }  // namespace taccl
+
+// ===========================================================================
+// Register-resident Alltoall kernel (paths of <= 6 hops, <= 8 levels,
+// <= 4096 chunks). One 512-thread block evaluates one candidate at a time.
+// Thread t owns chunks t, t+512, ...: their route option's record (hop count,
+// level and class of every hop) and the priorities of their hops are loaded
+// once into registers. Each level then takes O(1) work per send:
+//   A. count the level's sends per (class, top priority bits) bucket;
+//   B. block scan of the bucket counts (classes are ordered by link, then
+//      travelled cost, so a link's sends form one contiguous run);
+//   C. scatter the sends into their buckets;
+//   D. order the few sends that share a bucket by (priority, chunk);
+//   E. time every link's run at once: with link cost c, carried busy time F
+//      and ready times r_j of the run's sends in order, the k-th send
+//      finishes at (k+1)c + max(F, max_{j<=k}(r_j - j c)) (App. B.3 without
+//      contiguity), so one segmented prefix max over the level gives every
+//      finish time.
+// ===========================================================================
+
+namespace taccl {
+namespace {
+
+constexpr uint64_t kBias = 1ull << 32;      // keeps r - k c non-negative
+constexpr uint32_t kUnset = 0xFFFFFFFFu;
+
+__device__ __forceinline__ uint64_t shfl_up64(uint64_t v, int o) {
+  const uint32_t lo = (uint32_t)__shfl_up((int)(uint32_t)v, o);
+  const uint32_t hi = (uint32_t)__shfl_up((int)(uint32_t)(v >> 32), o);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// exclusive scan of cnt[0..n) in place, cnt[n] = total (all threads call)
+__device__ void block_excl_scan(uint32_t *cnt, int n, uint32_t *wsum) {
+  const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63, wave = tid >> 6;
+  const int per = (n + nt - 1) / nt;
+  const int b = min(tid * per, n), e = min(b + per, n);
+  uint32_t sum = 0;
+  for (int j = b; j < e; j++) sum += cnt[j];
+  uint32_t incl = sum;
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t t = (uint32_t)__shfl_up((int)incl, o);
+    if (lane >= o) incl += t;
+  }
+  if (lane == 63) wsum[wave] = incl;
+  __syncthreads();
+  uint32_t off = 0;
+  for (int w = 0; w < wave; w++) off += wsum[w];
+  uint32_t run = off + incl - sum;
+  for (int j = b; j < e; j++) {
+    const uint32_t x = cnt[j];
+    cnt[j] = run;
+    run += x;
+  }
+  if (tid == nt - 1) cnt[n] = off + incl;
+  __syncthreads();
+}
+
+template <int CPT>
+__global__ __launch_bounds__(kPathFastThreads) void path_eval_fast(PathArgs a) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int NT = kPathFastThreads;
+  const int C = a.C, E = a.E, H = a.H, nlev = a.nlev;
+
+  uint32_t *s_cost = (uint32_t *)(lds + a.o_fcost);
+  uint32_t *s_cinfo = (uint32_t *)(lds + a.o_fcinfo);
+  uint32_t *s_cbkt = (uint32_t *)(lds + a.o_fcbkt);
+  uint32_t *s_lcb = (uint32_t *)(lds + a.o_flcb);
+  uint32_t *ctime = (uint32_t *)(lds + a.o_fctime);  // a chunk's arrival so far
+  uint32_t *lfree = (uint32_t *)(lds + a.o_flfree);  // [2][E]: busy time, next
+  uint32_t *bcnt = (uint32_t *)(lds + a.o_fbcnt);    // bucket counts, then starts
+  uint32_t *epr = (uint32_t *)(lds + a.o_fepr);
+  uint16_t *ech = (uint16_t *)(lds + a.o_fech);
+  uint32_t *pinfo = (uint32_t *)(lds + a.o_fsrt);   // chunk | index in its link run << 16
+  uint16_t *plink = (uint16_t *)(lds + a.o_fscl);    // link of every sorted send
+  uint32_t *red = (uint32_t *)(lds + a.o_fred);      // [2][NT/64] scan scratch
+  uint64_t *red64 = (uint64_t *)(lds + a.o_fred64);  // [NT/64] segmented max
+  uint32_t *redf = (uint32_t *)(lds + a.o_fredf);    // [NT/64] segment-head flags
+  for (int j = tid; j < E; j += NT) s_cost[j] = a.cost[j];
+  for (int j = tid; j < a.ncls; j += NT) {
+    s_cinfo[j] = a.cinfo[j];
+    s_cbkt[j] = a.cbkt[j];
+  }
+  for (int j = tid; j <= nlev; j += NT) s_lcb[j] = a.lvl_cls_begin[j];
+  __syncthreads();
+
+  for (int64_t i = blockIdx.x; i < a.n; i += gridDim.x) {
+    // ---- setup: owned chunks' records and priorities in registers --------
+    const uint8_t *grt = a.routes + (size_t)i * a.route_stride;
+    const uint32_t *gpr = a.prio + (size_t)i * a.prio_stride;
+    uint32_t rw0[CPT], rcl[CPT][3], pr[CPT][kFastMaxHops], hmap[CPT];
+    bool unrouted = false;
+#pragma unroll
+    for (int j = 0; j < CPT; j++) {
+      const int c = tid + NT * j;
+      rw0[j] = 0;
+      rcl[j][0] = rcl[j][1] = rcl[j][2] = 0;
+      if (c < C) {
+        const uint32_t k = grt[c];
+        const uint32_t cp = a.cpath[c];
+#pragma unroll
+        for (int h = 0; h < kFastMaxHops; h++)
+          pr[j][h] = h < H ? gpr[(size_t)c * H + h] : 0u;
+        const uint32_t np = cp >> 24;
+        if (np) {
+          if (k < np) {
+            const uint4 r = *(const uint4 *)(a.arec + 4 * (size_t)((cp & 0xFFFFFFu) + k));
+            rw0[j] = r.x;
+            rcl[j][0] = r.y;
+            rcl[j][1] = r.z;
+            rcl[j][2] = r.w;
+          } else {
+            unrouted = true;  // the pair is left unrouted
+          }
+        }
+        ctime[c] = 0;
+      }
+      // level -> hop index (3 bits per level, 7 = none)
+      hmap[j] = 0xFFFFFFu;
+      const int hops = rw0[j] & 0xFF;
+#pragma unroll
+      for (int t = 0; t < kFastMaxHops; t++)
+        if (t < hops) {
+          const uint32_t lv = (rw0[j] >> (8 + 3 * t)) & 7;
+          hmap[j] = (hmap[j] & ~(7u << (3 * lv))) | ((uint32_t)t << (3 * lv));
+        }
+    }
+    for (int l = tid; l < E; l += NT) lfree[l] = 0;
+    const bool any_unrouted = __syncthreads_or(unrouted);
+
+    uint32_t mk = 0;
+    for (int L = 0; L < nlev; L++) {
+      const uint32_t lo = s_lcb[L];
+      const int ncl = (int)(s_lcb[L + 1] - lo);
+      // buckets of this level: after its last class's first bucket
+      const uint32_t lastb = s_cbkt[lo + ncl - 1];
+      const int NB = ncl ? (int)((lastb & 0xFFFFFF) + (1u << (lastb >> 24))) : 0;
+      for (int j = tid; j <= NB; j += NT) bcnt[j] = 0;
+      for (int l = tid; l < E; l += NT) lfree[E + l] = kUnset;
+      __syncthreads();
+
+      // ---- A. the level's sends per bucket ---------------------------------
+      int bk[CPT];
+      uint32_t slot[CPT], pl[CPT], loc[CPT];
+#pragma unroll
+      for (int j = 0; j < CPT; j++) {
+        bk[j] = -1;
+        const int h = (int)((hmap[j] >> (3 * L)) & 7);  // 7: no hop at this level
+        if (h < kFastMaxHops) {
+          uint32_t cw = rcl[j][0], pv = pr[j][0];
+#pragma unroll
+          for (int t = 1; t < kFastMaxHops; t++)
+            if (h == t) pv = pr[j][t];
+          if (h >= 2) cw = rcl[j][1];
+          if (h >= 4) cw = rcl[j][2];
+          const uint32_t cls = (h & 1) ? (cw >> 16) : (cw & 0xFFFF);
+          const uint32_t cb = s_cbkt[cls];
+          const uint32_t bits = cb >> 24;
+          loc[j] = cls - lo;
+          pl[j] = pv;
+          bk[j] = (int)((cb & 0xFFFFFF) + (bits ? (pv >> (32 - bits)) : 0u));
+          slot[j] = atomicAdd(&bcnt[bk[j]], 1u);
+        }
+      }
+      __syncthreads();
+      // ---- B. bucket starts --------------------------------------------------
+      block_excl_scan(bcnt, NB, red);
+      const uint32_t tot = bcnt[NB];
+      // ---- C. scatter --------------------------------------------------------
+#pragma unroll
+      for (int j = 0; j < CPT; j++)
+        if (bk[j] >= 0) {
+          const uint32_t pos = bcnt[bk[j]] + slot[j];
+          epr[pos] = pl[j];
+          ech[pos] = (uint16_t)(tid + NT * j);
+        }
+      __syncthreads();
+      // ---- D. order inside buckets by (priority, chunk); record each send's
+      //      link and its index in the link's run -----------------------------
+#pragma unroll
+      for (int j = 0; j < CPT; j++)
+        if (bk[j] >= 0) {
+          const uint32_t b0 = bcnt[bk[j]], b1 = bcnt[bk[j] + 1];
+          const uint32_t c = tid + NT * j, px = pl[j];
+          uint32_t rank = 0;
+          for (uint32_t y = b0; y < b1; y++) {
+            const uint32_t py = epr[y], cy = ech[y];
+            rank += (py < px) || (py == px && cy < c);
+          }
+          const uint32_t ci = s_cinfo[lo + loc[j]];
+          const uint32_t start = bcnt[s_cbkt[lo + (ci >> 16)] & 0xFFFFFF];
+          const uint32_t pos = b0 + rank;
+          pinfo[pos] = c | ((pos - start) << 16);
+          plink[pos] = (uint16_t)(ci & 0xFFFF);
+        }
+      __syncthreads();
+      // ---- E. finish times of every link run (segmented prefix max) ---------
+      const uint32_t ept = (tot + NT - 1) / NT;  // <= CPT: a level has <= C sends
+      const uint32_t x0 = min((uint32_t)tid * ept, tot), x1 = min(x0 + ept, tot);
+      // E1: this thread's tail aggregate
+      uint64_t agg = 0;
+      bool seen_head = false;
+#pragma unroll
+      for (int q = 0; q < CPT; q++) {
+        const uint32_t x = x0 + q;
+        if (x < x1) {
+          const uint32_t pi = pinfo[x];
+          const uint32_t k = pi >> 16;
+          const uint64_t g =
+              (uint64_t)ctime[pi & 0xFFFF] + kBias - (uint64_t)k * s_cost[plink[x]];
+          if (k == 0) {
+            agg = g;
+            seen_head = true;
+          } else {
+            agg = max(agg, g);
+          }
+        }
+      }
+      // E2: exclusive segmented-max scan across threads
+      uint64_t v = agg;
+      bool hf = seen_head;
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint64_t tv = shfl_up64(v, o);
+        const bool th = __shfl_up((int)hf, o) != 0;
+        if (lane >= o) {
+          if (!hf) v = max(v, tv);
+          hf = hf || th;
+        }
+      }
+      if (lane == 63) {
+        red64[wave] = v;
+        redf[wave] = hf;
+      }
+      __syncthreads();
+      // inclusive value of the previous lane, then fold in earlier waves
+      uint64_t carry = shfl_up64(v, 1);
+      bool carry_h = __shfl_up((int)hf, 1) != 0;
+      if (lane == 0) {
+        carry = 0;
+        carry_h = false;
+      }
+      if (!carry_h)
+        for (int w = wave - 1; w >= 0; w--) {
+          carry = max(carry, red64[w]);
+          if (redf[w]) break;
+        }
+      // E3: finish times
+      uint64_t run = carry;
+#pragma unroll
+      for (int q = 0; q < CPT; q++) {
+        const uint32_t x = x0 + q;
+        if (x < x1) {
+          const uint32_t pi = pinfo[x];
+          const uint32_t c = pi & 0xFFFF, k = pi >> 16;
+          const uint32_t l = plink[x];
+          const uint32_t cl = s_cost[l];
+          const uint64_t g = (uint64_t)ctime[c] + kBias - (uint64_t)k * cl;
+          run = (k == 0) ? g : max(run, g);
+          const int64_t best = max((int64_t)lfree[l], (int64_t)run - (int64_t)kBias);
+          const uint32_t f = (uint32_t)((int64_t)(k + 1) * cl + best);
+          ctime[c] = f;
+          mk = max(mk, f);
+          const bool last = (x + 1 == tot) || (plink[x + 1] != l);
+          if (last) lfree[E + l] = f;
+        }
+      }
+      __syncthreads();
+      for (int l = tid; l < E; l += NT)
+        if (lfree[E + l] != kUnset) lfree[l] = lfree[E + l];
+      __syncthreads();
+    }
+    // makespan: block max
+    for (int o = 32; o > 0; o >>= 1) mk = max(mk, (uint32_t)__shfl_xor((int)mk, o));
+    if (lane == 0) red[wave] = mk;
+    __syncthreads();
+    if (tid == 0) {
+      uint32_t m = 0;
+      for (int w = 0; w < NT / 64; w++) m = max(m, red[w]);
+      a.makespan[i] = m;
+      a.valid[i] = (uint8_t)!any_unrouted;
+    }
+    __syncthreads();
+  }
+}
+
+}  // namespace
+
+int32_t path_fast_layout(const taccl_plan &p, PathArgs &a) {
+  const int32_t C = p.coll.C, E = p.topo.E;
+  const int32_t M = std::max(p.max_lvl_sends, 1);
+  int32_t off = 0;
+  auto take = [&](int32_t bytes) {
+    int32_t o = off;
+    off = (off + bytes + 15) & ~15;
+    return o;
+  };
+  a.ncls = p.ncls;
+  a.o_fcost = take(4 * E);
+  a.o_fcinfo = take(4 * std::max(p.ncls, 1));
+  a.o_fcbkt = take(4 * std::max(p.ncls, 1));
+  a.o_flcb = take(4 * (p.nlev + 1));
+  a.o_fctime = take(4 * C);
+  a.o_flfree = take(8 * E);
+  a.o_fbcnt = take(4 * (p.max_lvl_nb + 1));
+  a.o_fepr = take(4 * M);
+  a.o_fech = take(2 * M);
+  a.o_fsrt = take(4 * M);
+  a.o_fscl = take(2 * M + 2);  // one spare entry read past the end
+  a.o_fred = take(4 * 2 * (kPathFastThreads / 64));
+  a.o_fred64 = take(8 * (kPathFastThreads / 64));
+  a.o_fredf = take(4 * (kPathFastThreads / 64));
+  a.lds_bytes = off;
+  return off;
+}
+
+int path_fast_cpt(const taccl_plan &p) {
+  const int per = (p.coll.C + kPathFastThreads - 1) / kPathFastThreads;
+  return per <= 1 ? 1 : per <= 2 ? 2 : per <= 4 ? 4 : per <= 8 ? 8 : 0;
+}
+
+hipError_t launch_path_fast(const PathArgs &a, int cpt, int grid, hipStream_t stream) {
+  const dim3 g(grid), b(kPathFastThreads);
+  switch (cpt) {
+    case 1: hipLaunchKernelGGL(path_eval_fast<1>, g, b, a.lds_bytes, stream, a); break;
+    case 2: hipLaunchKernelGGL(path_eval_fast<2>, g, b, a.lds_bytes, stream, a); break;
+    case 4: hipLaunchKernelGGL(path_eval_fast<4>, g, b, a.lds_bytes, stream, a); break;
+    case 8: hipLaunchKernelGGL(path_eval_fast<8>, g, b, a.lds_bytes, stream, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace taccl

@@ -54,19 +54,28 @@ struct PathArgs {
   int64_t n;
   int32_t o_rt, o_ctime, o_lfree, o_ccnt, o_cbase, o_ccur, o_echunk, o_eprio, o_ecls, o_sorted,
       o_red;
+  // register-resident kernel
+  int32_t ncls;
+  const uint32_t *arec, *cpath, *cinfo, *cbkt;
+  int32_t o_fcost, o_fcinfo, o_fcbkt, o_flcb, o_fctime, o_flfree, o_fbcnt, o_fepr, o_fech, o_fsrt, o_fscl,
+      o_fred, o_fred64, o_fredf;
   int32_t lds_bytes;
 };
 
 constexpr int kTreeMaxThreads = 512;  // up to 8 wavefronts per block
 constexpr int kTreeRecLdsMax = 32768;  // route records kept in LDS up to this size
 constexpr int kPathThreads = 256;
+constexpr int kPathFastThreads = 512;
 
 // Fill the LDS layout; returns the bytes needed by a one-wavefront block.
 int32_t tree_layout(const taccl_plan &p, TreeArgs &a);
 int32_t tree_block_bytes(const TreeArgs &a, int waves);
 int32_t path_layout(const taccl_plan &p, PathArgs &a);
+int32_t path_fast_layout(const taccl_plan &p, PathArgs &a);
+int path_fast_cpt(const taccl_plan &p);  // chunks per thread, 0 = too many
 
 hipError_t launch_tree(const TreeArgs &a, int grid, hipStream_t stream);
 hipError_t launch_path(const PathArgs &a, int grid, hipStream_t stream);
+hipError_t launch_path_fast(const PathArgs &a, int cpt, int grid, hipStream_t stream);
 
 }  // namespace taccl

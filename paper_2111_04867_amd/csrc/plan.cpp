@@ -316,6 +316,68 @@ static taccl_status_t build_levels(taccl_plan *p) {
     }
   for (int32_t L = 0; L < p->nlev; L++)
     p->max_lvl_sends = std::max<int32_t>(p->max_lvl_sends, (int32_t)per_level[L]);
+
+  // compact tables of the register-resident kernel (paths of <= 6 hops,
+  // <= 8 levels, <= 2^24 route options)
+  p->path_fast = p->H <= kFastMaxHops && p->nlev <= 8 && npath < (1u << 24) &&
+                 p->coll.C <= kFastMaxChunks;
+  if (p->path_fast) {
+    p->arec.assign(npath * 4, 0);
+    for (size_t q = 0; q < npath; q++) {
+      if (!used_path[q]) continue;
+      uint32_t *r = &p->arec[q * 4];
+      uint64_t rem = p->path_cost[q];
+      int32_t h = 0;
+      for (uint32_t j = p->path_off[q]; j < p->path_off[q + 1]; j++, h++) {
+        r[0] |= (uint32_t)level_of(rem) << (8 + 3 * h);
+        r[1 + h / 2] |= (uint32_t)p->hop_class[j] << (16 * (h & 1));
+        rem -= p->cost[p->path_links[j]];
+      }
+      r[0] |= (uint32_t)h;
+    }
+    const int32_t C = p->coll.C, cpr = p->coll.cpr;
+    p->cpath.assign(C, 0);
+    for (int32_t ch = 0; ch < C; ch++) {
+      const int32_t pair = ch / cpr, s = pair / P, d = pair % P;
+      if (s == d) continue;
+      const size_t pp = (size_t)s * P + d;
+      p->cpath[ch] = p->pair_base[pp] | ((uint32_t)p->npaths[pp] << 24);
+    }
+    // priority sub-buckets per class, sized from the class's expected
+    // membership under uniform route choice so a bucket holds 1-2 sends
+    // (any input stays exact: a crowded bucket is only slower to order)
+    std::vector<double> expect(p->ncls, 0.0);
+    for (int32_t s2 = 0; s2 < P; s2++)
+      for (int32_t d2 = 0; d2 < P; d2++) {
+        if (s2 == d2) continue;
+        const size_t pp = (size_t)s2 * P + d2;
+        const int32_t np = p->npaths[pp];
+        for (int32_t k = 0; k < np; k++) {
+          const uint32_t q = p->pair_base[pp] + k;
+          for (uint32_t j = p->path_off[q]; j < p->path_off[q + 1]; j++)
+            expect[p->hop_class[j]] += (double)cpr / np;
+        }
+      }
+    p->cbkt.assign(p->ncls, 0);
+    p->max_lvl_nb = 1;
+    for (int32_t L = 0; L < p->nlev; L++) {
+      uint32_t nb = 0;
+      for (uint32_t k = p->lvl_cls_begin[L]; k < p->lvl_cls_begin[L + 1]; k++) {
+        int bits = 0;
+        while (bits < 10 && (double)(2u << bits) <= expect[k]) bits++;
+        p->cbkt[k] = nb | ((uint32_t)bits << 24);
+        nb += 1u << bits;
+      }
+      p->max_lvl_nb = std::max<int32_t>(p->max_lvl_nb, (int32_t)nb);
+    }
+    p->cinfo.assign(p->ncls, 0);
+    for (int32_t L = 0; L < p->nlev; L++)
+      for (uint32_t k = p->lvl_cls_begin[L]; k < p->lvl_cls_begin[L + 1]; k++) {
+        const uint32_t l = p->cls_link[k];
+        const uint32_t first = p->llc[((size_t)L * E + l) * 2];
+        p->cinfo[k] = l | ((first - p->lvl_cls_begin[L]) << 16);
+      }
+  }
   return TACCL_OK;
 }
 
@@ -557,7 +619,7 @@ taccl_status_t taccl_sketch_apply(taccl_topology_t topo, taccl_collective_t coll
   }
   if (coll->kind == TACCL_ALLTOALL) {
     PathArgs a{};
-    p->path_lds = path_layout(*p, a);
+    p->path_lds = (p->path_fast && path_fast_cpt(*p)) ? path_fast_layout(*p, a) : path_layout(*p, a);
   } else {
     TreeArgs a{};
     p->tree_lds = tree_layout(*p, a);

@@ -11,6 +11,10 @@
 
 namespace taccl {
 
+// Limits of the register-resident Alltoall kernel.
+constexpr int kFastMaxHops = 6;
+constexpr int kFastMaxChunks = 4096;
+
 // Set the thread-local error message and return the status.
 taccl_status_t fail(taccl_status_t st, const std::string &msg);
 
@@ -49,6 +53,7 @@ struct DeviceTables {
   const int8_t *path_lvl_hop = nullptr;
   const uint32_t *lvl_cls_begin = nullptr;
   const uint32_t *llc = nullptr;
+  const uint32_t *arec = nullptr, *cpath = nullptr, *cinfo = nullptr, *cbkt = nullptr;
   int max_lds = 0;  // bytes of LDS a block may use on this device
   int lds_per_cu = 0;
   int num_cus = 0;
@@ -92,6 +97,15 @@ struct taccl_plan {
   std::vector<uint32_t> lvl_cls_begin; // [nlev+1]
   std::vector<uint32_t> llc;           // [nlev*E*2] class range of a link at a level
   std::vector<uint16_t> cls_link;      // [ncls]
+  // register-resident Alltoall kernel: per route option {hops | level of
+  // hop h << (8+3h), classes of hops 0..5 as u16 pairs}; per chunk its pair's
+  // first option | option count << 24; per class link | (first class of the
+  // same level and link, level-relative) << 16
+  bool path_fast = false;
+  std::vector<uint32_t> arec, cpath, cinfo;
+  // per class: first priority sub-bucket (level-relative) | bits << 24
+  std::vector<uint32_t> cbkt;
+  int32_t max_lvl_nb = 0;
 
   // launch shape
   int32_t tree_lds = 0, path_lds = 0;
