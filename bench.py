@@ -8,8 +8,10 @@ HBM. Prints one JSON line (rank 0).
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
 """
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -20,6 +22,39 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 DEFAULT_WORKLOAD = "twonode16_ag"
+
+
+# Kernel that dominates each workload's launch (the only kernel it runs).
+KERNEL_OF = {"ring4_ag": "tree_eval", "cubemesh8_ag": "tree_eval", "twonode16_ag": "tree_eval",
+             "switch16_a2a": "path_eval_fast", "fournode64_a2a": "path_eval_fast"}
+
+
+def csrc_digest():
+    """SHA-256 over the library sources; measured HBM traffic is only reported
+    while the sources are the ones the counters were taken from."""
+    d = os.path.join(ROOT, "paper_2111_04867_amd", "csrc")
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".hip", ".cpp", ".h")):
+            h.update(f.encode())
+            with open(os.path.join(d, f), "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload):
+    """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated) from the
+    committed counter summary of this workload's kernel, or None when that
+    summary is missing or was taken from different sources."""
+    path = os.path.join(ROOT, "profiles", f"{KERNEL_OF.get(workload, '?')}_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    src = re.search(r"^csrc_sha256: ([0-9a-f]{64})$", text, re.M)
+    val = re.search(r"^traffic_bytes_per_launch: ([0-9]+)$", text, re.M)
+    if not src or not val or src.group(1) != csrc_digest():
+        return None
+    return int(val.group(1))
 
 
 def log(msg):
@@ -139,7 +174,10 @@ def main():
                    "chunk_bytes": w.chunk_bytes, "bytes_per_candidate":
                        plan.bytes_per_candidate, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None},
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": measured_traffic(w.name),
+                     "algorithmic_bytes_per_launch": bytes_launch,
+                     "kernel": KERNEL_OF.get(w.name)},
     }
     if not args.no_all:
         table = {}
