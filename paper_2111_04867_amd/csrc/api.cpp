@@ -48,7 +48,7 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
          o_plh = pk.add(p->path_lvl_hop), o_lcb = pk.add(p->lvl_cls_begin),
          o_llc = pk.add(p->llc), o_trec = pk.add(p->tree_rec), o_own8 = pk.add(p->owner8),
          o_arec = pk.add(p->arec), o_cpath = pk.add(p->cpath), o_cinfo = pk.add(p->cinfo),
-         o_cbkt = pk.add(p->cbkt);
+         o_cbkt = pk.add(p->cbkt), o_topt = pk.add(p->topt);
   void *blk = nullptr;
   e = hipMalloc(&blk, pk.bytes.size());
   if (e != hipSuccess) return fail(TACCL_ERR_NO_MEMORY, "hipMalloc of plan tables failed");
@@ -75,6 +75,7 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
   t.llc = (const uint32_t *)at(o_llc);
   t.tree_rec = (const uint32_t *)at(o_trec);
   t.owner8 = (const uint8_t *)at(o_own8);
+  t.topt = p->topt.empty() ? nullptr : (const uint8_t *)at(o_topt);
   t.arec = (const uint32_t *)at(o_arec);
   t.cpath = (const uint32_t *)at(o_cpath);
   t.cinfo = (const uint32_t *)at(o_cinfo);
@@ -180,13 +181,17 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     a.rec = t->tree_rec;
     a.npaths = t->npaths;
     a.owner8 = t->owner8;
+    a.topt = t->topt;
     a.post_mask = t->post_mask;
     a.routes = d_routes;
     a.prio = d_prio;
     a.makespan = d_makespan;
     a.valid = d_valid;
     a.n = n;
-    if (tree_layout(*p, a) > t->max_lds)
+    // the layered kernel needs whole route words and priorities in registers
+    const bool layered = a.routes_word_aligned && tree_layers_layout(*p, a) > 0 &&
+                         tree_block_bytes(a, 1) <= t->max_lds;
+    if (!layered && tree_layout(*p, a) > t->max_lds)
       return fail(TACCL_ERR_UNSUPPORTED, "multicast plan needs more LDS than a block has");
     // wavefronts per block: most resident wavefronts per CU within the LDS
     int best_w = 1, best_res = 0, best_bpc = 1;
@@ -204,7 +209,7 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     a.waves_per_block = best_w;
     const int64_t want = (n + best_w - 1) / best_w;
     const int tgrid = (int)std::min<int64_t>(want, (int64_t)std::max(t->num_cus, 1) * best_bpc);
-    e = launch_tree(a, tgrid, s);
+    e = layered ? launch_tree_layers(a, tgrid, s) : launch_tree(a, tgrid, s);
   }
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
   return TACCL_OK;

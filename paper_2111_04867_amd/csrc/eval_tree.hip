@@ -74,13 +74,87 @@ __device__ __forceinline__ uint32_t div_v(uint32_t n, uint32_t m) {
   return (uint32_t)(((uint64_t)n * m) >> 32);
 }
 
+// Lane = chunk: the routed paths of the chunk (destinations ascending) are
+// merged into a tree by first reach, one send per reached vertex (one
+// is_sent per chunk and link, App. B.1); distances from the owner (the
+// travelled path of Sec. 5.1) ride along each path in registers. Then one
+// reverse sweep over the discovery order (children come after their
+// parents) gives the longest remaining tree path below each vertex (the
+// remaining path of Sec. 5.1) and writes every send's packed Step-2 key
+// (~rem << 32 | trav, ascending = rem desc, trav asc) over the vertex's dead
+// distance slot. kMasks also sets the chunk's bit in its link's mask.
+// par[] must be zero on entry; returns whether every chunk reached its
+// postcondition ranks.
+template <bool kMasks>
+__device__ __forceinline__ bool build_trees(const TreeArgs &a, const uint32_t *s_rec,
+                                            const uint32_t *s_cost, const uint8_t *s_own,
+                                            const uint64_t *s_post, const uint8_t *rt,
+                                            uint64_t *key, uint16_t *par, uint32_t *ord,
+                                            uint32_t *lmask, int lane) {
+  const int C = a.C, P = a.P, V = a.V, K = a.K, H = a.H, MW = a.mask_words;
+  uint32_t *dh = (uint32_t *)key;  // dh[2s] = dist, dh[2s+1] = height
+  bool ok = true;
+  for (int c = lane; c < C; c += 64) {
+    const int o = s_own[c];
+    const uint64_t pm = s_post[c];
+    const int base = c * V;
+    uint64_t reached = 1ull << o;
+    int cnt = 0;
+    dh[2 * (base + o)] = 0;
+    dh[2 * (base + o) + 1] = 0;
+    for (int d = 0; d < P; d++) {
+      if (d == o || !((pm >> d) & 1)) continue;
+      const int k = rt[c * P + d];
+      if (k >= K) continue;  // pair left unrouted (no such option)
+      const uint32_t *r = s_rec + ((o * P + d) * K + k) * H;
+      const uint32_t w0 = r[0];
+      const int hops = w0 >> 24;  // 0: the pair has no option k
+      int u = o;
+      uint32_t du = 0;  // distance of u when `known`
+      bool known = true;
+      for (int j = 0; j < hops; j++) {
+        const uint32_t w = j ? r[j] : w0;
+        const int l = w & 0xFFFF;
+        const int v = (w >> 16) & 0xFF;
+        if (!((reached >> v) & 1)) {
+          if (!known) du = dh[2 * (base + u)];
+          du += s_cost[l];
+          known = true;
+          reached |= 1ull << v;
+          par[base + v] = (uint16_t)(l + 1);
+          dh[2 * (base + v)] = du;
+          dh[2 * (base + v) + 1] = 0;
+          ord[base + cnt++] = (uint32_t)v | ((uint32_t)u << 8) | ((uint32_t)l << 16);
+        } else {
+          known = false;
+        }
+        u = v;
+      }
+    }
+    ok &= (reached & pm) == pm;
+    // reverse discovery order visits children before their parents: a
+    // vertex's height is final when it is visited, and its parent's
+    // distance is still in place
+    for (int j = cnt - 1; j >= 0; j--) {
+      const uint32_t e = ord[base + j];
+      const int v = e & 0xFF, u = (e >> 8) & 0xFF, l = e >> 16;
+      const uint32_t rem = s_cost[l] + dh[2 * (base + v) + 1];
+      const uint32_t trav = dh[2 * (base + u)];
+      if (rem > dh[2 * (base + u) + 1]) dh[2 * (base + u) + 1] = rem;
+      key[base + v] = ((uint64_t)(~rem) << 32) | trav;
+      if (kMasks) atomicOr(&lmask[l * MW + (c >> 5)], 1u << (c & 31));
+    }
+  }
+  return ok;
+}
+
 // kRecLds: the route records fit in LDS (else they are read from global
 // memory, where they stay cache resident). kPrefetch: a candidate's routes
 // (whole words) and priorities fit the prefetch registers.
 template <bool kRecLds, bool kPrefetch>
 __global__ __launch_bounds__(kTreeMaxThreads) void tree_eval_kernel(TreeArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
-  const int C = a.C, P = a.P, V = a.V, E = a.E, K = a.K, H = a.H, MW = a.mask_words;
+  const int C = a.C, V = a.V, E = a.E, MW = a.mask_words;
   const int CV = C * V;
 
   // ---- block-wide copy of the plan tables --------------------------------
@@ -113,7 +187,6 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_eval_kernel(TreeArgs a) 
   uint8_t *rt = wl + a.w_rt;
   uint32_t *rt32 = (uint32_t *)rt;
   uint64_t *key = (uint64_t *)(wl + a.w_key);
-  uint32_t *dh = (uint32_t *)key;  // dh[2s] = dist, dh[2s+1] = height
   uint32_t *prio = (uint32_t *)(wl + a.w_prio);
   uint32_t *fin = prio;
   uint32_t *chain = (uint32_t *)(wl + a.w_chain);
@@ -172,58 +245,8 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_eval_kernel(TreeArgs a) 
     wave_sync();
 
     // ---- 2+3. lane = chunk: first-reach tree, then heights and keys -------
-    bool ok = true;
-    for (int c = lane; c < C; c += 64) {
-      const int o = s_own[c];
-      const uint64_t pm = s_post[c];
-      const int base = c * V;
-      uint64_t reached = 1ull << o;
-      int cnt = 0;
-      dh[2 * (base + o)] = 0;
-      dh[2 * (base + o) + 1] = 0;
-      for (int d = 0; d < P; d++) {
-        if (d == o || !((pm >> d) & 1)) continue;
-        const int k = rt[c * P + d];
-        if (k >= K) continue;  // pair left unrouted (no such option)
-        const uint32_t *r = s_rec + ((o * P + d) * K + k) * H;
-        const uint32_t w0 = r[0];
-        const int hops = w0 >> 24;  // 0: the pair has no option k
-        int u = o;
-        uint32_t du = 0;  // distance of u when `known`
-        bool known = true;
-        for (int j = 0; j < hops; j++) {
-          const uint32_t w = j ? r[j] : w0;
-          const int l = w & 0xFFFF;
-          const int v = (w >> 16) & 0xFF;
-          if (!((reached >> v) & 1)) {
-            if (!known) du = dh[2 * (base + u)];
-            du += s_cost[l];
-            known = true;
-            reached |= 1ull << v;
-            par[base + v] = (uint16_t)(l + 1);
-            dh[2 * (base + v)] = du;
-            dh[2 * (base + v) + 1] = 0;
-            ord[base + cnt++] = (uint32_t)v | ((uint32_t)u << 8) | ((uint32_t)l << 16);
-          } else {
-            known = false;
-          }
-          u = v;
-        }
-      }
-      ok &= (reached & pm) == pm;
-      // reverse discovery order visits children before their parents: a
-      // vertex's height is final when it is visited, and its parent's
-      // distance is still in place
-      for (int j = cnt - 1; j >= 0; j--) {
-        const uint32_t e = ord[base + j];
-        const int v = e & 0xFF, u = (e >> 8) & 0xFF, l = e >> 16;
-        const uint32_t rem = s_cost[l] + dh[2 * (base + v) + 1];
-        const uint32_t trav = dh[2 * (base + u)];
-        if (rem > dh[2 * (base + u) + 1]) dh[2 * (base + u) + 1] = rem;
-        key[base + v] = ((uint64_t)(~rem) << 32) | trav;  // ascending = rem desc, trav asc
-        atomicOr(&lmask[l * MW + (c >> 5)], 1u << (c & 31));
-      }
-    }
+    const bool ok = build_trees<true>(a, s_rec, s_cost, s_own, s_post, rt, key, par, ord,
+                                      lmask, lane);
     wave_sync();
     {
       // link bases: exclusive scan of the mask popcounts
@@ -332,6 +355,384 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_eval_kernel(TreeArgs a) 
   }
 }
 
+
+// Layered variant for plans with at most 4 hops and 8 options per pair,
+// 4 | P <= 32 and C*V <= 1024.
+//
+// Trees, one lane per (chunk c, vertex v) slot. Merging the destinations'
+// paths by first reach in ascending destination order gives v the hop that
+// enters it on the path of the smallest destination whose path contains v;
+// that destination is found from the route bytes and a plan table of the
+// options passing through each vertex, with no walk. Distances from the
+// owner follow in rounds (a slot waits for its parent's distance), then the
+// largest distance below each vertex is pushed up the tree deepest level
+// first; a send into v from u then has trav = dist(u) and
+// rem = cost + height(v) = maxdist_below(v) - dist(u) (Sec. 5.1).
+//
+// Order and timing. A send's layer is floor(rem / c_min) (computed as
+// (rem * ceil(2^32 / c_min)) >> 32). Along a tree edge rem grows by at
+// least one link cost, so a send's parent send lies in a higher layer; a
+// link's Step-2 order sorts by rem first, so the sends of one layer on one
+// link are a contiguous run of that link's order. Taking the layers from
+// the top down, every dependency inside a layer runs along a link run, and
+// the k-th send of a run with ready times r_j, cost c and link busy time F
+// finishes at
+//     f_k = max(F + (k+1)c, max_{j<=k} r_j + (k-j+1)c),
+// the unrolled form of f = max(ready, link free) + c (App. B.3).
+// The sends are counting-sorted by (non-empty layer from the top, link)
+// with 16-bit counters, each bucket is ordered by the full key
+// (rem, trav, priority, chunk), and the layers are timed in turn, one lane
+// per send.
+template <int J, int PW>
+__global__ __launch_bounds__(kTreeMaxThreads) void tree_layers_kernel(TreeArgs a) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int C = a.C, V = a.V, E = a.E, K = a.K, H = a.H;
+  constexpr int P = 4 * PW;  // ranks; route bytes per chunk
+  const int CV = C * V;
+
+  uint32_t *s_cost = (uint32_t *)(lds + a.o_cost);
+  uint8_t *s_src = lds + a.o_src;
+  uint8_t *s_own = lds + a.o_own;
+  uint64_t *s_post = (uint64_t *)(lds + a.o_post);
+  uint4 *s_rec = (uint4 *)(lds + a.o_rec4);       // one 16-byte record per option
+  uint32_t *s_opt = (uint32_t *)(lds + a.o_opt);  // option bytes, PW words per (o, v)
+  for (int j = threadIdx.x; j < E; j += blockDim.x) {
+    s_cost[j] = a.cost[j];
+    s_src[j] = (uint8_t)a.lsrc[j];
+  }
+  for (int r = threadIdx.x; r < P * P * K; r += blockDim.x) {
+    const uint32_t *g = a.rec + (size_t)r * H;
+    s_rec[r] = make_uint4(g[0], H > 1 ? g[1] : 0u, H > 2 ? g[2] : 0u, H > 3 ? g[3] : 0u);
+  }
+  for (int j = threadIdx.x; j < P * V * PW; j += blockDim.x)
+    s_opt[j] = ((const uint32_t *)a.topt)[j];
+  for (int j = threadIdx.x; j < C; j += blockDim.x) {
+    s_own[j] = a.owner8[j];
+    s_post[j] = a.post_mask[j];
+  }
+  __syncthreads();
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  unsigned char *wl = lds + a.o_wave + wave * a.wave_bytes;
+  // Regions reused as their contents die. Trees: route words and per-slot
+  // distances (later the largest distance below). Bucketing: 16-bit
+  // counters, then bucket entries {~rem, trav, priority, slot}. Ordered
+  // sends: slot | parent send's slot << 16 and link | index in its run
+  // << 16. Timing: finish times per slot and ready times per position.
+  uint32_t *rt32 = (uint32_t *)wl;
+  uint32_t *dist = (uint32_t *)(wl + a.w_dist);
+  uint32_t *cnt = (uint32_t *)(wl + a.w_cnt);
+  uint4 *erec = (uint4 *)(wl + a.w_erec);
+  uint32_t *ord2 = (uint32_t *)(wl + a.w_ord2);
+  uint32_t *info2 = (uint32_t *)(wl + a.w_info2);
+  uint32_t *fin = (uint32_t *)(wl + a.w_fin);
+  uint32_t *rq = (uint32_t *)(wl + a.w_rq);
+  uint32_t *lfree = (uint32_t *)(wl + a.w_free);
+  uint64_t *lmask64 = (uint64_t *)(wl + a.w_lmask);
+  uint32_t *lst = (uint32_t *)(wl + a.w_lst);  // first ordered position of each layer
+  auto start_of = [&](uint32_t b) -> uint32_t {
+    return (cnt[b >> 1] >> ((b & 1) << 4)) & 0xFFFFu;
+  };
+
+  const int64_t stride = (int64_t)gridDim.x * a.waves_per_block;
+  const int64_t first = (int64_t)blockIdx.x * a.waves_per_block + wave;
+  const int nrw = a.route_stride >> 2;
+  uint32_t pf_r[kPfRoute], pf_p[J];
+  // the next candidate's routes and priorities stream into registers while
+  // the current one is evaluated
+  auto prefetch = [&](int64_t i) {
+    if (i >= a.n) return;
+    const uint32_t *g32 = (const uint32_t *)(a.routes + (size_t)i * a.route_stride);
+    const uint32_t *gpr = a.prio + (size_t)i * a.prio_stride;
+#pragma unroll
+    for (int k = 0; k < kPfRoute; k++) {
+      const int j = lane + 64 * k;
+      if (j < nrw) pf_r[k] = __builtin_nontemporal_load(g32 + j);
+    }
+#pragma unroll
+    for (int k = 0; k < J; k++) {
+      const int j = lane + 64 * k;
+      if (j < CV) pf_p[k] = __builtin_nontemporal_load(gpr + j);
+    }
+  };
+  prefetch(first);
+  for (int64_t i = first; i < a.n; i += stride) {
+    // ---- stage: routes to LDS, own slots' priorities stay in registers --
+#pragma unroll
+    for (int k = 0; k < kPfRoute; k++) {
+      const int j = lane + 64 * k;
+      if (j < nrw) rt32[j] = pf_r[k];
+    }
+    uint32_t px[J];
+#pragma unroll
+    for (int k = 0; k < J; k++) px[k] = pf_p[k];
+    prefetch(i + stride);
+    for (int l = lane; l < E; l += 64) lfree[l] = 0;
+    if (lane == 0) *lmask64 = 0;
+    wave_sync();
+
+    // ---- trees: the hop into every reached (chunk, vertex) ---------------
+    // pe: link | parent vertex << 16 of the send into the slot, ~0 if none
+    uint32_t pe[J], ps[J], dv[J];
+    bool bad = false;
+#pragma unroll
+    for (int j = 0; j < J; j++) {
+      const uint32_t sl = lane + 64 * j;
+      pe[j] = ~0u;
+      ps[j] = kNoPred;
+      dv[j] = kNotYet;
+      if (sl < (uint32_t)CV) {
+        const uint32_t c = div_v(sl, a.vmagic), v = sl - c * V;
+        const uint32_t o = s_own[c];
+        if (v == o) {
+          dist[sl] = 0;
+        } else {
+          uint32_t kw[PW], ow[PW];
+#pragma unroll
+          for (int w = 0; w < PW; w++) {
+            kw[w] = rt32[c * PW + w];
+            ow[w] = s_opt[(o * V + v) * PW + w];
+          }
+          // destinations whose drawn path passes through v
+          uint32_t m = 0;
+#pragma unroll
+          for (int d = 0; d < P; d++) {
+            const uint32_t kd = (kw[d >> 2] >> (8 * (d & 3))) & 0xFFu;
+            const uint32_t od = (ow[d >> 2] >> (8 * (d & 3))) & 0xFFu;
+            m |= ((od >> min(kd, 8u)) & 1u) << d;
+          }
+          const uint64_t pm = s_post[c];
+          m &= (uint32_t)pm;  // only postcondition destinations are routed
+          if (m) {
+            const uint32_t d = __builtin_ctz(m);
+            const uint32_t kd = (kw[d >> 2] >> (8 * (d & 3))) & 0xFFu;
+            const uint4 r = s_rec[(o * P + d) * K + kd];
+            const uint32_t x0 = r.x & 0xFFFFFFu, x1 = r.y, x2 = r.z, x3 = r.w;
+            uint32_t e, u;
+            if ((x0 >> 16) == v) {
+              e = x0; u = o;
+            } else if (((x1 >> 16) & 0xFFu) == v) {
+              e = x1; u = (x0 >> 16) & 0xFFu;
+            } else if (((x2 >> 16) & 0xFFu) == v) {
+              e = x2; u = (x1 >> 16) & 0xFFu;
+            } else {
+              e = x3; u = (x2 >> 16) & 0xFFu;
+            }
+            const uint32_t l = e & 0xFFFFu;
+            pe[j] = l | (u << 16);
+            if (u == o) {
+              dv[j] = s_cost[l];
+              dist[sl] = dv[j];
+            } else {
+              ps[j] = c * V + u;
+              dist[sl] = kNotYet;
+            }
+          } else if ((pm >> v) & 1) {
+            bad = true;  // a rank of the postcondition is never reached
+          }
+        }
+      }
+    }
+    wave_sync();
+    // distances: a slot takes its parent's once that is known
+    uint32_t dep[J];
+#pragma unroll
+    for (int j = 0; j < J; j++) dep[j] = (pe[j] != ~0u) ? 1u : 0u;
+    bool fault = false;
+    for (int round = 2;; round++) {
+      bool pend = false;
+#pragma unroll
+      for (int j = 0; j < J; j++)
+        if (dv[j] == kNotYet && pe[j] != ~0u) {
+          const uint32_t du = lds_get(&dist[ps[j]]);
+          if (du != kNotYet) {
+            dv[j] = du + s_cost[pe[j] & 0xFFFFu];
+            lds_put(&dist[lane + 64 * j], dv[j]);
+            dep[j] = round;
+          } else {
+            pend = true;
+          }
+        }
+      if (__ballot(pend) == 0) break;
+      if (round > V) {  // unreachable: parents form a tree
+        fault = true;
+        break;
+      }
+    }
+    // largest distance below each vertex, deepest sends first
+    uint32_t dmax = 0;
+#pragma unroll
+    for (int j = 0; j < J; j++) dmax = max(dmax, dep[j]);
+    dmax = wave_max(dmax);
+    wave_sync();
+    for (uint32_t t = dmax; t >= 2; t--) {
+#pragma unroll
+      for (int j = 0; j < J; j++)
+        if (dep[j] == t) atomicMax(&dist[ps[j]], lds_get(&dist[lane + 64 * j]));
+      wave_sync();
+    }
+
+    // ---- keys and layers of this lane's sends ----------------------------
+    uint32_t bl[J];  // link | layer << 16, or ~0 for no send
+    uint64_t kk[J];
+    uint64_t lm = 0;
+    bool clamped = false;
+#pragma unroll
+    for (int j = 0; j < J; j++) {
+      bl[j] = ~0u;
+      kk[j] = 0;
+      if (pe[j] != ~0u) {
+        const uint32_t l = pe[j] & 0xFFFFu;
+        const uint32_t trav = dv[j] - s_cost[l];
+        const uint32_t rem = lds_get(&dist[lane + 64 * j]) - trav;
+        uint32_t L = (uint32_t)(((uint64_t)rem * a.lmagic) >> 32);
+        if (L >= (uint32_t)a.nl_max) {  // unreachable: rem is bounded at plan time
+          L = a.nl_max - 1;
+          clamped = true;
+        }
+        bl[j] = l | (L << 16);
+        kk[j] = ((uint64_t)(~rem) << 32) | trav;  // ascending = rem desc, trav asc
+        lm |= 1ull << L;
+      }
+    }
+    if (lm) atomicOr((unsigned long long *)lmask64, (unsigned long long)lm);
+    wave_sync();
+    const uint64_t layers = *lmask64;
+    const int nl = __popcll(layers);
+    const uint32_t NB = (uint32_t)nl * E;  // buckets (layer from the top, link)
+    const int NW = (int)((NB + 2) >> 1);   // u16 counters for NB + 1 starts
+    for (int w = lane; w < NW; w += 64) cnt[w] = 0;
+    wave_sync();
+
+    // ---- counting sort by (layer from the top, link) ---------------------
+    uint32_t bb[J], idx[J];
+#pragma unroll
+    for (int k = 0; k < J; k++) {
+      bb[k] = 0;
+      idx[k] = 0;
+      if (bl[k] != ~0u) {
+        const uint32_t L = bl[k] >> 16;
+        const uint32_t above = (uint32_t)__popcll((layers >> L) >> 1);
+        const uint32_t b = above * E + (bl[k] & 0xFFFFu);
+        const uint32_t sh = (b & 1) << 4;
+        const uint32_t old = atomicAdd(&cnt[b >> 1], 1u << sh);
+        bb[k] = b;
+        idx[k] = (old >> sh) & 0xFFFFu;
+      }
+    }
+    wave_sync();
+    {
+      // exclusive scan over the 16-bit counters
+      const int per = (NW + 63) >> 6;
+      const int w0 = min(lane * per, NW), w1 = min(w0 + per, NW);
+      uint32_t sum = 0;
+      for (int w = w0; w < w1; w++) {
+        const uint32_t x = cnt[w];
+        sum += (x & 0xFFFFu) + (x >> 16);
+      }
+      const uint32_t incl = wave_incl_scan(sum, lane);
+      uint32_t run = incl - sum;
+      for (int w = w0; w < w1; w++) {
+        const uint32_t x = cnt[w];
+        const uint32_t lo = x & 0xFFFFu;
+        cnt[w] = run | ((run + lo) << 16);
+        run += lo + (x >> 16);
+      }
+    }
+    wave_sync();
+    uint32_t b0[J], b1[J];
+#pragma unroll
+    for (int k = 0; k < J; k++) {
+      b0[k] = b1[k] = 0;
+      if (bl[k] != ~0u) {
+        b0[k] = start_of(bb[k]);
+        b1[k] = start_of(bb[k] + 1);
+      }
+    }
+    for (int ly = lane; ly <= nl; ly += 64) lst[ly] = start_of((uint32_t)ly * E);
+    wave_sync();  // the counters are dead from here on
+#pragma unroll
+    for (int k = 0; k < J; k++)
+      if (bl[k] != ~0u)
+        erec[b0[k] + idx[k]] = make_uint4((uint32_t)(kk[k] >> 32), (uint32_t)kk[k], px[k],
+                                          (uint32_t)(lane + 64 * k));
+    wave_sync();
+
+    // ---- order inside each bucket by (rem, trav, priority, chunk) --------
+#pragma unroll
+    for (int k = 0; k < J; k++) {
+      if (bl[k] != ~0u) {
+        const uint32_t sl = lane + 64 * k;
+        const uint64_t kx = kk[k];
+        // every send of a link enters the same vertex: slot order = chunk order
+        const uint64_t qx = ((uint64_t)px[k] << 32) | sl;
+        uint32_t rank = 0;
+        // four members per step; indexes past the bucket are clamped to its
+        // last entry (always loaded, never counted) so the loads issue together
+        for (uint32_t y = b0[k]; y < b1[k]; y += 4) {
+          uint4 m[4];
+#pragma unroll
+          for (int t = 0; t < 4; t++) m[t] = erec[min(y + t, b1[k] - 1)];
+#pragma unroll
+          for (int t = 0; t < 4; t++) {
+            const uint64_t ky = ((uint64_t)m[t].x << 32) | m[t].y;
+            const uint64_t qy = ((uint64_t)m[t].z << 32) | m[t].w;
+            rank += (uint32_t)((y + t < b1[k]) & ((ky < kx) | ((ky == kx) & (qy < qx))));
+          }
+        }
+        const uint32_t q = b0[k] + rank;
+        ord2[q] = sl | (ps[k] << 16);
+        info2[q] = (pe[k] & 0xFFFFu) | (rank << 16);
+      }
+    }
+    wave_sync();
+
+    // ---- least schedule, layer by layer ----------------------------------
+    uint32_t mk = 0;
+    for (int ly = 0; ly < nl; ly++) {
+      const uint32_t qs = lst[ly], qe = lst[ly + 1];
+      // ready time of every send of the layer: its parent send is in a
+      // layer above
+      for (uint32_t q = qs + lane; q < qe; q += 64) {
+        const uint32_t pj = ord2[q] >> 16;
+        rq[q] = (pj == kNoPred) ? 0u : fin[pj];
+      }
+      wave_sync();
+      for (uint32_t q = qs + lane; q < qe; q += 64) {
+        const uint32_t inf = info2[q];
+        const uint32_t l = inf & 0xFFFFu, k = inf >> 16;
+        const uint32_t cl = s_cost[l];
+        uint32_t f = lfree[l] + (k + 1) * cl;
+        // earlier sends of the run, four at a time
+        for (uint32_t j = q - k; j <= q; j += 4) {
+          uint32_t r[4];
+#pragma unroll
+          for (int t = 0; t < 4; t++) r[t] = rq[min(j + t, q)];
+#pragma unroll
+          for (int t = 0; t < 4; t++) {
+            const uint32_t jt = min(j + t, q);  // a repeat of q adds nothing new
+            f = max(f, r[t] + (q - jt + 1) * cl);
+          }
+        }
+        fin[ord2[q] & 0xFFFFu] = f;
+        mk = max(mk, f);
+        if (q + 1 == qe || (info2[q + 1] >> 16) == 0) lfree[l] = f;
+      }
+      wave_sync();
+    }
+
+    // ---- postcondition and makespan ---------------------------------------
+    const bool all_ok = __ballot(bad) == 0;
+    const bool failed = __ballot(clamped || fault) != 0;
+    mk = wave_max(mk);
+    if (lane == 0) {
+      a.makespan[i] = failed ? 0xFFFFFFFFu : mk;
+      a.valid[i] = (uint8_t)(all_ok && !failed);
+    }
+    wave_sync();
+  }
+}
+
 int32_t align16(int32_t x) { return (x + 15) & ~15; }
 
 }  // namespace
@@ -397,4 +798,81 @@ hipError_t launch_tree(const TreeArgs &a, int grid, hipStream_t stream) {
   return hipGetLastError();
 }
 
+int32_t tree_layers_layout(const taccl_plan &p, TreeArgs &a) {
+  if (tree_layout(p, a) <= 0) return 0;
+  const int32_t C = p.coll.C, V = p.topo.V, E = p.topo.E, P = p.topo.P;
+  const int32_t CV = C * V;
+  const int32_t K = std::max(p.max_paths, 1), H = std::max(p.H, 1);
+  const int32_t pw = P / 4;  // route words per chunk: 1, 2, 4 or 8
+  if (p.topt.empty() || K > 8 || H > 4 || P % 4 || (pw != 1 && pw != 2 && pw != 4 && pw != 8) ||
+      V > 64 || E < 1 ||
+      CV > 64 * 16 || p.route_stride > 4 * 64 * kPfRoute)
+    return 0;
+  uint64_t cmin = ~0ull, cmax = 0;
+  for (uint32_t c : p.cost) {
+    cmin = std::min<uint64_t>(cmin, c);
+    cmax = std::max<uint64_t>(cmax, c);
+  }
+  if (cmin == 0) return 0;  // layers need every link cost to be positive
+  // rem is at most the cost of a tree path: V - 1 links
+  const uint64_t max_rem = (uint64_t)(V - 1) * cmax;
+  if (max_rem >= (1ull << 32)) return 0;
+  a.lmagic = ((1ull << 32) + cmin - 1) / cmin;  // ceil(2^32 / c_min) <= 2^32
+  const uint64_t nl = ((max_rem * a.lmagic) >> 32) + 1;
+  if (nl > 64) return 0;
+  a.nl_max = (int32_t)nl;
+  // shared tables: 16-byte route records and the option bytes
+  int32_t off = a.o_rec;  // replaces the fixed-stride records
+  a.o_rec4 = off;
+  off = align16(off + 16 * P * P * K);
+  a.o_opt = off;
+  off = align16(off + P * V * P);
+  a.o_wave = off;
+  const int32_t S = std::max<int64_t>(std::min<int64_t>(p.max_sends, CV), 1);
+  // region X: route words and distances, then bucket entries, then finish
+  // and ready times
+  const int32_t x_tree = align16(p.route_stride) + align16(4 * CV);
+  a.w_dist = align16(p.route_stride);
+  a.w_erec = 0;
+  a.w_fin = 0;
+  a.w_rq = align16(4 * CV);
+  const int32_t x = std::max({x_tree, align16(16 * S), a.w_rq + align16(4 * S)});
+  // region Y: bucket counters, then the ordered sends
+  a.w_cnt = x;
+  a.w_ord2 = x;
+  a.w_info2 = x + align16(4 * S);
+  int32_t w = x + std::max(align16(4 * (int32_t)((nl * E + 2) / 2)), 2 * align16(4 * S));
+  a.w_free = w;
+  w = align16(w + 4 * E);
+  a.w_lmask = w;
+  w = align16(w + 8);
+  a.w_lst = w;
+  w = align16(w + 4 * 65);
+  a.wave_bytes = w;
+  return a.o_wave + a.wave_bytes;
+}
+
+template <int J>
+static void launch_layers_j(const TreeArgs &a, dim3 g, dim3 b, int bytes, hipStream_t stream) {
+  switch (a.P / 4) {
+    case 1: hipLaunchKernelGGL((tree_layers_kernel<J, 1>), g, b, bytes, stream, a); break;
+    case 2: hipLaunchKernelGGL((tree_layers_kernel<J, 2>), g, b, bytes, stream, a); break;
+    case 4: hipLaunchKernelGGL((tree_layers_kernel<J, 4>), g, b, bytes, stream, a); break;
+    default: hipLaunchKernelGGL((tree_layers_kernel<J, 8>), g, b, bytes, stream, a); break;
+  }
+}
+
+hipError_t launch_tree_layers(const TreeArgs &a, int grid, hipStream_t stream) {
+  const int pw = a.P / 4;
+  if (a.P % 4 || (pw != 1 && pw != 2 && pw != 4 && pw != 8)) return hipErrorInvalidValue;
+  const dim3 g(grid), b(64 * a.waves_per_block);
+  const int bytes = tree_block_bytes(a, a.waves_per_block);
+  const int J = (a.C * a.V + 63) / 64;
+  if (J <= 1) launch_layers_j<1>(a, g, b, bytes, stream);
+  else if (J <= 2) launch_layers_j<2>(a, g, b, bytes, stream);
+  else if (J <= 4) launch_layers_j<4>(a, g, b, bytes, stream);
+  else if (J <= 8) launch_layers_j<8>(a, g, b, bytes, stream);
+  else launch_layers_j<16>(a, g, b, bytes, stream);
+  return hipGetLastError();
+}
 }  // namespace taccl

@@ -33,6 +33,12 @@ struct TreeArgs {
   // per-wavefront state (byte offsets from the wavefront's base)
   int32_t w_rt, w_key, w_prio, w_chain, w_par, w_mask, w_base, w_head, w_free;
   int32_t wave_bytes;
+  // layered variant: layer of a send = (rem * lmagic) >> 32, below nl_max
+  uint64_t lmagic;
+  int32_t nl_max;
+  const uint8_t *topt;  // options of (o, d) through vertex v, one byte per d
+  int32_t o_rec4, o_opt;
+  int32_t w_dist, w_cnt, w_erec, w_rq, w_lst, w_ord2, w_info2, w_fin, w_lmask;
 };
 
 // Alltoall evaluation: one block per candidate, level by level.
@@ -70,11 +76,15 @@ constexpr int kPathFastThreads = 512;
 // Fill the LDS layout; returns the bytes needed by a one-wavefront block.
 int32_t tree_layout(const taccl_plan &p, TreeArgs &a);
 int32_t tree_block_bytes(const TreeArgs &a, int waves);
+// Layered multicast kernel: fills the layout and returns the bytes of a
+// one-wavefront block, or 0 when the plan does not meet its conditions.
+int32_t tree_layers_layout(const taccl_plan &p, TreeArgs &a);
 int32_t path_layout(const taccl_plan &p, PathArgs &a);
 int32_t path_fast_layout(const taccl_plan &p, PathArgs &a);
 int path_fast_cpt(const taccl_plan &p);  // chunks per thread, 0 = too many
 
 hipError_t launch_tree(const TreeArgs &a, int grid, hipStream_t stream);
+hipError_t launch_tree_layers(const TreeArgs &a, int grid, hipStream_t stream);
 hipError_t launch_path(const PathArgs &a, int grid, hipStream_t stream);
 hipError_t launch_path_fast(const PathArgs &a, int cpt, int grid, hipStream_t stream);
 

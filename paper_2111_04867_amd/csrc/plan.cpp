@@ -437,6 +437,21 @@ static taccl_status_t build_layout(taccl_plan *p) {
       }
     p->owner8.resize(C);
     for (int32_t ch = 0; ch < C; ch++) p->owner8[ch] = (uint8_t)c.owner[ch];
+    p->topt.clear();
+    if (K <= 8) {
+      p->topt.assign((size_t)P * V * P, 0);
+      for (int32_t o = 0; o < P; o++)
+        for (int32_t d = 0; d < P; d++) {
+          const int32_t pp = o * P + d;
+          for (int32_t k = 0; k < p->npaths[pp]; k++) {
+            const uint32_t q = p->pair_base[pp] + k;
+            for (uint32_t j = p->path_off[q]; j < p->path_off[q + 1]; j++) {
+              const int32_t v = p->ldst[p->path_links[j]];
+              p->topt[((size_t)o * V + v) * P + d] |= (uint8_t)(1u << k);
+            }
+          }
+        }
+    }
   }
   return TACCL_OK;
 }
