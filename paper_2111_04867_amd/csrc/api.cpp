@@ -48,7 +48,7 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
          o_plh = pk.add(p->path_lvl_hop), o_lcb = pk.add(p->lvl_cls_begin),
          o_llc = pk.add(p->llc), o_trec = pk.add(p->tree_rec), o_own8 = pk.add(p->owner8),
          o_arec = pk.add(p->arec), o_cpath = pk.add(p->cpath), o_cinfo = pk.add(p->cinfo),
-         o_cbkt = pk.add(p->cbkt), o_topt = pk.add(p->topt);
+         o_cbkt = pk.add(p->cbkt), o_topt = pk.add(p->topt), o_trec4 = pk.add(p->tree_rec4);
   void *blk = nullptr;
   e = hipMalloc(&blk, pk.bytes.size());
   if (e != hipSuccess) return fail(TACCL_ERR_NO_MEMORY, "hipMalloc of plan tables failed");
@@ -76,6 +76,7 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
   t.tree_rec = (const uint32_t *)at(o_trec);
   t.owner8 = (const uint8_t *)at(o_own8);
   t.topt = p->topt.empty() ? nullptr : (const uint8_t *)at(o_topt);
+  t.tree_rec4 = p->tree_rec4.empty() ? nullptr : (const uint32_t *)at(o_trec4);
   t.arec = (const uint32_t *)at(o_arec);
   t.cpath = (const uint32_t *)at(o_cpath);
   t.cinfo = (const uint32_t *)at(o_cinfo);
@@ -182,6 +183,7 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     a.npaths = t->npaths;
     a.owner8 = t->owner8;
     a.topt = t->topt;
+    a.rec4 = (const uint4 *)t->tree_rec4;
     a.post_mask = t->post_mask;
     a.routes = d_routes;
     a.prio = d_prio;
@@ -193,12 +195,18 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
                          tree_block_bytes(a, 1) <= t->max_lds;
     if (!layered && tree_layout(*p, a) > t->max_lds)
       return fail(TACCL_ERR_UNSUPPORTED, "multicast plan needs more LDS than a block has");
-    // wavefronts per block: most resident wavefronts per CU within the LDS
+    // wavefronts per block: most resident wavefronts per CU (LDS, and for
+    // the layered kernel registers too, by the runtime's occupancy query)
     int best_w = 1, best_res = 0, best_bpc = 1;
     for (int w = 1; w <= kTreeMaxThreads / 64; w++) {
       const int bytes = tree_block_bytes(a, w);
       if (bytes > t->max_lds) break;
-      const int bpc = std::min(t->lds_per_cu / bytes, 32 / w);
+      int bpc = std::min(t->lds_per_cu / bytes, 32 / w);
+      if (layered) {
+        a.waves_per_block = w;
+        const int nb = tree_layers_blocks_per_cu(a);
+        if (nb > 0) bpc = std::min(bpc, nb);
+      }
       const int res = std::min(bpc * w, 32);
       if (res > best_res) {
         best_res = res;

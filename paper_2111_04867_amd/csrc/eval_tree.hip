@@ -384,9 +384,10 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_eval_kernel(TreeArgs a) 
 // (rem, trav, priority, chunk), and the layers are timed in turn, one lane
 // per send.
 template <int J, int PW>
-__global__ __launch_bounds__(kTreeMaxThreads) void tree_layers_kernel(TreeArgs a) {
+__global__ __launch_bounds__(kTreeMaxThreads)
+void tree_layers_kernel(TreeArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
-  const int C = a.C, V = a.V, E = a.E, K = a.K, H = a.H;
+  const int C = a.C, V = a.V, E = a.E, K = a.K;
   constexpr int P = 4 * PW;  // ranks; route bytes per chunk
   const int CV = C * V;
 
@@ -400,10 +401,7 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_layers_kernel(TreeArgs a
     s_cost[j] = a.cost[j];
     s_src[j] = (uint8_t)a.lsrc[j];
   }
-  for (int r = threadIdx.x; r < P * P * K; r += blockDim.x) {
-    const uint32_t *g = a.rec + (size_t)r * H;
-    s_rec[r] = make_uint4(g[0], H > 1 ? g[1] : 0u, H > 2 ? g[2] : 0u, H > 3 ? g[3] : 0u);
-  }
+  for (int r = threadIdx.x; r < P * P * K; r += blockDim.x) s_rec[r] = a.rec4[r];
   for (int j = threadIdx.x; j < P * V * PW; j += blockDim.x)
     s_opt[j] = ((const uint32_t *)a.topt)[j];
   for (int j = threadIdx.x; j < C; j += blockDim.x) {
@@ -430,6 +428,7 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_layers_kernel(TreeArgs a
   uint32_t *lfree = (uint32_t *)(wl + a.w_free);
   uint64_t *lmask64 = (uint64_t *)(wl + a.w_lmask);
   uint32_t *lst = (uint32_t *)(wl + a.w_lst);  // first ordered position of each layer
+  uint32_t *bnd = (uint32_t *)(wl + a.w_bnd);  // bucket start | end << 16 per position
   auto start_of = [&](uint32_t b) -> uint32_t {
     return (cnt[b >> 1] >> ((b & 1) << 4)) & 0xFFFFu;
   };
@@ -458,10 +457,20 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_layers_kernel(TreeArgs a
   prefetch(first);
   for (int64_t i = first; i < a.n; i += stride) {
     // ---- stage: routes to LDS, own slots' priorities stay in registers --
+    // route bytes become one-hot option bytes (1 << choice, 0 for a choice
+    // of 8 or more, which no pair has)
 #pragma unroll
     for (int k = 0; k < kPfRoute; k++) {
       const int j = lane + 64 * k;
-      if (j < nrw) rt32[j] = pf_r[k];
+      if (j < nrw) {
+        uint32_t oh = 0;
+#pragma unroll
+        for (int b = 0; b < 4; b++) {
+          const uint32_t kb = (pf_r[k] >> (8 * b)) & 0xFFu;
+          oh |= (kb < 8 ? (1u << kb) : 0u) << (8 * b);
+        }
+        rt32[j] = oh;
+      }
     }
     uint32_t px[J];
 #pragma unroll
@@ -493,19 +502,22 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_layers_kernel(TreeArgs a
             kw[w] = rt32[c * PW + w];
             ow[w] = s_opt[(o * V + v) * PW + w];
           }
-          // destinations whose drawn path passes through v
+          // destinations whose drawn path passes through v: a byte of
+          // (chosen option bit & options through v) is non-zero
           uint32_t m = 0;
 #pragma unroll
-          for (int d = 0; d < P; d++) {
-            const uint32_t kd = (kw[d >> 2] >> (8 * (d & 3))) & 0xFFu;
-            const uint32_t od = (ow[d >> 2] >> (8 * (d & 3))) & 0xFFu;
-            m |= ((od >> min(kd, 8u)) & 1u) << d;
+          for (int w = 0; w < PW; w++) {
+            const uint32_t t = kw[w] & ow[w];
+            uint32_t nz = ((t + 0x7F7F7F7Fu) & 0x80808080u) >> 7;  // bit 8b per byte b
+            nz |= nz >> 7;
+            nz |= nz >> 14;
+            m |= (nz & 0xFu) << (4 * w);
           }
           const uint64_t pm = s_post[c];
           m &= (uint32_t)pm;  // only postcondition destinations are routed
           if (m) {
             const uint32_t d = __builtin_ctz(m);
-            const uint32_t kd = (kw[d >> 2] >> (8 * (d & 3))) & 0xFFu;
+            const uint32_t kd = __builtin_ctz((kw[d >> 2] >> (8 * (d & 3))) & 0xFFu);
             const uint4 r = s_rec[(o * P + d) * K + kd];
             const uint32_t x0 = r.x & 0xFFFFFFu, x1 = r.y, x2 = r.z, x3 = r.w;
             uint32_t e, u;
@@ -651,39 +663,51 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_layers_kernel(TreeArgs a
     }
     for (int ly = lane; ly <= nl; ly += 64) lst[ly] = start_of((uint32_t)ly * E);
     wave_sync();  // the counters are dead from here on
+    // bucket entries {key lo, key hi, slot | link << 10, priority}: inside a
+    // bucket the link is fixed, so (priority, third word) orders as
+    // (priority, slot), and slot order is chunk order (every send of a link
+    // enters the same vertex)
 #pragma unroll
     for (int k = 0; k < J; k++)
-      if (bl[k] != ~0u)
-        erec[b0[k] + idx[k]] = make_uint4((uint32_t)(kk[k] >> 32), (uint32_t)kk[k], px[k],
-                                          (uint32_t)(lane + 64 * k));
+      if (bl[k] != ~0u) {
+        const uint32_t pos = b0[k] + idx[k];
+        erec[pos] = make_uint4((uint32_t)kk[k], (uint32_t)(kk[k] >> 32),
+                               (uint32_t)(lane + 64 * k) | ((bl[k] & 0xFFFFu) << 10), px[k]);
+        bnd[pos] = b0[k] | (b1[k] << 16);
+      }
     wave_sync();
 
     // ---- order inside each bucket by (rem, trav, priority, chunk) --------
+    // one lane per ordered position, so a pass waits only for the largest
+    // bucket among its 64 positions
+    const uint32_t total = lst[nl];
+    for (uint32_t x = lane; x < total; x += 64) {
+      const uint4 rx = erec[x];
+      const uint32_t bd = bnd[x];
+      const uint32_t bs = bd & 0xFFFFu, be = bd >> 16;
+      const uint64_t kx = ((uint64_t)rx.y << 32) | rx.x;
+      const uint64_t qx = ((uint64_t)rx.w << 32) | rx.z;
+      uint32_t rank = 0;
+      // four members per step; the array has three spare entries past its
+      // end, so the loads need no clamping (entries past the bucket never count)
+      for (uint32_t y = bs; y < be; y += 4) {
+        uint4 m[4];
 #pragma unroll
-    for (int k = 0; k < J; k++) {
-      if (bl[k] != ~0u) {
-        const uint32_t sl = lane + 64 * k;
-        const uint64_t kx = kk[k];
-        // every send of a link enters the same vertex: slot order = chunk order
-        const uint64_t qx = ((uint64_t)px[k] << 32) | sl;
-        uint32_t rank = 0;
-        // four members per step; indexes past the bucket are clamped to its
-        // last entry (always loaded, never counted) so the loads issue together
-        for (uint32_t y = b0[k]; y < b1[k]; y += 4) {
-          uint4 m[4];
+        for (int t = 0; t < 4; t++) m[t] = erec[y + t];
 #pragma unroll
-          for (int t = 0; t < 4; t++) m[t] = erec[min(y + t, b1[k] - 1)];
-#pragma unroll
-          for (int t = 0; t < 4; t++) {
-            const uint64_t ky = ((uint64_t)m[t].x << 32) | m[t].y;
-            const uint64_t qy = ((uint64_t)m[t].z << 32) | m[t].w;
-            rank += (uint32_t)((y + t < b1[k]) & ((ky < kx) | ((ky == kx) & (qy < qx))));
-          }
+        for (int t = 0; t < 4; t++) {
+          const uint64_t ky = ((uint64_t)m[t].y << 32) | m[t].x;
+          const uint64_t qy = ((uint64_t)m[t].w << 32) | m[t].z;
+          rank += (uint32_t)((y + t < be) & ((ky < kx) | ((ky == kx) & (qy < qx))));
         }
-        const uint32_t q = b0[k] + rank;
-        ord2[q] = sl | (ps[k] << 16);
-        info2[q] = (pe[k] & 0xFFFFu) | (rank << 16);
       }
+      const uint32_t sl = rx.z & 0x3FFu, l = rx.z >> 10;
+      const uint32_t c = div_v(sl, a.vmagic);
+      const uint32_t u = s_src[l];
+      const uint32_t pred = (u == s_own[c]) ? kNoPred : c * V + u;
+      const uint32_t q = bs + rank;
+      ord2[q] = sl | (pred << 16);
+      info2[q] = l | (rank << 16);
     }
     wave_sync();
 
@@ -806,7 +830,7 @@ int32_t tree_layers_layout(const taccl_plan &p, TreeArgs &a) {
   const int32_t pw = P / 4;  // route words per chunk: 1, 2, 4 or 8
   if (p.topt.empty() || K > 8 || H > 4 || P % 4 || (pw != 1 && pw != 2 && pw != 4 && pw != 8) ||
       V > 64 || E < 1 ||
-      CV > 64 * 16 || p.route_stride > 4 * 64 * kPfRoute)
+      CV > 64 * 16 || p.route_stride > 4 * 64 * kPfRoute || E > (1 << 22))
     return 0;
   uint64_t cmin = ~0ull, cmax = 0;
   for (uint32_t c : p.cost) {
@@ -821,8 +845,10 @@ int32_t tree_layers_layout(const taccl_plan &p, TreeArgs &a) {
   const uint64_t nl = ((max_rem * a.lmagic) >> 32) + 1;
   if (nl > 64) return 0;
   a.nl_max = (int32_t)nl;
-  // shared tables: 16-byte route records and the option bytes
-  int32_t off = a.o_rec;  // replaces the fixed-stride records
+  if (p.tree_rec4.empty()) return 0;
+  // shared tables: 16-byte route records and the option bytes, in place of
+  // the fixed-stride records
+  int32_t off = a.o_rec;
   a.o_rec4 = off;
   off = align16(off + 16 * P * P * K);
   a.o_opt = off;
@@ -836,12 +862,13 @@ int32_t tree_layers_layout(const taccl_plan &p, TreeArgs &a) {
   a.w_erec = 0;
   a.w_fin = 0;
   a.w_rq = align16(4 * CV);
-  const int32_t x = std::max({x_tree, align16(16 * S), a.w_rq + align16(4 * S)});
-  // region Y: bucket counters, then the ordered sends
+  const int32_t x = std::max({x_tree, align16(16 * (S + 3)), a.w_rq + align16(4 * S)});
+  // region Y: bucket counters, then the ordered sends and bucket bounds
   a.w_cnt = x;
   a.w_ord2 = x;
   a.w_info2 = x + align16(4 * S);
-  int32_t w = x + std::max(align16(4 * (int32_t)((nl * E + 2) / 2)), 2 * align16(4 * S));
+  a.w_bnd = x + 2 * align16(4 * S);
+  int32_t w = x + std::max(align16(4 * (int32_t)((nl * E + 2) / 2)), 3 * align16(4 * S));
   a.w_free = w;
   w = align16(w + 4 * E);
   a.w_lmask = w;
@@ -860,6 +887,34 @@ static void launch_layers_j(const TreeArgs &a, dim3 g, dim3 b, int bytes, hipStr
     case 4: hipLaunchKernelGGL((tree_layers_kernel<J, 4>), g, b, bytes, stream, a); break;
     default: hipLaunchKernelGGL((tree_layers_kernel<J, 8>), g, b, bytes, stream, a); break;
   }
+}
+
+template <int J>
+static const void *layers_fn_j(int pw) {
+  switch (pw) {
+    case 1: return (const void *)tree_layers_kernel<J, 1>;
+    case 2: return (const void *)tree_layers_kernel<J, 2>;
+    case 4: return (const void *)tree_layers_kernel<J, 4>;
+    default: return (const void *)tree_layers_kernel<J, 8>;
+  }
+}
+
+static const void *layers_fn(const TreeArgs &a) {
+  const int J = (a.C * a.V + 63) / 64, pw = a.P / 4;
+  if (J <= 1) return layers_fn_j<1>(pw);
+  if (J <= 2) return layers_fn_j<2>(pw);
+  if (J <= 4) return layers_fn_j<4>(pw);
+  if (J <= 8) return layers_fn_j<8>(pw);
+  return layers_fn_j<16>(pw);
+}
+
+int tree_layers_blocks_per_cu(const TreeArgs &a) {
+  int nb = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, layers_fn(a), 64 * a.waves_per_block,
+                                                   tree_block_bytes(a, a.waves_per_block)) !=
+      hipSuccess)
+    return 0;
+  return nb;
 }
 
 hipError_t launch_tree_layers(const TreeArgs &a, int grid, hipStream_t stream) {

@@ -37,8 +37,9 @@ struct TreeArgs {
   uint64_t lmagic;
   int32_t nl_max;
   const uint8_t *topt;  // options of (o, d) through vertex v, one byte per d
+  const uint4 *rec4;    // route records, one 16-byte record per option
   int32_t o_rec4, o_opt;
-  int32_t w_dist, w_cnt, w_erec, w_rq, w_lst, w_ord2, w_info2, w_fin, w_lmask;
+  int32_t w_dist, w_cnt, w_erec, w_rq, w_lst, w_bnd, w_ord2, w_info2, w_fin, w_lmask;
 };
 
 // Alltoall evaluation: one block per candidate, level by level.
@@ -85,6 +86,8 @@ int path_fast_cpt(const taccl_plan &p);  // chunks per thread, 0 = too many
 
 hipError_t launch_tree(const TreeArgs &a, int grid, hipStream_t stream);
 hipError_t launch_tree_layers(const TreeArgs &a, int grid, hipStream_t stream);
+// resident blocks per CU of the layered kernel at a.waves_per_block
+int tree_layers_blocks_per_cu(const TreeArgs &a);
 hipError_t launch_path(const PathArgs &a, int grid, hipStream_t stream);
 hipError_t launch_path_fast(const PathArgs &a, int cpt, int grid, hipStream_t stream);
 

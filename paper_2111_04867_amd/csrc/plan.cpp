@@ -437,6 +437,12 @@ static taccl_status_t build_layout(taccl_plan *p) {
       }
     p->owner8.resize(C);
     for (int32_t ch = 0; ch < C; ch++) p->owner8[ch] = (uint8_t)c.owner[ch];
+    p->tree_rec4.clear();
+    if (H <= 4) {
+      p->tree_rec4.assign((size_t)P * P * K * 4, 0);
+      for (size_t r = 0; r < (size_t)P * P * K; r++)
+        for (int32_t j = 0; j < H; j++) p->tree_rec4[r * 4 + j] = p->tree_rec[r * H + j];
+    }
     p->topt.clear();
     if (K <= 8) {
       p->topt.assign((size_t)P * V * P, 0);

@@ -50,6 +50,7 @@ struct DeviceTables {
   const uint32_t *tree_rec = nullptr;
   const uint8_t *owner8 = nullptr;
   const uint8_t *topt = nullptr;
+  const uint32_t *tree_rec4 = nullptr;
   const uint16_t *hop_class = nullptr;
   const int8_t *path_lvl_hop = nullptr;
   const uint32_t *lvl_cls_begin = nullptr;
@@ -93,6 +94,9 @@ struct taccl_plan {
   // [(o*V + v)*P + d]: bit k set when option k of pair (o, d) passes
   // through vertex v (v != o); empty unless every pair has at most 8 options
   std::vector<uint8_t> topt;
+  // the route records again with 4 words per option (zero padded), for
+  // plans with at most 4 hops
+  std::vector<uint32_t> tree_rec4;
 
   // Alltoall (path) evaluation: levels of equal remaining cost
   int32_t nlev = 0, ncls = 0, max_lvl_cls = 0, max_lvl_sends = 0;
