@@ -159,9 +159,12 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     a.cbkt = t->cbkt;
     const int cpt = p->path_fast ? path_fast_cpt(*p) : 0;
     if (cpt && path_fast_layout(*p, a) <= t->max_lds) {
-      const int bpc = std::max(1, std::min(t->lds_per_cu / a.lds_bytes, 4));
+      const int nt = path_fast_threads(*p);
+      int bpc = std::max(1, std::min(t->lds_per_cu / a.lds_bytes, 4));
+      const int nb = path_fast_blocks_per_cu(a, cpt, nt);
+      if (nb > 0) bpc = std::min(bpc, nb);
       const int fgrid = (int)std::min<int64_t>(n, (int64_t)std::max(t->num_cus, 1) * bpc);
-      e = launch_path_fast(a, cpt, fgrid, s);
+      e = launch_path_fast(a, cpt, nt, fgrid, s);
     } else {
       if (path_layout(*p, a) > t->max_lds)
         return fail(TACCL_ERR_UNSUPPORTED, "Alltoall plan needs more LDS than a block has");

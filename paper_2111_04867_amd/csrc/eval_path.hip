@@ -265,11 +265,10 @@ __device__ void block_excl_scan(uint32_t *cnt, int n, uint32_t *wsum) {
   __syncthreads();
 }
 
-template <int CPT>
-__global__ __launch_bounds__(kPathFastThreads) void path_eval_fast(PathArgs a) {
+template <int CPT, int NT>
+__global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  constexpr int NT = kPathFastThreads;
   const int C = a.C, E = a.E, H = a.H, nlev = a.nlev;
 
   uint32_t *s_cost = (uint32_t *)(lds + a.o_fcost);
@@ -281,8 +280,11 @@ __global__ __launch_bounds__(kPathFastThreads) void path_eval_fast(PathArgs a) {
   uint32_t *bcnt = (uint32_t *)(lds + a.o_fbcnt);    // bucket counts, then starts
   uint32_t *epr = (uint32_t *)(lds + a.o_fepr);
   uint16_t *ech = (uint16_t *)(lds + a.o_fech);
-  uint32_t *pinfo = (uint32_t *)(lds + a.o_fsrt);   // chunk | index in its link run << 16
-  uint16_t *plink = (uint16_t *)(lds + a.o_fscl);    // link of every sorted send
+  // sorted sends, chunk | link << cb | index in its link run << (cb + lb),
+  // stored transposed: position t*ept + q of thread t's range at q*NT + t
+  uint32_t *pinfo = (uint32_t *)(lds + a.o_fsrt);
+  const uint32_t cb = a.cbits, lb = a.lbits, kb = cb + lb;
+  const uint32_t cmask = (1u << cb) - 1, lmask = (1u << lb) - 1;
   uint32_t *red = (uint32_t *)(lds + a.o_fred);      // [2][NT/64] scan scratch
   uint64_t *red64 = (uint64_t *)(lds + a.o_fred64);  // [NT/64] segmented max
   uint32_t *redf = (uint32_t *)(lds + a.o_fredf);    // [NT/64] segment-head flags
@@ -364,11 +366,11 @@ __global__ __launch_bounds__(kPathFastThreads) void path_eval_fast(PathArgs a) {
           if (h >= 2) cw = rcl[j][1];
           if (h >= 4) cw = rcl[j][2];
           const uint32_t cls = (h & 1) ? (cw >> 16) : (cw & 0xFFFF);
-          const uint32_t cb = s_cbkt[cls];
-          const uint32_t bits = cb >> 24;
+          const uint32_t cbk = s_cbkt[cls];
+          const uint32_t bits = cbk >> 24;
           loc[j] = cls - lo;
           pl[j] = pv;
-          bk[j] = (int)((cb & 0xFFFFFF) + (bits ? (pv >> (32 - bits)) : 0u));
+          bk[j] = (int)((cbk & 0xFFFFFF) + (bits ? (pv >> (32 - bits)) : 0u));
           slot[j] = atomicAdd(&bcnt[bk[j]], 1u);
         }
       }
@@ -376,6 +378,9 @@ __global__ __launch_bounds__(kPathFastThreads) void path_eval_fast(PathArgs a) {
       // ---- B. bucket starts --------------------------------------------------
       block_excl_scan(bcnt, NB, red);
       const uint32_t tot = bcnt[NB];
+      const uint32_t ept = (tot + NT - 1) / NT;  // <= CPT: a level has <= C sends
+      // pos / ept = (pos * em) >> 32 with em = floor((2^32 - 1) / ept) + 1 <= 2^32
+      const uint64_t em = ept ? 0xFFFFFFFFull / ept + 1 : 0;
       // ---- C. scatter --------------------------------------------------------
 #pragma unroll
       for (int j = 0; j < CPT; j++)
@@ -400,24 +405,31 @@ __global__ __launch_bounds__(kPathFastThreads) void path_eval_fast(PathArgs a) {
           const uint32_t ci = s_cinfo[lo + loc[j]];
           const uint32_t start = bcnt[s_cbkt[lo + (ci >> 16)] & 0xFFFFFF];
           const uint32_t pos = b0 + rank;
-          pinfo[pos] = c | ((pos - start) << 16);
-          plink[pos] = (uint16_t)(ci & 0xFFFF);
+          const uint32_t t = (uint32_t)(((uint64_t)pos * em) >> 32), q = pos - t * ept;
+          pinfo[q * NT + t] = c | ((ci & 0xFFFFu) << cb) | ((pos - start) << kb);
         }
       __syncthreads();
       // ---- E. finish times of every link run (segmented prefix max) ---------
-      const uint32_t ept = (tot + NT - 1) / NT;  // <= CPT: a level has <= C sends
-      const uint32_t x0 = min((uint32_t)tid * ept, tot), x1 = min(x0 + ept, tot);
+      // thread tid owns sorted positions [tid*ept, tid*ept + ept); every load
+      // is issued unmasked (stale entries are clamped to in-range indexes and
+      // never used)
+      const uint32_t x0 = (uint32_t)tid * ept;
+      uint32_t pis[CPT], ct[CPT], cs[CPT];
+#pragma unroll
+      for (int q = 0; q < CPT; q++) pis[q] = pinfo[q * NT + tid];
+#pragma unroll
+      for (int q = 0; q < CPT; q++) {
+        ct[q] = ctime[min(pis[q] & cmask, (uint32_t)C - 1)];
+        cs[q] = s_cost[min((pis[q] >> cb) & lmask, (uint32_t)E - 1)];
+      }
       // E1: this thread's tail aggregate
       uint64_t agg = 0;
       bool seen_head = false;
 #pragma unroll
       for (int q = 0; q < CPT; q++) {
-        const uint32_t x = x0 + q;
-        if (x < x1) {
-          const uint32_t pi = pinfo[x];
-          const uint32_t k = pi >> 16;
-          const uint64_t g =
-              (uint64_t)ctime[pi & 0xFFFF] + kBias - (uint64_t)k * s_cost[plink[x]];
+        if ((uint32_t)q < ept && x0 + q < tot) {
+          const uint32_t k = pis[q] >> kb;
+          const uint64_t g = (uint64_t)ct[q] + kBias - (uint64_t)k * cs[q];
           if (k == 0) {
             agg = g;
             seen_head = true;
@@ -455,23 +467,25 @@ __global__ __launch_bounds__(kPathFastThreads) void path_eval_fast(PathArgs a) {
           if (redf[w]) break;
         }
       // E3: finish times
+      const uint32_t nxt0 = (tid + 1 < NT) ? pinfo[tid + 1] : 0u;  // next thread's first
+      uint32_t lf[CPT];
+#pragma unroll
+      for (int q = 0; q < CPT; q++) lf[q] = lfree[min((pis[q] >> cb) & lmask, (uint32_t)E - 1)];
       uint64_t run = carry;
 #pragma unroll
       for (int q = 0; q < CPT; q++) {
         const uint32_t x = x0 + q;
-        if (x < x1) {
-          const uint32_t pi = pinfo[x];
-          const uint32_t c = pi & 0xFFFF, k = pi >> 16;
-          const uint32_t l = plink[x];
-          const uint32_t cl = s_cost[l];
-          const uint64_t g = (uint64_t)ctime[c] + kBias - (uint64_t)k * cl;
+        if ((uint32_t)q < ept && x < tot) {
+          const uint32_t c = pis[q] & cmask, l = (pis[q] >> cb) & lmask, k = pis[q] >> kb;
+          const uint32_t cl = cs[q];
+          const uint64_t g = (uint64_t)ct[q] + kBias - (uint64_t)k * cl;
           run = (k == 0) ? g : max(run, g);
-          const int64_t best = max((int64_t)lfree[l], (int64_t)run - (int64_t)kBias);
+          const int64_t best = max((int64_t)lf[q], (int64_t)run - (int64_t)kBias);
           const uint32_t f = (uint32_t)((int64_t)(k + 1) * cl + best);
           ctime[c] = f;
           mk = max(mk, f);
-          const bool last = (x + 1 == tot) || (plink[x + 1] != l);
-          if (last) lfree[E + l] = f;
+          const uint32_t nk = ((uint32_t)q + 1 < ept ? pis[q < CPT - 1 ? q + 1 : q] : nxt0) >> kb;
+          if (x + 1 == tot || nk == 0) lfree[E + l] = f;  // last send of the link's run
         }
       }
       __syncthreads();
@@ -514,29 +528,72 @@ int32_t path_fast_layout(const taccl_plan &p, PathArgs &a) {
   a.o_fbcnt = take(4 * (p.max_lvl_nb + 1));
   a.o_fepr = take(4 * M);
   a.o_fech = take(2 * M);
-  a.o_fsrt = take(4 * M);
-  a.o_fscl = take(2 * M + 2);  // one spare entry read past the end
-  a.o_fred = take(4 * 2 * (kPathFastThreads / 64));
+  a.o_fsrt = take(4 * path_fast_threads(p) * path_fast_cpt(p));
+  a.o_fscl = 0;
+  // packed sorted sends: chunk, link and run index in one word
+  auto bits = [](uint32_t n) {  // bits to hold 0 .. n-1
+    uint32_t b = 0;
+    while ((1ull << b) < n) b++;
+    return b;
+  };
+  a.cbits = (int32_t)bits((uint32_t)C);
+  a.lbits = (int32_t)bits((uint32_t)E);
+  a.o_fred = take(4 * 2 * (kPathFastThreads / 64));  // sized for the largest block
   a.o_fred64 = take(8 * (kPathFastThreads / 64));
   a.o_fredf = take(4 * (kPathFastThreads / 64));
   a.lds_bytes = off;
   return off;
 }
 
-int path_fast_cpt(const taccl_plan &p) {
-  const int per = (p.coll.C + kPathFastThreads - 1) / kPathFastThreads;
-  return per <= 1 ? 1 : per <= 2 ? 2 : per <= 4 ? 4 : per <= 8 ? 8 : 0;
+int path_fast_threads(const taccl_plan &p) {
+  const int C = p.coll.C;
+  return C <= 256 ? 256 : C <= 512 ? 512 : kPathFastThreads;
 }
 
-hipError_t launch_path_fast(const PathArgs &a, int cpt, int grid, hipStream_t stream) {
-  const dim3 g(grid), b(kPathFastThreads);
-  switch (cpt) {
-    case 1: hipLaunchKernelGGL(path_eval_fast<1>, g, b, a.lds_bytes, stream, a); break;
-    case 2: hipLaunchKernelGGL(path_eval_fast<2>, g, b, a.lds_bytes, stream, a); break;
-    case 4: hipLaunchKernelGGL(path_eval_fast<4>, g, b, a.lds_bytes, stream, a); break;
-    case 8: hipLaunchKernelGGL(path_eval_fast<8>, g, b, a.lds_bytes, stream, a); break;
-    default: return hipErrorInvalidValue;
-  }
+int path_fast_cpt(const taccl_plan &p) {
+  // a sorted send packs chunk, link and run index (< C) into 32 bits
+  auto bits = [](uint32_t n) {
+    uint32_t b = 0;
+    while ((1ull << b) < n) b++;
+    return b;
+  };
+  if (2 * bits((uint32_t)p.coll.C) + bits((uint32_t)p.topo.E) > 32) return 0;
+  const int nt = path_fast_threads(p);
+  const int per = (p.coll.C + nt - 1) / nt;
+  return per <= 1 ? 1 : per <= 2 ? 2 : per <= 4 ? 4 : 0;
+}
+
+static const void *path_fast_fn(int cpt, int nt) {
+  if (nt == 256 && cpt == 1) return (const void *)path_eval_fast<1, 256>;
+  if (nt == 512 && cpt == 1) return (const void *)path_eval_fast<1, 512>;
+  if (nt == 1024 && cpt == 1) return (const void *)path_eval_fast<1, 1024>;
+  if (nt == 1024 && cpt == 2) return (const void *)path_eval_fast<2, 1024>;
+  if (nt == 1024 && cpt == 4) return (const void *)path_eval_fast<4, 1024>;
+  return nullptr;
+}
+
+int path_fast_blocks_per_cu(const PathArgs &a, int cpt, int nt) {
+  const void *fn = path_fast_fn(cpt, nt);
+  int nb = 0;
+  if (!fn || hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fn, nt, a.lds_bytes) != hipSuccess)
+    return 0;
+  return nb;
+}
+
+hipError_t launch_path_fast(const PathArgs &a, int cpt, int nt, int grid, hipStream_t stream) {
+  const void *fn = path_fast_fn(cpt, nt);
+  if (!fn) return hipErrorInvalidValue;
+  const dim3 g(grid), b(nt);
+  if (nt == 256)
+    hipLaunchKernelGGL((path_eval_fast<1, 256>), g, b, a.lds_bytes, stream, a);
+  else if (nt == 512)
+    hipLaunchKernelGGL((path_eval_fast<1, 512>), g, b, a.lds_bytes, stream, a);
+  else if (cpt == 1)
+    hipLaunchKernelGGL((path_eval_fast<1, 1024>), g, b, a.lds_bytes, stream, a);
+  else if (cpt == 2)
+    hipLaunchKernelGGL((path_eval_fast<2, 1024>), g, b, a.lds_bytes, stream, a);
+  else
+    hipLaunchKernelGGL((path_eval_fast<4, 1024>), g, b, a.lds_bytes, stream, a);
   return hipGetLastError();
 }
 

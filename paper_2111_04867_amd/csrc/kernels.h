@@ -67,12 +67,13 @@ struct PathArgs {
   int32_t o_fcost, o_fcinfo, o_fcbkt, o_flcb, o_fctime, o_flfree, o_fbcnt, o_fepr, o_fech, o_fsrt, o_fscl,
       o_fred, o_fred64, o_fredf;
   int32_t lds_bytes;
+  int32_t cbits, lbits;  // chunk and link fields of a packed sorted send
 };
 
 constexpr int kTreeMaxThreads = 512;  // up to 8 wavefronts per block
 constexpr int kTreeRecLdsMax = 32768;  // route records kept in LDS up to this size
 constexpr int kPathThreads = 256;
-constexpr int kPathFastThreads = 512;
+constexpr int kPathFastThreads = 1024;  // largest block of the register-resident kernel
 
 // Fill the LDS layout; returns the bytes needed by a one-wavefront block.
 int32_t tree_layout(const taccl_plan &p, TreeArgs &a);
@@ -82,13 +83,15 @@ int32_t tree_block_bytes(const TreeArgs &a, int waves);
 int32_t tree_layers_layout(const taccl_plan &p, TreeArgs &a);
 int32_t path_layout(const taccl_plan &p, PathArgs &a);
 int32_t path_fast_layout(const taccl_plan &p, PathArgs &a);
-int path_fast_cpt(const taccl_plan &p);  // chunks per thread, 0 = too many
+int path_fast_cpt(const taccl_plan &p);      // chunks per thread, 0 = not eligible
+int path_fast_threads(const taccl_plan &p);  // threads per block: 256, 512 or 1024
+int path_fast_blocks_per_cu(const PathArgs &a, int cpt, int nt);
 
 hipError_t launch_tree(const TreeArgs &a, int grid, hipStream_t stream);
 hipError_t launch_tree_layers(const TreeArgs &a, int grid, hipStream_t stream);
 // resident blocks per CU of the layered kernel at a.waves_per_block
 int tree_layers_blocks_per_cu(const TreeArgs &a);
 hipError_t launch_path(const PathArgs &a, int grid, hipStream_t stream);
-hipError_t launch_path_fast(const PathArgs &a, int cpt, int grid, hipStream_t stream);
+hipError_t launch_path_fast(const PathArgs &a, int cpt, int nt, int grid, hipStream_t stream);
 
 }  // namespace taccl
