@@ -300,23 +300,39 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
     // ---- setup: owned chunks' records and priorities in registers --------
     const uint8_t *grt = a.routes + (size_t)i * a.route_stride;
     const uint32_t *gpr = a.prio + (size_t)i * a.prio_stride;
+    // the thread index is hidden from the optimiser once per candidate, so
+    // per-chunk addresses are recomputed instead of being hoisted out of the
+    // candidate loop and spilled
+    int tv = tid;
+    asm volatile("" : "+v"(tv));
     uint32_t rw0[CPT], rcl[CPT][3], pr[CPT][kFastMaxHops], hmap[CPT];
+    uint32_t kk[CPT], cp[CPT];
     bool unrouted = false;
+    // first batch: route choices, chunk tables and priorities (independent)
 #pragma unroll
     for (int j = 0; j < CPT; j++) {
-      const int c = tid + NT * j;
+      const int c = tv + NT * j;
+      kk[j] = 0;
+      cp[j] = 0;
+      if (c < C) {
+        kk[j] = grt[c];
+        cp[j] = a.cpath[c];
+#pragma unroll
+        for (int h = 0; h < kFastMaxHops; h++)
+          pr[j][h] = h < H ? gpr[(uint32_t)(c * H + h)] : 0u;
+      }
+    }
+    // second batch: the chosen route records
+#pragma unroll
+    for (int j = 0; j < CPT; j++) {
+      const int c = tv + NT * j;
       rw0[j] = 0;
       rcl[j][0] = rcl[j][1] = rcl[j][2] = 0;
       if (c < C) {
-        const uint32_t k = grt[c];
-        const uint32_t cp = a.cpath[c];
-#pragma unroll
-        for (int h = 0; h < kFastMaxHops; h++)
-          pr[j][h] = h < H ? gpr[(size_t)c * H + h] : 0u;
-        const uint32_t np = cp >> 24;
+        const uint32_t np = cp[j] >> 24;
         if (np) {
-          if (k < np) {
-            const uint4 r = *(const uint4 *)(a.arec + 4 * (size_t)((cp & 0xFFFFFFu) + k));
+          if (kk[j] < np) {
+            const uint4 r = ((const uint4 *)a.arec)[(cp[j] & 0xFFFFFFu) + kk[j]];
             rw0[j] = r.x;
             rcl[j][0] = r.y;
             rcl[j][1] = r.z;
@@ -327,6 +343,9 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
         }
         ctime[c] = 0;
       }
+    }
+#pragma unroll
+    for (int j = 0; j < CPT; j++) {
       // level -> hop index (3 bits per level, 7 = none)
       hmap[j] = 0xFFFFFFu;
       const int hops = rw0[j] & 0xFF;
