@@ -45,6 +45,8 @@ def _load():
     lib.orc_path.argtypes = [P, ct.c_int, ct.c_int, ct.c_int, P, ct.c_int]
     lib.orc_route_options.restype = ct.c_int
     lib.orc_route_options.argtypes = [P, ct.c_int]
+    lib.orc_set_contiguity.restype = ct.c_int
+    lib.orc_set_contiguity.argtypes = [P, ct.c_int]
     lib.orc_eval.restype = ct.c_int
     lib.orc_eval.argtypes = [P, ct.c_int64, P, P, P, P]
     lib.orc_eval_detail.restype = ct.c_int
@@ -104,10 +106,19 @@ class OraclePlan:
     @classmethod
     def from_workload(cls, w):
         """Build from a workloads.Workload descriptor."""
-        return cls(w.V, w.P, w.row_ptr, w.col, w.alpha_ns, w.beta_ps_per_byte, w.node_of,
+        plan = cls(w.V, w.P, w.row_ptr, w.col, w.alpha_ns, w.beta_ps_per_byte, w.node_of,
                    w.kind, w.chunks_per_rank, w.chunk_bytes, allowed=w.allowed, relay=w.relay,
                    max_cross=w.max_cross, route_mode=w.route_mode, k=w.k, owner=w.owner,
                    post_ptr=w.post_ptr, post=w.post)
+        plan.set_contiguity(getattr(w, "contiguity", 0))
+        return plan
+
+    def set_contiguity(self, mode):
+        """0: one chunk per transfer; 1: contiguous transfers of equal-remaining,
+        already-ready sends on links between nodes."""
+        if _load().orc_set_contiguity(self._h, int(mode)) != 0:
+            raise OracleError(f"bad contiguity mode {mode}")
+        self.contiguity = int(mode)
 
     def __del__(self):
         if getattr(self, "_h", None):

@@ -21,7 +21,14 @@
  *   4. the exact schedule of App. B.3 with no contiguity (every send carries
  *      one chunk): send >= start at the source, start = send + lat, and the
  *      strict per-link order. The least solution of these difference
- *      constraints is found by a topological sweep (Kahn's algorithm);
+ *      constraints is found by a topological sweep (Kahn's algorithm).
+ *      Optionally (orc_set_contiguity), sends on links between nodes are
+ *      merged into contiguous transfers (Sec. 4.1, Step 3 of Sec. 5.1, the
+ *      is_together constraints of App. B.3): a transfer carries the next
+ *      send of the link's order and every following send of that order with
+ *      the same remaining length that is ready when it starts; it costs
+ *      alpha + ceil(beta * m * S / 1000) for m chunks and all of them
+ *      arrive when it ends;
  *   5. the postcondition of App. B (every (chunk, rank) pair it lists holds)
  *      and the makespan, the objective of App. B.1 (latest finishing send).
  *
@@ -75,6 +82,7 @@ typedef struct orc_plan {
   int H;          /* longest path in hops */
   int route_stride, prio_stride;
   int max_sends;
+  int contig; /* merge contiguous sends on links between nodes */
   char err[256];
 } orc_plan;
 
@@ -366,6 +374,14 @@ void orc_destroy(orc_plan *p) {
 }
 
 const char *orc_error(const orc_plan *p) { return p ? p->err : "null plan"; }
+
+/* 0: every send is its own transfer (App. B.3 without contiguity);
+ * 1: contiguous transfers on links whose endpoints lie in different nodes. */
+int orc_set_contiguity(orc_plan *p, int mode) {
+  if (!p || mode < 0 || mode > 1) return ORC_EINVAL;
+  p->contig = mode;
+  return ORC_OK;
+}
 
 /*
  * Build a plan.
@@ -731,6 +747,79 @@ static void build_path_sends(const orc_plan *p, const uint8_t *rt, const uint32_
 
 /* Evaluate one candidate. If detail is non-NULL the sends are copied there
  * (at most cap of them) and *nsends is set. Returns ORC_OK. */
+/* every (chunk, rank) pair of the postcondition holds the chunk (App. B) */
+static int postcondition(const orc_plan *p, const oscratch *w) {
+  for (int c = 0; c < p->C; c++)
+    for (int j = p->post_ptr[c]; j < p->post_ptr[c + 1]; j++)
+      if (!w->present[(size_t)c * p->V + p->post[j]]) return 0;
+  return 1;
+}
+
+/* cost of one transfer of m chunks on link e: alpha + ceil(beta * m * S / 1000) */
+static uint64_t transfer_cost(const orc_plan *p, int e, uint64_t m) {
+  unsigned __int128 b = (unsigned __int128)p->beta[e] * m * p->S;
+  return (uint64_t)p->alpha[e] + (uint64_t)((b + 999) / 1000);
+}
+
+/* Schedule with contiguous transfers. Sends are taken in the global Step-2
+ * key order, which is a topological order of the schedule: a send's chunk
+ * arrives by a send with a strictly longer remaining path, and a link's
+ * order is the key order. A send joins the link's open transfer when the
+ * link is between nodes, its remaining length equals the transfer's and its
+ * chunk was ready when the transfer started; the transfer then ends later
+ * and so do all of its sends. Every send that could still join a transfer
+ * precedes, in key order, every send that depends on it (shorter remaining
+ * path), so finish times are final when they are read. */
+static int contig_sweep(const orc_plan *p, oscratch *w, uint32_t *makespan, uint8_t *valid) {
+  int n = w->n, E = p->E;
+  int *order = w->queue;
+  for (int i = 0; i < n; i++) order[i] = i;
+  g_sort_base = w->s;
+  if (n > 1) qsort(order, (size_t)n, sizeof(int), send_order_cmp);
+  uint64_t *busy = (uint64_t *)calloc((size_t)(E > 0 ? E : 1), sizeof(uint64_t));
+  uint64_t *g_start = (uint64_t *)calloc((size_t)(E > 0 ? E : 1), sizeof(uint64_t));
+  uint64_t *g_rem = (uint64_t *)calloc((size_t)(E > 0 ? E : 1), sizeof(uint64_t));
+  int *g_m = (int *)calloc((size_t)(E > 0 ? E : 1), sizeof(int));
+  uint64_t span = 0;
+  for (int t = 0; t < n; t++) {
+    int i = order[t];
+    osend *s = &w->s[i];
+    int e = s->link;
+    uint64_t ready = s->cpred >= 0 ? w->s[s->cpred].finish : 0;
+    int between_nodes = p->node[p->lsrc[e]] != p->node[p->col[e]];
+    if (between_nodes && g_m[e] > 0 && s->rem == g_rem[e] && ready <= g_start[e]) {
+      g_m[e]++;
+      uint64_t f = g_start[e] + transfer_cost(p, e, (uint64_t)g_m[e]);
+      s->start = g_start[e];
+      /* this send and the g_m - 1 sends before it on the link */
+      int j = i;
+      for (int q = 0; q < g_m[e]; q++) {
+        w->s[j].finish = f;
+        j = w->s[j].lpred;
+      }
+      busy[e] = f;
+      if (f > span) span = f;
+    } else {
+      uint64_t start = ready > busy[e] ? ready : busy[e];
+      s->start = start;
+      s->finish = start + transfer_cost(p, e, 1);
+      g_start[e] = start;
+      g_rem[e] = s->rem;
+      g_m[e] = 1;
+      busy[e] = s->finish;
+      if (s->finish > span) span = s->finish;
+    }
+  }
+  free(busy);
+  free(g_start);
+  free(g_rem);
+  free(g_m);
+  if (span >= (1ull << 32)) return ORC_ELIMIT;
+  *makespan = (uint32_t)span;
+  *valid = (uint8_t)postcondition(p, w);
+  return ORC_OK;
+}
+
 static int eval_one(const orc_plan *p, const uint8_t *rt, const uint32_t *pr, oscratch *w,
                     uint32_t *makespan, uint8_t *valid) {
   w->n = 0;
@@ -769,6 +858,7 @@ static int eval_one(const orc_plan *p, const uint8_t *rt, const uint32_t *pr, os
     free(cnt);
     free(fill);
   }
+  if (p->contig) return contig_sweep(p, w, makespan, valid);
   /* the difference constraints of App. B.3 without contiguity form a DAG
    * (chunk edges and link-order edges); sweep it in topological order */
   for (int i = 0; i <= n; i++) w->succ_ptr[i] = 0;
@@ -809,16 +899,8 @@ static int eval_one(const orc_plan *p, const uint8_t *rt, const uint32_t *pr, os
   }
   if (tail != n) return ORC_EINVAL; /* a cycle: cannot happen under this order */
   if (span >= (1ull << 32)) return ORC_ELIMIT;
-  /* postcondition: every listed (chunk, rank) pair holds the chunk */
-  int ok = 1;
-  for (int c = 0; c < p->C && ok; c++)
-    for (int j = p->post_ptr[c]; j < p->post_ptr[c + 1]; j++)
-      if (!w->present[(size_t)c * p->V + p->post[j]]) {
-        ok = 0;
-        break;
-      }
   *makespan = (uint32_t)span;
-  *valid = (uint8_t)ok;
+  *valid = (uint8_t)postcondition(p, w);
   return ORC_OK;
 }
 

@@ -235,6 +235,62 @@ def least_schedule(sends, cost, orders):
     return t, finish
 
 
+def contiguous_schedule(w, sends, orders):
+    """Schedule with contiguous transfers, by simulation in time order: the
+    transfer that can start earliest (a link's next send whose chunk has
+    arrived) starts; on a link between two nodes it also carries the
+    following sends of the link's order that have the same remaining length
+    and whose chunk has already arrived at that moment; m chunks cost
+    alpha + ceil(beta * m * S / 1000) and all arrive when the transfer ends.
+    A chunk whose delivering send has not started yet cannot have arrived:
+    that send ends after the current time."""
+    pred = chunk_pred(sends)
+    n = len(sends)
+    start = [None] * n
+    finish = [None] * n
+    head = {l: 0 for l in orders}
+    free = {l: 0 for l in orders}
+    done = 0
+    while done < n:
+        best = None
+        for l, order in orders.items():
+            if head[l] == len(order):
+                continue
+            x = order[head[l]]
+            if pred[x] is not None and finish[pred[x]] is None:
+                continue
+            ready = 0 if pred[x] is None else finish[pred[x]]
+            t = max(free[l], ready)
+            if best is None or t < best[0]:
+                best = (t, l)
+        if best is None:
+            raise RuntimeError("no transfer can start")
+        t, l = best
+        order = orders[l]
+        x = order[head[l]]
+        group = [x]
+        u, v = _src(w, l), int(w.col[l])
+        if node(w, u) != node(w, v):
+            j = head[l] + 1
+            while j < len(order):
+                y = order[j]
+                if sends[y]["rem"] != sends[x]["rem"]:
+                    break
+                if pred[y] is not None and (finish[pred[y]] is None or finish[pred[y]] > t):
+                    break
+                group.append(y)
+                j += 1
+        m = len(group)
+        lat = int(w.alpha_ns[l]) + (int(w.beta_ps_per_byte[l]) * m * int(w.chunk_bytes) + 999) // 1000
+        for y in group:
+            start[y] = t
+            finish[y] = t + lat
+        free[l] = t + lat
+        head[l] += m
+        done += m
+    return start, finish
+
+
 def evaluate(w, table, routes, prio, H=None):
     """Makespan, valid and per-send detail of one candidate."""
     cost = costs_of(w)
@@ -256,7 +312,10 @@ def evaluate(w, table, routes, prio, H=None):
                      for c in range(len(owner))]
         sends, present = tree_sends(w, cost, table, routes, prio, owner, posts)
     orders = link_orders(sends)
-    start, finish = least_schedule(sends, cost, orders)
+    if getattr(w, "contiguity", 0):
+        start, finish = contiguous_schedule(w, sends, orders)
+    else:
+        start, finish = least_schedule(sends, cost, orders)
     valid = all(r in present[c] for c in range(len(posts)) for r in posts[c])
     makespan = max(finish) if finish else 0
     return makespan, int(valid), sends, start, finish, orders

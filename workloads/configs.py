@@ -19,7 +19,7 @@ measured on DGX-2 and NDv2 clusters; none of that hardware is needed here):
 alpha/beta come from Table 1 (NVLink 0.7 us with 46 or 8 us/MB, IB 1.7 us
 with 106 us/MB); us/MB equals ps/B with MB = 10^6 B.
 """
-from dataclasses import dataclass, field
+from dataclasses import dataclass, field, replace
 from typing import Optional
 
 import numpy as np
@@ -63,6 +63,9 @@ class Workload:
     seed: int = 0
     description: str = ""
     extra: dict = field(default_factory=dict)
+    # 1: merge ready sends of equal remaining length into contiguous
+    # transfers on links between nodes
+    contiguity: int = 0
 
     @property
     def E(self):
@@ -225,6 +228,17 @@ NAMED = {
     "fournode64_a2a": fournode64_a2a,
 }
 ORDER = ["ring4_ag", "cubemesh8_ag", "switch16_a2a", "twonode16_ag", "fournode64_a2a"]
+
+
+def with_contiguity(w):
+    """The same workload with contiguous transfers on links between nodes."""
+    return replace(w, name=w.name + "_contig", contiguity=1,
+                   description=w.description + "; contiguous transfers on IB links")
+
+
+NAMED["twonode16_ag_contig"] = lambda **kw: with_contiguity(twonode16_ag(**kw))
+NAMED["fournode64_a2a_contig"] = lambda **kw: with_contiguity(fournode64_a2a(**kw))
+CONTIG_ORDER = ["twonode16_ag_contig", "fournode64_a2a_contig"]
 
 
 def named(name, **kw):
