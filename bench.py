@@ -26,7 +26,8 @@ DEFAULT_WORKLOAD = "twonode16_ag"
 
 # Kernel that dominates each workload's launch (the only kernel it runs).
 KERNEL_OF = {"ring4_ag": "tree_eval", "cubemesh8_ag": "tree_eval", "twonode16_ag": "tree_eval",
-             "switch16_a2a": "path_eval_fast", "fournode64_a2a": "path_eval_fast"}
+             "switch16_a2a": "path_eval_fast", "fournode64_a2a": "path_eval_fast",
+             "twonode16_ag_contig": "tree_eval", "fournode64_a2a_contig": "path_eval_fast"}
 
 
 def csrc_digest():
@@ -143,7 +144,7 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": args.calibrate_copy, "copies": args.steps}))
         return
-    from workloads import ORDER
+    from workloads import CONTIG_ORDER, ORDER
 
     w, plan, routes, prio, bufs = setup(args.workload)
     per, wall = time_launches(plan, *bufs, args.steps, args.warmup)
@@ -181,7 +182,7 @@ def main():
     }
     if not args.no_all:
         table = {}
-        for name in ORDER:
+        for name in ORDER + CONTIG_ORDER:
             if name == args.workload:
                 wl, pl, pr_ = w, plan, per
             else:

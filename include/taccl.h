@@ -122,7 +122,16 @@ void taccl_collective_destroy(taccl_collective_t coll);
  *   max_node_crossings: node-boundary crossings allowed per path, -1 = any.
  *     With 1, a path between nodes crosses exactly once and a path inside a
  *     node never leaves it (App. B.1, inter-node constraint);
- *   route_mode, k: see taccl_route_mode_t.
+ *   route_mode, k: see taccl_route_mode_t;
+ *   contiguity: 0 = every send is its own transfer (App. B.3 without
+ *     contiguity); 1 = contiguous transfers on links whose endpoints lie in
+ *     different nodes (the IB links of Sec. 4.1 and Step 3 of Sec. 5.1): a
+ *     transfer carries the next send of the link's order and every following
+ *     send of that order with the same remaining path length whose chunk is
+ *     already at the link's source when the transfer starts; m chunks cost
+ *     alpha + ceil(beta * m * chunk_bytes / 1000) ns and all of them arrive
+ *     when the transfer ends. Plans whose multicast evaluation needs the
+ *     round-based kernel (see taccl_eval_batch) refuse contiguity.
  */
 typedef struct {
   const uint8_t *allowed_link;
@@ -130,6 +139,7 @@ typedef struct {
   int32_t max_node_crossings;
   int32_t route_mode;
   int32_t k;
+  int32_t contiguity;
 } taccl_sketch_desc_t;
 
 /*

@@ -48,7 +48,8 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
          o_plh = pk.add(p->path_lvl_hop), o_lcb = pk.add(p->lvl_cls_begin),
          o_llc = pk.add(p->llc), o_trec = pk.add(p->tree_rec), o_own8 = pk.add(p->owner8),
          o_arec = pk.add(p->arec), o_cpath = pk.add(p->cpath), o_cinfo = pk.add(p->cinfo),
-         o_cbkt = pk.add(p->cbkt), o_topt = pk.add(p->topt), o_trec4 = pk.add(p->tree_rec4);
+         o_cbkt = pk.add(p->cbkt), o_topt = pk.add(p->topt), o_trec4 = pk.add(p->tree_rec4),
+         o_lal = pk.add(p->lalpha), o_lbs = pk.add(p->lbs), o_lmg = pk.add(p->lmerge);
   void *blk = nullptr;
   e = hipMalloc(&blk, pk.bytes.size());
   if (e != hipSuccess) return fail(TACCL_ERR_NO_MEMORY, "hipMalloc of plan tables failed");
@@ -77,6 +78,9 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
   t.owner8 = (const uint8_t *)at(o_own8);
   t.topt = p->topt.empty() ? nullptr : (const uint8_t *)at(o_topt);
   t.tree_rec4 = p->tree_rec4.empty() ? nullptr : (const uint32_t *)at(o_trec4);
+  t.lalpha = (const uint32_t *)at(o_lal);
+  t.lbs = (const uint64_t *)at(o_lbs);
+  t.lmerge = (const uint8_t *)at(o_lmg);
   t.arec = (const uint32_t *)at(o_arec);
   t.cpath = (const uint32_t *)at(o_cpath);
   t.cinfo = (const uint32_t *)at(o_cinfo);
@@ -153,6 +157,10 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     a.makespan = d_makespan;
     a.valid = d_valid;
     a.n = n;
+    a.contig = p->contig;
+    a.lalpha = t->lalpha;
+    a.lbs = t->lbs;
+    a.lmerge = t->lmerge;
     a.arec = t->arec;
     a.cpath = t->cpath;
     a.cinfo = t->cinfo;
@@ -186,6 +194,10 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     a.npaths = t->npaths;
     a.owner8 = t->owner8;
     a.topt = t->topt;
+    a.contig = p->contig;
+    a.lalpha = t->lalpha;
+    a.lbs = t->lbs;
+    a.lmerge = t->lmerge;
     a.rec4 = (const uint4 *)t->tree_rec4;
     a.post_mask = t->post_mask;
     a.routes = d_routes;
@@ -196,6 +208,10 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     // the layered kernel needs whole route words and priorities in registers
     const bool layered = a.routes_word_aligned && tree_layers_layout(*p, a) > 0 &&
                          tree_block_bytes(a, 1) <= t->max_lds;
+    if (!layered && p->contig)
+      return fail(TACCL_ERR_UNSUPPORTED,
+                  "contiguous transfers need the layered multicast kernel, which this plan "
+                  "does not fit");
     if (!layered && tree_layout(*p, a) > t->max_lds)
       return fail(TACCL_ERR_UNSUPPORTED, "multicast plan needs more LDS than a block has");
     // wavefronts per block: most resident wavefronts per CU (LDS, and for

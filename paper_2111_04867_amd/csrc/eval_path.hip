@@ -151,10 +151,36 @@ __global__ __launch_bounds__(kPathThreads) void path_eval_kernel(PathArgs a) {
         const uint32_t xb = ccnt[cb - lo], xe = ccnt[ce - lo];
         uint32_t f = lfree[l];
         const uint32_t cl = a.cost[l];
-        for (uint32_t x = xb; x < xe; x++) {
-          const int c = sorted[x];
-          f = max(ctime[c], f) + cl;
-          ctime[c] = f;
+        if (a.contig && a.lmerge[l]) {
+          // contiguous transfers (every send of a level has the same
+          // remaining length): a send joins the open transfer when its chunk
+          // was ready when the transfer started
+          const uint32_t al = a.lalpha[l];
+          const uint64_t bsz = a.lbs[l];
+          uint32_t gs = 0, gm = 0, g0 = xb;
+          for (uint32_t x = xb;; x++) {
+            const bool end = x == xe;
+            const uint32_t r = end ? 0u : ctime[sorted[x]];
+            const bool join = !end && gm > 0 && r <= gs;
+            if (gm > 0 && !join) {
+              f = gs + al + (uint32_t)((bsz * gm + 999) / 1000);
+              for (uint32_t t = g0; t < g0 + gm; t++) ctime[sorted[t]] = f;
+            }
+            if (end) break;
+            if (join) {
+              gm++;
+            } else {
+              gs = max(f, r);
+              gm = 1;
+              g0 = x;
+            }
+          }
+        } else {
+          for (uint32_t x = xb; x < xe; x++) {
+            const int c = sorted[x];
+            f = max(ctime[c], f) + cl;
+            ctime[c] = f;
+          }
         }
         lfree[l] = f;
         mk = max(mk, f);
@@ -288,7 +314,11 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
   uint32_t *red = (uint32_t *)(lds + a.o_fred);      // [2][NT/64] scan scratch
   uint64_t *red64 = (uint64_t *)(lds + a.o_fred64);  // [NT/64] segmented max
   uint32_t *redf = (uint32_t *)(lds + a.o_fredf);    // [NT/64] segment-head flags
-  for (int j = tid; j < E; j += NT) s_cost[j] = a.cost[j];
+  uint8_t *s_merge = lds + a.o_fmerge;  // links that carry contiguous transfers
+  for (int j = tid; j < E; j += NT) {
+    s_cost[j] = a.cost[j];
+    s_merge[j] = a.contig ? a.lmerge[j] : 0;
+  }
   for (int j = tid; j < a.ncls; j += NT) {
     s_cinfo[j] = a.cinfo[j];
     s_cbkt[j] = a.cbkt[j];
@@ -496,6 +526,42 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
         const uint32_t x = x0 + q;
         if ((uint32_t)q < ept && x < tot) {
           const uint32_t c = pis[q] & cmask, l = (pis[q] >> cb) & lmask, k = pis[q] >> kb;
+          if (s_merge[l]) {
+            // contiguous transfers: the run's first position walks the run
+            // (every send of a level has the same remaining length); a send
+            // joins the open transfer when its chunk was ready at its start
+            if (k == 0) {
+              const uint32_t al = a.lalpha[l];
+              const uint64_t bsz = a.lbs[l];
+              uint32_t F = lf[q], gs = 0, gm = 0, g0 = x;
+              auto at = [&](uint32_t y) {  // packed send at sorted position y
+                const uint32_t ty = (uint32_t)(((uint64_t)y * em) >> 32);
+                return pinfo[(y - ty * ept) * NT + ty];
+              };
+              for (uint32_t y = x;; y++) {
+                const uint32_t py = (y < tot) ? at(y) : 0u;
+                const bool end = y == tot || (y > x && (py >> kb) == 0);
+                const uint32_t ry = end ? 0u : ctime[py & cmask];
+                const bool join = !end && gm > 0 && ry <= gs;
+                if (gm > 0 && !join) {  // close the open transfer
+                  const uint32_t f = gs + al + (uint32_t)((bsz * gm + 999) / 1000);
+                  for (uint32_t t = g0; t < g0 + gm; t++) ctime[at(t) & cmask] = f;
+                  F = f;
+                  mk = max(mk, f);
+                }
+                if (end) break;
+                if (join) {
+                  gm++;
+                } else {
+                  gs = max(F, ry);
+                  gm = 1;
+                  g0 = y;
+                }
+              }
+              lfree[E + l] = F;
+            }
+            continue;
+          }
           const uint32_t cl = cs[q];
           const uint64_t g = (uint64_t)ct[q] + kBias - (uint64_t)k * cl;
           run = (k == 0) ? g : max(run, g);
@@ -539,6 +605,7 @@ int32_t path_fast_layout(const taccl_plan &p, PathArgs &a) {
   };
   a.ncls = p.ncls;
   a.o_fcost = take(4 * E);
+  a.o_fmerge = take(E);
   a.o_fcinfo = take(4 * std::max(p.ncls, 1));
   a.o_fcbkt = take(4 * std::max(p.ncls, 1));
   a.o_flcb = take(4 * (p.nlev + 1));

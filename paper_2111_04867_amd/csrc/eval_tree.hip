@@ -397,9 +397,11 @@ void tree_layers_kernel(TreeArgs a) {
   uint64_t *s_post = (uint64_t *)(lds + a.o_post);
   uint4 *s_rec = (uint4 *)(lds + a.o_rec4);       // one 16-byte record per option
   uint32_t *s_opt = (uint32_t *)(lds + a.o_opt);  // option bytes, PW words per (o, v)
+  uint8_t *s_merge = lds + a.o_merge;             // links that carry contiguous transfers
   for (int j = threadIdx.x; j < E; j += blockDim.x) {
     s_cost[j] = a.cost[j];
     s_src[j] = (uint8_t)a.lsrc[j];
+    s_merge[j] = a.contig ? a.lmerge[j] : 0;
   }
   for (int r = threadIdx.x; r < P * P * K; r += blockDim.x) s_rec[r] = a.rec4[r];
   for (int j = threadIdx.x; j < P * V * PW; j += blockDim.x)
@@ -687,7 +689,7 @@ void tree_layers_kernel(TreeArgs a) {
       const uint32_t bs = bd & 0xFFFFu, be = bd >> 16;
       const uint64_t kx = ((uint64_t)rx.y << 32) | rx.x;
       const uint64_t qx = ((uint64_t)rx.w << 32) | rx.z;
-      uint32_t rank = 0;
+      uint32_t rank = 0, same = 0;
       // four members per step; the array has three spare entries past its
       // end, so the loads need no clamping (entries past the bucket never count)
       for (uint32_t y = bs; y < be; y += 4) {
@@ -698,7 +700,11 @@ void tree_layers_kernel(TreeArgs a) {
         for (int t = 0; t < 4; t++) {
           const uint64_t ky = ((uint64_t)m[t].y << 32) | m[t].x;
           const uint64_t qy = ((uint64_t)m[t].w << 32) | m[t].z;
-          rank += (uint32_t)((y + t < be) & ((ky < kx) | ((ky == kx) & (qy < qx))));
+          const uint32_t before = (uint32_t)((y + t < be) & ((ky < kx) | ((ky == kx) & (qy < qx))));
+          rank += before;
+          // an earlier send of the bucket with the same remaining length
+          // (the order puts equal remaining lengths next to each other)
+          same |= before & (uint32_t)(m[t].y == rx.y);
         }
       }
       const uint32_t sl = rx.z & 0x3FFu, l = rx.z >> 10;
@@ -707,7 +713,7 @@ void tree_layers_kernel(TreeArgs a) {
       const uint32_t pred = (u == s_own[c]) ? kNoPred : c * V + u;
       const uint32_t q = bs + rank;
       ord2[q] = sl | (pred << 16);
-      info2[q] = l | (rank << 16);
+      info2[q] = l | (rank << 16) | (same << 31);  // rank < 2^15: at most 1024 sends
     }
     wave_sync();
 
@@ -724,8 +730,37 @@ void tree_layers_kernel(TreeArgs a) {
       wave_sync();
       for (uint32_t q = qs + lane; q < qe; q += 64) {
         const uint32_t inf = info2[q];
-        const uint32_t l = inf & 0xFFFFu, k = inf >> 16;
+        const uint32_t l = inf & 0xFFFFu, k = (inf >> 16) & 0x7FFFu;
         const uint32_t cl = s_cost[l];
+        if (s_merge[l]) {
+          // contiguous transfers: the run's first lane walks the run; a send
+          // joins the open transfer when its remaining length equals the
+          // previous send's and its chunk was ready when the transfer started
+          if (k != 0) continue;
+          const uint32_t al = a.lalpha[l];
+          const uint64_t bsz = a.lbs[l];
+          uint32_t F = lfree[l], gs = 0, gm = 0, g0 = q;
+          for (uint32_t j = q;; j++) {
+            const bool end = j == qe || (j > q && ((info2[j] >> 16) & 0x7FFFu) == 0);
+            const bool join = !end && gm > 0 && (info2[j] >> 31) && rq[j] <= gs;
+            if (gm > 0 && !join) {  // close the open transfer
+              const uint32_t f = gs + al + (uint32_t)((bsz * gm + 999) / 1000);
+              for (uint32_t t = g0; t < g0 + gm; t++) fin[ord2[t] & 0xFFFFu] = f;
+              F = f;
+              mk = max(mk, f);
+            }
+            if (end) break;
+            if (join) {
+              gm++;
+            } else {
+              gs = max(F, rq[j]);
+              gm = 1;
+              g0 = j;
+            }
+          }
+          lfree[l] = F;
+          continue;
+        }
         uint32_t f = lfree[l] + (k + 1) * cl;
         // earlier sends of the run, four at a time
         for (uint32_t j = q - k; j <= q; j += 4) {
@@ -740,7 +775,7 @@ void tree_layers_kernel(TreeArgs a) {
         }
         fin[ord2[q] & 0xFFFFu] = f;
         mk = max(mk, f);
-        if (q + 1 == qe || (info2[q + 1] >> 16) == 0) lfree[l] = f;
+        if (q + 1 == qe || ((info2[q + 1] >> 16) & 0x7FFFu) == 0) lfree[l] = f;
       }
       wave_sync();
     }
@@ -853,6 +888,8 @@ int32_t tree_layers_layout(const taccl_plan &p, TreeArgs &a) {
   off = align16(off + 16 * P * P * K);
   a.o_opt = off;
   off = align16(off + P * V * P);
+  a.o_merge = off;
+  off = align16(off + E);
   a.o_wave = off;
   const int32_t S = std::max<int64_t>(std::min<int64_t>(p.max_sends, CV), 1);
   // region X: route words and distances, then bucket entries, then finish

@@ -36,6 +36,12 @@ struct TreeArgs {
   // layered variant: layer of a send = (rem * lmagic) >> 32, below nl_max
   uint64_t lmagic;
   int32_t nl_max;
+  // contiguous transfers on links between nodes (contig != 0)
+  int32_t contig;
+  const uint32_t *lalpha;
+  const uint64_t *lbs;    // beta * chunk_bytes per link
+  const uint8_t *lmerge;  // 1: the link joins two nodes
+  int32_t o_merge;
   const uint8_t *topt;  // options of (o, d) through vertex v, one byte per d
   const uint4 *rec4;    // route records, one 16-byte record per option
   int32_t o_rec4, o_opt;
@@ -68,6 +74,12 @@ struct PathArgs {
       o_fred, o_fred64, o_fredf;
   int32_t lds_bytes;
   int32_t cbits, lbits;  // chunk and link fields of a packed sorted send
+  // contiguous transfers on links between nodes (contig != 0)
+  int32_t contig;
+  const uint32_t *lalpha;
+  const uint64_t *lbs;    // beta * chunk_bytes per link
+  const uint8_t *lmerge;  // 1: the link joins two nodes
+  int32_t o_fmerge;
 };
 
 constexpr int kTreeMaxThreads = 512;  // up to 8 wavefronts per block

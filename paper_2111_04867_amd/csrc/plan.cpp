@@ -600,6 +600,9 @@ taccl_status_t taccl_sketch_apply(taccl_topology_t topo, taccl_collective_t coll
   p->mode = sk->route_mode;
   p->k = sk->k;
   p->max_cross = sk->max_node_crossings;
+  if (sk->contiguity < 0 || sk->contiguity > 1)
+    return fail(TACCL_ERR_INVALID_ARGUMENT, "contiguity must be 0 or 1");
+  p->contig = sk->contiguity;
   const int32_t E = topo->E;
   // integer alpha-beta cost of one chunk on every link (Sec. 4.1)
   p->cost.resize(E);
@@ -617,6 +620,16 @@ taccl_status_t taccl_sketch_apply(taccl_topology_t topo, taccl_collective_t coll
     max_cost = std::max(max_cost, c);
     p->lsrc[e] = (uint16_t)topo->src[e];
     p->ldst[e] = (uint16_t)topo->col[e];
+  }
+  p->lalpha.assign(topo->alpha.begin(), topo->alpha.end());
+  p->lbs.resize(E);
+  p->lmerge.assign(E, 0);
+  for (int32_t e = 0; e < E; e++) {
+    p->lbs[e] = (uint64_t)topo->beta[e] * coll->S;
+    p->lmerge[e] = p->contig && topo->node[topo->src[e]] != topo->node[topo->col[e]];
+    // a transfer of up to C chunks: beta * S * C must fit 64 bits
+    if (p->lmerge[e] && (unsigned __int128)p->lbs[e] * (uint64_t)coll->C >= ((unsigned __int128)1 << 64))
+      return fail(TACCL_ERR_LIMIT, "beta * chunk_bytes * chunks overflows 64 bits");
   }
   taccl_status_t st = build_routes(p, sk->allowed_link, sk->is_relay);
   if (st) return st;

@@ -51,6 +51,9 @@ struct DeviceTables {
   const uint8_t *owner8 = nullptr;
   const uint8_t *topt = nullptr;
   const uint32_t *tree_rec4 = nullptr;
+  const uint32_t *lalpha = nullptr;
+  const uint64_t *lbs = nullptr;
+  const uint8_t *lmerge = nullptr;
   const uint16_t *hop_class = nullptr;
   const int8_t *path_lvl_hop = nullptr;
   const uint32_t *lvl_cls_begin = nullptr;
@@ -71,6 +74,12 @@ struct taccl_plan {
   // link tables
   std::vector<uint32_t> cost;  // [E] integer alpha-beta cost in ns
   std::vector<uint16_t> lsrc, ldst;
+  // contiguous transfers: per link alpha, beta * chunk_bytes and whether the
+  // link joins two nodes (only those merge)
+  int32_t contig = 0;
+  std::vector<uint32_t> lalpha;
+  std::vector<uint64_t> lbs;
+  std::vector<uint8_t> lmerge;
 
   // route options per ordered rank pair (s, d), pair index s*P + d
   std::vector<uint32_t> pair_base;  // [P*P] first option's global path index

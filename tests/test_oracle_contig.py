@@ -129,40 +129,11 @@ def test_no_inter_node_link_means_no_change(name):
 
 
 def two_node_ag(P_per, chunks_per_rank, k=3):
-    """Two nodes of P_per fully connected ranks, IB between rank i of node 0
-    and rank i of node 1 (both directions), Allgather."""
-    P = 2 * P_per
-    edges = []
-    for n in range(2):
-        for u in range(P_per):
-            for v in range(P_per):
-                if u != v:
-                    edges.append((n * P_per + u, n * P_per + v, NV_A, NV_B))
-    for i in range(P_per):
-        edges.append((i, P_per + i, IB_A, IB_B))
-        edges.append((P_per + i, i, IB_A, IB_B))
-    row_ptr, col, a, b = cf.csr_from_edges(P, edges)
-    node_of = np.array([r // P_per for r in range(P)], dtype=np.int32)
-    return cf.Workload("twonode_small", P, P, row_ptr, col, a, b, node_of, cf.ALLGATHER,
-                       chunks_per_rank, 65536, cf.KSHORTEST, k=k, contiguity=1)
+    return cf.two_node_full(P_per, cf.ALLGATHER, chunks_per_rank=chunks_per_rank, k=k)
 
 
 def two_node_a2a(P_per):
-    P = 2 * P_per
-    edges = []
-    for n in range(2):
-        for u in range(P_per):
-            for v in range(P_per):
-                if u != v:
-                    edges.append((n * P_per + u, n * P_per + v, NV_A, NV_B))
-    for i in range(P_per):
-        edges.append((i, P_per + i, IB_A, IB_B))
-        edges.append((P_per + i, i, IB_A, IB_B))
-    row_ptr, col, a, b = cf.csr_from_edges(P, edges)
-    node_of = np.array([r // P_per for r in range(P)], dtype=np.int32)
-    relay = np.ones(P, dtype=np.uint8)
-    return cf.Workload("twonode_small_a2a", P, P, row_ptr, col, a, b, node_of, cf.ALLTOALL, 1,
-                       65536, cf.HIER_RELAY, max_cross=1, relay=relay, contiguity=1)
+    return cf.two_node_full(P_per, cf.ALLTOALL)
 
 
 def bf_table(w, hop_limit):

@@ -289,3 +289,46 @@ def explicit_multicast(base, owner, posts, n_candidates=1, seed=0):
                  relay=base.relay, owner=np.asarray(owner, dtype=np.int32), post_ptr=post_ptr,
                  post=post, n_candidates=n_candidates, seed=seed)
     return w
+
+
+def two_node_full(P_per, kind, chunks_per_rank=1, k=3, chunk_bytes=64 * KIB, contiguity=1):
+    """Two nodes of P_per fully connected ranks (NVLink inside a node), IB
+    between rank i of one node and rank i of the other, both directions.
+    Allgather: k shortest paths; Alltoall: hierarchical relays."""
+    P = 2 * P_per
+    edges = []
+    for n in range(2):
+        for u in range(P_per):
+            for v in range(P_per):
+                if u != v:
+                    edges.append((n * P_per + u, n * P_per + v, NVLINK_ALPHA, NDV2_NVLINK_BETA))
+    for i in range(P_per):
+        edges.append((i, P_per + i, IB_ALPHA, IB_BETA))
+        edges.append((P_per + i, i, IB_ALPHA, IB_BETA))
+    row_ptr, col, a, b = csr_from_edges(P, edges)
+    node_of = np.array([r // P_per for r in range(P)], dtype=np.int32)
+    if kind == ALLGATHER:
+        return Workload(f"twonode{P}_full_ag", P, P, row_ptr, col, a, b, node_of, ALLGATHER,
+                        chunks_per_rank, chunk_bytes, KSHORTEST, k=k, contiguity=contiguity)
+    relay = np.ones(P, dtype=np.uint8)
+    return Workload(f"twonode{P}_full_a2a", P, P, row_ptr, col, a, b, node_of, ALLTOALL,
+                    chunks_per_rank, chunk_bytes, HIER_RELAY, max_cross=1, relay=relay,
+                    contiguity=contiguity)
+
+
+def two_node_rings_a2a(P_per, chunk_bytes=64 * KIB, contiguity=1):
+    """Two nodes whose ranks form a one-way ring, IB between rank i of one
+    node and rank i of the other: Alltoall paths run up to 2*P_per - 1 links."""
+    P = 2 * P_per
+    edges = []
+    for n in range(2):
+        for u in range(P_per):
+            edges.append((n * P_per + u, n * P_per + (u + 1) % P_per, NVLINK_ALPHA,
+                          NDV2_NVLINK_BETA))
+    for i in range(P_per):
+        edges.append((i, P_per + i, IB_ALPHA, IB_BETA))
+        edges.append((P_per + i, i, IB_ALPHA, IB_BETA))
+    row_ptr, col, a, b = csr_from_edges(P, edges)
+    node_of = np.array([r // P_per for r in range(P)], dtype=np.int32)
+    return Workload(f"tworings{P}_a2a", P, P, row_ptr, col, a, b, node_of, ALLTOALL, 1,
+                    chunk_bytes, KSHORTEST, k=2, max_cross=1, contiguity=contiguity)
