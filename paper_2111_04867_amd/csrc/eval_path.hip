@@ -291,7 +291,7 @@ __device__ void block_excl_scan(uint32_t *cnt, int n, uint32_t *wsum) {
   __syncthreads();
 }
 
-template <int CPT, int NT>
+template <int CPT, int NT, bool kContig>
 __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -526,7 +526,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
         const uint32_t x = x0 + q;
         if ((uint32_t)q < ept && x < tot) {
           const uint32_t c = pis[q] & cmask, l = (pis[q] >> cb) & lmask, k = pis[q] >> kb;
-          if (s_merge[l]) {
+          if (kContig && s_merge[l]) {
             // contiguous transfers: the run's first position walks the run
             // (every send of a level has the same remaining length); a send
             // joins the open transfer when its chunk was ready at its start
@@ -649,17 +649,22 @@ int path_fast_cpt(const taccl_plan &p) {
   return per <= 1 ? 1 : per <= 2 ? 2 : per <= 4 ? 4 : 0;
 }
 
-static const void *path_fast_fn(int cpt, int nt) {
-  if (nt == 256 && cpt == 1) return (const void *)path_eval_fast<1, 256>;
-  if (nt == 512 && cpt == 1) return (const void *)path_eval_fast<1, 512>;
-  if (nt == 1024 && cpt == 1) return (const void *)path_eval_fast<1, 1024>;
-  if (nt == 1024 && cpt == 2) return (const void *)path_eval_fast<2, 1024>;
-  if (nt == 1024 && cpt == 4) return (const void *)path_eval_fast<4, 1024>;
+template <bool kC>
+static const void *path_fast_fn_c(int cpt, int nt) {
+  if (nt == 256 && cpt == 1) return (const void *)path_eval_fast<1, 256, kC>;
+  if (nt == 512 && cpt == 1) return (const void *)path_eval_fast<1, 512, kC>;
+  if (nt == 1024 && cpt == 1) return (const void *)path_eval_fast<1, 1024, kC>;
+  if (nt == 1024 && cpt == 2) return (const void *)path_eval_fast<2, 1024, kC>;
+  if (nt == 1024 && cpt == 4) return (const void *)path_eval_fast<4, 1024, kC>;
   return nullptr;
 }
 
+static const void *path_fast_fn(const PathArgs &a, int cpt, int nt) {
+  return a.contig ? path_fast_fn_c<true>(cpt, nt) : path_fast_fn_c<false>(cpt, nt);
+}
+
 int path_fast_blocks_per_cu(const PathArgs &a, int cpt, int nt) {
-  const void *fn = path_fast_fn(cpt, nt);
+  const void *fn = path_fast_fn(a, cpt, nt);
   int nb = 0;
   if (!fn || hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fn, nt, a.lds_bytes) != hipSuccess)
     return 0;
@@ -667,20 +672,10 @@ int path_fast_blocks_per_cu(const PathArgs &a, int cpt, int nt) {
 }
 
 hipError_t launch_path_fast(const PathArgs &a, int cpt, int nt, int grid, hipStream_t stream) {
-  const void *fn = path_fast_fn(cpt, nt);
+  const void *fn = path_fast_fn(a, cpt, nt);
   if (!fn) return hipErrorInvalidValue;
-  const dim3 g(grid), b(nt);
-  if (nt == 256)
-    hipLaunchKernelGGL((path_eval_fast<1, 256>), g, b, a.lds_bytes, stream, a);
-  else if (nt == 512)
-    hipLaunchKernelGGL((path_eval_fast<1, 512>), g, b, a.lds_bytes, stream, a);
-  else if (cpt == 1)
-    hipLaunchKernelGGL((path_eval_fast<1, 1024>), g, b, a.lds_bytes, stream, a);
-  else if (cpt == 2)
-    hipLaunchKernelGGL((path_eval_fast<2, 1024>), g, b, a.lds_bytes, stream, a);
-  else
-    hipLaunchKernelGGL((path_eval_fast<4, 1024>), g, b, a.lds_bytes, stream, a);
-  return hipGetLastError();
+  void *args[] = {(void *)&a};
+  return hipLaunchKernel(fn, dim3(grid), dim3(nt), args, a.lds_bytes, stream);
 }
 
 }  // namespace taccl

@@ -383,7 +383,7 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_eval_kernel(TreeArgs a) 
 // with 16-bit counters, each bucket is ordered by the full key
 // (rem, trav, priority, chunk), and the layers are timed in turn, one lane
 // per send.
-template <int J, int PW>
+template <int J, int PW, bool kContig>
 __global__ __launch_bounds__(kTreeMaxThreads)
 void tree_layers_kernel(TreeArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
@@ -704,7 +704,7 @@ void tree_layers_kernel(TreeArgs a) {
           rank += before;
           // an earlier send of the bucket with the same remaining length
           // (the order puts equal remaining lengths next to each other)
-          same |= before & (uint32_t)(m[t].y == rx.y);
+          if (kContig) same |= before & (uint32_t)(m[t].y == rx.y);
         }
       }
       const uint32_t sl = rx.z & 0x3FFu, l = rx.z >> 10;
@@ -732,7 +732,7 @@ void tree_layers_kernel(TreeArgs a) {
         const uint32_t inf = info2[q];
         const uint32_t l = inf & 0xFFFFu, k = (inf >> 16) & 0x7FFFu;
         const uint32_t cl = s_cost[l];
-        if (s_merge[l]) {
+        if (kContig && s_merge[l]) {
           // contiguous transfers: the run's first lane walks the run; a send
           // joins the open transfer when its remaining length equals the
           // previous send's and its chunk was ready when the transfer started
@@ -916,33 +916,28 @@ int32_t tree_layers_layout(const taccl_plan &p, TreeArgs &a) {
   return a.o_wave + a.wave_bytes;
 }
 
-template <int J>
-static void launch_layers_j(const TreeArgs &a, dim3 g, dim3 b, int bytes, hipStream_t stream) {
-  switch (a.P / 4) {
-    case 1: hipLaunchKernelGGL((tree_layers_kernel<J, 1>), g, b, bytes, stream, a); break;
-    case 2: hipLaunchKernelGGL((tree_layers_kernel<J, 2>), g, b, bytes, stream, a); break;
-    case 4: hipLaunchKernelGGL((tree_layers_kernel<J, 4>), g, b, bytes, stream, a); break;
-    default: hipLaunchKernelGGL((tree_layers_kernel<J, 8>), g, b, bytes, stream, a); break;
+template <int J, bool kC>
+static const void *layers_fn_j(int pw) {
+  switch (pw) {
+    case 1: return (const void *)tree_layers_kernel<J, 1, kC>;
+    case 2: return (const void *)tree_layers_kernel<J, 2, kC>;
+    case 4: return (const void *)tree_layers_kernel<J, 4, kC>;
+    default: return (const void *)tree_layers_kernel<J, 8, kC>;
   }
 }
 
-template <int J>
-static const void *layers_fn_j(int pw) {
-  switch (pw) {
-    case 1: return (const void *)tree_layers_kernel<J, 1>;
-    case 2: return (const void *)tree_layers_kernel<J, 2>;
-    case 4: return (const void *)tree_layers_kernel<J, 4>;
-    default: return (const void *)tree_layers_kernel<J, 8>;
-  }
+template <bool kC>
+static const void *layers_fn_c(const TreeArgs &a) {
+  const int J = (a.C * a.V + 63) / 64, pw = a.P / 4;
+  if (J <= 1) return layers_fn_j<1, kC>(pw);
+  if (J <= 2) return layers_fn_j<2, kC>(pw);
+  if (J <= 4) return layers_fn_j<4, kC>(pw);
+  if (J <= 8) return layers_fn_j<8, kC>(pw);
+  return layers_fn_j<16, kC>(pw);
 }
 
 static const void *layers_fn(const TreeArgs &a) {
-  const int J = (a.C * a.V + 63) / 64, pw = a.P / 4;
-  if (J <= 1) return layers_fn_j<1>(pw);
-  if (J <= 2) return layers_fn_j<2>(pw);
-  if (J <= 4) return layers_fn_j<4>(pw);
-  if (J <= 8) return layers_fn_j<8>(pw);
-  return layers_fn_j<16>(pw);
+  return a.contig ? layers_fn_c<true>(a) : layers_fn_c<false>(a);
 }
 
 int tree_layers_blocks_per_cu(const TreeArgs &a) {
@@ -959,12 +954,8 @@ hipError_t launch_tree_layers(const TreeArgs &a, int grid, hipStream_t stream) {
   if (a.P % 4 || (pw != 1 && pw != 2 && pw != 4 && pw != 8)) return hipErrorInvalidValue;
   const dim3 g(grid), b(64 * a.waves_per_block);
   const int bytes = tree_block_bytes(a, a.waves_per_block);
-  const int J = (a.C * a.V + 63) / 64;
-  if (J <= 1) launch_layers_j<1>(a, g, b, bytes, stream);
-  else if (J <= 2) launch_layers_j<2>(a, g, b, bytes, stream);
-  else if (J <= 4) launch_layers_j<4>(a, g, b, bytes, stream);
-  else if (J <= 8) launch_layers_j<8>(a, g, b, bytes, stream);
-  else launch_layers_j<16>(a, g, b, bytes, stream);
-  return hipGetLastError();
+  void *args[] = {(void *)&a};
+  return hipLaunchKernel(layers_fn(a), g, b, args, bytes, stream);
 }
+
 }  // namespace taccl
