@@ -186,7 +186,7 @@ class OraclePlan:
         dict of per-send arrays."""
         routes = np.ascontiguousarray(routes, dtype=np.uint8).reshape(self.route_stride)
         prio = np.ascontiguousarray(prio, dtype=np.uint32).reshape(self.prio_stride)
-        cap = max(self.max_sends, 1)
+        cap = max(self.max_sends, 1) * (2 if self.kind == 4 else 1)  # Allreduce: two phases
         out = {k: np.zeros(cap, dtype=np.int32) for k in ("chunk", "link", "from", "to", "hop",
                                                            "pos")}
         out.update({k: np.zeros(cap, dtype=np.uint64) for k in ("rem", "trav", "start",

@@ -32,6 +32,15 @@
  *   5. the postcondition of App. B (every (chunk, rank) pair it lists holds)
  *      and the makespan, the objective of App. B.1 (latest finishing send).
  *
+ * ReduceScatter and Allreduce (Sec. 5.2, which builds them from an
+ * Allgather algorithm): ReduceScatter runs every chunk's Allgather tree
+ * backwards. The send from v to its tree parent carries v's partial
+ * reduction, so it waits for every send into v; Step 2 measures remaining
+ * and travelled lengths on the reversed tree (remaining: reversed distance
+ * from v to the owner; travelled: longest reversed path from a vertex below
+ * v up to v). Allreduce is ReduceScatter then Allgather on the same trees,
+ * timed back to back, with a separate priority row for each phase.
+ *
  * Paths: the sketch of Sec. 3.1 restricts links; routes are limited to
  * shortest paths in the logical topology (Sec. 5.1, Step 1). Paths are found
  * here by exhaustive depth-first search with cost pruning and sorted by
@@ -42,7 +51,8 @@
 #include <stdlib.h>
 #include <string.h>
 
-enum { ORC_ALLGATHER = 0, ORC_ALLTOALL = 1, ORC_EXPLICIT = 2 };
+enum { ORC_ALLGATHER = 0, ORC_ALLTOALL = 1, ORC_EXPLICIT = 2, ORC_REDUCESCATTER = 3,
+       ORC_ALLREDUCE = 4 };
 enum { ORC_SHORTEST_ONLY = 0, ORC_KSHORTEST = 1, ORC_RELAY1 = 2, ORC_HIER_RELAY = 3 };
 
 #define ORC_OK 0
@@ -83,6 +93,7 @@ typedef struct orc_plan {
   int route_stride, prio_stride;
   int max_sends;
   int contig; /* merge contiguous sends on links between nodes */
+  int *rev;   /* [E] link in the opposite direction, or -1 */
   char err[256];
 } orc_plan;
 
@@ -350,6 +361,7 @@ static int build_paths(orc_plan *p) {
 /* ------------------------------------------------------------------ */
 
 void orc_destroy(orc_plan *p) {
+  if (p) free(p->rev);
   if (!p) return;
   if (p->paths) {
     for (int i = 0; i < p->P * p->P; i++) {
@@ -447,7 +459,7 @@ int orc_create(int V, int P, const int *row_ptr, const int *col, const uint32_t 
   /* collective */
   p->kind = kind;
   p->cpr = cpr;
-  if (kind == ORC_ALLGATHER) {
+  if (kind == ORC_ALLGATHER || kind == ORC_REDUCESCATTER || kind == ORC_ALLREDUCE) {
     if (cpr <= 0) return ORC_EINVAL;
     p->C = P * cpr;
     p->owner = (int *)malloc(sizeof(int) * p->C);
@@ -510,6 +522,21 @@ int orc_create(int V, int P, const int *row_ptr, const int *col, const uint32_t 
   }
   int rc = build_paths(p);
   if (rc) return rc;
+  /* reductions run the trees backwards: every routed link needs a reverse */
+  p->rev = (int *)malloc(sizeof(int) * (p->E > 0 ? p->E : 1));
+  for (int e = 0; e < p->E; e++) {
+    p->rev[e] = -1;
+    for (int f = p->row_ptr[p->col[e]]; f < p->row_ptr[p->col[e] + 1]; f++)
+      if (p->col[f] == p->lsrc[e]) p->rev[e] = f;
+  }
+  if (kind == ORC_REDUCESCATTER || kind == ORC_ALLREDUCE)
+    for (int pp = 0; pp < P * P; pp++)
+      for (int i = 0; i < p->paths[pp].n; i++)
+        for (int j = 0; j < p->paths[pp].p[i].hops; j++)
+          if (p->rev[p->paths[pp].p[i].link[j]] < 0) {
+            snprintf(p->err, sizeof p->err, "a routed link has no reverse link");
+            return ORC_EINVAL;
+          }
   /* layouts: Allgather-like (tree) chunks read route c*P+d and priority
    * c*V+v; Alltoall chunks read route c and priority c*H+h */
   if (kind == ORC_ALLTOALL) {
@@ -518,7 +545,8 @@ int orc_create(int V, int P, const int *row_ptr, const int *col, const uint32_t 
     p->max_sends = p->C * p->H;
   } else {
     p->route_stride = p->C * P;
-    p->prio_stride = p->C * V;
+    /* Allreduce: the ReduceScatter row, then the Allgather row */
+    p->prio_stride = p->C * V * (kind == ORC_ALLREDUCE ? 2 : 1);
     p->max_sends = p->C * (V - 1);
   }
   return ORC_OK;
@@ -567,6 +595,7 @@ typedef struct {
   uint64_t rem, trav;
   uint32_t prio;
   int cpred;   /* send that brings the chunk to `from`, or -1 */
+  int csucc;   /* reduction: the send that carries this partial on, or -1 */
   int lpred;   /* previous send on the same link, or -1 */
   int pos;     /* position in the link's order */
   uint64_t start, finish;
@@ -593,6 +622,7 @@ typedef struct {
   int *send_of;     /* [C*V] send index that brings c into v */
   uint8_t *present; /* [C*V] */
   int *idx, *succ_ptr, *succ, *indeg, *queue;
+  int *pred_ptr, *pred; /* chunk predecessors of every send (CSR) */
   uint64_t *dist, *height;
 } oscratch;
 
@@ -608,6 +638,8 @@ static void scratch_init(const orc_plan *p, oscratch *w) {
   w->succ = (int *)malloc(sizeof(int) * 2 * ms);
   w->indeg = (int *)malloc(sizeof(int) * ms);
   w->queue = (int *)malloc(sizeof(int) * ms);
+  w->pred_ptr = (int *)malloc(sizeof(int) * (ms + 1));
+  w->pred = (int *)malloc(sizeof(int) * ms);
   w->dist = (uint64_t *)malloc(sizeof(uint64_t) * p->V);
   w->height = (uint64_t *)malloc(sizeof(uint64_t) * p->V);
 }
@@ -622,6 +654,8 @@ static void scratch_free(oscratch *w) {
   free(w->succ);
   free(w->indeg);
   free(w->queue);
+  free(w->pred_ptr);
+  free(w->pred);
   free(w->dist);
   free(w->height);
 }
@@ -709,6 +743,58 @@ static void build_tree_sends(const orc_plan *p, const uint8_t *rt, const uint32_
   for (int i = 0; i < w->n; i++) {
     osend *s = &w->s[i];
     s->cpred = (s->from == p->owner[s->chunk]) ? -1 : w->send_of[(size_t)s->chunk * V + s->from];
+    s->csucc = -1;
+  }
+}
+
+/* ReduceScatter sends: the Allgather tree of every chunk backwards. The
+ * Allgather send u -> v (link l) becomes v -> u on the reverse of l and
+ * carries the partial reduction of v's subtree: it waits for every send into
+ * v, and the send out of u waits for it. Keys on the reversed tree:
+ * remaining = reversed distance from v to the owner (this send included),
+ * travelled = longest reversed path from a vertex below v up to v. */
+static void reverse_tree_sends(const orc_plan *p, oscratch *w) {
+  int V = p->V;
+  for (int c = 0; c < p->C; c++) {
+    int o = p->owner[c];
+    const int *par = &w->tree_parent[(size_t)c * V];
+    const uint8_t *pres = &w->present[(size_t)c * V];
+    /* up[v]: reversed distance from v to the owner */
+    for (int v = 0; v < V; v++) {
+      uint64_t t = 0;
+      int x = v;
+      if (pres[v])
+        while (x != o) {
+          t += p->cost[p->rev[par[x]]];
+          x = p->lsrc[par[x]];
+        }
+      w->dist[v] = t;
+    }
+    /* below[a]: longest reversed path from a vertex of a's subtree up to a */
+    for (int v = 0; v < V; v++) w->height[v] = 0;
+    for (int v = 0; v < V; v++) {
+      if (!pres[v]) continue;
+      int x = v;
+      while (x != o) {
+        int a = p->lsrc[par[x]];
+        uint64_t h = w->dist[v] - w->dist[a];
+        if (h > w->height[a]) w->height[a] = h;
+        x = a;
+      }
+    }
+    for (int v = 0; v < V; v++) {
+      int i = w->send_of[(size_t)c * V + v];
+      if (i < 0) continue;
+      osend *s = &w->s[i];
+      int u = s->from;
+      s->link = p->rev[par[v]];
+      s->from = v;
+      s->to = u;
+      s->rem = w->dist[v];
+      s->trav = w->height[v];
+      s->cpred = -1;
+      s->csucc = (u == o) ? -1 : w->send_of[(size_t)c * V + u];
+    }
   }
 }
 
@@ -738,6 +824,7 @@ static void build_path_sends(const orc_plan *p, const uint8_t *rt, const uint32_
       s->rem = total - before;
       s->prio = pr[(size_t)c * H + j];
       s->cpred = j == 0 ? -1 : w->n - 1;
+      s->csucc = -1;
       before += p->cost[q->link[j]];
       w->n++;
     }
@@ -759,6 +846,32 @@ static int postcondition(const orc_plan *p, const oscratch *w) {
 static uint64_t transfer_cost(const orc_plan *p, int e, uint64_t m) {
   unsigned __int128 b = (unsigned __int128)p->beta[e] * m * p->S;
   return (uint64_t)p->alpha[e] + (uint64_t)((b + 999) / 1000);
+}
+
+/* Chunk predecessors of every send: the send that brings the chunk to its
+ * source (cpred), or, in a reduction, every send whose partial it carries on
+ * (the sends whose csucc it is). A send is ready when all of them ended. */
+static void chunk_preds(oscratch *w) {
+  int n = w->n;
+  for (int i = 0; i <= n; i++) w->pred_ptr[i] = 0;
+  for (int i = 0; i < n; i++) {
+    if (w->s[i].cpred >= 0) w->pred_ptr[i + 1]++;
+    if (w->s[i].csucc >= 0) w->pred_ptr[w->s[i].csucc + 1]++;
+  }
+  for (int i = 0; i < n; i++) w->pred_ptr[i + 1] += w->pred_ptr[i];
+  int *fill = w->indeg; /* cursor, before the sweep uses it */
+  for (int i = 0; i < n; i++) fill[i] = w->pred_ptr[i];
+  for (int i = 0; i < n; i++) {
+    if (w->s[i].cpred >= 0) w->pred[fill[i]++] = w->s[i].cpred;
+    if (w->s[i].csucc >= 0) w->pred[fill[w->s[i].csucc]++] = i;
+  }
+}
+
+static uint64_t ready_time(const oscratch *w, int i) {
+  uint64_t r = 0;
+  for (int j = w->pred_ptr[i]; j < w->pred_ptr[i + 1]; j++)
+    if (w->s[w->pred[j]].finish > r) r = w->s[w->pred[j]].finish;
+  return r;
 }
 
 /* Schedule with contiguous transfers. Sends are taken in the global Step-2
@@ -785,7 +898,7 @@ static int contig_sweep(const orc_plan *p, oscratch *w, uint32_t *makespan, uint
     int i = order[t];
     osend *s = &w->s[i];
     int e = s->link;
-    uint64_t ready = s->cpred >= 0 ? w->s[s->cpred].finish : 0;
+    uint64_t ready = ready_time(w, i);
     int between_nodes = p->node[p->lsrc[e]] != p->node[p->col[e]];
     if (between_nodes && g_m[e] > 0 && s->rem == g_rem[e] && ready <= g_start[e]) {
       g_m[e]++;
@@ -820,13 +933,16 @@ static int contig_sweep(const orc_plan *p, oscratch *w, uint32_t *makespan, uint
   return ORC_OK;
 }
 
-static int eval_one(const orc_plan *p, const uint8_t *rt, const uint32_t *pr, oscratch *w,
-                    uint32_t *makespan, uint8_t *valid) {
+/* One schedule: `phase` is ORC_ALLGATHER, ORC_ALLTOALL, ORC_EXPLICIT or
+ * ORC_REDUCESCATTER (the send sets differ; ordering and timing do not). */
+static int eval_phase(const orc_plan *p, int phase, const uint8_t *rt, const uint32_t *pr,
+                      oscratch *w, uint32_t *makespan, uint8_t *valid) {
   w->n = 0;
-  if (p->kind == ORC_ALLTOALL)
+  if (phase == ORC_ALLTOALL)
     build_path_sends(p, rt, pr, w);
   else
     build_tree_sends(p, rt, pr, w);
+  if (phase == ORC_REDUCESCATTER) reverse_tree_sends(p, w);
   int n = w->n;
   /* per-link total order chunk_order(l) (App. B.2) */
   for (int i = 0; i < n; i++) w->idx[i] = i;
@@ -858,16 +974,14 @@ static int eval_one(const orc_plan *p, const uint8_t *rt, const uint32_t *pr, os
     free(cnt);
     free(fill);
   }
+  chunk_preds(w);
   if (p->contig) return contig_sweep(p, w, makespan, valid);
   /* the difference constraints of App. B.3 without contiguity form a DAG
    * (chunk edges and link-order edges); sweep it in topological order */
   for (int i = 0; i <= n; i++) w->succ_ptr[i] = 0;
   for (int i = 0; i < n; i++) {
-    w->indeg[i] = 0;
-    if (w->s[i].cpred >= 0) {
-      w->succ_ptr[w->s[i].cpred + 1]++;
-      w->indeg[i]++;
-    }
+    w->indeg[i] = w->pred_ptr[i + 1] - w->pred_ptr[i];
+    for (int j = w->pred_ptr[i]; j < w->pred_ptr[i + 1]; j++) w->succ_ptr[w->pred[j] + 1]++;
     if (w->s[i].lpred >= 0) {
       w->succ_ptr[w->s[i].lpred + 1]++;
       w->indeg[i]++;
@@ -878,7 +992,7 @@ static int eval_one(const orc_plan *p, const uint8_t *rt, const uint32_t *pr, os
     int *fill = w->queue; /* reuse as a cursor array before the sweep */
     for (int i = 0; i < n; i++) fill[i] = w->succ_ptr[i];
     for (int i = 0; i < n; i++) {
-      if (w->s[i].cpred >= 0) w->succ[fill[w->s[i].cpred]++] = i;
+      for (int j = w->pred_ptr[i]; j < w->pred_ptr[i + 1]; j++) w->succ[fill[w->pred[j]]++] = i;
       if (w->s[i].lpred >= 0) w->succ[fill[w->s[i].lpred]++] = i;
     }
   }
@@ -889,7 +1003,7 @@ static int eval_one(const orc_plan *p, const uint8_t *rt, const uint32_t *pr, os
   while (head < tail) {
     int i = w->queue[head++];
     osend *s = &w->s[i];
-    uint64_t ready = s->cpred >= 0 ? w->s[s->cpred].finish : 0;
+    uint64_t ready = ready_time(w, i);
     uint64_t busy = s->lpred >= 0 ? w->s[s->lpred].finish : 0;
     s->start = ready > busy ? ready : busy;
     s->finish = s->start + p->cost[s->link];
@@ -901,6 +1015,22 @@ static int eval_one(const orc_plan *p, const uint8_t *rt, const uint32_t *pr, os
   if (span >= (1ull << 32)) return ORC_ELIMIT;
   *makespan = (uint32_t)span;
   *valid = (uint8_t)postcondition(p, w);
+  return ORC_OK;
+}
+
+static int eval_one(const orc_plan *p, const uint8_t *rt, const uint32_t *pr, oscratch *w,
+                    uint32_t *makespan, uint8_t *valid) {
+  if (p->kind != ORC_ALLREDUCE) return eval_phase(p, p->kind, rt, pr, w, makespan, valid);
+  /* Allreduce: ReduceScatter, then Allgather starting when it has ended */
+  uint32_t m1, m2;
+  uint8_t v1, v2;
+  int rc = eval_phase(p, ORC_REDUCESCATTER, rt, pr, w, &m1, &v1);
+  if (rc) return rc;
+  rc = eval_phase(p, ORC_ALLGATHER, rt, pr + (size_t)p->C * p->V, w, &m2, &v2);
+  if (rc) return rc;
+  if ((uint64_t)m1 + m2 >= (1ull << 32)) return ORC_ELIMIT;
+  *makespan = m1 + m2;
+  *valid = (uint8_t)(v1 && v2);
   return ORC_OK;
 }
 
@@ -919,29 +1049,61 @@ int orc_eval(const orc_plan *p, int64_t n, const uint8_t *routes, const uint32_t
 }
 
 /* One candidate with every send reported: chunk, link, from, to, hop,
- * rem, trav, prio, position in its link's order, start, finish. */
+ * rem, trav, prio, position in its link's order, start, finish. For
+ * Allreduce the ReduceScatter sends come first, then the Allgather sends
+ * with their times shifted by the ReduceScatter makespan. */
+typedef struct {
+  int *chunk, *link, *from, *to, *hop, *pos;
+  uint64_t *rem, *trav, *start, *finish;
+  uint32_t *pr;
+} odetail;
+
+static void copy_detail(const oscratch *w, const odetail *o, int at, int cap, uint64_t shift) {
+  for (int i = 0; i < w->n && at + i < cap; i++) {
+    const osend *s = &w->s[i];
+    o->chunk[at + i] = s->chunk;
+    o->link[at + i] = s->link;
+    o->from[at + i] = s->from;
+    o->to[at + i] = s->to;
+    o->hop[at + i] = s->hop;
+    o->rem[at + i] = s->rem;
+    o->trav[at + i] = s->trav;
+    o->pr[at + i] = s->prio;
+    o->pos[at + i] = s->pos;
+    o->start[at + i] = s->start + shift;
+    o->finish[at + i] = s->finish + shift;
+  }
+}
+
 int orc_eval_detail(const orc_plan *p, const uint8_t *routes, const uint32_t *prio, int cap,
                     int *nsends, int *chunk, int *link, int *from, int *to, int *hop,
                     uint64_t *rem, uint64_t *trav, uint32_t *pr, int *pos, uint64_t *start,
                     uint64_t *finish, uint32_t *makespan, uint8_t *valid) {
+  odetail o = {chunk, link, from, to, hop, pos, rem, trav, start, finish, pr};
   oscratch w;
   scratch_init(p, &w);
-  int rc = eval_one(p, routes, prio, &w, makespan, valid);
-  if (rc == ORC_OK) {
-    *nsends = w.n;
-    if (w.n > cap) rc = ORC_ELIMIT;
-    for (int i = 0; i < w.n && i < cap; i++) {
-      chunk[i] = w.s[i].chunk;
-      link[i] = w.s[i].link;
-      from[i] = w.s[i].from;
-      to[i] = w.s[i].to;
-      hop[i] = w.s[i].hop;
-      rem[i] = w.s[i].rem;
-      trav[i] = w.s[i].trav;
-      pr[i] = w.s[i].prio;
-      pos[i] = w.s[i].pos;
-      start[i] = w.s[i].start;
-      finish[i] = w.s[i].finish;
+  int rc;
+  if (p->kind != ORC_ALLREDUCE) {
+    rc = eval_phase(p, p->kind, routes, prio, &w, makespan, valid);
+    if (rc == ORC_OK) {
+      *nsends = w.n;
+      if (w.n > cap) rc = ORC_ELIMIT;
+      copy_detail(&w, &o, 0, cap, 0);
+    }
+  } else {
+    uint32_t m1, m2;
+    uint8_t v1, v2;
+    rc = eval_phase(p, ORC_REDUCESCATTER, routes, prio, &w, &m1, &v1);
+    int n1 = w.n;
+    if (rc == ORC_OK) copy_detail(&w, &o, 0, cap, 0);
+    if (rc == ORC_OK)
+      rc = eval_phase(p, ORC_ALLGATHER, routes, prio + (size_t)p->C * p->V, &w, &m2, &v2);
+    if (rc == ORC_OK) {
+      copy_detail(&w, &o, n1, cap, m1);
+      *nsends = n1 + w.n;
+      if (n1 + w.n > cap) rc = ORC_ELIMIT;
+      *makespan = m1 + m2;
+      *valid = (uint8_t)(v1 && v2);
     }
   }
   scratch_free(&w);

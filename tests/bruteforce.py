@@ -291,8 +291,95 @@ def contiguous_schedule(w, sends, orders):
     return start, finish
 
 
+def reverse_link(w, e):
+    u, v = _src(w, e), int(w.col[e])
+    for f, x in out_links(w, v):
+        if x == u:
+            return f
+    raise ValueError(f"link {e} has no reverse")
+
+
+def reduce_sends(w, cost, ag_sends, owner):
+    """ReduceScatter sends: every Allgather tree edge u -> v run backwards,
+    v -> u on the reverse link, carrying v's partial. Remaining length: the
+    reversed path from v to the owner, walked edge by edge; travelled: the
+    longest reversed path from any vertex below v up to v, by enumerating the
+    vertices whose walk to the owner passes v."""
+    into = {(s["chunk"], s["to"]): s for s in ag_sends}
+
+    def walk(c, y, stop):
+        t, x = 0, y
+        while x != owner[c] and x != stop:
+            p = into[(c, x)]
+            t += cost[reverse_link(w, p["link"])]
+            x = p["frm"]
+        return t, x
+
+    rs = []
+    for s in ag_sends:
+        c, u, v = s["chunk"], s["frm"], s["to"]
+        up, _ = walk(c, v, None)
+        below = 0
+        for (cc, y) in into:
+            if cc == c:
+                t, x = walk(c, y, v)
+                if x == v:
+                    below = max(below, t)
+        rs.append(dict(chunk=c, link=reverse_link(w, s["link"]), frm=v, to=u, rem=up,
+                       trav=below, prio=s["prio"]))
+    return rs
+
+
+def reduce_least_schedule(sends, cost, orders):
+    """Least send times of a reduction: a send from v waits for every send
+    into v (same chunk); link order as in App. B.3. Relaxed to a fixpoint."""
+    deps = [[j for j, y in enumerate(sends) if y["chunk"] == x["chunk"] and y["to"] == x["frm"]]
+            for x in sends]
+    t = [0] * len(sends)
+    changed, rounds = True, 0
+    while changed:
+        changed = False
+        rounds += 1
+        if rounds > len(sends) + 2:
+            raise RuntimeError("constraint graph has a positive cycle")
+        for i in range(len(sends)):
+            lo = max([t[j] + cost[sends[j]["link"]] for j in deps[i]], default=0)
+            if lo > t[i]:
+                t[i] = lo
+                changed = True
+        for l, order in orders.items():
+            for a_pos in range(len(order)):
+                for b_pos in range(a_pos + 1, len(order)):
+                    a, b = order[a_pos], order[b_pos]
+                    if t[a] + cost[l] > t[b]:
+                        t[b] = t[a] + cost[l]
+                        changed = True
+    return t, [t[i] + cost[s["link"]] for i, s in enumerate(sends)]
+
+
 def evaluate(w, table, routes, prio, H=None):
     """Makespan, valid and per-send detail of one candidate."""
+    if w.kind in (3, 4):  # ReduceScatter, Allreduce
+        cost = costs_of(w)
+        P, V = w.P, w.V
+        C = P * w.chunks_per_rank
+        owner = [c // w.chunks_per_rank for c in range(C)]
+        posts = [list(range(P)) for _ in range(C)]
+        CV = C * V
+        ag, present = tree_sends(w, cost, table, routes, prio[:CV], owner, posts)
+        rs = reduce_sends(w, cost, ag, owner)
+        orders = link_orders(rs)
+        start, finish = reduce_least_schedule(rs, cost, orders)
+        valid = all(r in present[c] for c in range(C) for r in posts[c])
+        mk = max(finish) if finish else 0
+        if w.kind == 3:
+            return mk, int(valid), rs, start, finish, orders
+        ag2, _ = tree_sends(w, cost, table, routes, prio[CV:], owner, posts)
+        orders2 = link_orders(ag2)
+        start2, finish2 = least_schedule(ag2, cost, orders2)
+        mk2 = max(finish2) if finish2 else 0
+        return (mk + mk2, int(valid), rs + ag2, start + [x + mk for x in start2],
+                finish + [x + mk for x in finish2], None)
     cost = costs_of(w)
     P = w.P
     if w.kind == 1:  # Alltoall

@@ -4,6 +4,7 @@ Holds workload descriptors (topology, collective, sketch, batch size, seed)
 and the counter-based candidate generator; none of the evaluation's
 arithmetic lives here.
 """
-from .configs import (ALLGATHER, ALLTOALL, CONTIG_ORDER, EXPLICIT, HIER_RELAY, KSHORTEST,  # noqa
-                      NAMED, ORDER, RELAY1, SHORTEST_ONLY, Workload, named, with_contiguity)
+from .configs import (ALLGATHER, ALLREDUCE, ALLTOALL, CONTIG_ORDER, EXPLICIT, HIER_RELAY,  # noqa
+                      KSHORTEST, NAMED, ORDER, REDUCE_ORDER, REDUCESCATTER, RELAY1,
+                      SHORTEST_ONLY, Workload, as_reduction, named, with_contiguity)
 from .candgen import build_candgen, generate  # noqa: F401

@@ -24,7 +24,7 @@ from typing import Optional
 
 import numpy as np
 
-ALLGATHER, ALLTOALL, EXPLICIT = 0, 1, 2
+ALLGATHER, ALLTOALL, EXPLICIT, REDUCESCATTER, ALLREDUCE = 0, 1, 2, 3, 4
 SHORTEST_ONLY, KSHORTEST, RELAY1, HIER_RELAY = 0, 1, 2, 3
 
 KIB = 1024
@@ -239,6 +239,23 @@ def with_contiguity(w):
 NAMED["twonode16_ag_contig"] = lambda **kw: with_contiguity(twonode16_ag(**kw))
 NAMED["fournode64_a2a_contig"] = lambda **kw: with_contiguity(fournode64_a2a(**kw))
 CONTIG_ORDER = ["twonode16_ag_contig", "fournode64_a2a_contig"]
+
+
+def as_reduction(w, kind):
+    """The same topology, sketch and trees as an Allgather workload, as
+    ReduceScatter (the trees run backwards) or Allreduce (ReduceScatter then
+    Allgather)."""
+    suffix = {REDUCESCATTER: "_rs", ALLREDUCE: "_ar"}[kind]
+    base = w.name[:-3] if w.name.endswith("_ag") else w.name
+    what = {REDUCESCATTER: "ReduceScatter", ALLREDUCE: "Allreduce"}[kind]
+    return replace(w, name=base + suffix, kind=kind,
+                   description=w.description.replace("Allgather", what))
+
+
+NAMED["cubemesh8_ar"] = lambda **kw: as_reduction(cubemesh8_ag(**kw), ALLREDUCE)
+NAMED["twonode16_rs"] = lambda **kw: as_reduction(twonode16_ag(**kw), REDUCESCATTER)
+NAMED["twonode16_ar"] = lambda **kw: as_reduction(twonode16_ag(**kw), ALLREDUCE)
+REDUCE_ORDER = ["cubemesh8_ar", "twonode16_rs", "twonode16_ar"]
 
 
 def named(name, **kw):
