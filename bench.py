@@ -27,7 +27,8 @@ DEFAULT_WORKLOAD = "twonode16_ag"
 # Kernel that dominates each workload's launch (the only kernel it runs).
 KERNEL_OF = {"ring4_ag": "tree_eval", "cubemesh8_ag": "tree_eval", "twonode16_ag": "tree_eval",
              "switch16_a2a": "path_eval_fast", "fournode64_a2a": "path_eval_fast",
-             "twonode16_ag_contig": "tree_eval", "fournode64_a2a_contig": "path_eval_fast"}
+             "twonode16_ag_contig": "tree_eval", "fournode64_a2a_contig": "path_eval_fast",
+             "cubemesh8_ar": "tree_eval", "twonode16_rs": "tree_eval", "twonode16_ar": "tree_eval"}
 
 
 def csrc_digest():
@@ -144,7 +145,7 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": args.calibrate_copy, "copies": args.steps}))
         return
-    from workloads import CONTIG_ORDER, ORDER
+    from workloads import CONTIG_ORDER, ORDER, REDUCE_ORDER
 
     w, plan, routes, prio, bufs = setup(args.workload)
     per, wall = time_launches(plan, *bufs, args.steps, args.warmup)
@@ -171,7 +172,8 @@ def main():
         "data": "synthetic (seeded SplitMix64 routes and priorities)",
         "config": {"workload": w.name, "candidates": n, "ranks": w.P, "vertices": w.V,
                    "links": w.E, "chunks": plan.num_chunks,
-                   "collective": ["allgather", "alltoall", "explicit"][w.kind],
+                   "collective": ["allgather", "alltoall", "explicit", "reducescatter",
+                                  "allreduce"][w.kind],
                    "chunk_bytes": w.chunk_bytes, "bytes_per_candidate":
                        plan.bytes_per_candidate, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
@@ -182,7 +184,7 @@ def main():
     }
     if not args.no_all:
         table = {}
-        for name in ORDER + CONTIG_ORDER:
+        for name in ORDER + CONTIG_ORDER + REDUCE_ORDER:
             if name == args.workload:
                 wl, pl, pr_ = w, plan, per
             else:

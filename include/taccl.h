@@ -53,7 +53,18 @@ typedef enum {
   /* chunk c = (s*P + d)*chunks_per_rank + j starts at s, must reach d */
   TACCL_ALLTOALL = 1,
   /* one owner per chunk and an explicit list of ranks to reach (multicast) */
-  TACCL_EXPLICIT = 2
+  TACCL_EXPLICIT = 2,
+  /* chunk c = r*chunks_per_rank + j is reduced from every rank into rank r
+   * along its Allgather tree run backwards (Sec. 5.2 builds ReduceScatter
+   * from an Allgather algorithm): the send from v to its tree parent carries
+   * v's partial, waits for every send into v and uses the reverse of the
+   * tree link (every routed link needs one); Step-2 lengths are measured on
+   * the reversed tree. Routes and priorities are indexed as for Allgather. */
+  TACCL_REDUCESCATTER = 3,
+  /* ReduceScatter then Allgather on the same trees, timed back to back; the
+   * priority row is two Allgather rows, ReduceScatter's first (prio_stride
+   * = 2*C*V). The makespan is the sum of the two phases. */
+  TACCL_ALLREDUCE = 4
 } taccl_kind_t;
 
 /* How the candidate route options of a (source, destination) pair are
@@ -95,9 +106,10 @@ taccl_status_t taccl_topology_create(int32_t num_vertices, int32_t num_ranks,
 void taccl_topology_destroy(taccl_topology_t topo);
 
 /*
- * Allgather or Alltoall over num_ranks ranks with chunks_per_rank chunks
- * per rank (Allgather) or per ordered rank pair (Alltoall), each
- * chunk_bytes long (Sec. 5.2, buffer size and chunk partitioning).
+ * Allgather, Alltoall, ReduceScatter or Allreduce over num_ranks ranks with
+ * chunks_per_rank chunks per rank (Allgather, ReduceScatter, Allreduce) or
+ * per ordered rank pair (Alltoall), each chunk_bytes long (Sec. 5.2, buffer
+ * size and chunk partitioning).
  */
 taccl_status_t taccl_collective_create(taccl_kind_t kind, int32_t num_ranks,
                                        int32_t chunks_per_rank, uint64_t chunk_bytes,

@@ -49,7 +49,8 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
          o_llc = pk.add(p->llc), o_trec = pk.add(p->tree_rec), o_own8 = pk.add(p->owner8),
          o_arec = pk.add(p->arec), o_cpath = pk.add(p->cpath), o_cinfo = pk.add(p->cinfo),
          o_cbkt = pk.add(p->cbkt), o_topt = pk.add(p->topt), o_trec4 = pk.add(p->tree_rec4),
-         o_lal = pk.add(p->lalpha), o_lbs = pk.add(p->lbs), o_lmg = pk.add(p->lmerge);
+         o_lal = pk.add(p->lalpha), o_lbs = pk.add(p->lbs), o_lmg = pk.add(p->lmerge),
+         o_lrev = pk.add(p->lrev);
   void *blk = nullptr;
   e = hipMalloc(&blk, pk.bytes.size());
   if (e != hipSuccess) return fail(TACCL_ERR_NO_MEMORY, "hipMalloc of plan tables failed");
@@ -81,6 +82,7 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
   t.lalpha = (const uint32_t *)at(o_lal);
   t.lbs = (const uint64_t *)at(o_lbs);
   t.lmerge = (const uint8_t *)at(o_lmg);
+  t.lrev = (const uint16_t *)at(o_lrev);
   t.arec = (const uint32_t *)at(o_arec);
   t.cpath = (const uint32_t *)at(o_cpath);
   t.cinfo = (const uint32_t *)at(o_cinfo);
@@ -208,35 +210,63 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     // the layered kernel needs whole route words and priorities in registers
     const bool layered = a.routes_word_aligned && tree_layers_layout(*p, a) > 0 &&
                          tree_block_bytes(a, 1) <= t->max_lds;
+    const int kind = p->coll.kind;
+    const bool reduction = kind == TACCL_REDUCESCATTER || kind == TACCL_ALLREDUCE;
     if (!layered && p->contig)
       return fail(TACCL_ERR_UNSUPPORTED,
                   "contiguous transfers need the layered multicast kernel, which this plan "
                   "does not fit");
+    if (!layered && reduction)
+      return fail(TACCL_ERR_UNSUPPORTED,
+                  "ReduceScatter and Allreduce need the layered multicast kernel, which this "
+                  "plan does not fit");
     if (!layered && tree_layout(*p, a) > t->max_lds)
       return fail(TACCL_ERR_UNSUPPORTED, "multicast plan needs more LDS than a block has");
+    a.lrev = t->lrev;
     // wavefronts per block: most resident wavefronts per CU (LDS, and for
     // the layered kernel registers too, by the runtime's occupancy query)
-    int best_w = 1, best_res = 0, best_bpc = 1;
-    for (int w = 1; w <= kTreeMaxThreads / 64; w++) {
-      const int bytes = tree_block_bytes(a, w);
-      if (bytes > t->max_lds) break;
-      int bpc = std::min(t->lds_per_cu / bytes, 32 / w);
-      if (layered) {
-        a.waves_per_block = w;
-        const int nb = tree_layers_blocks_per_cu(a);
-        if (nb > 0) bpc = std::min(bpc, nb);
+    auto launch = [&](TreeArgs &x) {
+      int best_w = 1, best_res = 0, best_bpc = 1;
+      for (int w = 1; w <= kTreeMaxThreads / 64; w++) {
+        const int bytes = tree_block_bytes(x, w);
+        if (bytes > t->max_lds) break;
+        int bpc = std::min(t->lds_per_cu / bytes, 32 / w);
+        if (layered) {
+          x.waves_per_block = w;
+          const int nb = tree_layers_blocks_per_cu(x);
+          if (nb > 0) bpc = std::min(bpc, nb);
+        }
+        const int res = std::min(bpc * w, 32);
+        if (res > best_res) {
+          best_res = res;
+          best_w = w;
+          best_bpc = bpc;
+        }
       }
-      const int res = std::min(bpc * w, 32);
-      if (res > best_res) {
-        best_res = res;
-        best_w = w;
-        best_bpc = bpc;
+      x.waves_per_block = best_w;
+      const int64_t want = (n + best_w - 1) / best_w;
+      const int tgrid =
+          (int)std::min<int64_t>(want, (int64_t)std::max(t->num_cus, 1) * best_bpc);
+      return layered ? launch_tree_layers(x, tgrid, s) : launch_tree(x, tgrid, s);
+    };
+    if (kind == TACCL_ALLREDUCE) {
+      // ReduceScatter on the first priority row, then Allgather on the
+      // second, adding its makespan (same stream, so in order)
+      a.reduce = 1;
+      a.accumulate = 0;
+      e = launch(a);
+      if (e == hipSuccess) {
+        TreeArgs b = a;
+        b.reduce = 0;
+        b.accumulate = 1;
+        b.prio = d_prio + (size_t)p->coll.C * p->topo.V;
+        e = launch(b);
       }
+    } else {
+      a.reduce = kind == TACCL_REDUCESCATTER;
+      a.accumulate = 0;
+      e = launch(a);
     }
-    a.waves_per_block = best_w;
-    const int64_t want = (n + best_w - 1) / best_w;
-    const int tgrid = (int)std::min<int64_t>(want, (int64_t)std::max(t->num_cus, 1) * best_bpc);
-    e = layered ? launch_tree_layers(a, tgrid, s) : launch_tree(a, tgrid, s);
   }
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
   return TACCL_OK;

@@ -383,7 +383,7 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_eval_kernel(TreeArgs a) 
 // with 16-bit counters, each bucket is ordered by the full key
 // (rem, trav, priority, chunk), and the layers are timed in turn, one lane
 // per send.
-template <int J, int PW, bool kContig>
+template <int J, int PW, bool kContig, bool kRS>
 __global__ __launch_bounds__(kTreeMaxThreads)
 void tree_layers_kernel(TreeArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
@@ -398,10 +398,16 @@ void tree_layers_kernel(TreeArgs a) {
   uint4 *s_rec = (uint4 *)(lds + a.o_rec4);       // one 16-byte record per option
   uint32_t *s_opt = (uint32_t *)(lds + a.o_opt);  // option bytes, PW words per (o, v)
   uint8_t *s_merge = lds + a.o_merge;             // links that carry contiguous transfers
+  uint16_t *s_rev = (uint16_t *)(lds + a.o_rev);  // ReduceScatter: reverse link
+  uint8_t *s_dst = lds + a.o_ldst;
   for (int j = threadIdx.x; j < E; j += blockDim.x) {
     s_cost[j] = a.cost[j];
     s_src[j] = (uint8_t)a.lsrc[j];
     s_merge[j] = a.contig ? a.lmerge[j] : 0;
+    if (kRS) {
+      s_rev[j] = a.lrev[j];
+      s_dst[j] = (uint8_t)a.ldst[j];
+    }
   }
   for (int r = threadIdx.x; r < P * P * K; r += blockDim.x) s_rec[r] = a.rec4[r];
   for (int j = threadIdx.x; j < P * V * PW; j += blockDim.x)
@@ -433,6 +439,16 @@ void tree_layers_kernel(TreeArgs a) {
   uint32_t *bnd = (uint32_t *)(wl + a.w_bnd);  // bucket start | end << 16 per position
   auto start_of = [&](uint32_t b) -> uint32_t {
     return (cnt[b >> 1] >> ((b & 1) << 4)) & 0xFFFFu;
+  };
+  // a send (slot | parent or consumer slot << 16) ends at f: Allgather
+  // records it for the sends it feeds; ReduceScatter raises the ready time
+  // of the send that carries its partial on
+  auto finish = [&](uint32_t e, uint32_t f) {
+    if (kRS) {
+      if ((e >> 16) != kNoPred) atomicMax(&fin[e >> 16], f);
+    } else {
+      fin[e & 0xFFFFu] = f;
+    }
   };
 
   const int64_t stride = (int64_t)gridDim.x * a.waves_per_block;
@@ -535,7 +551,8 @@ void tree_layers_kernel(TreeArgs a) {
             const uint32_t l = e & 0xFFFFu;
             pe[j] = l | (u << 16);
             if (u == o) {
-              dv[j] = s_cost[l];
+              // ReduceScatter measures the tree backwards, on reverse links
+              dv[j] = s_cost[kRS ? s_rev[l] : l];
               dist[sl] = dv[j];
             } else {
               ps[j] = c * V + u;
@@ -560,7 +577,8 @@ void tree_layers_kernel(TreeArgs a) {
         if (dv[j] == kNotYet && pe[j] != ~0u) {
           const uint32_t du = lds_get(&dist[ps[j]]);
           if (du != kNotYet) {
-            dv[j] = du + s_cost[pe[j] & 0xFFFFu];
+            const uint32_t l = pe[j] & 0xFFFFu;
+            dv[j] = du + s_cost[kRS ? s_rev[l] : l];
             lds_put(&dist[lane + 64 * j], dv[j]);
             dep[j] = round;
           } else {
@@ -579,11 +597,27 @@ void tree_layers_kernel(TreeArgs a) {
     for (int j = 0; j < J; j++) dmax = max(dmax, dep[j]);
     dmax = wave_max(dmax);
     wave_sync();
-    for (uint32_t t = dmax; t >= 2; t--) {
+    if (kRS) {
+      // ReduceScatter: longest reversed path from a vertex below v up to v
 #pragma unroll
       for (int j = 0; j < J; j++)
-        if (dep[j] == t) atomicMax(&dist[ps[j]], lds_get(&dist[lane + 64 * j]));
+        if (lane + 64 * j < CV) lds_put(&dist[lane + 64 * j], 0u);
       wave_sync();
+      for (uint32_t t = dmax; t >= 2; t--) {
+#pragma unroll
+        for (int j = 0; j < J; j++)
+          if (dep[j] == t)
+            atomicMax(&dist[ps[j]], lds_get(&dist[lane + 64 * j]) +
+                                        s_cost[s_rev[pe[j] & 0xFFFFu]]);
+        wave_sync();
+      }
+    } else {
+      for (uint32_t t = dmax; t >= 2; t--) {
+#pragma unroll
+        for (int j = 0; j < J; j++)
+          if (dep[j] == t) atomicMax(&dist[ps[j]], lds_get(&dist[lane + 64 * j]));
+        wave_sync();
+      }
     }
 
     // ---- keys and layers of this lane's sends ----------------------------
@@ -596,9 +630,13 @@ void tree_layers_kernel(TreeArgs a) {
       bl[j] = ~0u;
       kk[j] = 0;
       if (pe[j] != ~0u) {
-        const uint32_t l = pe[j] & 0xFFFFu;
-        const uint32_t trav = dv[j] - s_cost[l];
-        const uint32_t rem = lds_get(&dist[lane + 64 * j]) - trav;
+        // Allgather: trav = dist(u), rem = cost + height(v) = maxdist_below(v)
+        // - dist(u). ReduceScatter (send v -> u on the reverse link): rem =
+        // reversed distance from v to the owner, trav = longest reversed path
+        // up to v
+        const uint32_t l = kRS ? s_rev[pe[j] & 0xFFFFu] : pe[j] & 0xFFFFu;
+        const uint32_t trav = kRS ? lds_get(&dist[lane + 64 * j]) : dv[j] - s_cost[l];
+        const uint32_t rem = kRS ? dv[j] : lds_get(&dist[lane + 64 * j]) - trav;
         uint32_t L = (uint32_t)(((uint64_t)rem * a.lmagic) >> 32);
         if (L >= (uint32_t)a.nl_max) {  // unreachable: rem is bounded at plan time
           L = a.nl_max - 1;
@@ -709,7 +747,10 @@ void tree_layers_kernel(TreeArgs a) {
       }
       const uint32_t sl = rx.z & 0x3FFu, l = rx.z >> 10;
       const uint32_t c = div_v(sl, a.vmagic);
-      const uint32_t u = s_src[l];
+      // Allgather: the send that brings the chunk to the link's source;
+      // ReduceScatter: the send out of the link's destination, which waits
+      // for this one
+      const uint32_t u = kRS ? s_dst[l] : s_src[l];
       const uint32_t pred = (u == s_own[c]) ? kNoPred : c * V + u;
       const uint32_t q = bs + rank;
       ord2[q] = sl | (pred << 16);
@@ -718,14 +759,22 @@ void tree_layers_kernel(TreeArgs a) {
     wave_sync();
 
     // ---- least schedule, layer by layer ----------------------------------
+    if (kRS) {  // ready times are raised by the sends that feed each send
+      for (int j = lane; j < CV; j += 64) fin[j] = 0;
+      wave_sync();
+    }
     uint32_t mk = 0;
     for (int ly = 0; ly < nl; ly++) {
       const uint32_t qs = lst[ly], qe = lst[ly + 1];
       // ready time of every send of the layer: its parent send is in a
       // layer above
       for (uint32_t q = qs + lane; q < qe; q += 64) {
-        const uint32_t pj = ord2[q] >> 16;
-        rq[q] = (pj == kNoPred) ? 0u : fin[pj];
+        if (kRS) {
+          rq[q] = fin[ord2[q] & 0xFFFFu];
+        } else {
+          const uint32_t pj = ord2[q] >> 16;
+          rq[q] = (pj == kNoPred) ? 0u : fin[pj];
+        }
       }
       wave_sync();
       for (uint32_t q = qs + lane; q < qe; q += 64) {
@@ -745,7 +794,7 @@ void tree_layers_kernel(TreeArgs a) {
             const bool join = !end && gm > 0 && (info2[j] >> 31) && rq[j] <= gs;
             if (gm > 0 && !join) {  // close the open transfer
               const uint32_t f = gs + al + (uint32_t)((bsz * gm + 999) / 1000);
-              for (uint32_t t = g0; t < g0 + gm; t++) fin[ord2[t] & 0xFFFFu] = f;
+              for (uint32_t t = g0; t < g0 + gm; t++) finish(ord2[t], f);
               F = f;
               mk = max(mk, f);
             }
@@ -773,7 +822,7 @@ void tree_layers_kernel(TreeArgs a) {
             f = max(f, r[t] + (q - jt + 1) * cl);
           }
         }
-        fin[ord2[q] & 0xFFFFu] = f;
+        finish(ord2[q], f);
         mk = max(mk, f);
         if (q + 1 == qe || ((info2[q + 1] >> 16) & 0x7FFFu) == 0) lfree[l] = f;
       }
@@ -785,8 +834,14 @@ void tree_layers_kernel(TreeArgs a) {
     const bool failed = __ballot(clamped || fault) != 0;
     mk = wave_max(mk);
     if (lane == 0) {
-      a.makespan[i] = failed ? 0xFFFFFFFFu : mk;
-      a.valid[i] = (uint8_t)(all_ok && !failed);
+      if (a.accumulate) {  // second phase of an Allreduce
+        const uint32_t m0 = a.makespan[i];
+        a.makespan[i] = (failed || m0 == 0xFFFFFFFFu) ? 0xFFFFFFFFu : m0 + mk;
+        a.valid[i] = (uint8_t)(a.valid[i] && all_ok && !failed);
+      } else {
+        a.makespan[i] = failed ? 0xFFFFFFFFu : mk;
+        a.valid[i] = (uint8_t)(all_ok && !failed);
+      }
     }
     wave_sync();
   }
@@ -890,6 +945,10 @@ int32_t tree_layers_layout(const taccl_plan &p, TreeArgs &a) {
   off = align16(off + P * V * P);
   a.o_merge = off;
   off = align16(off + E);
+  a.o_rev = off;
+  off = align16(off + 2 * E);
+  a.o_ldst = off;
+  off = align16(off + E);
   a.o_wave = off;
   const int32_t S = std::max<int64_t>(std::min<int64_t>(p.max_sends, CV), 1);
   // region X: route words and distances, then bucket entries, then finish
@@ -916,28 +975,30 @@ int32_t tree_layers_layout(const taccl_plan &p, TreeArgs &a) {
   return a.o_wave + a.wave_bytes;
 }
 
-template <int J, bool kC>
+template <int J, bool kC, bool kR>
 static const void *layers_fn_j(int pw) {
   switch (pw) {
-    case 1: return (const void *)tree_layers_kernel<J, 1, kC>;
-    case 2: return (const void *)tree_layers_kernel<J, 2, kC>;
-    case 4: return (const void *)tree_layers_kernel<J, 4, kC>;
-    default: return (const void *)tree_layers_kernel<J, 8, kC>;
+    case 1: return (const void *)tree_layers_kernel<J, 1, kC, kR>;
+    case 2: return (const void *)tree_layers_kernel<J, 2, kC, kR>;
+    case 4: return (const void *)tree_layers_kernel<J, 4, kC, kR>;
+    default: return (const void *)tree_layers_kernel<J, 8, kC, kR>;
   }
 }
 
-template <bool kC>
+template <bool kC, bool kR>
 static const void *layers_fn_c(const TreeArgs &a) {
   const int J = (a.C * a.V + 63) / 64, pw = a.P / 4;
-  if (J <= 1) return layers_fn_j<1, kC>(pw);
-  if (J <= 2) return layers_fn_j<2, kC>(pw);
-  if (J <= 4) return layers_fn_j<4, kC>(pw);
-  if (J <= 8) return layers_fn_j<8, kC>(pw);
-  return layers_fn_j<16, kC>(pw);
+  if (J <= 1) return layers_fn_j<1, kC, kR>(pw);
+  if (J <= 2) return layers_fn_j<2, kC, kR>(pw);
+  if (J <= 4) return layers_fn_j<4, kC, kR>(pw);
+  if (J <= 8) return layers_fn_j<8, kC, kR>(pw);
+  return layers_fn_j<16, kC, kR>(pw);
 }
 
+// a.reduce selects the ReduceScatter variant (trees run backwards)
 static const void *layers_fn(const TreeArgs &a) {
-  return a.contig ? layers_fn_c<true>(a) : layers_fn_c<false>(a);
+  if (a.reduce) return a.contig ? layers_fn_c<true, true>(a) : layers_fn_c<false, true>(a);
+  return a.contig ? layers_fn_c<true, false>(a) : layers_fn_c<false, false>(a);
 }
 
 int tree_layers_blocks_per_cu(const TreeArgs &a) {

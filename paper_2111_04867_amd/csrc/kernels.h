@@ -42,6 +42,10 @@ struct TreeArgs {
   const uint64_t *lbs;    // beta * chunk_bytes per link
   const uint8_t *lmerge;  // 1: the link joins two nodes
   int32_t o_merge;
+  // reductions: reverse of every link; 1 = add makespan to the output and
+  // and valid into it (the Allgather phase of an Allreduce)
+  const uint16_t *lrev;
+  int32_t o_rev, o_ldst, accumulate, reduce;
   const uint8_t *topt;  // options of (o, d) through vertex v, one byte per d
   const uint4 *rec4;    // route records, one 16-byte record per option
   int32_t o_rec4, o_opt;

@@ -406,7 +406,8 @@ static taccl_status_t build_layout(taccl_plan *p) {
     p->max_sends = sends;
   } else {
     p->route_stride = C * P;
-    p->prio_stride = C * V;
+    // Allreduce: the ReduceScatter row, then the Allgather row
+    p->prio_stride = C * V * (c.kind == TACCL_ALLREDUCE ? 2 : 1);
     p->route_options.assign((size_t)C * P, 0);
     p->post_mask.assign(C, 0);
     std::vector<uint8_t> used((size_t)C * P, 0);
@@ -519,10 +520,12 @@ taccl_status_t taccl_collective_create(taccl_kind_t kind, int32_t P, int32_t cpr
   *out = nullptr;
   if (P <= 0 || cpr <= 0 || chunk_bytes == 0)
     return fail(TACCL_ERR_INVALID_ARGUMENT, "need num_ranks, chunks_per_rank, chunk_bytes > 0");
-  int64_t C = kind == TACCL_ALLGATHER ? (int64_t)P * cpr
-            : kind == TACCL_ALLTOALL  ? (int64_t)P * P * cpr
-                                      : -1;
-  if (C < 0) return fail(TACCL_ERR_INVALID_ARGUMENT, "kind must be ALLGATHER or ALLTOALL");
+  const bool tree = kind == TACCL_ALLGATHER || kind == TACCL_REDUCESCATTER ||
+                    kind == TACCL_ALLREDUCE;
+  int64_t C = tree ? (int64_t)P * cpr : kind == TACCL_ALLTOALL ? (int64_t)P * P * cpr : -1;
+  if (C < 0)
+    return fail(TACCL_ERR_INVALID_ARGUMENT,
+                "kind must be ALLGATHER, ALLTOALL, REDUCESCATTER or ALLREDUCE");
   if (C > 65536) return fail(TACCL_ERR_LIMIT, "more than 65536 chunks");
   auto *c = new (std::nothrow) taccl_collective();
   if (!c) return fail(TACCL_ERR_NO_MEMORY, "collective allocation failed");
@@ -535,7 +538,7 @@ taccl_status_t taccl_collective_create(taccl_kind_t kind, int32_t P, int32_t cpr
   c->post_ptr.resize(C + 1);
   for (int32_t ch = 0; ch < C; ch++) {
     c->post_ptr[ch] = (int32_t)c->post.size();
-    if (kind == TACCL_ALLGATHER) {
+    if (tree) {
       c->owner[ch] = ch / cpr;
       for (int32_t r = 0; r < P; r++) c->post.push_back(r);
     } else {
@@ -633,6 +636,15 @@ taccl_status_t taccl_sketch_apply(taccl_topology_t topo, taccl_collective_t coll
   }
   taccl_status_t st = build_routes(p, sk->allowed_link, sk->is_relay);
   if (st) return st;
+  // reverse of every link (reductions run the trees backwards)
+  p->lrev.assign(E, 0xFFFF);
+  for (int32_t e = 0; e < E; e++)
+    for (int32_t f = topo->row_ptr[topo->col[e]]; f < topo->row_ptr[topo->col[e] + 1]; f++)
+      if (topo->col[f] == topo->src[e]) p->lrev[e] = (uint16_t)f;
+  if (coll->kind == TACCL_REDUCESCATTER || coll->kind == TACCL_ALLREDUCE)
+    for (uint16_t l : p->path_links)
+      if (p->lrev[l] == 0xFFFF)
+        return fail(TACCL_ERR_INVALID_ARGUMENT, "a routed link has no reverse link");
   st = build_layout(p);
   if (st) return st;
   // every time is at most the sum of all send costs

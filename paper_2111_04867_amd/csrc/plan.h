@@ -54,6 +54,7 @@ struct DeviceTables {
   const uint32_t *lalpha = nullptr;
   const uint64_t *lbs = nullptr;
   const uint8_t *lmerge = nullptr;
+  const uint16_t *lrev = nullptr;
   const uint16_t *hop_class = nullptr;
   const int8_t *path_lvl_hop = nullptr;
   const uint32_t *lvl_cls_begin = nullptr;
@@ -80,6 +81,7 @@ struct taccl_plan {
   std::vector<uint32_t> lalpha;
   std::vector<uint64_t> lbs;
   std::vector<uint8_t> lmerge;
+  std::vector<uint16_t> lrev;  // link in the opposite direction, 0xFFFF if none
 
   // route options per ordered rank pair (s, d), pair index s*P + d
   std::vector<uint32_t> pair_base;  // [P*P] first option's global path index

@@ -38,7 +38,8 @@ SMALL = [lambda: cf.uni_ring_ag(7), lambda: cf.full_a2a(5), lambda: cf.full_ag(5
                                        [[1, 3], [0, 2, 4], [2], [0, 1, 2, 4]])]
 
 
-@pytest.mark.parametrize("make", [lambda n=n: cf.named(n) for n in cf.ORDER] + SMALL)
+@pytest.mark.parametrize("make", [lambda n=n: cf.named(n)
+                                  for n in cf.ORDER + cf.CONTIG_ORDER + cf.REDUCE_ORDER] + SMALL)
 def test_plan_tables_equal_oracle(make):
     w = make()
     plan = B.Plan.from_workload(w)
@@ -60,6 +61,15 @@ def test_bytes_per_candidate():
             "fournode64_a2a": 86021}
     for name, b in want.items():
         assert B.Plan.from_workload(cf.named(name)).bytes_per_candidate == b
+    # Allreduce reads two priority rows
+    assert B.Plan.from_workload(cf.named("twonode16_ar")).bytes_per_candidate == 512 + 8 * 512 + 5
+
+
+def test_reduction_needs_reverse_links():
+    w = cf.as_reduction(cf.uni_ring_ag(4), cf.REDUCESCATTER)
+    with pytest.raises(B.TacclError) as e:
+        B.Plan.from_workload(w)
+    assert e.value.status == B.ERR_INVALID_ARGUMENT
 
 
 # ----------------------------------------------------------------------------
