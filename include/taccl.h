@@ -10,8 +10,9 @@
  *     App. B.2): longest remaining path first, then shortest path already
  *     travelled, then a per-send 32-bit priority, then chunk id;
  *   - times every send under the alpha-beta model (Sec. 4.1) with strict
- *     per-link bandwidth and no contiguity (App. B.3 with every send carrying
- *     one chunk), in integer nanoseconds;
+ *     per-link bandwidth (App. B.3), in integer nanoseconds: by default every
+ *     send carries one chunk; optionally sends on links between nodes merge
+ *     into contiguous transfers (taccl_sketch_desc_t.contiguity);
  *   - checks the collective's postcondition (App. B) and returns the
  *     makespan (the objective of App. B.1).
  *
