@@ -45,6 +45,8 @@ def _load():
     lib.orc_path.argtypes = [P, ct.c_int, ct.c_int, ct.c_int, P, ct.c_int]
     lib.orc_route_options.restype = ct.c_int
     lib.orc_route_options.argtypes = [P, ct.c_int]
+    lib.orc_set_order.restype = ct.c_int
+    lib.orc_set_order.argtypes = [P, ct.c_int]
     lib.orc_set_contiguity.restype = ct.c_int
     lib.orc_set_contiguity.argtypes = [P, ct.c_int]
     lib.orc_eval.restype = ct.c_int
@@ -111,7 +113,14 @@ class OraclePlan:
                    max_cross=w.max_cross, route_mode=w.route_mode, k=w.k, owner=w.owner,
                    post_ptr=w.post_ptr, post=w.post)
         plan.set_contiguity(getattr(w, "contiguity", 0))
+        plan.set_order(getattr(w, "order", 0))
         return plan
+
+    def set_order(self, mode):
+        """0: static Step-2 orders; 1: time-aware greedy orders (App. B.2)."""
+        if _load().orc_set_order(self._h, int(mode)) != 0:
+            raise OracleError(f"bad order mode {mode}")
+        self.order = int(mode)
 
     def set_contiguity(self, mode):
         """0: one chunk per transfer; 1: contiguous transfers of equal-remaining,

@@ -32,6 +32,14 @@
  *   5. the postcondition of App. B (every (chunk, rank) pair it lists holds)
  *      and the makespan, the objective of App. B.1 (latest finishing send).
  *
+ * Optionally (orc_set_order), the per-link orders come from the time-aware
+ * greedy of App. B.2 instead of the static rule: round by round, among the
+ * sends whose chunk has arrived at their source, the one that can start
+ * earliest (max of its link's time and its chunk's time) is scheduled next,
+ * ties broken by the Step-2 heuristics, then priority, then chunk id; its
+ * link and chunk times advance by the link latency. The orders it produces
+ * are timed by the same rule as above (the greedy's own times).
+ *
  * ReduceScatter and Allreduce (Sec. 5.2, which builds them from an
  * Allgather algorithm): ReduceScatter runs every chunk's Allgather tree
  * backwards. The send from v to its tree parent carries v's partial
@@ -93,6 +101,7 @@ typedef struct orc_plan {
   int route_stride, prio_stride;
   int max_sends;
   int contig; /* merge contiguous sends on links between nodes */
+  int greedy; /* per-link orders from the time-aware greedy (App. B.2) */
   int *rev;   /* [E] link in the opposite direction, or -1 */
   char err[256];
 } orc_plan;
@@ -386,6 +395,13 @@ void orc_destroy(orc_plan *p) {
 }
 
 const char *orc_error(const orc_plan *p) { return p ? p->err : "null plan"; }
+
+/* 0: static Step-2 orders (Sec. 5.1); 1: time-aware greedy (App. B.2). */
+int orc_set_order(orc_plan *p, int mode) {
+  if (!p || mode < 0 || mode > 1) return ORC_EINVAL;
+  p->greedy = mode;
+  return ORC_OK;
+}
 
 /* 0: every send is its own transfer (App. B.3 without contiguity);
  * 1: contiguous transfers on links whose endpoints lie in different nodes. */
@@ -933,6 +949,59 @@ static int contig_sweep(const orc_plan *p, oscratch *w, uint32_t *makespan, uint
   return ORC_OK;
 }
 
+/* Time-aware greedy (App. B.2): repeatedly schedule, among the sends whose
+ * chunk predecessors are all scheduled, the one with the smallest
+ * (max(link time, ready time), Step-2 key); it starts there and ends one
+ * link latency later. Writes start/finish and each send's position in its
+ * link's order. Plain O(n^2) scan. */
+static int greedy_sweep(const orc_plan *p, oscratch *w, uint32_t *makespan, uint8_t *valid) {
+  int n = w->n, E = p->E;
+  uint64_t *busy = (uint64_t *)calloc((size_t)(E > 0 ? E : 1), sizeof(uint64_t));
+  int *count = (int *)calloc((size_t)(E > 0 ? E : 1), sizeof(int));
+  int *waiting = w->indeg; /* unscheduled chunk predecessors */
+  uint8_t *done = (uint8_t *)calloc((size_t)(n > 0 ? n : 1), 1);
+  for (int i = 0; i < n; i++) waiting[i] = w->pred_ptr[i + 1] - w->pred_ptr[i];
+  g_sort_base = w->s;
+  uint64_t span = 0;
+  for (int step = 0; step < n; step++) {
+    int best = -1;
+    uint64_t best_t = 0;
+    for (int i = 0; i < n; i++) {
+      if (done[i] || waiting[i]) continue;
+      uint64_t r = ready_time(w, i), b = busy[w->s[i].link];
+      uint64_t t = r > b ? r : b;
+      if (best < 0 || t < best_t || (t == best_t && send_order_cmp(&i, &best) < 0)) {
+        best = i;
+        best_t = t;
+      }
+    }
+    if (best < 0) {
+      free(busy);
+      free(count);
+      free(done);
+      return ORC_EINVAL; /* nothing schedulable: cannot happen */
+    }
+    osend *s = &w->s[best];
+    s->start = best_t;
+    s->finish = best_t + p->cost[s->link];
+    s->pos = count[s->link]++;
+    busy[s->link] = s->finish;
+    done[best] = 1;
+    if (s->finish > span) span = s->finish;
+    /* its chunk successors lose one unscheduled predecessor */
+    if (s->csucc >= 0) waiting[s->csucc]--;
+    for (int j = 0; j < n; j++)
+      if (w->s[j].cpred == best) waiting[j]--;
+  }
+  free(busy);
+  free(count);
+  free(done);
+  if (span >= (1ull << 32)) return ORC_ELIMIT;
+  *makespan = (uint32_t)span;
+  *valid = (uint8_t)postcondition(p, w);
+  return ORC_OK;
+}
+
 /* One schedule: `phase` is ORC_ALLGATHER, ORC_ALLTOALL, ORC_EXPLICIT or
  * ORC_REDUCESCATTER (the send sets differ; ordering and timing do not). */
 static int eval_phase(const orc_plan *p, int phase, const uint8_t *rt, const uint32_t *pr,
@@ -975,6 +1044,8 @@ static int eval_phase(const orc_plan *p, int phase, const uint8_t *rt, const uin
     free(fill);
   }
   chunk_preds(w);
+  if (p->greedy && p->contig) return ORC_EINVAL; /* not combined */
+  if (p->greedy) return greedy_sweep(p, w, makespan, valid);
   if (p->contig) return contig_sweep(p, w, makespan, valid);
   /* the difference constraints of App. B.3 without contiguity form a DAG
    * (chunk edges and link-order edges); sweep it in topological order */

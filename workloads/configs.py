@@ -66,6 +66,8 @@ class Workload:
     # 1: merge ready sends of equal remaining length into contiguous
     # transfers on links between nodes
     contiguity: int = 0
+    # 0: static Step-2 link orders; 1: time-aware greedy orders
+    order: int = 0
 
     @property
     def E(self):
@@ -256,6 +258,17 @@ NAMED["cubemesh8_ar"] = lambda **kw: as_reduction(cubemesh8_ag(**kw), ALLREDUCE)
 NAMED["twonode16_rs"] = lambda **kw: as_reduction(twonode16_ag(**kw), REDUCESCATTER)
 NAMED["twonode16_ar"] = lambda **kw: as_reduction(twonode16_ag(**kw), ALLREDUCE)
 REDUCE_ORDER = ["cubemesh8_ar", "twonode16_rs", "twonode16_ar"]
+
+
+def with_greedy(w):
+    """The same workload with link orders from the time-aware greedy."""
+    return replace(w, name=w.name + "_greedy", order=1,
+                   description=w.description + "; time-aware greedy link orders")
+
+
+NAMED["twonode16_ag_greedy"] = lambda **kw: with_greedy(twonode16_ag(**kw))
+NAMED["cubemesh8_ag_greedy"] = lambda **kw: with_greedy(cubemesh8_ag(**kw))
+GREEDY_ORDER = ["cubemesh8_ag_greedy", "twonode16_ag_greedy"]
 
 
 def named(name, **kw):
