@@ -356,6 +356,161 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_eval_kernel(TreeArgs a) 
 }
 
 
+// LDS views that the slot-parallel tree construction reads and writes.
+struct TreeLds {
+  const uint32_t *cost;
+  const uint8_t *own;
+  const uint64_t *post;
+  const uint4 *rec;
+  const uint32_t *opt;
+  const uint16_t *rev;
+  const uint32_t *rt32;
+  uint32_t *dist;
+};
+
+// Trees, one lane per (chunk c, vertex v) slot (slots lane + 64j). The
+// first-reach merge gives v the hop that enters it on the path of the
+// smallest destination whose path contains v (found from the one-hot route
+// bytes and the per-vertex option bytes, no walk). Distances from the owner
+// follow in rounds; then a push-up deepest first. On return, per slot with a
+// send: pe = link | parent vertex << 16, ps = parent's slot (or kNoPred when
+// the parent is the owner), dv = distance from the owner to v; dist[slot] =
+// largest distance below v (Allgather) or, for ReduceScatter (kRS: costs of
+// the reverse links), the longest reversed path from below up to v. `bad`:
+// a rank of the postcondition is unreached; `fault`: an impossible cycle.
+template <int J, int PW, bool kRS>
+__device__ __forceinline__ void slot_trees(const TreeArgs &a, const TreeLds &tl, int lane,
+                                           uint32_t (&pe)[J], uint32_t (&ps)[J],
+                                           uint32_t (&dv)[J], bool &bad, bool &fault) {
+  const int C = a.C, V = a.V, K = a.K;
+  constexpr int P = 4 * PW;
+  const int CV = C * V;
+  const uint32_t *s_cost = tl.cost;
+  const uint8_t *s_own = tl.own;
+  const uint64_t *s_post = tl.post;
+  const uint4 *s_rec = tl.rec;
+  const uint32_t *s_opt = tl.opt;
+  const uint16_t *s_rev = tl.rev;
+  const uint32_t *rt32 = tl.rt32;
+  uint32_t *dist = tl.dist;
+#pragma unroll
+  for (int j = 0; j < J; j++) {
+    const uint32_t sl = lane + 64 * j;
+    pe[j] = ~0u;
+    ps[j] = kNoPred;
+    dv[j] = kNotYet;
+    if (sl < (uint32_t)CV) {
+      const uint32_t c = div_v(sl, a.vmagic), v = sl - c * V;
+      const uint32_t o = s_own[c];
+      if (v == o) {
+        dist[sl] = 0;
+      } else {
+        uint32_t kw[PW], ow[PW];
+#pragma unroll
+        for (int w = 0; w < PW; w++) {
+          kw[w] = rt32[c * PW + w];
+          ow[w] = s_opt[(o * V + v) * PW + w];
+        }
+        // destinations whose drawn path passes through v: a byte of
+        // (chosen option bit & options through v) is non-zero
+        uint32_t m = 0;
+#pragma unroll
+        for (int w = 0; w < PW; w++) {
+          const uint32_t t = kw[w] & ow[w];
+          uint32_t nz = ((t + 0x7F7F7F7Fu) & 0x80808080u) >> 7;  // bit 8b per byte b
+          nz |= nz >> 7;
+          nz |= nz >> 14;
+          m |= (nz & 0xFu) << (4 * w);
+        }
+        const uint64_t pm = s_post[c];
+        m &= (uint32_t)pm;  // only postcondition destinations are routed
+        if (m) {
+          const uint32_t d = __builtin_ctz(m);
+          const uint32_t kd = __builtin_ctz((kw[d >> 2] >> (8 * (d & 3))) & 0xFFu);
+          const uint4 r = s_rec[(o * P + d) * K + kd];
+          const uint32_t x0 = r.x & 0xFFFFFFu, x1 = r.y, x2 = r.z, x3 = r.w;
+          uint32_t e, u;
+          if ((x0 >> 16) == v) {
+            e = x0; u = o;
+          } else if (((x1 >> 16) & 0xFFu) == v) {
+            e = x1; u = (x0 >> 16) & 0xFFu;
+          } else if (((x2 >> 16) & 0xFFu) == v) {
+            e = x2; u = (x1 >> 16) & 0xFFu;
+          } else {
+            e = x3; u = (x2 >> 16) & 0xFFu;
+          }
+          const uint32_t l = e & 0xFFFFu;
+          pe[j] = l | (u << 16);
+          if (u == o) {
+            // ReduceScatter measures the tree backwards, on reverse links
+            dv[j] = s_cost[kRS ? s_rev[l] : l];
+            dist[sl] = dv[j];
+          } else {
+            ps[j] = c * V + u;
+            dist[sl] = kNotYet;
+          }
+        } else if ((pm >> v) & 1) {
+          bad = true;  // a rank of the postcondition is never reached
+        }
+      }
+    }
+  }
+  wave_sync();
+  // distances: a slot takes its parent's once that is known
+  uint32_t dep[J];
+#pragma unroll
+  for (int j = 0; j < J; j++) dep[j] = (pe[j] != ~0u) ? 1u : 0u;
+  for (int round = 2;; round++) {
+    bool pend = false;
+#pragma unroll
+    for (int j = 0; j < J; j++)
+      if (dv[j] == kNotYet && pe[j] != ~0u) {
+        const uint32_t du = lds_get(&dist[ps[j]]);
+        if (du != kNotYet) {
+          const uint32_t l = pe[j] & 0xFFFFu;
+          dv[j] = du + s_cost[kRS ? s_rev[l] : l];
+          lds_put(&dist[lane + 64 * j], dv[j]);
+          dep[j] = round;
+        } else {
+          pend = true;
+        }
+      }
+    if (__ballot(pend) == 0) break;
+    if (round > V) {  // unreachable: parents form a tree
+      fault = true;
+      break;
+    }
+  }
+  // largest distance below each vertex, deepest sends first
+  uint32_t dmax = 0;
+#pragma unroll
+  for (int j = 0; j < J; j++) dmax = max(dmax, dep[j]);
+  dmax = wave_max(dmax);
+  wave_sync();
+  if (kRS) {
+    // ReduceScatter: longest reversed path from a vertex below v up to v
+#pragma unroll
+    for (int j = 0; j < J; j++)
+      if (lane + 64 * j < CV) lds_put(&dist[lane + 64 * j], 0u);
+    wave_sync();
+    for (uint32_t t = dmax; t >= 2; t--) {
+#pragma unroll
+      for (int j = 0; j < J; j++)
+        if (dep[j] == t)
+          atomicMax(&dist[ps[j]], lds_get(&dist[lane + 64 * j]) +
+                                      s_cost[s_rev[pe[j] & 0xFFFFu]]);
+      wave_sync();
+    }
+  } else {
+    for (uint32_t t = dmax; t >= 2; t--) {
+#pragma unroll
+      for (int j = 0; j < J; j++)
+        if (dep[j] == t) atomicMax(&dist[ps[j]], lds_get(&dist[lane + 64 * j]));
+      wave_sync();
+    }
+  }
+}
+
 // Layered variant for plans with at most 4 hops and 8 options per pair,
 // 4 | P <= 32 and C*V <= 1024.
 //
@@ -501,124 +656,9 @@ void tree_layers_kernel(TreeArgs a) {
     // ---- trees: the hop into every reached (chunk, vertex) ---------------
     // pe: link | parent vertex << 16 of the send into the slot, ~0 if none
     uint32_t pe[J], ps[J], dv[J];
-    bool bad = false;
-#pragma unroll
-    for (int j = 0; j < J; j++) {
-      const uint32_t sl = lane + 64 * j;
-      pe[j] = ~0u;
-      ps[j] = kNoPred;
-      dv[j] = kNotYet;
-      if (sl < (uint32_t)CV) {
-        const uint32_t c = div_v(sl, a.vmagic), v = sl - c * V;
-        const uint32_t o = s_own[c];
-        if (v == o) {
-          dist[sl] = 0;
-        } else {
-          uint32_t kw[PW], ow[PW];
-#pragma unroll
-          for (int w = 0; w < PW; w++) {
-            kw[w] = rt32[c * PW + w];
-            ow[w] = s_opt[(o * V + v) * PW + w];
-          }
-          // destinations whose drawn path passes through v: a byte of
-          // (chosen option bit & options through v) is non-zero
-          uint32_t m = 0;
-#pragma unroll
-          for (int w = 0; w < PW; w++) {
-            const uint32_t t = kw[w] & ow[w];
-            uint32_t nz = ((t + 0x7F7F7F7Fu) & 0x80808080u) >> 7;  // bit 8b per byte b
-            nz |= nz >> 7;
-            nz |= nz >> 14;
-            m |= (nz & 0xFu) << (4 * w);
-          }
-          const uint64_t pm = s_post[c];
-          m &= (uint32_t)pm;  // only postcondition destinations are routed
-          if (m) {
-            const uint32_t d = __builtin_ctz(m);
-            const uint32_t kd = __builtin_ctz((kw[d >> 2] >> (8 * (d & 3))) & 0xFFu);
-            const uint4 r = s_rec[(o * P + d) * K + kd];
-            const uint32_t x0 = r.x & 0xFFFFFFu, x1 = r.y, x2 = r.z, x3 = r.w;
-            uint32_t e, u;
-            if ((x0 >> 16) == v) {
-              e = x0; u = o;
-            } else if (((x1 >> 16) & 0xFFu) == v) {
-              e = x1; u = (x0 >> 16) & 0xFFu;
-            } else if (((x2 >> 16) & 0xFFu) == v) {
-              e = x2; u = (x1 >> 16) & 0xFFu;
-            } else {
-              e = x3; u = (x2 >> 16) & 0xFFu;
-            }
-            const uint32_t l = e & 0xFFFFu;
-            pe[j] = l | (u << 16);
-            if (u == o) {
-              // ReduceScatter measures the tree backwards, on reverse links
-              dv[j] = s_cost[kRS ? s_rev[l] : l];
-              dist[sl] = dv[j];
-            } else {
-              ps[j] = c * V + u;
-              dist[sl] = kNotYet;
-            }
-          } else if ((pm >> v) & 1) {
-            bad = true;  // a rank of the postcondition is never reached
-          }
-        }
-      }
-    }
-    wave_sync();
-    // distances: a slot takes its parent's once that is known
-    uint32_t dep[J];
-#pragma unroll
-    for (int j = 0; j < J; j++) dep[j] = (pe[j] != ~0u) ? 1u : 0u;
-    bool fault = false;
-    for (int round = 2;; round++) {
-      bool pend = false;
-#pragma unroll
-      for (int j = 0; j < J; j++)
-        if (dv[j] == kNotYet && pe[j] != ~0u) {
-          const uint32_t du = lds_get(&dist[ps[j]]);
-          if (du != kNotYet) {
-            const uint32_t l = pe[j] & 0xFFFFu;
-            dv[j] = du + s_cost[kRS ? s_rev[l] : l];
-            lds_put(&dist[lane + 64 * j], dv[j]);
-            dep[j] = round;
-          } else {
-            pend = true;
-          }
-        }
-      if (__ballot(pend) == 0) break;
-      if (round > V) {  // unreachable: parents form a tree
-        fault = true;
-        break;
-      }
-    }
-    // largest distance below each vertex, deepest sends first
-    uint32_t dmax = 0;
-#pragma unroll
-    for (int j = 0; j < J; j++) dmax = max(dmax, dep[j]);
-    dmax = wave_max(dmax);
-    wave_sync();
-    if (kRS) {
-      // ReduceScatter: longest reversed path from a vertex below v up to v
-#pragma unroll
-      for (int j = 0; j < J; j++)
-        if (lane + 64 * j < CV) lds_put(&dist[lane + 64 * j], 0u);
-      wave_sync();
-      for (uint32_t t = dmax; t >= 2; t--) {
-#pragma unroll
-        for (int j = 0; j < J; j++)
-          if (dep[j] == t)
-            atomicMax(&dist[ps[j]], lds_get(&dist[lane + 64 * j]) +
-                                        s_cost[s_rev[pe[j] & 0xFFFFu]]);
-        wave_sync();
-      }
-    } else {
-      for (uint32_t t = dmax; t >= 2; t--) {
-#pragma unroll
-        for (int j = 0; j < J; j++)
-          if (dep[j] == t) atomicMax(&dist[ps[j]], lds_get(&dist[lane + 64 * j]));
-        wave_sync();
-      }
-    }
+    bool bad = false, fault = false;
+    slot_trees<J, PW, kRS>(a, TreeLds{s_cost, s_own, s_post, s_rec, s_opt, s_rev, rt32, dist},
+                           lane, pe, ps, dv, bad, fault);
 
     // ---- keys and layers of this lane's sends ----------------------------
     uint32_t bl[J];  // link | layer << 16, or ~0 for no send
