@@ -144,7 +144,16 @@ void taccl_collective_destroy(taccl_collective_t coll);
  *     already at the link's source when the transfer starts; m chunks cost
  *     alpha + ceil(beta * m * chunk_bytes / 1000) ns and all of them arrive
  *     when the transfer ends. Plans whose multicast evaluation needs the
- *     round-based kernel (see taccl_eval_batch) refuse contiguity.
+ *     round-based kernel (see taccl_eval_batch) refuse contiguity;
+ *   order: 0 = static Step-2 order per link (Sec. 5.1: remaining path desc,
+ *     travelled path asc, priority, chunk); 1 = the time-aware greedy of
+ *     App. B.2: round by round, among the sends whose chunk has arrived, the
+ *     one that can start earliest (max of link time and chunk time) goes
+ *     next, ties broken by the Step-2 key. Not combined with contiguity
+ *     (INVALID_ARGUMENT). On the GPU it is evaluated for multicast
+ *     collectives (Allgather, explicit, ReduceScatter, Allreduce) on plans
+ *     with at most 256 links that fit the layered kernel; Alltoall plans and
+ *     others are refused at evaluation (UNSUPPORTED).
  */
 typedef struct {
   const uint8_t *allowed_link;
@@ -153,6 +162,7 @@ typedef struct {
   int32_t route_mode;
   int32_t k;
   int32_t contiguity;
+  int32_t order;
 } taccl_sketch_desc_t;
 
 /*

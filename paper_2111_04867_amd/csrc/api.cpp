@@ -136,6 +136,9 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
   const int64_t cap = (int64_t)std::max(t->num_cus, 1) * 64;
   const int grid = (int)std::min<int64_t>(n, cap);
   hipError_t e;
+  if (p->coll.kind == TACCL_ALLTOALL && p->greedy)
+    return fail(TACCL_ERR_UNSUPPORTED, "time-aware greedy orders are evaluated for multicast "
+                                       "collectives only");
   if (p->coll.kind == TACCL_ALLTOALL) {
     PathArgs a{};
     a.C = p->coll.C;
@@ -208,8 +211,15 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     a.valid = d_valid;
     a.n = n;
     // the layered kernel needs whole route words and priorities in registers
-    const bool layered = a.routes_word_aligned && tree_layers_layout(*p, a) > 0 &&
-                         tree_block_bytes(a, 1) <= t->max_lds;
+    const bool greedy = p->greedy != 0;
+    const bool layered =
+        a.routes_word_aligned &&
+        (greedy ? tree_greedy_layout(*p, a) : tree_layers_layout(*p, a)) > 0 &&
+        tree_block_bytes(a, 1) <= t->max_lds;
+    if (greedy && !layered)
+      return fail(TACCL_ERR_UNSUPPORTED,
+                  "time-aware greedy orders need the layered multicast kernel (at most 256 "
+                  "links), which this plan does not fit");
     const int kind = p->coll.kind;
     const bool reduction = kind == TACCL_REDUCESCATTER || kind == TACCL_ALLREDUCE;
     if (!layered && p->contig)
@@ -233,7 +243,7 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
         int bpc = std::min(t->lds_per_cu / bytes, 32 / w);
         if (layered) {
           x.waves_per_block = w;
-          const int nb = tree_layers_blocks_per_cu(x);
+          const int nb = greedy ? tree_greedy_blocks_per_cu(x) : tree_layers_blocks_per_cu(x);
           if (nb > 0) bpc = std::min(bpc, nb);
         }
         const int res = std::min(bpc * w, 32);
@@ -247,6 +257,7 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
       const int64_t want = (n + best_w - 1) / best_w;
       const int tgrid =
           (int)std::min<int64_t>(want, (int64_t)std::max(t->num_cus, 1) * best_bpc);
+      if (greedy) return launch_tree_greedy(x, tgrid, s);
       return layered ? launch_tree_layers(x, tgrid, s) : launch_tree(x, tgrid, s);
     };
     if (kind == TACCL_ALLREDUCE) {

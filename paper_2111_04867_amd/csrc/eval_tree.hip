@@ -887,6 +887,249 @@ void tree_layers_kernel(TreeArgs a) {
   }
 }
 
+constexpr int kGreedyLinkSlots = 4;  // links per lane: at most 256 links
+
+// Time-aware greedy orders (App. B.2), multicast trees. After the trees and
+// Step-2 keys (as in the layered kernel), the greedy is simulated exactly in
+// windows: the earliest start W any ready send can take bounds every other
+// start, and a send whose chunk is not yet ready can only become ready at
+// least one link cost (c_min) after W, so on every link the best ready send
+// by (start, Step-2 key) with start < W + c_min is the greedy's next send
+// there and all of them can be committed at once. One lane holds up to four
+// links and scans each link's pending sends; committed sends are removed by
+// swapping in the link's last pending send.
+template <int J, int PW, bool kRS>
+__global__ __launch_bounds__(kTreeMaxThreads) void tree_greedy_kernel(TreeArgs a) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int C = a.C, V = a.V, E = a.E;
+  const int CV = C * V;
+
+  uint32_t *s_cost = (uint32_t *)(lds + a.o_cost);
+  uint8_t *s_src = lds + a.o_src;
+  uint8_t *s_own = lds + a.o_own;
+  uint64_t *s_post = (uint64_t *)(lds + a.o_post);
+  uint4 *s_rec = (uint4 *)(lds + a.o_rec4);
+  uint32_t *s_opt = (uint32_t *)(lds + a.o_opt);
+  uint16_t *s_rev = (uint16_t *)(lds + a.o_rev);
+  uint8_t *s_dst = lds + a.o_ldst;
+  for (int j = threadIdx.x; j < E; j += blockDim.x) {
+    s_cost[j] = a.cost[j];
+    s_src[j] = (uint8_t)a.lsrc[j];
+    if (kRS) {
+      s_rev[j] = a.lrev[j];
+      s_dst[j] = (uint8_t)a.ldst[j];
+    }
+  }
+  for (int r = threadIdx.x; r < 16 * PW * PW * a.K; r += blockDim.x) s_rec[r] = a.rec4[r];
+  for (int j = threadIdx.x; j < 4 * PW * V * PW; j += blockDim.x)
+    s_opt[j] = ((const uint32_t *)a.topt)[j];
+  for (int j = threadIdx.x; j < C; j += blockDim.x) {
+    s_own[j] = a.owner8[j];
+    s_post[j] = a.post_mask[j];
+  }
+  __syncthreads();
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  unsigned char *wl = lds + a.o_wave + wave * a.wave_bytes;
+  uint32_t *rt32 = (uint32_t *)wl;
+  uint32_t *dist = (uint32_t *)(wl + a.w_dist);
+  uint64_t *gkey = (uint64_t *)(wl + a.w_gkey);  // per slot: ~rem << 32 | trav
+  uint32_t *gpri = (uint32_t *)(wl + a.w_gpri);  // per slot: priority
+  uint32_t *glp = (uint32_t *)(wl + a.w_glp);    // per slot: link | other slot << 16
+  uint32_t *gfin = (uint32_t *)(wl + a.w_gfin);  // per slot: finish, kNotYet before
+  uint32_t *grdy = (uint32_t *)(wl + a.w_grdy);  // ReduceScatter: ready so far
+  uint32_t *gpend = (uint32_t *)(wl + a.w_gpend);  // ReduceScatter: unscheduled inputs
+  uint16_t *glist = (uint16_t *)(wl + a.w_glist);  // sends grouped by link
+  uint32_t *gofs = (uint32_t *)(wl + a.w_gofs);    // [E + 1] first list entry per link
+
+  const int64_t stride = (int64_t)gridDim.x * a.waves_per_block;
+  const int64_t first = (int64_t)blockIdx.x * a.waves_per_block + wave;
+  const int nrw = a.route_stride >> 2;
+  uint32_t pf_r[kPfRoute], pf_p[J];
+  auto prefetch = [&](int64_t i) {
+    if (i >= a.n) return;
+    const uint32_t *g32 = (const uint32_t *)(a.routes + (size_t)i * a.route_stride);
+    const uint32_t *gpr = a.prio + (size_t)i * a.prio_stride;
+#pragma unroll
+    for (int k = 0; k < kPfRoute; k++) {
+      const int j = lane + 64 * k;
+      if (j < nrw) pf_r[k] = __builtin_nontemporal_load(g32 + j);
+    }
+#pragma unroll
+    for (int k = 0; k < J; k++) {
+      const int j = lane + 64 * k;
+      if (j < CV) pf_p[k] = __builtin_nontemporal_load(gpr + j);
+    }
+  };
+  prefetch(first);
+  for (int64_t i = first; i < a.n; i += stride) {
+#pragma unroll
+    for (int k = 0; k < kPfRoute; k++) {
+      const int j = lane + 64 * k;
+      if (j < nrw) {
+        uint32_t oh = 0;
+#pragma unroll
+        for (int b = 0; b < 4; b++) {
+          const uint32_t kb = (pf_r[k] >> (8 * b)) & 0xFFu;
+          oh |= (kb < 8 ? (1u << kb) : 0u) << (8 * b);
+        }
+        rt32[j] = oh;
+      }
+    }
+    uint32_t px[J];
+#pragma unroll
+    for (int k = 0; k < J; k++) px[k] = pf_p[k];
+    prefetch(i + stride);
+    for (int l = lane; l <= E; l += 64) gofs[l] = 0;
+    wave_sync();
+
+    uint32_t pe[J], ps[J], dv[J];
+    bool bad = false, fault = false;
+    slot_trees<J, PW, kRS>(a, TreeLds{s_cost, s_own, s_post, s_rec, s_opt, s_rev, rt32, dist},
+                           lane, pe, ps, dv, bad, fault);
+
+    // ---- per-slot send records; sends counted per link ------------------
+    uint32_t lk[J], idx[J];
+#pragma unroll
+    for (int j = 0; j < J; j++) {
+      const uint32_t sl = lane + 64 * j;
+      lk[j] = ~0u;
+      if (sl < (uint32_t)CV) {
+        gfin[sl] = kNotYet;
+        if (kRS) {
+          grdy[sl] = 0;
+          gpend[sl] = 0;
+        }
+      }
+      if (pe[j] != ~0u) {
+        const uint32_t l0 = pe[j] & 0xFFFFu;
+        const uint32_t l = kRS ? s_rev[l0] : l0;
+        const uint32_t trav = kRS ? lds_get(&dist[sl]) : dv[j] - s_cost[l];
+        const uint32_t rem = kRS ? dv[j] : lds_get(&dist[sl]) - trav;
+        lk[j] = l;
+        gkey[sl] = ((uint64_t)(~rem) << 32) | trav;
+        gpri[sl] = px[j];
+        // Allgather: the slot whose send brings the chunk here; ReduceScatter:
+        // the slot whose send carries this partial on
+        glp[sl] = l | (ps[j] << 16);
+        idx[j] = atomicAdd(&gofs[l + 1], 1u);
+      }
+    }
+    wave_sync();
+    if (kRS) {
+#pragma unroll
+      for (int j = 0; j < J; j++)
+        if (pe[j] != ~0u && ps[j] != kNoPred) atomicAdd(&gpend[ps[j]], 1u);
+    }
+    {
+      // exclusive scan of the per-link counts (gofs[0] = 0)
+      const int n1 = E + 1;
+      const int per = (n1 + 63) >> 6;
+      const int b0 = min(lane * per, n1), b1 = min(b0 + per, n1);
+      uint32_t sum = 0;
+      for (int w = b0; w < b1; w++) sum += gofs[w];
+      const uint32_t incl = wave_incl_scan(sum, lane);
+      uint32_t run = incl - sum;
+      for (int w = b0; w < b1; w++) {
+        run += gofs[w];
+        gofs[w] = run;
+      }
+    }
+    wave_sync();
+#pragma unroll
+    for (int j = 0; j < J; j++)
+      if (lk[j] != ~0u) glist[gofs[lk[j]] + idx[j]] = (uint16_t)(lane + 64 * j);
+    wave_sync();
+
+    // ---- the greedy, window by window ------------------------------------
+    uint32_t lf[kGreedyLinkSlots], lb[kGreedyLinkSlots], ln[kGreedyLinkSlots];
+#pragma unroll
+    for (int t = 0; t < kGreedyLinkSlots; t++) {
+      const int l = lane + 64 * t;
+      lf[t] = 0;
+      lb[t] = l < E ? gofs[l] : 0;
+      ln[t] = l < E ? gofs[l + 1] - gofs[l] : 0;
+    }
+    uint32_t mk = 0;
+    for (int round = 0;; round++) {
+      uint32_t cs[kGreedyLinkSlots], cq[kGreedyLinkSlots];
+      uint32_t wmin = kNotYet;
+#pragma unroll
+      for (int t = 0; t < kGreedyLinkSlots; t++) {
+        cs[t] = kNotYet;
+        cq[t] = 0;
+        uint64_t bk = ~0ull;
+        uint64_t bq = ~0ull;
+        for (uint32_t q = 0; q < ln[t]; q++) {
+          const uint32_t x = glist[lb[t] + q];
+          const uint32_t other = glp[x] >> 16;
+          uint32_t r;
+          if (kRS) {
+            r = (gpend[x] == 0) ? grdy[x] : kNotYet;
+          } else {
+            r = (other == kNoPred) ? 0u : gfin[other];
+          }
+          if (r == kNotYet) continue;  // its chunk has not arrived yet
+          const uint32_t st = max(lf[t], r);
+          const uint64_t kx = gkey[x];
+          const uint64_t qx = ((uint64_t)gpri[x] << 32) | x;  // priority, then chunk
+          if (st < cs[t] || (st == cs[t] && (kx < bk || (kx == bk && qx < bq)))) {
+            cs[t] = st;
+            cq[t] = q;
+            bk = kx;
+            bq = qx;
+          }
+        }
+        wmin = min(wmin, cs[t]);
+      }
+      for (int o = 32; o > 0; o >>= 1) wmin = min(wmin, (uint32_t)__shfl_xor((int)wmin, o));
+      if (wmin == kNotYet) break;  // nothing left to schedule
+      if (round > CV) {  // unreachable: every window commits a send
+        fault = true;
+        break;
+      }
+      const uint64_t wend = (uint64_t)wmin + a.cmin;
+      wave_sync();
+#pragma unroll
+      for (int t = 0; t < kGreedyLinkSlots; t++) {
+        if (cs[t] != kNotYet && (uint64_t)cs[t] < wend) {
+          const int l = lane + 64 * t;
+          const uint32_t x = glist[lb[t] + cq[t]];
+          const uint32_t f = cs[t] + s_cost[l];
+          if (kRS) {
+            const uint32_t nxt = glp[x] >> 16;
+            if (nxt != kNoPred) {
+              atomicMax(&grdy[nxt], f);
+              atomicSub(&gpend[nxt], 1u);
+            }
+          }
+          gfin[x] = f;
+          lf[t] = f;
+          mk = max(mk, f);
+          glist[lb[t] + cq[t]] = glist[lb[t] + ln[t] - 1];
+          ln[t]--;
+        }
+      }
+      wave_sync();
+    }
+
+    const bool all_ok = __ballot(bad) == 0;
+    const bool failed = __ballot(fault) != 0;
+    mk = wave_max(mk);
+    if (lane == 0) {
+      if (a.accumulate) {  // second phase of an Allreduce
+        const uint32_t m0 = a.makespan[i];
+        a.makespan[i] = (failed || m0 == 0xFFFFFFFFu) ? 0xFFFFFFFFu : m0 + mk;
+        a.valid[i] = (uint8_t)(a.valid[i] && all_ok && !failed);
+      } else {
+        a.makespan[i] = failed ? 0xFFFFFFFFu : mk;
+        a.valid[i] = (uint8_t)(all_ok && !failed);
+      }
+    }
+    wave_sync();
+  }
+}
+
 int32_t align16(int32_t x) { return (x + 15) & ~15; }
 
 }  // namespace
@@ -1057,6 +1300,77 @@ hipError_t launch_tree_layers(const TreeArgs &a, int grid, hipStream_t stream) {
   const int bytes = tree_block_bytes(a, a.waves_per_block);
   void *args[] = {(void *)&a};
   return hipLaunchKernel(layers_fn(a), g, b, args, bytes, stream);
+}
+
+int32_t tree_greedy_layout(const taccl_plan &p, TreeArgs &a) {
+  if (tree_layers_layout(p, a) <= 0) return 0;
+  const int32_t C = p.coll.C, V = p.topo.V, E = p.topo.E;
+  const int32_t CV = C * V;
+  if (E > 64 * kGreedyLinkSlots) return 0;
+  uint32_t cmin = ~0u;
+  for (uint32_t c : p.cost) cmin = std::min(cmin, c);
+  a.cmin = cmin;
+  const int32_t S = std::max<int64_t>(std::min<int64_t>(p.max_sends, CV), 1);
+  int32_t w = 0;
+  auto wtake = [&](int32_t bytes) {
+    int32_t o = w;
+    w = align16(w + bytes);
+    return o;
+  };
+  a.w_rt = wtake(p.route_stride);
+  a.w_dist = wtake(4 * CV);
+  a.w_gkey = wtake(8 * CV);
+  a.w_gpri = wtake(4 * CV);
+  a.w_glp = wtake(4 * CV);
+  a.w_gfin = wtake(4 * CV);
+  a.w_grdy = wtake(4 * CV);
+  a.w_gpend = wtake(4 * CV);
+  a.w_glist = wtake(2 * S);
+  a.w_gofs = wtake(4 * (E + 1));
+  a.wave_bytes = w;
+  return a.o_wave + a.wave_bytes;
+}
+
+template <int J, bool kR>
+static const void *greedy_fn_j(int pw) {
+  switch (pw) {
+    case 1: return (const void *)tree_greedy_kernel<J, 1, kR>;
+    case 2: return (const void *)tree_greedy_kernel<J, 2, kR>;
+    case 4: return (const void *)tree_greedy_kernel<J, 4, kR>;
+    default: return (const void *)tree_greedy_kernel<J, 8, kR>;
+  }
+}
+
+template <bool kR>
+static const void *greedy_fn_r(const TreeArgs &a) {
+  const int J = (a.C * a.V + 63) / 64, pw = a.P / 4;
+  if (J <= 1) return greedy_fn_j<1, kR>(pw);
+  if (J <= 2) return greedy_fn_j<2, kR>(pw);
+  if (J <= 4) return greedy_fn_j<4, kR>(pw);
+  if (J <= 8) return greedy_fn_j<8, kR>(pw);
+  return greedy_fn_j<16, kR>(pw);
+}
+
+static const void *greedy_fn(const TreeArgs &a) {
+  return a.reduce ? greedy_fn_r<true>(a) : greedy_fn_r<false>(a);
+}
+
+int tree_greedy_blocks_per_cu(const TreeArgs &a) {
+  int nb = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, greedy_fn(a), 64 * a.waves_per_block,
+                                                   tree_block_bytes(a, a.waves_per_block)) !=
+      hipSuccess)
+    return 0;
+  return nb;
+}
+
+hipError_t launch_tree_greedy(const TreeArgs &a, int grid, hipStream_t stream) {
+  const int pw = a.P / 4;
+  if (a.P % 4 || (pw != 1 && pw != 2 && pw != 4 && pw != 8)) return hipErrorInvalidValue;
+  const dim3 g(grid), b(64 * a.waves_per_block);
+  void *args[] = {(void *)&a};
+  return hipLaunchKernel(greedy_fn(a), g, b, args, tree_block_bytes(a, a.waves_per_block),
+                         stream);
 }
 
 }  // namespace taccl

@@ -46,6 +46,10 @@ struct TreeArgs {
   // and valid into it (the Allgather phase of an Allreduce)
   const uint16_t *lrev;
   int32_t o_rev, o_ldst, accumulate, reduce;
+  // time-aware greedy orders: smallest link cost (the simulation's
+  // lookahead) and per-wavefront arrays
+  uint32_t cmin;
+  int32_t w_gkey, w_gpri, w_glp, w_gfin, w_grdy, w_gpend, w_glist, w_gofs;
   const uint8_t *topt;  // options of (o, d) through vertex v, one byte per d
   const uint4 *rec4;    // route records, one 16-byte record per option
   int32_t o_rec4, o_opt;
@@ -97,6 +101,11 @@ int32_t tree_block_bytes(const TreeArgs &a, int waves);
 // Layered multicast kernel: fills the layout and returns the bytes of a
 // one-wavefront block, or 0 when the plan does not meet its conditions.
 int32_t tree_layers_layout(const taccl_plan &p, TreeArgs &a);
+// Time-aware greedy variant (same shared tables, own per-wavefront arrays):
+// bytes of a one-wavefront block, or 0 when the plan does not fit it.
+int32_t tree_greedy_layout(const taccl_plan &p, TreeArgs &a);
+hipError_t launch_tree_greedy(const TreeArgs &a, int grid, hipStream_t stream);
+int tree_greedy_blocks_per_cu(const TreeArgs &a);
 int32_t path_layout(const taccl_plan &p, PathArgs &a);
 int32_t path_fast_layout(const taccl_plan &p, PathArgs &a);
 int path_fast_cpt(const taccl_plan &p);      // chunks per thread, 0 = not eligible

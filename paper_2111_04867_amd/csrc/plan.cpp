@@ -606,6 +606,10 @@ taccl_status_t taccl_sketch_apply(taccl_topology_t topo, taccl_collective_t coll
   if (sk->contiguity < 0 || sk->contiguity > 1)
     return fail(TACCL_ERR_INVALID_ARGUMENT, "contiguity must be 0 or 1");
   p->contig = sk->contiguity;
+  if (sk->order < 0 || sk->order > 1) return fail(TACCL_ERR_INVALID_ARGUMENT, "order must be 0 or 1");
+  if (sk->order && sk->contiguity)
+    return fail(TACCL_ERR_INVALID_ARGUMENT, "greedy orders are not combined with contiguity");
+  p->greedy = sk->order;
   const int32_t E = topo->E;
   // integer alpha-beta cost of one chunk on every link (Sec. 4.1)
   p->cost.resize(E);

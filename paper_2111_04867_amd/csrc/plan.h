@@ -78,6 +78,7 @@ struct taccl_plan {
   // contiguous transfers: per link alpha, beta * chunk_bytes and whether the
   // link joins two nodes (only those merge)
   int32_t contig = 0;
+  int32_t greedy = 0;  // link orders from the time-aware greedy
   std::vector<uint32_t> lalpha;
   std::vector<uint64_t> lbs;
   std::vector<uint8_t> lmerge;

@@ -1,0 +1,120 @@
+"""GPU parity of the time-aware greedy link orders (App. B.2) for multicast
+collectives, bit for bit against the oracle, through the C ABI. Needs an
+MI355X."""
+import numpy as np
+import pytest
+
+from oracle import OraclePlan
+from workloads import configs as cf
+from workloads import generate
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+C1 = 48935
+
+
+def say(msg):
+    print(msg, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2111_04867_amd import binding
+    binding.lib()
+    torch.cuda.set_device(0)
+    yield
+
+
+def plans(w):
+    from paper_2111_04867_amd.binding import Plan
+    plan, ref = Plan.from_workload(w), OraclePlan.from_workload(w)
+    assert ref.order == 1
+    opts = plan.route_options()
+    assert (opts == ref.route_options()).all()
+    return plan, ref, opts
+
+
+def check(plan, ref, routes, prio, label):
+    say(f"[gpu] {label}: {routes.shape[0]} candidates")
+    mk, ok = plan.eval(routes, prio)
+    rmk, rok = ref.eval_threads(routes, prio)
+    bad = np.nonzero((mk != rmk) | (ok != rok))[0]
+    assert bad.size == 0, (f"{label}: {bad.size} mismatches, first at {bad[:5].tolist()}: "
+                           f"gpu {mk[bad[:5]].tolist()} oracle {rmk[bad[:5]].tolist()}")
+    return mk, ok
+
+
+@pytest.mark.parametrize("name", cf.GREEDY_ORDER)
+def test_full_size_parity(name):
+    w = cf.named(name)
+    plan, ref, opts = plans(w)
+    routes, prio = generate(w.seed, 0, w.n_candidates, opts, plan.prio_stride)
+    mk, ok = check(plan, ref, routes, prio, f"{name} full N={w.n_candidates}")
+    assert ok.all()
+
+
+@pytest.mark.parametrize("name", cf.GREEDY_ORDER)
+@pytest.mark.parametrize("n", [1, 65, 257])
+def test_ragged_batches(name, n):
+    w = cf.named(name)
+    plan, ref, opts = plans(w)
+    routes, prio = generate(w.seed + 90, 4, n, opts, plan.prio_stride)
+    check(plan, ref, routes, prio, f"{name} n={n}")
+
+
+@pytest.mark.parametrize("value", [0, 0xFFFFFFFF])
+def test_equal_priorities(value):
+    w = cf.named("twonode16_ag_greedy")
+    plan, ref, opts = plans(w)
+    routes, prio = generate(w.seed + 6, 0, 200, opts, plan.prio_stride)
+    prio[:] = value
+    check(plan, ref, routes, prio, f"twonode16_ag_greedy prio={value:#x}")
+
+
+def test_idle_link_case():
+    """0 -> 1 -> 2 -> 3: the greedy fills link 1 -> 2 while the longer chunk
+    is still on its way (3 link costs; the static order needs 4)."""
+    edges = [(0, 1, 700, 46), (1, 2, 700, 46), (2, 3, 700, 46)]
+    row_ptr, col, a, b = cf.csr_from_edges(4, edges)
+    base = cf.Workload("chain4", 4, 4, row_ptr, col, a, b, None, cf.ALLGATHER, 1, 1 << 20,
+                       cf.KSHORTEST, k=1)
+    w = cf.with_greedy(cf.explicit_multicast(base, [0, 1, 1], [[3], [2], [2]]))
+    plan, ref, opts = plans(w)
+    routes = np.zeros((8, plan.route_stride), dtype=np.uint8)
+    prio = np.zeros((8, plan.prio_stride), dtype=np.uint32)
+    mk, ok = check(plan, ref, routes, prio, "chain4")
+    assert ok.all() and (mk == 3 * C1).all()
+
+
+@pytest.mark.parametrize("kind", [cf.ALLGATHER, cf.REDUCESCATTER, cf.ALLREDUCE])
+@pytest.mark.parametrize("cpr", [1, 3])
+def test_full4(kind, cpr):
+    w = cf.full_ag(4, k=3, chunks_per_rank=cpr)
+    if kind != cf.ALLGATHER:
+        w = cf.as_reduction(w, kind)
+    w = cf.with_greedy(w)
+    plan, ref, opts = plans(w)
+    routes, prio = generate(81 + cpr, 0, 600, opts, plan.prio_stride)
+    check(plan, ref, routes, prio, f"{w.name} cpr={cpr}")
+
+
+@pytest.mark.parametrize("kind", [cf.REDUCESCATTER, cf.ALLREDUCE])
+def test_twonode_reductions(kind):
+    w = cf.with_greedy(cf.as_reduction(cf.twonode16_ag(), kind))
+    plan, ref, opts = plans(w)
+    routes, prio = generate(w.seed + 8, 0, 1024, opts, plan.prio_stride)
+    check(plan, ref, routes, prio, w.name)
+
+
+def test_alltoall_refused():
+    from paper_2111_04867_amd.binding import Plan, TacclError
+    w = cf.with_greedy(cf.full_a2a(4))
+    plan = Plan.from_workload(w)
+    routes, prio = generate(1, 0, 2, plan.route_options(), plan.prio_stride)
+    with pytest.raises(TacclError) as e:
+        plan.eval(routes, prio)
+    assert "greedy" in str(e.value)

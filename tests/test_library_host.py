@@ -65,6 +65,13 @@ def test_bytes_per_candidate():
     assert B.Plan.from_workload(cf.named("twonode16_ar")).bytes_per_candidate == 512 + 8 * 512 + 5
 
 
+def test_greedy_orders_are_not_combined_with_contiguity():
+    w = cf.with_greedy(cf.with_contiguity(cf.twonode16_ag(n_candidates=1)))
+    with pytest.raises(B.TacclError) as e:
+        B.Plan.from_workload(w)
+    assert e.value.status == B.ERR_INVALID_ARGUMENT
+
+
 def test_reduction_needs_reverse_links():
     w = cf.as_reduction(cf.uni_ring_ag(4), cf.REDUCESCATTER)
     with pytest.raises(B.TacclError) as e:
