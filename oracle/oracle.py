@@ -45,6 +45,8 @@ def _load():
     lib.orc_path.argtypes = [P, ct.c_int, ct.c_int, ct.c_int, P, ct.c_int]
     lib.orc_route_options.restype = ct.c_int
     lib.orc_route_options.argtypes = [P, ct.c_int]
+    lib.orc_set_switch_ports.restype = ct.c_int
+    lib.orc_set_switch_ports.argtypes = [P, ct.c_int]
     lib.orc_set_order.restype = ct.c_int
     lib.orc_set_order.argtypes = [P, ct.c_int]
     lib.orc_set_contiguity.restype = ct.c_int
@@ -114,7 +116,15 @@ class OraclePlan:
                    post_ptr=w.post_ptr, post=w.post)
         plan.set_contiguity(getattr(w, "contiguity", 0))
         plan.set_order(getattr(w, "order", 0))
+        plan.set_switch_ports(getattr(w, "switch_ports", 0))
         return plan
+
+    def set_switch_ports(self, mode):
+        """0: switch vertices store and forward; 1: a hop pair through a switch
+        is one send holding the sender's and the receiver's ports."""
+        if _load().orc_set_switch_ports(self._h, int(mode)) != 0:
+            raise OracleError(f"bad switch-port mode {mode}")
+        self.switch_ports = int(mode)
 
     def set_order(self, mode):
         """0: static Step-2 orders; 1: time-aware greedy orders (App. B.2)."""

@@ -40,6 +40,13 @@
  * link and chunk times advance by the link latency. The orders it produces
  * are timed by the same rule as above (the greedy's own times).
  *
+ * Optionally (orc_set_switch_ports), Alltoall hops through a switch vertex
+ * follow the switch model of App. B.3: the pair rank -> switch -> rank is one
+ * switched send costing one latency (the uplink's alpha and beta) that holds
+ * the sender's send port (its uplink) and the receiver's receive port (its
+ * downlink) for its whole duration; each port serves its sends in Step-2
+ * order (switch_send_order / switch_recv_order of App. B.2).
+ *
  * ReduceScatter and Allreduce (Sec. 5.2, which builds them from an
  * Allgather algorithm): ReduceScatter runs every chunk's Allgather tree
  * backwards. The send from v to its tree parent carries v's partial
@@ -102,6 +109,7 @@ typedef struct orc_plan {
   int max_sends;
   int contig; /* merge contiguous sends on links between nodes */
   int greedy; /* per-link orders from the time-aware greedy (App. B.2) */
+  int ports;  /* Alltoall: switched sends hold a send and a receive port */
   int *rev;   /* [E] link in the opposite direction, or -1 */
   char err[256];
 } orc_plan;
@@ -396,6 +404,13 @@ void orc_destroy(orc_plan *p) {
 
 const char *orc_error(const orc_plan *p) { return p ? p->err : "null plan"; }
 
+/* 0: switch vertices store and forward; 1: switched sends hold ports. */
+int orc_set_switch_ports(orc_plan *p, int mode) {
+  if (!p || mode < 0 || mode > 1) return ORC_EINVAL;
+  p->ports = mode;
+  return ORC_OK;
+}
+
 /* 0: static Step-2 orders (Sec. 5.1); 1: time-aware greedy (App. B.2). */
 int orc_set_order(orc_plan *p, int mode) {
   if (!p || mode < 0 || mode > 1) return ORC_EINVAL;
@@ -613,6 +628,8 @@ typedef struct {
   int cpred;   /* send that brings the chunk to `from`, or -1 */
   int csucc;   /* reduction: the send that carries this partial on, or -1 */
   int lpred;   /* previous send on the same link, or -1 */
+  int link2;   /* switched send: the receive port (downlink), else -1 */
+  int lpred2;  /* previous send on link2, or -1 */
   int pos;     /* position in the link's order */
   uint64_t start, finish;
 } osend;
@@ -760,6 +777,7 @@ static void build_tree_sends(const orc_plan *p, const uint8_t *rt, const uint32_
     osend *s = &w->s[i];
     s->cpred = (s->from == p->owner[s->chunk]) ? -1 : w->send_of[(size_t)s->chunk * V + s->from];
     s->csucc = -1;
+    s->link2 = -1;
   }
 }
 
@@ -828,21 +846,30 @@ static void build_path_sends(const orc_plan *p, const uint8_t *rt, const uint32_
     const oplist *L = &p->paths[s0 * P + d];
     if (ch >= L->n) continue; /* unrouted */
     const opath *q = &L->p[ch];
-    uint64_t total = q->cost, before = 0;
+    /* sends: one per hop, or with switch ports one per hop pair through a
+     * switch vertex (rank -> switch -> rank), costing the uplink's latency */
+    uint64_t total = 0, before = 0;
     for (int j = 0; j < q->hops; j++) {
+      total += p->cost[q->link[j]];
+      if (p->ports && q->vert[j + 1] >= P && j + 1 < q->hops) j++;
+    }
+    for (int j = 0; j < q->hops; j++) {
+      const int switched = p->ports && q->vert[j + 1] >= P && j + 1 < q->hops;
       osend *s = &w->s[w->n];
       s->chunk = c;
       s->link = q->link[j];
+      s->link2 = switched ? q->link[j + 1] : -1;
       s->from = q->vert[j];
-      s->to = q->vert[j + 1];
+      s->to = q->vert[j + 1 + switched];
       s->hop = j;
       s->trav = before;
       s->rem = total - before;
       s->prio = pr[(size_t)c * H + j];
-      s->cpred = j == 0 ? -1 : w->n - 1;
+      s->cpred = (j == 0) ? -1 : w->n - 1;
       s->csucc = -1;
       before += p->cost[q->link[j]];
       w->n++;
+      j += switched;
     }
     pres[d] = 1;
   }
@@ -1019,20 +1046,34 @@ static int eval_phase(const orc_plan *p, int phase, const uint8_t *rt, const uin
   /* sort by link first, then by the Step-2 key inside each link */
   for (int i = 0; i < n; i++) w->s[i].lpred = -1;
   {
-    /* bucket the send indices by link */
+    /* bucket the send indices by resource: its link, and for a switched
+     * send also its receive port (link2) */
     int E = p->E;
     int *cnt = (int *)calloc((size_t)E + 1, sizeof(int));
-    for (int i = 0; i < n; i++) cnt[w->s[i].link + 1]++;
+    for (int i = 0; i < n; i++) {
+      w->s[i].lpred2 = -1;
+      cnt[w->s[i].link + 1]++;
+      if (w->s[i].link2 >= 0) cnt[w->s[i].link2 + 1]++;
+    }
     for (int e = 0; e < E; e++) cnt[e + 1] += cnt[e];
     int *fill = (int *)malloc(sizeof(int) * (E > 0 ? E : 1));
     for (int e = 0; e < E; e++) fill[e] = cnt[e];
-    for (int i = 0; i < n; i++) w->idx[fill[w->s[i].link]++] = i;
+    for (int i = 0; i < n; i++) {
+      w->idx[fill[w->s[i].link]++] = i;
+      if (w->s[i].link2 >= 0) w->idx[fill[w->s[i].link2]++] = i;
+    }
     for (int e = 0; e < E; e++) {
       int a = cnt[e], b = cnt[e + 1];
       if (b - a > 1) qsort(&w->idx[a], (size_t)(b - a), sizeof(int), send_order_cmp);
       for (int j = a; j < b; j++) {
-        w->s[w->idx[j]].pos = j - a;
-        w->s[w->idx[j]].lpred = j > a ? w->idx[j - 1] : -1;
+        osend *s = &w->s[w->idx[j]];
+        int prev = j > a ? w->idx[j - 1] : -1;
+        if (s->link == e) {
+          s->pos = j - a;
+          s->lpred = prev;
+        } else {
+          s->lpred2 = prev;
+        }
         if (j > a && send_order_cmp(&w->idx[j - 1], &w->idx[j]) == 0) {
           free(cnt);
           free(fill);
@@ -1045,6 +1086,7 @@ static int eval_phase(const orc_plan *p, int phase, const uint8_t *rt, const uin
   }
   chunk_preds(w);
   if (p->greedy && p->contig) return ORC_EINVAL; /* not combined */
+  if (p->ports && (p->greedy || p->contig)) return ORC_EINVAL;
   if (p->greedy) return greedy_sweep(p, w, makespan, valid);
   if (p->contig) return contig_sweep(p, w, makespan, valid);
   /* the difference constraints of App. B.3 without contiguity form a DAG
@@ -1057,6 +1099,10 @@ static int eval_phase(const orc_plan *p, int phase, const uint8_t *rt, const uin
       w->succ_ptr[w->s[i].lpred + 1]++;
       w->indeg[i]++;
     }
+    if (w->s[i].lpred2 >= 0) {
+      w->succ_ptr[w->s[i].lpred2 + 1]++;
+      w->indeg[i]++;
+    }
   }
   for (int i = 0; i < n; i++) w->succ_ptr[i + 1] += w->succ_ptr[i];
   {
@@ -1065,6 +1111,7 @@ static int eval_phase(const orc_plan *p, int phase, const uint8_t *rt, const uin
     for (int i = 0; i < n; i++) {
       for (int j = w->pred_ptr[i]; j < w->pred_ptr[i + 1]; j++) w->succ[fill[w->pred[j]]++] = i;
       if (w->s[i].lpred >= 0) w->succ[fill[w->s[i].lpred]++] = i;
+      if (w->s[i].lpred2 >= 0) w->succ[fill[w->s[i].lpred2]++] = i;
     }
   }
   int head = 0, tail = 0;
@@ -1076,6 +1123,7 @@ static int eval_phase(const orc_plan *p, int phase, const uint8_t *rt, const uin
     osend *s = &w->s[i];
     uint64_t ready = ready_time(w, i);
     uint64_t busy = s->lpred >= 0 ? w->s[s->lpred].finish : 0;
+    if (s->lpred2 >= 0 && w->s[s->lpred2].finish > busy) busy = w->s[s->lpred2].finish;
     s->start = ready > busy ? ready : busy;
     s->finish = s->start + p->cost[s->link];
     if (s->finish > span) span = s->finish;

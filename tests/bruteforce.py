@@ -173,6 +173,75 @@ def path_sends(w, cost, table, routes, prio, owner, dest, H):
     return sends, present
 
 
+def port_units(w, cost, table, routes, prio, owner, dest, H):
+    """Alltoall sends under the switch-port model: a hop into a switch vertex
+    (index >= P) and the hop out of it form one unit holding both links (the
+    sender's send port and the receiver's receive port) for the uplink's
+    latency; other hops are units of their own."""
+    units, present = [], {}
+    for c, (s, d) in enumerate(zip(owner, dest)):
+        present[c] = {s}
+        if s == d:
+            continue
+        opts = table.get((s, d), [])
+        ch = int(routes[c])
+        if ch >= len(opts):
+            continue
+        links = opts[ch]
+        vs = path_vertices(w, links, s)
+        mine = []
+        h = 0
+        while h < len(links):
+            if vs[h + 1] >= w.P and h + 1 < len(links):
+                mine.append(dict(chunk=c, links=[links[h], links[h + 1]], frm=vs[h], to=vs[h + 2],
+                                 hop=h, lat=cost[links[h]], prio=int(prio[c * H + h])))
+                h += 2
+            else:
+                mine.append(dict(chunk=c, links=[links[h]], frm=vs[h], to=vs[h + 1], hop=h,
+                                 lat=cost[links[h]], prio=int(prio[c * H + h])))
+                h += 1
+        for q, u in enumerate(mine):
+            u["rem"] = sum(x["lat"] for x in mine[q:])
+            u["trav"] = sum(x["lat"] for x in mine[:q])
+            u["pred"] = len(units) - 1 if q > 0 else None
+            units.append(u)
+        present[c].add(d)
+    return units, present
+
+
+def port_least_schedule(units):
+    """Least start times: after the chunk's previous unit, and on every link
+    a unit holds, after the units before it in that link's Step-2 order."""
+    orders = {}
+    for i, u in enumerate(units):
+        for l in u["links"]:
+            orders.setdefault(l, []).append(i)
+    for l in orders:
+        orders[l].sort(key=lambda i: (-units[i]["rem"], units[i]["trav"], units[i]["prio"],
+                                      units[i]["chunk"]))
+    t = [0] * len(units)
+    changed, rounds = True, 0
+    while changed:
+        changed = False
+        rounds += 1
+        if rounds > len(units) + 2:
+            raise RuntimeError("constraint graph has a positive cycle")
+        for i, u in enumerate(units):
+            if u["pred"] is not None:
+                need = t[u["pred"]] + units[u["pred"]]["lat"]
+                if need > t[i]:
+                    t[i] = need
+                    changed = True
+        for order in orders.values():
+            for a_pos in range(len(order)):
+                for b_pos in range(a_pos + 1, len(order)):
+                    a, b = order[a_pos], order[b_pos]
+                    if t[a] + units[a]["lat"] > t[b]:
+                        t[b] = t[a] + units[a]["lat"]
+                        changed = True
+    return t, [t[i] + u["lat"] for i, u in enumerate(units)]
+
+
 def link_orders(sends):
     """chunk_order per link: the Step-2 heuristic (longest remaining path
     first, then shortest travelled path) with priority and chunk id last."""
@@ -382,6 +451,14 @@ def evaluate(w, table, routes, prio, H=None):
                 finish + [x + mk for x in finish2], None)
     cost = costs_of(w)
     P = w.P
+    if w.kind == 1 and getattr(w, "switch_ports", 0):  # Alltoall, switch ports
+        C = P * P * w.chunks_per_rank
+        owner = [(c // w.chunks_per_rank) // P for c in range(C)]
+        dest = [(c // w.chunks_per_rank) % P for c in range(C)]
+        units, present = port_units(w, cost, table, routes, prio, owner, dest, H)
+        start, finish = port_least_schedule(units)
+        valid = all(d in present[c] for c, d in enumerate(dest))
+        return max(finish) if finish else 0, int(valid), units, start, finish, None
     if w.kind == 1:  # Alltoall
         C = P * P * w.chunks_per_rank
         owner = [(c // w.chunks_per_rank) // P for c in range(C)]

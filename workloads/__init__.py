@@ -5,7 +5,7 @@ and the counter-based candidate generator; none of the evaluation's
 arithmetic lives here.
 """
 from .configs import (ALLGATHER, ALLREDUCE, ALLTOALL, CONTIG_ORDER, EXPLICIT, HIER_RELAY,  # noqa
-                      GREEDY_ORDER, KSHORTEST, NAMED, ORDER, REDUCE_ORDER, REDUCESCATTER,
-                      RELAY1, SHORTEST_ONLY, Workload, as_reduction, named, with_contiguity,
-                      with_greedy)
+                      GREEDY_ORDER, KSHORTEST, NAMED, ORDER, PORTS_ORDER, REDUCE_ORDER,
+                      REDUCESCATTER, RELAY1, SHORTEST_ONLY, Workload, as_reduction, named,
+                      with_contiguity, with_greedy, with_switch_ports)
 from .candgen import build_candgen, generate  # noqa: F401

@@ -68,6 +68,9 @@ class Workload:
     contiguity: int = 0
     # 0: static Step-2 link orders; 1: time-aware greedy orders
     order: int = 0
+    # 1: Alltoall hop pairs through a switch vertex are one send holding the
+    # sender's send port and the receiver's receive port
+    switch_ports: int = 0
 
     @property
     def E(self):
@@ -269,6 +272,17 @@ def with_greedy(w):
 NAMED["twonode16_ag_greedy"] = lambda **kw: with_greedy(twonode16_ag(**kw))
 NAMED["cubemesh8_ag_greedy"] = lambda **kw: with_greedy(cubemesh8_ag(**kw))
 GREEDY_ORDER = ["cubemesh8_ag_greedy", "twonode16_ag_greedy"]
+
+
+def with_switch_ports(w):
+    """The same workload with the switch-port model."""
+    return replace(w, name=w.name + "_ports", switch_ports=1,
+                   description=w.description + "; switched sends hold send and receive ports")
+
+
+NAMED["switch16_a2a_ports"] = lambda **kw: with_switch_ports(switch16_a2a(**kw))
+NAMED["fournode64_a2a_ports"] = lambda **kw: with_switch_ports(fournode64_a2a(**kw))
+PORTS_ORDER = ["switch16_a2a_ports", "fournode64_a2a_ports"]
 
 
 def named(name, **kw):
