@@ -29,7 +29,8 @@ KERNEL_OF = {"ring4_ag": "tree_eval", "cubemesh8_ag": "tree_eval", "twonode16_ag
              "switch16_a2a": "path_eval_fast", "fournode64_a2a": "path_eval_fast",
              "twonode16_ag_contig": "tree_eval", "fournode64_a2a_contig": "path_eval_fast",
              "cubemesh8_ar": "tree_eval", "twonode16_rs": "tree_eval", "twonode16_ar": "tree_eval",
-             "cubemesh8_ag_greedy": "tree_greedy", "twonode16_ag_greedy": "tree_greedy"}
+             "cubemesh8_ag_greedy": "tree_greedy", "twonode16_ag_greedy": "tree_greedy",
+             "switch16_a2a_ports": "path_eval", "fournode64_a2a_ports": "path_eval"}
 
 
 def csrc_digest():
@@ -146,7 +147,7 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": args.calibrate_copy, "copies": args.steps}))
         return
-    from workloads import CONTIG_ORDER, GREEDY_ORDER, ORDER, REDUCE_ORDER
+    from workloads import CONTIG_ORDER, GREEDY_ORDER, ORDER, PORTS_ORDER, REDUCE_ORDER
 
     w, plan, routes, prio, bufs = setup(args.workload)
     per, wall = time_launches(plan, *bufs, args.steps, args.warmup)
@@ -185,7 +186,7 @@ def main():
     }
     if not args.no_all:
         table = {}
-        for name in ORDER + CONTIG_ORDER + REDUCE_ORDER + GREEDY_ORDER:
+        for name in ORDER + CONTIG_ORDER + REDUCE_ORDER + GREEDY_ORDER + PORTS_ORDER:
             if name == args.workload:
                 wl, pl, pr_ = w, plan, per
             else:

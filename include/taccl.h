@@ -153,7 +153,17 @@ void taccl_collective_destroy(taccl_collective_t coll);
  *     (INVALID_ARGUMENT). On the GPU it is evaluated for multicast
  *     collectives (Allgather, explicit, ReduceScatter, Allreduce) on plans
  *     with at most 256 links that fit the layered kernel; Alltoall plans and
- *     others are refused at evaluation (UNSUPPORTED).
+ *     others are refused at evaluation (UNSUPPORTED);
+ *   switch_ports (Alltoall only): 0 = a switch vertex stores and forwards
+ *     (uplink, then downlink, each one latency); 1 = the switch model of
+ *     App. B.3: a hop pair rank -> switch -> rank is one send costing one
+ *     latency (the uplink's alpha and beta) that holds the sender's send
+ *     port (uplink) and the receiver's receive port (downlink) for its whole
+ *     duration, each port serving its sends in Step-2 order (App. B.2's
+ *     switch send and receive orders). Not combined with contiguity or
+ *     greedy orders (INVALID_ARGUMENT); other kinds, and topologies where a
+ *     link would be a send port of some switched sends and a receive port
+ *     of others (a switch-to-switch link), are refused (UNSUPPORTED).
  */
 typedef struct {
   const uint8_t *allowed_link;
@@ -163,6 +173,7 @@ typedef struct {
   int32_t k;
   int32_t contiguity;
   int32_t order;
+  int32_t switch_ports;
 } taccl_sketch_desc_t;
 
 /*

@@ -27,7 +27,8 @@ class TacclError(RuntimeError):
 class SketchDesc(ct.Structure):
     _fields_ = [("allowed_link", ct.c_void_p), ("is_relay", ct.c_void_p),
                 ("max_node_crossings", ct.c_int32), ("route_mode", ct.c_int32),
-                ("k", ct.c_int32), ("contiguity", ct.c_int32), ("order", ct.c_int32)]
+                ("k", ct.c_int32), ("contiguity", ct.c_int32), ("order", ct.c_int32),
+                ("switch_ports", ct.c_int32)]
 
 
 class PlanInfo(ct.Structure):
@@ -115,7 +116,7 @@ class Plan:
     def __init__(self, V, P, row_ptr, col, alpha_ns, beta_ps_per_byte, node_of, kind,
                  chunks_per_rank, chunk_bytes, allowed=None, relay=None, max_cross=-1,
                  route_mode=KSHORTEST, k=1, owner=None, post_ptr=None, post=None, contiguity=0,
-                 order=0):
+                 order=0, switch_ports=0):
         L = lib()
         i32 = lambda a: None if a is None else np.ascontiguousarray(a, dtype=np.int32)  # noqa
         u32 = lambda a: np.ascontiguousarray(a, dtype=np.uint32)  # noqa: E731
@@ -137,7 +138,7 @@ class Plan:
                                                  int(chunk_bytes), ct.byref(coll)))
             alw, rl = u8(allowed), u8(relay)
             sk = SketchDesc(_np_ptr(alw), _np_ptr(rl), int(max_cross), int(route_mode), int(k),
-                            int(contiguity), int(order))
+                            int(contiguity), int(order), int(switch_ports))
             _check(L.taccl_sketch_apply(topo, coll, ct.byref(sk), ct.byref(plan)))
         finally:
             L.taccl_topology_destroy(topo)
@@ -159,7 +160,7 @@ class Plan:
                    w.kind, w.chunks_per_rank, w.chunk_bytes, allowed=w.allowed, relay=w.relay,
                    max_cross=w.max_cross, route_mode=w.route_mode, k=w.k, owner=w.owner,
                    post_ptr=w.post_ptr, post=w.post, contiguity=getattr(w, "contiguity", 0),
-                   order=getattr(w, "order", 0))
+                   order=getattr(w, "order", 0), switch_ports=getattr(w, "switch_ports", 0))
 
     def __del__(self):
         if getattr(self, "_h", None) and _lib is not None:

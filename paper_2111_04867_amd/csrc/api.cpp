@@ -50,7 +50,8 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
          o_arec = pk.add(p->arec), o_cpath = pk.add(p->cpath), o_cinfo = pk.add(p->cinfo),
          o_cbkt = pk.add(p->cbkt), o_topt = pk.add(p->topt), o_trec4 = pk.add(p->tree_rec4),
          o_lal = pk.add(p->lalpha), o_lbs = pk.add(p->lbs), o_lmg = pk.add(p->lmerge),
-         o_lrev = pk.add(p->lrev);
+         o_lrev = pk.add(p->lrev), o_hc2 = pk.add(p->hop_class2),
+         o_lcb2 = pk.add(p->lvl_cls2_begin), o_llc2 = pk.add(p->llc2);
   void *blk = nullptr;
   e = hipMalloc(&blk, pk.bytes.size());
   if (e != hipSuccess) return fail(TACCL_ERR_NO_MEMORY, "hipMalloc of plan tables failed");
@@ -83,6 +84,9 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
   t.lbs = (const uint64_t *)at(o_lbs);
   t.lmerge = (const uint8_t *)at(o_lmg);
   t.lrev = (const uint16_t *)at(o_lrev);
+  t.hop_class2 = (const uint16_t *)at(o_hc2);
+  t.lvl_cls2_begin = (const uint32_t *)at(o_lcb2);
+  t.llc2 = (const uint32_t *)at(o_llc2);
   t.arec = (const uint32_t *)at(o_arec);
   t.cpath = (const uint32_t *)at(o_cpath);
   t.cinfo = (const uint32_t *)at(o_cinfo);
@@ -166,6 +170,10 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     a.lalpha = t->lalpha;
     a.lbs = t->lbs;
     a.lmerge = t->lmerge;
+    a.ports = p->ports;
+    a.hop_class2 = t->hop_class2;
+    a.lvl_cls2_begin = t->lvl_cls2_begin;
+    a.llc2 = t->llc2;
     a.arec = t->arec;
     a.cpath = t->cpath;
     a.cinfo = t->cinfo;

@@ -60,6 +60,163 @@ __device__ void block_scan(uint32_t *in_out, uint32_t *cur, int n, uint32_t *wsu
   __syncthreads();
 }
 
+// LDS reads and writes of values that other threads update in the same
+// pass (relaxed workgroup atomics: plain LDS instructions, never cached)
+__device__ __forceinline__ uint32_t lds_get(uint32_t *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ void lds_put(uint32_t *p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// Switch ports, one level (App. B.3 switch constraints): a switched send
+// holds its send port (its class's link, already ordered in `sorted`) and
+// its receive port (the downlink), each port serving its sends in Step-2
+// order. The level's switched sends are ordered a second time by receive
+// port; then every send-port run is timed in order, taking as a further
+// bound the finish of the send before it on its receive port, and the
+// passes repeat until nothing changes. The update is monotone and starts
+// below the least schedule, so it stops exactly there. Returns the level's
+// latest finish (a block-uniform value is not needed: callers max-reduce);
+// updates ctime (arrivals) and lfree (port free times). Sets *fault when
+// the passes do not settle (impossible: each pass fixes at least one more
+// send).
+__device__ uint32_t ports_level(const PathArgs &a, int L, const uint32_t *gpr, uint32_t *ctime,
+                                uint32_t *lfree, const uint32_t *ccnt, const uint16_t *sorted,
+                                uint32_t *red, bool *fault) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  uint32_t *ccnt2 = (uint32_t *)(lds + a.o_ccnt2);
+  uint32_t *ccur2 = (uint32_t *)(lds + a.o_ccur2);
+  uint16_t *echunk2 = (uint16_t *)(lds + a.o_echunk2);
+  uint32_t *eprio2 = (uint32_t *)(lds + a.o_eprio2);
+  uint16_t *ecls2 = (uint16_t *)(lds + a.o_ecls2);
+  uint16_t *sorted2 = (uint16_t *)(lds + a.o_sorted2);
+  uint32_t *fcur = (uint32_t *)(lds + a.o_fcur);
+  uint16_t *pd = (uint16_t *)(lds + a.o_pd);  // send before it on its receive port
+  uint16_t *dl = (uint16_t *)(lds + a.o_dl);  // its receive port (downlink)
+  const uint8_t *rt = lds + a.o_rt;
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const int C = a.C, P = a.P, E = a.E, nlev = a.nlev;
+  const uint32_t lo = a.lvl_cls_begin[L], lo2 = a.lvl_cls2_begin[L];
+  const int ncl2 = (int)(a.lvl_cls2_begin[L + 1] - lo2);
+  for (int j = tid; j <= ncl2; j += nt) ccnt2[j] = 0;
+  for (int c = tid; c < C; c += nt) {
+    dl[c] = 0xFFFF;
+    fcur[c] = 0;
+  }
+  __syncthreads();
+  // the chunk's send at this level: route option q, first hop h
+  auto unit = [&](int c, uint32_t &q, int &h) {
+    const int pair = c / a.cpr;
+    const int s = pair / P, d = pair % P;
+    if (s == d) return false;
+    const int pp = s * P + d;
+    const int k = rt[c];
+    if (k >= a.npaths[pp]) return false;
+    q = a.pair_base[pp] + k;
+    h = a.path_lvl_hop[(size_t)q * nlev + L];
+    return h >= 0;
+  };
+  // receive-port order of the level's switched sends: count, scan, scatter,
+  // rank by (priority, chunk) inside each class
+  for (int c = tid; c < C; c += nt) {
+    uint32_t q;
+    int h;
+    if (!unit(c, q, h)) continue;
+    const uint32_t k2 = a.hop_class2[a.path_off[q] + h];
+    if (k2 != 0xFFFF) atomicAdd(&ccnt2[k2 - lo2], 1u);
+  }
+  __syncthreads();
+  block_scan(ccnt2, ccur2, ncl2, red);
+  for (int c = tid; c < C; c += nt) {
+    uint32_t q;
+    int h;
+    if (!unit(c, q, h)) continue;
+    const uint32_t k2 = a.hop_class2[a.path_off[q] + h];
+    if (k2 == 0xFFFF) continue;
+    const uint32_t slot = atomicAdd(&ccur2[k2 - lo2], 1u);
+    echunk2[slot] = (uint16_t)c;
+    ecls2[slot] = (uint16_t)(k2 - lo2);
+    eprio2[slot] = gpr[(size_t)c * a.H + h];
+  }
+  __syncthreads();
+  const uint32_t tot2 = ccnt2[ncl2];
+  for (uint32_t x = tid; x < tot2; x += nt) {
+    const int k = ecls2[x];
+    const uint32_t b = ccnt2[k], e = ccnt2[k + 1];
+    const uint32_t px = eprio2[x], cx = echunk2[x];
+    uint32_t rank = 0;
+    for (uint32_t y = b; y < e; y++) {
+      const uint32_t py = eprio2[y], cy = echunk2[y];
+      rank += (py < px) || (py == px && cy < cx);
+    }
+    sorted2[b + rank] = (uint16_t)cx;
+  }
+  __syncthreads();
+  for (int l = tid; l < E; l += nt) {
+    const uint32_t cb = a.llc2[((size_t)L * E + l) * 2], ce = a.llc2[((size_t)L * E + l) * 2 + 1];
+    if (cb == ce) continue;
+    const uint32_t xb = ccnt2[cb - lo2], xe = ccnt2[ce - lo2];
+    for (uint32_t x = xb; x < xe; x++) {
+      const int c = sorted2[x];
+      dl[c] = (uint16_t)l;
+      pd[c] = (x == xb) ? (uint16_t)0xFFFF : sorted2[x - 1];
+    }
+  }
+  __syncthreads();
+  // send-port passes until the finishes settle
+  for (int pass = 0;; pass++) {
+    bool changed = false;
+    for (int l = tid; l < E; l += nt) {
+      const uint32_t cb = a.llc[((size_t)L * E + l) * 2], ce = a.llc[((size_t)L * E + l) * 2 + 1];
+      if (cb == ce) continue;
+      const uint32_t xb = ccnt[cb - lo], xe = ccnt[ce - lo];
+      uint32_t f = lfree[l];
+      const uint32_t cl = a.cost[l];
+      for (uint32_t x = xb; x < xe; x++) {
+        const int c = sorted[x];
+        uint32_t r = max(ctime[c], f);
+        if (dl[c] != 0xFFFF)
+          r = max(r, pd[c] == 0xFFFF ? lfree[dl[c]] : lds_get(&fcur[pd[c]]));
+        f = r + cl;
+        if (f != lds_get(&fcur[c])) {
+          lds_put(&fcur[c], f);
+          changed = true;
+        }
+      }
+    }
+    if (!__syncthreads_or(changed)) break;
+    if (pass > C) {  // unreachable
+      *fault = true;
+      break;
+    }
+  }
+  // arrivals and port free times after the level
+  uint32_t mk = 0;
+  const uint32_t tot = ccnt[a.lvl_cls_begin[L + 1] - lo];
+  for (uint32_t x = tid; x < tot; x += nt) {
+    const int c = sorted[x];
+    ctime[c] = fcur[c];
+    mk = max(mk, fcur[c]);
+  }
+  // a link with classes at this level may still carry no send of this
+  // candidate: only a nonempty run moves the port's free time
+  for (int l = tid; l < E; l += nt) {
+    const uint32_t cb = a.llc[((size_t)L * E + l) * 2], ce = a.llc[((size_t)L * E + l) * 2 + 1];
+    if (cb != ce) {
+      const uint32_t xb = ccnt[cb - lo], xe = ccnt[ce - lo];
+      if (xe > xb) lfree[l] = fcur[sorted[xe - 1]];
+    }
+    const uint32_t cb2 = a.llc2[((size_t)L * E + l) * 2], ce2 = a.llc2[((size_t)L * E + l) * 2 + 1];
+    if (cb2 != ce2) {
+      const uint32_t xb = ccnt2[cb2 - lo2], xe = ccnt2[ce2 - lo2];
+      if (xe > xb) lfree[l] = fcur[sorted2[xe - 1]];
+    }
+  }
+  __syncthreads();
+  return mk;
+}
+
 __global__ __launch_bounds__(kPathThreads) void path_eval_kernel(PathArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   uint8_t *rt = lds + a.o_rt;
@@ -92,6 +249,7 @@ __global__ __launch_bounds__(kPathThreads) void path_eval_kernel(PathArgs a) {
     const bool any_unrouted = __syncthreads_or(unrouted);
 
     uint32_t mk = 0;
+    bool fault = false;
     for (int L = 0; L < nlev; L++) {
       const uint32_t lo = a.lvl_cls_begin[L];
       const int ncl = (int)(a.lvl_cls_begin[L + 1] - lo);
@@ -144,6 +302,10 @@ __global__ __launch_bounds__(kPathThreads) void path_eval_kernel(PathArgs a) {
         sorted[b + rank] = (uint16_t)cx;
       }
       __syncthreads();
+      if (a.ports) {
+        mk = max(mk, ports_level(a, L, gpr, ctime, lfree, ccnt, sorted, red, &fault));
+        continue;
+      }
       // time every link's sends of this level in order
       for (int l = tid; l < E; l += nt) {
         const uint32_t cb = a.llc[((size_t)L * E + l) * 2], ce = a.llc[((size_t)L * E + l) * 2 + 1];
@@ -190,11 +352,12 @@ __global__ __launch_bounds__(kPathThreads) void path_eval_kernel(PathArgs a) {
     mk = wave_max(mk);
     if (lane == 0) red[wave] = mk;
     __syncthreads();
+    const bool failed = __syncthreads_or(fault);
     if (tid == 0) {
       uint32_t m = 0;
       for (int w = 0; w < nt / 64; w++) m = max(m, red[w]);
-      a.makespan[i] = m;
-      a.valid[i] = (uint8_t)!any_unrouted;
+      a.makespan[i] = failed ? 0xFFFFFFFFu : m;
+      a.valid[i] = (uint8_t)(!any_unrouted && !failed);
     }
     __syncthreads();
   }
@@ -224,6 +387,18 @@ int32_t path_layout(const taccl_plan &p, PathArgs &a) {
   a.o_ecls = take(2 * M);
   a.o_sorted = take(2 * M);
   a.o_red = take(4 * (kPathThreads / 64));
+  if (p.ports) {  // receive-port order and per-chunk state
+    const int32_t K2 = std::max(p.max_lvl_cls2, 1);
+    a.o_ccnt2 = take(4 * (K2 + 1));
+    a.o_ccur2 = take(4 * K2);
+    a.o_echunk2 = take(2 * M);
+    a.o_eprio2 = take(4 * M);
+    a.o_ecls2 = take(2 * M);
+    a.o_sorted2 = take(2 * M);
+    a.o_fcur = take(4 * C);
+    a.o_pd = take(2 * C);
+    a.o_dl = take(2 * C);
+  }
   a.lds_bytes = off;
   return off;
 }

@@ -88,6 +88,11 @@ struct PathArgs {
   const uint64_t *lbs;    // beta * chunk_bytes per link
   const uint8_t *lmerge;  // 1: the link joins two nodes
   int32_t o_fmerge;
+  // switch ports (LDS-record kernel): receive-port classes and state
+  int32_t ports;
+  const uint16_t *hop_class2;
+  const uint32_t *lvl_cls2_begin, *llc2;
+  int32_t o_ccnt2, o_ccur2, o_echunk2, o_eprio2, o_ecls2, o_sorted2, o_fcur, o_pd, o_dl;
 };
 
 constexpr int kTreeMaxThreads = 512;  // up to 8 wavefronts per block

@@ -239,13 +239,35 @@ static taccl_status_t build_levels(taccl_plan *p) {
       size_t pp = (size_t)s * P + d;
       for (int32_t k = 0; k < p->npaths[pp]; k++) used_path[p->pair_base[pp] + k] = 1;
     }
-  std::set<uint64_t, std::greater<uint64_t>> rems;
+  // sends of every path: one per hop, or with switch ports one per hop pair
+  // rank -> switch -> rank (first hop j, send-port link, receive-port link,
+  // cost of the uplink)
+  struct Unit {
+    uint32_t j;
+    int32_t link, link2;
+    uint64_t cost;
+  };
+  std::vector<std::vector<Unit>> units(npath);
+  std::vector<uint64_t> ucost(npath, 0);
   for (size_t q = 0; q < npath; q++) {
     if (!used_path[q]) continue;
-    uint64_t rem = p->path_cost[q];
     for (uint32_t j = p->path_off[q]; j < p->path_off[q + 1]; j++) {
+      const int32_t l = p->path_links[j];
+      Unit x{j - p->path_off[q], l, -1, p->cost[l]};
+      if (p->ports && p->topo.col[l] >= P && j + 1 < p->path_off[q + 1]) {
+        x.link2 = p->path_links[j + 1];
+        j++;
+      }
+      units[q].push_back(x);
+      ucost[q] += x.cost;
+    }
+  }
+  std::set<uint64_t, std::greater<uint64_t>> rems;
+  for (size_t q = 0; q < npath; q++) {
+    uint64_t rem = ucost[q];
+    for (const Unit &x : units[q]) {
       rems.insert(rem);
-      rem -= p->cost[p->path_links[j]];
+      rem -= x.cost;
     }
   }
   std::vector<uint64_t> lv(rems.begin(), rems.end());  // descending
@@ -255,50 +277,75 @@ static taccl_status_t build_levels(taccl_plan *p) {
     return (int32_t)(std::lower_bound(lv.begin(), lv.end(), rem, std::greater<uint64_t>()) -
                      lv.begin());
   };
-  // classes sorted by (level, link, travelled)
-  std::set<std::tuple<int32_t, int32_t, uint64_t>> cls;
+  // classes sorted by (level, link, travelled): the send-port link; with
+  // switch ports also receive-port classes (level, downlink, travelled)
+  std::set<std::tuple<int32_t, int32_t, uint64_t>> cls, cls2;
   for (size_t q = 0; q < npath; q++) {
-    if (!used_path[q]) continue;
-    uint64_t rem = p->path_cost[q], trav = 0;
-    for (uint32_t j = p->path_off[q]; j < p->path_off[q + 1]; j++) {
-      cls.insert({level_of(rem), (int32_t)p->path_links[j], trav});
-      rem -= p->cost[p->path_links[j]];
-      trav += p->cost[p->path_links[j]];
+    uint64_t rem = ucost[q], trav = 0;
+    for (const Unit &x : units[q]) {
+      cls.insert({level_of(rem), x.link, trav});
+      if (x.link2 >= 0) cls2.insert({level_of(rem), x.link2, trav});
+      rem -= x.cost;
+      trav += x.cost;
     }
   }
-  if (cls.size() > 65535) return fail(TACCL_ERR_UNSUPPORTED, "more than 65535 send classes");
+  if (cls.size() > 65535 || cls2.size() > 65535)
+    return fail(TACCL_ERR_UNSUPPORTED, "more than 65535 send classes");
+  if (p->ports) {
+    // the kernel keeps a link's send-port and receive-port orders apart, so
+    // no link may serve as both (only a switch-to-switch link could)
+    std::vector<uint8_t> role((size_t)E, 0);
+    for (const auto &x : cls) role[std::get<1>(x)] |= 1;
+    for (const auto &x : cls2) role[std::get<1>(x)] |= 2;
+    for (int32_t l = 0; l < E; l++)
+      if (role[l] == 3)
+        return fail(TACCL_ERR_UNSUPPORTED,
+                    "switch ports: a link is both a send port and a receive port");
+  }
   std::vector<std::tuple<int32_t, int32_t, uint64_t>> cv(cls.begin(), cls.end());
+  std::vector<std::tuple<int32_t, int32_t, uint64_t>> cv2(cls2.begin(), cls2.end());
   p->ncls = (int32_t)cv.size();
   p->cls_link.resize(cv.size());
-  p->lvl_cls_begin.assign((size_t)p->nlev + 1, 0);
-  p->llc.assign((size_t)p->nlev * E * 2, 0);
-  for (size_t i = 0; i < cv.size(); i++) {
-    int32_t L = std::get<0>(cv[i]), l = std::get<1>(cv[i]);
-    p->cls_link[i] = (uint16_t)l;
-    p->lvl_cls_begin[L + 1] = (uint32_t)(i + 1);
-    uint32_t *r = &p->llc[((size_t)L * E + l) * 2];
-    if (r[0] == r[1]) r[0] = (uint32_t)i;
-    r[1] = (uint32_t)(i + 1);
-  }
-  for (int32_t L = 0; L < p->nlev; L++) {
-    p->lvl_cls_begin[L + 1] = std::max(p->lvl_cls_begin[L + 1], p->lvl_cls_begin[L]);
-    p->max_lvl_cls = std::max<int32_t>(p->max_lvl_cls,
-                                       (int32_t)(p->lvl_cls_begin[L + 1] - p->lvl_cls_begin[L]));
-  }
-  p->hop_class.assign(p->path_links.size(), 0);
+  auto class_tables = [&](const std::vector<std::tuple<int32_t, int32_t, uint64_t>> &v,
+                          std::vector<uint32_t> &begin, std::vector<uint32_t> &llc,
+                          int32_t &maxcls) {
+    begin.assign((size_t)p->nlev + 1, 0);
+    llc.assign((size_t)p->nlev * E * 2, 0);
+    for (size_t i = 0; i < v.size(); i++) {
+      int32_t L = std::get<0>(v[i]), l = std::get<1>(v[i]);
+      begin[L + 1] = (uint32_t)(i + 1);
+      uint32_t *r = &llc[((size_t)L * E + l) * 2];
+      if (r[0] == r[1]) r[0] = (uint32_t)i;
+      r[1] = (uint32_t)(i + 1);
+    }
+    maxcls = 0;
+    for (int32_t L = 0; L < p->nlev; L++) {
+      begin[L + 1] = std::max(begin[L + 1], begin[L]);
+      maxcls = std::max<int32_t>(maxcls, (int32_t)(begin[L + 1] - begin[L]));
+    }
+  };
+  for (size_t i = 0; i < cv.size(); i++) p->cls_link[i] = (uint16_t)std::get<1>(cv[i]);
+  class_tables(cv, p->lvl_cls_begin, p->llc, p->max_lvl_cls);
+  if (p->ports) class_tables(cv2, p->lvl_cls2_begin, p->llc2, p->max_lvl_cls2);
+  // per hop: its send's class (first hop of a unit; 0xFFFF for the second
+  // hop of a switched send) and receive-port class (0xFFFF if none)
+  p->hop_class.assign(p->path_links.size(), 0xFFFF);
+  p->hop_class2.assign(p->ports ? p->path_links.size() : 0, 0xFFFF);
   p->path_lvl_hop.assign(npath * (size_t)std::max(p->nlev, 1), (int8_t)-1);
   for (size_t q = 0; q < npath; q++) {
-    if (!used_path[q]) continue;
-    uint64_t rem = p->path_cost[q], trav = 0;
-    int32_t h = 0;
-    for (uint32_t j = p->path_off[q]; j < p->path_off[q + 1]; j++, h++) {
+    uint64_t rem = ucost[q], trav = 0;
+    for (const Unit &x : units[q]) {
       int32_t L = level_of(rem);
-      auto it = std::lower_bound(cv.begin(), cv.end(),
-                                 std::make_tuple(L, (int32_t)p->path_links[j], trav));
+      const uint32_t j = p->path_off[q] + x.j;
+      auto it = std::lower_bound(cv.begin(), cv.end(), std::make_tuple(L, x.link, trav));
       p->hop_class[j] = (uint16_t)(it - cv.begin());
-      p->path_lvl_hop[q * p->nlev + L] = (int8_t)h;
-      rem -= p->cost[p->path_links[j]];
-      trav += p->cost[p->path_links[j]];
+      if (x.link2 >= 0) {
+        auto it2 = std::lower_bound(cv2.begin(), cv2.end(), std::make_tuple(L, x.link2, trav));
+        p->hop_class2[j] = (uint16_t)(it2 - cv2.begin());
+      }
+      p->path_lvl_hop[q * p->nlev + L] = (int8_t)x.j;
+      rem -= x.cost;
+      trav += x.cost;
     }
   }
   // sends a level can hold: pairs with some option having a hop there
@@ -319,7 +366,7 @@ static taccl_status_t build_levels(taccl_plan *p) {
 
   // compact tables of the register-resident kernel (paths of <= 6 hops,
   // <= 8 levels, <= 2^24 route options)
-  p->path_fast = p->H <= kFastMaxHops && p->nlev <= 8 && npath < (1u << 24) &&
+  p->path_fast = !p->ports && p->H <= kFastMaxHops && p->nlev <= 8 && npath < (1u << 24) &&
                  p->coll.C <= kFastMaxChunks;
   if (p->path_fast) {
     p->arec.assign(npath * 4, 0);
@@ -607,6 +654,14 @@ taccl_status_t taccl_sketch_apply(taccl_topology_t topo, taccl_collective_t coll
     return fail(TACCL_ERR_INVALID_ARGUMENT, "contiguity must be 0 or 1");
   p->contig = sk->contiguity;
   if (sk->order < 0 || sk->order > 1) return fail(TACCL_ERR_INVALID_ARGUMENT, "order must be 0 or 1");
+  if (sk->switch_ports < 0 || sk->switch_ports > 1)
+    return fail(TACCL_ERR_INVALID_ARGUMENT, "switch_ports must be 0 or 1");
+  if (sk->switch_ports && (sk->order || sk->contiguity))
+    return fail(TACCL_ERR_INVALID_ARGUMENT,
+                "switch ports are not combined with greedy orders or contiguity");
+  if (sk->switch_ports && coll->kind != TACCL_ALLTOALL)
+    return fail(TACCL_ERR_UNSUPPORTED, "switch ports are modelled for Alltoall");
+  p->ports = sk->switch_ports;
   if (sk->order && sk->contiguity)
     return fail(TACCL_ERR_INVALID_ARGUMENT, "greedy orders are not combined with contiguity");
   p->greedy = sk->order;

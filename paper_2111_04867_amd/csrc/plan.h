@@ -55,6 +55,8 @@ struct DeviceTables {
   const uint64_t *lbs = nullptr;
   const uint8_t *lmerge = nullptr;
   const uint16_t *lrev = nullptr;
+  const uint16_t *hop_class2 = nullptr;
+  const uint32_t *lvl_cls2_begin = nullptr, *llc2 = nullptr;
   const uint16_t *hop_class = nullptr;
   const int8_t *path_lvl_hop = nullptr;
   const uint32_t *lvl_cls_begin = nullptr;
@@ -79,6 +81,7 @@ struct taccl_plan {
   // link joins two nodes (only those merge)
   int32_t contig = 0;
   int32_t greedy = 0;  // link orders from the time-aware greedy
+  int32_t ports = 0;   // Alltoall: switched sends hold a send and a receive port
   std::vector<uint32_t> lalpha;
   std::vector<uint64_t> lbs;
   std::vector<uint8_t> lmerge;
@@ -112,7 +115,11 @@ struct taccl_plan {
 
   // Alltoall (path) evaluation: levels of equal remaining cost
   int32_t nlev = 0, ncls = 0, max_lvl_cls = 0, max_lvl_sends = 0;
-  std::vector<uint16_t> hop_class;     // [path_links.size()] class of each hop
+  std::vector<uint16_t> hop_class;     // [path_links.size()] class of each hop's send
+  // switch ports: receive-port class of each switched send's first hop
+  std::vector<uint16_t> hop_class2;
+  std::vector<uint32_t> lvl_cls2_begin, llc2;
+  int32_t max_lvl_cls2 = 0;
   std::vector<int8_t> path_lvl_hop;    // [NPATH*nlev] hop at each level or -1
   std::vector<uint32_t> lvl_cls_begin; // [nlev+1]
   std::vector<uint32_t> llc;           // [nlev*E*2] class range of a link at a level

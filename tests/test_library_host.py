@@ -39,7 +39,8 @@ SMALL = [lambda: cf.uni_ring_ag(7), lambda: cf.full_a2a(5), lambda: cf.full_ag(5
 
 
 @pytest.mark.parametrize("make", [lambda n=n: cf.named(n)
-                                  for n in cf.ORDER + cf.CONTIG_ORDER + cf.REDUCE_ORDER] + SMALL)
+                                  for n in cf.ORDER + cf.CONTIG_ORDER + cf.REDUCE_ORDER
+                                  + cf.PORTS_ORDER] + SMALL)
 def test_plan_tables_equal_oracle(make):
     w = make()
     plan = B.Plan.from_workload(w)
@@ -77,6 +78,27 @@ def test_reduction_needs_reverse_links():
     with pytest.raises(B.TacclError) as e:
         B.Plan.from_workload(w)
     assert e.value.status == B.ERR_INVALID_ARGUMENT
+
+
+def test_switch_ports_limits():
+    """Switch ports apply to Alltoall only; a switch-to-switch link would be
+    a send port of some switched sends and a receive port of others, which
+    the oracle times and the kernel does not: the library refuses it."""
+    w = cf.with_switch_ports(cf.cubemesh8_ag(n_candidates=1))
+    with pytest.raises(B.TacclError) as e:
+        B.Plan.from_workload(w)
+    assert e.value.status == B.ERR_UNSUPPORTED
+    edges = (cf.switch_edges(range(2), 4, 700, 8) + cf.switch_edges(range(2, 4), 5, 700, 8)
+             + [(4, 5, 1000, 10), (5, 4, 1000, 10)])
+    row_ptr, col, a, b = cf.csr_from_edges(6, edges)
+    w = cf.Workload("twoswitch_linked", 6, 4, row_ptr, col, a, b, None, cf.ALLTOALL, 1, 65536,
+                    cf.KSHORTEST, k=1, switch_ports=1)
+    ref = OraclePlan.from_workload(w)
+    assert ref.max_hops == 3
+    with pytest.raises(B.TacclError) as e:
+        B.Plan.from_workload(w)
+    assert e.value.status == B.ERR_UNSUPPORTED
+    assert "send port and a receive port" in str(e.value)
 
 
 # ----------------------------------------------------------------------------
