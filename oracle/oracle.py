@@ -53,6 +53,8 @@ def _load():
     lib.orc_set_contiguity.argtypes = [P, ct.c_int]
     lib.orc_eval.restype = ct.c_int
     lib.orc_eval.argtypes = [P, ct.c_int64, P, P, P, P]
+    lib.orc_connections.restype = ct.c_int
+    lib.orc_connections.argtypes = [P, ct.c_int64, P, P]
     lib.orc_eval_detail.restype = ct.c_int
     lib.orc_eval_detail.argtypes = [P, P, P, ct.c_int, P] + [P] * 13
     _lib = lib
@@ -199,6 +201,16 @@ class OraclePlan:
             parts = list(ex.map(lambda ab: self.eval(routes[ab[0]:ab[1]], prio[ab[0]:ab[1]]),
                                 zip(bounds[:-1], bounds[1:])))
         return np.concatenate([p[0] for p in parts]), np.concatenate([p[1] for p in parts])
+
+    def connections(self, routes):
+        """Per candidate, the ordered rank pairs that exchange a chunk through
+        switch vertices only (the uc-max / uc-min count)."""
+        routes = np.ascontiguousarray(routes, dtype=np.uint8).reshape(-1, self.route_stride)
+        out = np.zeros(routes.shape[0], dtype=np.uint32)
+        rc = _load().orc_connections(self._h, routes.shape[0], _ptr(routes), _ptr(out))
+        if rc != 0:
+            raise OracleError(f"orc_connections failed ({rc})")
+        return out
 
     def eval_detail(self, routes, prio):
         """One candidate; returns (makespan, valid, sends) where sends is a

@@ -56,6 +56,11 @@
  * v up to v). Allreduce is ReduceScatter then Allgather on the same trees,
  * timed back to back, with a separate priority row for each phase.
  *
+ * Connections (orc_connections): per candidate, the number of ordered rank
+ * pairs that exchange a chunk through switch vertices only, the is_util
+ * count that the uc-max / uc-min switch-hyperedge policies weigh in the
+ * objective (Sec. 5.1, App. B.3).
+ *
  * Paths: the sketch of Sec. 3.1 restricts links; routes are limited to
  * shortest paths in the logical topology (Sec. 5.1, Step 1). Paths are found
  * here by exhaustive depth-first search with cost pruning and sorted by
@@ -1150,6 +1155,74 @@ static int eval_one(const orc_plan *p, const uint8_t *rt, const uint32_t *pr, os
   if ((uint64_t)m1 + m2 >= (1ull << 32)) return ORC_ELIMIT;
   *makespan = m1 + m2;
   *valid = (uint8_t)(v1 && v2);
+  return ORC_OK;
+}
+
+/* Switch-hyperedge connections: the count that the uc-max and uc-min
+ * policies (Sec. 5.1, switch-hyperedge policy; App. B.3, is_util with the
+ * objective time + gamma * sum of is_util) weigh. A connection is an ordered
+ * rank pair (a, b) that carries some chunk through switch vertices only.
+ * Alltoall: along each routed path, two ranks with only switch vertices
+ * between them. Multicast: a rank b whose tree parent is a switch, paired
+ * with the nearest rank above it in the tree. ReduceScatter runs the trees
+ * backwards, so each pair is (b, a); Allreduce has both directions. The
+ * count does not depend on priorities. */
+static uint32_t connections_one(const orc_plan *p, const uint8_t *rt, oscratch *w,
+                                const uint32_t *zero_prio, uint8_t *mark) {
+  const int P = p->P, V = p->V;
+  memset(mark, 0, (size_t)P * P);
+  if (p->kind == ORC_ALLTOALL) {
+    for (int c = 0; c < p->C; c++) {
+      int s0 = p->owner[c], d = p->post[p->post_ptr[c]];
+      if (s0 == d) continue;
+      const oplist *L = &p->paths[s0 * P + d];
+      int ch = rt[c];
+      if (ch >= L->n) continue;
+      const opath *q = &L->p[ch];
+      int last = 0; /* index of the latest rank on the path */
+      for (int j = 1; j <= q->hops; j++) {
+        int v = q->vert[j];
+        if (v >= P) continue;
+        if (j - last > 1) mark[q->vert[last] * P + v] = 1;
+        last = j;
+      }
+    }
+  } else {
+    w->n = 0;
+    build_tree_sends(p, rt, zero_prio, w);
+    for (int c = 0; c < p->C; c++) {
+      const int *par = &w->tree_parent[(size_t)c * V];
+      for (int b = 0; b < P; b++) {
+        if (par[b] < 0) continue;
+        int x = p->lsrc[par[b]];
+        if (x < P) continue;
+        while (x >= P) x = p->lsrc[par[x]]; /* the owner is a rank */
+        if (p->kind != ORC_REDUCESCATTER) mark[x * P + b] = 1;
+        if (p->kind == ORC_REDUCESCATTER || p->kind == ORC_ALLREDUCE) mark[b * P + x] = 1;
+      }
+    }
+  }
+  uint32_t n = 0;
+  for (int i = 0; i < P * P; i++) n += mark[i];
+  return n;
+}
+
+int orc_connections(const orc_plan *p, int64_t n, const uint8_t *routes, uint32_t *out) {
+  oscratch w;
+  scratch_init(p, &w);
+  uint32_t *zero = (uint32_t *)calloc((size_t)p->C * p->V + 1, sizeof(uint32_t));
+  uint8_t *mark = (uint8_t *)malloc((size_t)p->P * p->P);
+  if (!zero || !mark) {
+    free(zero);
+    free(mark);
+    scratch_free(&w);
+    return ORC_ENOMEM;
+  }
+  for (int64_t i = 0; i < n; i++)
+    out[i] = connections_one(p, routes + (size_t)i * p->route_stride, &w, zero, mark);
+  free(zero);
+  free(mark);
+  scratch_free(&w);
   return ORC_OK;
 }
 
