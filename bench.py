@@ -85,6 +85,22 @@ def time_launches(plan, d_r, d_p, d_m, d_v, steps, warmup):
     return per, wall
 
 
+def time_calls(fn, steps, warmup):
+    """Per-call durations (ms) of fn() from HIP events on torch's current stream."""
+    import torch
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev[0].record(stream)
+    for k in range(steps):
+        fn()
+        ev[k + 1].record(stream)
+    torch.cuda.synchronize()
+    return np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(steps)])
+
+
 def setup(name):
     import torch
     from paper_2111_04867_amd.binding import Plan
@@ -201,6 +217,19 @@ def main():
             log(f"[bench] {name}: {table[name]['candidates_per_s']:.3e} cand/s, "
                 f"{gbs:.1f} GB/s ({100 * gbs / HBM_PEAK_GBS:.2f}% of HBM)")
         rec["all_workloads"] = table
+        # switch-hyperedge connection counts (the uc-max / uc-min term)
+        conn = {}
+        for name in ("switch16_a2a", "fournode64_a2a"):
+            wl, pl, _, _, b2 = setup(name)
+            d_c = torch.empty(wl.n_candidates, dtype=torch.int32, device="cuda")
+            pr_ = time_calls(lambda: pl.connections_tensors(b2[0], d_c),
+                             max(10, args.steps // 2), args.warmup)
+            a_s = pr_.mean() / 1e3
+            conn[name] = {"candidates": wl.n_candidates, "ms_per_launch": pr_.mean(),
+                          "candidates_per_s": wl.n_candidates / a_s}
+            log(f"[bench] {name} connections: {conn[name]['candidates_per_s']:.3e} cand/s")
+            del b2
+        rec["connections"] = conn
     if not args.no_cpu:
         rec["cpu_baseline"] = cpu_baseline(w, routes, prio, args.cpu_seconds)
     print(json.dumps(rec), flush=True)

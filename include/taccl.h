@@ -249,6 +249,33 @@ taccl_status_t taccl_eval_batch(taccl_plan_t plan, int64_t n, const uint8_t *d_r
                                 const uint32_t *d_prio, uint32_t *d_makespan, uint8_t *d_valid,
                                 taccl_stream_t stream);
 
+/*
+ * Switch-hyperedge connections of n candidates on the current device,
+ * asynchronously on `stream` (Sec. 3.2; Sec. 5.1, switch-hyperedge policy;
+ * App. B.3: is_util[src, r] = 1 when some chunk goes from GPU src to GPU r
+ * over switched links, and the uc-max / uc-min policies minimise
+ * time + gamma * sum(is_util) with gamma < 0 for uc-max and gamma > 0 for
+ * uc-min).
+ *   d_routes: device, n*route_stride bytes, laid out as for taccl_eval_batch
+ *     (priorities play no part in the count);
+ *   d_connections: device, n uint32, 4-byte aligned: the number of ordered
+ *     rank pairs (a, b) that exchange a chunk through switch vertices only.
+ *     Alltoall: two ranks of a chunk's routed path with only switch
+ *     vertices between them. Multicast (Allgather, explicit): a rank whose
+ *     tree parent is a switch vertex, paired with the nearest rank above it
+ *     in the chunk's tree (first-reach merge of its routed paths,
+ *     destinations ascending); ReduceScatter reverses every pair and
+ *     Allreduce counts both directions. 0 on topologies without switch
+ *     vertices. Unrouted pairs contribute nothing.
+ * A caller ranks candidates under a policy by makespan + gamma * count.
+ * Errors (synchronous): INVALID_ARGUMENT for null pointers with n > 0,
+ * n < 0 or a misaligned d_connections; UNSUPPORTED for more than 256 ranks
+ * (multicast: more than 64 ranks or 255 vertices); HIP if the plan upload or
+ * the launch fails. n == 0 is a no-op.
+ */
+taccl_status_t taccl_connections_batch(taccl_plan_t plan, int64_t n, const uint8_t *d_routes,
+                                       uint32_t *d_connections, taccl_stream_t stream);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char *taccl_last_error(void);
 

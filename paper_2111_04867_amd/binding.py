@@ -46,7 +46,7 @@ EXPORTS = ["taccl_topology_create", "taccl_topology_destroy", "taccl_collective_
            "taccl_collective_create_explicit", "taccl_collective_destroy", "taccl_sketch_apply",
            "taccl_plan_destroy", "taccl_plan_info", "taccl_plan_route_options",
            "taccl_plan_path", "taccl_plan_link_costs", "taccl_plan_upload", "taccl_eval_batch",
-           "taccl_last_error", "taccl_version"]
+           "taccl_connections_batch", "taccl_last_error", "taccl_version"]
 
 _lib = None
 
@@ -91,6 +91,8 @@ def lib():
     L.taccl_plan_upload.argtypes = [P]
     L.taccl_eval_batch.restype = st
     L.taccl_eval_batch.argtypes = [P, ct.c_int64, P, P, P, P, P]
+    L.taccl_connections_batch.restype = st
+    L.taccl_connections_batch.argtypes = [P, ct.c_int64, P, P, P]
     L.taccl_last_error.restype = ct.c_char_p
     L.taccl_last_error.argtypes = []
     L.taccl_version.restype = ct.c_int32
@@ -240,3 +242,35 @@ class Plan:
         self.eval_tensors(d_r, d_p, d_m, d_v)
         torch.cuda.synchronize()
         return d_m[:n].cpu().numpy().view(np.uint32), d_v[:n].cpu().numpy()
+
+    # ---- switch-hyperedge connections --------------------------------------
+    def connections_batch(self, n, d_routes, d_connections, stream=0):
+        """Raw call: device pointers (ints) and a hipStream_t handle (int)."""
+        _check(lib().taccl_connections_batch(self._h, int(n), ct.c_void_p(int(d_routes)),
+                                             ct.c_void_p(int(d_connections)),
+                                             ct.c_void_p(int(stream))))
+
+    def connections_tensors(self, routes, out, stream=None):
+        """torch CUDA tensors: routes uint8 [n, route_stride], out int32/uint32
+        [n]. Runs on `stream` (default: torch's current stream)."""
+        import torch
+        n = routes.shape[0]
+        if not routes.is_cuda or not routes.is_contiguous() or routes.dim() != 2 or \
+                routes.shape[1] != self.route_stride or routes.element_size() != 1:
+            raise ValueError(f"routes must be a contiguous CUDA uint8 tensor [n, "
+                             f"{self.route_stride}]")
+        if out.numel() < n or out.element_size() != 4:
+            raise ValueError("out must hold n 32-bit counts")
+        s = (stream if stream is not None else torch.cuda.current_stream()).cuda_stream
+        self.connections_batch(n, routes.data_ptr(), out.data_ptr(), s)
+
+    def connections(self, routes, device="cuda"):
+        """Convenience: host numpy routes in, host numpy counts out."""
+        import torch
+        routes = np.ascontiguousarray(routes, dtype=np.uint8).reshape(-1, self.route_stride)
+        n = routes.shape[0]
+        d_r = torch.from_numpy(routes).to(device)
+        d_c = torch.empty(max(n, 1), dtype=torch.int32, device=device)
+        self.connections_tensors(d_r, d_c)
+        torch.cuda.synchronize()
+        return d_c[:n].cpu().numpy().view(np.uint32)

@@ -291,4 +291,53 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
   return TACCL_OK;
 }
 
+taccl_status_t taccl_connections_batch(taccl_plan_t p, int64_t n, const uint8_t *d_routes,
+                                       uint32_t *d_connections, taccl_stream_t stream) {
+  if (!p) return fail(TACCL_ERR_INVALID_ARGUMENT, "null plan");
+  if (n < 0) return fail(TACCL_ERR_INVALID_ARGUMENT, "negative candidate count");
+  if (n == 0) return TACCL_OK;
+  if (!d_routes || !d_connections) return fail(TACCL_ERR_INVALID_ARGUMENT, "null device pointer");
+  if ((uintptr_t)d_connections & 3)
+    return fail(TACCL_ERR_INVALID_ARGUMENT, "d_connections must be 4-byte aligned");
+  const int32_t P = p->topo.P, V = p->topo.V;
+  const bool tree = p->coll.kind != TACCL_ALLTOALL;
+  if (P > 256 || (tree && (P > 64 || V > 255)))
+    return fail(TACCL_ERR_UNSUPPORTED, "connection counts need at most 256 ranks (multicast: "
+                                       "64 ranks and 255 vertices)");
+  DeviceTables *t = nullptr;
+  taccl_status_t st = ensure_device(p, &t);
+  if (st) return st;
+  ConnArgs a{};
+  a.C = p->coll.C;
+  a.P = P;
+  a.V = V;
+  a.cpr = std::max(p->coll.cpr, 1);
+  a.kind = p->coll.kind;
+  a.tree = tree ? 1 : 0;
+  a.mask_words = (P * P + 31) / 32;
+  a.route_stride = p->route_stride;
+  a.ldst = t->ldst;
+  a.pair_base = t->pair_base;
+  a.npaths = t->npaths;
+  a.path_off = t->path_off;
+  a.path_links = t->path_links;
+  a.owner = t->owner;
+  a.post_mask = t->post_mask;
+  a.routes = d_routes;
+  a.out = d_connections;
+  a.n = n;
+  // one chunk per thread at a time; multicast blocks keep a parent byte per
+  // vertex and thread in LDS
+  int threads = std::min(kConnMaxThreads, std::max(64, (a.C + 63) / 64 * 64));
+  while (threads > 64 && connections_lds_bytes(a, threads) > t->max_lds) threads -= 64;
+  if (connections_lds_bytes(a, threads) > t->max_lds)
+    return fail(TACCL_ERR_UNSUPPORTED, "connection count needs more LDS than a block has");
+  const int per_cu = std::max(1, std::min(t->lds_per_cu / std::max(connections_lds_bytes(a, threads), 1),
+                                          2048 / threads));
+  const int grid = (int)std::min<int64_t>(n, (int64_t)std::max(t->num_cus, 1) * per_cu);
+  hipError_t e = launch_connections(a, threads, grid, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "kernel launch");
+  return TACCL_OK;
+}
+
 }  // extern "C"

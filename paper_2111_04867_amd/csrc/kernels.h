@@ -95,6 +95,24 @@ struct PathArgs {
   int32_t o_ccnt2, o_ccur2, o_echunk2, o_eprio2, o_ecls2, o_sorted2, o_fcur, o_pd, o_dl;
 };
 
+// Switch-hyperedge connection count: one block per candidate at a time.
+struct ConnArgs {
+  int32_t C, P, V, cpr, kind, tree, mask_words;  // mask_words: ceil(P*P / 32)
+  int32_t route_stride;
+  const uint16_t *ldst;
+  const uint32_t *pair_base;
+  const uint8_t *npaths;
+  const uint32_t *path_off;
+  const uint16_t *path_links;
+  const int32_t *owner;
+  const uint64_t *post_mask;
+  const uint8_t *routes;
+  uint32_t *out;
+  int64_t n;
+};
+
+constexpr int kConnMaxThreads = 256;
+
 constexpr int kTreeMaxThreads = 512;  // up to 8 wavefronts per block
 constexpr int kTreeRecLdsMax = 32768;  // route records kept in LDS up to this size
 constexpr int kPathThreads = 256;
@@ -118,6 +136,9 @@ int path_fast_threads(const taccl_plan &p);  // threads per block: 256, 512 or 1
 int path_fast_blocks_per_cu(const PathArgs &a, int cpt, int nt);
 
 hipError_t launch_tree(const TreeArgs &a, int grid, hipStream_t stream);
+// connection count: LDS bytes of a block of `threads`, and the launch
+int32_t connections_lds_bytes(const ConnArgs &a, int threads);
+hipError_t launch_connections(const ConnArgs &a, int threads, int grid, hipStream_t stream);
 hipError_t launch_tree_layers(const TreeArgs &a, int grid, hipStream_t stream);
 // resident blocks per CU of the layered kernel at a.waves_per_block
 int tree_layers_blocks_per_cu(const TreeArgs &a);

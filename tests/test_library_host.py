@@ -181,3 +181,17 @@ def test_plan_path_errors():
         plan.path(0, 1, 5)
     with pytest.raises(B.TacclError):
         plan.path(0, 9, 0)
+
+
+def test_connections_argument_checks():
+    """taccl_connections_batch rejects bad arguments before touching a device."""
+    L = B.lib()
+    plan = B.Plan.from_workload(cf.switch16_a2a(n_candidates=1))
+    buf = ct.c_void_p(64)  # never dereferenced: every call below fails its checks first
+    assert L.taccl_connections_batch(None, 1, buf, buf, None) == B.ERR_INVALID_ARGUMENT
+    assert L.taccl_connections_batch(plan._h, -1, buf, buf, None) == B.ERR_INVALID_ARGUMENT
+    assert L.taccl_connections_batch(plan._h, 1, None, buf, None) == B.ERR_INVALID_ARGUMENT
+    assert L.taccl_connections_batch(plan._h, 1, buf, None, None) == B.ERR_INVALID_ARGUMENT
+    assert L.taccl_connections_batch(plan._h, 1, buf, ct.c_void_p(66), None) == \
+        B.ERR_INVALID_ARGUMENT
+    assert L.taccl_connections_batch(plan._h, 0, None, None, None) == B.OK
