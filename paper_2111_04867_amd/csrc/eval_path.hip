@@ -440,6 +440,64 @@ __device__ __forceinline__ uint64_t shfl_up64(uint64_t v, int o) {
   return ((uint64_t)hi << 32) | lo;
 }
 
+// Cross-lane moves through DPP (a VALU operand modifier, so no trip
+// through the LDS crossbar as with ds_bpermute): row_shr:n reads lane i - n
+// of the same 16-lane row, row_bcast:15 / :31 read lane 15 / 31 into the
+// next row(s) selected by the row mask, wave_shr:1 reads lane i - 1. Lanes
+// without a source (and rows outside the mask) read 0, the identity of the
+// unsigned add and max used here.
+template <int Ctrl, int RowMask = 0xf>
+__device__ __forceinline__ uint32_t dpp(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, Ctrl, RowMask, 0xf, false);
+}
+template <int Ctrl, int RowMask = 0xf>
+__device__ __forceinline__ uint64_t dpp64(uint64_t v) {
+  const uint32_t lo = dpp<Ctrl, RowMask>((uint32_t)v), hi = dpp<Ctrl, RowMask>((uint32_t)(v >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+constexpr int kRowShr = 0x110, kBcast15 = 0x142, kBcast31 = 0x143, kWaveShr1 = 0x138;
+
+// inclusive scans over the 64 lanes of a wavefront (Hillis-Steele inside
+// each row, then the row broadcasts)
+__device__ __forceinline__ uint32_t wave_scan_add(uint32_t v) {
+  v += dpp<kRowShr + 1>(v);
+  v += dpp<kRowShr + 2>(v);
+  v += dpp<kRowShr + 4>(v);
+  v += dpp<kRowShr + 8>(v);
+  v += dpp<kBcast15, 0xa>(v);
+  v += dpp<kBcast31, 0xc>(v);
+  return v;
+}
+__device__ __forceinline__ uint64_t wave_scan_max64(uint64_t v) {
+  v = max(v, dpp64<kRowShr + 1>(v));
+  v = max(v, dpp64<kRowShr + 2>(v));
+  v = max(v, dpp64<kRowShr + 4>(v));
+  v = max(v, dpp64<kRowShr + 8>(v));
+  v = max(v, dpp64<kBcast15, 0xa>(v));
+  v = max(v, dpp64<kBcast31, 0xc>(v));
+  return v;
+}
+// inclusive scans over lanes 0..15 only (the other rows hold garbage)
+__device__ __forceinline__ uint32_t row_scan_add(uint32_t v) {
+  v += dpp<kRowShr + 1>(v);
+  v += dpp<kRowShr + 2>(v);
+  v += dpp<kRowShr + 4>(v);
+  v += dpp<kRowShr + 8>(v);
+  return v;
+}
+__device__ __forceinline__ uint64_t row_scan_max64(uint64_t v) {
+  v = max(v, dpp64<kRowShr + 1>(v));
+  v = max(v, dpp64<kRowShr + 2>(v));
+  v = max(v, dpp64<kRowShr + 4>(v));
+  v = max(v, dpp64<kRowShr + 8>(v));
+  return v;
+}
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, uint32_t lane) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), lane);
+  return ((uint64_t)hi << 32) | lo;
+}
+
 // exclusive scan of cnt[0..n) in place, cnt[n] = total (all threads call)
 __device__ void block_excl_scan(uint32_t *cnt, int n, uint32_t *wsum) {
   const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63, wave = tid >> 6;
@@ -447,15 +505,14 @@ __device__ void block_excl_scan(uint32_t *cnt, int n, uint32_t *wsum) {
   const int b = min(tid * per, n), e = min(b + per, n);
   uint32_t sum = 0;
   for (int j = b; j < e; j++) sum += cnt[j];
-  uint32_t incl = sum;
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint32_t t = (uint32_t)__shfl_up((int)incl, o);
-    if (lane >= o) incl += t;
-  }
+  const uint32_t incl = wave_scan_add(sum);
   if (lane == 63) wsum[wave] = incl;
   __syncthreads();
-  uint32_t off = 0;
-  for (int w = 0; w < wave; w++) off += wsum[w];
+  // offset of this wave: every wave scans the (at most 16) wave totals
+  // itself instead of summing them one by one
+  const uint32_t ws = row_scan_add(lane < (nt >> 6) ? wsum[lane] : 0u);
+  const uint32_t w = (uint32_t)__builtin_amdgcn_readfirstlane(wave);
+  const uint32_t off = w ? (uint32_t)__builtin_amdgcn_readlane((int)ws, w - 1) : 0u;
   uint32_t run = off + incl - sum;
   for (int j = b; j < e; j++) {
     const uint32_t x = cnt[j];
@@ -479,8 +536,8 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
   uint32_t *ctime = (uint32_t *)(lds + a.o_fctime);  // a chunk's arrival so far
   uint32_t *lfree = (uint32_t *)(lds + a.o_flfree);  // [2][E]: busy time, next
   uint32_t *bcnt = (uint32_t *)(lds + a.o_fbcnt);    // bucket counts, then starts
-  uint32_t *epr = (uint32_t *)(lds + a.o_fepr);
-  uint16_t *ech = (uint16_t *)(lds + a.o_fech);
+  // bucket entries: priority << 32 | chunk (ascending = Step-2 tie order)
+  uint64_t *e64 = (uint64_t *)(lds + a.o_fepr);
   // sorted sends, chunk | link << cb | index in its link run << (cb + lb),
   // stored transposed: position t*ept + q of thread t's range at q*NT + t
   uint32_t *pinfo = (uint32_t *)(lds + a.o_fsrt);
@@ -488,7 +545,6 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
   const uint32_t cmask = (1u << cb) - 1, lmask = (1u << lb) - 1;
   uint32_t *red = (uint32_t *)(lds + a.o_fred);      // [2][NT/64] scan scratch
   uint64_t *red64 = (uint64_t *)(lds + a.o_fred64);  // [NT/64] segmented max
-  uint32_t *redf = (uint32_t *)(lds + a.o_fredf);    // [NT/64] segment-head flags
   uint8_t *s_merge = lds + a.o_fmerge;  // links that carry contiguous transfers
   for (int j = tid; j < E; j += NT) {
     s_cost[j] = a.cost[j];
@@ -561,7 +617,10 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
           hmap[j] = (hmap[j] & ~(7u << (3 * lv))) | ((uint32_t)t << (3 * lv));
         }
     }
-    for (int l = tid; l < E; l += NT) lfree[l] = 0;
+    for (int l = tid; l < E; l += NT) {
+      lfree[l] = 0;
+      lfree[E + l] = kUnset;
+    }
     const bool any_unrouted = __syncthreads_or(unrouted);
 
     uint32_t mk = 0;
@@ -572,15 +631,24 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       const uint32_t lastb = s_cbkt[lo + ncl - 1];
       const int NB = ncl ? (int)((lastb & 0xFFFFFF) + (1u << (lastb >> 24))) : 0;
       for (int j = tid; j <= NB; j += NT) bcnt[j] = 0;
-      for (int l = tid; l < E; l += NT) lfree[E + l] = kUnset;
+      // busy times after the previous level (a link without a send there
+      // keeps its time)
+      for (int l = tid; l < E; l += NT) {
+        const uint32_t nx = lfree[E + l];
+        if (nx != kUnset) lfree[l] = nx;
+        lfree[E + l] = kUnset;
+      }
       __syncthreads();
 
       // ---- A. the level's sends per bucket ---------------------------------
-      int bk[CPT];
-      uint32_t slot[CPT], pl[CPT], loc[CPT];
+      // wa: bucket | first bucket of the send's link run << 16 (kUnset: no
+      // send at this level); wb: index in the bucket | link << 16
+      uint32_t wa[CPT], wb[CPT], pl[CPT];
 #pragma unroll
       for (int j = 0; j < CPT; j++) {
-        bk[j] = -1;
+        wa[j] = kUnset;
+        wb[j] = 0;
+        pl[j] = 0;
         const int h = (int)((hmap[j] >> (3 * L)) & 7);  // 7: no hop at this level
         if (h < kFastMaxHops) {
           uint32_t cw = rcl[j][0], pv = pr[j][0];
@@ -590,12 +658,13 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
           if (h >= 2) cw = rcl[j][1];
           if (h >= 4) cw = rcl[j][2];
           const uint32_t cls = (h & 1) ? (cw >> 16) : (cw & 0xFFFF);
-          const uint32_t cbk = s_cbkt[cls];
+          const uint32_t cbk = s_cbkt[cls], ci = s_cinfo[cls];
+          const uint32_t fb = s_cbkt[lo + (ci >> 16)] & 0xFFFFFF;
           const uint32_t bits = cbk >> 24;
-          loc[j] = cls - lo;
+          const uint32_t b = (cbk & 0xFFFFFF) + (bits ? (pv >> (32 - bits)) : 0u);
           pl[j] = pv;
-          bk[j] = (int)((cbk & 0xFFFFFF) + (bits ? (pv >> (32 - bits)) : 0u));
-          slot[j] = atomicAdd(&bcnt[bk[j]], 1u);
+          wa[j] = b | (fb << 16);
+          wb[j] = atomicAdd(&bcnt[b], 1u) | ((ci & 0xFFFFu) << 16);
         }
       }
       __syncthreads();
@@ -608,93 +677,91 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       // ---- C. scatter --------------------------------------------------------
 #pragma unroll
       for (int j = 0; j < CPT; j++)
-        if (bk[j] >= 0) {
-          const uint32_t pos = bcnt[bk[j]] + slot[j];
-          epr[pos] = pl[j];
-          ech[pos] = (uint16_t)(tid + NT * j);
+        if (wa[j] != kUnset) {
+          const uint32_t pos = bcnt[wa[j] & 0xFFFFu] + (wb[j] & 0xFFFFu);
+          e64[pos] = ((uint64_t)pl[j] << 32) | (uint32_t)(tid + NT * j);
         }
       __syncthreads();
       // ---- D. order inside buckets by (priority, chunk); record each send's
       //      link and its index in the link's run -----------------------------
+      {
+        uint32_t b0[CPT], nb[CPT], rs[CPT], rank[CPT];
+        uint64_t me[CPT];
+        uint32_t nmax = 0;
 #pragma unroll
-      for (int j = 0; j < CPT; j++)
-        if (bk[j] >= 0) {
-          const uint32_t b0 = bcnt[bk[j]], b1 = bcnt[bk[j] + 1];
-          const uint32_t c = tid + NT * j, px = pl[j];
-          uint32_t rank = 0;
-          for (uint32_t y = b0; y < b1; y++) {
-            const uint32_t py = epr[y], cy = ech[y];
-            rank += (py < px) || (py == px && cy < c);
+        for (int j = 0; j < CPT; j++) {
+          b0[j] = nb[j] = rs[j] = rank[j] = 0;
+          me[j] = ((uint64_t)pl[j] << 32) | (uint32_t)(tid + NT * j);
+          if (wa[j] != kUnset) {
+            const uint32_t b = wa[j] & 0xFFFFu;
+            b0[j] = bcnt[b];
+            nb[j] = bcnt[b + 1] - b0[j];
+            rs[j] = bcnt[wa[j] >> 16];
           }
-          const uint32_t ci = s_cinfo[lo + loc[j]];
-          const uint32_t start = bcnt[s_cbkt[lo + (ci >> 16)] & 0xFFFFFF];
-          const uint32_t pos = b0 + rank;
-          const uint32_t t = (uint32_t)(((uint64_t)pos * em) >> 32), q = pos - t * ept;
-          pinfo[q * NT + t] = c | ((ci & 0xFFFFu) << cb) | ((pos - start) << kb);
+          nmax = max(nmax, nb[j]);
         }
+        // the members of all this thread's buckets are read together, one
+        // from each bucket per step (entry 0 stands in for a finished bucket)
+        for (uint32_t t = 0; t < nmax; t++) {
+          uint64_t e[CPT];
+#pragma unroll
+          for (int j = 0; j < CPT; j++) e[j] = e64[t < nb[j] ? b0[j] + t : 0u];
+#pragma unroll
+          for (int j = 0; j < CPT; j++) rank[j] += (uint32_t)((t < nb[j]) & (e[j] < me[j]));
+        }
+#pragma unroll
+        for (int j = 0; j < CPT; j++)
+          if (wa[j] != kUnset) {
+            const uint32_t pos = b0[j] + rank[j];
+            const uint32_t t = (uint32_t)(((uint64_t)pos * em) >> 32), q = pos - t * ept;
+            pinfo[q * NT + t] = (uint32_t)(tid + NT * j) | ((wb[j] >> 16) << cb) |
+                                ((pos - rs[j]) << kb);
+          }
+      }
       __syncthreads();
-      // ---- E. finish times of every link run (segmented prefix max) ---------
-      // thread tid owns sorted positions [tid*ept, tid*ept + ept); every load
-      // is issued unmasked (stale entries are clamped to in-range indexes and
-      // never used)
+      // ---- E. finish times of every link run --------------------------------
+      // The k-th send of a link run with cost c, ready times r_j and busy
+      // time F finishes at (k+1)c + max(F, max_{j<=k}(r_j - j c)). Runs lie
+      // in ascending link order along the sorted positions (classes are
+      // ordered by link), so one plain prefix max over
+      // link << 33 | (r_j - j c + 2^32) yields, at every position, the max
+      // over the earlier sends of its own run. Thread tid owns sorted
+      // positions [tid*ept, tid*ept + ept); every load is issued unmasked
+      // (stale entries are clamped to in-range indexes and never used).
       const uint32_t x0 = (uint32_t)tid * ept;
-      uint32_t pis[CPT], ct[CPT], cs[CPT];
+      uint32_t pis[CPT], ct[CPT], cs[CPT], lf[CPT];
 #pragma unroll
       for (int q = 0; q < CPT; q++) pis[q] = pinfo[q * NT + tid];
 #pragma unroll
       for (int q = 0; q < CPT; q++) {
+        const uint32_t l = min((pis[q] >> cb) & lmask, (uint32_t)E - 1);
         ct[q] = ctime[min(pis[q] & cmask, (uint32_t)C - 1)];
-        cs[q] = s_cost[min((pis[q] >> cb) & lmask, (uint32_t)E - 1)];
+        cs[q] = s_cost[l];
+        lf[q] = lfree[l];
       }
-      // E1: this thread's tail aggregate
+      uint64_t comp[CPT];
       uint64_t agg = 0;
-      bool seen_head = false;
 #pragma unroll
       for (int q = 0; q < CPT; q++) {
+        comp[q] = 0;
         if ((uint32_t)q < ept && x0 + q < tot) {
-          const uint32_t k = pis[q] >> kb;
-          const uint64_t g = (uint64_t)ct[q] + kBias - (uint64_t)k * cs[q];
-          if (k == 0) {
-            agg = g;
-            seen_head = true;
-          } else {
-            agg = max(agg, g);
-          }
+          const uint32_t k = pis[q] >> kb, l = (pis[q] >> cb) & lmask;
+          comp[q] = ((uint64_t)l << 33) | ((uint64_t)ct[q] + kBias - (uint64_t)k * cs[q]);
+          agg = max(agg, comp[q]);
         }
       }
-      // E2: exclusive segmented-max scan across threads
-      uint64_t v = agg;
-      bool hf = seen_head;
-      for (int o = 1; o < 64; o <<= 1) {
-        const uint64_t tv = shfl_up64(v, o);
-        const bool th = __shfl_up((int)hf, o) != 0;
-        if (lane >= o) {
-          if (!hf) v = max(v, tv);
-          hf = hf || th;
-        }
-      }
-      if (lane == 63) {
-        red64[wave] = v;
-        redf[wave] = hf;
-      }
+      // exclusive prefix across threads: lanes (DPP), then waves
+      const uint64_t incl = wave_scan_max64(agg);
+      if (lane == 63) red64[wave] = incl;
       __syncthreads();
-      // inclusive value of the previous lane, then fold in earlier waves
-      uint64_t carry = shfl_up64(v, 1);
-      bool carry_h = __shfl_up((int)hf, 1) != 0;
-      if (lane == 0) {
-        carry = 0;
-        carry_h = false;
+      uint64_t carry = dpp64<kWaveShr1>(incl);
+      {
+        const uint64_t wv = row_scan_max64(lane < NT / 64 ? red64[lane] : 0ull);
+        const uint32_t w = (uint32_t)__builtin_amdgcn_readfirstlane(wave);
+        if (w) carry = max(carry, readlane64(wv, w - 1));
       }
-      if (!carry_h)
-        for (int w = wave - 1; w >= 0; w--) {
-          carry = max(carry, red64[w]);
-          if (redf[w]) break;
-        }
-      // E3: finish times
+      // finish times
       const uint32_t nxt0 = (tid + 1 < NT) ? pinfo[tid + 1] : 0u;  // next thread's first
-      uint32_t lf[CPT];
-#pragma unroll
-      for (int q = 0; q < CPT; q++) lf[q] = lfree[min((pis[q] >> cb) & lmask, (uint32_t)E - 1)];
       uint64_t run = carry;
 #pragma unroll
       for (int q = 0; q < CPT; q++) {
@@ -738,9 +805,9 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
             continue;
           }
           const uint32_t cl = cs[q];
-          const uint64_t g = (uint64_t)ct[q] + kBias - (uint64_t)k * cl;
-          run = (k == 0) ? g : max(run, g);
-          const int64_t best = max((int64_t)lf[q], (int64_t)run - (int64_t)kBias);
+          run = max(run, comp[q]);  // the run's own link: earlier links compare lower
+          const int64_t g = (int64_t)(run & ((1ull << 33) - 1));
+          const int64_t best = max((int64_t)lf[q], g - (int64_t)kBias);
           const uint32_t f = (uint32_t)((int64_t)(k + 1) * cl + best);
           ctime[c] = f;
           mk = max(mk, f);
@@ -748,9 +815,6 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
           if (x + 1 == tot || nk == 0) lfree[E + l] = f;  // last send of the link's run
         }
       }
-      __syncthreads();
-      for (int l = tid; l < E; l += NT)
-        if (lfree[E + l] != kUnset) lfree[l] = lfree[E + l];
       __syncthreads();
     }
     // makespan: block max
@@ -787,8 +851,8 @@ int32_t path_fast_layout(const taccl_plan &p, PathArgs &a) {
   a.o_fctime = take(4 * C);
   a.o_flfree = take(8 * E);
   a.o_fbcnt = take(4 * (p.max_lvl_nb + 1));
-  a.o_fepr = take(4 * M);
-  a.o_fech = take(2 * M);
+  a.o_fepr = take(8 * M);
+  a.o_fech = 0;
   a.o_fsrt = take(4 * path_fast_threads(p) * path_fast_cpt(p));
   a.o_fscl = 0;
   // packed sorted sends: chunk, link and run index in one word
@@ -819,6 +883,8 @@ int path_fast_cpt(const taccl_plan &p) {
     return b;
   };
   if (2 * bits((uint32_t)p.coll.C) + bits((uint32_t)p.topo.E) > 32) return 0;
+  // bucket and link fields are packed into 16 bits
+  if (p.max_lvl_nb >= (1 << 16) || p.topo.E > (1 << 16)) return 0;
   const int nt = path_fast_threads(p);
   const int per = (p.coll.C + nt - 1) / nt;
   return per <= 1 ? 1 : per <= 2 ? 2 : per <= 4 ? 4 : 0;
