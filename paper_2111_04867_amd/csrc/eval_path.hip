@@ -557,19 +557,20 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
   for (int j = tid; j <= nlev; j += NT) s_lcb[j] = a.lvl_cls_begin[j];
   __syncthreads();
 
-  for (int64_t i = blockIdx.x; i < a.n; i += gridDim.x) {
-    // ---- setup: owned chunks' records and priorities in registers --------
+  // The candidate's route choices, chunk tables and priorities (one batch
+  // of independent loads). The next candidate's batch is issued as soon as
+  // the last level has taken what it needs from these registers, so its
+  // HBM latency overlaps that level's ordering and timing.
+  uint32_t pr[CPT][kFastMaxHops], kk[CPT], cp[CPT];
+  auto load_inputs = [&](int64_t i) {
+    if (i >= a.n) return;
     const uint8_t *grt = a.routes + (size_t)i * a.route_stride;
     const uint32_t *gpr = a.prio + (size_t)i * a.prio_stride;
-    // the thread index is hidden from the optimiser once per candidate, so
-    // per-chunk addresses are recomputed instead of being hoisted out of the
-    // candidate loop and spilled
+    // the thread index is hidden from the optimiser, so per-chunk addresses
+    // are recomputed instead of being hoisted out of the candidate loop and
+    // spilled
     int tv = tid;
     asm volatile("" : "+v"(tv));
-    uint32_t rw0[CPT], rcl[CPT][3], pr[CPT][kFastMaxHops], hmap[CPT];
-    uint32_t kk[CPT], cp[CPT];
-    bool unrouted = false;
-    // first batch: route choices, chunk tables and priorities (independent)
 #pragma unroll
     for (int j = 0; j < CPT; j++) {
       const int c = tv + NT * j;
@@ -583,6 +584,14 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
           pr[j][h] = h < H ? gpr[(uint32_t)(c * H + h)] : 0u;
       }
     }
+  };
+  load_inputs(blockIdx.x);
+  for (int64_t i = blockIdx.x; i < a.n; i += gridDim.x) {
+    // ---- setup: owned chunks' records in registers -----------------------
+    int tv = tid;
+    asm volatile("" : "+v"(tv));
+    uint32_t rw0[CPT], rcl[CPT][3], hmap[CPT];
+    bool unrouted = false;
     // second batch: the chosen route records
 #pragma unroll
     for (int j = 0; j < CPT; j++) {
@@ -659,7 +668,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
           if (h >= 4) cw = rcl[j][2];
           const uint32_t cls = (h & 1) ? (cw >> 16) : (cw & 0xFFFF);
           const uint32_t cbk = s_cbkt[cls], ci = s_cinfo[cls];
-          const uint32_t fb = s_cbkt[lo + (ci >> 16)] & 0xFFFFFF;
+          const uint32_t fb = ci >> 16;
           const uint32_t bits = cbk >> 24;
           const uint32_t b = (cbk & 0xFFFFFF) + (bits ? (pv >> (32 - bits)) : 0u);
           pl[j] = pv;
@@ -667,6 +676,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
           wb[j] = atomicAdd(&bcnt[b], 1u) | ((ci & 0xFFFFu) << 16);
         }
       }
+      if (L == nlev - 1) load_inputs(i + gridDim.x);  // this candidate's inputs are dead
       __syncthreads();
       // ---- B. bucket starts --------------------------------------------------
       block_excl_scan(bcnt, NB, red);
@@ -817,6 +827,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       }
       __syncthreads();
     }
+    if (nlev == 0) load_inputs(i + gridDim.x);
     // makespan: block max
     for (int o = 32; o > 0; o >>= 1) mk = max(mk, (uint32_t)__shfl_xor((int)mk, o));
     if (lane == 0) red[wave] = mk;

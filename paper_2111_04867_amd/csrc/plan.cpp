@@ -422,7 +422,7 @@ static taccl_status_t build_levels(taccl_plan *p) {
       for (uint32_t k = p->lvl_cls_begin[L]; k < p->lvl_cls_begin[L + 1]; k++) {
         const uint32_t l = p->cls_link[k];
         const uint32_t first = p->llc[((size_t)L * E + l) * 2];
-        p->cinfo[k] = l | ((first - p->lvl_cls_begin[L]) << 16);
+        p->cinfo[k] = l | ((p->cbkt[first] & 0xFFFFFFu) << 16);
       }
   }
   return TACCL_OK;

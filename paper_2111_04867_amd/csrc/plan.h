@@ -126,7 +126,7 @@ struct taccl_plan {
   std::vector<uint16_t> cls_link;      // [ncls]
   // register-resident Alltoall kernel: per route option {hops | level of
   // hop h << (8+3h), classes of hops 0..5 as u16 pairs}; per chunk its pair's
-  // first option | option count << 24; per class link | (first class of the
+  // first option | option count << 24; per class link | (first bucket of the
   // same level and link, level-relative) << 16
   bool path_fast = false;
   std::vector<uint32_t> arec, cpath, cinfo;
