@@ -393,88 +393,92 @@ __device__ __forceinline__ void slot_trees(const TreeArgs &a, const TreeLds &tl,
   const uint16_t *s_rev = tl.rev;
   const uint32_t *rt32 = tl.rt32;
   uint32_t *dist = tl.dist;
+  // The parent hop of every slot, straight-line code (selects instead of
+  // branches) so the LDS loads of all slots can be in flight together.
+  uint32_t ec[J];  // cost of the link into the slot
 #pragma unroll
   for (int j = 0; j < J; j++) {
     const uint32_t sl = lane + 64 * j;
-    pe[j] = ~0u;
-    ps[j] = kNoPred;
-    dv[j] = kNotYet;
-    if (sl < (uint32_t)CV) {
-      const uint32_t c = div_v(sl, a.vmagic), v = sl - c * V;
-      const uint32_t o = s_own[c];
-      if (v == o) {
-        dist[sl] = 0;
-      } else {
-        uint32_t kw[PW], ow[PW];
+    const bool in = sl < (uint32_t)CV;
+    const uint32_t slc = in ? sl : 0u;
+    const uint32_t c = div_v(slc, a.vmagic), v = slc - c * V;
+    const uint32_t o = s_own[c];
+    const uint64_t pm = s_post[c];
+    // destinations whose drawn path passes through v: a byte of
+    // (chosen option bit & options through v) is non-zero
+    uint32_t kw[PW], m = 0;
 #pragma unroll
-        for (int w = 0; w < PW; w++) {
-          kw[w] = rt32[c * PW + w];
-          ow[w] = s_opt[(o * V + v) * PW + w];
-        }
-        // destinations whose drawn path passes through v: a byte of
-        // (chosen option bit & options through v) is non-zero
-        uint32_t m = 0;
-#pragma unroll
-        for (int w = 0; w < PW; w++) {
-          const uint32_t t = kw[w] & ow[w];
-          uint32_t nz = ((t + 0x7F7F7F7Fu) & 0x80808080u) >> 7;  // bit 8b per byte b
-          nz |= nz >> 7;
-          nz |= nz >> 14;
-          m |= (nz & 0xFu) << (4 * w);
-        }
-        const uint64_t pm = s_post[c];
-        m &= (uint32_t)pm;  // only postcondition destinations are routed
-        if (m) {
-          const uint32_t d = __builtin_ctz(m);
-          const uint32_t kd = __builtin_ctz((kw[d >> 2] >> (8 * (d & 3))) & 0xFFu);
-          const uint4 r = s_rec[(o * P + d) * K + kd];
-          const uint32_t x0 = r.x & 0xFFFFFFu, x1 = r.y, x2 = r.z, x3 = r.w;
-          uint32_t e, u;
-          if ((x0 >> 16) == v) {
-            e = x0; u = o;
-          } else if (((x1 >> 16) & 0xFFu) == v) {
-            e = x1; u = (x0 >> 16) & 0xFFu;
-          } else if (((x2 >> 16) & 0xFFu) == v) {
-            e = x2; u = (x1 >> 16) & 0xFFu;
-          } else {
-            e = x3; u = (x2 >> 16) & 0xFFu;
-          }
-          const uint32_t l = e & 0xFFFFu;
-          pe[j] = l | (u << 16);
-          if (u == o) {
-            // ReduceScatter measures the tree backwards, on reverse links
-            dv[j] = s_cost[kRS ? s_rev[l] : l];
-            dist[sl] = dv[j];
-          } else {
-            ps[j] = c * V + u;
-            dist[sl] = kNotYet;
-          }
-        } else if ((pm >> v) & 1) {
-          bad = true;  // a rank of the postcondition is never reached
-        }
-      }
+    for (int w = 0; w < PW; w++) {
+      kw[w] = rt32[c * PW + w];
+      const uint32_t t = kw[w] & s_opt[(o * V + v) * PW + w];
+      uint32_t nz = ((t + 0x7F7F7F7Fu) & 0x80808080u) >> 7;  // bit 8b per byte b
+      nz |= nz >> 7;
+      nz |= nz >> 14;
+      m |= (nz & 0xFu) << (4 * w);
     }
+    m &= (uint32_t)pm;  // only postcondition destinations are routed
+    const bool root = v == o;
+    const bool has = in && !root && m != 0;
+    bad |= in && !root && m == 0 && ((pm >> v) & 1);  // a rank is never reached
+    // the smallest such destination d and its chosen option kd
+    const uint32_t d = m ? (uint32_t)__builtin_ctz(m) : 0u;
+    uint32_t kwd = kw[0];
+#pragma unroll
+    for (int w = 1; w < PW; w++)
+      if ((d >> 2) == (uint32_t)w) kwd = kw[w];
+    const uint32_t kd = __builtin_ctz(((kwd >> (8 * (d & 3))) & 0xFFu) | 0x100u) & 7u;
+    const uint4 r = s_rec[(o * P + d) * K + kd];
+    // the hop of that path that enters v
+    const uint32_t x0 = r.x & 0xFFFFFFu, x1 = r.y, x2 = r.z, x3 = r.w;
+    uint32_t e = x3, u = (x2 >> 16) & 0xFFu;
+    if (((x2 >> 16) & 0xFFu) == v) {
+      e = x2;
+      u = (x1 >> 16) & 0xFFu;
+    }
+    if (((x1 >> 16) & 0xFFu) == v) {
+      e = x1;
+      u = (x0 >> 16) & 0xFFu;
+    }
+    if ((x0 >> 16) == v) {
+      e = x0;
+      u = o;
+    }
+    const uint32_t l = e & 0xFFFFu;
+    // ReduceScatter measures the tree backwards, on reverse links
+    ec[j] = s_cost[has ? (kRS ? s_rev[l] : l) : 0u];
+    const bool top = u == o;  // the parent is the chunk's owner
+    pe[j] = has ? (l | (u << 16)) : ~0u;
+    ps[j] = (has && !top) ? c * V + u : kNoPred;
+    dv[j] = (has && top) ? ec[j] : kNotYet;
+    if (in) dist[sl] = root ? 0u : dv[j];
   }
   wave_sync();
-  // distances: a slot takes its parent's once that is known
+  // distances: a slot takes its parent's once that is known (the loads of
+  // all slots are issued together)
   uint32_t dep[J];
 #pragma unroll
   for (int j = 0; j < J; j++) dep[j] = (pe[j] != ~0u) ? 1u : 0u;
   for (int round = 2;; round++) {
+    uint32_t du[J];
+#pragma unroll
+    for (int j = 0; j < J; j++) {
+      const bool want = dv[j] == kNotYet && pe[j] != ~0u;
+      du[j] = dist[want ? ps[j] : 0u];
+      if (!want) du[j] = 0u;
+    }
     bool pend = false;
 #pragma unroll
     for (int j = 0; j < J; j++)
       if (dv[j] == kNotYet && pe[j] != ~0u) {
-        const uint32_t du = lds_get(&dist[ps[j]]);
-        if (du != kNotYet) {
-          const uint32_t l = pe[j] & 0xFFFFu;
-          dv[j] = du + s_cost[kRS ? s_rev[l] : l];
-          lds_put(&dist[lane + 64 * j], dv[j]);
+        if (du[j] != kNotYet) {
+          dv[j] = du[j] + ec[j];
+          dist[lane + 64 * j] = dv[j];
           dep[j] = round;
         } else {
           pend = true;
         }
       }
+    wave_sync();
     if (__ballot(pend) == 0) break;
     if (round > V) {  // unreachable: parents form a tree
       fault = true;
@@ -503,9 +507,12 @@ __device__ __forceinline__ void slot_trees(const TreeArgs &a, const TreeLds &tl,
     }
   } else {
     for (uint32_t t = dmax; t >= 2; t--) {
+      uint32_t own[J];
+#pragma unroll
+      for (int j = 0; j < J; j++) own[j] = dist[(lane + 64 * j) < (uint32_t)CV ? lane + 64 * j : 0];
 #pragma unroll
       for (int j = 0; j < J; j++)
-        if (dep[j] == t) atomicMax(&dist[ps[j]], lds_get(&dist[lane + 64 * j]));
+        if (dep[j] == t) atomicMax(&dist[ps[j]], own[j]);
       wave_sync();
     }
   }

@@ -209,3 +209,30 @@ def test_runs_on_a_side_stream():
     s.synchronize()
     rmk, rok = ref.eval(routes, prio)
     assert (mk.cpu().numpy().view(np.uint32) == rmk).all() and (ok.cpu().numpy() == rok).all()
+
+
+def hybrid_multicast(P, kind, cpr, k=4):
+    """P ranks on one switch (vertex P) plus a bidirectional ring of direct
+    links. V = P + 1 does not divide 64, so a chunk's vertex slots straddle
+    the kernel's 64-slot groups and a parent can sit in an earlier group than
+    its child; trees mix direct and switched hops and run several levels deep."""
+    edges = cf.switch_edges(range(P), P, 700, 8) + cf.ring_edges(range(P), 1500, 8)
+    row_ptr, col, a, b = cf.csr_from_edges(P + 1, edges)
+    return cf.Workload(f"hybrid{P}_{kind}_{cpr}", P + 1, P, row_ptr, col, a, b, None, kind, cpr,
+                       65536, cf.KSHORTEST, k=k)
+
+
+@pytest.mark.parametrize("kind", [cf.ALLGATHER, cf.REDUCESCATTER, cf.ALLREDUCE])
+@pytest.mark.parametrize("P,cpr", [(8, 1), (8, 2), (16, 1), (16, 2)])
+def test_multicast_slots_straddling_groups(kind, P, cpr):
+    from paper_2111_04867_amd.binding import Plan
+    w = hybrid_multicast(P, kind, cpr)
+    plan, ref = Plan.from_workload(w), OraclePlan.from_workload(w)
+    opts = plan.route_options()
+    assert (opts == ref.route_options()).all()
+    routes, prio = generate(31 + P + cpr, 0, 600, opts, plan.prio_stride)
+    say(f"[gpu] {w.name}: 600 candidates")
+    mk, ok = plan.eval(routes, prio)
+    rmk, rok = ref.eval_threads(routes, prio)
+    bad = np.nonzero((mk != rmk) | (ok != rok))[0]
+    assert bad.size == 0, f"{w.name}: {bad.size} mismatches, first at {bad[:5].tolist()}"
