@@ -26,6 +26,7 @@
 #include <hip/hip_runtime.h>
 
 #include "kernels.h"
+#include "wave.h"
 
 namespace taccl {
 
@@ -56,18 +57,9 @@ __device__ __forceinline__ void wave_sync() {
   asm volatile("" ::: "memory");
 }
 
-__device__ __forceinline__ uint32_t wave_max(uint32_t v) {
-  for (int o = 32; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o));
-  return v;
-}
+__device__ __forceinline__ uint32_t wave_max(uint32_t v) { return wave_reduce_max(v); }
 
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v, int lane) {
-  for (int o = 1; o < 64; o <<= 1) {
-    uint32_t t = (uint32_t)__shfl_up((int)v, o);
-    if (lane >= o) v += t;
-  }
-  return v;
-}
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v, int) { return wave_scan_add(v); }
 
 // n / V for n, V < 2^16 with a precomputed m = floor(2^32 / V) + 1
 __device__ __forceinline__ uint32_t div_v(uint32_t n, uint32_t m) {
@@ -813,6 +805,46 @@ void tree_layers_kernel(TreeArgs a) {
     uint32_t mk = 0;
     for (int ly = 0; ly < nl; ly++) {
       const uint32_t qs = lst[ly], qe = lst[ly + 1];
+      if (!kContig) {
+        // Every send's ready time is known (its parent send lies in a layer
+        // above), so the k-th send of a link run with cost c and busy time
+        // F finishes at (k+1)c + max(F, max_{j<=k}(r_j - j c)). The layer's
+        // runs lie in ascending link order, so one plain prefix max over
+        // link << 33 | (r_j - j c + 2^32) gives every position the max over
+        // the earlier sends of its own run (DPP scan, 64 positions a step).
+        uint64_t carry = 0;
+        for (uint32_t base = qs; base < qe; base += 64) {
+          const uint32_t q = base + lane;
+          const bool ok = q < qe;
+          const uint32_t qq = ok ? q : qs;
+          const uint32_t e = ord2[qq], inf = info2[qq];
+          const uint32_t l = inf & 0xFFFFu, k = (inf >> 16) & 0x7FFFu;
+          uint32_t r;
+          if (kRS) {
+            r = fin[e & 0xFFFFu];
+          } else {
+            const uint32_t pj = e >> 16;
+            r = fin[pj == kNoPred ? 0u : pj];
+            if (pj == kNoPred) r = 0;
+          }
+          const uint32_t cl = s_cost[l], F = lfree[l];
+          const uint32_t kn = (q + 1 < qe) ? ((info2[q + 1] >> 16) & 0x7FFFu) : 0u;
+          const uint64_t comp =
+              ok ? (((uint64_t)l << 33) | ((uint64_t)r + (1ull << 32) - (uint64_t)k * cl)) : 0ull;
+          const uint64_t incl = max(wave_scan_max64(comp), carry);
+          carry = readlane64(incl, 63);
+          const int64_t best =
+              max((int64_t)F, (int64_t)(incl & ((1ull << 33) - 1)) - (int64_t)(1ull << 32));
+          const uint32_t f = (uint32_t)((int64_t)(k + 1) * cl + best);
+          if (ok) {
+            finish(e, f);
+            mk = max(mk, f);
+            if (kn == 0) lfree[l] = f;  // the run's last send
+          }
+        }
+        wave_sync();
+        continue;
+      }
       // ready time of every send of the layer: its parent send is in a
       // layer above
       for (uint32_t q = qs + lane; q < qe; q += 64) {

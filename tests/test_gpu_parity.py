@@ -222,11 +222,14 @@ def hybrid_multicast(P, kind, cpr, k=4):
                        65536, cf.KSHORTEST, k=k)
 
 
+@pytest.mark.parametrize("greedy", [0, 1])
 @pytest.mark.parametrize("kind", [cf.ALLGATHER, cf.REDUCESCATTER, cf.ALLREDUCE])
 @pytest.mark.parametrize("P,cpr", [(8, 1), (8, 2), (16, 1), (16, 2)])
-def test_multicast_slots_straddling_groups(kind, P, cpr):
+def test_multicast_slots_straddling_groups(kind, P, cpr, greedy):
     from paper_2111_04867_amd.binding import Plan
     w = hybrid_multicast(P, kind, cpr)
+    if greedy:
+        w = cf.with_greedy(w)
     plan, ref = Plan.from_workload(w), OraclePlan.from_workload(w)
     opts = plan.route_options()
     assert (opts == ref.route_options()).all()
