@@ -348,6 +348,22 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_eval_kernel(TreeArgs a) 
 }
 
 
+// Route word j (route bytes of chunk j / PW, destinations 4 (j % PW) ..
+// +3) as one-hot option bytes: 1 << choice, 0 for a choice of 8 or more
+// (no pair has that many options) and 0 for a destination outside the
+// chunk's postcondition (such an entry is never routed).
+template <int PW>
+__device__ __forceinline__ uint32_t one_hot_word(uint32_t w, uint32_t j, const uint64_t *s_post) {
+  const uint32_t pm4 = (uint32_t)(s_post[j / PW] >> (4 * (j % PW))) & 0xFu;
+  uint32_t oh = 0;
+#pragma unroll
+  for (int b = 0; b < 4; b++) {
+    const uint32_t kb = (w >> (8 * b)) & 0xFFu;
+    oh |= ((kb < 8 && ((pm4 >> b) & 1)) ? (1u << kb) : 0u) << (8 * b);
+  }
+  return oh;
+}
+
 // LDS views that the slot-parallel tree construction reads and writes.
 struct TreeLds {
   const uint32_t *cost;
@@ -396,29 +412,26 @@ __device__ __forceinline__ void slot_trees(const TreeArgs &a, const TreeLds &tl,
     const uint32_t c = div_v(slc, a.vmagic), v = slc - c * V;
     const uint32_t o = s_own[c];
     const uint64_t pm = s_post[c];
-    // destinations whose drawn path passes through v: a byte of
-    // (chosen option bit & options through v) is non-zero
-    uint32_t kw[PW], m = 0;
+    // (chosen option bit & options through v), one byte per destination
+    // (destinations outside the postcondition were zeroed when staged): its
+    // lowest set bit is byte 4w + b of the smallest destination d whose drawn
+    // path passes through v, and the bit inside the byte is that path's
+    // option kd
+    uint32_t t[PW];
 #pragma unroll
-    for (int w = 0; w < PW; w++) {
-      kw[w] = rt32[c * PW + w];
-      const uint32_t t = kw[w] & s_opt[(o * V + v) * PW + w];
-      uint32_t nz = ((t + 0x7F7F7F7Fu) & 0x80808080u) >> 7;  // bit 8b per byte b
-      nz |= nz >> 7;
-      nz |= nz >> 14;
-      m |= (nz & 0xFu) << (4 * w);
-    }
-    m &= (uint32_t)pm;  // only postcondition destinations are routed
+    for (int w = 0; w < PW; w++) t[w] = rt32[c * PW + w] & s_opt[(o * V + v) * PW + w];
+    uint32_t tw = t[PW - 1], wi = PW - 1;
+#pragma unroll
+    for (int w = PW - 2; w >= 0; w--)
+      if (t[w]) {
+        tw = t[w];
+        wi = w;
+      }
     const bool root = v == o;
-    const bool has = in && !root && m != 0;
-    bad |= in && !root && m == 0 && ((pm >> v) & 1);  // a rank is never reached
-    // the smallest such destination d and its chosen option kd
-    const uint32_t d = m ? (uint32_t)__builtin_ctz(m) : 0u;
-    uint32_t kwd = kw[0];
-#pragma unroll
-    for (int w = 1; w < PW; w++)
-      if ((d >> 2) == (uint32_t)w) kwd = kw[w];
-    const uint32_t kd = __builtin_ctz(((kwd >> (8 * (d & 3))) & 0xFFu) | 0x100u) & 7u;
+    const bool has = in && !root && tw != 0;
+    bad |= in && !root && tw == 0 && ((pm >> v) & 1);  // a rank is never reached
+    const uint32_t bit = tw ? (uint32_t)__builtin_ctz(tw) : 0u;
+    const uint32_t d = 4 * wi + (bit >> 3), kd = bit & 7;
     const uint4 r = s_rec[(o * P + d) * K + kd];
     // the hop of that path that enters v
     const uint32_t x0 = r.x & 0xFFFFFFu, x1 = r.y, x2 = r.z, x3 = r.w;
@@ -634,15 +647,7 @@ void tree_layers_kernel(TreeArgs a) {
 #pragma unroll
     for (int k = 0; k < kPfRoute; k++) {
       const int j = lane + 64 * k;
-      if (j < nrw) {
-        uint32_t oh = 0;
-#pragma unroll
-        for (int b = 0; b < 4; b++) {
-          const uint32_t kb = (pf_r[k] >> (8 * b)) & 0xFFu;
-          oh |= (kb < 8 ? (1u << kb) : 0u) << (8 * b);
-        }
-        rt32[j] = oh;
-      }
+      if (j < nrw) rt32[j] = one_hot_word<PW>(pf_r[k], j, s_post);
     }
     uint32_t px[J];
 #pragma unroll
@@ -1005,15 +1010,7 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_greedy_kernel(TreeArgs a
 #pragma unroll
     for (int k = 0; k < kPfRoute; k++) {
       const int j = lane + 64 * k;
-      if (j < nrw) {
-        uint32_t oh = 0;
-#pragma unroll
-        for (int b = 0; b < 4; b++) {
-          const uint32_t kb = (pf_r[k] >> (8 * b)) & 0xFFu;
-          oh |= (kb < 8 ? (1u << kb) : 0u) << (8 * b);
-        }
-        rt32[j] = oh;
-      }
+      if (j < nrw) rt32[j] = one_hot_word<PW>(pf_r[k], j, s_post);
     }
     uint32_t px[J];
 #pragma unroll
