@@ -435,12 +435,6 @@ namespace {
 constexpr uint64_t kBias = 1ull << 32;      // keeps r - k c non-negative
 constexpr uint32_t kUnset = 0xFFFFFFFFu;
 
-__device__ __forceinline__ uint64_t shfl_up64(uint64_t v, int o) {
-  const uint32_t lo = (uint32_t)__shfl_up((int)(uint32_t)v, o);
-  const uint32_t hi = (uint32_t)__shfl_up((int)(uint32_t)(v >> 32), o);
-  return ((uint64_t)hi << 32) | lo;
-}
-
 // exclusive scan of cnt[0..n) in place, cnt[n] = total (all threads call)
 __device__ void block_excl_scan(uint32_t *cnt, int n, uint32_t *wsum) {
   const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63, wave = tid >> 6;

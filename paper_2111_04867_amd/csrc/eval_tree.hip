@@ -374,18 +374,21 @@ struct TreeLds {
   const uint16_t *rev;
   const uint32_t *rt32;
   uint32_t *dist;
+  uint16_t *anc;  // pj_rounds arrays of anc_stride slots: 2^k-th ancestor
 };
 
 // Trees, one lane per (chunk c, vertex v) slot (slots lane + 64j). The
 // first-reach merge gives v the hop that enters it on the path of the
 // smallest destination whose path contains v (found from the one-hot route
 // bytes and the per-vertex option bytes, no walk). Distances from the owner
-// follow in rounds; then a push-up deepest first. On return, per slot with a
-// send: pe = link | parent vertex << 16, ps = parent's slot (or kNoPred when
-// the parent is the owner), dv = distance from the owner to v; dist[slot] =
-// largest distance below v (Allgather) or, for ReduceScatter (kRS: costs of
-// the reverse links), the longest reversed path from below up to v. `bad`:
-// a rank of the postcondition is unreached; `fault`: an impossible cycle.
+// and the largest distance below every vertex then follow by doubling over
+// ancestors (pointer jumping), in ceil(log2 V) rounds each, whatever the
+// depth of the trees. On return, per slot with a send: pe = link | parent
+// vertex << 16, ps = parent's slot (or kNoPred when the parent is the owner),
+// dv = distance from the owner to v; dist[slot] = largest distance below v
+// (Allgather) or, for ReduceScatter (kRS: costs of the reverse links), the
+// longest reversed path from below up to v. `bad`: a rank of the
+// postcondition is unreached; `fault` is never set (parents form a tree).
 template <int J, int PW, bool kRS>
 __device__ __forceinline__ void slot_trees(const TreeArgs &a, const TreeLds &tl, int lane,
                                            uint32_t (&pe)[J], uint32_t (&ps)[J],
@@ -401,9 +404,11 @@ __device__ __forceinline__ void slot_trees(const TreeArgs &a, const TreeLds &tl,
   const uint16_t *s_rev = tl.rev;
   const uint32_t *rt32 = tl.rt32;
   uint32_t *dist = tl.dist;
+  uint16_t *anc = tl.anc;
   // The parent hop of every slot, straight-line code (selects instead of
   // branches) so the LDS loads of all slots can be in flight together.
-  uint32_t ec[J];  // cost of the link into the slot
+  uint32_t ec[J];          // cost of the link into the slot
+  uint32_t an[J], acc[J];  // 2^k-th ancestor slot, cost of the path up to it
 #pragma unroll
   for (int j = 0; j < J; j++) {
     const uint32_t sl = lane + 64 * j;
@@ -454,73 +459,70 @@ __device__ __forceinline__ void slot_trees(const TreeArgs &a, const TreeLds &tl,
     const bool top = u == o;  // the parent is the chunk's owner
     pe[j] = has ? (l | (u << 16)) : ~0u;
     ps[j] = (has && !top) ? c * V + u : kNoPred;
-    dv[j] = (has && top) ? ec[j] : kNotYet;
-    if (in) dist[sl] = root ? 0u : dv[j];
+    // ancestor chain: the parent's slot; the owner's slot (and a slot
+    // without a send) is its own ancestor, with distance 0
+    an[j] = has ? (top ? c * V + o : c * V + u) : slc;
+    acc[j] = has ? ec[j] : 0u;
+    if (in) {
+      dist[sl] = acc[j];
+      anc[sl] = (uint16_t)an[j];
+    }
   }
   wave_sync();
-  // distances: a slot takes its parent's once that is known (the loads of
-  // all slots are issued together)
-  uint32_t dep[J];
-#pragma unroll
-  for (int j = 0; j < J; j++) dep[j] = (pe[j] != ~0u) ? 1u : 0u;
-  for (int round = 2;; round++) {
-    uint32_t du[J];
+  // distances by doubling: acc covers 2^k links up the chain (or reaches the
+  // owner, whose slot adds 0 and is its own ancestor); every slot reads its
+  // ancestor's pair before any slot writes
+  const int R = a.pj_rounds;
+  const int AS = a.anc_stride;
+  for (int k = 0; k < R; k++) {
+    uint32_t ra[J], rn[J];
 #pragma unroll
     for (int j = 0; j < J; j++) {
-      const bool want = dv[j] == kNotYet && pe[j] != ~0u;
-      du[j] = dist[want ? ps[j] : 0u];
-      if (!want) du[j] = 0u;
+      ra[j] = dist[an[j]];
+      rn[j] = anc[k * AS + an[j]];
     }
-    bool pend = false;
+    wave_sync();
 #pragma unroll
-    for (int j = 0; j < J; j++)
-      if (dv[j] == kNotYet && pe[j] != ~0u) {
-        if (du[j] != kNotYet) {
-          dv[j] = du[j] + ec[j];
-          dist[lane + 64 * j] = dv[j];
-          dep[j] = round;
-        } else {
-          pend = true;
-        }
+    for (int j = 0; j < J; j++) {
+      const uint32_t sl = lane + 64 * j;
+      acc[j] += ra[j];
+      an[j] = rn[j];
+      if (sl < (uint32_t)CV) {
+        dist[sl] = acc[j];
+        if (k + 1 < R) anc[(k + 1) * AS + sl] = (uint16_t)rn[j];
       }
-    wave_sync();
-    if (__ballot(pend) == 0) break;
-    if (round > V) {  // unreachable: parents form a tree
-      fault = true;
-      break;
     }
+    wave_sync();
   }
-  // largest distance below each vertex, deepest sends first
-  uint32_t dmax = 0;
+  // largest distance below every vertex: in round k each slot pushes the
+  // largest distance it knows below it to its 2^k-th ancestor, so after
+  // round k a slot knows every descendant less than 2^(k+1) links down
+  // (values only ever grow, each is a descendant's distance)
 #pragma unroll
-  for (int j = 0; j < J; j++) dmax = max(dmax, dep[j]);
-  dmax = wave_max(dmax);
-  wave_sync();
-  if (kRS) {
-    // ReduceScatter: longest reversed path from a vertex below v up to v
+  for (int j = 0; j < J; j++) dv[j] = (pe[j] != ~0u) ? acc[j] : kNotYet;
+  for (int k = 0; k < R; k++) {
+    uint32_t m[J], up[J];
+#pragma unroll
+    for (int j = 0; j < J; j++) {
+      const uint32_t sl = lane + 64 * j;
+      const uint32_t slc = sl < (uint32_t)CV ? sl : 0u;
+      m[j] = dist[slc];
+      up[j] = anc[k * AS + slc];
+    }
 #pragma unroll
     for (int j = 0; j < J; j++)
-      if (lane + 64 * j < CV) lds_put(&dist[lane + 64 * j], 0u);
+      if (pe[j] != ~0u) atomicMax(&dist[up[j]], m[j]);
     wave_sync();
-    for (uint32_t t = dmax; t >= 2; t--) {
-#pragma unroll
-      for (int j = 0; j < J; j++)
-        if (dep[j] == t)
-          atomicMax(&dist[ps[j]], lds_get(&dist[lane + 64 * j]) +
-                                      s_cost[s_rev[pe[j] & 0xFFFFu]]);
-      wave_sync();
-    }
-  } else {
-    for (uint32_t t = dmax; t >= 2; t--) {
-      uint32_t own[J];
-#pragma unroll
-      for (int j = 0; j < J; j++) own[j] = dist[(lane + 64 * j) < (uint32_t)CV ? lane + 64 * j : 0];
-#pragma unroll
-      for (int j = 0; j < J; j++)
-        if (dep[j] == t) atomicMax(&dist[ps[j]], own[j]);
-      wave_sync();
-    }
   }
+  if (kRS) {
+    // ReduceScatter: longest reversed path from a vertex below v up to v =
+    // largest reversed distance below v minus v's own
+#pragma unroll
+    for (int j = 0; j < J; j++)
+      if (pe[j] != ~0u) dist[lane + 64 * j] -= acc[j];
+    wave_sync();
+  }
+  (void)fault;
 }
 
 // Layered variant for plans with at most 4 hops and 8 options per pair,
@@ -594,6 +596,7 @@ void tree_layers_kernel(TreeArgs a) {
   // << 16. Timing: finish times per slot and ready times per position.
   uint32_t *rt32 = (uint32_t *)wl;
   uint32_t *dist = (uint32_t *)(wl + a.w_dist);
+  uint16_t *anc = (uint16_t *)(wl + a.w_anc);
   uint32_t *cnt = (uint32_t *)(wl + a.w_cnt);
   uint4 *erec = (uint4 *)(wl + a.w_erec);
   uint32_t *ord2 = (uint32_t *)(wl + a.w_ord2);
@@ -661,7 +664,7 @@ void tree_layers_kernel(TreeArgs a) {
     // pe: link | parent vertex << 16 of the send into the slot, ~0 if none
     uint32_t pe[J], ps[J], dv[J];
     bool bad = false, fault = false;
-    slot_trees<J, PW, kRS>(a, TreeLds{s_cost, s_own, s_post, s_rec, s_opt, s_rev, rt32, dist},
+    slot_trees<J, PW, kRS>(a, TreeLds{s_cost, s_own, s_post, s_rec, s_opt, s_rev, rt32, dist, anc},
                            lane, pe, ps, dv, bad, fault);
 
     // ---- keys and layers of this lane's sends ----------------------------
@@ -977,6 +980,7 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_greedy_kernel(TreeArgs a
   unsigned char *wl = lds + a.o_wave + wave * a.wave_bytes;
   uint32_t *rt32 = (uint32_t *)wl;
   uint32_t *dist = (uint32_t *)(wl + a.w_dist);
+  uint16_t *anc = (uint16_t *)(wl + a.w_anc);
   uint64_t *gkey = (uint64_t *)(wl + a.w_gkey);  // per slot: ~rem << 32 | trav
   uint32_t *gpri = (uint32_t *)(wl + a.w_gpri);  // per slot: priority
   uint32_t *glp = (uint32_t *)(wl + a.w_glp);    // per slot: link | other slot << 16
@@ -1021,7 +1025,7 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_greedy_kernel(TreeArgs a
 
     uint32_t pe[J], ps[J], dv[J];
     bool bad = false, fault = false;
-    slot_trees<J, PW, kRS>(a, TreeLds{s_cost, s_own, s_post, s_rec, s_opt, s_rev, rt32, dist},
+    slot_trees<J, PW, kRS>(a, TreeLds{s_cost, s_own, s_post, s_rec, s_opt, s_rev, rt32, dist, anc},
                            lane, pe, ps, dv, bad, fault);
 
     // ---- per-slot send records; sends counted per link ------------------
@@ -1231,6 +1235,14 @@ hipError_t launch_tree(const TreeArgs &a, int grid, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// ancestor doubling: 2^rounds >= V covers the deepest tree (V - 1 links)
+static void set_pj(TreeArgs &a, int32_t V, int32_t CV) {
+  int r = 0;
+  while ((1 << r) < V) r++;
+  a.pj_rounds = std::max(r, 1);
+  a.anc_stride = align16(2 * CV) / 2;
+}
+
 int32_t tree_layers_layout(const taccl_plan &p, TreeArgs &a) {
   if (tree_layout(p, a) <= 0) return 0;
   const int32_t C = p.coll.C, V = p.topo.V, E = p.topo.E, P = p.topo.P;
@@ -1272,8 +1284,11 @@ int32_t tree_layers_layout(const taccl_plan &p, TreeArgs &a) {
   const int32_t S = std::max<int64_t>(std::min<int64_t>(p.max_sends, CV), 1);
   // region X: route words and distances, then bucket entries, then finish
   // and ready times
-  const int32_t x_tree = align16(p.route_stride) + align16(4 * CV);
+  set_pj(a, V, CV);
+  const int32_t x_tree =
+      align16(p.route_stride) + align16(4 * CV) + a.pj_rounds * align16(2 * CV);
   a.w_dist = align16(p.route_stride);
+  a.w_anc = a.w_dist + align16(4 * CV);
   a.w_erec = 0;
   a.w_fin = 0;
   a.w_rq = align16(4 * CV);
@@ -1355,9 +1370,14 @@ int32_t tree_greedy_layout(const taccl_plan &p, TreeArgs &a) {
   };
   a.w_rt = wtake(p.route_stride);
   a.w_dist = wtake(4 * CV);
+  set_pj(a, V, CV);
+  // the ancestor arrays die with the trees, before the keys, priorities and
+  // link records of the slots (at most 6 * align16(2 CV) <= 16 CV bytes)
+  a.w_anc = w;
   a.w_gkey = wtake(8 * CV);
   a.w_gpri = wtake(4 * CV);
   a.w_glp = wtake(4 * CV);
+  w = std::max(w, align16(a.w_anc + a.pj_rounds * align16(2 * CV)));
   a.w_gfin = wtake(4 * CV);
   a.w_grdy = wtake(4 * CV);
   a.w_gpend = wtake(4 * CV);

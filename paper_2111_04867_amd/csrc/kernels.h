@@ -54,6 +54,9 @@ struct TreeArgs {
   const uint4 *rec4;    // route records, one 16-byte record per option
   int32_t o_rec4, o_opt;
   int32_t w_dist, w_cnt, w_erec, w_rq, w_lst, w_bnd, w_ord2, w_info2, w_fin, w_lmask;
+  // ancestor doubling of the slot-parallel trees: rounds (2^rounds >= V) and
+  // the per-round arrays of 16-bit slots (anc_stride slots apart)
+  int32_t w_anc, pj_rounds, anc_stride;
 };
 
 // Alltoall evaluation: one block per candidate, level by level.
