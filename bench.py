@@ -25,10 +25,11 @@ DEFAULT_WORKLOAD = "twonode16_ag"
 
 
 # Kernel that dominates each workload's launch (the only kernel it runs).
-KERNEL_OF = {"ring4_ag": "tree_eval", "cubemesh8_ag": "tree_eval", "twonode16_ag": "tree_eval",
-             "switch16_a2a": "path_eval_fast", "fournode64_a2a": "path_eval_fast",
-             "twonode16_ag_contig": "tree_eval", "fournode64_a2a_contig": "path_eval_fast",
-             "cubemesh8_ar": "tree_eval", "twonode16_rs": "tree_eval", "twonode16_ar": "tree_eval",
+KERNEL_OF = {"ring4_ag": "tree_layers", "cubemesh8_ag": "tree_layers",
+             "twonode16_ag": "tree_layers", "switch16_a2a": "path_eval_fast",
+             "fournode64_a2a": "path_eval_fast", "twonode16_ag_contig": "tree_layers",
+             "fournode64_a2a_contig": "path_eval_fast", "cubemesh8_ar": "tree_layers",
+             "twonode16_rs": "tree_layers", "twonode16_ar": "tree_layers",
              "cubemesh8_ag_greedy": "tree_greedy", "twonode16_ag_greedy": "tree_greedy",
              "switch16_a2a_ports": "path_eval", "fournode64_a2a_ports": "path_eval"}
 
