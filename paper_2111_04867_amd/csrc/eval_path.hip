@@ -589,29 +589,28 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       // ---- A. the level's sends per bucket ---------------------------------
       // wa: bucket | first bucket of the send's link run << 16 (kUnset: no
       // send at this level); wb: index in the bucket | link << 16
+      // Straight-line code (selects, and a per-lane dummy counter past the
+      // level's buckets for a slot without a send) so that the LDS loads and
+      // counter updates of all slots are in flight together.
       uint32_t wa[CPT], wb[CPT], pl[CPT];
 #pragma unroll
       for (int j = 0; j < CPT; j++) {
-        wa[j] = kUnset;
-        wb[j] = 0;
-        pl[j] = 0;
-        const int h = (int)((hmap[j] >> (3 * L)) & 7);  // 7: no hop at this level
-        if (h < kFastMaxHops) {
-          uint32_t cw = rcl[j][0], pv = pr[j][0];
+        const uint32_t h = (hmap[j] >> (3 * L)) & 7;  // 7: no hop at this level
+        const bool act = h < (uint32_t)kFastMaxHops;
+        uint32_t cw = rcl[j][0], pv = pr[j][0];
 #pragma unroll
-          for (int t = 1; t < kFastMaxHops; t++)
-            if (h == t) pv = pr[j][t];
-          if (h >= 2) cw = rcl[j][1];
-          if (h >= 4) cw = rcl[j][2];
-          const uint32_t cls = (h & 1) ? (cw >> 16) : (cw & 0xFFFF);
-          const uint32_t cbk = s_cbkt[cls], ci = s_cinfo[cls];
-          const uint32_t fb = ci >> 16;
-          const uint32_t bits = cbk >> 24;
-          const uint32_t b = (cbk & 0xFFFFFF) + (bits ? (pv >> (32 - bits)) : 0u);
-          pl[j] = pv;
-          wa[j] = b | (fb << 16);
-          wb[j] = atomicAdd(&bcnt[b], 1u) | ((ci & 0xFFFFu) << 16);
-        }
+        for (int t = 1; t < kFastMaxHops; t++)
+          if (h == (uint32_t)t) pv = pr[j][t];
+        if (h >= 2) cw = rcl[j][1];
+        if (h >= 4) cw = rcl[j][2];
+        const uint32_t cls = act ? ((h & 1) ? (cw >> 16) : (cw & 0xFFFF)) : lo;
+        const uint32_t cbk = s_cbkt[cls], ci = s_cinfo[cls];
+        const uint32_t bits = cbk >> 24;
+        const uint32_t b = (cbk & 0xFFFFFF) + (bits ? (pv >> (32 - bits)) : 0u);
+        const uint32_t slot = atomicAdd(&bcnt[act ? b : (uint32_t)NB + 1 + lane], 1u);
+        pl[j] = pv;
+        wa[j] = act ? (b | ((ci >> 16) << 16)) : kUnset;
+        wb[j] = slot | ((ci & 0xFFFFu) << 16);
       }
       if (L == nlev - 1) load_inputs(i + gridDim.x);  // this candidate's inputs are dead
       __syncthreads();
@@ -622,12 +621,15 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       // pos / ept = (pos * em) >> 32 with em = floor((2^32 - 1) / ept) + 1 <= 2^32
       const uint64_t em = ept ? 0xFFFFFFFFull / ept + 1 : 0;
       // ---- C. scatter --------------------------------------------------------
+      {
+        uint32_t pos[CPT];
 #pragma unroll
-      for (int j = 0; j < CPT; j++)
-        if (wa[j] != kUnset) {
-          const uint32_t pos = bcnt[wa[j] & 0xFFFFu] + (wb[j] & 0xFFFFu);
-          e64[pos] = ((uint64_t)pl[j] << 32) | (uint32_t)(tid + NT * j);
-        }
+        for (int j = 0; j < CPT; j++)
+          pos[j] = bcnt[wa[j] != kUnset ? wa[j] & 0xFFFFu : 0u] + (wb[j] & 0xFFFFu);
+#pragma unroll
+        for (int j = 0; j < CPT; j++)
+          if (wa[j] != kUnset) e64[pos[j]] = ((uint64_t)pl[j] << 32) | (uint32_t)(tid + NT * j);
+      }
       __syncthreads();
       // ---- D. order inside buckets by (priority, chunk); record each send's
       //      link and its index in the link's run -----------------------------
@@ -637,14 +639,14 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
         uint32_t nmax = 0;
 #pragma unroll
         for (int j = 0; j < CPT; j++) {
-          b0[j] = nb[j] = rs[j] = rank[j] = 0;
+          const bool act = wa[j] != kUnset;
+          const uint32_t b = act ? wa[j] & 0xFFFFu : 0u;
+          b0[j] = bcnt[b];
+          const uint32_t b1 = bcnt[b + 1];
+          rs[j] = bcnt[act ? wa[j] >> 16 : 0u];
+          nb[j] = act ? b1 - b0[j] : 0u;
+          rank[j] = 0;
           me[j] = ((uint64_t)pl[j] << 32) | (uint32_t)(tid + NT * j);
-          if (wa[j] != kUnset) {
-            const uint32_t b = wa[j] & 0xFFFFu;
-            b0[j] = bcnt[b];
-            nb[j] = bcnt[b + 1] - b0[j];
-            rs[j] = bcnt[wa[j] >> 16];
-          }
           nmax = max(nmax, nb[j]);
         }
         // the members of all this thread's buckets are read together, one
@@ -798,7 +800,9 @@ int32_t path_fast_layout(const taccl_plan &p, PathArgs &a) {
   a.o_flcb = take(4 * (p.nlev + 1));
   a.o_fctime = take(4 * C);
   a.o_flfree = take(8 * E);
-  a.o_fbcnt = take(4 * (p.max_lvl_nb + 1));
+  // bucket counters, the level's total, and one dummy counter per lane of a
+  // wavefront (slots without a send count there)
+  a.o_fbcnt = take(4 * (p.max_lvl_nb + 1 + 64));
   a.o_fepr = take(8 * M);
   a.o_fech = 0;
   a.o_fsrt = take(4 * path_fast_threads(p) * path_fast_cpt(p));
