@@ -405,67 +405,100 @@ __device__ __forceinline__ void slot_trees(const TreeArgs &a, const TreeLds &tl,
   const uint32_t *rt32 = tl.rt32;
   uint32_t *dist = tl.dist;
   uint16_t *anc = tl.anc;
-  // The parent hop of every slot, straight-line code (selects instead of
-  // branches) so the LDS loads of all slots can be in flight together.
+  // The parent hop of every slot, in groups of (up to) four slots and in
+  // stages, each stage issuing the LDS loads of the whole group before any
+  // is used (selects instead of branches).
   uint32_t ec[J];          // cost of the link into the slot
   uint32_t an[J], acc[J];  // 2^k-th ancestor slot, cost of the path up to it
+  constexpr int G = J < 4 ? J : 4;
 #pragma unroll
-  for (int j = 0; j < J; j++) {
-    const uint32_t sl = lane + 64 * j;
-    const bool in = sl < (uint32_t)CV;
-    const uint32_t slc = in ? sl : 0u;
-    const uint32_t c = div_v(slc, a.vmagic), v = slc - c * V;
-    const uint32_t o = s_own[c];
-    const uint64_t pm = s_post[c];
+  for (int g0 = 0; g0 < J; g0 += G) {
+    uint32_t c[G], v[G], o[G], slc[G];
+    uint64_t pm[G];
+#pragma unroll
+    for (int q = 0; q < G; q++) {
+      const uint32_t sl = lane + 64 * (g0 + q);
+      slc[q] = sl < (uint32_t)CV ? sl : 0u;
+      c[q] = div_v(slc[q], a.vmagic);
+      v[q] = slc[q] - c[q] * V;
+    }
+#pragma unroll
+    for (int q = 0; q < G; q++) {
+      o[q] = s_own[c[q]];
+      pm[q] = s_post[c[q]];
+    }
     // (chosen option bit & options through v), one byte per destination
     // (destinations outside the postcondition were zeroed when staged): its
-    // lowest set bit is byte 4w + b of the smallest destination d whose drawn
-    // path passes through v, and the bit inside the byte is that path's
-    // option kd
-    uint32_t t[PW];
+    // lowest set bit is byte 4w + b of the smallest destination d whose
+    // drawn path passes through v, and the bit inside the byte is that
+    // path's option kd
+    uint32_t t[G][PW];
 #pragma unroll
-    for (int w = 0; w < PW; w++) t[w] = rt32[c * PW + w] & s_opt[(o * V + v) * PW + w];
-    uint32_t tw = t[PW - 1], wi = PW - 1;
+    for (int q = 0; q < G; q++)
 #pragma unroll
-    for (int w = PW - 2; w >= 0; w--)
-      if (t[w]) {
-        tw = t[w];
-        wi = w;
+      for (int w = 0; w < PW; w++)
+        t[q][w] = rt32[c[q] * PW + w] & s_opt[(o[q] * V + v[q]) * PW + w];
+    uint32_t d[G], kd[G];
+    bool has[G];
+#pragma unroll
+    for (int q = 0; q < G; q++) {
+      uint32_t tw = t[q][PW - 1], wi = PW - 1;
+#pragma unroll
+      for (int w = PW - 2; w >= 0; w--)
+        if (t[q][w]) {
+          tw = t[q][w];
+          wi = w;
+        }
+      const bool in = lane + 64 * (g0 + q) < (uint32_t)CV;
+      const bool root = v[q] == o[q];
+      has[q] = in && !root && tw != 0;
+      bad |= in && !root && tw == 0 && ((pm[q] >> v[q]) & 1);  // a rank is never reached
+      const uint32_t bit = tw ? (uint32_t)__builtin_ctz(tw) : 0u;
+      d[q] = 4 * wi + (bit >> 3);
+      kd[q] = bit & 7;
+    }
+    uint4 r[G];
+#pragma unroll
+    for (int q = 0; q < G; q++) r[q] = s_rec[(o[q] * P + d[q]) * K + kd[q]];
+    uint32_t l[G], u[G];
+#pragma unroll
+    for (int q = 0; q < G; q++) {
+      // the hop of that path that enters v
+      const uint32_t x0 = r[q].x & 0xFFFFFFu, x1 = r[q].y, x2 = r[q].z, x3 = r[q].w;
+      uint32_t e = x3, uu = (x2 >> 16) & 0xFFu;
+      if (((x2 >> 16) & 0xFFu) == v[q]) {
+        e = x2;
+        uu = (x1 >> 16) & 0xFFu;
       }
-    const bool root = v == o;
-    const bool has = in && !root && tw != 0;
-    bad |= in && !root && tw == 0 && ((pm >> v) & 1);  // a rank is never reached
-    const uint32_t bit = tw ? (uint32_t)__builtin_ctz(tw) : 0u;
-    const uint32_t d = 4 * wi + (bit >> 3), kd = bit & 7;
-    const uint4 r = s_rec[(o * P + d) * K + kd];
-    // the hop of that path that enters v
-    const uint32_t x0 = r.x & 0xFFFFFFu, x1 = r.y, x2 = r.z, x3 = r.w;
-    uint32_t e = x3, u = (x2 >> 16) & 0xFFu;
-    if (((x2 >> 16) & 0xFFu) == v) {
-      e = x2;
-      u = (x1 >> 16) & 0xFFu;
+      if (((x1 >> 16) & 0xFFu) == v[q]) {
+        e = x1;
+        uu = (x0 >> 16) & 0xFFu;
+      }
+      if ((x0 >> 16) == v[q]) {
+        e = x0;
+        uu = o[q];
+      }
+      l[q] = e & 0xFFFFu;
+      u[q] = uu;
     }
-    if (((x1 >> 16) & 0xFFu) == v) {
-      e = x1;
-      u = (x0 >> 16) & 0xFFu;
-    }
-    if ((x0 >> 16) == v) {
-      e = x0;
-      u = o;
-    }
-    const uint32_t l = e & 0xFFFFu;
     // ReduceScatter measures the tree backwards, on reverse links
-    ec[j] = s_cost[has ? (kRS ? s_rev[l] : l) : 0u];
-    const bool top = u == o;  // the parent is the chunk's owner
-    pe[j] = has ? (l | (u << 16)) : ~0u;
-    ps[j] = (has && !top) ? c * V + u : kNoPred;
-    // ancestor chain: the parent's slot; the owner's slot (and a slot
-    // without a send) is its own ancestor, with distance 0
-    an[j] = has ? (top ? c * V + o : c * V + u) : slc;
-    acc[j] = has ? ec[j] : 0u;
-    if (in) {
-      dist[sl] = acc[j];
-      anc[sl] = (uint16_t)an[j];
+#pragma unroll
+    for (int q = 0; q < G; q++) ec[g0 + q] = s_cost[has[q] ? (kRS ? s_rev[l[q]] : l[q]) : 0u];
+#pragma unroll
+    for (int q = 0; q < G; q++) {
+      const int j = g0 + q;
+      const bool top = u[q] == o[q];  // the parent is the chunk's owner
+      pe[j] = has[q] ? (l[q] | (u[q] << 16)) : ~0u;
+      ps[j] = (has[q] && !top) ? c[q] * V + u[q] : kNoPred;
+      // ancestor chain: the parent's slot; the owner's slot (and a slot
+      // without a send) is its own ancestor, with distance 0
+      an[j] = has[q] ? (top ? c[q] * V + o[q] : c[q] * V + u[q]) : slc[q];
+      acc[j] = has[q] ? ec[j] : 0u;
+      const uint32_t sl = lane + 64 * j;
+      if (sl < (uint32_t)CV) {
+        dist[sl] = acc[j];
+        anc[sl] = (uint16_t)an[j];
+      }
     }
   }
   wave_sync();
@@ -672,26 +705,38 @@ void tree_layers_kernel(TreeArgs a) {
     uint64_t kk[J];
     uint64_t lm = 0;
     bool clamped = false;
+    {
+      // Allgather: trav = dist(u), rem = cost + height(v) = maxdist_below(v)
+      // - dist(u). ReduceScatter (send v -> u on the reverse link): rem =
+      // reversed distance from v to the owner, trav = longest reversed path
+      // up to v. The loads of all slots first, then the arithmetic.
+      uint32_t lk[J], cl[J], dd[J];
 #pragma unroll
-    for (int j = 0; j < J; j++) {
-      bl[j] = ~0u;
-      kk[j] = 0;
-      if (pe[j] != ~0u) {
-        // Allgather: trav = dist(u), rem = cost + height(v) = maxdist_below(v)
-        // - dist(u). ReduceScatter (send v -> u on the reverse link): rem =
-        // reversed distance from v to the owner, trav = longest reversed path
-        // up to v
-        const uint32_t l = kRS ? s_rev[pe[j] & 0xFFFFu] : pe[j] & 0xFFFFu;
-        const uint32_t trav = kRS ? lds_get(&dist[lane + 64 * j]) : dv[j] - s_cost[l];
-        const uint32_t rem = kRS ? dv[j] : lds_get(&dist[lane + 64 * j]) - trav;
-        uint32_t L = (uint32_t)(((uint64_t)rem * a.lmagic) >> 32);
-        if (L >= (uint32_t)a.nl_max) {  // unreachable: rem is bounded at plan time
-          L = a.nl_max - 1;
-          clamped = true;
+      for (int j = 0; j < J; j++) {
+        const bool has = pe[j] != ~0u;
+        const uint32_t l0 = has ? pe[j] & 0xFFFFu : 0u;
+        lk[j] = kRS ? (has ? s_rev[l0] : 0u) : l0;
+        const uint32_t sl = lane + 64 * j;
+        dd[j] = dist[sl < (uint32_t)CV ? sl : 0u];
+      }
+#pragma unroll
+      for (int j = 0; j < J; j++) cl[j] = kRS ? 0u : s_cost[lk[j]];
+#pragma unroll
+      for (int j = 0; j < J; j++) {
+        bl[j] = ~0u;
+        kk[j] = 0;
+        if (pe[j] != ~0u) {
+          const uint32_t trav = kRS ? dd[j] : dv[j] - cl[j];
+          const uint32_t rem = kRS ? dv[j] : dd[j] - trav;
+          uint32_t L = (uint32_t)(((uint64_t)rem * a.lmagic) >> 32);
+          if (L >= (uint32_t)a.nl_max) {  // unreachable: rem is bounded at plan time
+            L = a.nl_max - 1;
+            clamped = true;
+          }
+          bl[j] = lk[j] | (L << 16);
+          kk[j] = ((uint64_t)(~rem) << 32) | trav;  // ascending = rem desc, trav asc
+          lm |= 1ull << L;
         }
-        bl[j] = l | (L << 16);
-        kk[j] = ((uint64_t)(~rem) << 32) | trav;  // ascending = rem desc, trav asc
-        lm |= 1ull << L;
       }
     }
     if (lm) atomicOr((unsigned long long *)lmask64, (unsigned long long)lm);
@@ -704,20 +749,19 @@ void tree_layers_kernel(TreeArgs a) {
     wave_sync();
 
     // ---- counting sort by (layer from the top, link) ---------------------
+    // a slot without a send counts in a per-lane dummy word past the
+    // counters, so every slot issues its update without a branch
     uint32_t bb[J], idx[J];
 #pragma unroll
     for (int k = 0; k < J; k++) {
-      bb[k] = 0;
-      idx[k] = 0;
-      if (bl[k] != ~0u) {
-        const uint32_t L = bl[k] >> 16;
-        const uint32_t above = (uint32_t)__popcll((layers >> L) >> 1);
-        const uint32_t b = above * E + (bl[k] & 0xFFFFu);
-        const uint32_t sh = (b & 1) << 4;
-        const uint32_t old = atomicAdd(&cnt[b >> 1], 1u << sh);
-        bb[k] = b;
-        idx[k] = (old >> sh) & 0xFFFFu;
-      }
+      const bool has = bl[k] != ~0u;
+      const uint32_t L = (bl[k] >> 16) & 63u;
+      const uint32_t above = (uint32_t)__popcll((layers >> L) >> 1);
+      const uint32_t b = above * E + (bl[k] & 0xFFFFu);
+      const uint32_t sh = (b & 1) << 4;
+      const uint32_t old = atomicAdd(&cnt[has ? b >> 1 : (uint32_t)NW + lane], 1u << sh);
+      bb[k] = has ? b : 0u;
+      idx[k] = (old >> sh) & 0xFFFFu;
     }
     wave_sync();
     {
@@ -742,11 +786,8 @@ void tree_layers_kernel(TreeArgs a) {
     uint32_t b0[J], b1[J];
 #pragma unroll
     for (int k = 0; k < J; k++) {
-      b0[k] = b1[k] = 0;
-      if (bl[k] != ~0u) {
-        b0[k] = start_of(bb[k]);
-        b1[k] = start_of(bb[k] + 1);
-      }
+      b0[k] = start_of(bb[k]);
+      b1[k] = start_of(bb[k] + 1);
     }
     for (int ly = lane; ly <= nl; ly += 64) lst[ly] = start_of((uint32_t)ly * E);
     wave_sync();  // the counters are dead from here on
@@ -1298,7 +1339,9 @@ int32_t tree_layers_layout(const taccl_plan &p, TreeArgs &a) {
   a.w_ord2 = x;
   a.w_info2 = x + align16(4 * S);
   a.w_bnd = x + 2 * align16(4 * S);
-  int32_t w = x + std::max(align16(4 * (int32_t)((nl * E + 2) / 2)), 3 * align16(4 * S));
+  // counters: u16 pairs for nl_max * E + 1 bucket starts, then one dummy
+  // word per lane (slots without a send count there)
+  int32_t w = x + std::max(align16(4 * (int32_t)((nl * E + 2) / 2 + 64)), 3 * align16(4 * S));
   a.w_free = w;
   w = align16(w + 4 * E);
   a.w_lmask = w;
