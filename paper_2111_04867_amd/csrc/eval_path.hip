@@ -165,36 +165,138 @@ __device__ uint32_t ports_level(const PathArgs &a, int L, const uint32_t *gpr, u
     }
   }
   __syncthreads();
-  // send-port passes until the finishes settle
-  for (int pass = 0;; pass++) {
-    bool changed = false;
-    for (int l = tid; l < E; l += nt) {
-      const uint32_t cb = a.llc[((size_t)L * E + l) * 2], ce = a.llc[((size_t)L * E + l) * 2 + 1];
-      if (cb == ce) continue;
-      const uint32_t xb = ccnt[cb - lo], xe = ccnt[ce - lo];
-      uint32_t f = lfree[l];
-      const uint32_t cl = a.cost[l];
-      for (uint32_t x = xb; x < xe; x++) {
-        const int c = sorted[x];
-        uint32_t r = max(ctime[c], f);
-        if (dl[c] != 0xFFFF)
-          r = max(r, pd[c] == 0xFFFF ? lfree[dl[c]] : lds_get(&fcur[pd[c]]));
-        f = r + cl;
+  // every position of the level's send-port order: its link and its index
+  // in that link's run (one thread per link labels its run)
+  const uint32_t tot = ccnt[a.lvl_cls_begin[L + 1] - lo];
+  uint32_t *pinf = (uint32_t *)(lds + a.o_eprio);  // the send-order staging is dead
+  for (int l = tid; l < E; l += nt) {
+    const uint32_t cb = a.llc[((size_t)L * E + l) * 2], ce = a.llc[((size_t)L * E + l) * 2 + 1];
+    if (cb == ce) continue;
+    const uint32_t xb = ccnt[cb - lo], xe = ccnt[ce - lo];
+    for (uint32_t x = xb; x < xe; x++) pinf[x] = (uint32_t)l | ((x - xb) << 16);
+  }
+  for (int c = tid; c < C; c += nt) fcur[c] = 0;
+  __syncthreads();
+  // Passes until the finishes settle. In a pass every send takes as its
+  // ready time max(arrival of its chunk, current finish of the send before
+  // it on its receive port, or that port's busy time); every send-port run
+  // is then timed in closed form, the k-th send finishing at
+  // (k+1)c + max(F, max_{j<=k}(r_j - j c)): runs lie in ascending link order
+  // along the positions, so one block-wide prefix max over
+  // link << 33 | (r_j - j c + 2^32) serves all runs. Each thread owns a
+  // contiguous range of positions. Finishes start at zero, every update is
+  // monotone and bounded by the least schedule, so a pass that changes
+  // nothing has reached it (reads racing with writes of the same pass see
+  // either value, which keeps both properties).
+  uint64_t *red64 = (uint64_t *)(lds + a.o_fred64);
+  const int lane = tid & 63, wave = tid >> 6;
+  const uint32_t per = (tot + nt - 1) / nt;
+  const uint32_t x0 = min((uint32_t)tid * per, tot), x1 = min(x0 + per, tot);
+  // exclusive prefix max of this thread's aggregate over the block
+  auto block_carry = [&](uint64_t agg) {
+    const uint64_t incl = wave_scan_max64(agg);
+    if (lane == 63) red64[wave] = incl;
+    __syncthreads();
+    uint64_t run = dpp64<kWaveShr1>(incl);
+    const uint64_t wv = row_scan_max64(lane < nt / 64 ? red64[lane] : 0ull);
+    const uint32_t w = (uint32_t)__builtin_amdgcn_readfirstlane(wave);
+    if (w) run = max(run, readlane64(wv, w - 1));
+    return run;
+  };
+  constexpr int kReg = 4;  // positions per thread kept in registers
+  if (per <= kReg) {
+    // the fixed part of every owned position once: chunk, link, index in
+    // the run, cost, send-port busy time, ready time without the receive
+    // port's predecessor, and that predecessor (0xFFFF: none or a port
+    // without one, whose busy time is already in the ready time)
+    uint32_t pc[kReg], pl[kReg], pk[kReg], pcl[kReg], pF[kReg], pr0[kReg], prp[kReg];
+#pragma unroll
+    for (int q = 0; q < kReg; q++) {
+      const uint32_t x = x0 + q < x1 ? x0 + q : 0u;
+      pc[q] = sorted[x];
+      const uint32_t inf = pinf[x];
+      pl[q] = inf & 0xFFFFu;
+      pk[q] = inf >> 16;
+    }
+#pragma unroll
+    for (int q = 0; q < kReg; q++) {
+      pcl[q] = a.cost[pl[q]];
+      pF[q] = lfree[pl[q]];
+      const uint32_t c = pc[q], d = dl[c], pj = pd[c];
+      pr0[q] = ctime[c];
+      prp[q] = 0xFFFF;
+      if (d != 0xFFFF) {
+        if (pj == 0xFFFF) pr0[q] = max(pr0[q], lfree[d]);
+        else prp[q] = pj;
+      }
+    }
+    for (int pass = 0;; pass++) {
+      uint64_t comp[kReg], agg = 0;
+#pragma unroll
+      for (int q = 0; q < kReg; q++) {
+        uint32_t r = pr0[q];
+        const uint32_t fp = lds_get(&fcur[prp[q] != 0xFFFF ? prp[q] : 0u]);
+        if (prp[q] != 0xFFFF) r = max(r, fp);
+        comp[q] = x0 + q < x1 ? ((uint64_t)pl[q] << 33) |
+                                    ((uint64_t)r + (1ull << 32) - (uint64_t)pk[q] * pcl[q])
+                              : 0ull;
+        agg = max(agg, comp[q]);
+      }
+      uint64_t run = block_carry(agg);
+      bool changed = false;
+#pragma unroll
+      for (int q = 0; q < kReg; q++) {
+        run = max(run, comp[q]);
+        const int64_t best =
+            max((int64_t)pF[q], (int64_t)(run & ((1ull << 33) - 1)) - (int64_t)(1ull << 32));
+        const uint32_t f = (uint32_t)((int64_t)(pk[q] + 1) * pcl[q] + best);
+        if (x0 + q < x1 && f != lds_get(&fcur[pc[q]])) {
+          lds_put(&fcur[pc[q]], f);
+          changed = true;
+        }
+      }
+      if (!__syncthreads_or(changed)) break;
+      if (pass > C) {  // unreachable
+        *fault = true;
+        break;
+      }
+    }
+  } else {
+    for (int pass = 0;; pass++) {
+      uint64_t agg = 0;
+      for (uint32_t x = x0; x < x1; x++) {
+        const uint32_t c = sorted[x], inf = pinf[x];
+        const uint32_t l = inf & 0xFFFFu, k = inf >> 16;
+        uint32_t r = ctime[c];
+        if (dl[c] != 0xFFFF) r = max(r, pd[c] == 0xFFFF ? lfree[dl[c]] : lds_get(&fcur[pd[c]]));
+        agg = max(agg, ((uint64_t)l << 33) | ((uint64_t)r + (1ull << 32) - (uint64_t)k * a.cost[l]));
+      }
+      uint64_t run = block_carry(agg);
+      bool changed = false;
+      for (uint32_t x = x0; x < x1; x++) {
+        const uint32_t c = sorted[x], inf = pinf[x];
+        const uint32_t l = inf & 0xFFFFu, k = inf >> 16;
+        const uint32_t cl = a.cost[l];
+        uint32_t r = ctime[c];
+        if (dl[c] != 0xFFFF) r = max(r, pd[c] == 0xFFFF ? lfree[dl[c]] : lds_get(&fcur[pd[c]]));
+        run = max(run, ((uint64_t)l << 33) | ((uint64_t)r + (1ull << 32) - (uint64_t)k * cl));
+        const int64_t best =
+            max((int64_t)lfree[l], (int64_t)(run & ((1ull << 33) - 1)) - (int64_t)(1ull << 32));
+        const uint32_t f = (uint32_t)((int64_t)(k + 1) * cl + best);
         if (f != lds_get(&fcur[c])) {
           lds_put(&fcur[c], f);
           changed = true;
         }
       }
-    }
-    if (!__syncthreads_or(changed)) break;
-    if (pass > C) {  // unreachable
-      *fault = true;
-      break;
+      if (!__syncthreads_or(changed)) break;
+      if (pass > C) {  // unreachable
+        *fault = true;
+        break;
+      }
     }
   }
   // arrivals and port free times after the level
   uint32_t mk = 0;
-  const uint32_t tot = ccnt[a.lvl_cls_begin[L + 1] - lo];
   for (uint32_t x = tid; x < tot; x += nt) {
     const int c = sorted[x];
     ctime[c] = fcur[c];
@@ -218,7 +320,8 @@ __device__ uint32_t ports_level(const PathArgs &a, int L, const uint32_t *gpr, u
   return mk;
 }
 
-__global__ __launch_bounds__(kPathThreads) void path_eval_kernel(PathArgs a) {
+template <int NT>
+__global__ __launch_bounds__(NT) void path_eval_kernel(PathArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   uint8_t *rt = lds + a.o_rt;
   uint32_t *ctime = (uint32_t *)(lds + a.o_ctime);  // chunk's arrival so far
@@ -387,7 +490,7 @@ int32_t path_layout(const taccl_plan &p, PathArgs &a) {
   a.o_eprio = take(4 * M);
   a.o_ecls = take(2 * M);
   a.o_sorted = take(2 * M);
-  a.o_red = take(4 * (kPathThreads / 64));
+  a.o_red = take(4 * (kPathPortThreads / 64));
   if (p.ports) {  // receive-port order and per-chunk state
     const int32_t K2 = std::max(p.max_lvl_cls2, 1);
     a.o_ccnt2 = take(4 * (K2 + 1));
@@ -399,13 +502,23 @@ int32_t path_layout(const taccl_plan &p, PathArgs &a) {
     a.o_fcur = take(4 * C);
     a.o_pd = take(2 * C);
     a.o_dl = take(2 * C);
+    a.o_fred64 = take(8 * (kPathPortThreads / 64));
   }
+  a.lr_threads = (p.ports && p.max_lvl_sends > 4 * kPathThreads) ? kPathPortThreads : kPathThreads;
   a.lds_bytes = off;
   return off;
 }
 
 hipError_t launch_path(const PathArgs &a, int grid, hipStream_t stream) {
-  hipLaunchKernelGGL(path_eval_kernel, dim3(grid), dim3(kPathThreads), a.lds_bytes, stream, a);
+  // switch-port plans whose levels hold more sends than four per thread of
+  // a 256-thread block run 1024-thread blocks (the port passes keep four
+  // positions per thread in registers)
+  if (a.lr_threads == kPathPortThreads)
+    hipLaunchKernelGGL(path_eval_kernel<kPathPortThreads>, dim3(grid), dim3(kPathPortThreads),
+                       a.lds_bytes, stream, a);
+  else
+    hipLaunchKernelGGL(path_eval_kernel<kPathThreads>, dim3(grid), dim3(kPathThreads),
+                       a.lds_bytes, stream, a);
   return hipGetLastError();
 }
 

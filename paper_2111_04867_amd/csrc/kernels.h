@@ -96,6 +96,7 @@ struct PathArgs {
   const uint16_t *hop_class2;
   const uint32_t *lvl_cls2_begin, *llc2;
   int32_t o_ccnt2, o_ccur2, o_echunk2, o_eprio2, o_ecls2, o_sorted2, o_fcur, o_pd, o_dl;
+  int32_t lr_threads;  // block size of the LDS-record kernel for this plan
 };
 
 // Switch-hyperedge connection count: one block per candidate at a time.
@@ -119,6 +120,7 @@ constexpr int kConnMaxThreads = 256;
 constexpr int kTreeMaxThreads = 512;  // up to 8 wavefronts per block
 constexpr int kTreeRecLdsMax = 32768;  // route records kept in LDS up to this size
 constexpr int kPathThreads = 256;
+constexpr int kPathPortThreads = 1024;  // LDS-record kernel on switch-port plans
 constexpr int kPathFastThreads = 1024;  // largest block of the register-resident kernel
 
 // Fill the LDS layout; returns the bytes needed by a one-wavefront block.

@@ -129,3 +129,15 @@ def test_two_switches(per):
     plan, ref, opts = plans(w)
     routes, prio = generate(60 + per, 0, 400, opts, plan.prio_stride)
     check(plan, ref, routes, prio, w.name)
+
+
+@pytest.mark.parametrize("P,cpr,relays", [(48, 2, True), (36, 3, False)])
+def test_large_levels(P, cpr, relays):
+    """Levels of thousands of switched sends in 1024-thread blocks: up to
+    four positions per thread are kept in registers through the port passes
+    (36 ranks, 3 chunks per pair: 3780 sends in one level), more are looped
+    over (48 ranks with relays: up to 4512 sends in the last level)."""
+    w = star(P, relays=relays, cpr=cpr, chunk_bytes=64 * 1024)
+    plan, ref, opts = plans(w)
+    routes, prio = generate(70 + P, 0, 24, opts, plan.prio_stride)
+    check(plan, ref, routes, prio, f"{w.name} cpr={cpr}")
