@@ -854,105 +854,99 @@ void tree_layers_kernel(TreeArgs a) {
     uint32_t mk = 0;
     for (int ly = 0; ly < nl; ly++) {
       const uint32_t qs = lst[ly], qe = lst[ly + 1];
-      if (!kContig) {
-        // Every send's ready time is known (its parent send lies in a layer
-        // above), so the k-th send of a link run with cost c and busy time
-        // F finishes at (k+1)c + max(F, max_{j<=k}(r_j - j c)). The layer's
-        // runs lie in ascending link order, so one plain prefix max over
-        // link << 33 | (r_j - j c + 2^32) gives every position the max over
-        // the earlier sends of its own run (DPP scan, 64 positions a step).
-        uint64_t carry = 0;
-        for (uint32_t base = qs; base < qe; base += 64) {
-          const uint32_t q = base + lane;
-          const bool ok = q < qe;
-          const uint32_t qq = ok ? q : qs;
-          const uint32_t e = ord2[qq], inf = info2[qq];
-          const uint32_t l = inf & 0xFFFFu, k = (inf >> 16) & 0x7FFFu;
-          uint32_t r;
+      if (kContig) {
+        // ready times of the layer's sends, for the walkers below (parent
+        // sends lie in layers above)
+        for (uint32_t q = qs + lane; q < qe; q += 64) {
           if (kRS) {
-            r = fin[e & 0xFFFFu];
+            rq[q] = fin[ord2[q] & 0xFFFFu];
           } else {
-            const uint32_t pj = e >> 16;
-            r = fin[pj == kNoPred ? 0u : pj];
-            if (pj == kNoPred) r = 0;
-          }
-          const uint32_t cl = s_cost[l], F = lfree[l];
-          const uint32_t kn = (q + 1 < qe) ? ((info2[q + 1] >> 16) & 0x7FFFu) : 0u;
-          const uint64_t comp =
-              ok ? (((uint64_t)l << 33) | ((uint64_t)r + (1ull << 32) - (uint64_t)k * cl)) : 0ull;
-          const uint64_t incl = max(wave_scan_max64(comp), carry);
-          carry = readlane64(incl, 63);
-          const int64_t best =
-              max((int64_t)F, (int64_t)(incl & ((1ull << 33) - 1)) - (int64_t)(1ull << 32));
-          const uint32_t f = (uint32_t)((int64_t)(k + 1) * cl + best);
-          if (ok) {
-            finish(e, f);
-            mk = max(mk, f);
-            if (kn == 0) lfree[l] = f;  // the run's last send
+            const uint32_t pj = ord2[q] >> 16;
+            rq[q] = (pj == kNoPred) ? 0u : fin[pj];
           }
         }
         wave_sync();
-        continue;
       }
-      // ready time of every send of the layer: its parent send is in a
-      // layer above
-      for (uint32_t q = qs + lane; q < qe; q += 64) {
-        if (kRS) {
-          rq[q] = fin[ord2[q] & 0xFFFFu];
-        } else {
-          const uint32_t pj = ord2[q] >> 16;
-          rq[q] = (pj == kNoPred) ? 0u : fin[pj];
-        }
-      }
-      wave_sync();
-      for (uint32_t q = qs + lane; q < qe; q += 64) {
-        const uint32_t inf = info2[q];
+      // Every send's ready time is known (its parent send lies in a layer
+      // above), so the k-th send of a link run with cost c and busy time F
+      // finishes at (k+1)c + max(F, max_{j<=k}(r_j - j c)). The layer's runs
+      // lie in ascending link order, so one plain prefix max over
+      // link << 33 | (r_j - j c + 2^32) gives every position the max over the
+      // earlier sends of its own run (DPP scan, 64 positions a step). Runs
+      // on links that carry contiguous transfers are walked instead.
+      uint64_t carry = 0;
+      for (uint32_t base = qs; base < qe; base += 64) {
+        const uint32_t q = base + lane;
+        const bool ok = q < qe;
+        const uint32_t qq = ok ? q : qs;
+        const uint32_t e = ord2[qq], inf = info2[qq];
         const uint32_t l = inf & 0xFFFFu, k = (inf >> 16) & 0x7FFFu;
-        const uint32_t cl = s_cost[l];
-        if (kContig && s_merge[l]) {
+        uint32_t r;
+        if (kRS) {
+          r = fin[e & 0xFFFFu];
+        } else {
+          const uint32_t pj = e >> 16;
+          r = fin[pj == kNoPred ? 0u : pj];
+          if (pj == kNoPred) r = 0;
+        }
+        const uint32_t cl = s_cost[l], F = lfree[l];
+        const uint32_t kn = (q + 1 < qe) ? ((info2[q + 1] >> 16) & 0x7FFFu) : 0u;
+        const uint64_t comp =
+            ok ? (((uint64_t)l << 33) | ((uint64_t)r + (1ull << 32) - (uint64_t)k * cl)) : 0ull;
+        const uint64_t incl = max(wave_scan_max64(comp), carry);
+        carry = readlane64(incl, 63);
+        const int64_t best =
+            max((int64_t)F, (int64_t)(incl & ((1ull << 33) - 1)) - (int64_t)(1ull << 32));
+        const uint32_t f = (uint32_t)((int64_t)(k + 1) * cl + best);
+        const bool merge = kContig && s_merge[l];
+        if (ok && !merge) {
+          finish(e, f);
+          mk = max(mk, f);
+          if (kn == 0) lfree[l] = f;  // the run's last send
+        }
+        if (ok && merge && k == 0) {
           // contiguous transfers: the run's first lane walks the run; a send
           // joins the open transfer when its remaining length equals the
-          // previous send's and its chunk was ready when the transfer started
-          if (k != 0) continue;
+          // previous send's and its chunk was ready when the transfer
+          // started
           const uint32_t al = a.lalpha[l];
           const uint64_t bsz = a.lbs[l];
-          uint32_t F = lfree[l], gs = 0, gm = 0, g0 = q;
-          for (uint32_t j = q;; j++) {
-            const bool end = j == qe || (j > q && ((info2[j] >> 16) & 0x7FFFu) == 0);
-            const bool join = !end && gm > 0 && (info2[j] >> 31) && rq[j] <= gs;
-            if (gm > 0 && !join) {  // close the open transfer
-              const uint32_t f = gs + al + (uint32_t)((bsz * gm + 999) / 1000);
-              for (uint32_t t = g0; t < g0 + gm; t++) finish(ord2[t], f);
-              F = f;
-              mk = max(mk, f);
+          uint32_t Fw = F, gs = 0, gm = 0, g0 = q;
+          bool done = false;
+          // the run's entries are read four at a time (clamped to the layer)
+          for (uint32_t j0 = q; !done; j0 += 4) {
+            uint32_t inf4[4], r4[4];
+#pragma unroll
+            for (int u = 0; u < 4; u++) {
+              const uint32_t jj = min(j0 + u, qe - 1);
+              inf4[u] = info2[jj];
+              r4[u] = rq[jj];
             }
-            if (end) break;
-            if (join) {
-              gm++;
-            } else {
-              gs = max(F, rq[j]);
-              gm = 1;
-              g0 = j;
+#pragma unroll
+            for (int u = 0; u < 4; u++) {
+              if (done) break;
+              const uint32_t j = j0 + u;
+              const bool end = j >= qe || (j > q && ((inf4[u] >> 16) & 0x7FFFu) == 0);
+              const bool join = !end && gm > 0 && (inf4[u] >> 31) && r4[u] <= gs;
+              if (gm > 0 && !join) {  // close the open transfer
+                const uint32_t fw = gs + al + (uint32_t)((bsz * gm + 999) / 1000);
+                for (uint32_t t = g0; t < g0 + gm; t++) finish(ord2[t], fw);
+                Fw = fw;
+                mk = max(mk, fw);
+              }
+              if (end) {
+                done = true;
+              } else if (join) {
+                gm++;
+              } else {
+                gs = max(Fw, r4[u]);
+                gm = 1;
+                g0 = j;
+              }
             }
           }
-          lfree[l] = F;
-          continue;
+          lfree[l] = Fw;
         }
-        uint32_t f = lfree[l] + (k + 1) * cl;
-        // earlier sends of the run, four at a time
-        for (uint32_t j = q - k; j <= q; j += 4) {
-          uint32_t r[4];
-#pragma unroll
-          for (int t = 0; t < 4; t++) r[t] = rq[min(j + t, q)];
-#pragma unroll
-          for (int t = 0; t < 4; t++) {
-            const uint32_t jt = min(j + t, q);  // a repeat of q adds nothing new
-            f = max(f, r[t] + (q - jt + 1) * cl);
-          }
-        }
-        finish(ord2[q], f);
-        mk = max(mk, f);
-        if (q + 1 == qe || ((info2[q + 1] >> 16) & 0x7FFFu) == 0) lfree[l] = f;
       }
       wave_sync();
     }
