@@ -1016,14 +1016,15 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_greedy_kernel(TreeArgs a
   uint32_t *rt32 = (uint32_t *)wl;
   uint32_t *dist = (uint32_t *)(wl + a.w_dist);
   uint16_t *anc = (uint16_t *)(wl + a.w_anc);
-  uint64_t *gkey = (uint64_t *)(wl + a.w_gkey);  // per slot: ~rem << 32 | trav
-  uint32_t *gpri = (uint32_t *)(wl + a.w_gpri);  // per slot: priority
-  uint32_t *glp = (uint32_t *)(wl + a.w_glp);    // per slot: link | other slot << 16
   uint32_t *gfin = (uint32_t *)(wl + a.w_gfin);  // per slot: finish, kNotYet before
   uint32_t *grdy = (uint32_t *)(wl + a.w_grdy);  // ReduceScatter: ready so far
   uint32_t *gpend = (uint32_t *)(wl + a.w_gpend);  // ReduceScatter: unscheduled inputs
-  uint16_t *glist = (uint16_t *)(wl + a.w_glist);  // sends grouped by link
-  uint32_t *gofs = (uint32_t *)(wl + a.w_gofs);    // [E + 1] first list entry per link
+  // pending sends grouped by link, one 16-byte record each: {key lo, key hi
+  // (~rem << 32 | trav), priority, slot | other slot << 16} where the other
+  // slot is the send that brings the chunk (Allgather) or carries the partial
+  // on (ReduceScatter)
+  uint4 *grec = (uint4 *)(wl + a.w_glist);
+  uint32_t *gofs = (uint32_t *)(wl + a.w_gofs);  // [E + 1] first list entry per link
 
   const int64_t stride = (int64_t)gridDim.x * a.waves_per_block;
   const int64_t first = (int64_t)blockIdx.x * a.waves_per_block + wave;
@@ -1065,10 +1066,13 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_greedy_kernel(TreeArgs a
 
     // ---- per-slot send records; sends counted per link ------------------
     uint32_t lk[J], idx[J];
+    uint64_t kk[J];
 #pragma unroll
     for (int j = 0; j < J; j++) {
       const uint32_t sl = lane + 64 * j;
       lk[j] = ~0u;
+      kk[j] = 0;
+      idx[j] = 0;
       if (sl < (uint32_t)CV) {
         gfin[sl] = kNotYet;
         if (kRS) {
@@ -1082,11 +1086,7 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_greedy_kernel(TreeArgs a
         const uint32_t trav = kRS ? lds_get(&dist[sl]) : dv[j] - s_cost[l];
         const uint32_t rem = kRS ? dv[j] : lds_get(&dist[sl]) - trav;
         lk[j] = l;
-        gkey[sl] = ((uint64_t)(~rem) << 32) | trav;
-        gpri[sl] = px[j];
-        // Allgather: the slot whose send brings the chunk here; ReduceScatter:
-        // the slot whose send carries this partial on
-        glp[sl] = l | (ps[j] << 16);
+        kk[j] = ((uint64_t)(~rem) << 32) | trav;
         idx[j] = atomicAdd(&gofs[l + 1], 1u);
       }
     }
@@ -1113,7 +1113,9 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_greedy_kernel(TreeArgs a
     wave_sync();
 #pragma unroll
     for (int j = 0; j < J; j++)
-      if (lk[j] != ~0u) glist[gofs[lk[j]] + idx[j]] = (uint16_t)(lane + 64 * j);
+      if (lk[j] != ~0u)
+        grec[gofs[lk[j]] + idx[j]] = make_uint4((uint32_t)kk[j], (uint32_t)(kk[j] >> 32), px[j],
+                                                (lane + 64 * j) | (ps[j] << 16));
     wave_sync();
 
     // ---- the greedy, window by window ------------------------------------
@@ -1135,29 +1137,40 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_greedy_kernel(TreeArgs a
         cq[t] = 0;
         uint64_t bk = ~0ull;
         uint64_t bq = ~0ull;
-        for (uint32_t q = 0; q < ln[t]; q++) {
-          const uint32_t x = glist[lb[t] + q];
-          const uint32_t other = glp[x] >> 16;
-          uint32_t r;
-          if (kRS) {
-            r = (gpend[x] == 0) ? grdy[x] : kNotYet;
-          } else {
-            r = (other == kNoPred) ? 0u : gfin[other];
+        // two pending sends per step: their records, then their ready times
+        for (uint32_t q0 = 0; q0 < ln[t]; q0 += 2) {
+          uint4 rc[2];
+          uint32_t r[2];
+#pragma unroll
+          for (int u = 0; u < 2; u++) rc[u] = grec[lb[t] + min(q0 + u, ln[t] - 1)];
+#pragma unroll
+          for (int u = 0; u < 2; u++) {
+            const uint32_t x = rc[u].w & 0xFFFFu, other = rc[u].w >> 16;
+            if (kRS) {
+              const uint32_t pend = gpend[x], rd = grdy[x];
+              r[u] = pend == 0 ? rd : kNotYet;
+            } else {
+              const uint32_t fo = gfin[other == kNoPred ? 0u : other];
+              r[u] = other == kNoPred ? 0u : fo;
+            }
           }
-          if (r == kNotYet) continue;  // its chunk has not arrived yet
-          const uint32_t st = max(lf[t], r);
-          const uint64_t kx = gkey[x];
-          const uint64_t qx = ((uint64_t)gpri[x] << 32) | x;  // priority, then chunk
-          if (st < cs[t] || (st == cs[t] && (kx < bk || (kx == bk && qx < bq)))) {
-            cs[t] = st;
-            cq[t] = q;
-            bk = kx;
-            bq = qx;
+#pragma unroll
+          for (int u = 0; u < 2; u++) {
+            if (q0 + u >= ln[t] || r[u] == kNotYet) continue;  // its chunk has not arrived yet
+            const uint32_t st = max(lf[t], r[u]);
+            const uint64_t kx = ((uint64_t)rc[u].y << 32) | rc[u].x;
+            const uint64_t qx = ((uint64_t)rc[u].z << 32) | (rc[u].w & 0xFFFFu);  // priority, then chunk
+            if (st < cs[t] || (st == cs[t] && (kx < bk || (kx == bk && qx < bq)))) {
+              cs[t] = st;
+              cq[t] = q0 + u;
+              bk = kx;
+              bq = qx;
+            }
           }
         }
         wmin = min(wmin, cs[t]);
       }
-      for (int o = 32; o > 0; o >>= 1) wmin = min(wmin, (uint32_t)__shfl_xor((int)wmin, o));
+      wmin = ~wave_reduce_max(~wmin);
       if (wmin == kNotYet) break;  // nothing left to schedule
       if (round > CV) {  // unreachable: every window commits a send
         fault = true;
@@ -1169,10 +1182,11 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_greedy_kernel(TreeArgs a
       for (int t = 0; t < kGreedyLinkSlots; t++) {
         if (cs[t] != kNotYet && (uint64_t)cs[t] < wend) {
           const int l = lane + 64 * t;
-          const uint32_t x = glist[lb[t] + cq[t]];
+          const uint4 rc = grec[lb[t] + cq[t]];
+          const uint32_t x = rc.w & 0xFFFFu;
           const uint32_t f = cs[t] + s_cost[l];
           if (kRS) {
-            const uint32_t nxt = glp[x] >> 16;
+            const uint32_t nxt = rc.w >> 16;
             if (nxt != kNoPred) {
               atomicMax(&grdy[nxt], f);
               atomicSub(&gpend[nxt], 1u);
@@ -1181,7 +1195,7 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_greedy_kernel(TreeArgs a
           gfin[x] = f;
           lf[t] = f;
           mk = max(mk, f);
-          glist[lb[t] + cq[t]] = glist[lb[t] + ln[t] - 1];
+          grec[lb[t] + cq[t]] = grec[lb[t] + ln[t] - 1];
           ln[t]--;
         }
       }
@@ -1408,18 +1422,14 @@ int32_t tree_greedy_layout(const taccl_plan &p, TreeArgs &a) {
   a.w_rt = wtake(p.route_stride);
   a.w_dist = wtake(4 * CV);
   set_pj(a, V, CV);
-  // the ancestor arrays die with the trees, before the keys, priorities and
-  // link records of the slots (at most 6 * align16(2 CV) <= 16 CV bytes)
-  a.w_anc = w;
-  a.w_gkey = wtake(8 * CV);
-  a.w_gpri = wtake(4 * CV);
-  a.w_glp = wtake(4 * CV);
-  w = std::max(w, align16(a.w_anc + a.pj_rounds * align16(2 * CV)));
   a.w_gfin = wtake(4 * CV);
   a.w_grdy = wtake(4 * CV);
   a.w_gpend = wtake(4 * CV);
-  a.w_glist = wtake(2 * S);
   a.w_gofs = wtake(4 * (E + 1));
+  // the ancestor arrays die with the trees, before the pending-send records
+  // are written
+  a.w_anc = w;
+  a.w_glist = wtake(std::max(16 * S, a.pj_rounds * align16(2 * CV)));
   a.wave_bytes = w;
   return a.o_wave + a.wave_bytes;
 }
