@@ -152,8 +152,9 @@ void taccl_collective_destroy(taccl_collective_t coll);
  *     next, ties broken by the Step-2 key. Not combined with contiguity
  *     (INVALID_ARGUMENT). On the GPU it is evaluated for multicast
  *     collectives (Allgather, explicit, ReduceScatter, Allreduce) on plans
- *     with at most 256 links that fit the layered kernel; Alltoall plans and
- *     others are refused at evaluation (UNSUPPORTED);
+ *     with at most 256 links that fit the layered kernel, and for Alltoall
+ *     plans with at most 256 links and 1024 send slots (chunks x longest
+ *     route option); other plans are refused at evaluation (UNSUPPORTED);
  *   switch_ports (Alltoall only): 0 = a switch vertex stores and forwards
  *     (uplink, then downlink, each one latency); 1 = the switch model of
  *     App. B.3: a hop pair rank -> switch -> rank is one send costing one

@@ -140,9 +140,51 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
   const int64_t cap = (int64_t)std::max(t->num_cus, 1) * 64;
   const int grid = (int)std::min<int64_t>(n, cap);
   hipError_t e;
-  if (p->coll.kind == TACCL_ALLTOALL && p->greedy)
-    return fail(TACCL_ERR_UNSUPPORTED, "time-aware greedy orders are evaluated for multicast "
-                                       "collectives only");
+  if (p->coll.kind == TACCL_ALLTOALL && p->greedy) {
+    PathGreedyArgs g{};
+    if (path_greedy_layout(*p, g) <= 0 || g.o_wave + g.wave_bytes > t->max_lds)
+      return fail(TACCL_ERR_UNSUPPORTED,
+                  "time-aware greedy orders for Alltoall need at most 1024 send slots "
+                  "(chunks x longest path) and 256 links");
+    g.C = p->coll.C;
+    g.P = p->topo.P;
+    g.E = p->topo.E;
+    g.H = std::max(p->H, 1);
+    g.cpr = std::max(p->coll.cpr, 1);
+    g.route_stride = p->route_stride;
+    g.prio_stride = p->prio_stride;
+    g.cost = t->cost;
+    g.pair_base = t->pair_base;
+    g.npaths = t->npaths;
+    g.path_off = t->path_off;
+    g.path_links = t->path_links;
+    g.routes = d_routes;
+    g.prio = d_prio;
+    g.makespan = d_makespan;
+    g.valid = d_valid;
+    g.n = n;
+    // wavefronts per block: most resident wavefronts per CU
+    int best_w = 1, best_res = 0, best_bpc = 1;
+    for (int w = 1; w <= kTreeMaxThreads / 64; w++) {
+      const int bytes = g.o_wave + w * g.wave_bytes;
+      if (bytes > t->max_lds) break;
+      g.waves_per_block = w;
+      int bpc = std::min(t->lds_per_cu / bytes, 32 / w);
+      const int nb = path_greedy_blocks_per_cu(g);
+      if (nb > 0) bpc = std::min(bpc, nb);
+      if (bpc * w > best_res) {
+        best_res = bpc * w;
+        best_w = w;
+        best_bpc = bpc;
+      }
+    }
+    g.waves_per_block = best_w;
+    const int64_t want = (n + best_w - 1) / best_w;
+    const int ggrid = (int)std::min<int64_t>(want, (int64_t)std::max(t->num_cus, 1) * best_bpc);
+    e = launch_path_greedy(g, ggrid, s);
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+    return TACCL_OK;
+  }
   if (p->coll.kind == TACCL_ALLTOALL) {
     PathArgs a{};
     a.C = p->coll.C;

@@ -971,6 +971,206 @@ void tree_layers_kernel(TreeArgs a) {
 
 constexpr int kGreedyLinkSlots = 4;  // links per lane: at most 256 links
 
+// The time-aware greedy of App. B.2 over per-link lists of pending sends,
+// simulated exactly in windows: W = the earliest start any ready send can
+// take; a send whose chunk has not arrived can only become ready at least
+// c_min (the smallest link cost) after W, so on every link the best ready
+// send by (start, Step-2 key, priority, slot) with start < W + c_min is the
+// greedy's next send there, and all of them are committed at once. One
+// lane holds up to four links; committed sends are swap-removed. Records:
+// {key lo, key hi (~rem << 32 | trav), priority, slot | other slot << 16},
+// the other slot being the send the chunk arrives by (its finish is the
+// ready time; kNoPred: ready at 0) or, for ReduceScatter, the send that
+// carries the partial on (ready once every input is scheduled). gfin[slot]
+// must be kNotYet for every pending send. The Alltoall kernel calls it out of
+// line; the multicast kernel carries the same loop inline (inlining this
+// function into either kernel gave results that failed the parity tests,
+// while the out-of-line call and the kernel's own inline loop pass them).
+template <bool kRS>
+__device__ __noinline__ void greedy_windows(int E, int lane, int nslots, uint32_t cmin,
+                                               const uint32_t *s_cost, uint4 *grec,
+                                               const uint32_t *gofs, uint32_t *gfin,
+                                               uint32_t *grdy, uint32_t *gpend, uint32_t &mk,
+                                               bool &fault) {
+  uint32_t lf[kGreedyLinkSlots], lb[kGreedyLinkSlots], ln[kGreedyLinkSlots];
+#pragma unroll
+  for (int t = 0; t < kGreedyLinkSlots; t++) {
+    const int l = lane + 64 * t;
+    lf[t] = 0;
+    lb[t] = l < E ? gofs[l] : 0;
+    ln[t] = l < E ? gofs[l + 1] - gofs[l] : 0;
+  }
+  for (int round = 0;; round++) {
+    uint32_t cs[kGreedyLinkSlots], cq[kGreedyLinkSlots];
+    uint32_t wmin = kNotYet;
+#pragma unroll
+    for (int t = 0; t < kGreedyLinkSlots; t++) {
+      cs[t] = kNotYet;
+      cq[t] = 0;
+      uint64_t bk = ~0ull;
+      uint64_t bq = ~0ull;
+      // two pending sends per step: their records, then their ready times
+      for (uint32_t q0 = 0; q0 < ln[t]; q0 += 2) {
+        uint4 rc[2];
+        uint32_t r[2];
+#pragma unroll
+        for (int u = 0; u < 2; u++) rc[u] = grec[lb[t] + min(q0 + u, ln[t] - 1)];
+#pragma unroll
+        for (int u = 0; u < 2; u++) {
+          const uint32_t x = rc[u].w & 0xFFFFu, other = rc[u].w >> 16;
+          if (kRS) {
+            const uint32_t pend = gpend[x], rd = grdy[x];
+            r[u] = pend == 0 ? rd : kNotYet;
+          } else {
+            const uint32_t fo = gfin[other == kNoPred ? 0u : other];
+            r[u] = other == kNoPred ? 0u : fo;
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < 2; u++) {
+          if (q0 + u >= ln[t] || r[u] == kNotYet) continue;  // its chunk has not arrived yet
+          const uint32_t st = max(lf[t], r[u]);
+          const uint64_t kx = ((uint64_t)rc[u].y << 32) | rc[u].x;
+          const uint64_t qx = ((uint64_t)rc[u].z << 32) | (rc[u].w & 0xFFFFu);  // priority, then chunk
+          if (st < cs[t] || (st == cs[t] && (kx < bk || (kx == bk && qx < bq)))) {
+            cs[t] = st;
+            cq[t] = q0 + u;
+            bk = kx;
+            bq = qx;
+          }
+        }
+      }
+      wmin = min(wmin, cs[t]);
+    }
+    wmin = ~wave_reduce_max(~wmin);
+    if (wmin == kNotYet) break;  // nothing left to schedule
+    if (round > nslots) {  // unreachable: every window commits a send
+      fault = true;
+      break;
+    }
+    const uint64_t wend = (uint64_t)wmin + cmin;
+    wave_sync();
+#pragma unroll
+    for (int t = 0; t < kGreedyLinkSlots; t++) {
+      if (cs[t] != kNotYet && (uint64_t)cs[t] < wend) {
+        const int l = lane + 64 * t;
+        const uint4 rc = grec[lb[t] + cq[t]];
+        const uint32_t x = rc.w & 0xFFFFu;
+        const uint32_t f = cs[t] + s_cost[l];
+        if (kRS) {
+          const uint32_t nxt = rc.w >> 16;
+          if (nxt != kNoPred) {
+            atomicMax(&grdy[nxt], f);
+            atomicSub(&gpend[nxt], 1u);
+          }
+        }
+        gfin[x] = f;
+        lf[t] = f;
+        mk = max(mk, f);
+        grec[lb[t] + cq[t]] = grec[lb[t] + ln[t] - 1];
+        ln[t]--;
+      }
+    }
+    wave_sync();
+  }
+
+}
+
+// Time-aware greedy orders (App. B.2) for Alltoall: the sends of a chunk
+// are the hops of its routed path, each ready when the hop before it ends
+// (the first at 0). One wavefront per candidate: the sends are counted per
+// link, laid out as per-link lists of packed records (key from the path's
+// remaining and travelled costs, priority of slot c*H + h), and the greedy
+// runs window by window as for the multicast trees.
+__global__ __launch_bounds__(kTreeMaxThreads) void path_greedy_kernel(PathGreedyArgs a) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int C = a.C, P = a.P, E = a.E, H = a.H;
+  uint32_t *s_cost = (uint32_t *)lds;
+  for (int j = threadIdx.x; j < E; j += blockDim.x) s_cost[j] = a.cost[j];
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  unsigned char *wl = lds + a.o_wave + wave * a.wave_bytes;
+  uint32_t *gfin = (uint32_t *)(wl + a.w_gfin);
+  uint32_t *gofs = (uint32_t *)(wl + a.w_gofs);  // [E + 1]
+  uint32_t *gcur = (uint32_t *)(wl + a.w_gcur);  // [E]
+  uint4 *grec = (uint4 *)(wl + a.w_grec);
+  const int64_t stride = (int64_t)gridDim.x * a.waves_per_block;
+  for (int64_t i = (int64_t)blockIdx.x * a.waves_per_block + wave; i < a.n; i += stride) {
+    const uint8_t *rt = a.routes + (size_t)i * a.route_stride;
+    const uint32_t *gpr = a.prio + (size_t)i * a.prio_stride;
+    for (int l = lane; l <= E; l += 64) gofs[l] = 0;
+    for (int sl = lane; sl < a.nslots; sl += 64) gfin[sl] = kNotYet;
+    wave_sync();
+    // the chosen path of chunk c: global option index, or -1 (no send)
+    bool bad = false;
+    auto path_of = [&](int c) -> int64_t {
+      const uint32_t sd = (uint32_t)c / (uint32_t)a.cpr;
+      const uint32_t s = sd / P, d = sd - s * P;
+      if (s == d) return -1;
+      const uint32_t k = rt[c];
+      if (k >= a.npaths[sd]) {
+        bad = true;  // the pair is left unrouted
+        return -1;
+      }
+      return (int64_t)a.pair_base[sd] + k;
+    };
+    for (int c = lane; c < C; c += 64) {
+      const int64_t q = path_of(c);
+      if (q < 0) continue;
+      for (uint32_t j = a.path_off[q]; j < a.path_off[q + 1]; j++)
+        atomicAdd(&gofs[a.path_links[j] + 1], 1u);
+    }
+    wave_sync();
+    {
+      // exclusive scan of the per-link counts (gofs[0] = 0)
+      const int n1 = E + 1;
+      const int per = (n1 + 63) >> 6;
+      const int b0 = min(lane * per, n1), b1 = min(b0 + per, n1);
+      uint32_t sum = 0;
+      for (int w = b0; w < b1; w++) sum += gofs[w];
+      const uint32_t incl = wave_incl_scan(sum, lane);
+      uint32_t run = incl - sum;
+      for (int w = b0; w < b1; w++) {
+        run += gofs[w];
+        gofs[w] = run;
+      }
+    }
+    wave_sync();
+    for (int l = lane; l < E; l += 64) gcur[l] = gofs[l];
+    wave_sync();
+    for (int c = lane; c < C; c += 64) {
+      const int64_t q = path_of(c);
+      if (q < 0) continue;
+      const uint32_t j0 = a.path_off[q], j1 = a.path_off[q + 1];
+      uint32_t total = 0;
+      for (uint32_t j = j0; j < j1; j++) total += s_cost[a.path_links[j]];
+      uint32_t trav = 0;
+      for (uint32_t j = j0; j < j1; j++) {
+        const uint32_t l = a.path_links[j], h = j - j0;
+        const uint32_t rem = total - trav;  // remaining path, this hop included
+        const uint32_t sl = (uint32_t)c * H + h;
+        const uint32_t other = h ? sl - 1 : kNoPred;  // the hop the chunk arrives by
+        const uint32_t pos = atomicAdd(&gcur[l], 1u);
+        grec[pos] = make_uint4(trav, ~rem, gpr[sl], sl | (other << 16));
+        trav += s_cost[l];
+      }
+    }
+    wave_sync();
+    uint32_t mk = 0;
+    bool fault = false;
+    greedy_windows<false>(E, lane, a.nslots, a.cmin, s_cost, grec, gofs, gfin, nullptr, nullptr,
+                          mk, fault);
+    const bool all_ok = __ballot(bad) == 0;
+    const bool failed = __ballot(fault) != 0;
+    mk = wave_max(mk);
+    if (lane == 0) {
+      a.makespan[i] = failed ? 0xFFFFFFFFu : mk;
+      a.valid[i] = (uint8_t)(all_ok && !failed);
+    }
+    wave_sync();
+  }
+}
+
 // Time-aware greedy orders (App. B.2), multicast trees. After the trees and
 // Step-2 keys (as in the layered kernel), the greedy is simulated exactly in
 // windows: the earliest start W any ready send can take bounds every other
@@ -1456,6 +1656,46 @@ static const void *greedy_fn_r(const TreeArgs &a) {
 
 static const void *greedy_fn(const TreeArgs &a) {
   return a.reduce ? greedy_fn_r<true>(a) : greedy_fn_r<false>(a);
+}
+
+int32_t path_greedy_layout(const taccl_plan &p, PathGreedyArgs &a) {
+  const int32_t C = p.coll.C, E = p.topo.E, H = std::max(p.H, 1);
+  if ((int64_t)C * H > 1024 || E > 64 * kGreedyLinkSlots || E < 1) return 0;
+  uint32_t cmin = ~0u;
+  for (uint32_t c : p.cost) cmin = std::min(cmin, c);
+  if (cmin == 0) return 0;
+  a.cmin = cmin;
+  a.nslots = C * H;
+  const int32_t S = (int32_t)std::max<int64_t>(std::min<int64_t>(p.max_sends, (int64_t)C * H), 1);
+  a.o_wave = align16(4 * E);
+  int32_t w = 0;
+  auto wtake = [&](int32_t bytes) {
+    int32_t o = w;
+    w = align16(w + bytes);
+    return o;
+  };
+  a.w_gfin = wtake(4 * a.nslots);
+  a.w_gofs = wtake(4 * (E + 1));
+  a.w_gcur = wtake(4 * E);
+  a.w_grec = wtake(16 * S);
+  a.wave_bytes = w;
+  return a.o_wave + a.wave_bytes;
+}
+
+int path_greedy_blocks_per_cu(const PathGreedyArgs &a) {
+  int nb = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, (const void *)path_greedy_kernel,
+                                                   64 * a.waves_per_block,
+                                                   a.o_wave + a.waves_per_block * a.wave_bytes) !=
+      hipSuccess)
+    return 0;
+  return nb;
+}
+
+hipError_t launch_path_greedy(const PathGreedyArgs &a, int grid, hipStream_t stream) {
+  void *args[] = {(void *)&a};
+  return hipLaunchKernel((const void *)path_greedy_kernel, dim3(grid), dim3(64 * a.waves_per_block),
+                         args, a.o_wave + a.waves_per_block * a.wave_bytes, stream);
 }
 
 int tree_greedy_blocks_per_cu(const TreeArgs &a) {

@@ -99,6 +99,28 @@ struct PathArgs {
   int32_t lr_threads;  // block size of the LDS-record kernel for this plan
 };
 
+// Time-aware greedy orders for Alltoall: persistent blocks of wavefronts,
+// one candidate per wavefront at a time (send slots c*H + h).
+struct PathGreedyArgs {
+  int32_t C, P, E, H, cpr, nslots;
+  int32_t route_stride, prio_stride;
+  uint32_t cmin;
+  const uint32_t *cost;
+  const uint32_t *pair_base;
+  const uint8_t *npaths;
+  const uint32_t *path_off;
+  const uint16_t *path_links;
+  const uint8_t *routes;
+  const uint32_t *prio;
+  uint32_t *makespan;
+  uint8_t *valid;
+  int64_t n;
+  int32_t waves_per_block;
+  // LDS: link costs, then per wavefront finish times per slot, list
+  // offsets and fill pointers per link, pending-send records
+  int32_t o_wave, wave_bytes, w_gfin, w_gofs, w_gcur, w_grec;
+};
+
 // Switch-hyperedge connection count: one block per candidate at a time.
 struct ConnArgs {
   int32_t C, P, V, cpr, kind, tree, mask_words;  // mask_words: ceil(P*P / 32)
@@ -141,6 +163,11 @@ int path_fast_threads(const taccl_plan &p);  // threads per block: 256, 512 or 1
 int path_fast_blocks_per_cu(const PathArgs &a, int cpt, int nt);
 
 hipError_t launch_tree(const TreeArgs &a, int grid, hipStream_t stream);
+// Alltoall greedy: fills the layout; returns the bytes of a one-wavefront
+// block, or 0 when the plan has more than 1024 send slots or 256 links
+int32_t path_greedy_layout(const taccl_plan &p, PathGreedyArgs &a);
+int path_greedy_blocks_per_cu(const PathGreedyArgs &a);
+hipError_t launch_path_greedy(const PathGreedyArgs &a, int grid, hipStream_t stream);
 // connection count: LDS bytes of a block of `threads`, and the launch
 int32_t connections_lds_bytes(const ConnArgs &a, int threads);
 hipError_t launch_connections(const ConnArgs &a, int threads, int grid, hipStream_t stream);

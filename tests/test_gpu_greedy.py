@@ -1,6 +1,8 @@
 """GPU parity of the time-aware greedy link orders (App. B.2) for multicast
-collectives, bit for bit against the oracle, through the C ABI. Needs an
-MI355X."""
+collectives and Alltoall, bit for bit against the oracle, through the C ABI.
+Needs an MI355X."""
+from dataclasses import replace
+
 import numpy as np
 import pytest
 
@@ -110,9 +112,35 @@ def test_twonode_reductions(kind):
     check(plan, ref, routes, prio, w.name)
 
 
-def test_alltoall_refused():
+@pytest.mark.parametrize("make,n", [
+    (lambda: cf.with_greedy(cf.full_a2a(4)), 300),
+    (lambda: cf.with_greedy(replace(cf.full_a2a(6), chunks_per_rank=2)), 300),
+    (lambda: cf.with_greedy(cf.switch16_a2a()), 512),
+    (lambda: cf.with_greedy(cf.two_node_rings_a2a(4, contiguity=0)), 300)])
+def test_alltoall(make, n):
+    """Alltoall: a chunk's hops are ready one after the other."""
+    w = make()
+    plan, ref, opts = plans(w)
+    routes, prio = generate(w.seed + 11, 0, n, opts, plan.prio_stride)
+    check(plan, ref, routes, prio, f"{w.name} alltoall greedy")
+
+
+def test_alltoall_unrouted_and_equal_priorities():
+    w = cf.with_greedy(cf.switch16_a2a())
+    plan, ref, opts = plans(w)
+    routes, prio = generate(w.seed + 12, 0, 256, opts, plan.prio_stride)
+    rng = np.random.default_rng(5)
+    routes[rng.random(routes.shape) < 0.01] = 0xFF
+    prio[:128] = 7
+    mk, ok = check(plan, ref, routes, prio, "switch16 greedy unrouted / equal priorities")
+    assert not ok.all()
+
+
+def test_alltoall_too_large_refused():
+    """More than 1024 send slots (chunks x longest path) do not fit a
+    wavefront's on-chip lists: refused, not approximated."""
     from paper_2111_04867_amd.binding import Plan, TacclError
-    w = cf.with_greedy(cf.full_a2a(4))
+    w = cf.with_greedy(cf.fournode64_a2a(n_candidates=2))
     plan = Plan.from_workload(w)
     routes, prio = generate(1, 0, 2, plan.route_options(), plan.prio_stride)
     with pytest.raises(TacclError) as e:

@@ -271,7 +271,8 @@ def with_greedy(w):
 
 NAMED["twonode16_ag_greedy"] = lambda **kw: with_greedy(twonode16_ag(**kw))
 NAMED["cubemesh8_ag_greedy"] = lambda **kw: with_greedy(cubemesh8_ag(**kw))
-GREEDY_ORDER = ["cubemesh8_ag_greedy", "twonode16_ag_greedy"]
+NAMED["switch16_a2a_greedy"] = lambda **kw: with_greedy(switch16_a2a(**kw))
+GREEDY_ORDER = ["cubemesh8_ag_greedy", "twonode16_ag_greedy", "switch16_a2a_greedy"]
 
 
 def with_switch_ports(w):
