@@ -272,7 +272,11 @@ static taccl_status_t build_levels(taccl_plan *p) {
   }
   std::vector<uint64_t> lv(rems.begin(), rems.end());  // descending
   p->nlev = (int32_t)lv.size();
-  if (p->nlev > 127) return fail(TACCL_ERR_UNSUPPORTED, "more than 127 remaining-cost levels");
+  // the level tables hold a signed byte per (route option, level) and a
+  // class range per (level, link)
+  if (p->H > 127) return fail(TACCL_ERR_UNSUPPORTED, "Alltoall paths of more than 127 hops");
+  if ((double)npath * p->nlev + 8.0 * p->nlev * E > (double)(256u << 20))
+    return fail(TACCL_ERR_UNSUPPORTED, "remaining-cost level tables beyond 256 MiB");
   auto level_of = [&](uint64_t rem) {
     return (int32_t)(std::lower_bound(lv.begin(), lv.end(), rem, std::greater<uint64_t>()) -
                      lv.begin());

@@ -7,5 +7,6 @@ arithmetic lives here.
 from .configs import (ALLGATHER, ALLREDUCE, ALLTOALL, CONTIG_ORDER, EXPLICIT, HIER_RELAY,  # noqa
                       GREEDY_ORDER, KSHORTEST, NAMED, ORDER, PORTS_ORDER, REDUCE_ORDER,
                       REDUCESCATTER, RELAY1, SHORTEST_ONLY, Workload, as_reduction, named,
+                      random_workload,
                       with_contiguity, with_greedy, with_switch_ports)
 from .candgen import build_candgen, generate  # noqa: F401

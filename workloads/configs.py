@@ -377,3 +377,80 @@ def two_node_rings_a2a(P_per, chunk_bytes=64 * KIB, contiguity=1):
     node_of = np.array([r // P_per for r in range(P)], dtype=np.int32)
     return Workload(f"tworings{P}_a2a", P, P, row_ptr, col, a, b, node_of, ALLTOALL, 1,
                     chunk_bytes, KSHORTEST, k=2, max_cross=1, contiguity=contiguity)
+
+
+def random_workload(seed):
+    """A seeded random small plan for parity sweeps: a bidirectional ring of
+    3..16 ranks with random extra link pairs, alpha/beta drawn either from
+    Table 1's values or from wide uniform ranges, half the time a switch
+    vertex linked to most ranks, sometimes two nodes joined
+    only between relay ranks; any collective kind (explicit ones with random
+    owners and postconditions), a random route mode and k, and one of static
+    orders, greedy orders, contiguous transfers (two nodes) or switch ports
+    (Alltoall with a switch). Some draws give plans a route search refuses
+    (a relay route through one link twice); callers skip those."""
+    rng = np.random.default_rng(seed)
+    kind = int(rng.choice([ALLGATHER, ALLTOALL, REDUCESCATTER, ALLREDUCE, EXPLICIT]))
+    P = int(rng.integers(3, 13)) if rng.random() < 0.5 else int(rng.choice([4, 8, 12, 16]))
+    switch = bool(rng.random() < 0.5)
+    two_nodes = bool(rng.random() < 0.35) and P >= 4
+    V = P + (1 if switch else 0)
+    table1 = bool(rng.random() < 0.5)  # only Table 1's link parameters
+    links = {}
+
+    def add(u, v):
+        if u != v and (u, v) not in links:
+            if table1:
+                links[(u, v)] = (int(rng.choice([NVLINK_ALPHA, IB_ALPHA])),
+                                 int(rng.choice([DGX2_NVLINK_BETA, NDV2_NVLINK_BETA, IB_BETA])))
+            else:
+                links[(u, v)] = (int(rng.integers(100, 2000)), int(rng.integers(1, 120)))
+
+    for i in range(P):
+        add(i, (i + 1) % P)
+        add((i + 1) % P, i)
+    for _ in range(int(rng.integers(0, 2 * P))):
+        u, v = (int(x) for x in rng.integers(0, P, 2))
+        add(u, v)
+        add(v, u)
+    if switch:
+        for r in range(P):
+            if rng.random() < 0.8:
+                add(r, P)
+                add(P, r)
+    node_of = relay = None
+    max_cross = -1
+    if two_nodes:
+        half = P // 2
+        node_of = np.array([0 if r < half else 1 for r in range(P)] + [0] * (V - P),
+                           dtype=np.int32)
+        relay = np.zeros(V, dtype=np.uint8)
+        relay[[0, half - 1, half, P - 1]] = 1
+        # links between the nodes only join relay ranks (the ring's crossing
+        # links 0 <-> P-1 and half-1 <-> half do); the switch is node 0's
+        links = {(u, v): ab for (u, v), ab in links.items()
+                 if node_of[u] == node_of[v] or (relay[u] and relay[v] and u < P and v < P)}
+        max_cross = 1
+    row_ptr, col, a, b = csr_from_edges(V, [(u, v, ab[0], ab[1]) for (u, v), ab in links.items()])
+    modes = [SHORTEST_ONLY, KSHORTEST, KSHORTEST, RELAY1] + ([HIER_RELAY] if two_nodes else [])
+    mode = int(rng.choice(modes))
+    owner = post_ptr = post = None
+    if kind == EXPLICIT:
+        C = int(rng.integers(1, 2 * P))
+        owner = rng.integers(0, P, C).astype(np.int32)
+        posts = [sorted(set(int(x) for x in rng.integers(0, P, int(rng.integers(1, P + 1)))))
+                 for _ in range(C)]
+        post_ptr = np.cumsum([0] + [len(p) for p in posts]).astype(np.int32)
+        post = np.array([x for p in posts for x in p], dtype=np.int32)
+    w = Workload(f"random{seed}", V, P, row_ptr, col, a, b, node_of, kind,
+                 int(rng.integers(1, 3)), int(rng.choice([4096, 65536, 1 << 20])), mode,
+                 k=int(rng.integers(1, 5)), max_cross=max_cross, relay=relay, owner=owner,
+                 post_ptr=post_ptr, post=post, seed=seed)
+    extra = rng.choice(["static", "greedy", "contig", "ports"])
+    if extra == "greedy":
+        w = with_greedy(w)
+    elif extra == "contig" and two_nodes:
+        w = with_contiguity(w)
+    elif extra == "ports" and kind == ALLTOALL and switch:
+        w = with_switch_ports(w)
+    return w
