@@ -143,18 +143,17 @@ void taccl_collective_destroy(taccl_collective_t coll);
  *     send of that order with the same remaining path length whose chunk is
  *     already at the link's source when the transfer starts; m chunks cost
  *     alpha + ceil(beta * m * chunk_bytes / 1000) ns and all of them arrive
- *     when the transfer ends. Plans whose multicast evaluation needs the
- *     round-based kernel (see taccl_eval_batch) refuse contiguity;
+ *     when the transfer ends;
  *   order: 0 = static Step-2 order per link (Sec. 5.1: remaining path desc,
  *     travelled path asc, priority, chunk); 1 = the time-aware greedy of
  *     App. B.2: round by round, among the sends whose chunk has arrived, the
  *     one that can start earliest (max of link time and chunk time) goes
  *     next, ties broken by the Step-2 key. Not combined with contiguity
- *     (INVALID_ARGUMENT). On the GPU it is evaluated for multicast
- *     collectives (Allgather, explicit, ReduceScatter, Allreduce) on plans
- *     with at most 256 links that fit the layered kernel, and for Alltoall
+ *     (INVALID_ARGUMENT). On the GPU it is evaluated for every multicast
+ *     plan (Allgather, explicit, ReduceScatter, Allreduce) and for Alltoall
  *     plans with at most 256 links and 1024 send slots (chunks x longest
- *     route option); other plans are refused at evaluation (UNSUPPORTED);
+ *     route option); larger Alltoall plans are refused at evaluation
+ *     (UNSUPPORTED);
  *   switch_ports (Alltoall only): 0 = a switch vertex stores and forwards
  *     (uplink, then downlink, each one latency); 1 = the switch model of
  *     App. B.3: a hop pair rank -> switch -> rank is one send costing one
@@ -242,7 +241,9 @@ taccl_status_t taccl_plan_upload(taccl_plan_t plan);
  *     postcondition holds at the end, else 0.
  * Each candidate is evaluated independently; results are exact (integer).
  * Errors (synchronous): INVALID_ARGUMENT for null pointers with n > 0,
- * n < 0 or a misaligned d_prio; HIP if the plan upload or the launch fails.
+ * n < 0 or a misaligned d_prio; UNSUPPORTED when a candidate's state does
+ * not fit one block's LDS or an Alltoall greedy plan exceeds its limits;
+ * HIP if the plan upload or the launch fails.
  * Faults inside the kernel surface at the caller's next synchronisation.
  * n == 0 is a no-op.
  */

@@ -266,21 +266,13 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
         a.routes_word_aligned &&
         (greedy ? tree_greedy_layout(*p, a) : tree_layers_layout(*p, a)) > 0 &&
         tree_block_bytes(a, 1) <= t->max_lds;
-    if (greedy && !layered)
-      return fail(TACCL_ERR_UNSUPPORTED,
-                  "time-aware greedy orders need the layered multicast kernel (at most 256 "
-                  "links), which this plan does not fit");
     const int kind = p->coll.kind;
     const bool reduction = kind == TACCL_REDUCESCATTER || kind == TACCL_ALLREDUCE;
-    if (!layered && p->contig)
-      return fail(TACCL_ERR_UNSUPPORTED,
-                  "contiguous transfers need the layered multicast kernel, which this plan "
-                  "does not fit");
-    if (!layered && reduction)
-      return fail(TACCL_ERR_UNSUPPORTED,
-                  "ReduceScatter and Allreduce need the layered multicast kernel, which this "
-                  "plan does not fit");
-    if (!layered && tree_layout(*p, a) > t->max_lds)
+    // plans outside the layered kernel's limits: the general kernel, whose
+    // variant with reductions, contiguity and greedy orders keeps more state
+    a.any = !layered && (reduction || p->contig || greedy);
+    a.greedy = greedy;
+    if (!layered && (a.any ? tree_any_layout(*p, a) : tree_layout(*p, a)) > t->max_lds)
       return fail(TACCL_ERR_UNSUPPORTED, "multicast plan needs more LDS than a block has");
     a.lrev = t->lrev;
     // wavefronts per block: most resident wavefronts per CU (LDS, and for
@@ -307,8 +299,8 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
       const int64_t want = (n + best_w - 1) / best_w;
       const int tgrid =
           (int)std::min<int64_t>(want, (int64_t)std::max(t->num_cus, 1) * best_bpc);
-      if (greedy) return launch_tree_greedy(x, tgrid, s);
-      return layered ? launch_tree_layers(x, tgrid, s) : launch_tree(x, tgrid, s);
+      if (!layered) return launch_tree(x, tgrid, s);
+      return greedy ? launch_tree_greedy(x, tgrid, s) : launch_tree_layers(x, tgrid, s);
     };
     if (kind == TACCL_ALLREDUCE) {
       // ReduceScatter on the first priority row, then Allgather on the

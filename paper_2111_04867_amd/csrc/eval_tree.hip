@@ -75,14 +75,18 @@ __device__ __forceinline__ uint32_t div_v(uint32_t n, uint32_t m) {
 // remaining path of Sec. 5.1) and writes every send's packed Step-2 key
 // (~rem << 32 | trav, ascending = rem desc, trav asc) over the vertex's dead
 // distance slot. kMasks also sets the chunk's bit in its link's mask.
-// par[] must be zero on entry; returns whether every chunk reached its
-// postcondition ranks.
-template <bool kMasks>
+// kRS (ReduceScatter; s_cost then holds the cost of every link's reverse):
+// the send v -> u has rem = reversed distance from v to the owner and trav =
+// longest reversed path up to v, and pend[] counts the sends into each
+// vertex other than the owner (the partials its own send waits for).
+// par[] (and pend[] for kRS) must be zero on entry; returns whether every
+// chunk reached its postcondition ranks.
+template <bool kMasks, bool kRS = false>
 __device__ __forceinline__ bool build_trees(const TreeArgs &a, const uint32_t *s_rec,
                                             const uint32_t *s_cost, const uint8_t *s_own,
                                             const uint64_t *s_post, const uint8_t *rt,
                                             uint64_t *key, uint16_t *par, uint32_t *ord,
-                                            uint32_t *lmask, int lane) {
+                                            uint32_t *lmask, int lane, uint32_t *pend = nullptr) {
   const int C = a.C, P = a.P, V = a.V, K = a.K, H = a.H, MW = a.mask_words;
   uint32_t *dh = (uint32_t *)key;  // dh[2s] = dist, dh[2s+1] = height
   bool ok = true;
@@ -130,24 +134,203 @@ __device__ __forceinline__ bool build_trees(const TreeArgs &a, const uint32_t *s
     for (int j = cnt - 1; j >= 0; j--) {
       const uint32_t e = ord[base + j];
       const int v = e & 0xFF, u = (e >> 8) & 0xFF, l = e >> 16;
-      const uint32_t rem = s_cost[l] + dh[2 * (base + v) + 1];
-      const uint32_t trav = dh[2 * (base + u)];
-      if (rem > dh[2 * (base + u) + 1]) dh[2 * (base + u) + 1] = rem;
-      key[base + v] = ((uint64_t)(~rem) << 32) | trav;
+      const uint32_t hv = dh[2 * (base + v) + 1];
+      const uint32_t up = s_cost[l] + hv;  // longest path below u through v
+      if (up > dh[2 * (base + u) + 1]) dh[2 * (base + u) + 1] = up;
+      if (kRS) {
+        key[base + v] = ((uint64_t)(~dh[2 * (base + v)]) << 32) | hv;
+        if (u != o) pend[base + u]++;
+      } else {
+        key[base + v] = ((uint64_t)(~up) << 32) | dh[2 * (base + u)];
+      }
       if (kMasks) atomicOr(&lmask[l * MW + (c >> 5)], 1u << (c & 31));
     }
   }
   return ok;
 }
 
+// Step 5' of the general variant, one wavefront per candidate. Sends sit
+// in chain[] in link order (pred << 16 | slot, pred = the slot whose send
+// brings the chunk to the link's source, or kNoPred), fin[] = kNotYet.
+//  * Allgather: a send is ready when its pred has finished.
+//  * ReduceScatter (rs): the send of slot (c,v) goes v -> u on the reverse
+//    of its tree link and carries v's partial, so it is ready when every
+//    send into v has finished: pend[] counts them down and rdy[] keeps the
+//    latest finish (the decrement is a release and its read an acquire, so
+//    a zero count sees every max before it).
+//  * Contiguous transfers (a.contig) on links between nodes: the link's
+//    next send either joins the open transfer (same remaining length, chunk
+//    ready by the transfer's start; m sends cost alpha + ceil(beta*m*S/1000))
+//    or closes it and opens a new one. Finish times of a transfer's sends
+//    are published only when it closes, so no dependant reads a time that
+//    could still grow. A joiner's pred has a strictly longer remaining path
+//    than the transfer, so waiting for it never waits on the transfer.
+//  * Time-aware greedy (a.greedy, App. B.2): send by send, the unscheduled
+//    ready send with the smallest (max(ready, link free), Step-2 key,
+//    priority, slot) is scheduled, by four wavefront reductions.
+// Returns true on a fault (no progress; unreachable for valid orders).
+__device__ __noinline__ bool any_schedule(const TreeArgs &a, bool rs, int lane,
+                                          const uint32_t *s_cost, const uint8_t *s_src,
+                                          const uint8_t *s_own, const uint64_t *key,
+                                          const uint32_t *prio, const uint16_t *par,
+                                          const uint32_t *chain, const uint32_t *lbase,
+                                          uint32_t *lhead, uint32_t *lfree, uint32_t *fin,
+                                          uint32_t *pend, uint32_t *rdy, uint32_t *gst,
+                                          uint32_t *grem, uint32_t *gcnt, uint32_t *gfirst,
+                                          uint32_t &mk) {
+  const int V = a.V, E = a.E, CV = a.C * a.V;
+  const uint32_t total = lbase[E];
+  auto ready_of = [&](uint32_t ent) -> uint32_t {
+    const uint32_t s = ent & 0xFFFFu;
+    if (rs) {
+      if (__hip_atomic_load(&pend[s], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP))
+        return kNotYet;
+      return lds_get(&rdy[s]);
+    }
+    const uint32_t p = ent >> 16;
+    return p == kNoPred ? 0u : lds_get(&fin[p]);
+  };
+  auto publish = [&](uint32_t s, uint32_t f, int l) {
+    lds_put(&fin[s], f);
+    if (rs) {
+      const uint32_t c = div_v(s, a.vmagic);
+      const int u = s_src[l];
+      if (u != s_own[c]) {
+        const uint32_t q = c * V + u;
+        __hip_atomic_fetch_max(&rdy[q], f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        __hip_atomic_fetch_sub(&pend[q], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+      }
+    }
+  };
+
+  if (a.greedy) {
+    for (uint32_t step = 0; step < total; step++) {
+      uint32_t bt = ~0u, bp = ~0u, bs = ~0u;
+      uint64_t bk = ~0ull;
+      for (int s = lane; s < CV; s += 64) {
+        const int pl = par[s];
+        if (!pl || lds_get(&fin[s]) != kNotYet) continue;
+        const int l = pl - 1;
+        uint32_t r;
+        if (rs) {
+          if (lds_get(&pend[s])) continue;
+          r = lds_get(&rdy[s]);
+        } else {
+          const uint32_t c = div_v(s, a.vmagic);
+          const int u = s_src[l];
+          r = (u == s_own[c]) ? 0u : lds_get(&fin[c * V + u]);
+          if (r == kNotYet) continue;
+        }
+        const uint32_t t = max(r, lfree[l]);
+        const uint64_t k = key[s];
+        const uint32_t p = prio[s];
+        if (t < bt || (t == bt && (k < bk || (k == bk && (p < bp || (p == bp && (uint32_t)s < bs)))))) {
+          bt = t;
+          bk = k;
+          bp = p;
+          bs = (uint32_t)s;
+        }
+      }
+      const uint32_t tmin = ~wave_reduce_max(~bt);
+      const bool at = bt == tmin;
+      const uint64_t kmin = ~wave_reduce_max64(at ? ~bk : 0ull);
+      const bool ak = at && bk == kmin;
+      const uint32_t pmin = ~wave_reduce_max(ak ? ~bp : 0u);
+      const uint32_t smin = ~wave_reduce_max(ak && bp == pmin ? ~bs : 0u);
+      if (smin == ~0u) return true;
+      const int l = par[smin] - 1;
+      const uint32_t f = tmin + s_cost[l];
+      if (lane == 0) {
+        lfree[l] = f;
+        publish(smin, f, l);
+      }
+      mk = max(mk, f);
+      wave_sync();
+    }
+    return false;
+  }
+
+  for (uint32_t round = 0;; round++) {
+    bool pending = false;
+    for (int l = lane; l < E; l += 64) {
+      uint32_t h = lhead[l];
+      const uint32_t e = lbase[l + 1];
+      uint32_t f = lfree[l];
+      if (!(a.contig && a.lmerge[l])) {
+        if (h == e) continue;
+        const uint32_t cl = s_cost[l];
+        while (h < e) {
+          const uint32_t ent = chain[h];
+          const uint32_t r = ready_of(ent);
+          if (r == kNotYet) break;
+          f = max(r, f) + cl;
+          publish(ent & 0xFFFFu, f, l);
+          h++;
+        }
+        pending |= h < e;
+      } else {
+        uint32_t gs = gst[l], gr = grem[l], gm = gcnt[l], g0 = gfirst[l];
+        if (h == e && gm == 0) continue;
+        const uint32_t le = rs ? a.lrev[l] : (uint32_t)l;  // the link the sends use
+        const uint32_t al = a.lalpha[le];
+        const uint64_t bsz = a.lbs[le];
+        while (true) {
+          if (h == e) {
+            for (uint32_t j = g0; j < h && gm; j++) publish(chain[j] & 0xFFFFu, f, l);
+            gm = 0;
+            break;
+          }
+          const uint32_t ent = chain[h];
+          const uint32_t rem = ~(uint32_t)(key[ent & 0xFFFFu] >> 32);
+          uint32_t r = kNotYet;
+          if (gm && rem == gr) {
+            r = ready_of(ent);
+            if (r == kNotYet) break;
+            if (r <= gs) {  // joins the open transfer
+              gm++;
+              f = gs + al + (uint32_t)((bsz * gm + 999) / 1000);
+              h++;
+              continue;
+            }
+          }
+          for (uint32_t j = g0; j < h && gm; j++) publish(chain[j] & 0xFFFFu, f, l);
+          gm = 0;
+          if (r == kNotYet) r = ready_of(ent);
+          if (r == kNotYet) break;
+          gs = max(r, f);
+          f = gs + al + (uint32_t)((bsz + 999) / 1000);
+          gm = 1;
+          g0 = h;
+          gr = rem;
+          h++;
+        }
+        gst[l] = gs;
+        grem[l] = gr;
+        gcnt[l] = gm;
+        gfirst[l] = g0;
+        pending |= h < e || gm;
+      }
+      lhead[l] = h;
+      lfree[l] = f;
+      mk = max(mk, f);
+    }
+    if (__ballot(pending) == 0) return false;
+    if (round > 2 * total + 2) return true;  // unreachable: key order is topological
+  }
+}
+
 // kRecLds: the route records fit in LDS (else they are read from global
 // memory, where they stay cache resident). kPrefetch: a candidate's routes
-// (whole words) and priorities fit the prefetch registers.
-template <bool kRecLds, bool kPrefetch>
+// (whole words) and priorities fit the prefetch registers. kAny: the
+// variant for plans outside the layered kernel's limits that also times
+// ReduceScatter (a.reduce), contiguous transfers (a.contig) and the
+// time-aware greedy (a.greedy); see step 5' below.
+template <bool kRecLds, bool kPrefetch, bool kAny>
 __global__ __launch_bounds__(kTreeMaxThreads) void tree_eval_kernel(TreeArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int C = a.C, V = a.V, E = a.E, MW = a.mask_words;
   const int CV = C * V;
+  const bool rs = kAny && a.reduce;
 
   // ---- block-wide copy of the plan tables --------------------------------
   uint32_t *s_cost = (uint32_t *)(lds + a.o_cost);
@@ -156,7 +339,12 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_eval_kernel(TreeArgs a) 
   uint64_t *s_post = (uint64_t *)(lds + a.o_post);
   const uint32_t *s_rec = kRecLds ? (const uint32_t *)(lds + a.o_rec) : a.rec;
   for (int j = threadIdx.x; j < E; j += blockDim.x) {
-    s_cost[j] = a.cost[j];
+    uint32_t cj = a.cost[j];
+    if (rs) {  // a ReduceScatter send on the reverse of a tree link
+      const uint32_t r = a.lrev[j];
+      cj = r != 0xFFFFu ? a.cost[r] : 0u;
+    }
+    s_cost[j] = cj;
     s_src[j] = (uint8_t)a.lsrc[j];
   }
   if (kRecLds)
@@ -188,6 +376,13 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_eval_kernel(TreeArgs a) 
   uint32_t *lbase = (uint32_t *)(wl + a.w_base);  // [E+1]
   uint32_t *lhead = (uint32_t *)(wl + a.w_head);  // [E]
   uint32_t *lfree = (uint32_t *)(wl + a.w_free);  // [E]
+  if (kAny) fin = (uint32_t *)(wl + a.w_gfin);     // priorities stay for the greedy
+  // kAny: ReduceScatter partials still to come into (c,v) and the latest of
+  // them; contiguous transfer open on each link (start, remaining length,
+  // sends, first position)
+  uint32_t *pend = (uint32_t *)(wl + a.w_gpend);
+  uint32_t *rdy = (uint32_t *)(wl + a.w_grdy);
+  uint32_t *gst = (uint32_t *)(wl + a.w_gst), *grem = gst + E, *gcnt = grem + E, *gfirst = gcnt + E;
 
   const int64_t stride = (int64_t)gridDim.x * a.waves_per_block;
   const int64_t first = (int64_t)blockIdx.x * a.waves_per_block + wave;
@@ -234,11 +429,21 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_eval_kernel(TreeArgs a) 
     }
     for (int j = lane; j < CV; j += 64) par[j] = 0;
     for (int j = lane; j < E * MW; j += 64) lmask[j] = 0;
+    if (kAny) {
+      for (int j = lane; j < CV; j += 64) {
+        pend[j] = 0;
+        rdy[j] = 0;
+        fin[j] = kNotYet;
+      }
+      for (int j = lane; j < E; j += 64) gcnt[j] = 0;
+    }
     wave_sync();
 
     // ---- 2+3. lane = chunk: first-reach tree, then heights and keys -------
-    const bool ok = build_trees<true>(a, s_rec, s_cost, s_own, s_post, rt, key, par, ord,
-                                      lmask, lane);
+    const bool ok = rs ? build_trees<true, true>(a, s_rec, s_cost, s_own, s_post, rt, key, par,
+                                                 ord, lmask, lane, pend)
+                       : build_trees<true>(a, s_rec, s_cost, s_own, s_post, rt, key, par, ord,
+                                           lmask, lane);
     wave_sync();
     {
       // link bases: exclusive scan of the mask popcounts
@@ -298,50 +503,64 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_eval_kernel(TreeArgs a) 
       chain[lbase[l] + rank] = (pred << 16) | (uint32_t)s;
     }
     wave_sync();
-    for (int s = lane; s < CV; s += 64) lds_put(&fin[s], kNotYet);
-    wave_sync();
+    if (!kAny) {
+      for (int s = lane; s < CV; s += 64) lds_put(&fin[s], kNotYet);
+      wave_sync();
+    }
 
     // ---- 5. least schedule: links advance through their orders -----------
     const uint32_t total = lbase[E];
     uint32_t mk = 0;
     bool fault = false;
-    for (uint32_t round = 0;; round++) {
-      bool pending = false;
-      for (int l = lane; l < E; l += 64) {
-        uint32_t h = lhead[l];
-        const uint32_t e = lbase[l + 1];
-        if (h == e) continue;
-        uint32_t f = lfree[l];
-        const uint32_t cl = s_cost[l];
-        uint32_t ent = chain[h];
-        while (true) {
-          const uint32_t nxt = (h + 1 < e) ? chain[h + 1] : 0u;  // read ahead
-          const uint32_t p = ent >> 16;
-          const uint32_t ready = (p == kNoPred) ? 0u : lds_get(&fin[p]);
-          if (ready == kNotYet) break;
-          f = max(ready, f) + cl;
-          lds_put(&fin[ent & 0xFFFFu], f);
-          if (++h == e) break;
-          ent = nxt;
+    if (kAny) {
+      fault = any_schedule(a, rs, lane, s_cost, s_src, s_own, key, prio, par, chain, lbase, lhead,
+                           lfree, fin, pend, rdy, gst, grem, gcnt, gfirst, mk);
+    } else {
+      for (uint32_t round = 0;; round++) {
+        bool pending = false;
+        for (int l = lane; l < E; l += 64) {
+          uint32_t h = lhead[l];
+          const uint32_t e = lbase[l + 1];
+          if (h == e) continue;
+          uint32_t f = lfree[l];
+          const uint32_t cl = s_cost[l];
+          uint32_t ent = chain[h];
+          while (true) {
+            const uint32_t nxt = (h + 1 < e) ? chain[h + 1] : 0u;  // read ahead
+            const uint32_t p = ent >> 16;
+            const uint32_t ready = (p == kNoPred) ? 0u : lds_get(&fin[p]);
+            if (ready == kNotYet) break;
+            f = max(ready, f) + cl;
+            lds_put(&fin[ent & 0xFFFFu], f);
+            if (++h == e) break;
+            ent = nxt;
+          }
+          lhead[l] = h;
+          lfree[l] = f;
+          mk = max(mk, f);
+          pending |= h < e;
         }
-        lhead[l] = h;
-        lfree[l] = f;
-        mk = max(mk, f);
-        pending |= h < e;
-      }
-      if (__ballot(pending) == 0) break;
-      if (round > total) {  // unreachable: the order is acyclic
-        fault = true;
-        break;
+        if (__ballot(pending) == 0) break;
+        if (round > total) {  // unreachable: the order is acyclic
+          fault = true;
+          break;
+        }
       }
     }
 
     // ---- 6. postcondition and makespan -----------------------------------
     const bool all_ok = __ballot(!ok) == 0;
+    fault = __ballot(fault) != 0;
     mk = wave_max(mk);
     if (lane == 0) {
-      a.makespan[i] = fault ? 0xFFFFFFFFu : mk;
-      a.valid[i] = (uint8_t)(all_ok && !fault);
+      if (kAny && a.accumulate) {  // second phase of an Allreduce
+        const uint32_t m0 = a.makespan[i];
+        a.makespan[i] = (fault || m0 == 0xFFFFFFFFu) ? 0xFFFFFFFFu : m0 + mk;
+        a.valid[i] = (uint8_t)(a.valid[i] && all_ok && !fault);
+      } else {
+        a.makespan[i] = fault ? 0xFFFFFFFFu : mk;
+        a.valid[i] = (uint8_t)(all_ok && !fault);
+      }
     }
     wave_sync();
   }
@@ -1466,21 +1685,46 @@ int32_t tree_layout(const taccl_plan &p, TreeArgs &a) {
   return a.o_wave + a.wave_bytes;  // bytes for a one-wave block
 }
 
+int32_t tree_any_layout(const taccl_plan &p, TreeArgs &a) {
+  if (tree_layout(p, a) <= 0) return 0;
+  const int32_t CV = p.coll.C * p.topo.V, E = p.topo.E;
+  int32_t w = a.wave_bytes;
+  auto wtake = [&](int32_t bytes) {
+    int32_t o = w;
+    w = align16(w + bytes);
+    return o;
+  };
+  a.w_gfin = wtake(4 * CV);
+  a.w_grdy = wtake(4 * CV);
+  a.w_gpend = wtake(4 * CV);
+  a.w_gst = wtake(16 * E);
+  a.wave_bytes = w;
+  return a.o_wave + a.wave_bytes;
+}
+
 int32_t tree_block_bytes(const TreeArgs &a, int waves) { return a.o_wave + waves * a.wave_bytes; }
 
-hipError_t launch_tree(const TreeArgs &a, int grid, hipStream_t stream) {
+template <bool kAny>
+static void launch_tree_v(const TreeArgs &a, int grid, hipStream_t stream) {
   const bool pf = a.routes_word_aligned && a.route_stride <= 4 * 64 * kPfRoute &&
                   a.C * a.V <= 64 * kPfPrio;
   const dim3 g(grid), b(64 * a.waves_per_block);
   const int bytes = tree_block_bytes(a, a.waves_per_block);
   if (a.rec_in_lds && pf)
-    hipLaunchKernelGGL((tree_eval_kernel<true, true>), g, b, bytes, stream, a);
+    hipLaunchKernelGGL((tree_eval_kernel<true, true, kAny>), g, b, bytes, stream, a);
   else if (a.rec_in_lds)
-    hipLaunchKernelGGL((tree_eval_kernel<true, false>), g, b, bytes, stream, a);
+    hipLaunchKernelGGL((tree_eval_kernel<true, false, kAny>), g, b, bytes, stream, a);
   else if (pf)
-    hipLaunchKernelGGL((tree_eval_kernel<false, true>), g, b, bytes, stream, a);
+    hipLaunchKernelGGL((tree_eval_kernel<false, true, kAny>), g, b, bytes, stream, a);
   else
-    hipLaunchKernelGGL((tree_eval_kernel<false, false>), g, b, bytes, stream, a);
+    hipLaunchKernelGGL((tree_eval_kernel<false, false, kAny>), g, b, bytes, stream, a);
+}
+
+hipError_t launch_tree(const TreeArgs &a, int grid, hipStream_t stream) {
+  if (a.any)
+    launch_tree_v<true>(a, grid, stream);
+  else
+    launch_tree_v<false>(a, grid, stream);
   return hipGetLastError();
 }
 

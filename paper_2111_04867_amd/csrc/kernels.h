@@ -57,6 +57,9 @@ struct TreeArgs {
   // ancestor doubling of the slot-parallel trees: rounds (2^rounds >= V) and
   // the per-round arrays of 16-bit slots (anc_stride slots apart)
   int32_t w_anc, pj_rounds, anc_stride;
+  // general variant (any != 0): time-aware greedy instead of the static
+  // order, and the per-link state of open contiguous transfers
+  int32_t any, greedy, w_gst;
 };
 
 // Alltoall evaluation: one block per candidate, level by level.
@@ -147,6 +150,9 @@ constexpr int kPathFastThreads = 1024;  // largest block of the register-residen
 
 // Fill the LDS layout; returns the bytes needed by a one-wavefront block.
 int32_t tree_layout(const taccl_plan &p, TreeArgs &a);
+// The same for the general variant (ReduceScatter, contiguous transfers and
+// greedy orders on plans outside the layered kernel's limits).
+int32_t tree_any_layout(const taccl_plan &p, TreeArgs &a);
 int32_t tree_block_bytes(const TreeArgs &a, int waves);
 // Layered multicast kernel: fills the layout and returns the bytes of a
 // one-wavefront block, or 0 when the plan does not meet its conditions.

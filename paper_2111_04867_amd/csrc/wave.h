@@ -78,5 +78,8 @@ __device__ __forceinline__ uint32_t wave_scan_max(uint32_t v) {
 __device__ __forceinline__ uint32_t wave_reduce_max(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_readlane((int)wave_scan_max(v), 63);
 }
+__device__ __forceinline__ uint64_t wave_reduce_max64(uint64_t v) {
+  return readlane64(wave_scan_max64(v), 63);
+}
 
 }  // namespace taccl

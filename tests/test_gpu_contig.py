@@ -132,15 +132,14 @@ def test_closed_forms(m):
     assert ok.all() and (mk == cost(IB_A, IB_B, m * S) + m * cost(NV_A, NV_B, S)).all()
 
 
-def test_round_based_kernel_refuses_contiguity():
+def test_large_plan_on_the_general_kernel():
     """A multicast plan too large for the layered kernel (C*V > 1024) runs on
-    the round-based kernel, which has no contiguous transfers: refused."""
-    from paper_2111_04867_amd.binding import Plan, TacclError
-    w = cf.uni_ring_ag(40)
+    the general kernel's variant, contiguous transfers included."""
+    w = cf.uni_ring_ag(40, chunk_bytes=65536)
     w.node_of = np.array([r // 20 for r in range(40)], dtype=np.int32)
     w.contiguity = 1
-    plan = Plan.from_workload(w)
-    routes, prio = generate(1, 0, 4, plan.route_options(), plan.prio_stride)
-    with pytest.raises(TacclError) as e:
-        plan.eval(routes, prio)
-    assert "contiguous" in str(e.value)
+    plan, ref, opts = plans(w)
+    routes, prio = generate(1, 0, 24, opts, plan.prio_stride)
+    prio[:, ::3] = 9
+    mk, ok = check(plan, ref, routes, prio, "uniring40 contig")
+    assert ok.all()

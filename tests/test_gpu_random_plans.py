@@ -5,8 +5,8 @@ mode, static or greedy orders, contiguity, switch ports), each evaluated on
 bit against the oracle through the C ABI. Plans the route search refuses on
 both sides are skipped (the host test checks that both sides agree on
 which), and so are plans outside the documented limits of the kernel an
-option needs (reductions, contiguity and greedy orders run only in the
-layered multicast kernel); the test counts both. Needs an MI355X."""
+option needs (Alltoall greedy orders hold at most 1024 send slots); the test
+counts both. Needs an MI355X."""
 import numpy as np
 import pytest
 
@@ -65,4 +65,4 @@ def test_random_plans(block):
                                f"{rok[bad[:5]].tolist()}")
         checked += 1
     print(f"[gpu] block {block}: {checked} plans checked, {refused} refused", flush=True)
-    assert checked >= 40
+    assert checked >= 75

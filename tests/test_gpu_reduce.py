@@ -105,12 +105,11 @@ def test_equal_priorities(value):
     check(plan, ref, routes, prio, f"twonode16_ar prio={value:#x}")
 
 
-def test_plans_outside_the_layered_kernel_are_refused():
-    """Three ranks: not a multiple of 4, so no layered kernel, so refused."""
-    from paper_2111_04867_amd.binding import Plan, TacclError
-    w = cf.as_reduction(cf.full_ag(3, k=2), cf.REDUCESCATTER)
-    plan = Plan.from_workload(w)
-    routes, prio = generate(1, 0, 4, plan.route_options(), plan.prio_stride)
-    with pytest.raises(TacclError) as e:
-        plan.eval(routes, prio)
-    assert "ReduceScatter" in str(e.value)
+@pytest.mark.parametrize("kind", [cf.REDUCESCATTER, cf.ALLREDUCE])
+def test_plans_outside_the_layered_kernel(kind):
+    """Three ranks: not a multiple of 4, so the general kernel's variant."""
+    w = cf.as_reduction(cf.full_ag(3, k=2), kind)
+    plan, ref, opts = plans(w)
+    routes, prio = generate(1, 0, 200, opts, plan.prio_stride)
+    prio[::2, ::2] = 3
+    check(plan, ref, routes, prio, f"full3 kind={kind}")
