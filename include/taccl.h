@@ -148,8 +148,13 @@ void taccl_collective_destroy(taccl_collective_t coll);
  *     travelled path asc, priority, chunk); 1 = the time-aware greedy of
  *     App. B.2: round by round, among the sends whose chunk has arrived, the
  *     one that can start earliest (max of link time and chunk time) goes
- *     next, ties broken by the Step-2 key. Not combined with contiguity
- *     (INVALID_ARGUMENT). On the GPU it is evaluated for every multicast
+ *     next, ties broken by the Step-2 key; 2 = the same greedy in reverse
+ *     path order (App. B.2): it serves the mirrored schedule (every chunk
+ *     dependency reversed, remaining and travelled lengths measured from
+ *     the other end), each link's order is the reverse of the order it was
+ *     served in, and those orders are timed as for 0. Greedy orders are not
+ *     combined with contiguity (INVALID_ARGUMENT). On the GPU they are
+ *     evaluated for every multicast
  *     plan (Allgather, explicit, ReduceScatter, Allreduce) and for Alltoall
  *     plans with at most 256 links and 1024 send slots (chunks x longest
  *     route option); larger Alltoall plans are refused at evaluation

@@ -129,7 +129,8 @@ class OraclePlan:
         self.switch_ports = int(mode)
 
     def set_order(self, mode):
-        """0: static Step-2 orders; 1: time-aware greedy orders (App. B.2)."""
+        """0: static Step-2 orders; 1: time-aware greedy orders (App. B.2) in
+        path order; 2: the same greedy in reverse path order."""
         if _load().orc_set_order(self._h, int(mode)) != 0:
             raise OracleError(f"bad order mode {mode}")
         self.order = int(mode)

@@ -38,7 +38,8 @@
  * earliest (max of its link's time and its chunk's time) is scheduled next,
  * ties broken by the Step-2 heuristics, then priority, then chunk id; its
  * link and chunk times advance by the link latency. The orders it produces
- * are timed by the same rule as above (the greedy's own times).
+ * are timed by the same rule as above (the greedy's own times). Mode 2 runs
+ * the greedy in reverse path order (see reverse_greedy_orders).
  *
  * Optionally (orc_set_switch_ports), Alltoall hops through a switch vertex
  * follow the switch model of App. B.3: the pair rank -> switch -> rank is one
@@ -416,9 +417,10 @@ int orc_set_switch_ports(orc_plan *p, int mode) {
   return ORC_OK;
 }
 
-/* 0: static Step-2 orders (Sec. 5.1); 1: time-aware greedy (App. B.2). */
+/* 0: static Step-2 orders (Sec. 5.1); 1: time-aware greedy (App. B.2) in
+ * path order; 2: the same greedy in reverse path order. */
 int orc_set_order(orc_plan *p, int mode) {
-  if (!p || mode < 0 || mode > 1) return ORC_EINVAL;
+  if (!p || mode < 0 || mode > 2) return ORC_EINVAL;
   p->greedy = mode;
   return ORC_OK;
 }
@@ -1034,6 +1036,91 @@ static int greedy_sweep(const orc_plan *p, oscratch *w, uint32_t *makespan, uint
   return ORC_OK;
 }
 
+/* Greedy in reverse path order. App. B.2 notes that the greedy may start
+ * from the first link of every path or from the last one. Reading: the
+ * greedy of greedy_sweep runs on the mirrored schedule, in which every
+ * chunk dependency points the other way (a send waits for every send that
+ * waited for it) and the two Step-2 lengths trade places (remaining' =
+ * travelled + the send's own latency, travelled' = remaining - that
+ * latency); links and latencies stay. The mirrored greedy serves every link
+ * in some order; the link's order in the real schedule is the reverse, and
+ * the real times then come from the App. B.3 rule with these orders (the
+ * caller's DAG sweep). Sets pos and lpred of every send. */
+static int reverse_greedy_orders(const orc_plan *p, oscratch *w) {
+  int n = w->n, E = p->E;
+  int *waiting = w->indeg; /* mirrored: forward successors not yet served */
+  uint64_t *ready = (uint64_t *)calloc((size_t)(n > 0 ? n : 1), sizeof(uint64_t));
+  uint64_t *busy = (uint64_t *)calloc((size_t)(E > 0 ? E : 1), sizeof(uint64_t));
+  int *count = (int *)calloc((size_t)(E > 0 ? E : 1) + 1, sizeof(int));
+  uint8_t *done = (uint8_t *)calloc((size_t)(n > 0 ? n : 1), 1);
+  for (int i = 0; i < n; i++) waiting[i] = 0;
+  for (int i = 0; i < n; i++)
+    for (int j = w->pred_ptr[i]; j < w->pred_ptr[i + 1]; j++) waiting[w->pred[j]]++;
+  for (int i = 0; i < n; i++) { /* mirrored lengths */
+    osend *s = &w->s[i];
+    uint64_t c = p->cost[s->link], rem = s->rem;
+    s->rem = s->trav + c;
+    s->trav = rem - c;
+  }
+  g_sort_base = w->s;
+  int rc = ORC_OK;
+  for (int step = 0; step < n; step++) {
+    int best = -1;
+    uint64_t best_t = 0;
+    for (int i = 0; i < n; i++) {
+      if (done[i] || waiting[i]) continue;
+      uint64_t b = busy[w->s[i].link];
+      uint64_t t = ready[i] > b ? ready[i] : b;
+      if (best < 0 || t < best_t || (t == best_t && send_order_cmp(&i, &best) < 0)) {
+        best = i;
+        best_t = t;
+      }
+    }
+    if (best < 0) {
+      rc = ORC_EINVAL; /* nothing servable: cannot happen */
+      break;
+    }
+    osend *s = &w->s[best];
+    uint64_t f = best_t + p->cost[s->link];
+    busy[s->link] = f;
+    s->pos = count[s->link]++;
+    done[best] = 1;
+    /* the sends it waited for in the real schedule may now be served */
+    for (int j = w->pred_ptr[best]; j < w->pred_ptr[best + 1]; j++) {
+      int q = w->pred[j];
+      waiting[q]--;
+      if (f > ready[q]) ready[q] = f;
+    }
+  }
+  for (int i = 0; i < n; i++) { /* lengths back */
+    osend *s = &w->s[i];
+    uint64_t c = p->cost[s->link], trav = s->rem - c;
+    s->rem = s->trav + c;
+    s->trav = trav;
+  }
+  if (rc == ORC_OK) {
+    /* the real order of each link is the reverse of the mirrored one */
+    int *off = (int *)calloc((size_t)(E > 0 ? E : 1) + 1, sizeof(int));
+    for (int e = 0; e < E; e++) off[e + 1] = off[e] + count[e];
+    for (int i = 0; i < n; i++) {
+      osend *s = &w->s[i];
+      s->pos = count[s->link] - 1 - s->pos;
+      w->idx[off[s->link] + s->pos] = i;
+    }
+    for (int i = 0; i < n; i++) {
+      osend *s = &w->s[i];
+      s->lpred = s->pos > 0 ? w->idx[off[s->link] + s->pos - 1] : -1;
+      s->lpred2 = -1;
+    }
+    free(off);
+  }
+  free(ready);
+  free(busy);
+  free(count);
+  free(done);
+  return rc;
+}
+
 /* One schedule: `phase` is ORC_ALLGATHER, ORC_ALLTOALL, ORC_EXPLICIT or
  * ORC_REDUCESCATTER (the send sets differ; ordering and timing do not). */
 static int eval_phase(const orc_plan *p, int phase, const uint8_t *rt, const uint32_t *pr,
@@ -1092,7 +1179,11 @@ static int eval_phase(const orc_plan *p, int phase, const uint8_t *rt, const uin
   chunk_preds(w);
   if (p->greedy && p->contig) return ORC_EINVAL; /* not combined */
   if (p->ports && (p->greedy || p->contig)) return ORC_EINVAL;
-  if (p->greedy) return greedy_sweep(p, w, makespan, valid);
+  if (p->greedy == 1) return greedy_sweep(p, w, makespan, valid);
+  if (p->greedy == 2) {
+    int rc = reverse_greedy_orders(p, w);
+    if (rc) return rc;
+  }
   if (p->contig) return contig_sweep(p, w, makespan, valid);
   /* the difference constraints of App. B.3 without contiguity form a DAG
    * (chunk edges and link-order edges); sweep it in topological order */

@@ -146,6 +146,7 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
       return fail(TACCL_ERR_UNSUPPORTED,
                   "time-aware greedy orders for Alltoall need at most 1024 send slots "
                   "(chunks x longest path) and 256 links");
+    g.mirror = p->greedy == 2;
     g.C = p->coll.C;
     g.P = p->topo.P;
     g.E = p->topo.E;
@@ -261,9 +262,10 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     a.valid = d_valid;
     a.n = n;
     // the layered kernel needs whole route words and priorities in registers
+    // greedy orders in reverse path order run on the general kernel only
     const bool greedy = p->greedy != 0;
     const bool layered =
-        a.routes_word_aligned &&
+        p->greedy != 2 && a.routes_word_aligned &&
         (greedy ? tree_greedy_layout(*p, a) : tree_layers_layout(*p, a)) > 0 &&
         tree_block_bytes(a, 1) <= t->max_lds;
     const int kind = p->coll.kind;
@@ -271,7 +273,7 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     // plans outside the layered kernel's limits: the general kernel, whose
     // variant with reductions, contiguity and greedy orders keeps more state
     a.any = !layered && (reduction || p->contig || greedy);
-    a.greedy = greedy;
+    a.greedy = p->greedy;
     if (!layered && (a.any ? tree_any_layout(*p, a) : tree_layout(*p, a)) > t->max_lds)
       return fail(TACCL_ERR_UNSUPPORTED, "multicast plan needs more LDS than a block has");
     a.lrev = t->lrev;

@@ -152,37 +152,48 @@ __device__ __forceinline__ bool build_trees(const TreeArgs &a, const uint32_t *s
 // Step 5' of the general variant, one wavefront per candidate. Sends sit
 // in chain[] in link order (pred << 16 | slot, pred = the slot whose send
 // brings the chunk to the link's source, or kNoPred), fin[] = kNotYet.
-//  * Allgather: a send is ready when its pred has finished.
-//  * ReduceScatter (rs): the send of slot (c,v) goes v -> u on the reverse
+// Two dependency forms:
+//  * pull (Allgather): a send is ready when the send of slot (c, src) into
+//    its source has finished;
+//  * push (ReduceScatter): the send of slot (c,v) goes v -> u on the reverse
 //    of its tree link and carries v's partial, so it is ready when every
 //    send into v has finished: pend[] counts them down and rdy[] keeps the
 //    latest finish (the decrement is a release and its read an acquire, so
 //    a zero count sees every max before it).
-//  * Contiguous transfers (a.contig) on links between nodes: the link's
-//    next send either joins the open transfer (same remaining length, chunk
-//    ready by the transfer's start; m sends cost alpha + ceil(beta*m*S/1000))
-//    or closes it and opens a new one. Finish times of a transfer's sends
-//    are published only when it closes, so no dependant reads a time that
-//    could still grow. A joiner's pred has a strictly longer remaining path
-//    than the transfer, so waiting for it never waits on the transfer.
-//  * Time-aware greedy (a.greedy, App. B.2): send by send, the unscheduled
-//    ready send with the smallest (max(ready, link free), Step-2 key,
-//    priority, slot) is scheduled, by four wavefront reductions.
+// Timing:
+//  * static orders: links advance through chain[] in rounds. Contiguous
+//    transfers (a.contig) on links between nodes: the link's next send
+//    either joins the open transfer (same remaining length, chunk ready by
+//    the transfer's start; m sends cost alpha + ceil(beta*m*S/1000)) or
+//    closes it and opens a new one. Finish times of a transfer's sends are
+//    published only when it closes, so no dependant reads a time that could
+//    still grow; a joiner's pred has a strictly longer remaining path than
+//    the transfer, so waiting for it never waits on the transfer;
+//  * time-aware greedy (a.greedy == 1, App. B.2): send by send, the
+//    unserved ready send with the smallest (max(ready, link free), Step-2
+//    key, priority, slot) is served, by four wavefront reductions;
+//  * greedy in reverse path order (a.greedy == 2): the same greedy on the
+//    mirrored schedule, whose dependencies are the other form (Allgather
+//    sends wait for the sends out of their destination, ReduceScatter sends
+//    for the send that carries their partial on) and whose keys the caller
+//    built with the lengths measured from the other end; a link's real
+//    order is the reverse of the order the mirrored greedy served it in,
+//    and the real times come from the static rounds over those orders.
 // Returns true on a fault (no progress; unreachable for valid orders).
 __device__ __noinline__ bool any_schedule(const TreeArgs &a, bool rs, int lane,
                                           const uint32_t *s_cost, const uint8_t *s_src,
                                           const uint8_t *s_own, const uint64_t *key,
                                           const uint32_t *prio, const uint16_t *par,
-                                          const uint32_t *chain, const uint32_t *lbase,
+                                          uint32_t *chain, const uint32_t *lbase,
                                           uint32_t *lhead, uint32_t *lfree, uint32_t *fin,
                                           uint32_t *pend, uint32_t *rdy, uint32_t *gst,
                                           uint32_t *grem, uint32_t *gcnt, uint32_t *gfirst,
                                           uint32_t &mk) {
   const int V = a.V, E = a.E, CV = a.C * a.V;
   const uint32_t total = lbase[E];
-  auto ready_of = [&](uint32_t ent) -> uint32_t {
+  auto ready_of = [&](uint32_t ent, bool push) -> uint32_t {
     const uint32_t s = ent & 0xFFFFu;
-    if (rs) {
+    if (push) {
       if (__hip_atomic_load(&pend[s], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP))
         return kNotYet;
       return lds_get(&rdy[s]);
@@ -190,9 +201,9 @@ __device__ __noinline__ bool any_schedule(const TreeArgs &a, bool rs, int lane,
     const uint32_t p = ent >> 16;
     return p == kNoPred ? 0u : lds_get(&fin[p]);
   };
-  auto publish = [&](uint32_t s, uint32_t f, int l) {
+  auto publish = [&](uint32_t s, uint32_t f, int l, bool push) {
     lds_put(&fin[s], f);
-    if (rs) {
+    if (push) {
       const uint32_t c = div_v(s, a.vmagic);
       const int u = s_src[l];
       if (u != s_own[c]) {
@@ -204,6 +215,9 @@ __device__ __noinline__ bool any_schedule(const TreeArgs &a, bool rs, int lane,
   };
 
   if (a.greedy) {
+    // served sends get fin; mirrored runs record the service position on
+    // the link in pend[] (dead once a send is served) and leave mk alone
+    const bool mirror = a.greedy == 2, push = rs != mirror;
     for (uint32_t step = 0; step < total; step++) {
       uint32_t bt = ~0u, bp = ~0u, bs = ~0u;
       uint64_t bk = ~0ull;
@@ -212,7 +226,7 @@ __device__ __noinline__ bool any_schedule(const TreeArgs &a, bool rs, int lane,
         if (!pl || lds_get(&fin[s]) != kNotYet) continue;
         const int l = pl - 1;
         uint32_t r;
-        if (rs) {
+        if (push) {
           if (lds_get(&pend[s])) continue;
           r = lds_get(&rdy[s]);
         } else {
@@ -242,12 +256,46 @@ __device__ __noinline__ bool any_schedule(const TreeArgs &a, bool rs, int lane,
       const uint32_t f = tmin + s_cost[l];
       if (lane == 0) {
         lfree[l] = f;
-        publish(smin, f, l);
+        publish(smin, f, l, push);
+        if (mirror) lds_put(&pend[smin], gcnt[l]++);
       }
-      mk = max(mk, f);
+      if (!mirror) mk = max(mk, f);
       wave_sync();
     }
-    return false;
+    if (!mirror) return false;
+    // the real orders: reversed service orders, with the pred slot of the
+    // real schedule's pull form
+    for (int s = lane; s < CV; s += 64) {
+      const int pl = par[s];
+      if (!pl) continue;
+      const int l = pl - 1;
+      const uint32_t c = div_v(s, a.vmagic);
+      const int u = s_src[l];
+      const uint32_t pred = (u == s_own[c]) ? kNoPred : c * V + u;
+      const uint32_t n_l = lbase[l + 1] - lbase[l];
+      chain[lbase[l] + n_l - 1 - pend[s]] = (pred << 16) | (uint32_t)s;
+    }
+    wave_sync();
+    for (int s = lane; s < CV; s += 64) {
+      fin[s] = kNotYet;
+      pend[s] = 0;
+      rdy[s] = 0;
+    }
+    for (int l = lane; l < E; l += 64) {
+      lhead[l] = lbase[l];
+      lfree[l] = 0;
+      gcnt[l] = 0;
+    }
+    wave_sync();
+    if (rs)  // the real ReduceScatter counts the sends into every vertex
+      for (int s = lane; s < CV; s += 64) {
+        const int pl = par[s];
+        if (!pl) continue;
+        const uint32_t c = div_v(s, a.vmagic);
+        const int u = s_src[pl - 1];
+        if (u != s_own[c]) atomicAdd(&pend[c * V + u], 1u);
+      }
+    wave_sync();
   }
 
   for (uint32_t round = 0;; round++) {
@@ -261,10 +309,10 @@ __device__ __noinline__ bool any_schedule(const TreeArgs &a, bool rs, int lane,
         const uint32_t cl = s_cost[l];
         while (h < e) {
           const uint32_t ent = chain[h];
-          const uint32_t r = ready_of(ent);
+          const uint32_t r = ready_of(ent, rs);
           if (r == kNotYet) break;
           f = max(r, f) + cl;
-          publish(ent & 0xFFFFu, f, l);
+          publish(ent & 0xFFFFu, f, l, rs);
           h++;
         }
         pending |= h < e;
@@ -276,7 +324,7 @@ __device__ __noinline__ bool any_schedule(const TreeArgs &a, bool rs, int lane,
         const uint64_t bsz = a.lbs[le];
         while (true) {
           if (h == e) {
-            for (uint32_t j = g0; j < h && gm; j++) publish(chain[j] & 0xFFFFu, f, l);
+            for (uint32_t j = g0; j < h && gm; j++) publish(chain[j] & 0xFFFFu, f, l, rs);
             gm = 0;
             break;
           }
@@ -284,7 +332,7 @@ __device__ __noinline__ bool any_schedule(const TreeArgs &a, bool rs, int lane,
           const uint32_t rem = ~(uint32_t)(key[ent & 0xFFFFu] >> 32);
           uint32_t r = kNotYet;
           if (gm && rem == gr) {
-            r = ready_of(ent);
+            r = ready_of(ent, rs);
             if (r == kNotYet) break;
             if (r <= gs) {  // joins the open transfer
               gm++;
@@ -293,9 +341,9 @@ __device__ __noinline__ bool any_schedule(const TreeArgs &a, bool rs, int lane,
               continue;
             }
           }
-          for (uint32_t j = g0; j < h && gm; j++) publish(chain[j] & 0xFFFFu, f, l);
+          for (uint32_t j = g0; j < h && gm; j++) publish(chain[j] & 0xFFFFu, f, l, rs);
           gm = 0;
-          if (r == kNotYet) r = ready_of(ent);
+          if (r == kNotYet) r = ready_of(ent, rs);
           if (r == kNotYet) break;
           gs = max(r, f);
           f = gs + al + (uint32_t)((bsz + 999) / 1000);
@@ -440,7 +488,10 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_eval_kernel(TreeArgs a) 
     wave_sync();
 
     // ---- 2+3. lane = chunk: first-reach tree, then heights and keys -------
-    const bool ok = rs ? build_trees<true, true>(a, s_rec, s_cost, s_own, s_post, rt, key, par,
+    // reverse path order measures the Step-2 lengths from the other end:
+    // the keys (and child counts) of the other direction
+    const bool up = rs != (kAny && a.greedy == 2);
+    const bool ok = up ? build_trees<true, true>(a, s_rec, s_cost, s_own, s_post, rt, key, par,
                                                  ord, lmask, lane, pend)
                        : build_trees<true>(a, s_rec, s_cost, s_own, s_post, rt, key, par, ord,
                                            lmask, lane);
@@ -1201,7 +1252,8 @@ constexpr int kGreedyLinkSlots = 4;  // links per lane: at most 256 links
 // the other slot being the send the chunk arrives by (its finish is the
 // ready time; kNoPred: ready at 0) or, for ReduceScatter, the send that
 // carries the partial on (ready once every input is scheduled). gfin[slot]
-// must be kNotYet for every pending send. The Alltoall kernel calls it out of
+// must be kNotYet for every pending send. On return every link's list holds
+// its sends in the reverse of the order they were served in. The Alltoall kernel calls it out of
 // line; the multicast kernel carries the same loop inline (inlining this
 // function into either kernel gave results that failed the parity tests,
 // while the out-of-line call and the kernel's own inline loop pass them).
@@ -1286,7 +1338,10 @@ __device__ __noinline__ void greedy_windows(int E, int lane, int nslots, uint32_
         gfin[x] = f;
         lf[t] = f;
         mk = max(mk, f);
+        // swap with the last pending record: the served ones collect at the
+        // end of the link's list, latest first
         grec[lb[t] + cq[t]] = grec[lb[t] + ln[t] - 1];
+        grec[lb[t] + ln[t] - 1] = rc;
         ln[t]--;
       }
     }
@@ -1300,7 +1355,11 @@ __device__ __noinline__ void greedy_windows(int E, int lane, int nslots, uint32_
 // (the first at 0). One wavefront per candidate: the sends are counted per
 // link, laid out as per-link lists of packed records (key from the path's
 // remaining and travelled costs, priority of slot c*H + h), and the greedy
-// runs window by window as for the multicast trees.
+// runs window by window as for the multicast trees. In reverse path order
+// (a.mirror) the greedy runs on the mirrored schedule: a hop waits for the
+// hop after it, the Step-2 lengths are measured from the path's end, and
+// the lists it leaves (served order reversed) are the real link orders,
+// which links then advance through in rounds to give the real times.
 __global__ __launch_bounds__(kTreeMaxThreads) void path_greedy_kernel(PathGreedyArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int C = a.C, P = a.P, E = a.E, H = a.H;
@@ -1368,10 +1427,16 @@ __global__ __launch_bounds__(kTreeMaxThreads) void path_greedy_kernel(PathGreedy
         const uint32_t l = a.path_links[j], h = j - j0;
         const uint32_t rem = total - trav;  // remaining path, this hop included
         const uint32_t sl = (uint32_t)c * H + h;
-        const uint32_t other = h ? sl - 1 : kNoPred;  // the hop the chunk arrives by
+        const uint32_t cl = s_cost[l];
         const uint32_t pos = atomicAdd(&gcur[l], 1u);
-        grec[pos] = make_uint4(trav, ~rem, gpr[sl], sl | (other << 16));
-        trav += s_cost[l];
+        if (a.mirror) {  // waits for the next hop; lengths from the path's end
+          const uint32_t other = (j + 1 < j1) ? sl + 1 : kNoPred;
+          grec[pos] = make_uint4(rem - cl, ~(trav + cl), gpr[sl], sl | (other << 16));
+        } else {
+          const uint32_t other = h ? sl - 1 : kNoPred;  // the hop the chunk arrives by
+          grec[pos] = make_uint4(trav, ~rem, gpr[sl], sl | (other << 16));
+        }
+        trav += cl;
       }
     }
     wave_sync();
@@ -1379,6 +1444,45 @@ __global__ __launch_bounds__(kTreeMaxThreads) void path_greedy_kernel(PathGreedy
     bool fault = false;
     greedy_windows<false>(E, lane, a.nslots, a.cmin, s_cost, grec, gofs, gfin, nullptr, nullptr,
                           mk, fault);
+    if (a.mirror && !__ballot(fault)) {
+      // the real schedule: links advance through the lists in rounds, a hop
+      // ready when the hop before it (slot - 1) has ended
+      mk = 0;
+      wave_sync();
+      for (int sl = lane; sl < a.nslots; sl += 64) gfin[sl] = kNotYet;
+      uint32_t lh[kGreedyLinkSlots], lf[kGreedyLinkSlots];
+#pragma unroll
+      for (int t = 0; t < kGreedyLinkSlots; t++) {
+        const int l = lane + 64 * t;
+        lh[t] = l < E ? gofs[l] : 0u;
+        lf[t] = 0;
+      }
+      wave_sync();
+      for (int round = 0;; round++) {
+        bool pending = false;
+#pragma unroll
+        for (int t = 0; t < kGreedyLinkSlots; t++) {
+          const int l = lane + 64 * t;
+          if (l >= E) continue;
+          const uint32_t e = gofs[l + 1], cl = s_cost[l];
+          while (lh[t] < e) {
+            const uint32_t x = grec[lh[t]].w & 0xFFFFu;
+            const uint32_t r = (x % (uint32_t)H) ? lds_get(&gfin[x - 1]) : 0u;
+            if (r == kNotYet) break;
+            lf[t] = max(r, lf[t]) + cl;
+            lds_put(&gfin[x], lf[t]);
+            mk = max(mk, lf[t]);
+            lh[t]++;
+          }
+          pending |= lh[t] < e;
+        }
+        if (__ballot(pending) == 0) break;
+        if (round > a.nslots) {  // unreachable: the orders come from a schedule
+          fault = true;
+          break;
+        }
+      }
+    }
     const bool all_ok = __ballot(bad) == 0;
     const bool failed = __ballot(fault) != 0;
     mk = wave_max(mk);

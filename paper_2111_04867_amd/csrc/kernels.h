@@ -122,6 +122,7 @@ struct PathGreedyArgs {
   // LDS: link costs, then per wavefront finish times per slot, list
   // offsets and fill pointers per link, pending-send records
   int32_t o_wave, wave_bytes, w_gfin, w_gofs, w_gcur, w_grec;
+  int32_t mirror;  // greedy in reverse path order
 };
 
 // Switch-hyperedge connection count: one block per candidate at a time.

@@ -657,7 +657,8 @@ taccl_status_t taccl_sketch_apply(taccl_topology_t topo, taccl_collective_t coll
   if (sk->contiguity < 0 || sk->contiguity > 1)
     return fail(TACCL_ERR_INVALID_ARGUMENT, "contiguity must be 0 or 1");
   p->contig = sk->contiguity;
-  if (sk->order < 0 || sk->order > 1) return fail(TACCL_ERR_INVALID_ARGUMENT, "order must be 0 or 1");
+  if (sk->order < 0 || sk->order > 2)
+    return fail(TACCL_ERR_INVALID_ARGUMENT, "order must be 0, 1 or 2");
   if (sk->switch_ports < 0 || sk->switch_ports > 1)
     return fail(TACCL_ERR_INVALID_ARGUMENT, "switch_ports must be 0 or 1");
   if (sk->switch_ports && (sk->order || sk->contiguity))

@@ -426,6 +426,53 @@ def reduce_least_schedule(sends, cost, orders):
     return t, [t[i] + cost[s["link"]] for i, s in enumerate(sends)]
 
 
+def reduce_deps(sends):
+    """Chunk predecessors of every ReduceScatter send: the sends into its source."""
+    return [[j for j, y in enumerate(sends) if y["chunk"] == x["chunk"] and y["to"] == x["frm"]]
+            for x in sends]
+
+
+def greedy_link_orders(sends, cost, deps, reverse=False):
+    """The time-aware greedy of App. B.2 as a plain event loop: at every step
+    every unserved send whose dependencies are all served gets the start
+    max(its link's time, the latest finish among them); the smallest
+    (start, Step-2 key, priority, chunk) is served. deps[i] lists the sends
+    that send i waits for. reverse: the mirrored run, in which a send waits
+    for the sends that waited for it and the Step-2 lengths are measured
+    from the other end (remaining' = travelled + latency, travelled' =
+    remaining - latency); each link's order is then the reverse of the order
+    it was served in. Returns {link: [send index, ...]} in schedule order."""
+    n = len(sends)
+    if reverse:
+        waits = [[j for j in range(n) if i in deps[j]] for i in range(n)]
+    else:
+        waits = deps
+
+    def key(i):
+        s, c = sends[i], cost[sends[i]["link"]]
+        rem, trav = (s["trav"] + c, s["rem"] - c) if reverse else (s["rem"], s["trav"])
+        return (-rem, trav, s["prio"], s["chunk"])
+
+    finish = [None] * n
+    link_time = {}
+    served = {}
+    for _ in range(n):
+        ready = [i for i in range(n)
+                 if finish[i] is None and all(finish[j] is not None for j in waits[i])]
+
+        def start(i):
+            return max([link_time.get(sends[i]["link"], 0)] + [finish[j] for j in waits[i]])
+
+        i = min(ready, key=lambda i: (start(i), key(i)))
+        t = start(i)
+        finish[i] = t + cost[sends[i]["link"]]
+        link_time[sends[i]["link"]] = finish[i]
+        served.setdefault(sends[i]["link"], []).append(i)
+    if reverse:
+        served = {l: order[::-1] for l, order in served.items()}
+    return served
+
+
 def evaluate(w, table, routes, prio, H=None):
     """Makespan, valid and per-send detail of one candidate."""
     if w.kind in (3, 4):  # ReduceScatter, Allreduce

@@ -34,7 +34,7 @@ def gpu():
 def plans(w):
     from paper_2111_04867_amd.binding import Plan
     plan, ref = Plan.from_workload(w), OraclePlan.from_workload(w)
-    assert ref.order == 1
+    assert ref.order == w.order and w.order in (1, 2)
     opts = plan.route_options()
     assert (opts == ref.route_options()).all()
     return plan, ref, opts
@@ -146,3 +146,41 @@ def test_alltoall_too_large_refused():
     with pytest.raises(TacclError) as e:
         plan.eval(routes, prio)
     assert "greedy" in str(e.value)
+
+
+# ---- greedy in reverse path order --------------------------------------------
+# multicast plans run it on the general kernel, Alltoall on the greedy kernel
+
+
+@pytest.mark.parametrize("make,n", [
+    (lambda: cf.cubemesh8_ag(), 512),
+    (lambda: cf.twonode16_ag(), 256),
+    (lambda: cf.as_reduction(cf.twonode16_ag(), cf.REDUCESCATTER), 256),
+    (lambda: cf.as_reduction(cf.twonode16_ag(), cf.ALLREDUCE), 128),
+    (lambda: cf.as_reduction(cf.full_ag(4, k=3, chunks_per_rank=3), cf.ALLREDUCE), 400),
+    (lambda: cf.full_ag(6, k=3, chunks_per_rank=2), 300),
+    (lambda: cf.explicit_multicast(cf.cubemesh8_ag(), [0, 3, 5, 5, 7],
+                                   [[1, 2], [0, 4, 6], [1, 3, 7], [2], [0, 1, 2, 3, 4, 5, 6]]),
+     400),
+    (lambda: cf.full_a2a(4), 300),
+    (lambda: replace(cf.full_a2a(6), chunks_per_rank=2), 300),
+    (lambda: cf.switch16_a2a(), 512),
+    (lambda: cf.two_node_rings_a2a(4, contiguity=0), 300)])
+def test_reverse_path_order(make, n):
+    w = cf.with_reverse_greedy(make())
+    plan, ref, opts = plans(w)
+    routes, prio = generate(w.seed + 21, 0, n, opts, plan.prio_stride)
+    rng = np.random.default_rng(n)
+    routes[rng.random(routes.shape) < 0.01] = 0xFF
+    prio[::3] = 11
+    check(plan, ref, routes, prio, f"{w.name} reverse path order")
+
+
+def test_reverse_path_order_differs_from_path_order():
+    """The two greedy directions give different orders on twonode16_ag."""
+    w = cf.twonode16_ag()
+    fwd, rev = plans(cf.with_greedy(w)), plans(cf.with_reverse_greedy(w))
+    routes, prio = generate(w.seed, 0, 128, fwd[2], fwd[0].prio_stride)
+    m1, _ = check(fwd[0], fwd[1], routes, prio, "twonode16 path order")
+    m2, _ = check(rev[0], rev[1], routes, prio, "twonode16 reverse path order")
+    assert (m1 != m2).any()

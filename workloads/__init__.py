@@ -8,5 +8,5 @@ from .configs import (ALLGATHER, ALLREDUCE, ALLTOALL, CONTIG_ORDER, EXPLICIT, HI
                       GREEDY_ORDER, KSHORTEST, NAMED, ORDER, PORTS_ORDER, REDUCE_ORDER,
                       REDUCESCATTER, RELAY1, SHORTEST_ONLY, Workload, as_reduction, named,
                       random_workload,
-                      with_contiguity, with_greedy, with_switch_ports)
+                      with_contiguity, with_greedy, with_reverse_greedy, with_switch_ports)
 from .candgen import build_candgen, generate  # noqa: F401

@@ -269,6 +269,12 @@ def with_greedy(w):
                    description=w.description + "; time-aware greedy link orders")
 
 
+def with_reverse_greedy(w):
+    """The same workload with time-aware greedy orders in reverse path order."""
+    return replace(w, name=w.name + "_rgreedy", order=2,
+                   description=w.description + "; time-aware greedy in reverse path order")
+
+
 NAMED["twonode16_ag_greedy"] = lambda **kw: with_greedy(twonode16_ag(**kw))
 NAMED["cubemesh8_ag_greedy"] = lambda **kw: with_greedy(cubemesh8_ag(**kw))
 NAMED["switch16_a2a_greedy"] = lambda **kw: with_greedy(switch16_a2a(**kw))
@@ -386,8 +392,8 @@ def random_workload(seed):
     vertex linked to most ranks, sometimes two nodes joined
     only between relay ranks; any collective kind (explicit ones with random
     owners and postconditions), a random route mode and k, and one of static
-    orders, greedy orders, contiguous transfers (two nodes) or switch ports
-    (Alltoall with a switch). Some draws give plans a route search refuses
+    orders, greedy orders in path or reverse path order, contiguous transfers
+    (two nodes) or switch ports (Alltoall with a switch). Some draws give plans a route search refuses
     (a relay route through one link twice); callers skip those."""
     rng = np.random.default_rng(seed)
     kind = int(rng.choice([ALLGATHER, ALLTOALL, REDUCESCATTER, ALLREDUCE, EXPLICIT]))
@@ -446,9 +452,11 @@ def random_workload(seed):
                  int(rng.integers(1, 3)), int(rng.choice([4096, 65536, 1 << 20])), mode,
                  k=int(rng.integers(1, 5)), max_cross=max_cross, relay=relay, owner=owner,
                  post_ptr=post_ptr, post=post, seed=seed)
-    extra = rng.choice(["static", "greedy", "contig", "ports"])
+    extra = rng.choice(["static", "greedy", "rgreedy", "contig", "ports"])
     if extra == "greedy":
         w = with_greedy(w)
+    elif extra == "rgreedy":
+        w = with_reverse_greedy(w)
     elif extra == "contig" and two_nodes:
         w = with_contiguity(w)
     elif extra == "ports" and kind == ALLTOALL and switch:
