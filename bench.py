@@ -164,7 +164,8 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": args.calibrate_copy, "copies": args.steps}))
         return
-    from workloads import CONTIG_ORDER, GREEDY_ORDER, ORDER, PORTS_ORDER, REDUCE_ORDER
+    from workloads import (CONTIG_ORDER, GREEDY_LARGE_ORDER, GREEDY_ORDER, ORDER, PORTS_ORDER,
+                           REDUCE_ORDER)
 
     w, plan, routes, prio, bufs = setup(args.workload)
     per, wall = time_launches(plan, *bufs, args.steps, args.warmup)
@@ -203,7 +204,8 @@ def main():
     }
     if not args.no_all:
         table = {}
-        for name in ORDER + CONTIG_ORDER + REDUCE_ORDER + GREEDY_ORDER + PORTS_ORDER:
+        for name in (ORDER + CONTIG_ORDER + REDUCE_ORDER + GREEDY_ORDER + GREEDY_LARGE_ORDER +
+                     PORTS_ORDER):
             if name == args.workload:
                 wl, pl, pr_ = w, plan, per
             else:

@@ -156,9 +156,9 @@ void taccl_collective_destroy(taccl_collective_t coll);
  *     combined with contiguity (INVALID_ARGUMENT). On the GPU they are
  *     evaluated for every multicast
  *     plan (Allgather, explicit, ReduceScatter, Allreduce) and for Alltoall
- *     plans with at most 256 links and 1024 send slots (chunks x longest
- *     route option); larger Alltoall plans are refused at evaluation
- *     (UNSUPPORTED);
+ *     plans with at most 8192 chunks and 65535 send slots (chunks x longest
+ *     route option) and no zero-cost link; larger Alltoall plans are
+ *     refused at evaluation (UNSUPPORTED);
  *   switch_ports (Alltoall only): 0 = a switch vertex stores and forwards
  *     (uplink, then downlink, each one latency); 1 = the switch model of
  *     App. B.3: a hop pair rank -> switch -> rank is one send costing one

@@ -51,7 +51,8 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
          o_cbkt = pk.add(p->cbkt), o_topt = pk.add(p->topt), o_trec4 = pk.add(p->tree_rec4),
          o_lal = pk.add(p->lalpha), o_lbs = pk.add(p->lbs), o_lmg = pk.add(p->lmerge),
          o_lrev = pk.add(p->lrev), o_hc2 = pk.add(p->hop_class2),
-         o_lcb2 = pk.add(p->lvl_cls2_begin), o_llc2 = pk.add(p->llc2);
+         o_lcb2 = pk.add(p->lvl_cls2_begin), o_llc2 = pk.add(p->llc2),
+         o_gkr = pk.add(p->gkrank);
   void *blk = nullptr;
   e = hipMalloc(&blk, pk.bytes.size());
   if (e != hipSuccess) return fail(TACCL_ERR_NO_MEMORY, "hipMalloc of plan tables failed");
@@ -91,6 +92,7 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
   t.cpath = (const uint32_t *)at(o_cpath);
   t.cinfo = (const uint32_t *)at(o_cinfo);
   t.cbkt = (const uint32_t *)at(o_cbkt);
+  t.gkrank = (const uint32_t *)at(o_gkr);
   t.max_lds = (int)prop.sharedMemPerBlock;
   t.lds_per_cu = (int)std::max<size_t>(prop.maxSharedMemoryPerMultiProcessor, prop.sharedMemPerBlock);
   t.num_cus = prop.multiProcessorCount;
@@ -142,11 +144,15 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
   hipError_t e;
   if (p->coll.kind == TACCL_ALLTOALL && p->greedy) {
     PathGreedyArgs g{};
-    if (path_greedy_layout(*p, g) <= 0 || g.o_wave + g.wave_bytes > t->max_lds)
+    // one wavefront per candidate while its lists fit, else one block
+    const bool wave =
+        path_greedy_layout(*p, g) > 0 && g.o_wave + g.wave_bytes <= t->max_lds;
+    if (!wave && (path_greedy_block_layout(*p, g) <= 0 || g.block_bytes > t->max_lds))
       return fail(TACCL_ERR_UNSUPPORTED,
-                  "time-aware greedy orders for Alltoall need at most 1024 send slots "
-                  "(chunks x longest path) and 256 links");
+                  "time-aware greedy orders for Alltoall need at most 65535 send slots "
+                  "(chunks x longest path), 8192 chunks and no zero-cost link");
     g.mirror = p->greedy == 2;
+    g.gkrank = t->gkrank;
     g.C = p->coll.C;
     g.P = p->topo.P;
     g.E = p->topo.E;
@@ -164,6 +170,13 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     g.makespan = d_makespan;
     g.valid = d_valid;
     g.n = n;
+    if (!wave) {
+      const int nb = std::max(1, path_greedy_block_per_cu(g));
+      const int bgrid = (int)std::min<int64_t>(n, (int64_t)std::max(t->num_cus, 1) * nb);
+      e = launch_path_greedy_block(g, bgrid, s);
+      if (e != hipSuccess) return hip_fail(e, "kernel launch");
+      return TACCL_OK;
+    }
     // wavefronts per block: most resident wavefronts per CU
     int best_w = 1, best_res = 0, best_bpc = 1;
     for (int w = 1; w <= kTreeMaxThreads / 64; w++) {

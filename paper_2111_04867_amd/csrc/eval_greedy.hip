@@ -1,0 +1,288 @@
+// Time-aware greedy orders (App. B.2) for Alltoall plans too large for one
+// wavefront's on-chip lists, for gfx950.
+//
+// One block per candidate at a time, one thread per chunk (CPT chunks per
+// thread). The greedy only ever holds one candidate send per chunk: the
+// next hop of its routed path (in reverse path order, the hop before the
+// last one served). So instead of per-link lists the block keeps per chunk
+// its time and next hop in registers, and simulates the greedy exactly in
+// windows, as the wavefront kernels do: W = the earliest start any chunk's
+// next hop can take (max of its link's busy time and the chunk's time); a
+// hop that is not a candidate yet can only become one at least c_min (the
+// smallest link latency) after W, so on every link the best candidate by
+// (start, Step-2 key, priority, chunk) with start < W + c_min is the
+// greedy's next send there. Per window:
+//   1. every thread computes its chunks' starts; block minimum -> W;
+//   2. per link, an LDS 64-bit atomicMin of start << 32 | key rank (the
+//      rank of the hop's (remaining desc, travelled asc) pair among all
+//      hops of the plan, from a plan table);
+//   3. among the hops that hold that minimum, atomicMin of
+//      priority << 16 | chunk;
+//   4. the single winner per link commits: finish = start + latency, the
+//      link and the chunk advance, and the link's two minima are reset.
+// In reverse path order the greedy serves the mirrored schedule (a chunk's
+// hops from its last link back, key ranks of the mirrored lengths) and
+// records each send's service position on its link; a link's real order is
+// the reverse, and the real times then come from rounds in which, on every
+// link, the send at the link's next position goes once its chunk's previous
+// hop has ended.
+#include <hip/hip_runtime.h>
+
+#include "kernels.h"
+#include "wave.h"
+
+namespace taccl {
+
+namespace {
+
+constexpr uint32_t kNone = 0xFFFFFFFFu;
+
+int32_t align16(int32_t x) { return (x + 15) & ~15; }
+
+template <int CPT, int NT>
+__global__ __launch_bounds__(NT) void path_greedy_block(PathGreedyArgs a) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int P = a.P, E = a.E, H = a.H;
+  constexpr int NW = NT / 64;
+  uint32_t *s_cost = (uint32_t *)(lds + a.b_cost);
+  uint32_t *lfree = (uint32_t *)(lds + a.b_lfree);
+  unsigned long long *best1 = (unsigned long long *)(lds + a.b_best1);
+  unsigned long long *best2 = (unsigned long long *)(lds + a.b_best2);
+  uint32_t *lserv = (uint32_t *)(lds + a.b_lserv);  // sends served per link
+  uint32_t *lnext = (uint32_t *)(lds + a.b_lnext);  // real order: next position
+  uint32_t *red = (uint32_t *)(lds + a.b_red);      // [2][NW] window minima
+  uint16_t *fpos = (uint16_t *)(lds + a.b_fpos);    // service position per slot
+  for (int l = tid; l < E; l += NT) s_cost[l] = a.cost[l];
+
+  for (int64_t i = blockIdx.x; i < a.n; i += gridDim.x) {
+    const uint8_t *rt = a.routes + (size_t)i * a.route_stride;
+    const uint32_t *gpr = a.prio + (size_t)i * a.prio_stride;
+    for (int l = tid; l < E; l += NT) {
+      lfree[l] = 0;
+      lserv[l] = 0;
+      lnext[l] = 0;
+      best1[l] = ~0ull;
+      best2[l] = ~0ull;
+    }
+    // per chunk: first hop of its option in path_links, hop count, hops
+    // served, time, and the current hop's link, key rank and priority
+    uint32_t qo[CPT], hops[CPT], cur[CPT], ct[CPT], cl[CPT], kr[CPT], pv[CPT];
+    bool bad = false;
+    auto load_hop = [&](int j, int c) {
+      const uint32_t h = a.mirror ? hops[j] - 1 - cur[j] : cur[j];
+      cl[j] = a.path_links[qo[j] + h];
+      kr[j] = a.gkrank[qo[j] + h];
+      pv[j] = gpr[(uint32_t)c * H + h];
+    };
+#pragma unroll
+    for (int j = 0; j < CPT; j++) {
+      const int c = tid + NT * j;
+      hops[j] = 0;
+      cur[j] = 0;
+      ct[j] = 0;
+      qo[j] = 0;
+      if (c < a.C) {
+        const uint32_t sd = (uint32_t)c / (uint32_t)a.cpr;
+        const uint32_t s = sd / P, d = sd - s * P;
+        if (s != d) {
+          const uint32_t k = rt[c];
+          if (k < a.npaths[sd]) {
+            const uint32_t q = a.pair_base[sd] + k;
+            qo[j] = a.path_off[q];
+            hops[j] = a.path_off[q + 1] - qo[j];
+            load_hop(j, c);
+          } else {
+            bad = true;  // the pair is left unrouted
+          }
+        }
+      }
+    }
+    __syncthreads();
+
+    uint32_t mk = 0;
+    bool fault = false;
+    for (int round = 0, buf = 0;; round++, buf ^= 1) {
+      // 1. starts and their block minimum
+      uint32_t st[CPT];
+      uint32_t wmin = kNone;
+#pragma unroll
+      for (int j = 0; j < CPT; j++) {
+        st[j] = kNone;
+        if (cur[j] < hops[j]) {
+          st[j] = max(ct[j], lfree[cl[j]]);
+          wmin = min(wmin, st[j]);
+        }
+      }
+      wmin = ~wave_reduce_max(~wmin);
+      if (lane == 0) red[buf * NW + wave] = wmin;
+      __syncthreads();
+      uint32_t W = kNone;
+#pragma unroll
+      for (int w = 0; w < NW; w++) W = min(W, red[buf * NW + w]);
+      if (W == kNone) break;  // every chunk is through
+      if (round > a.nslots) {  // unreachable: every window serves a send
+        fault = true;
+        break;
+      }
+      const uint64_t wend = (uint64_t)W + a.cmin;
+      // 2. per link the smallest (start, key rank) of the window
+      uint64_t k1[CPT];
+#pragma unroll
+      for (int j = 0; j < CPT; j++) {
+        k1[j] = ((uint64_t)st[j] << 32) | kr[j];
+        if (st[j] != kNone && (uint64_t)st[j] < wend) atomicMin(&best1[cl[j]], k1[j]);
+      }
+      __syncthreads();
+      // 3. then the smallest (priority, chunk)
+#pragma unroll
+      for (int j = 0; j < CPT; j++) {
+        const int c = tid + NT * j;
+        if (st[j] != kNone && (uint64_t)st[j] < wend && best1[cl[j]] == k1[j])
+          atomicMin(&best2[cl[j]], ((uint64_t)pv[j] << 16) | (uint32_t)c);
+      }
+      __syncthreads();
+      // 4. the winner of every link commits
+#pragma unroll
+      for (int j = 0; j < CPT; j++) {
+        const int c = tid + NT * j;
+        if (st[j] != kNone && (uint64_t)st[j] < wend && best1[cl[j]] == k1[j] &&
+            best2[cl[j]] == (((uint64_t)pv[j] << 16) | (uint32_t)c)) {
+          const uint32_t l = cl[j];
+          const uint32_t f = st[j] + s_cost[l];
+          ct[j] = f;
+          lfree[l] = f;
+          mk = max(mk, f);
+          if (a.mirror) {
+            const uint32_t h = hops[j] - 1 - cur[j];
+            fpos[(uint32_t)c * H + h] = (uint16_t)lserv[l];
+          }
+          lserv[l]++;
+          best1[l] = ~0ull;
+          best2[l] = ~0ull;
+          if (++cur[j] < hops[j]) load_hop(j, c);
+        }
+      }
+      __syncthreads();
+    }
+
+    if (a.mirror && !fault) {
+      // the real schedule: every link's order is its service order reversed
+      mk = 0;
+      for (int l = tid; l < E; l += NT) lfree[l] = 0;
+#pragma unroll
+      for (int j = 0; j < CPT; j++) {
+        cur[j] = 0;
+        ct[j] = 0;
+        if (hops[j]) cl[j] = a.path_links[qo[j]];
+      }
+      __syncthreads();
+      for (int round = 0;; round++) {
+        // a chunk's next hop goes when it is at its link's next position
+        bool go[CPT], pending = false;
+#pragma unroll
+        for (int j = 0; j < CPT; j++) {
+          const int c = tid + NT * j;
+          go[j] = false;
+          if (cur[j] < hops[j]) {
+            pending = true;
+            const uint32_t l = cl[j];
+            const uint32_t pos = lserv[l] - 1u - fpos[(uint32_t)c * H + cur[j]];
+            go[j] = lnext[l] == pos;
+          }
+        }
+        if (!__syncthreads_or(pending)) break;
+        if (round > a.nslots) {  // unreachable: the orders come from a schedule
+          fault = true;
+          break;
+        }
+#pragma unroll
+        for (int j = 0; j < CPT; j++)
+          if (go[j]) {
+            const uint32_t l = cl[j];
+            const uint32_t f = max(ct[j], lfree[l]) + s_cost[l];
+            ct[j] = f;
+            lfree[l] = f;
+            lnext[l]++;
+            mk = max(mk, f);
+            if (++cur[j] < hops[j]) cl[j] = a.path_links[qo[j] + cur[j]];
+          }
+        __syncthreads();
+      }
+    }
+
+    // makespan and validity (after a barrier: the last window's minima
+    // may still be read)
+    __syncthreads();
+    const uint32_t wm = wave_reduce_max(mk);
+    if (lane == 0) red[wave] = wm;
+    const bool any_bad = __syncthreads_or(bad);
+    const bool any_fault = __syncthreads_or(fault);
+    if (tid == 0) {
+      uint32_t m = 0;
+      for (int w = 0; w < NW; w++) m = max(m, red[w]);
+      a.makespan[i] = any_fault ? 0xFFFFFFFFu : m;
+      a.valid[i] = (uint8_t)(!any_bad && !any_fault);
+    }
+    __syncthreads();
+  }
+}
+
+template <int NT>
+const void *block_fn(int cpt) {
+  switch (cpt) {
+    case 1: return (const void *)path_greedy_block<1, NT>;
+    case 2: return (const void *)path_greedy_block<2, NT>;
+    case 4: return (const void *)path_greedy_block<4, NT>;
+    default: return (const void *)path_greedy_block<8, NT>;
+  }
+}
+
+}  // namespace
+
+int32_t path_greedy_block_layout(const taccl_plan &p, PathGreedyArgs &a) {
+  const int32_t C = p.coll.C, E = p.topo.E, H = std::max(p.H, 1);
+  if (E < 1 || p.gkrank.size() != p.path_links.size() || (int64_t)C * H > 65535) return 0;
+  uint32_t cmin = ~0u;
+  for (uint32_t c : p.cost) cmin = std::min(cmin, c);
+  if (cmin == 0) return 0;
+  int cpt = 1;
+  while (cpt * kGreedyBlockThreads < C) cpt *= 2;
+  if (cpt > 8) return 0;  // 1024 threads leave 128 registers per thread
+  a.cmin = cmin;
+  a.nslots = C * H;
+  a.cpt = cpt;
+  int32_t off = 0;
+  auto take = [&](int32_t bytes) {
+    int32_t o = off;
+    off = align16(off + bytes);
+    return o;
+  };
+  a.b_cost = take(4 * E);
+  a.b_lfree = take(4 * E);
+  a.b_best1 = take(8 * E);
+  a.b_best2 = take(8 * E);
+  a.b_lserv = take(4 * E);
+  a.b_lnext = take(4 * E);
+  a.b_red = take(4 * 2 * (kGreedyBlockThreads / 64));
+  a.b_fpos = take(p.greedy == 2 ? 2 * a.nslots : 0);
+  a.block_bytes = off;
+  return off;
+}
+
+int path_greedy_block_per_cu(const PathGreedyArgs &a) {
+  int nb = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, block_fn<kGreedyBlockThreads>(a.cpt),
+                                                   kGreedyBlockThreads, a.block_bytes) !=
+      hipSuccess)
+    return 0;
+  return nb;
+}
+
+hipError_t launch_path_greedy_block(const PathGreedyArgs &a, int grid, hipStream_t stream) {
+  void *args[] = {(void *)&a};
+  return hipLaunchKernel(block_fn<kGreedyBlockThreads>(a.cpt), dim3(grid),
+                         dim3(kGreedyBlockThreads), args, a.block_bytes, stream);
+}
+
+}  // namespace taccl

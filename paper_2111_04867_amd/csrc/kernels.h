@@ -123,6 +123,11 @@ struct PathGreedyArgs {
   // offsets and fill pointers per link, pending-send records
   int32_t o_wave, wave_bytes, w_gfin, w_gofs, w_gcur, w_grec;
   int32_t mirror;  // greedy in reverse path order
+  // block-per-candidate variant for larger plans: Step-2 key rank of every
+  // hop (plan table), chunks per thread and the LDS carve-up
+  const uint32_t *gkrank;
+  int32_t cpt, block_bytes;
+  int32_t b_cost, b_lfree, b_best1, b_best2, b_lserv, b_lnext, b_red, b_fpos;
 };
 
 // Switch-hyperedge connection count: one block per candidate at a time.
@@ -175,6 +180,14 @@ hipError_t launch_tree(const TreeArgs &a, int grid, hipStream_t stream);
 int32_t path_greedy_layout(const taccl_plan &p, PathGreedyArgs &a);
 int path_greedy_blocks_per_cu(const PathGreedyArgs &a);
 hipError_t launch_path_greedy(const PathGreedyArgs &a, int grid, hipStream_t stream);
+// Alltoall greedy, one block per candidate (plans beyond the wavefront
+// kernel): fills the layout; returns the block's LDS bytes, or 0 when the
+// plan has more than 8 chunks per thread (8192 chunks), 65535 send slots or
+// a zero-cost link
+constexpr int kGreedyBlockThreads = 1024;
+int32_t path_greedy_block_layout(const taccl_plan &p, PathGreedyArgs &a);
+int path_greedy_block_per_cu(const PathGreedyArgs &a);
+hipError_t launch_path_greedy_block(const PathGreedyArgs &a, int grid, hipStream_t stream);
 // connection count: LDS bytes of a block of `threads`, and the launch
 int32_t connections_lds_bytes(const ConnArgs &a, int threads);
 hipError_t launch_connections(const ConnArgs &a, int threads, int grid, hipStream_t stream);

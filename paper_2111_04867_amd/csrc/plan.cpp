@@ -368,6 +368,31 @@ static taccl_status_t build_levels(taccl_plan *p) {
   for (int32_t L = 0; L < p->nlev; L++)
     p->max_lvl_sends = std::max<int32_t>(p->max_lvl_sends, (int32_t)per_level[L]);
 
+  // greedy orders: rank of every hop's Step-2 key (remaining desc,
+  // travelled asc; in reverse path order the mirrored lengths, remaining' =
+  // travelled + latency and travelled' = remaining - latency)
+  p->gkrank.clear();
+  if (p->greedy) {
+    std::vector<std::pair<uint64_t, uint64_t>> keys(p->path_links.size());
+    for (size_t q = 0; q < npath; q++) {
+      const uint64_t total = p->path_cost[q];
+      uint64_t trav = 0;
+      for (uint32_t j = p->path_off[q]; j < p->path_off[q + 1]; j++) {
+        const uint64_t c = p->cost[p->path_links[j]], rem = total - trav;
+        // ascending pair order = Step-2 order: (~remaining, travelled)
+        keys[j] = p->greedy == 2 ? std::make_pair(~(trav + c), rem - c)
+                                 : std::make_pair(~rem, trav);
+        trav += c;
+      }
+    }
+    std::vector<std::pair<uint64_t, uint64_t>> uniq(keys);
+    std::sort(uniq.begin(), uniq.end());
+    uniq.erase(std::unique(uniq.begin(), uniq.end()), uniq.end());
+    p->gkrank.resize(keys.size());
+    for (size_t j = 0; j < keys.size(); j++)
+      p->gkrank[j] = (uint32_t)(std::lower_bound(uniq.begin(), uniq.end(), keys[j]) - uniq.begin());
+  }
+
   // compact tables of the register-resident kernel (paths of <= 6 hops,
   // <= 8 levels, <= 2^24 route options)
   p->path_fast = !p->ports && p->H <= kFastMaxHops && p->nlev <= 8 && npath < (1u << 24) &&

@@ -62,6 +62,7 @@ struct DeviceTables {
   const uint32_t *lvl_cls_begin = nullptr;
   const uint32_t *llc = nullptr;
   const uint32_t *arec = nullptr, *cpath = nullptr, *cinfo = nullptr, *cbkt = nullptr;
+  const uint32_t *gkrank = nullptr;
   int max_lds = 0;  // bytes of LDS a block may use on this device
   int lds_per_cu = 0;
   int num_cus = 0;
@@ -133,6 +134,11 @@ struct taccl_plan {
   // per class: first priority sub-bucket (level-relative) | bits << 24
   std::vector<uint32_t> cbkt;
   int32_t max_lvl_nb = 0;
+  // Alltoall greedy orders: per hop (index into path_links) the rank of its
+  // Step-2 key (remaining desc, travelled asc) among all hops of the plan,
+  // with the lengths of the greedy's direction (mirrored in reverse path
+  // order)
+  std::vector<uint32_t> gkrank;
 
   // launch shape
   int32_t tree_lds = 0, path_lds = 0;

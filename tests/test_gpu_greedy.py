@@ -136,11 +136,46 @@ def test_alltoall_unrouted_and_equal_priorities():
     assert not ok.all()
 
 
+@pytest.mark.parametrize("order", [1, 2])
+@pytest.mark.parametrize("make,n", [
+    (lambda: cf.full_a2a(40, chunk_bytes=65536), 64),
+    (lambda: cf.two_node_rings_a2a(8, contiguity=0), 64),
+    (lambda: replace(cf.full_a2a(24, chunk_bytes=65536), chunks_per_rank=3), 48),
+    (lambda: cf.fournode64_a2a(n_candidates=16), 16)])
+def test_alltoall_block_kernel(make, n, order):
+    """Plans beyond a wavefront's lists (more than 1024 send slots) run one
+    block per candidate."""
+    w = make()
+    w = cf.with_greedy(w) if order == 1 else cf.with_reverse_greedy(w)
+    plan, ref, opts = plans(w)
+    routes, prio = generate(w.seed + 13, 0, n, opts, plan.prio_stride)
+    rng = np.random.default_rng(n + order)
+    routes[rng.random(routes.shape) < 0.002] = 0xFF
+    prio[1::2] = 4
+    check(plan, ref, routes, prio, f"{w.name} alltoall greedy, block kernel")
+
+
+@pytest.mark.parametrize("name", cf.GREEDY_LARGE_ORDER)
+def test_full_batch_sampled(name):
+    """The whole batch in the benchmark's launch shape; 24 sampled
+    candidates (first, last, spread) against the oracle."""
+    w = cf.named(name)
+    plan, ref, opts = plans(w)
+    routes, prio = generate(w.seed, 0, w.n_candidates, opts, plan.prio_stride)
+    say(f"[gpu] {name}: full batch N={w.n_candidates}")
+    mk, ok = plan.eval(routes, prio)
+    idx = np.unique(np.r_[0, w.n_candidates - 1,
+                          np.random.default_rng(3).choice(w.n_candidates, 22, replace=False)])
+    rmk, rok = ref.eval_threads(routes[idx], prio[idx])
+    assert (mk[idx] == rmk).all() and (ok[idx] == rok).all()
+    assert ok.all()
+
+
 def test_alltoall_too_large_refused():
-    """More than 1024 send slots (chunks x longest path) do not fit a
-    wavefront's on-chip lists: refused, not approximated."""
+    """More than 8192 chunks (8 per thread of a 1024-thread block): refused,
+    not approximated."""
     from paper_2111_04867_amd.binding import Plan, TacclError
-    w = cf.with_greedy(cf.fournode64_a2a(n_candidates=2))
+    w = cf.with_greedy(replace(cf.full_a2a(24, chunk_bytes=4096), chunks_per_rank=15))
     plan = Plan.from_workload(w)
     routes, prio = generate(1, 0, 2, plan.route_options(), plan.prio_stride)
     with pytest.raises(TacclError) as e:

@@ -278,7 +278,13 @@ def with_reverse_greedy(w):
 NAMED["twonode16_ag_greedy"] = lambda **kw: with_greedy(twonode16_ag(**kw))
 NAMED["cubemesh8_ag_greedy"] = lambda **kw: with_greedy(cubemesh8_ag(**kw))
 NAMED["switch16_a2a_greedy"] = lambda **kw: with_greedy(switch16_a2a(**kw))
-GREEDY_ORDER = ["cubemesh8_ag_greedy", "twonode16_ag_greedy", "switch16_a2a_greedy"]
+NAMED["fournode64_a2a_greedy"] = lambda **kw: with_greedy(fournode64_a2a(**kw))
+NAMED["twonode16_ag_rgreedy"] = lambda **kw: with_reverse_greedy(twonode16_ag(**kw))
+GREEDY_ORDER = ["cubemesh8_ag_greedy", "twonode16_ag_greedy", "switch16_a2a_greedy",
+                "twonode16_ag_rgreedy"]
+# timed by the benchmark; the oracle needs about a second per candidate, so
+# parity tests sample them
+GREEDY_LARGE_ORDER = ["fournode64_a2a_greedy"]
 
 
 def with_switch_ports(w):
