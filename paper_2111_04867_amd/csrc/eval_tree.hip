@@ -169,9 +169,9 @@ __device__ __forceinline__ bool build_trees(const TreeArgs &a, const uint32_t *s
 //    published only when it closes, so no dependant reads a time that could
 //    still grow; a joiner's pred has a strictly longer remaining path than
 //    the transfer, so waiting for it never waits on the transfer;
-//  * time-aware greedy (a.greedy == 1, App. B.2): send by send, the
-//    unserved ready send with the smallest (max(ready, link free), Step-2
-//    key, priority, slot) is served, by four wavefront reductions;
+//  * time-aware greedy (a.greedy == 1, App. B.2): the unserved ready send
+//    with the smallest (max(ready, link free), Step-2 key, priority, slot)
+//    goes next, simulated exactly in windows (below);
 //  * greedy in reverse path order (a.greedy == 2): the same greedy on the
 //    mirrored schedule, whose dependencies are the other form (Allgather
 //    sends wait for the sends out of their destination, ReduceScatter sends
@@ -215,66 +215,66 @@ __device__ __noinline__ bool any_schedule(const TreeArgs &a, bool rs, int lane,
   };
 
   if (a.greedy) {
-    // served sends get fin; mirrored runs record the service position on
-    // the link in pend[] (dead once a send is served) and leave mk alone
+    // plans have no zero-cost link, so c_min > 0 and every window serves
     const bool mirror = a.greedy == 2, push = rs != mirror;
-    for (uint32_t step = 0; step < total; step++) {
-      uint32_t bt = ~0u, bp = ~0u, bs = ~0u;
-      uint64_t bk = ~0ull;
-      for (int s = lane; s < CV; s += 64) {
-        const int pl = par[s];
-        if (!pl || lds_get(&fin[s]) != kNotYet) continue;
-        const int l = pl - 1;
-        uint32_t r;
-        if (push) {
-          if (lds_get(&pend[s])) continue;
-          r = lds_get(&rdy[s]);
-        } else {
-          const uint32_t c = div_v(s, a.vmagic);
-          const int u = s_src[l];
-          r = (u == s_own[c]) ? 0u : lds_get(&fin[c * V + u]);
+    // windows (as in the layered greedy kernel): W = the earliest start
+    // any ready send can take; a send not ready yet can only start c_min
+    // or more after W, so on every link the best ready send with start <
+    // W + c_min is the greedy's next there. Each link's pending sends are
+    // the front of its chain[] segment (count in lhead[]); a served send
+    // is swapped to the end of the pending part, so the segment ends up
+    // in reverse service order.
+    for (int l = lane; l < E; l += 64) lhead[l] = lbase[l + 1] - lbase[l];
+    wave_sync();
+    for (uint32_t round = 0;; round++) {
+      uint32_t wmin = kNotYet;
+      for (int l = lane; l < E; l += 64) {
+        const uint32_t b = lbase[l], n = lhead[l], F = lfree[l];
+        uint32_t cs = kNotYet, cq = 0, bp = ~0u, bs = ~0u;
+        uint64_t bk = ~0ull;
+        for (uint32_t q = 0; q < n; q++) {
+          const uint32_t ent = chain[b + q];
+          const uint32_t r = ready_of(ent, push);
           if (r == kNotYet) continue;
+          const uint32_t sl = ent & 0xFFFFu, st = max(F, r);
+          const uint64_t k = key[sl];
+          const uint32_t p = prio[sl];
+          if (st < cs || (st == cs && (k < bk || (k == bk && (p < bp || (p == bp && sl < bs)))))) {
+            cs = st;
+            cq = q;
+            bk = k;
+            bp = p;
+            bs = sl;
+          }
         }
-        const uint32_t t = max(r, lfree[l]);
-        const uint64_t k = key[s];
-        const uint32_t p = prio[s];
-        if (t < bt || (t == bt && (k < bk || (k == bk && (p < bp || (p == bp && (uint32_t)s < bs)))))) {
-          bt = t;
-          bk = k;
-          bp = p;
-          bs = (uint32_t)s;
-        }
+        gst[l] = cs;
+        gfirst[l] = cq;
+        wmin = min(wmin, cs);
       }
-      const uint32_t tmin = ~wave_reduce_max(~bt);
-      const bool at = bt == tmin;
-      const uint64_t kmin = ~wave_reduce_max64(at ? ~bk : 0ull);
-      const bool ak = at && bk == kmin;
-      const uint32_t pmin = ~wave_reduce_max(ak ? ~bp : 0u);
-      const uint32_t smin = ~wave_reduce_max(ak && bp == pmin ? ~bs : 0u);
-      if (smin == ~0u) return true;
-      const int l = par[smin] - 1;
-      const uint32_t f = tmin + s_cost[l];
-      if (lane == 0) {
+      wmin = ~wave_reduce_max(~wmin);
+      if (wmin == kNotYet) break;
+      if (round > total) return true;  // unreachable: every window serves a send
+      const uint64_t wend = (uint64_t)wmin + a.cmin;
+      wave_sync();
+      for (int l = lane; l < E; l += 64) {
+        const uint32_t cs = gst[l];
+        if (cs == kNotYet || (uint64_t)cs >= wend) continue;
+        const uint32_t b = lbase[l], n = lhead[l], cq = gfirst[l];
+        const uint32_t ent = chain[b + cq];
+        const uint32_t f = cs + s_cost[l];
+        publish(ent & 0xFFFFu, f, l, push);
         lfree[l] = f;
-        publish(smin, f, l, push);
-        if (mirror) lds_put(&pend[smin], gcnt[l]++);
+        if (!mirror) mk = max(mk, f);
+        chain[b + cq] = chain[b + n - 1];
+        chain[b + n - 1] = ent;
+        lhead[l] = n - 1;
       }
-      if (!mirror) mk = max(mk, f);
       wave_sync();
     }
+    bool left = false;  // a send that never became ready: unreachable
+    for (int l = lane; l < E; l += 64) left |= lhead[l] != 0;
+    if (__ballot(left)) return true;
     if (!mirror) return false;
-    // the real orders: reversed service orders, with the pred slot of the
-    // real schedule's pull form
-    for (int s = lane; s < CV; s += 64) {
-      const int pl = par[s];
-      if (!pl) continue;
-      const int l = pl - 1;
-      const uint32_t c = div_v(s, a.vmagic);
-      const int u = s_src[l];
-      const uint32_t pred = (u == s_own[c]) ? kNoPred : c * V + u;
-      const uint32_t n_l = lbase[l + 1] - lbase[l];
-      chain[lbase[l] + n_l - 1 - pend[s]] = (pred << 16) | (uint32_t)s;
-    }
     wave_sync();
     for (int s = lane; s < CV; s += 64) {
       fin[s] = kNotYet;
@@ -1803,6 +1803,9 @@ int32_t tree_any_layout(const taccl_plan &p, TreeArgs &a) {
   a.w_gpend = wtake(4 * CV);
   a.w_gst = wtake(16 * E);
   a.wave_bytes = w;
+  uint32_t cmin = ~0u;  // the greedy's window (plans have no zero-cost link)
+  for (uint32_t c : p.cost) cmin = std::min(cmin, c);
+  a.cmin = cmin;
   return a.o_wave + a.wave_bytes;
 }
 

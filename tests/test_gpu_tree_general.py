@@ -115,3 +115,12 @@ def test_explicit_greedy_and_contiguity():
     w = cf.explicit_multicast(base, owner, posts)
     check(cf.with_greedy(w), n=128)
     check(cf.with_contiguity(w))
+
+
+@pytest.mark.parametrize("kind", KINDS)
+def test_reverse_greedy_general_shapes(kind):
+    """Reverse path order on the general variant's shapes (long routes,
+    wide cost ratios, two nodes)."""
+    for make in (lambda k: long_ring(10, k), lambda k: skewed(5, k), lambda k: two_nodes(3, k),
+                 lambda k: ring(6, k, cpr=2)):
+        check(cf.with_reverse_greedy(make(kind)), n=96)
