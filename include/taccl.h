@@ -205,7 +205,9 @@ typedef struct {
   int64_t max_sends;    /* most sends one candidate can have */
   uint64_t bytes_per_candidate; /* routes + priorities + 5 output bytes */
   int32_t num_classes;  /* Alltoall: (level, link, travelled) send classes */
-  int32_t lds_bytes;    /* on-chip memory one evaluating block needs */
+  int32_t lds_bytes;    /* LDS of one block (one wavefront's, where blocks
+                           hold several) of the kernel the plan runs on;
+                           above the device's limit, evaluation refuses */
 } taccl_plan_info_t;
 
 /*

@@ -6,6 +6,7 @@
 // sequence); with positive link costs the complete paths leave the queue in
 // exactly that order, so the first k popped are the k best.
 #include <algorithm>
+#include <unordered_map>
 #include <cstring>
 #include <memory>
 #include <queue>
@@ -146,6 +147,23 @@ static taccl_status_t build_routes(taccl_plan *p, const uint8_t *allowed, const 
   const taccl_topology &t = p->topo;
   const int32_t P = t.P;
   Router R(t, p->cost, allowed, relay);
+  // relay routes join best single paths, and the same legs recur for many
+  // pairs: each (s, d, crossing limit) is searched once
+  std::unordered_map<uint64_t, int32_t> memo;  // -> index into legs, -1 = none
+  std::vector<Path> legs;
+  auto best = [&](int32_t s, int32_t d, int32_t mc, Path &out, bool &ok) {
+    const uint64_t key = ((uint64_t)(uint32_t)s << 32 | (uint32_t)d) * 4 + (uint64_t)(mc + 1);
+    auto it = memo.find(key);
+    if (it == memo.end()) {
+      Path q;
+      const int32_t idx = R.best(s, d, mc, q, ok) ? (int32_t)legs.size() : -1;
+      if (idx >= 0) legs.push_back(std::move(q));
+      it = memo.emplace(key, idx).first;
+    }
+    if (it->second < 0) return false;
+    out = legs[it->second];
+    return true;
+  };
   p->pair_base.assign((size_t)P * P, 0);
   p->npaths.assign((size_t)P * P, 0);
   p->path_off.assign(1, 0);
@@ -170,12 +188,12 @@ static taccl_status_t build_routes(taccl_plan *p, const uint8_t *allowed, const 
             break;
           case TACCL_ROUTE_RELAY1: {
             Path q;
-            if (R.best(s, d, p->max_cross, q, budget_ok)) opts.push_back(q);
+            if (best(s, d, p->max_cross, q, budget_ok)) opts.push_back(q);
             for (int32_t m = 0; m < P; m++) {
               if (m == s || m == d || (relay && !relay[m])) continue;
               Path a, b;
-              if (!R.best(s, m, p->max_cross, a, budget_ok)) continue;
-              if (!R.best(m, d, p->max_cross, b, budget_ok)) continue;
+              if (!best(s, m, p->max_cross, a, budget_ok)) continue;
+              if (!best(m, d, p->max_cross, b, budget_ok)) continue;
               opts.push_back(R.join(a, -1, b));
             }
             break;
@@ -183,7 +201,7 @@ static taccl_status_t build_routes(taccl_plan *p, const uint8_t *allowed, const 
           case TACCL_ROUTE_HIER_RELAY: {
             if (t.node[s] == t.node[d]) {
               Path q;
-              if (R.best(s, d, 0, q, budget_ok)) opts.push_back(q);
+              if (best(s, d, 0, q, budget_ok)) opts.push_back(q);
             } else {
               const auto &rs = relays_of_node[t.node[s]];
               const auto &rd = relays_of_node[t.node[d]];
@@ -192,8 +210,8 @@ static taccl_status_t build_routes(taccl_plan *p, const uint8_t *allowed, const 
                 int32_t mid = R.link(rs[i], rd[i]);
                 if (mid < 0) continue;
                 Path a, b;
-                if (!R.best(s, rs[i], 0, a, budget_ok)) continue;
-                if (!R.best(rd[i], d, 0, b, budget_ok)) continue;
+                if (!best(s, rs[i], 0, a, budget_ok)) continue;
+                if (!best(rd[i], d, 0, b, budget_ok)) continue;
                 opts.push_back(R.join(a, mid, b));
               }
             }
@@ -752,12 +770,24 @@ taccl_status_t taccl_sketch_apply(taccl_topology_t topo, taccl_collective_t coll
     if (p->H > 255)
       return fail(TACCL_ERR_UNSUPPORTED, "multicast evaluation holds paths of at most 255 hops");
   }
+  // on-chip bytes of one block (of one wavefront, where blocks hold
+  // several) of the kernel the plan runs on, as the launch picks it
   if (coll->kind == TACCL_ALLTOALL) {
     PathArgs a{};
-    p->path_lds = (p->path_fast && path_fast_cpt(*p)) ? path_fast_layout(*p, a) : path_layout(*p, a);
+    PathGreedyArgs g{};
+    if (p->greedy)
+      p->path_lds = path_greedy_layout(*p, g) > 0 ? g.o_wave + g.wave_bytes
+                                                  : path_greedy_block_layout(*p, g);
+    else
+      p->path_lds =
+          (p->path_fast && path_fast_cpt(*p)) ? path_fast_layout(*p, a) : path_layout(*p, a);
   } else {
     TreeArgs a{};
-    p->tree_lds = tree_layout(*p, a);
+    const bool any = coll->kind == TACCL_REDUCESCATTER || coll->kind == TACCL_ALLREDUCE ||
+                     p->contig || p->greedy;
+    const int32_t layered =
+        p->greedy == 2 ? 0 : (p->greedy ? tree_greedy_layout(*p, a) : tree_layers_layout(*p, a));
+    p->tree_lds = layered > 0 ? layered : any ? tree_any_layout(*p, a) : tree_layout(*p, a);
   }
   *out = guard.release();
   clear_error();
