@@ -1,9 +1,17 @@
-// Multicast (Allgather / explicit) evaluation kernel for gfx950.
+// Multicast evaluation kernels for gfx950 (Allgather, explicit, and the
+// ReduceScatter / Allreduce built from them), and the time-aware greedy for
+// Alltoall plans that fit one wavefront:
+//   tree_eval_kernel     general kernel, described below; its kAny variant
+//                        adds ReduceScatter, contiguity and greedy orders;
+//   tree_layers_kernel   layered kernel for plans within its limits (the
+//                        fast path), static orders;
+//   tree_greedy_kernel   the layered kernel's trees with greedy orders;
+//   path_greedy_kernel   Alltoall greedy orders, one wavefront per candidate.
 //
-// Persistent blocks of several wavefronts. Each block copies the plan's
-// route records and link costs into LDS once; each wavefront then evaluates
-// one candidate at a time, its state in LDS, while the next candidate's
-// routes and priorities stream from HBM into registers:
+// tree_eval_kernel: persistent blocks of several wavefronts. Each block
+// copies the plan's route records and link costs into LDS once; each
+// wavefront then evaluates one candidate at a time, its state in LDS, while
+// the next candidate's routes and priorities stream from HBM into registers:
 //   1. stage the candidate: route choices and priorities go to LDS;
 //   2. lane = chunk: the routed paths of the chunk (destinations ascending)
 //      are merged into a tree by first reach, one send per reached vertex
