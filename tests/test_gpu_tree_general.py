@@ -124,3 +124,31 @@ def test_reverse_greedy_general_shapes(kind):
     for make in (lambda k: long_ring(10, k), lambda k: skewed(5, k), lambda k: two_nodes(3, k),
                  lambda k: ring(6, k, cpr=2)):
         check(cf.with_reverse_greedy(make(kind)), n=96)
+
+
+@pytest.mark.parametrize("option", ["static", "greedy", "rgreedy", "contig"])
+@pytest.mark.parametrize("base", ["cubemesh8", "twonode6"])
+def test_degenerate_explicit(base, option):
+    """Postconditions that need no send (every chunk only at its owner): no
+    sends, makespan 0, valid; then a single chunk with one destination."""
+    from paper_2111_04867_amd.binding import Plan
+    b = cf.cubemesh8_ag() if base == "cubemesh8" else two_nodes(3, cf.ALLGATHER)
+    for owner, posts in (([0, 3, 5], [[0], [3], [5]]), ([2], [[b.P - 1]])):
+        w = cf.explicit_multicast(b, owner, posts)
+        if option == "greedy":
+            w = cf.with_greedy(w)
+        elif option == "rgreedy":
+            w = cf.with_reverse_greedy(w)
+        elif option == "contig":
+            if w.node_of is None:
+                continue
+            w = cf.with_contiguity(w)
+        plan, ref = Plan.from_workload(w), OraclePlan.from_workload(w)
+        routes, prio = generate(3, 0, 64, plan.route_options(), plan.prio_stride)
+        mk, ok = plan.eval(routes, prio)
+        rmk, rok = ref.eval(routes, prio)
+        assert (mk == rmk).all() and (ok == rok).all()
+        if len(owner) == 3:
+            assert (mk == 0).all() and ok.all()
+        else:
+            assert (mk > 0).all() and ok.all()
