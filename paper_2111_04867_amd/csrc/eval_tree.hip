@@ -188,7 +188,7 @@ __device__ __forceinline__ bool build_trees(const TreeArgs &a, const uint32_t *s
 //    order is the reverse of the order the mirrored greedy served it in,
 //    and the real times come from the static rounds over those orders.
 // Returns true on a fault (no progress; unreachable for valid orders).
-__device__ __noinline__ bool any_schedule(const TreeArgs &a, bool rs, int lane,
+__device__ __forceinline__ bool any_schedule(const TreeArgs &a, bool rs, int lane,
                                           const uint32_t *s_cost, const uint8_t *s_src,
                                           const uint8_t *s_own, const uint64_t *key,
                                           const uint32_t *prio, const uint16_t *par,
