@@ -285,6 +285,23 @@ taccl_status_t taccl_eval_batch(taccl_plan_t plan, int64_t n, const uint8_t *d_r
 taccl_status_t taccl_connections_batch(taccl_plan_t plan, int64_t n, const uint8_t *d_routes,
                                        uint32_t *d_connections, taccl_stream_t stream);
 
+/*
+ * Seeded synthetic candidates on the host: the counter-based generator the
+ * tests and the benchmark feed to taccl_eval_batch (SplitMix64 of a counter
+ * keyed by stream, candidate and entry, so any candidate range comes out the
+ * same on its own). For candidates first .. first+count-1 it writes
+ *   routes[count][route_stride]: per route entry a uniform choice among its
+ *     route options (Sec. 5.1 Step 1 leaves each chunk a set of shortest
+ *     paths), 0 for entries without options;
+ *   prio[count][prio_stride]: uniform 32-bit priorities (the final tie-break
+ *     of the Step-2 order).
+ * Host buffers, owned by the caller. Errors: INVALID_ARGUMENT for a null
+ * plan, null buffers with count > 0, first < 0, count < 0 or
+ * first + count > 2^32. count == 0 is a no-op.
+ */
+taccl_status_t taccl_generate_host(taccl_plan_t plan, uint64_t seed, int64_t first, int64_t count,
+                                   uint8_t *routes, uint32_t *prio);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char *taccl_last_error(void);
 

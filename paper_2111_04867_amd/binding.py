@@ -46,7 +46,8 @@ EXPORTS = ["taccl_topology_create", "taccl_topology_destroy", "taccl_collective_
            "taccl_collective_create_explicit", "taccl_collective_destroy", "taccl_sketch_apply",
            "taccl_plan_destroy", "taccl_plan_info", "taccl_plan_route_options",
            "taccl_plan_path", "taccl_plan_link_costs", "taccl_plan_upload", "taccl_eval_batch",
-           "taccl_connections_batch", "taccl_last_error", "taccl_version"]
+           "taccl_connections_batch", "taccl_generate_host", "taccl_last_error",
+           "taccl_version"]
 
 _lib = None
 
@@ -93,6 +94,8 @@ def lib():
     L.taccl_eval_batch.argtypes = [P, ct.c_int64, P, P, P, P, P]
     L.taccl_connections_batch.restype = st
     L.taccl_connections_batch.argtypes = [P, ct.c_int64, P, P, P]
+    L.taccl_generate_host.restype = st
+    L.taccl_generate_host.argtypes = [P, ct.c_uint64, ct.c_int64, ct.c_int64, P, P]
     L.taccl_last_error.restype = ct.c_char_p
     L.taccl_last_error.argtypes = []
     L.taccl_version.restype = ct.c_int32
@@ -174,6 +177,15 @@ class Plan:
         out = np.zeros(self.route_stride, dtype=np.int32)
         _check(lib().taccl_plan_route_options(self._h, _np_ptr(out)))
         return out
+
+    def generate(self, seed, first, count):
+        """Seeded candidates first .. first+count-1 on the host:
+        (routes u8 [count, route_stride], prio u32 [count, prio_stride])."""
+        routes = np.zeros((count, self.route_stride), dtype=np.uint8)
+        prio = np.zeros((count, self.prio_stride), dtype=np.uint32)
+        _check(lib().taccl_generate_host(self._h, int(seed), int(first), int(count),
+                                         _np_ptr(routes), _np_ptr(prio)))
+        return routes, prio
 
     def link_costs(self):
         out = np.zeros(self.E, dtype=np.uint32)

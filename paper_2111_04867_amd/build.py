@@ -30,6 +30,12 @@ def build_library(verbose=False, jobs=8):
         procs.append(subprocess.Popen(cmd, stderr=subprocess.PIPE, text=True))
         if len([p for p in procs if p.poll() is None]) >= jobs:
             procs[0].wait()
+    # the seeded input generator (plain C, shared with the tests)
+    gen_o = os.path.join(objdir, "candgen.c.o")
+    objs.append(gen_o)
+    procs.append(subprocess.Popen(["gcc", "-O3", "-std=c11", "-Wall", "-fPIC", "-fvisibility=hidden",
+                                   "-c", os.path.join(ROOT, "workloads", "candgen.c"), "-o", gen_o],
+                                  stderr=subprocess.PIPE, text=True))
     failed = False
     for p in procs:
         err = p.communicate()[1]

@@ -340,6 +340,24 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
   return TACCL_OK;
 }
 
+// the seeded input generator shared with the tests (workloads/candgen.c)
+extern "C" int candgen_fill(uint64_t seed, int64_t first, int64_t count, int route_stride,
+                            const int32_t *options, int prio_stride, uint8_t *routes,
+                            uint32_t *prio);
+
+taccl_status_t taccl_generate_host(taccl_plan_t p, uint64_t seed, int64_t first, int64_t count,
+                                   uint8_t *routes, uint32_t *prio) {
+  if (!p) return fail(TACCL_ERR_INVALID_ARGUMENT, "null plan");
+  if (first < 0 || count < 0)
+    return fail(TACCL_ERR_INVALID_ARGUMENT, "negative first candidate or count");
+  if (count == 0) return TACCL_OK;
+  if (!routes || !prio) return fail(TACCL_ERR_INVALID_ARGUMENT, "null output buffer");
+  if (candgen_fill(seed, first, count, p->route_stride, p->route_options.data(), p->prio_stride,
+                   routes, prio) != 0)
+    return fail(TACCL_ERR_INVALID_ARGUMENT, "candidate range beyond 2^32");
+  return TACCL_OK;
+}
+
 taccl_status_t taccl_connections_batch(taccl_plan_t p, int64_t n, const uint8_t *d_routes,
                                        uint32_t *d_connections, taccl_stream_t stream) {
   if (!p) return fail(TACCL_ERR_INVALID_ARGUMENT, "null plan");

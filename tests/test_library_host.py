@@ -14,6 +14,7 @@ import pytest
 from oracle import OraclePlan
 from paper_2111_04867_amd import binding as B
 from workloads import configs as cf
+from workloads import generate
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -195,3 +196,25 @@ def test_connections_argument_checks():
     assert L.taccl_connections_batch(plan._h, 1, buf, ct.c_void_p(66), None) == \
         B.ERR_INVALID_ARGUMENT
     assert L.taccl_connections_batch(plan._h, 0, None, None, None) == B.OK
+
+
+def test_generate_host_matches_the_shared_generator():
+    """taccl_generate_host draws exactly what the tests' generator draws, for
+    any candidate range on its own."""
+    for name in ("twonode16_ag", "fournode64_a2a", "switch16_a2a"):
+        w = cf.named(name)
+        plan = B.Plan.from_workload(w)
+        r1, p1 = plan.generate(w.seed, 5, 7)
+        r2, p2 = generate(w.seed, 5, 7, plan.route_options(), plan.prio_stride)
+        assert np.array_equal(r1, r2) and np.array_equal(p1, p2)
+        r3, p3 = plan.generate(w.seed, 0, 12)
+        assert np.array_equal(r3[5:], r1) and np.array_equal(p3[5:], p1)
+        opts = plan.route_options()
+        assert ((r3 < np.maximum(opts, 1)) | (opts == 0)).all()
+
+
+def test_generate_host_argument_checks():
+    plan = B.Plan.from_workload(cf.ring4_ag())
+    assert status_of(lambda: plan.generate(1, -1, 2)) == B.ERR_INVALID_ARGUMENT
+    assert status_of(lambda: plan.generate(1, (1 << 32) - 1, 2)) == B.ERR_INVALID_ARGUMENT
+    assert plan.generate(1, 0, 0)[0].shape == (0, plan.route_stride)
