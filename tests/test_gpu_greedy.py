@@ -171,6 +171,20 @@ def test_full_batch_sampled(name):
     assert ok.all()
 
 
+@pytest.mark.parametrize("order", [1, 2])
+def test_alltoall_block_kernel_eight_chunks_per_thread(order):
+    """8192 chunks: the block kernel's largest shape (8 chunks per thread)."""
+    edges = [(u, v, 700, 8) for u in range(64) for v in range(64) if u != v]
+    row_ptr, col, a, b = cf.csr_from_edges(64, edges)
+    w = cf.Workload("mesh64_a2a", 64, 64, row_ptr, col, a, b, None, cf.ALLTOALL, 2, 4096,
+                    cf.KSHORTEST, k=2, order=order)
+    plan, ref, opts = plans(w)
+    assert plan.num_chunks == 8192
+    routes, prio = generate(9, 0, 6, opts, plan.prio_stride)
+    prio[:, ::5] = 2
+    check(plan, ref, routes, prio, f"mesh64 cpr=2 alltoall greedy order={order}")
+
+
 def test_alltoall_too_large_refused():
     """More than 8192 chunks (8 per thread of a 1024-thread block): refused,
     not approximated."""
