@@ -650,6 +650,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       rcl[j][0] = rcl[j][1] = rcl[j][2] = 0;
       if (c < C) {
         const uint32_t np = cp[j] >> 24;
+        if (cp[j] == kNoRoute) unrouted = true;  // no route option at all: never delivered
         if (np) {
           if (kk[j] < np) {
             const uint4 r = ((const uint4 *)a.arec)[(cp[j] & 0xFFFFFFu) + kk[j]];

@@ -435,7 +435,10 @@ static taccl_status_t build_levels(taccl_plan *p) {
       const int32_t pair = ch / cpr, s = pair / P, d = pair % P;
       if (s == d) continue;
       const size_t pp = (size_t)s * P + d;
-      p->cpath[ch] = p->pair_base[pp] | ((uint32_t)p->npaths[pp] << 24);
+      // a pair without any route option can never be delivered: marked by
+      // an all-ones option index and no options
+      p->cpath[ch] = p->npaths[pp] ? p->pair_base[pp] | ((uint32_t)p->npaths[pp] << 24)
+                                   : kNoRoute;
     }
     // priority sub-buckets per class, sized from the class's expected
     // membership under uniform route choice so a bucket holds 1-2 sends

@@ -14,6 +14,8 @@ namespace taccl {
 // Limits of the register-resident Alltoall kernel.
 constexpr int kFastMaxHops = 6;
 constexpr int kFastMaxChunks = 4096;
+// chunk table entry of a pair that has no route option at all
+constexpr uint32_t kNoRoute = 0x00FFFFFFu;
 
 // Set the thread-local error message and return the status.
 taccl_status_t fail(taccl_status_t st, const std::string &msg);
@@ -127,8 +129,9 @@ struct taccl_plan {
   std::vector<uint16_t> cls_link;      // [ncls]
   // register-resident Alltoall kernel: per route option {hops | level of
   // hop h << (8+3h), classes of hops 0..5 as u16 pairs}; per chunk its pair's
-  // first option | option count << 24; per class link | (first bucket of the
-  // same level and link, level-relative) << 16
+  // first option | option count << 24 (kNoRoute: the pair has no option);
+  // per class link | (first bucket of the same level and link,
+  // level-relative) << 16
   bool path_fast = false;
   std::vector<uint32_t> arec, cpath, cinfo;
   // per class: first priority sub-bucket (level-relative) | bits << 24

@@ -239,3 +239,24 @@ def test_multicast_slots_straddling_groups(kind, P, cpr, greedy):
     rmk, rok = ref.eval_threads(routes, prio)
     bad = np.nonzero((mk != rmk) | (ok != rok))[0]
     assert bad.size == 0, f"{w.name}: {bad.size} mismatches, first at {bad[:5].tolist()}"
+
+
+@pytest.mark.parametrize("option", ["static", "contig", "greedy", "rgreedy"])
+def test_alltoall_pairs_without_any_route(option):
+    """Pairs the sketch leaves without any route option can never be
+    delivered: every candidate is invalid (regression: the register-resident
+    kernel once skipped such pairs and reported valid)."""
+    edges = [(0, 1, 700, 46), (1, 0, 700, 46), (2, 3, 700, 46), (3, 2, 700, 46),
+             (1, 3, 1700, 106), (3, 1, 1700, 106)]
+    row_ptr, col, a, b = cf.csr_from_edges(4, edges)
+    node_of = np.array([0, 0, 1, 1], dtype=np.int32)
+    relay = np.array([1, 0, 1, 0], dtype=np.uint8)  # the IB link joins two non-relays
+    w = cf.Workload("split4_a2a", 4, 4, row_ptr, col, a, b, node_of, cf.ALLTOALL, 2, 65536,
+                    cf.KSHORTEST, k=2, max_cross=1, relay=relay)
+    w = {"static": w, "contig": cf.with_contiguity(w), "greedy": cf.with_greedy(w),
+         "rgreedy": cf.with_reverse_greedy(w)}[option]
+    plan, ref, opts = plans(w)
+    assert (opts == 0).any() and (opts > 0).any()
+    routes, prio = generate(3, 0, 64, opts, plan.prio_stride)
+    mk, ok = check(plan, ref, routes, prio, f"split4 {option}")
+    assert not ok.any() and (mk > 0).all()
