@@ -66,3 +66,39 @@ def test_random_plans(block):
         checked += 1
     print(f"[gpu] block {block}: {checked} plans checked, {refused} refused", flush=True)
     assert checked >= 75
+
+
+def test_random_larger_plans():
+    """300 larger seeded plans (up to 24 ranks, two switches, three nodes,
+    six options per pair, three chunks per rank), 32 candidates each. Plans
+    whose switch links would be both send and receive ports are refused at
+    plan time (a documented limit of the port model) and skipped."""
+    from paper_2111_04867_amd.binding import ERR_UNSUPPORTED, Plan, TacclError
+    from workloads import random_workload_large
+    checked = 0
+    for seed in range(300):
+        w = random_workload_large(seed)
+        try:
+            ref = OraclePlan.from_workload(w)
+        except Exception:
+            continue
+        try:
+            plan = Plan.from_workload(w)
+        except TacclError as e:
+            assert e.status == ERR_UNSUPPORTED and w.switch_ports, (seed, str(e))
+            continue
+        routes, prio = generate(seed, 0, 32, plan.route_options(), plan.prio_stride)
+        rng = np.random.default_rng(seed)
+        routes[rng.random(routes.shape) < 0.02] = 0xFF
+        prio[rng.random(prio.shape) < 0.3] = 5
+        print(f"[gpu] larger random plan {seed}: kind={w.kind} P={w.P} V={w.V} "
+              f"mode={w.route_mode} k={w.k} cpr={w.chunks_per_rank} contig={w.contiguity} "
+              f"greedy={w.order} ports={w.switch_ports}", flush=True)
+        mk, ok = plan.eval(routes, prio)
+        rmk, rok = ref.eval(routes, prio)
+        bad = np.nonzero((mk != rmk) | (ok != rok))[0]
+        assert bad.size == 0, (f"larger random plan {seed}: {bad.size} mismatches, first at "
+                               f"{bad[:5].tolist()}: gpu {mk[bad[:5]].tolist()} "
+                               f"oracle {rmk[bad[:5]].tolist()}")
+        checked += 1
+    assert checked >= 200

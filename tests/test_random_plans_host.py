@@ -43,3 +43,26 @@ def test_many_remaining_cost_levels():
             continue
         most = max(most, plan.info["num_levels"])
     assert most > 127
+
+
+def test_library_and_oracle_agree_on_larger_plans():
+    """The larger random plans: the same acceptance (apart from the switch
+    port model's documented limit, which only the library has) and the same
+    route options."""
+    from workloads import random_workload_large
+    accepted = 0
+    for seed in range(300):
+        w = random_workload_large(seed)
+        try:
+            ref = OraclePlan.from_workload(w)
+        except Exception:
+            ref = None
+        try:
+            plan = B.Plan.from_workload(w)
+        except B.TacclError as e:
+            assert ref is None or (w.switch_ports and "port" in str(e)), (seed, str(e))
+            continue
+        assert ref is not None, seed
+        assert (plan.route_options() == ref.route_options()).all(), seed
+        accepted += 1
+    assert accepted >= 200

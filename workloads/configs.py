@@ -468,3 +468,78 @@ def random_workload(seed):
     elif extra == "ports" and kind == ALLTOALL and switch:
         w = with_switch_ports(w)
     return w
+
+
+def random_workload_large(seed):
+    """A seeded random larger plan for parity sweeps: 2..24 ranks on a
+    bidirectional ring plus random link pairs, up to two switch vertices
+    (possibly linked to each other), up to three nodes with random relay
+    ranks and inter-node links only between relays, any collective kind,
+    any route mode, up to 6 options per pair and 3 chunks per rank, and one
+    of static orders, greedy orders in path or reverse path order,
+    contiguous transfers or switch ports."""
+    rng = np.random.default_rng(seed)
+    kind = int(rng.choice([ALLGATHER, ALLTOALL, REDUCESCATTER, ALLREDUCE, EXPLICIT]))
+    P = int(rng.integers(2, 25))
+    nsw = int(rng.choice([0, 0, 1, 2]))
+    nn = int(rng.choice([1, 1, 2, 3])) if P >= 3 else 1
+    V = P + nsw
+    node_of = np.array([min(r * nn // P, nn - 1) for r in range(P)] +
+                       [int(rng.integers(0, nn)) for _ in range(nsw)], dtype=np.int32)
+    relay = (rng.random(V) < 0.5).astype(np.uint8)
+    for n in range(nn):
+        ranks = [r for r in range(P) if node_of[r] == n]
+        if ranks:
+            relay[ranks[0]] = 1
+    links = {}
+
+    def add(u, v):
+        if u != v and (u, v) not in links:
+            links[(u, v)] = (int(rng.choice([700, 1700, 300])), int(rng.choice([8, 46, 106, 3])))
+
+    for i in range(P):
+        add(i, (i + 1) % P)
+        add((i + 1) % P, i)
+    for _ in range(int(rng.integers(0, 3 * P))):
+        u, v = (int(x) for x in rng.integers(0, P, 2))
+        add(u, v)
+        add(v, u)
+    for k in range(nsw):
+        sw = P + k
+        for r in range(P):
+            if node_of[r] == node_of[sw] and rng.random() < 0.9:
+                add(r, sw)
+                add(sw, r)
+    if nsw == 2 and rng.random() < 0.5:
+        add(P, P + 1)
+        add(P + 1, P)
+    cross = bool(rng.random() < 0.7) and nn > 1
+    if cross:
+        links = {(u, v): x for (u, v), x in links.items()
+                 if node_of[u] == node_of[v] or (relay[u] and relay[v])}
+    row_ptr, col, a, b = csr_from_edges(V, [(u, v, x[0], x[1]) for (u, v), x in links.items()])
+    modes = [SHORTEST_ONLY, KSHORTEST, KSHORTEST, RELAY1] + ([HIER_RELAY] if nn > 1 else [])
+    mode = int(rng.choice(modes))
+    owner = post_ptr = post = None
+    if kind == EXPLICIT:
+        C = int(rng.integers(1, 3 * P))
+        owner = rng.integers(0, P, C).astype(np.int32)
+        posts = [sorted(set(int(x) for x in rng.integers(0, P, int(rng.integers(1, P + 1)))))
+                 for _ in range(C)]
+        post_ptr = np.cumsum([0] + [len(p) for p in posts]).astype(np.int32)
+        post = np.array([x for p in posts for x in p], dtype=np.int32)
+    w = Workload(f"large{seed}", V, P, row_ptr, col, a, b, node_of if nn > 1 else None, kind,
+                 int(rng.integers(1, 4)), int(rng.choice([4096, 65536, 1 << 20])), mode,
+                 k=int(rng.integers(1, 7)), max_cross=1 if cross else -1,
+                 relay=relay if (cross or mode in (RELAY1, HIER_RELAY)) else None,
+                 owner=owner, post_ptr=post_ptr, post=post, seed=seed)
+    extra = rng.choice(["static", "greedy", "rgreedy", "contig", "ports"])
+    if extra == "greedy":
+        w = with_greedy(w)
+    elif extra == "rgreedy":
+        w = with_reverse_greedy(w)
+    elif extra == "contig" and nn > 1:
+        w = with_contiguity(w)
+    elif extra == "ports" and kind == ALLTOALL and nsw:
+        w = with_switch_ports(w)
+    return w
