@@ -1,10 +1,16 @@
 // Host-side plan builder: topology, collective, sketch -> evaluation plan.
 //
 // Route options follow the sketch (Sec. 3.1) and the shortest-path
-// restriction of routing (Sec. 5.1, Step 1). Paths are produced by a
-// best-first search over partial paths ordered by (cost, hops, vertex
-// sequence); with positive link costs the complete paths leave the queue in
-// exactly that order, so the first k popped are the k best.
+// restriction of routing (Sec. 5.1, Step 1): the k best simple paths by
+// (cost, hops, vertex sequence). They are found by a best-first search over
+// partial paths ordered by cost so far plus a lower bound of the cost still
+// to go (the distance to the destination over the usable links, ignoring
+// the simple-path and crossing rules). Complete paths then leave the queue
+// in nondecreasing cost, and every path of cost <= C is out before a
+// partial path whose bound exceeds C; so once k complete paths are out, the
+// search goes on only while the bound is at most the k-th cost (to collect
+// its ties), and the collected paths sorted by (cost, hops, vertex
+// sequence) give the k best exactly.
 #include <algorithm>
 #include <unordered_map>
 #include <cstring>
@@ -37,26 +43,35 @@ struct Path {
 };
 
 struct Partial {
+  uint64_t bound;  // cost + lower bound of the cost still to go
   uint64_t cost;
   int32_t cross;
   std::vector<int32_t> verts;
   std::vector<int32_t> links;
 };
 
-// priority_queue keeps the largest on top; invert (cost, hops, verts)
+// priority_queue keeps the largest on top; invert (bound, hops, verts)
 struct PartialAfter {
   bool operator()(const Partial &a, const Partial &b) const {
-    if (a.cost != b.cost) return a.cost > b.cost;
+    if (a.bound != b.bound) return a.bound > b.bound;
     if (a.links.size() != b.links.size()) return a.links.size() > b.links.size();
     return a.verts > b.verts;
   }
 };
 
+bool path_before(const Path &a, const Path &b) {
+  if (a.cost != b.cost) return a.cost < b.cost;
+  if (a.links.size() != b.links.size()) return a.links.size() < b.links.size();
+  return a.verts < b.verts;
+}
+
 class Router {
  public:
   Router(const taccl_topology &t, const std::vector<uint32_t> &cost, const uint8_t *allowed,
          const uint8_t *relay)
-      : t_(t), cost_(cost), allowed_(allowed), relay_(relay) {}
+      : t_(t), cost_(cost), allowed_(allowed), relay_(relay), in_(t.V) {
+    for (int32_t e = 0; e < t.E; e++) in_[t.col[e]].push_back(e);
+  }
 
   // Up to k best simple paths s -> d with at most max_cross node crossings.
   // only_min keeps just the minimal-cost ones. Returns false if the search
@@ -64,22 +79,28 @@ class Router {
   bool k_best(int32_t s, int32_t d, int32_t k, int32_t max_cross, bool only_min,
               std::vector<Path> &out) const {
     out.clear();
+    const std::vector<uint64_t> &h = to_go(d);
+    if (h[s] == kFar) return true;  // no path at all
     std::priority_queue<Partial, std::vector<Partial>, PartialAfter> q;
-    q.push(Partial{0, 0, {s}, {}});
+    q.push(Partial{h[s], 0, 0, {s}, {}});
     int64_t budget = 20000000;
-    while (!q.empty() && (int32_t)out.size() < k) {
+    while (!q.empty()) {
       Partial cur = q.top();
       q.pop();
+      // enough paths, and no cheaper or equally cheap one can follow
+      if (!out.empty() && (int32_t)out.size() >= (only_min ? 1 : k) &&
+          cur.bound > out[only_min ? 0 : k - 1].cost)
+        break;
       if (--budget < 0) return false;
       int32_t u = cur.verts.back();
       if (u == d) {
-        if (only_min && !out.empty() && cur.cost != out[0].cost) break;
         out.push_back(Path{cur.verts, cur.links, cur.cost});
         continue;
       }
       for (int32_t e = t_.row_ptr[u]; e < t_.row_ptr[u + 1]; e++) {
         if (allowed_ && !allowed_[e]) continue;
         int32_t v = t_.col[e];
+        if (h[v] == kFar) continue;
         if (std::find(cur.verts.begin(), cur.verts.end(), v) != cur.verts.end()) continue;
         int32_t cross = cur.cross;
         if (t_.node[u] != t_.node[v]) {
@@ -87,12 +108,17 @@ class Router {
           if (max_cross >= 0 && cross > max_cross) continue;
           if (relay_ && !(relay_[u] && relay_[v])) continue;
         }
-        Partial nxt{cur.cost + cost_[e], cross, cur.verts, cur.links};
+        const uint64_t c = cur.cost + cost_[e];
+        Partial nxt{c + h[v], c, cross, cur.verts, cur.links};
         nxt.verts.push_back(v);
         nxt.links.push_back(e);
         q.push(std::move(nxt));
       }
     }
+    std::sort(out.begin(), out.end(), path_before);
+    if (only_min)
+      while (!out.empty() && out.back().cost != out[0].cost) out.pop_back();
+    if ((int32_t)out.size() > k) out.resize(k);
     return true;
   }
 
@@ -131,10 +157,43 @@ class Router {
   }
 
  private:
+  static constexpr uint64_t kFar = ~0ull;
+  // cost of the cheapest walk from every vertex to d over the usable links
+  // (allowed, and between nodes only between relays): a lower bound of any
+  // simple path's remaining cost, cached per destination
+  const std::vector<uint64_t> &to_go(int32_t d) const {
+    auto it = h_.find(d);
+    if (it != h_.end()) return it->second;
+    std::vector<uint64_t> dist(t_.V, kFar);
+    using Item = std::pair<uint64_t, int32_t>;
+    std::priority_queue<Item, std::vector<Item>, std::greater<Item>> q;
+    dist[d] = 0;
+    q.push({0, d});
+    while (!q.empty()) {
+      auto [du, v] = q.top();
+      q.pop();
+      if (du != dist[v]) continue;
+      // links u -> v: scan every link whose head is v
+      for (int32_t e : in_[v]) {
+        const int32_t u = t_.src[e];
+        if (allowed_ && !allowed_[e]) continue;
+        if (t_.node[u] != t_.node[v] && relay_ && !(relay_[u] && relay_[v])) continue;
+        const uint64_t nd = du + cost_[e];
+        if (nd < dist[u]) {
+          dist[u] = nd;
+          q.push({nd, u});
+        }
+      }
+    }
+    return h_.emplace(d, std::move(dist)).first->second;
+  }
+
   const taccl_topology &t_;
   const std::vector<uint32_t> &cost_;
   const uint8_t *allowed_;
   const uint8_t *relay_;
+  std::vector<std::vector<int32_t>> in_;  // links into every vertex
+  mutable std::unordered_map<int32_t, std::vector<uint64_t>> h_;
 };
 
 }  // namespace
