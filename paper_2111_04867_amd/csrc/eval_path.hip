@@ -484,7 +484,6 @@ int32_t path_layout(const taccl_plan &p, PathArgs &a) {
   a.o_ctime = take(4 * C);
   a.o_lfree = take(4 * E);
   a.o_ccnt = take(4 * (K + 1));
-  a.o_cbase = a.o_ccnt;
   a.o_ccur = take(4 * K);
   a.o_echunk = take(2 * M);
   a.o_eprio = take(4 * M);
@@ -918,9 +917,7 @@ int32_t path_fast_layout(const taccl_plan &p, PathArgs &a) {
   // wavefront (slots without a send count there)
   a.o_fbcnt = take(4 * (p.max_lvl_nb + 1 + 64));
   a.o_fepr = take(8 * M);
-  a.o_fech = 0;
   a.o_fsrt = take(4 * path_fast_threads(p) * path_fast_cpt(p));
-  a.o_fscl = 0;
   // packed sorted sends: chunk, link and run index in one word
   auto bits = [](uint32_t n) {  // bits to hold 0 .. n-1
     uint32_t b = 0;

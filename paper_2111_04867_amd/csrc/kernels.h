@@ -29,7 +29,7 @@ struct TreeArgs {
   int64_t n;
   int32_t waves_per_block;
   // LDS carve-up: shared tables (byte offsets from the block's base)
-  int32_t o_cost, o_src, o_dst, o_rec, o_np, o_own, o_post, o_wave;
+  int32_t o_cost, o_src, o_rec, o_own, o_post, o_wave;
   // per-wavefront state (byte offsets from the wavefront's base)
   int32_t w_rt, w_key, w_prio, w_chain, w_par, w_mask, w_base, w_head, w_free;
   int32_t wave_bytes;
@@ -49,7 +49,7 @@ struct TreeArgs {
   // time-aware greedy orders: smallest link cost (the simulation's
   // lookahead) and per-wavefront arrays
   uint32_t cmin;
-  int32_t w_gkey, w_gpri, w_glp, w_gfin, w_grdy, w_gpend, w_glist, w_gofs;
+  int32_t w_gfin, w_grdy, w_gpend, w_glist, w_gofs;
   const uint8_t *topt;  // options of (o, d) through vertex v, one byte per d
   const uint4 *rec4;    // route records, one 16-byte record per option
   int32_t o_rec4, o_opt;
@@ -79,13 +79,12 @@ struct PathArgs {
   uint32_t *makespan;
   uint8_t *valid;
   int64_t n;
-  int32_t o_rt, o_ctime, o_lfree, o_ccnt, o_cbase, o_ccur, o_echunk, o_eprio, o_ecls, o_sorted,
-      o_red;
+  int32_t o_rt, o_ctime, o_lfree, o_ccnt, o_ccur, o_echunk, o_eprio, o_ecls, o_sorted, o_red;
   // register-resident kernel
   int32_t ncls;
   const uint32_t *arec, *cpath, *cinfo, *cbkt;
-  int32_t o_fcost, o_fcinfo, o_fcbkt, o_flcb, o_fctime, o_flfree, o_fbcnt, o_fepr, o_fech, o_fsrt, o_fscl,
-      o_fred, o_fred64, o_fredf;
+  int32_t o_fcost, o_fcinfo, o_fcbkt, o_flcb, o_fctime, o_flfree, o_fbcnt, o_fepr, o_fsrt, o_fred,
+      o_fred64, o_fredf;
   int32_t lds_bytes;
   int32_t cbits, lbits;  // chunk and link fields of a packed sorted send
   // contiguous transfers on links between nodes (contig != 0)
