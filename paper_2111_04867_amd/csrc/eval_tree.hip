@@ -1856,8 +1856,9 @@ int32_t tree_layers_layout(const taccl_plan &p, TreeArgs &a) {
   const int32_t C = p.coll.C, V = p.topo.V, E = p.topo.E, P = p.topo.P;
   const int32_t CV = C * V;
   const int32_t K = std::max(p.max_paths, 1), H = std::max(p.H, 1);
-  const int32_t pw = P / 4;  // route words per chunk: 1, 2, 4 or 8
-  if (p.topt.empty() || K > 8 || H > 4 || P % 4 || (pw != 1 && pw != 2 && pw != 4 && pw != 8) ||
+  const int32_t pw = P / 4;  // route words per chunk: 1, 2, 3, 4, 6 or 8
+  if (p.topt.empty() || K > 8 || H > 4 || P % 4 ||
+      (pw != 1 && pw != 2 && pw != 3 && pw != 4 && pw != 6 && pw != 8) ||
       V > 64 || E < 1 ||
       CV > 64 * 16 || p.route_stride > 4 * 64 * kPfRoute || E > (1 << 22))
     return 0;
@@ -1924,7 +1925,9 @@ static const void *layers_fn_j(int pw) {
   switch (pw) {
     case 1: return (const void *)tree_layers_kernel<J, 1, kC, kR>;
     case 2: return (const void *)tree_layers_kernel<J, 2, kC, kR>;
+    case 3: return (const void *)tree_layers_kernel<J, 3, kC, kR>;
     case 4: return (const void *)tree_layers_kernel<J, 4, kC, kR>;
+    case 6: return (const void *)tree_layers_kernel<J, 6, kC, kR>;
     default: return (const void *)tree_layers_kernel<J, 8, kC, kR>;
   }
 }
@@ -1956,7 +1959,7 @@ int tree_layers_blocks_per_cu(const TreeArgs &a) {
 
 hipError_t launch_tree_layers(const TreeArgs &a, int grid, hipStream_t stream) {
   const int pw = a.P / 4;
-  if (a.P % 4 || (pw != 1 && pw != 2 && pw != 4 && pw != 8)) return hipErrorInvalidValue;
+  if (a.P % 4 || (pw != 1 && pw != 2 && pw != 3 && pw != 4 && pw != 6 && pw != 8)) return hipErrorInvalidValue;
   const dim3 g(grid), b(64 * a.waves_per_block);
   const int bytes = tree_block_bytes(a, a.waves_per_block);
   void *args[] = {(void *)&a};
@@ -1998,7 +2001,9 @@ static const void *greedy_fn_j(int pw) {
   switch (pw) {
     case 1: return (const void *)tree_greedy_kernel<J, 1, kR>;
     case 2: return (const void *)tree_greedy_kernel<J, 2, kR>;
+    case 3: return (const void *)tree_greedy_kernel<J, 3, kR>;
     case 4: return (const void *)tree_greedy_kernel<J, 4, kR>;
+    case 6: return (const void *)tree_greedy_kernel<J, 6, kR>;
     default: return (const void *)tree_greedy_kernel<J, 8, kR>;
   }
 }
@@ -2068,7 +2073,7 @@ int tree_greedy_blocks_per_cu(const TreeArgs &a) {
 
 hipError_t launch_tree_greedy(const TreeArgs &a, int grid, hipStream_t stream) {
   const int pw = a.P / 4;
-  if (a.P % 4 || (pw != 1 && pw != 2 && pw != 4 && pw != 8)) return hipErrorInvalidValue;
+  if (a.P % 4 || (pw != 1 && pw != 2 && pw != 3 && pw != 4 && pw != 6 && pw != 8)) return hipErrorInvalidValue;
   const dim3 g(grid), b(64 * a.waves_per_block);
   void *args[] = {(void *)&a};
   return hipLaunchKernel(greedy_fn(a), g, b, args, tree_block_bytes(a, a.waves_per_block),

@@ -152,3 +152,26 @@ def test_degenerate_explicit(base, option):
             assert (mk == 0).all() and ok.all()
         else:
             assert (mk > 0).all() and ok.all()
+
+
+def quads(P, kind, k=3):
+    """P ranks in fully connected groups of four, rank i linked to i + 4:
+    a cube-mesh-like graph that 12 and 24 ranks keep within the layered
+    kernel's limits (route words of 3 and 6 per chunk)."""
+    edges = set()
+    for g in range(0, P, 4):
+        edges |= {(u, v) for u in range(g, g + 4) for v in range(g, g + 4) if u != v}
+    for i in range(P):
+        edges |= {(i, (i + 4) % P), ((i + 4) % P, i)}
+    row_ptr, col, a, b = cf.csr_from_edges(P, [(u, v, 700, 46) for u, v in sorted(edges)])
+    return cf.Workload(f"quads{P}", P, P, row_ptr, col, a, b, None, kind, 1, 65536,
+                       cf.KSHORTEST, k=k)
+
+
+@pytest.mark.parametrize("option", ["static", "greedy", "rgreedy"])
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("P,k", [(12, 3), (24, 2)])
+def test_twelve_and_twenty_four_ranks(P, k, kind, option):
+    w = quads(P, kind, k)
+    w = {"static": w, "greedy": cf.with_greedy(w), "rgreedy": cf.with_reverse_greedy(w)}[option]
+    check(w, n=128)
