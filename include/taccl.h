@@ -247,6 +247,14 @@ taccl_status_t taccl_plan_upload(taccl_plan_t plan);
  *   d_valid: device, n uint8: 1 if every (chunk, rank) pair of the
  *     postcondition holds at the end, else 0.
  * Each candidate is evaluated independently; results are exact (integer).
+ * Every real makespan is below TACCL_MAKESPAN_FAULT (taccl_sketch_apply
+ * refuses plans whose worst case, the sum of all send costs over both
+ * phases of an Allreduce, could reach it). A candidate whose evaluation
+ * exceeded a bound the kernel relies on (a round limit of an iterative
+ * schedule, a layer index past the plan's bound; none is reachable for a
+ * plan that taccl_sketch_apply accepted) comes back as makespan ==
+ * TACCL_MAKESPAN_FAULT with valid == 0, so such an internal fault is never
+ * mistaken for a bad candidate; taccl_count_faults counts them.
  * Errors (synchronous): INVALID_ARGUMENT for null pointers with n > 0,
  * n < 0 or a misaligned d_prio; UNSUPPORTED when a candidate's state does
  * not fit one block's LDS or an Alltoall greedy plan exceeds its limits;
@@ -257,6 +265,17 @@ taccl_status_t taccl_plan_upload(taccl_plan_t plan);
 taccl_status_t taccl_eval_batch(taccl_plan_t plan, int64_t n, const uint8_t *d_routes,
                                 const uint32_t *d_prio, uint32_t *d_makespan, uint8_t *d_valid,
                                 taccl_stream_t stream);
+
+/* Makespan written for a candidate whose evaluation hit an internal fault. */
+#define TACCL_MAKESPAN_FAULT 0xFFFFFFFFu
+
+/*
+ * Host check of a batch's results after synchronisation: the number of
+ * candidates i < n with makespan[i] == TACCL_MAKESPAN_FAULT (host arrays,
+ * owned by the caller). A nonzero count means a kernel fault, not a bad
+ * candidate. Errors: INVALID_ARGUMENT for a null array with n > 0 or n < 0.
+ */
+taccl_status_t taccl_count_faults(int64_t n, const uint32_t *makespan, int64_t *faults);
 
 /*
  * Switch-hyperedge connections of n candidates on the current device,

@@ -20,5 +20,19 @@ def build_oracle(verbose=False):
     return LIB
 
 
+def build_oracle_sanitized(out_dir, verbose=False):
+    """The oracle under AddressSanitizer and UndefinedBehaviorSanitizer (clang,
+    so that one runtime serves every sanitized library of the process)."""
+    os.makedirs(out_dir, exist_ok=True)
+    out = os.path.join(out_dir, "liboracle_san.so")
+    cmd = ["/opt/rocm/llvm/bin/clang", "-O1", "-g", "-std=c11", "-Wall", "-Wextra", "-fPIC",
+           "-shared", "-fsanitize=address,undefined", "-fno-omit-frame-pointer",
+           "-fno-sanitize-recover=all", "-shared-libsan", SRC, "-o", out]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    return out
+
+
 if __name__ == "__main__":
     print(build_oracle(verbose=True))

@@ -53,6 +53,8 @@ def _load():
     lib.orc_set_contiguity.argtypes = [P, ct.c_int]
     lib.orc_eval.restype = ct.c_int
     lib.orc_eval.argtypes = [P, ct.c_int64, P, P, P, P]
+    lib.orc_eval_ops.restype = ct.c_int
+    lib.orc_eval_ops.argtypes = [P, ct.c_int64, P, P, P, P, P]
     lib.orc_connections.restype = ct.c_int
     lib.orc_connections.argtypes = [P, ct.c_int64, P, P]
     lib.orc_eval_detail.restype = ct.c_int
@@ -186,6 +188,23 @@ class OraclePlan:
         if rc != 0:
             raise OracleError(f"orc_eval failed ({rc})")
         return mk, ok
+
+    def eval_ops(self, routes, prio):
+        """eval() plus the algorithmic operation count of every candidate (the
+        op model of orc_eval_ops); returns (makespan, valid, ops)."""
+        routes = np.ascontiguousarray(routes, dtype=np.uint8).reshape(-1, self.route_stride)
+        prio = np.ascontiguousarray(prio, dtype=np.uint32).reshape(-1, self.prio_stride)
+        n = routes.shape[0]
+        if prio.shape[0] != n:
+            raise ValueError("routes and prio disagree on the candidate count")
+        mk = np.zeros(n, dtype=np.uint32)
+        ok = np.zeros(n, dtype=np.uint8)
+        ops = np.zeros(n, dtype=np.uint64)
+        rc = _load().orc_eval_ops(self._h, n, _ptr(routes), _ptr(prio), _ptr(mk), _ptr(ok),
+                                  _ptr(ops))
+        if rc != 0:
+            raise OracleError(f"orc_eval_ops failed ({rc})")
+        return mk, ok, ops
 
     def eval_threads(self, routes, prio, threads=None):
         """eval() split over threads on disjoint candidate ranges (the C call

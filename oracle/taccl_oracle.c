@@ -57,6 +57,10 @@
  * v up to v). Allreduce is ReduceScatter then Allgather on the same trees,
  * timed back to back, with a separate priority row for each phase.
  *
+ * Operation count (orc_eval_ops): per candidate, the algorithmic integer
+ * operations of the op model described at phase_ops, for pricing the
+ * evaluation against an integer-issue roofline.
+ *
  * Connections (orc_connections): per candidate, the number of ordered rank
  * pairs that exchange a chunk through switch vertices only, the is_util
  * count that the uc-max / uc-min switch-hyperedge policies weigh in the
@@ -1327,6 +1331,93 @@ int orc_eval(const orc_plan *p, int64_t n, const uint8_t *routes, const uint32_t
   for (int64_t i = 0; i < n && rc == ORC_OK; i++)
     rc = eval_one(p, routes + (size_t)i * p->route_stride, prio + (size_t)i * p->prio_stride, &w,
                   &makespan[i], &valid[i]);
+  scratch_free(&w);
+  return rc;
+}
+
+/* Algorithmic integer operations of one schedule, the op model that prices
+ * the evaluation against the chip's integer issue rate:
+ *   one per link of every routed path walked while building the send set
+ *     (route decode and tree merge, or the path hops of an Alltoall);
+ *   three per send for its Step-2 keys (remaining, travelled, priority);
+ *   n_l * ceil(log2 n_l) comparisons to order the n_l sends of each link
+ *     (the per-link total order of Sec. 5.1 / App. B.2);
+ *   four per send for the timing sweep of App. B.3 (max of ready and link
+ *     free, add the latency, update the link, fold into the makespan);
+ *   two per word of the presence bitmasks the postcondition reads (App. B):
+ *     one bit per chunk at every vertex for multicast, one bit per source
+ *     chunk at every rank for Alltoall.
+ * Called after eval_phase, whose sends it reads. */
+static uint64_t ceil_log2(uint64_t n) {
+  uint64_t b = 0;
+  while ((1ull << b) < n) b++;
+  return b;
+}
+
+static uint64_t phase_ops(const orc_plan *p, int phase, const uint8_t *rt, const oscratch *w) {
+  const int P = p->P;
+  uint64_t visits = 0;
+  for (int c = 0; c < p->C; c++) {
+    const int o = p->owner[c];
+    if (phase == ORC_ALLTOALL) {
+      const int d = p->post[p->post_ptr[c]];
+      if (d == o) continue;
+      const oplist *L = &p->paths[o * P + d];
+      if (rt[c] < L->n) visits += (uint64_t)L->p[rt[c]].hops;
+      continue;
+    }
+    for (int d = 0; d < P; d++) {
+      if (d == o || !in_post(p, c, d)) continue;
+      const oplist *L = &p->paths[o * P + d];
+      const int ch = rt[(size_t)c * P + d];
+      if (ch < L->n) visits += (uint64_t)L->p[ch].hops;
+    }
+  }
+  uint64_t *per_link = (uint64_t *)calloc((size_t)p->E + 1, sizeof(uint64_t));
+  uint64_t order = 0;
+  if (per_link) {
+    for (int i = 0; i < w->n; i++) per_link[w->s[i].link]++;
+    for (int e = 0; e < p->E; e++) order += per_link[e] * ceil_log2(per_link[e]);
+    free(per_link);
+  }
+  uint64_t words;
+  if (phase == ORC_ALLTOALL)
+    words = (uint64_t)P * (((uint64_t)P * (uint64_t)p->cpr + 31) / 32);
+  else
+    words = (uint64_t)p->V * (((uint64_t)p->C + 31) / 32);
+  return visits + 3 * (uint64_t)w->n + order + 4 * (uint64_t)w->n + 2 * words;
+}
+
+/* Evaluate n candidates like orc_eval and also write ops[i], the algorithmic
+ * operation count of candidate i (both phases of an Allreduce). */
+int orc_eval_ops(const orc_plan *p, int64_t n, const uint8_t *routes, const uint32_t *prio,
+                 uint32_t *makespan, uint8_t *valid, uint64_t *ops) {
+  oscratch w;
+  scratch_init(p, &w);
+  int rc = ORC_OK;
+  for (int64_t i = 0; i < n && rc == ORC_OK; i++) {
+    const uint8_t *rt = routes + (size_t)i * p->route_stride;
+    const uint32_t *pr = prio + (size_t)i * p->prio_stride;
+    if (p->kind != ORC_ALLREDUCE) {
+      rc = eval_phase(p, p->kind, rt, pr, &w, &makespan[i], &valid[i]);
+      if (rc == ORC_OK) ops[i] = phase_ops(p, p->kind, rt, &w);
+      continue;
+    }
+    uint32_t m1, m2;
+    uint8_t v1, v2;
+    rc = eval_phase(p, ORC_REDUCESCATTER, rt, pr, &w, &m1, &v1);
+    if (rc) break;
+    const uint64_t o1 = phase_ops(p, ORC_REDUCESCATTER, rt, &w);
+    rc = eval_phase(p, ORC_ALLGATHER, rt, pr + (size_t)p->C * p->V, &w, &m2, &v2);
+    if (rc) break;
+    if ((uint64_t)m1 + m2 >= (1ull << 32)) {
+      rc = ORC_ELIMIT;
+      break;
+    }
+    makespan[i] = m1 + m2;
+    valid[i] = (uint8_t)(v1 && v2);
+    ops[i] = o1 + phase_ops(p, ORC_ALLGATHER, rt, &w);
+  }
   scratch_free(&w);
   return rc;
 }

@@ -11,7 +11,9 @@ import os
 import numpy as np
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "libtaccl.so")
+# TACCL_LIB selects another build of the same sources (the host-sanitizer
+# build of tests/sanitize.py); the default is the in-tree library
+LIB_PATH = os.environ.get("TACCL_LIB", os.path.join(PKG, "libtaccl.so"))
 
 OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_LIMIT, ERR_NO_MEMORY, ERR_HIP = range(6)
 ALLGATHER, ALLTOALL, EXPLICIT = 0, 1, 2
@@ -46,7 +48,8 @@ EXPORTS = ["taccl_topology_create", "taccl_topology_destroy", "taccl_collective_
            "taccl_collective_create_explicit", "taccl_collective_destroy", "taccl_sketch_apply",
            "taccl_plan_destroy", "taccl_plan_info", "taccl_plan_route_options",
            "taccl_plan_path", "taccl_plan_link_costs", "taccl_plan_upload", "taccl_eval_batch",
-           "taccl_connections_batch", "taccl_generate_host", "taccl_last_error",
+           "taccl_connections_batch", "taccl_generate_host", "taccl_count_faults",
+           "taccl_last_error",
            "taccl_version"]
 
 _lib = None
@@ -96,6 +99,8 @@ def lib():
     L.taccl_connections_batch.argtypes = [P, ct.c_int64, P, P, P]
     L.taccl_generate_host.restype = st
     L.taccl_generate_host.argtypes = [P, ct.c_uint64, ct.c_int64, ct.c_int64, P, P]
+    L.taccl_count_faults.restype = st
+    L.taccl_count_faults.argtypes = [ct.c_int64, P, ct.POINTER(ct.c_int64)]
     L.taccl_last_error.restype = ct.c_char_p
     L.taccl_last_error.argtypes = []
     L.taccl_version.restype = ct.c_int32
@@ -110,6 +115,17 @@ def _check(status):
 
 def _np_ptr(a):
     return None if a is None else a.ctypes.data_as(ct.c_void_p)
+
+
+MAKESPAN_FAULT = 0xFFFFFFFF  # makespan of a candidate whose evaluation faulted
+
+
+def count_faults(makespan):
+    """Number of host makespans equal to MAKESPAN_FAULT (taccl_count_faults)."""
+    m = np.ascontiguousarray(makespan).view(np.uint32).reshape(-1)
+    out = ct.c_int64()
+    _check(lib().taccl_count_faults(int(m.size), _np_ptr(m), ct.byref(out)))
+    return int(out.value)
 
 
 class Plan:

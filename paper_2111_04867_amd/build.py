@@ -10,19 +10,33 @@ LIB = os.path.join(PKG, "libtaccl.so")
 ARCH = "gfx950"
 
 
-def build_library(verbose=False, jobs=8):
+def build_library(verbose=False, jobs=8, only_changed=False, sanitize=False):
+    """Compile every source (only_changed: skip sources whose object is newer
+    than the source and every header, for quick rebuilds while editing).
+    sanitize: host code under AddressSanitizer and UndefinedBehaviorSanitizer
+    (device code unchanged), into _build/san/libtaccl_san.so; the process
+    that loads it must preload clang's ASan runtime (tests/sanitize.py)."""
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.cpp")) + glob.glob(os.path.join(CSRC, "*.hip")))
-    objdir = os.path.join(PKG, "_build")
+    headers = glob.glob(os.path.join(CSRC, "*.h")) + glob.glob(os.path.join(ROOT, "include", "*.h"))
+    newest_header = max(os.path.getmtime(h) for h in headers)
+    objdir = os.path.join(PKG, "_build", "san") if sanitize else os.path.join(PKG, "_build")
     os.makedirs(objdir, exist_ok=True)
     common = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-I" + os.path.join(ROOT, "include"),
               "-I" + CSRC]
+    # host-only sanitizers: each -fsanitize= goes to the host pass alone
+    san = (["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+            "-Xarch_host", "-fno-omit-frame-pointer", "-Xarch_host", "-fno-sanitize-recover=all"]
+           if sanitize else [])
     procs, objs = [], []
     for s in srcs:
         o = os.path.join(objdir, os.path.basename(s) + ".o")
         objs.append(o)
+        if only_changed and os.path.exists(o) and \
+                os.path.getmtime(o) > max(os.path.getmtime(s), newest_header):
+            continue
         # hipcc compiles every source as HIP; keep packed fp32 ops out of
         # device code (the host pass warns that it does not know the feature)
-        cmd = ["hipcc", "--offload-arch=" + ARCH] + common
+        cmd = ["hipcc", "--offload-arch=" + ARCH] + common + san
         cmd += ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
         cmd += ["-c", s, "-o", o]
         if verbose:
@@ -33,8 +47,11 @@ def build_library(verbose=False, jobs=8):
     # the seeded input generator (plain C, shared with the tests)
     gen_o = os.path.join(objdir, "candgen.c.o")
     objs.append(gen_o)
-    procs.append(subprocess.Popen(["gcc", "-O3", "-std=c11", "-Wall", "-fPIC", "-fvisibility=hidden",
-                                   "-c", os.path.join(ROOT, "workloads", "candgen.c"), "-o", gen_o],
+    cc = (["/opt/rocm/llvm/bin/clang", "-fsanitize=address,undefined", "-fno-omit-frame-pointer",
+           "-fno-sanitize-recover=all"] if sanitize else ["gcc"])
+    procs.append(subprocess.Popen(cc + ["-O3", "-std=c11", "-Wall", "-fPIC", "-fvisibility=hidden",
+                                        "-c", os.path.join(ROOT, "workloads", "candgen.c"),
+                                        "-o", gen_o],
                                   stderr=subprocess.PIPE, text=True))
     failed = False
     for p in procs:
@@ -46,13 +63,16 @@ def build_library(verbose=False, jobs=8):
         failed |= p.returncode != 0
     if failed:
         raise RuntimeError("hipcc failed")
-    tmp = LIB + ".tmp"
-    cmd = ["hipcc", "--offload-arch=" + ARCH, "-shared", "-fPIC"] + objs + ["-o", tmp]
+    out = os.path.join(objdir, "libtaccl_san.so") if sanitize else LIB
+    tmp = out + ".tmp"
+    link_san = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                "-shared-libsan"] if sanitize else []
+    cmd = ["hipcc", "--offload-arch=" + ARCH, "-shared", "-fPIC"] + link_san + objs + ["-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":

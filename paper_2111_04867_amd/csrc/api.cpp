@@ -340,6 +340,16 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
   return TACCL_OK;
 }
 
+taccl_status_t taccl_count_faults(int64_t n, const uint32_t *makespan, int64_t *faults) {
+  if (!faults) return fail(TACCL_ERR_INVALID_ARGUMENT, "null output");
+  if (n < 0) return fail(TACCL_ERR_INVALID_ARGUMENT, "negative candidate count");
+  if (n > 0 && !makespan) return fail(TACCL_ERR_INVALID_ARGUMENT, "null makespan array");
+  int64_t k = 0;
+  for (int64_t i = 0; i < n; i++) k += makespan[i] == TACCL_MAKESPAN_FAULT;
+  *faults = k;
+  return TACCL_OK;
+}
+
 // the seeded input generator shared with the tests (workloads/candgen.c)
 extern "C" int candgen_fill(uint64_t seed, int64_t first, int64_t count, int route_stride,
                             const int32_t *options, int prio_stride, uint8_t *routes,

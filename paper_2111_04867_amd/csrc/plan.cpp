@@ -816,9 +816,12 @@ taccl_status_t taccl_sketch_apply(taccl_topology_t topo, taccl_collective_t coll
         return fail(TACCL_ERR_INVALID_ARGUMENT, "a routed link has no reverse link");
   st = build_layout(p);
   if (st) return st;
-  // every time is at most the sum of all send costs
-  if ((unsigned __int128)p->max_sends * max_cost >= ((unsigned __int128)1 << 32))
-    return fail(TACCL_ERR_LIMIT, "worst-case makespan does not fit 32 bits");
+  // every time is at most the sum of all send costs (both phases of an
+  // Allreduce); it must stay below 0xFFFFFFFF, the value the kernels write
+  // for a candidate whose evaluation exceeded an internal bound
+  const unsigned __int128 phases = coll->kind == TACCL_ALLREDUCE ? 2 : 1;
+  if ((unsigned __int128)p->max_sends * max_cost * phases >= (unsigned __int128)0xFFFFFFFFu)
+    return fail(TACCL_ERR_LIMIT, "worst-case makespan does not fit below 2^32 - 1");
   if (coll->kind == TACCL_ALLTOALL) {
     st = build_levels(p);
     if (st) return st;

@@ -157,15 +157,19 @@ def test_alltoall_block_kernel(make, n, order):
 
 @pytest.mark.parametrize("name", cf.GREEDY_LARGE_ORDER)
 def test_full_batch_sampled(name):
-    """The whole batch in the benchmark's launch shape; 24 sampled
-    candidates (first, last, spread) against the oracle."""
+    """The whole batch in the benchmark's launch shape; 256 sampled
+    candidates (first, last, and a seeded spread over the batch) against
+    the oracle, on every host thread."""
     w = cf.named(name)
     plan, ref, opts = plans(w)
     routes, prio = generate(w.seed, 0, w.n_candidates, opts, plan.prio_stride)
     say(f"[gpu] {name}: full batch N={w.n_candidates}")
     mk, ok = plan.eval(routes, prio)
     idx = np.unique(np.r_[0, w.n_candidates - 1,
-                          np.random.default_rng(3).choice(w.n_candidates, 22, replace=False)])
+                          np.random.default_rng(3).choice(np.arange(1, w.n_candidates - 1), 254,
+                                                          replace=False)])
+    assert idx.size == 256
+    say(f"[gpu] {name}: oracle on {idx.size} sampled candidates")
     rmk, rok = ref.eval_threads(routes[idx], prio[idx])
     assert (mk[idx] == rmk).all() and (ok[idx] == rok).all()
     assert ok.all()

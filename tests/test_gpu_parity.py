@@ -61,6 +61,8 @@ def test_full_size_parity(name):
     routes, prio = generate(w.seed, 0, w.n_candidates, opts, plan.prio_stride)
     mk, ok = check(plan, ref, routes, prio, f"{name} full N={w.n_candidates}")
     assert ok.all()
+    from paper_2111_04867_amd.binding import count_faults
+    assert count_faults(mk) == 0
     if name == "ring4_ag":
         assert (mk == 97870).all()
 

@@ -218,3 +218,21 @@ def test_generate_host_argument_checks():
     assert status_of(lambda: plan.generate(1, -1, 2)) == B.ERR_INVALID_ARGUMENT
     assert status_of(lambda: plan.generate(1, (1 << 32) - 1, 2)) == B.ERR_INVALID_ARGUMENT
     assert plan.generate(1, 0, 0)[0].shape == (0, plan.route_stride)
+
+
+def test_count_faults():
+    """The fault sentinel is counted on the host; LIMIT keeps every real
+    makespan below it, both phases of an Allreduce included."""
+    m = np.array([0, 5, B.MAKESPAN_FAULT, 0xFFFFFFFE, B.MAKESPAN_FAULT], dtype=np.uint32)
+    assert B.count_faults(m) == 2
+    assert B.count_faults(np.zeros(0, dtype=np.uint32)) == 0
+    out = ct.c_int64()
+    assert B.lib().taccl_count_faults(-1, None, ct.byref(out)) == B.ERR_INVALID_ARGUMENT
+    assert B.lib().taccl_count_faults(3, None, ct.byref(out)) == B.ERR_INVALID_ARGUMENT
+    # 12 sends of 2^28 ns fit one phase (3 * 2^30 < 2^32 - 1) but not two
+    w = cf.ring4_ag()
+    cost = np.full(w.E, 1 << 28, dtype=np.uint32)
+    beta = np.zeros(w.E, dtype=np.uint32)
+    B.Plan(w.V, w.P, w.row_ptr, w.col, cost, beta, None, cf.ALLGATHER, 1, 1 << 20)
+    assert status_of(lambda: B.Plan(w.V, w.P, w.row_ptr, w.col, cost, beta, None,
+                                    cf.ALLREDUCE, 1, 1 << 20)) == B.ERR_LIMIT

@@ -142,3 +142,40 @@ def test_two_switches_bruteforce():
         pairs = pairs_alltoall(w, table, r)
         assert all(int(node_of[x]) == int(node_of[y]) for x, y in pairs)
         assert got[i] == len(pairs)
+
+
+def switch_plus_directed_ring(P, kind, cpr=1):
+    """Ranks on one switch plus a ring that is cheap one way (r -> r+1) and
+    dear the other way (every link has its reverse, as reductions need): a
+    chunk reaches some ranks over the ring and others through the switch, so
+    the pairs of a candidate are not closed under reversal."""
+    edges = cf.switch_edges(range(P), P, 700, 8)
+    for r in range(P):
+        edges += [(r, (r + 1) % P, 300, 8), ((r + 1) % P, r, 3000, 8)]
+    row_ptr, col, a, b = cf.csr_from_edges(P + 1, edges)
+    return cf.Workload(f"swring{P}", P + 1, P, row_ptr, col, a, b, None, kind, cpr, 65536,
+                       cf.KSHORTEST, k=3)
+
+
+@pytest.mark.parametrize("P,cpr", [(4, 1), (5, 2), (7, 1)])
+def test_bruteforce_reductions_asymmetric(P, cpr):
+    """ReduceScatter counts the reverse of every Allgather pair and Allreduce
+    the union of both directions (App. B.3 is_util over the links each phase
+    uses); on a topology whose pairs are asymmetric the three counts differ,
+    so dropping either direction of the Allreduce union fails here."""
+    w = switch_plus_directed_ring(P, cf.ALLGATHER, cpr=cpr)
+    plan = OraclePlan.from_workload(w)
+    table = table_of(plan, w)
+    routes, _ = generate(120 + P, 0, 48, plan.route_options(), plan.prio_stride)
+    rs = OraclePlan.from_workload(cf.as_reduction(w, cf.REDUCESCATTER))
+    ar = OraclePlan.from_workload(cf.as_reduction(w, cf.ALLREDUCE))
+    g, grs, gar = plan.connections(routes), rs.connections(routes), ar.connections(routes)
+    asym = 0
+    for i, r in enumerate(routes):
+        pairs = pairs_multicast(w, table, r)
+        rev = {(b, a) for a, b in pairs}
+        assert g[i] == len(pairs)
+        assert grs[i] == len(rev)
+        assert gar[i] == len(pairs | rev)
+        asym += gar[i] > g[i]
+    assert asym > len(routes) // 2  # the union is larger than one direction

@@ -26,12 +26,26 @@ def build_candgen(verbose=False):
     return LIB
 
 
+def build_candgen_sanitized(out_dir, verbose=False):
+    """The generator under AddressSanitizer and UndefinedBehaviorSanitizer."""
+    os.makedirs(out_dir, exist_ok=True)
+    out = os.path.join(out_dir, "libcandgen_san.so")
+    cmd = ["/opt/rocm/llvm/bin/clang", "-O1", "-g", "-std=c11", "-Wall", "-Wextra", "-fPIC",
+           "-shared", "-fsanitize=address,undefined", "-fno-omit-frame-pointer",
+           "-fno-sanitize-recover=all", "-shared-libsan", SRC, "-o", out]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    return out
+
+
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB):
+        path = os.environ.get("TACCL_CANDGEN_LIB", LIB)
+        if path == LIB and not os.path.exists(LIB):
             build_candgen()
-        lib = ct.CDLL(LIB)
+        lib = ct.CDLL(path)
         lib.candgen_fill.restype = ct.c_int
         lib.candgen_fill.argtypes = [ct.c_uint64, ct.c_int64, ct.c_int64, ct.c_int, ct.c_void_p,
                                      ct.c_int, ct.c_void_p, ct.c_void_p]
