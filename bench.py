@@ -21,7 +21,14 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
+# int32 VALU issue: 256 CUs x 64 lanes x 2.4 GHz (published unit counts and
+# clock), in tera lane-operations per second
+INT_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
+MAX_ORACLE_THREADS = 16
 DEFAULT_WORKLOAD = "twonode16_ag"
+# the two workloads the roofline targets are set on: the two-node 2x8-rank
+# Allgather and the four-node 64-rank Alltoall
+TARGETS = ("twonode16_ag", "fournode64_a2a")
 
 
 # Kernel that dominates each workload's launch (the only kernel it runs).
@@ -120,21 +127,91 @@ def setup(name):
     return w, plan, routes, prio, (d_r, d_p, d_m, d_v)
 
 
-def cpu_baseline(w, routes, prio, budget_s):
-    """The oracle, single-threaded, on a bounded prefix of the same batch."""
-    from oracle import OraclePlan
-    ref = OraclePlan.from_workload(w)
-    n_done, t_used, step = 0, 0.0, 1
-    while n_done < w.n_candidates and t_used < budget_s:
-        n = min(step, w.n_candidates - n_done)
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def host_threads():
+    """(hardware threads this process may run on, threads the oracle uses):
+    the oracle takes every visible hardware thread, at most MAX_ORACLE_THREADS
+    (a GPU machine grants one GPU's share of the host's cores)."""
+    try:
+        visible = len(os.sched_getaffinity(0))
+    except AttributeError:
+        visible = os.cpu_count() or 1
+    return visible, max(1, min(visible, MAX_ORACLE_THREADS))
+
+
+def time_oracle(ref, routes, prio, threads, budget_s):
+    """Candidates/s of the oracle on a growing prefix of the batch: the prefix
+    doubles until the last pass alone took budget_s / 2 or the batch ends.
+    Returns (rate, candidates in the last pass, its seconds)."""
+    n = max(1, min(threads, routes.shape[0]))
+    while True:
         t = time.perf_counter()
-        ref.eval(routes[n_done:n_done + n], prio[n_done:n_done + n])
-        t_used += time.perf_counter() - t
-        n_done += n
-        step = min(step * 2, 4096)
-    return {"value": n_done / t_used, "unit": "candidates/s", "cores": 1, "kind": "oracle",
-            "sample": f"first {n_done} of {w.n_candidates} {w.name} candidates "
-                      f"({t_used:.1f} s, one thread)"}
+        if threads == 1:
+            ref.eval(routes[:n], prio[:n])
+        else:
+            ref.eval_threads(routes[:n], prio[:n], threads=threads)
+        dt = time.perf_counter() - t
+        if dt >= budget_s / 2 or n == routes.shape[0]:
+            return n / dt, n, dt
+        n = min(routes.shape[0], n * 2 if dt > 0.05 else n * 8)
+
+
+def oracle_ops(ref, routes, prio, n):
+    """Mean algorithmic operations per candidate over the first n candidates
+    (the oracle's exact count of the op model)."""
+    _, _, ops = ref.eval_ops(routes[:n], prio[:n])
+    return float(ops.mean()), n
+
+
+def cpu_baselines(names, setups, budget_s):
+    """The oracle on the host cores, on one thread and on every visible
+    thread, for each named workload: candidates/s, with the samples stated.
+    `setups` maps a name to its (workload, routes, prio)."""
+    from oracle import OraclePlan
+    visible, T = host_threads()
+    out = {}
+    for name in names:
+        w, routes, prio = setups[name]
+        ref = OraclePlan.from_workload(w)
+        r1, n1, t1 = time_oracle(ref, routes, prio, 1, budget_s)
+        rT, nT, tT = time_oracle(ref, routes, prio, T, budget_s)
+        ops, n_ops = oracle_ops(ref, routes, prio, min(n1, 64))
+        out[name] = {"one_thread": r1, "threads": T, "all_threads": rT,
+                     "sample_one_thread": f"first {n1} of {w.n_candidates} ({t1:.2f} s)",
+                     "sample_all_threads": f"first {nT} of {w.n_candidates} ({tT:.2f} s)",
+                     "ops_per_candidate": ops, "ops_sample": n_ops}
+        log(f"[bench] oracle {name}: {r1:.3e} cand/s on 1 thread, {rT:.3e} on {T}; "
+            f"{ops:.0f} ops/candidate")
+    return out, visible, T
+
+
+def roofline_pair(n_cand_per_s, bytes_per_cand, ops_per_cand):
+    """Both bounds for one workload: achieved HBM bandwidth over algorithmic
+    bytes, achieved integer issue over the oracle's op count, and the
+    governing (lower) roofline in candidates/s."""
+    hbm = n_cand_per_s * bytes_per_cand / 1e9
+    out = {"hbm_GBs": hbm, "hbm_frac": hbm / HBM_PEAK_GBS,
+           "hbm_roofline_candidates_per_s": HBM_PEAK_GBS * 1e9 / bytes_per_cand}
+    if ops_per_cand:
+        ti = n_cand_per_s * ops_per_cand / 1e12
+        out.update({"int_Tops": ti, "int_issue_frac": ti / INT_PEAK_TOPS,
+                    "int_roofline_candidates_per_s": INT_PEAK_TOPS * 1e12 / ops_per_cand})
+        gov = min(out["hbm_roofline_candidates_per_s"], out["int_roofline_candidates_per_s"])
+        out["governing"] = ("hbm" if gov == out["hbm_roofline_candidates_per_s"]
+                            else "int_issue")
+        out["governing_frac"] = n_cand_per_s / gov
+    return out
 
 
 def main():
@@ -143,7 +220,8 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=3.0,
+                    help="oracle time budget per workload and thread count")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-all", action="store_true", help="skip the per-workload table")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
@@ -202,6 +280,9 @@ def main():
                      "algorithmic_bytes_per_launch": bytes_launch,
                      "kernel": KERNEL_OF.get(w.name)},
     }
+    # host inputs of the five configurations, for the oracle leg
+    host = {w.name: (w, routes, prio)}
+    timed = {w.name: (value, plan.bytes_per_candidate, per.mean())}
     if not args.no_all:
         table = {}
         for name in (ORDER + CONTIG_ORDER + REDUCE_ORDER + GREEDY_ORDER + GREEDY_LARGE_ORDER +
@@ -209,14 +290,17 @@ def main():
             if name == args.workload:
                 wl, pl, pr_ = w, plan, per
             else:
-                wl, pl, _, _, b2 = setup(name)
+                wl, pl, r2, p2, b2 = setup(name)
                 pr_, _ = time_launches(pl, *b2, max(10, args.steps // 2), args.warmup)
                 del b2
+                if name in ORDER:
+                    host[name] = (wl, r2, p2)
             a_s = pr_.mean() / 1e3
             gbs = wl.n_candidates * pl.bytes_per_candidate / a_s / 1e9
             table[name] = {"candidates": wl.n_candidates, "ms_per_launch": pr_.mean(),
                            "candidates_per_s": wl.n_candidates / a_s, "achieved_GBs": gbs,
                            "hbm_roofline_frac": gbs / HBM_PEAK_GBS}
+            timed[name] = (wl.n_candidates / a_s, pl.bytes_per_candidate, pr_.mean())
             log(f"[bench] {name}: {table[name]['candidates_per_s']:.3e} cand/s, "
                 f"{gbs:.1f} GB/s ({100 * gbs / HBM_PEAK_GBS:.2f}% of HBM)")
         rec["all_workloads"] = table
@@ -234,7 +318,39 @@ def main():
             del b2
         rec["connections"] = conn
     if not args.no_cpu:
-        rec["cpu_baseline"] = cpu_baseline(w, routes, prio, args.cpu_seconds)
+        names = [nm for nm in ORDER if nm in host] or [w.name]
+        if w.name not in names:
+            names.append(w.name)
+        base, visible, T = cpu_baselines(names, host, args.cpu_seconds)
+        hb = base[w.name]
+        rec["cpu_baseline"] = {
+            "value": hb["all_threads"], "unit": "candidates/s", "cores": T, "kind": "oracle",
+            "sample": f"{hb['sample_all_threads']} {w.name} candidates on {T} threads "
+                      f"(contiguous ranges); one thread: {hb['sample_one_thread']}",
+            "one_thread_value": hb["one_thread"], "cpu_model": cpu_model(),
+            "hardware_threads_visible": visible, "per_config": base}
+        ops = hb["ops_per_candidate"]
+        ti = value * ops / 1e12
+        rec["roofline_int_issue"] = {
+            "bound": "int_issue", "achieved": ti, "peak": INT_PEAK_TOPS, "unit": "Tops/s",
+            "frac": ti / INT_PEAK_TOPS, "ops_per_candidate": ops,
+            "ops_sample": f"oracle op count over the first {hb['ops_sample']} candidates"}
+        targets = {}
+        for name in names:
+            if name not in timed:
+                continue
+            cps, bpc, ms = timed[name]
+            b = base[name]
+            r = {"candidates_per_s": cps, "ms_per_launch": ms,
+                 "bytes_per_candidate": bpc, "ops_per_candidate": b["ops_per_candidate"],
+                 "oracle_one_thread": b["one_thread"], "oracle_all_threads": b["all_threads"],
+                 "oracle_threads": b["threads"]}
+            r.update(roofline_pair(cps, bpc, b["ops_per_candidate"]))
+            targets[name] = r
+            if "all_workloads" in rec and name in rec["all_workloads"]:
+                rec["all_workloads"][name]["int_issue_frac"] = r.get("int_issue_frac")
+        rec["configs"] = targets
+        rec["targets"] = {nm: targets[nm] for nm in TARGETS if nm in targets}
     print(json.dumps(rec), flush=True)
 
 
