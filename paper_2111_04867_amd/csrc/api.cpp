@@ -52,7 +52,7 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
          o_lal = pk.add(p->lalpha), o_lbs = pk.add(p->lbs), o_lmg = pk.add(p->lmerge),
          o_lrev = pk.add(p->lrev), o_hc2 = pk.add(p->hop_class2),
          o_lcb2 = pk.add(p->lvl_cls2_begin), o_llc2 = pk.add(p->llc2),
-         o_gkr = pk.add(p->gkrank);
+         o_gkr = pk.add(p->gkrank), o_tent = pk.add(p->tent);
   void *blk = nullptr;
   e = hipMalloc(&blk, pk.bytes.size());
   if (e != hipSuccess) return fail(TACCL_ERR_NO_MEMORY, "hipMalloc of plan tables failed");
@@ -93,6 +93,7 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
   t.cinfo = (const uint32_t *)at(o_cinfo);
   t.cbkt = (const uint32_t *)at(o_cbkt);
   t.gkrank = (const uint32_t *)at(o_gkr);
+  t.tent = p->tent.empty() ? nullptr : (const uint8_t *)at(o_tent);
   t.max_lds = (int)prop.sharedMemPerBlock;
   t.lds_per_cu = (int)std::max<size_t>(prop.maxSharedMemoryPerMultiProcessor, prop.sharedMemPerBlock);
   t.num_cus = prop.multiProcessorCount;
@@ -317,6 +318,35 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
       if (!layered) return launch_tree(x, tgrid, s);
       return greedy ? launch_tree_greedy(x, tgrid, s) : launch_tree_layers(x, tgrid, s);
     };
+    // Trees run forwards with the static order and one chunk per transfer
+    // (Allgather, explicit, the Allgather phase of an Allreduce): the ranked
+    // kernel, when the plan's path lengths have exact short codes
+    TreeArgs ra = a;
+    const bool ranked = !p->contig && !greedy && a.routes_word_aligned && t->tent &&
+                        tree_rank_layout(*p, ra) > 0 && tree_block_bytes(ra, 1) <= t->max_lds;
+    ra.ent = t->tent;
+    auto launch_ranked = [&](TreeArgs &x) {
+      int best_w = 1, best_res = 0, best_bpc = 1;
+      for (int w = 1; w <= kRankMaxThreads / 64; w++) {
+        const int bytes = tree_block_bytes(x, w);
+        if (bytes > t->max_lds) break;
+        int bpc = std::min(t->lds_per_cu / bytes, 32 / w);
+        x.waves_per_block = w;
+        const int nb = tree_rank_blocks_per_cu(x);
+        if (nb > 0) bpc = std::min(bpc, nb);
+        const int res = std::min(bpc * w, 32);
+        if (res > best_res) {
+          best_res = res;
+          best_w = w;
+          best_bpc = bpc;
+        }
+      }
+      x.waves_per_block = best_w;
+      const int64_t want = (n + best_w - 1) / best_w;
+      const int tgrid =
+          (int)std::min<int64_t>(want, (int64_t)std::max(t->num_cus, 1) * best_bpc);
+      return launch_tree_rank(x, tgrid, s);
+    };
     if (kind == TACCL_ALLREDUCE) {
       // ReduceScatter on the first priority row, then Allgather on the
       // second, adding its makespan (same stream, so in order)
@@ -324,12 +354,16 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
       a.accumulate = 0;
       e = launch(a);
       if (e == hipSuccess) {
-        TreeArgs b = a;
+        TreeArgs b = ranked ? ra : a;
         b.reduce = 0;
         b.accumulate = 1;
         b.prio = d_prio + (size_t)p->coll.C * p->topo.V;
-        e = launch(b);
+        e = ranked ? launch_ranked(b) : launch(b);
       }
+    } else if (kind != TACCL_REDUCESCATTER && ranked) {
+      ra.reduce = 0;
+      ra.accumulate = 0;
+      e = launch_ranked(ra);
     } else {
       a.reduce = kind == TACCL_REDUCESCATTER;
       a.accumulate = 0;

@@ -60,6 +60,13 @@ struct TreeArgs {
   // general variant (any != 0): time-aware greedy instead of the static
   // order, and the per-link state of open contiguous transfers
   int32_t any, greedy, w_gst;
+  // ranked variant: exact order-preserving codes of path lengths
+  // (code = (x * qmagic) >> 32 < qrange), the entering-link table and the
+  // per-slot heights
+  uint64_t qmagic;
+  int32_t qrange;
+  const uint8_t *ent;
+  int32_t o_ent, w_h, o_slot, opt_ostride;
 };
 
 // Alltoall evaluation: one block per candidate, level by level.
@@ -148,6 +155,7 @@ struct ConnArgs {
 constexpr int kConnMaxThreads = 256;
 
 constexpr int kTreeMaxThreads = 512;  // up to 8 wavefronts per block
+constexpr int kRankMaxThreads = 768;  // ranked multicast kernel: up to 12
 constexpr int kTreeRecLdsMax = 32768;  // route records kept in LDS up to this size
 constexpr int kPathThreads = 256;
 constexpr int kPathPortThreads = 1024;  // LDS-record kernel on switch-port plans
@@ -159,6 +167,12 @@ int32_t tree_layout(const taccl_plan &p, TreeArgs &a);
 // greedy orders on plans outside the layered kernel's limits).
 int32_t tree_any_layout(const taccl_plan &p, TreeArgs &a);
 int32_t tree_block_bytes(const TreeArgs &a, int waves);
+// Ranked multicast kernel (static orders, no contiguity, trees forwards):
+// fills the layout and returns the bytes of a one-wavefront block, or 0
+// when the plan does not meet its conditions.
+int32_t tree_rank_layout(const taccl_plan &p, TreeArgs &a);
+int tree_rank_blocks_per_cu(const TreeArgs &a);
+hipError_t launch_tree_rank(const TreeArgs &a, int grid, hipStream_t stream);
 // Layered multicast kernel: fills the layout and returns the bytes of a
 // one-wavefront block, or 0 when the plan does not meet its conditions.
 int32_t tree_layers_layout(const taccl_plan &p, TreeArgs &a);

@@ -537,6 +537,47 @@ static taccl_status_t build_levels(taccl_plan *p) {
   return TACCL_OK;
 }
 
+// Codes for the remaining and travelled lengths of multicast sends. Each is
+// the cost of a path of a chunk's tree (at most V - 1 links, every one a
+// hop of some route option), so it lies in S, the set of sums of at most
+// V - 1 costs of such links. With g the smallest gap between two elements
+// of S and m = ceil(2^32 / g), x -> floor(x * m / 2^32) is nondecreasing
+// everywhere and gains at least 1 per step of S (g * m >= 2^32), so it
+// orders and separates S exactly. Left at range 0 when S exceeds 16384
+// elements or the codes need more than 11 bits.
+static void path_sum_codes(taccl_plan *p) {
+  p->pq_magic = 0;
+  p->pq_range = 0;
+  std::vector<uint64_t> costs;
+  for (uint16_t l : p->path_links) costs.push_back(p->cost[l]);
+  std::sort(costs.begin(), costs.end());
+  costs.erase(std::unique(costs.begin(), costs.end()), costs.end());
+  if (costs.empty() || costs[0] == 0) return;
+  std::vector<uint64_t> S{0}, next;
+  for (int32_t step = 0; step < p->topo.V - 1; step++) {
+    next = S;
+    for (uint64_t s : S)
+      for (uint64_t c : costs) next.push_back(s + c);
+    std::sort(next.begin(), next.end());
+    next.erase(std::unique(next.begin(), next.end()), next.end());
+    if (next.size() > 16384) return;
+    if (next.size() == S.size()) break;  // closed: no longer sums appear
+    S.swap(next);
+  }
+  if (S.back() >= (1ull << 32)) return;
+  uint64_t gap = ~0ull;
+  for (size_t i = 1; i < S.size(); i++) gap = std::min(gap, S[i] - S[i - 1]);
+  if (S.size() == 1) gap = S[0] ? S[0] : 1;
+  const uint64_t m = ((1ull << 32) + gap - 1) / gap;  // <= 2^32
+  auto code = [&](uint64_t x) { return (x * m) >> 32; };
+  for (size_t i = 1; i < S.size(); i++)
+    if (code(S[i]) <= code(S[i - 1])) return;  // cannot happen (see above)
+  const uint64_t range = code(S.back()) + 1;
+  if (range > 2048) return;
+  p->pq_magic = m;
+  p->pq_range = (int32_t)range;
+}
+
 static taccl_status_t build_layout(taccl_plan *p) {
   const taccl_topology &t = p->topo;
   const taccl_collective &c = p->coll;
@@ -600,6 +641,25 @@ static taccl_status_t build_layout(taccl_plan *p) {
       for (size_t r = 0; r < (size_t)P * P * K; r++)
         for (int32_t j = 0; j < H; j++) p->tree_rec4[r * 4 + j] = p->tree_rec[r * H + j];
     }
+    p->tent.clear();
+    if (t.E <= 255) {
+      p->tent.assign((size_t)P * V * P * K, 0xFF);
+      for (int32_t o = 0; o < P; o++)
+        for (int32_t d = 0; d < P; d++) {
+          const int32_t pp = o * P + d;
+          for (int32_t k = 0; k < p->npaths[pp]; k++) {
+            const uint32_t q = p->pair_base[pp] + k;
+            // a relay route may enter a vertex twice (a switch on both
+            // legs); the first-reach merge takes the first entry
+            for (uint32_t j = p->path_off[q]; j < p->path_off[q + 1]; j++) {
+              const uint16_t l = p->path_links[j];
+              uint8_t &slot = p->tent[(((size_t)o * V + p->ldst[l]) * P + d) * K + k];
+              if (slot == 0xFF) slot = (uint8_t)l;
+            }
+          }
+        }
+    }
+    path_sum_codes(p);
     p->topt.clear();
     if (K <= 8) {
       p->topt.assign((size_t)P * V * P, 0);

@@ -53,6 +53,7 @@ struct DeviceTables {
   const uint8_t *owner8 = nullptr;
   const uint8_t *topt = nullptr;
   const uint32_t *tree_rec4 = nullptr;
+  const uint8_t *tent = nullptr;
   const uint32_t *lalpha = nullptr;
   const uint64_t *lbs = nullptr;
   const uint8_t *lmerge = nullptr;
@@ -115,6 +116,17 @@ struct taccl_plan {
   // the route records again with 4 words per option (zero padded), for
   // plans with at most 4 hops
   std::vector<uint32_t> tree_rec4;
+  // [((o*V + v)*P + d)*max_paths + k]: the link by which option k of pair
+  // (o, d) enters vertex v (0xFF where it does not pass v); empty unless
+  // every link id fits 8 bits
+  std::vector<uint8_t> tent;
+  // Exact order-preserving compression of tree-path lengths: every
+  // remaining or travelled length of a multicast send is a sum of at most
+  // V - 1 link costs, and x -> (x * pq_magic) >> 32 is strictly increasing
+  // on the set of such sums, with values below pq_range (0: the set is too
+  // large or too dense for 11-bit codes)
+  uint64_t pq_magic = 0;
+  int32_t pq_range = 0;
 
   // Alltoall (path) evaluation: levels of equal remaining cost
   int32_t nlev = 0, ncls = 0, max_lvl_cls = 0, max_lvl_sends = 0;
