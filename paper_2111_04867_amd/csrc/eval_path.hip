@@ -590,6 +590,8 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
   // sorted sends, chunk | link << cb | index in its link run << (cb + lb),
   // stored transposed: position t*ept + q of thread t's range at q*NT + t
   uint32_t *pinfo = (uint32_t *)(lds + a.o_fsrt);
+  // per bucket-sorted position: its bucket | its class << 16
+  uint32_t *aux = (uint32_t *)(lds + a.o_faux);
   const uint32_t cb = a.cbits, lb = a.lbits, kb = cb + lb;
   const uint32_t cmask = (1u << cb) - 1, lmask = (1u << lb) - 1;
   uint32_t *red = (uint32_t *)(lds + a.o_fred);      // [2][NT/64] scan scratch
@@ -705,7 +707,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       // Straight-line code (selects, and a per-lane dummy counter past the
       // level's buckets for a slot without a send) so that the LDS loads and
       // counter updates of all slots are in flight together.
-      uint32_t wa[CPT], wb[CPT], pl[CPT];
+      uint32_t wa[CPT], wb[CPT], pl[CPT], cls[CPT];
 #pragma unroll
       for (int j = 0; j < CPT; j++) {
         const uint32_t h = (hmap[j] >> (3 * L)) & 7;  // 7: no hop at this level
@@ -716,8 +718,8 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
           if (h == (uint32_t)t) pv = pr[j][t];
         if (h >= 2) cw = rcl[j][1];
         if (h >= 4) cw = rcl[j][2];
-        const uint32_t cls = act ? ((h & 1) ? (cw >> 16) : (cw & 0xFFFF)) : lo;
-        const uint32_t cbk = s_cbkt[cls], ci = s_cinfo[cls];
+        cls[j] = act ? ((h & 1) ? (cw >> 16) : (cw & 0xFFFF)) : lo;
+        const uint32_t cbk = s_cbkt[cls[j]], ci = s_cinfo[cls[j]];
         const uint32_t bits = cbk >> 24;
         const uint32_t b = (cbk & 0xFFFFFF) + (bits ? (pv >> (32 - bits)) : 0u);
         const uint32_t slot = atomicAdd(&bcnt[act ? b : (uint32_t)NB + 1 + lane], 1u);
@@ -741,44 +743,28 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
           pos[j] = bcnt[wa[j] != kUnset ? wa[j] & 0xFFFFu : 0u] + (wb[j] & 0xFFFFu);
 #pragma unroll
         for (int j = 0; j < CPT; j++)
-          if (wa[j] != kUnset) e64[pos[j]] = ((uint64_t)pl[j] << 32) | (uint32_t)(tid + NT * j);
+          if (wa[j] != kUnset) {
+            e64[pos[j]] = ((uint64_t)pl[j] << 32) | (uint32_t)(tid + NT * j);
+            aux[pos[j]] = (wa[j] & 0xFFFFu) | (cls[j] << 16);
+          }
       }
       __syncthreads();
       // ---- D. order inside buckets by (priority, chunk); record each send's
-      //      link and its index in the link's run -----------------------------
-      {
-        uint32_t b0[CPT], nb[CPT], rs[CPT], rank[CPT];
-        uint64_t me[CPT];
-        uint32_t nmax = 0;
-#pragma unroll
-        for (int j = 0; j < CPT; j++) {
-          const bool act = wa[j] != kUnset;
-          const uint32_t b = act ? wa[j] & 0xFFFFu : 0u;
-          b0[j] = bcnt[b];
-          const uint32_t b1 = bcnt[b + 1];
-          rs[j] = bcnt[act ? wa[j] >> 16 : 0u];
-          nb[j] = act ? b1 - b0[j] : 0u;
-          rank[j] = 0;
-          me[j] = ((uint64_t)pl[j] << 32) | (uint32_t)(tid + NT * j);
-          nmax = max(nmax, nb[j]);
-        }
-        // the members of all this thread's buckets are read together, one
-        // from each bucket per step (entry 0 stands in for a finished bucket)
-        for (uint32_t t = 0; t < nmax; t++) {
-          uint64_t e[CPT];
-#pragma unroll
-          for (int j = 0; j < CPT; j++) e[j] = e64[t < nb[j] ? b0[j] + t : 0u];
-#pragma unroll
-          for (int j = 0; j < CPT; j++) rank[j] += (uint32_t)((t < nb[j]) & (e[j] < me[j]));
-        }
-#pragma unroll
-        for (int j = 0; j < CPT; j++)
-          if (wa[j] != kUnset) {
-            const uint32_t pos = b0[j] + rank[j];
-            const uint32_t t = (uint32_t)(((uint64_t)pos * em) >> 32), q = pos - t * ept;
-            pinfo[q * NT + t] = (uint32_t)(tid + NT * j) | ((wb[j] >> 16) << cb) |
-                                ((pos - rs[j]) << kb);
-          }
+      //      link and its index in the link's run -------------------------
+      // One lane per bucket-sorted position: neighbouring lanes hold
+      // neighbouring buckets, so their members are read with few bank
+      // conflicts, and a pass waits only for the largest bucket among its
+      // 64 positions.
+      for (uint32_t x = (uint32_t)tid; x < tot; x += NT) {
+        const uint64_t me = e64[x];
+        const uint32_t ax = aux[x];
+        const uint32_t b = ax & 0xFFFFu, ci = s_cinfo[ax >> 16];
+        const uint32_t b0 = bcnt[b], b1 = bcnt[b + 1], rs = bcnt[ci >> 16];
+        uint32_t rank = 0;
+        for (uint32_t y = b0; y < b1; y++) rank += (uint32_t)(e64[y] < me);
+        const uint32_t pos = b0 + rank;
+        const uint32_t t = (uint32_t)(((uint64_t)pos * em) >> 32), q = pos - t * ept;
+        pinfo[q * NT + t] = (uint32_t)me | ((ci & 0xFFFFu) << cb) | ((pos - rs) << kb);
       }
       __syncthreads();
       // ---- E. finish times of every link run --------------------------------
@@ -917,6 +903,7 @@ int32_t path_fast_layout(const taccl_plan &p, PathArgs &a) {
   // wavefront (slots without a send count there)
   a.o_fbcnt = take(4 * (p.max_lvl_nb + 1 + 64));
   a.o_fepr = take(8 * M);
+  a.o_faux = take(4 * M);
   a.o_fsrt = take(4 * path_fast_threads(p) * path_fast_cpt(p));
   // packed sorted sends: chunk, link and run index in one word
   auto bits = [](uint32_t n) {  // bits to hold 0 .. n-1

@@ -90,6 +90,7 @@ struct PathArgs {
   // register-resident kernel
   int32_t ncls;
   const uint32_t *arec, *cpath, *cinfo, *cbkt;
+  int32_t o_faux;
   int32_t o_fcost, o_fcinfo, o_fcbkt, o_flcb, o_fctime, o_flfree, o_fbcnt, o_fepr, o_fsrt, o_fred,
       o_fred64, o_fredf;
   int32_t lds_bytes;
