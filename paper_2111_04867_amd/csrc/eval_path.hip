@@ -544,7 +544,6 @@ hipError_t launch_path(const PathArgs &a, int grid, hipStream_t stream) {
 namespace taccl {
 namespace {
 
-constexpr uint64_t kBias = 1ull << 32;      // keeps r - k c non-negative
 constexpr uint32_t kUnset = 0xFFFFFFFFu;
 
 // exclusive scan of cnt[0..n) in place, cnt[n] = total (all threads call)
@@ -595,7 +594,6 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
   const uint32_t cb = a.cbits, lb = a.lbits, kb = cb + lb;
   const uint32_t cmask = (1u << cb) - 1, lmask = (1u << lb) - 1;
   uint32_t *red = (uint32_t *)(lds + a.o_fred);      // [2][NT/64] scan scratch
-  uint64_t *red64 = (uint64_t *)(lds + a.o_fred64);  // [NT/64] segmented max
   uint8_t *s_merge = lds + a.o_fmerge;  // links that carry contiguous transfers
   for (int j = tid; j < E; j += NT) {
     s_cost[j] = a.cost[j];
@@ -769,13 +767,12 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       __syncthreads();
       // ---- E. finish times of every link run --------------------------------
       // The k-th send of a link run with cost c, ready times r_j and busy
-      // time F finishes at (k+1)c + max(F, max_{j<=k}(r_j - j c)). Runs lie
-      // in ascending link order along the sorted positions (classes are
-      // ordered by link), so one plain prefix max over
-      // link << 33 | (r_j - j c + 2^32) yields, at every position, the max
-      // over the earlier sends of its own run. Thread tid owns sorted
-      // positions [tid*ept, tid*ept + ept); every load is issued unmasked
-      // (stale entries are clamped to in-range indexes and never used).
+      // time F finishes at (k+1)c + max_{j<=k} a_j with a_0 = max(r_0, F)
+      // and a_j = max(r_j - j c, 0) after it (F >= 0 dominates the clipped
+      // values): a prefix maximum segmented by runs, which are contiguous
+      // along the sorted positions. Thread tid owns sorted positions
+      // [tid*ept, tid*ept + ept); every load is issued unmasked (stale
+      // entries are clamped to in-range indexes and never used).
       const uint32_t x0 = (uint32_t)tid * ept;
       uint32_t pis[CPT], ct[CPT], cs[CPT], lf[CPT];
 #pragma unroll
@@ -787,30 +784,69 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
         cs[q] = s_cost[l];
         lf[q] = lfree[l];
       }
-      uint64_t comp[CPT];
-      uint64_t agg = 0;
+      // this thread's positions: segmented running maxima s[q]
+      const uint32_t nv = tot > x0 ? min(ept, tot - x0) : 0u;  // valid positions
+      uint32_t sv[CPT];
+      uint32_t prev = 0;
 #pragma unroll
       for (int q = 0; q < CPT; q++) {
-        comp[q] = 0;
-        if ((uint32_t)q < ept && x0 + q < tot) {
-          const uint32_t k = pis[q] >> kb, l = (pis[q] >> cb) & lmask;
-          comp[q] = ((uint64_t)l << 33) | ((uint64_t)ct[q] + kBias - (uint64_t)k * cs[q]);
-          agg = max(agg, comp[q]);
-        }
+        const uint32_t k = pis[q] >> kb, kc = k * cs[q];
+        const uint32_t av = k == 0 ? max(ct[q], lf[q]) : (ct[q] > kc ? ct[q] - kc : 0u);
+        sv[q] = (k > 0 && q > 0) ? max(prev, av) : av;
+        prev = sv[q];
       }
-      // exclusive prefix across threads: lanes (DPP), then waves
-      const uint64_t incl = wave_scan_max64(agg);
-      if (lane == 63) red64[wave] = incl;
-      __syncthreads();
-      uint64_t carry = dpp64<kWaveShr1>(incl);
+      // the run of the thread's last position: its running maximum, and
+      // whether it began before the thread's first position (then the
+      // maximum of earlier threads of the same run joins in); a thread
+      // without positions passes its predecessors' value on
+      const uint32_t kl = nv ? (pis[nv - 1 < CPT ? nv - 1 : 0] >> kb) : 0u;
+      uint32_t gv = 0, pass = nv == 0 ? 1u : (kl >= nv ? 1u : 0u);
+#pragma unroll
+      for (int q = 0; q < CPT; q++)
+        if ((uint32_t)q + 1 == nv) gv = sv[q];
+      // inclusive scan of (value, pass) pairs over the lanes: a lane that
+      // passes takes the maximum of the lanes before it, up to and
+      // including the first one that does not pass
       {
-        const uint64_t wv = row_scan_max64(lane < NT / 64 ? red64[lane] : 0ull);
+#define TACCL_SEG_STEP(CTRL, RM)                                                         \
+  {                                                                                     \
+    const uint32_t ov = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)gv, CTRL, RM, 0xf, false); \
+    const uint32_t op = (uint32_t)__builtin_amdgcn_update_dpp(1, (int)pass, CTRL, RM, 0xf, false); \
+    if (pass) {                                                                         \
+      gv = max(gv, ov);                                                                 \
+      pass = op;                                                                        \
+    }                                                                                   \
+  }
+        TACCL_SEG_STEP(kRowShr + 1, 0xf)
+        TACCL_SEG_STEP(kRowShr + 2, 0xf)
+        TACCL_SEG_STEP(kRowShr + 4, 0xf)
+        TACCL_SEG_STEP(kRowShr + 8, 0xf)
+        TACCL_SEG_STEP(kBcast15, 0xa)
+        TACCL_SEG_STEP(kBcast31, 0xc)
+#undef TACCL_SEG_STEP
+      }
+      // across wavefronts: every wavefront combines the totals of the ones
+      // before it (value, pass of lane 63)
+      if (lane == 63) {
+        red[wave] = gv;
+        red[NT / 64 + wave] = pass;
+      }
+      __syncthreads();
+      uint32_t cin = 0;  // segmented maximum of the positions before x0
+      {
+        // exclusive within the wavefront: the lane before (wave_shr:1 gives
+        // lane 0 nothing: value 0, pass 1)
+        uint32_t ev = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)gv, kWaveShr1, 0xf, 0xf, false);
+        uint32_t ep = (uint32_t)__builtin_amdgcn_update_dpp(1, (int)pass, kWaveShr1, 0xf, 0xf, false);
         const uint32_t w = (uint32_t)__builtin_amdgcn_readfirstlane(wave);
-        if (w) carry = max(carry, readlane64(wv, w - 1));
+        for (int v = (int)w - 1; v >= 0 && ep; v--) {
+          ev = max(ev, red[v]);
+          ep = red[NT / 64 + v];
+        }
+        cin = ev;
       }
       // finish times
       const uint32_t nxt0 = (tid + 1 < NT) ? pinfo[tid + 1] : 0u;  // next thread's first
-      uint64_t run = carry;
 #pragma unroll
       for (int q = 0; q < CPT; q++) {
         const uint32_t x = x0 + q;
@@ -853,10 +889,9 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
             continue;
           }
           const uint32_t cl = cs[q];
-          run = max(run, comp[q]);  // the run's own link: earlier links compare lower
-          const int64_t g = (int64_t)(run & ((1ull << 33) - 1));
-          const int64_t best = max((int64_t)lf[q], g - (int64_t)kBias);
-          const uint32_t f = (uint32_t)((int64_t)(k + 1) * cl + best);
+          // the run began before this thread's first position: k > q
+          const uint32_t best = k > (uint32_t)q ? max(sv[q], cin) : sv[q];
+          const uint32_t f = (k + 1) * cl + best;
           ctime[c] = f;
           mk = max(mk, f);
           const uint32_t nk = ((uint32_t)q + 1 < ept ? pis[q < CPT - 1 ? q + 1 : q] : nxt0) >> kb;
