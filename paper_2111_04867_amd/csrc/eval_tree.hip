@@ -33,6 +33,7 @@
 //   6. postcondition (ballot over chunks) and makespan (wave max).
 #include <hip/hip_runtime.h>
 
+#include "greedy_window.h"
 #include "kernels.h"
 #include "wave.h"
 
@@ -1255,74 +1256,52 @@ constexpr int kGreedyLinkSlots = 4;  // links per lane: at most 256 links
 // c_min (the smallest link cost) after W, so on every link the best ready
 // send by (start, Step-2 key, priority, slot) with start < W + c_min is the
 // greedy's next send there, and all of them are committed at once. One
-// lane holds up to four links; committed sends are swap-removed. Records:
-// {key lo, key hi (~rem << 32 | trav), priority, slot | other slot << 16},
-// the other slot being the send the chunk arrives by (its finish is the
-// ready time; kNoPred: ready at 0) or, for ReduceScatter, the send that
-// carries the partial on (ready once every input is scheduled). gfin[slot]
-// must be kNotYet for every pending send. On return every link's list holds
-// its sends in the reverse of the order they were served in. The Alltoall kernel calls it out of
-// line; the multicast kernel carries the same loop inline (inlining this
-// function into either kernel gave results that failed the parity tests,
-// while the out-of-line call and the kernel's own inline loop pass them).
+// lane holds up to four links; a committed send is swapped to the end of
+// its link's pending part. Records: {key lo, key hi (~rem << 32 | trav),
+// priority, slot | other slot << 16}, the other slot being the send the
+// chunk arrives by (its finish is the ready time; kNoPred: ready at 0) or,
+// for ReduceScatter, the send that carries the partial on (ready once every
+// input is scheduled). gfin[slot] must be kNotYet for every pending send.
+// On return every link's list holds its sends in the reverse of the order
+// they were served in. Both record-based greedy kernels use this one loop.
+//
+// The best send of a link is kept as three packed words compared
+// lexicographically, (start, key hi), (key lo, priority), (slot, list
+// index), and replaced as a whole, so the list index always belongs to the
+// send that won; the commit checks the slot at that index and reports a
+// fault if it ever differs. The scan of one link and the commit of its
+// winner are plain functions of one lane's data (greedy_window.h), which a
+// host build also runs.
+// Several lanes of a window may push into the same send's ready time.
+struct LdsAtomics {
+  __device__ static void max_into(uint32_t *p, uint32_t v) { atomicMax(p, v); }
+  __device__ static void decrement(uint32_t *p) { atomicSub(p, 1u); }
+};
+
 template <bool kRS>
-__device__ __noinline__ void greedy_windows(int E, int lane, int nslots, uint32_t cmin,
-                                               const uint32_t *s_cost, uint4 *grec,
-                                               const uint32_t *gofs, uint32_t *gfin,
-                                               uint32_t *grdy, uint32_t *gpend, uint32_t &mk,
-                                               bool &fault) {
-  uint32_t lf[kGreedyLinkSlots], lb[kGreedyLinkSlots], ln[kGreedyLinkSlots];
+__device__ __forceinline__ void greedy_windows(int E, int lane, int nslots, uint32_t cmin,
+                                            const uint32_t *s_cost, uint4 *grec,
+                                            const uint32_t *gofs, uint32_t *gfin,
+                                            uint32_t *grdy, uint32_t *gpend, uint32_t &mk,
+                                            bool &fault) {
+  GreedyLink lk[kGreedyLinkSlots];
 #pragma unroll
   for (int t = 0; t < kGreedyLinkSlots; t++) {
     const int l = lane + 64 * t;
-    lf[t] = 0;
-    lb[t] = l < E ? gofs[l] : 0;
-    ln[t] = l < E ? gofs[l + 1] - gofs[l] : 0;
+    lk[t].free = 0;
+    lk[t].base = l < E ? gofs[l] : 0;
+    lk[t].len = l < E ? gofs[l + 1] - gofs[l] : 0;
   }
   for (int round = 0;; round++) {
-    uint32_t cs[kGreedyLinkSlots], cq[kGreedyLinkSlots];
-    uint32_t wmin = kNotYet;
+    GreedyBest best[kGreedyLinkSlots];
+    uint32_t wmin = kGreedyNone;
 #pragma unroll
     for (int t = 0; t < kGreedyLinkSlots; t++) {
-      cs[t] = kNotYet;
-      cq[t] = 0;
-      uint64_t bk = ~0ull;
-      uint64_t bq = ~0ull;
-      // two pending sends per step: their records, then their ready times
-      for (uint32_t q0 = 0; q0 < ln[t]; q0 += 2) {
-        uint4 rc[2];
-        uint32_t r[2];
-#pragma unroll
-        for (int u = 0; u < 2; u++) rc[u] = grec[lb[t] + min(q0 + u, ln[t] - 1)];
-#pragma unroll
-        for (int u = 0; u < 2; u++) {
-          const uint32_t x = rc[u].w & 0xFFFFu, other = rc[u].w >> 16;
-          if (kRS) {
-            const uint32_t pend = gpend[x], rd = grdy[x];
-            r[u] = pend == 0 ? rd : kNotYet;
-          } else {
-            const uint32_t fo = gfin[other == kNoPred ? 0u : other];
-            r[u] = other == kNoPred ? 0u : fo;
-          }
-        }
-#pragma unroll
-        for (int u = 0; u < 2; u++) {
-          if (q0 + u >= ln[t] || r[u] == kNotYet) continue;  // its chunk has not arrived yet
-          const uint32_t st = max(lf[t], r[u]);
-          const uint64_t kx = ((uint64_t)rc[u].y << 32) | rc[u].x;
-          const uint64_t qx = ((uint64_t)rc[u].z << 32) | (rc[u].w & 0xFFFFu);  // priority, then chunk
-          if (st < cs[t] || (st == cs[t] && (kx < bk || (kx == bk && qx < bq)))) {
-            cs[t] = st;
-            cq[t] = q0 + u;
-            bk = kx;
-            bq = qx;
-          }
-        }
-      }
-      wmin = min(wmin, cs[t]);
+      best[t] = greedy_scan_link<kRS>(lk[t], grec, gfin, grdy, gpend);
+      wmin = min(wmin, greedy_start(best[t]));
     }
     wmin = ~wave_reduce_max(~wmin);
-    if (wmin == kNotYet) break;  // nothing left to schedule
+    if (wmin == kGreedyNone) break;  // nothing left to schedule
     if (round > nslots) {  // unreachable: every window commits a send
       fault = true;
       break;
@@ -1331,43 +1310,15 @@ __device__ __noinline__ void greedy_windows(int E, int lane, int nslots, uint32_
     wave_sync();
 #pragma unroll
     for (int t = 0; t < kGreedyLinkSlots; t++) {
-      if (cs[t] != kNotYet && (uint64_t)cs[t] < wend) {
-        const int l = lane + 64 * t;
-        const uint4 rc = grec[lb[t] + cq[t]];
-        const uint32_t x = rc.w & 0xFFFFu;
-        const uint32_t f = cs[t] + s_cost[l];
-        if (kRS) {
-          const uint32_t nxt = rc.w >> 16;
-          if (nxt != kNoPred) {
-            atomicMax(&grdy[nxt], f);
-            atomicSub(&gpend[nxt], 1u);
-          }
-        }
-        gfin[x] = f;
-        lf[t] = f;
-        mk = max(mk, f);
-        // swap with the last pending record: the served ones collect at the
-        // end of the link's list, latest first
-        grec[lb[t] + cq[t]] = grec[lb[t] + ln[t] - 1];
-        grec[lb[t] + ln[t] - 1] = rc;
-        ln[t]--;
-      }
+      const int l = lane + 64 * t;
+      if (greedy_start(best[t]) != kGreedyNone && (uint64_t)greedy_start(best[t]) < wend)
+        fault |= greedy_commit<kRS, LdsAtomics>(lk[t], best[t], s_cost[l], grec, gfin, grdy, gpend,
+                                                mk);
     }
     wave_sync();
   }
-
 }
 
-// Time-aware greedy orders (App. B.2) for Alltoall: the sends of a chunk
-// are the hops of its routed path, each ready when the hop before it ends
-// (the first at 0). One wavefront per candidate: the sends are counted per
-// link, laid out as per-link lists of packed records (key from the path's
-// remaining and travelled costs, priority of slot c*H + h), and the greedy
-// runs window by window as for the multicast trees. In reverse path order
-// (a.mirror) the greedy runs on the mirrored schedule: a hop waits for the
-// hop after it, the Step-2 lengths are measured from the path's end, and
-// the lists it leaves (served order reversed) are the real link orders,
-// which links then advance through in rounds to give the real times.
 __global__ __launch_bounds__(kTreeMaxThreads) void path_greedy_kernel(PathGreedyArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int C = a.C, P = a.P, E = a.E, H = a.H;
@@ -1650,88 +1601,8 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_greedy_kernel(TreeArgs a
     wave_sync();
 
     // ---- the greedy, window by window ------------------------------------
-    uint32_t lf[kGreedyLinkSlots], lb[kGreedyLinkSlots], ln[kGreedyLinkSlots];
-#pragma unroll
-    for (int t = 0; t < kGreedyLinkSlots; t++) {
-      const int l = lane + 64 * t;
-      lf[t] = 0;
-      lb[t] = l < E ? gofs[l] : 0;
-      ln[t] = l < E ? gofs[l + 1] - gofs[l] : 0;
-    }
     uint32_t mk = 0;
-    for (int round = 0;; round++) {
-      uint32_t cs[kGreedyLinkSlots], cq[kGreedyLinkSlots];
-      uint32_t wmin = kNotYet;
-#pragma unroll
-      for (int t = 0; t < kGreedyLinkSlots; t++) {
-        cs[t] = kNotYet;
-        cq[t] = 0;
-        uint64_t bk = ~0ull;
-        uint64_t bq = ~0ull;
-        // two pending sends per step: their records, then their ready times
-        for (uint32_t q0 = 0; q0 < ln[t]; q0 += 2) {
-          uint4 rc[2];
-          uint32_t r[2];
-#pragma unroll
-          for (int u = 0; u < 2; u++) rc[u] = grec[lb[t] + min(q0 + u, ln[t] - 1)];
-#pragma unroll
-          for (int u = 0; u < 2; u++) {
-            const uint32_t x = rc[u].w & 0xFFFFu, other = rc[u].w >> 16;
-            if (kRS) {
-              const uint32_t pend = gpend[x], rd = grdy[x];
-              r[u] = pend == 0 ? rd : kNotYet;
-            } else {
-              const uint32_t fo = gfin[other == kNoPred ? 0u : other];
-              r[u] = other == kNoPred ? 0u : fo;
-            }
-          }
-#pragma unroll
-          for (int u = 0; u < 2; u++) {
-            if (q0 + u >= ln[t] || r[u] == kNotYet) continue;  // its chunk has not arrived yet
-            const uint32_t st = max(lf[t], r[u]);
-            const uint64_t kx = ((uint64_t)rc[u].y << 32) | rc[u].x;
-            const uint64_t qx = ((uint64_t)rc[u].z << 32) | (rc[u].w & 0xFFFFu);  // priority, then chunk
-            if (st < cs[t] || (st == cs[t] && (kx < bk || (kx == bk && qx < bq)))) {
-              cs[t] = st;
-              cq[t] = q0 + u;
-              bk = kx;
-              bq = qx;
-            }
-          }
-        }
-        wmin = min(wmin, cs[t]);
-      }
-      wmin = ~wave_reduce_max(~wmin);
-      if (wmin == kNotYet) break;  // nothing left to schedule
-      if (round > CV) {  // unreachable: every window commits a send
-        fault = true;
-        break;
-      }
-      const uint64_t wend = (uint64_t)wmin + a.cmin;
-      wave_sync();
-#pragma unroll
-      for (int t = 0; t < kGreedyLinkSlots; t++) {
-        if (cs[t] != kNotYet && (uint64_t)cs[t] < wend) {
-          const int l = lane + 64 * t;
-          const uint4 rc = grec[lb[t] + cq[t]];
-          const uint32_t x = rc.w & 0xFFFFu;
-          const uint32_t f = cs[t] + s_cost[l];
-          if (kRS) {
-            const uint32_t nxt = rc.w >> 16;
-            if (nxt != kNoPred) {
-              atomicMax(&grdy[nxt], f);
-              atomicSub(&gpend[nxt], 1u);
-            }
-          }
-          gfin[x] = f;
-          lf[t] = f;
-          mk = max(mk, f);
-          grec[lb[t] + cq[t]] = grec[lb[t] + ln[t] - 1];
-          ln[t]--;
-        }
-      }
-      wave_sync();
-    }
+    greedy_windows<kRS>(E, lane, CV, a.cmin, s_cost, grec, gofs, gfin, grdy, gpend, mk, fault);
 
     const bool all_ok = __ballot(bad) == 0;
     const bool failed = __ballot(fault) != 0;

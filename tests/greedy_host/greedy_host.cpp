@@ -1,0 +1,85 @@
+// Host run of the windowed greedy (App. B.2) with the library's own per-lane
+// steps (greedy_window.h), for the tests: the steps of every lane of a
+// 64-lane wavefront are executed one lane after another, with the window
+// minimum taken over all of them in between, exactly as the kernels
+// arrange them. Built for the host only, under AddressSanitizer and
+// UndefinedBehaviorSanitizer.
+//
+// stdin (little-endian u32): E, nslots, cmin, n_records, cost[E],
+// gofs[E + 1], records[n_records][4]. stdout: makespan, then the finish
+// time of every slot (kGreedyNone for a slot without a send), one a line.
+#include <cstdio>
+#include <vector>
+
+#include "greedy_window.h"
+
+using taccl::GreedyBest;
+using taccl::GreedyLink;
+using taccl::kGreedyNone;
+
+namespace {
+
+struct Plain {  // one lane at a time: plain updates
+  static void max_into(uint32_t *p, uint32_t v) { *p = *p > v ? *p : v; }
+  static void decrement(uint32_t *p) { --*p; }
+};
+
+bool read_u32(uint32_t *out, size_t n) { return fread(out, 4, n, stdin) == n; }
+
+}  // namespace
+
+int main() {
+  uint32_t hdr[4];
+  if (!read_u32(hdr, 4)) return 2;
+  const uint32_t E = hdr[0], nslots = hdr[1], cmin = hdr[2], nrec = hdr[3];
+  constexpr int kLanes = 64, kSlots = 4;  // a wavefront, four links per lane
+  if (E > (uint32_t)kLanes * kSlots || nslots > 65535) return 2;
+  std::vector<uint32_t> cost(E), gofs(E + 1);
+  std::vector<uint4> grec(nrec);
+  if (!read_u32(cost.data(), E) || !read_u32(gofs.data(), E + 1)) return 2;
+  for (uint32_t r = 0; r < nrec; r++) {
+    uint32_t w[4];
+    if (!read_u32(w, 4)) return 2;
+    grec[r] = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+  std::vector<uint32_t> gfin(nslots > 0 ? nslots : 1, kGreedyNone);
+  std::vector<GreedyLink> lk((size_t)kLanes * kSlots);
+  for (int lane = 0; lane < kLanes; lane++)
+    for (int t = 0; t < kSlots; t++) {
+      const uint32_t l = lane + kLanes * t;
+      GreedyLink &g = lk[(size_t)lane * kSlots + t];
+      g.free = 0;
+      g.base = l < E ? gofs[l] : 0;
+      g.len = l < E ? gofs[l + 1] - gofs[l] : 0;
+    }
+  uint32_t mk = 0;
+  bool fault = false;
+  std::vector<GreedyBest> best(lk.size());
+  for (uint32_t round = 0;; round++) {
+    uint32_t wmin = kGreedyNone;
+    for (size_t k = 0; k < lk.size(); k++) {
+      best[k] = taccl::greedy_scan_link<false>(lk[k], grec.data(), gfin.data(), nullptr, nullptr);
+      const uint32_t st = taccl::greedy_start(best[k]);
+      wmin = st < wmin ? st : wmin;
+    }
+    if (wmin == kGreedyNone) break;
+    if (round > nslots) {
+      fault = true;
+      break;
+    }
+    const uint64_t wend = (uint64_t)wmin + cmin;
+    for (int lane = 0; lane < kLanes; lane++)
+      for (int t = 0; t < kSlots; t++) {
+        const size_t k = (size_t)lane * kSlots + t;
+        const uint32_t st = taccl::greedy_start(best[k]);
+        if (st != kGreedyNone && (uint64_t)st < wend)
+          fault |= taccl::greedy_commit<false, Plain>(lk[k], best[k], cost[lane + kLanes * t],
+                                                      grec.data(), gfin.data(), nullptr, nullptr,
+                                                      mk);
+      }
+  }
+  if (fault) return 3;
+  printf("%u\n", mk);
+  for (uint32_t s = 0; s < nslots; s++) printf("%u\n", gfin[s]);
+  return 0;
+}
