@@ -32,8 +32,8 @@ TARGETS = ("twonode16_ag", "fournode64_a2a")
 
 
 # Kernel that dominates each workload's launch (the only kernel it runs).
-KERNEL_OF = {"ring4_ag": "tree_layers", "cubemesh8_ag": "tree_layers",
-             "twonode16_ag": "tree_layers", "switch16_a2a": "path_eval_fast",
+KERNEL_OF = {"ring4_ag": "tree_rank", "cubemesh8_ag": "tree_rank",
+             "twonode16_ag": "tree_rank", "switch16_a2a": "path_eval_fast",
              "fournode64_a2a": "path_eval_fast", "twonode16_ag_contig": "tree_layers",
              "fournode64_a2a_contig": "path_eval_fast", "cubemesh8_ar": "tree_layers",
              "twonode16_rs": "tree_layers", "twonode16_ar": "tree_layers",
