@@ -38,7 +38,9 @@ KERNEL_OF = {"ring4_ag": "tree_rank", "cubemesh8_ag": "tree_rank",
              "fournode64_a2a_contig": "path_eval_fast", "cubemesh8_ar": "tree_layers",
              "twonode16_rs": "tree_layers", "twonode16_ar": "tree_layers",
              "cubemesh8_ag_greedy": "tree_greedy", "twonode16_ag_greedy": "tree_greedy",
-             "switch16_a2a_ports": "path_eval", "fournode64_a2a_ports": "path_eval"}
+             "switch16_a2a_ports": "path_eval", "fournode64_a2a_ports": "path_eval",
+             "switch16_a2a_greedy": "path_greedy", "fournode64_a2a_greedy": "path_greedy_block",
+             "twonode16_ag_rgreedy": "tree_eval_general"}
 
 
 def csrc_digest():
