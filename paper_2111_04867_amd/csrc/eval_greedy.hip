@@ -20,6 +20,15 @@
 //      priority << 16 | chunk;
 //   4. the single winner per link commits: finish = start + latency, the
 //      link and the chunk advance, and the link's two minima are reset.
+// When the whole order fits one 64-bit word the window takes two barriers
+// instead of four: every start is at least the previous window's W, and an
+// eligible one is below it by less than 2 c_min + c_max (every time so far
+// is a finish of a send that started before the previous window's end), so
+// (start - previous W, clamped above that bound) | key rank | priority |
+// chunk orders exactly; one atomicMin per hop into its link's word and one
+// per wavefront of its smallest start, then the holder of each link's
+// minimum commits if that start is below W + c_min (two buffers of minima,
+// the one for the next window reset while this one is read).
 // In reverse path order the greedy serves the mirrored schedule (a chunk's
 // hops from its last link back, key ranks of the mirrored lengths) and
 // records each send's service position on its link; a link's real order is
@@ -39,8 +48,8 @@ constexpr uint32_t kNone = 0xFFFFFFFFu;
 
 int32_t align16(int32_t x) { return (x + 15) & ~15; }
 
-template <int CPT, int NT>
-__global__ __launch_bounds__(NT) void path_greedy_block(PathGreedyArgs a) {
+template <int CPT, int NT, bool kPack>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(8, 8))) void path_greedy_block(PathGreedyArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int P = a.P, E = a.E, H = a.H;
@@ -67,13 +76,21 @@ __global__ __launch_bounds__(NT) void path_greedy_block(PathGreedyArgs a) {
     }
     // per chunk: first hop of its option in path_links, hop count, hops
     // served, time, and the current hop's link, key rank and priority
+    // (one-word keys: the key's constant part, key rank | priority | chunk,
+    // in place of the rank and the priority)
     uint32_t qo[CPT], hops[CPT], cur[CPT], ct[CPT], cl[CPT], kr[CPT], pv[CPT];
+    uint64_t klo[CPT];
     bool bad = false;
     auto load_hop = [&](int j, int c) {
       const uint32_t h = a.mirror ? hops[j] - 1 - cur[j] : cur[j];
       cl[j] = a.path_links[qo[j] + h];
-      kr[j] = a.gkrank[qo[j] + h];
-      pv[j] = gpr[(uint32_t)c * H + h];
+      const uint32_t k = a.gkrank[qo[j] + h], pr = gpr[(uint32_t)c * H + h];
+      if (kPack) {
+        klo[j] = ((uint64_t)k << a.kr_shift) | ((uint64_t)pr << a.chunk_bits) | (uint32_t)c;
+      } else {
+        kr[j] = k;
+        pv[j] = pr;
+      }
     };
 #pragma unroll
     for (int j = 0; j < CPT; j++) {
@@ -102,7 +119,62 @@ __global__ __launch_bounds__(NT) void path_greedy_block(PathGreedyArgs a) {
 
     uint32_t mk = 0;
     bool fault = false;
-    for (int round = 0, buf = 0;; round++, buf ^= 1) {
+    // commit hop j of chunk c, which starts at st on link l
+    auto commit = [&](int j, int c, uint32_t st, uint32_t l) {
+      const uint32_t f = st + s_cost[l];
+      ct[j] = f;
+      lfree[l] = f;
+      mk = max(mk, f);
+      if (a.mirror) {
+        const uint32_t h = hops[j] - 1 - cur[j];
+        fpos[(uint32_t)c * H + h] = (uint16_t)lserv[l];
+      }
+      lserv[l]++;
+      if (++cur[j] < hops[j]) load_hop(j, c);
+    };
+    if (kPack) {
+      // best1 / best2 serve as the two buffers of per-link minima (best2 at
+      // best1 + bst), red as the two window starts
+      const int bst = (a.b_best2 - a.b_best1) / 8;
+      if (tid == 0) red[0] = red[1] = kNone;
+      __syncthreads();
+      uint32_t wp = 0;  // the previous window's W
+      for (int round = 0, buf = 0;; round++, buf ^= 1) {
+        uint32_t st[CPT];
+        uint32_t wmin = kNone;
+        auto key_of = [&](int j) {
+          return klo[j] | ((uint64_t)min(st[j] - wp, a.rel_max) << a.rel_shift);
+        };
+#pragma unroll
+        for (int j = 0; j < CPT; j++) {
+          st[j] = kNone;
+          if (cur[j] < hops[j]) {
+            st[j] = max(ct[j], lfree[cl[j]]);
+            wmin = min(wmin, st[j]);
+            atomicMin(&best1[buf * bst + cl[j]], key_of(j));
+          }
+        }
+        wmin = ~wave_reduce_max(~wmin);
+        if (lane == 0 && wmin != kNone) atomicMin(&red[buf], wmin);
+        __syncthreads();
+        const uint32_t W = red[buf];
+        if (W == kNone) break;  // every chunk is through
+        if (round > a.nslots) {  // unreachable: every window serves a send
+          fault = true;
+          break;
+        }
+        const uint64_t wend = (uint64_t)W + a.cmin;
+#pragma unroll
+        for (int j = 0; j < CPT; j++)
+          if (st[j] != kNone && (uint64_t)st[j] < wend && best1[buf * bst + cl[j]] == key_of(j))
+            commit(j, tid + NT * j, st[j], cl[j]);
+        for (int l = tid; l < E; l += NT) best1[(buf ^ 1) * bst + l] = ~0ull;
+        if (tid == 0) red[buf ^ 1] = kNone;
+        wp = W;
+        __syncthreads();
+      }
+    }
+    for (int round = 0, buf = 0; !kPack; round++, buf ^= 1) {
       // 1. starts and their block minimum
       uint32_t st[CPT];
       uint32_t wmin = kNone;
@@ -149,18 +221,9 @@ __global__ __launch_bounds__(NT) void path_greedy_block(PathGreedyArgs a) {
         if (st[j] != kNone && (uint64_t)st[j] < wend && best1[cl[j]] == k1[j] &&
             best2[cl[j]] == (((uint64_t)pv[j] << 16) | (uint32_t)c)) {
           const uint32_t l = cl[j];
-          const uint32_t f = st[j] + s_cost[l];
-          ct[j] = f;
-          lfree[l] = f;
-          mk = max(mk, f);
-          if (a.mirror) {
-            const uint32_t h = hops[j] - 1 - cur[j];
-            fpos[(uint32_t)c * H + h] = (uint16_t)lserv[l];
-          }
-          lserv[l]++;
           best1[l] = ~0ull;
           best2[l] = ~0ull;
-          if (++cur[j] < hops[j]) load_hop(j, c);
+          commit(j, c, st[j], l);
         }
       }
       __syncthreads();
@@ -228,14 +291,25 @@ __global__ __launch_bounds__(NT) void path_greedy_block(PathGreedyArgs a) {
   }
 }
 
-template <int NT>
-const void *block_fn(int cpt) {
+template <int NT, bool kPack>
+const void *block_fn_p(int cpt) {
   switch (cpt) {
-    case 1: return (const void *)path_greedy_block<1, NT>;
-    case 2: return (const void *)path_greedy_block<2, NT>;
-    case 4: return (const void *)path_greedy_block<4, NT>;
-    default: return (const void *)path_greedy_block<8, NT>;
+    case 1: return (const void *)path_greedy_block<1, NT, kPack>;
+    case 2: return (const void *)path_greedy_block<2, NT, kPack>;
+    case 4: return (const void *)path_greedy_block<4, NT, kPack>;
+    default: return (const void *)path_greedy_block<8, NT, kPack>;
   }
+}
+
+template <int NT>
+const void *block_fn(const PathGreedyArgs &a) {
+  return a.pack ? block_fn_p<NT, true>(a.cpt) : block_fn_p<NT, false>(a.cpt);
+}
+
+int bits_for(uint64_t x) {  // bits to hold values 0..x
+  int b = 0;
+  while (b < 64 && (x >> b) != 0) b++;
+  return b;
 }
 
 }  // namespace
@@ -252,6 +326,18 @@ int32_t path_greedy_block_layout(const taccl_plan &p, PathGreedyArgs &a) {
   a.cmin = cmin;
   a.nslots = C * H;
   a.cpt = cpt;
+  // one-word keys: a relative start below 2 c_min + c_max must stay below
+  // the clamp value 2^rb - 1
+  uint64_t cmax = 0;
+  for (uint32_t c : p.cost) cmax = std::max<uint64_t>(cmax, c);
+  const int rb = bits_for(2 * (uint64_t)cmin + cmax);
+  const int kb = bits_for(p.gk_count > 0 ? (uint64_t)(p.gk_count - 1) : 0);
+  const int cb = bits_for(C > 0 ? (uint64_t)(C - 1) : 0);
+  a.pack = rb + kb + 32 + cb <= 64 && rb < 32;
+  a.chunk_bits = cb;
+  a.kr_shift = cb + 32;
+  a.rel_shift = cb + 32 + kb;
+  a.rel_max = a.pack ? (uint32_t)((1ull << rb) - 1) : 0u;
   int32_t off = 0;
   auto take = [&](int32_t bytes) {
     int32_t o = off;
@@ -272,7 +358,7 @@ int32_t path_greedy_block_layout(const taccl_plan &p, PathGreedyArgs &a) {
 
 int path_greedy_block_per_cu(const PathGreedyArgs &a) {
   int nb = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, block_fn<kGreedyBlockThreads>(a.cpt),
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, block_fn<kGreedyBlockThreads>(a),
                                                    kGreedyBlockThreads, a.block_bytes) !=
       hipSuccess)
     return 0;
@@ -281,7 +367,7 @@ int path_greedy_block_per_cu(const PathGreedyArgs &a) {
 
 hipError_t launch_path_greedy_block(const PathGreedyArgs &a, int grid, hipStream_t stream) {
   void *args[] = {(void *)&a};
-  return hipLaunchKernel(block_fn<kGreedyBlockThreads>(a.cpt), dim3(grid),
+  return hipLaunchKernel(block_fn<kGreedyBlockThreads>(a), dim3(grid),
                          dim3(kGreedyBlockThreads), args, a.block_bytes, stream);
 }
 

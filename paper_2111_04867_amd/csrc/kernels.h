@@ -135,6 +135,11 @@ struct PathGreedyArgs {
   const uint32_t *gkrank;
   int32_t cpt, block_bytes;
   int32_t b_cost, b_lfree, b_best1, b_best2, b_lserv, b_lnext, b_red, b_fpos;
+  // one-word window keys: start - previous window start (clamped to
+  // rel_max) << rel_shift | key rank << kr_shift | priority << chunk_bits |
+  // chunk, when they fit 64 bits (pack != 0)
+  int32_t pack, rel_shift, kr_shift, chunk_bits;
+  uint32_t rel_max;
 };
 
 // Switch-hyperedge connection count: one block per candidate at a time.

@@ -449,6 +449,7 @@ static taccl_status_t build_levels(taccl_plan *p) {
   // travelled asc; in reverse path order the mirrored lengths, remaining' =
   // travelled + latency and travelled' = remaining - latency)
   p->gkrank.clear();
+  p->gk_count = 0;
   if (p->greedy) {
     std::vector<std::pair<uint64_t, uint64_t>> keys(p->path_links.size());
     for (size_t q = 0; q < npath; q++) {
@@ -468,6 +469,7 @@ static taccl_status_t build_levels(taccl_plan *p) {
     p->gkrank.resize(keys.size());
     for (size_t j = 0; j < keys.size(); j++)
       p->gkrank[j] = (uint32_t)(std::lower_bound(uniq.begin(), uniq.end(), keys[j]) - uniq.begin());
+    p->gk_count = (int32_t)uniq.size();
   }
 
   // compact tables of the register-resident kernel (paths of <= 6 hops,

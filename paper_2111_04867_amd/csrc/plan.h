@@ -152,8 +152,9 @@ struct taccl_plan {
   // Alltoall greedy orders: per hop (index into path_links) the rank of its
   // Step-2 key (remaining desc, travelled asc) among all hops of the plan,
   // with the lengths of the greedy's direction (mirrored in reverse path
-  // order)
+  // order), and the number of distinct ranks
   std::vector<uint32_t> gkrank;
+  int32_t gk_count = 0;
 
   // launch shape
   int32_t tree_lds = 0, path_lds = 0;

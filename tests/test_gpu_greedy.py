@@ -176,6 +176,22 @@ def test_full_batch_sampled(name):
 
 
 @pytest.mark.parametrize("order", [1, 2])
+def test_alltoall_block_kernel_two_word_keys(order):
+    """The block kernel packs (start - previous window start, key rank,
+    priority, chunk) into one word when the relative start (below 2 c_min +
+    c_max), the key rank and the chunk fit 32 bits together; 16 MiB chunks
+    on 1600 chunks do not fit, so the windows take the two-word minima."""
+    w = cf.full_a2a(40, chunk_bytes=16 << 20)
+    w = cf.with_greedy(w) if order == 1 else cf.with_reverse_greedy(w)
+    plan, ref, opts = plans(w)
+    cost = [int(x) for x in plan.link_costs()]
+    assert (2 * min(cost) + max(cost)).bit_length() + (plan.num_chunks - 1).bit_length() > 32
+    routes, prio = generate(w.seed + 14, 0, 48, opts, plan.prio_stride)
+    prio[::3] = 9
+    check(plan, ref, routes, prio, f"full40 16 MiB alltoall greedy order={order}")
+
+
+@pytest.mark.parametrize("order", [1, 2])
 def test_alltoall_block_kernel_eight_chunks_per_thread(order):
     """8192 chunks: the block kernel's largest shape (8 chunks per thread)."""
     edges = [(u, v, 700, 8) for u in range(64) for v in range(64) if u != v]
