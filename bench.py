@@ -40,7 +40,7 @@ KERNEL_OF = {"ring4_ag": "tree_rank", "cubemesh8_ag": "tree_rank",
              "cubemesh8_ag_greedy": "tree_greedy", "twonode16_ag_greedy": "tree_greedy",
              "switch16_a2a_ports": "path_eval", "fournode64_a2a_ports": "path_eval",
              "switch16_a2a_greedy": "path_greedy", "fournode64_a2a_greedy": "path_greedy_block",
-             "twonode16_ag_rgreedy": "tree_eval_general"}
+             "twonode16_ag_rgreedy": "tree_greedy"}
 
 
 def csrc_digest():

@@ -276,10 +276,9 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     a.valid = d_valid;
     a.n = n;
     // the layered kernel needs whole route words and priorities in registers
-    // greedy orders in reverse path order run on the general kernel only
     const bool greedy = p->greedy != 0;
     const bool layered =
-        p->greedy != 2 && a.routes_word_aligned &&
+        a.routes_word_aligned &&
         (greedy ? tree_greedy_layout(*p, a) : tree_layers_layout(*p, a)) > 0 &&
         tree_block_bytes(a, 1) <= t->max_lds;
     const int kind = p->coll.kind;

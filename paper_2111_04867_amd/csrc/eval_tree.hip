@@ -1319,6 +1319,68 @@ __device__ __forceinline__ void greedy_windows(int E, int lane, int nslots, uint
   }
 }
 
+// Reverse path order (App. B.2): after the greedy has served the mirrored
+// schedule, every link's list holds its sends in the reverse of the mirrored
+// service order, which is the real order. The real times then follow the
+// App. B.3 rule along those orders: in steps, every link serves the send at
+// the front of its list if it is ready (kPush: every send into the source
+// is scheduled, the ReduceScatter form; else the send that brings the chunk
+// has finished). The orders are acyclic with the chunk dependencies, so
+// every step serves a send until all are through.
+template <bool kPush>
+__device__ __forceinline__ void greedy_real_times(int E, int lane, int nslots,
+                                                  const uint32_t *s_cost, const uint4 *grec,
+                                                  const uint32_t *gofs, uint32_t *gfin,
+                                                  uint32_t *grdy, uint32_t *gpend, uint32_t &mk,
+                                                  bool &fault) {
+  uint32_t p[kGreedyLinkSlots], e[kGreedyLinkSlots], fr[kGreedyLinkSlots], c[kGreedyLinkSlots];
+  uint4 rc[kGreedyLinkSlots];  // the record at the front of each list
+#pragma unroll
+  for (int t = 0; t < kGreedyLinkSlots; t++) {
+    const int l = lane + 64 * t;
+    p[t] = l < E ? gofs[l] : 0;
+    e[t] = l < E ? gofs[l + 1] : 0;
+    c[t] = l < E ? s_cost[l] : 0;
+    fr[t] = 0;
+    rc[t] = p[t] < e[t] ? grec[p[t]] : make_uint4(0, 0, 0, 0);
+  }
+  for (int step = 0;; step++) {
+    bool pending = false;
+#pragma unroll
+    for (int t = 0; t < kGreedyLinkSlots; t++) {
+      if (p[t] >= e[t]) continue;
+      const uint32_t x = rc[t].w & 0xFFFFu, o = rc[t].w >> 16;
+      bool ready = true;
+      uint32_t r = 0;
+      if (kPush) {
+        ready = lds_get(&gpend[x]) == 0;
+        r = lds_get(&grdy[x]);
+      } else if (o != kNoPred) {
+        r = lds_get(&gfin[o]);
+        ready = r != kNotYet;
+      }
+      if (ready) {
+        const uint32_t f = max(r, fr[t]) + c[t];
+        gfin[x] = f;
+        fr[t] = f;
+        mk = max(mk, f);
+        if (kPush && o != kNoPred) {
+          atomicMax(&grdy[o], f);
+          atomicSub(&gpend[o], 1u);
+        }
+        if (++p[t] < e[t]) rc[t] = grec[p[t]];
+      }
+      pending |= p[t] < e[t];
+    }
+    if (__ballot(pending) == 0) break;
+    if (step > nslots) {  // unreachable: the orders come from a schedule
+      fault = true;
+      break;
+    }
+    wave_sync();
+  }
+}
+
 __global__ __launch_bounds__(kTreeMaxThreads) void path_greedy_kernel(PathGreedyArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int C = a.C, P = a.P, E = a.E, H = a.H;
@@ -1461,7 +1523,12 @@ __global__ __launch_bounds__(kTreeMaxThreads) void path_greedy_kernel(PathGreedy
 // by (start, Step-2 key) with start < W + c_min is the greedy's next send
 // there and all of them can be committed at once. One lane holds up to four
 // links and scans each link's pending sends; committed sends are removed by
-// swapping in the link's last pending send.
+// swapping in the link's last pending send. In reverse path order
+// (a.greedy == 2) the greedy serves the mirrored schedule (lengths measured
+// from the other end, every chunk dependency reversed: the Allgather waits
+// for the sends out of the destination, the ReduceScatter for the send that
+// carries the partial on), and the real times come from the orders it
+// leaves (greedy_real_times).
 template <int J, int PW, bool kRS>
 __global__ __launch_bounds__(kTreeMaxThreads) void tree_greedy_kernel(TreeArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
@@ -1547,6 +1614,7 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_greedy_kernel(TreeArgs a
                            lane, pe, ps, dv, bad, fault);
 
     // ---- per-slot send records; sends counted per link ------------------
+    const bool mirror = a.greedy == 2;
     uint32_t lk[J], idx[J];
     uint64_t kk[J];
 #pragma unroll
@@ -1557,7 +1625,7 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_greedy_kernel(TreeArgs a
       idx[j] = 0;
       if (sl < (uint32_t)CV) {
         gfin[sl] = kNotYet;
-        if (kRS) {
+        if (kRS || mirror) {
           grdy[sl] = 0;
           gpend[sl] = 0;
         }
@@ -1565,15 +1633,22 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_greedy_kernel(TreeArgs a
       if (pe[j] != ~0u) {
         const uint32_t l0 = pe[j] & 0xFFFFu;
         const uint32_t l = kRS ? s_rev[l0] : l0;
-        const uint32_t trav = kRS ? lds_get(&dist[sl]) : dv[j] - s_cost[l];
-        const uint32_t rem = kRS ? dv[j] : lds_get(&dist[sl]) - trav;
+        uint32_t trav = kRS ? lds_get(&dist[sl]) : dv[j] - s_cost[l];
+        uint32_t rem = kRS ? dv[j] : lds_get(&dist[sl]) - trav;
+        if (mirror) {  // remaining' = travelled + own cost, travelled' = remaining - own cost
+          const uint32_t c = s_cost[l], r2 = trav + c;
+          trav = rem - c;
+          rem = r2;
+        }
         lk[j] = l;
         kk[j] = ((uint64_t)(~rem) << 32) | trav;
         idx[j] = atomicAdd(&gofs[l + 1], 1u);
       }
     }
     wave_sync();
-    if (kRS) {
+    // inputs per send for the push form (the ReduceScatter's schedule, and
+    // the mirrored greedy of an Allgather)
+    if (kRS || mirror) {
 #pragma unroll
       for (int j = 0; j < J; j++)
         if (pe[j] != ~0u && ps[j] != kNoPred) atomicAdd(&gpend[ps[j]], 1u);
@@ -1602,7 +1677,23 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_greedy_kernel(TreeArgs a
 
     // ---- the greedy, window by window ------------------------------------
     uint32_t mk = 0;
-    greedy_windows<kRS>(E, lane, CV, a.cmin, s_cost, grec, gofs, gfin, grdy, gpend, mk, fault);
+    if (kRS == mirror) {
+      greedy_windows<false>(E, lane, CV, a.cmin, s_cost, grec, gofs, gfin, grdy, gpend, mk, fault);
+    } else {
+      greedy_windows<true>(E, lane, CV, a.cmin, s_cost, grec, gofs, gfin, grdy, gpend, mk, fault);
+    }
+    if (mirror && !fault) {
+      // the real schedule along the orders the mirrored greedy left
+      wave_sync();
+#pragma unroll
+      for (int j = 0; j < J; j++) {
+        const uint32_t sl = lane + 64 * j;
+        if (sl < (uint32_t)CV) gfin[sl] = kNotYet;
+      }
+      wave_sync();
+      mk = 0;
+      greedy_real_times<kRS>(E, lane, CV, s_cost, grec, gofs, gfin, grdy, gpend, mk, fault);
+    }
 
     const bool all_ok = __ballot(bad) == 0;
     const bool failed = __ballot(fault) != 0;

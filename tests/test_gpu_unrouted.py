@@ -38,7 +38,8 @@ CASES = [
     ("layered contig", lambda: cf.named("twonode16_ag_contig"), 200),
     ("general ring6", lambda: cf.uni_ring_ag(6), 200),
     ("general full5", lambda: cf.full_ag(5, k=3), 200),
-    ("general rgreedy", lambda: cf.named("twonode16_ag_rgreedy"), 100),
+    ("general rgreedy ring6", lambda: cf.with_reverse_greedy(cf.uni_ring_ag(6)), 200),
+    ("tree rgreedy twonode16", lambda: cf.named("twonode16_ag_rgreedy"), 100),
     ("tree greedy", lambda: cf.named("cubemesh8_ag_greedy"), 200),
     ("fast a2a switch16", lambda: cf.named("switch16_a2a"), 200),
     ("fast a2a fournode64", lambda: cf.named("fournode64_a2a"), 24),
