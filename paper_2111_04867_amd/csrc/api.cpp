@@ -52,7 +52,7 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
          o_lal = pk.add(p->lalpha), o_lbs = pk.add(p->lbs), o_lmg = pk.add(p->lmerge),
          o_lrev = pk.add(p->lrev), o_hc2 = pk.add(p->hop_class2),
          o_lcb2 = pk.add(p->lvl_cls2_begin), o_llc2 = pk.add(p->llc2),
-         o_gkr = pk.add(p->gkrank), o_tent = pk.add(p->tent);
+         o_gkr = pk.add(p->gkrank), o_tent = pk.add(p->tent), o_c2l = pk.add(p->cls2_link);
   void *blk = nullptr;
   e = hipMalloc(&blk, pk.bytes.size());
   if (e != hipSuccess) return fail(TACCL_ERR_NO_MEMORY, "hipMalloc of plan tables failed");
@@ -88,6 +88,7 @@ taccl_status_t ensure_device(taccl_plan *p, DeviceTables **out) {
   t.hop_class2 = (const uint16_t *)at(o_hc2);
   t.lvl_cls2_begin = (const uint32_t *)at(o_lcb2);
   t.llc2 = (const uint32_t *)at(o_llc2);
+  t.cls2_link = (const uint16_t *)at(o_c2l);
   t.arec = (const uint32_t *)at(o_arec);
   t.cpath = (const uint32_t *)at(o_cpath);
   t.cinfo = (const uint32_t *)at(o_cinfo);
@@ -231,6 +232,7 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     a.hop_class2 = t->hop_class2;
     a.lvl_cls2_begin = t->lvl_cls2_begin;
     a.llc2 = t->llc2;
+    a.cls2_link = t->cls2_link;
     a.arec = t->arec;
     a.cpath = t->cpath;
     a.cinfo = t->cinfo;
@@ -246,6 +248,8 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     } else {
       if (path_layout(*p, a) > t->max_lds)
         return fail(TACCL_ERR_UNSUPPORTED, "Alltoall plan needs more LDS than a block has");
+      if (a.ports && a.E > 4 * a.lr_threads)
+        return fail(TACCL_ERR_UNSUPPORTED, "switch ports take at most four links per thread");
       e = launch_path(a, grid, s);
     }
   } else {

@@ -74,14 +74,12 @@ __device__ __forceinline__ void lds_put(uint32_t *p, uint32_t v) {
 // holds its send port (its class's link, already ordered in `sorted`) and
 // its receive port (the downlink), each port serving its sends in Step-2
 // order. The level's switched sends are ordered a second time by receive
-// port; then every send-port run is timed in order, taking as a further
-// bound the finish of the send before it on its receive port, and the
-// passes repeat until nothing changes. The update is monotone and starts
-// below the least schedule, so it stops exactly there. Returns the level's
+// port; then every send port walks its run in order, each switched send
+// waiting for the send before it on its receive port. Returns the level's
 // latest finish (a block-uniform value is not needed: callers max-reduce);
-// updates ctime (arrivals) and lfree (port free times). Sets *fault when
-// the passes do not settle (impossible: each pass fixes at least one more
-// send).
+// updates ctime (arrivals) and lfree (port free times). Sets *fault when a
+// wavefront stops making progress (impossible: both ports order the same
+// key).
 __device__ uint32_t ports_level(const PathArgs &a, int L, const uint32_t *gpr, uint32_t *ctime,
                                 uint32_t *lfree, const uint32_t *ccnt, const uint16_t *sorted,
                                 uint32_t *red, bool *fault) {
@@ -152,149 +150,98 @@ __device__ uint32_t ports_level(const PathArgs &a, int L, const uint32_t *gpr, u
       rank += (py < px) || (py == px && cy < cx);
     }
     sorted2[b + rank] = (uint16_t)cx;
+    dl[cx] = a.cls2_link[lo2 + k];
   }
   __syncthreads();
-  for (int l = tid; l < E; l += nt) {
-    const uint32_t cb = a.llc2[((size_t)L * E + l) * 2], ce = a.llc2[((size_t)L * E + l) * 2 + 1];
-    if (cb == ce) continue;
-    const uint32_t xb = ccnt2[cb - lo2], xe = ccnt2[ce - lo2];
-    for (uint32_t x = xb; x < xe; x++) {
-      const int c = sorted2[x];
-      dl[c] = (uint16_t)l;
-      pd[c] = (x == xb) ? (uint16_t)0xFFFF : sorted2[x - 1];
-    }
+  // the send before each switched send on its receive port: a port's sends
+  // are one contiguous run of the receive-port order
+  for (uint32_t x = tid; x < tot2; x += nt) {
+    const uint32_t c = sorted2[x], prev = x ? (uint32_t)sorted2[x - 1] : 0u;
+    pd[c] = (x && dl[prev] == dl[c]) ? (uint16_t)prev : (uint16_t)0xFFFF;
   }
   __syncthreads();
-  // every position of the level's send-port order: its link and its index
-  // in that link's run (one thread per link labels its run)
+  // The level's schedule as a dataflow: every send port walks its run in
+  // the Step-2 order, and a switched send goes once the send before it on
+  // its receive port has finished (the first on a receive port takes the
+  // port's busy time instead). Both ports order the same key, so these
+  // waits follow one order of the level's sends and every send is reached;
+  // each finish is written once, from the finishes it depends on, so it is
+  // the least schedule. A wavefront whose lanes make no progress for far
+  // longer than the level can take reports a fault instead of waiting on.
+  constexpr uint32_t kUnsetF = 0xFFFFFFFFu;
+  constexpr int kPortSlots = 4;  // send ports per thread: E <= 4 x threads
   const uint32_t tot = ccnt[a.lvl_cls_begin[L + 1] - lo];
-  uint32_t *pinf = (uint32_t *)(lds + a.o_eprio);  // the send-order staging is dead
-  for (int l = tid; l < E; l += nt) {
-    const uint32_t cb = a.llc[((size_t)L * E + l) * 2], ce = a.llc[((size_t)L * E + l) * 2 + 1];
-    if (cb == ce) continue;
-    const uint32_t xb = ccnt[cb - lo], xe = ccnt[ce - lo];
-    for (uint32_t x = xb; x < xe; x++) pinf[x] = (uint32_t)l | ((x - xb) << 16);
+  // per send-order position: chunk | the send before it on its receive
+  // port << 16, and its ready time without that send (the receive port's
+  // busy time folded in for the first send on a port); the send-order and
+  // receive-port staging arrays are dead
+  uint32_t *wcp = eprio2, *wr0 = (uint32_t *)(lds + a.o_eprio);
+  for (uint32_t x = tid; x < tot; x += nt) {
+    const uint32_t c = sorted[x], d = dl[c];
+    const uint32_t pj = d != 0xFFFFu ? (uint32_t)pd[c] : 0xFFFFu;
+    uint32_t r0 = ctime[c];
+    if (d != 0xFFFFu && pj == 0xFFFFu) r0 = max(r0, lfree[d]);
+    wcp[x] = c | (pj << 16);
+    wr0[x] = r0;
   }
-  for (int c = tid; c < C; c += nt) fcur[c] = 0;
+  for (int c = tid; c < C; c += nt) lds_put(&fcur[c], kUnsetF);
+  uint32_t p[kPortSlots], e[kPortSlots], F[kPortSlots], cl[kPortSlots];
+#pragma unroll
+  for (int t = 0; t < kPortSlots; t++) {
+    const int l = tid + nt * t;
+    p[t] = e[t] = F[t] = cl[t] = 0;
+    if (l < E) {
+      const uint32_t cb = a.llc[((size_t)L * E + l) * 2], ce = a.llc[((size_t)L * E + l) * 2 + 1];
+      if (cb != ce) {
+        p[t] = ccnt[cb - lo];
+        e[t] = ccnt[ce - lo];
+      }
+      F[t] = lfree[l];
+      cl[t] = a.cost[l];
+    }
+  }
   __syncthreads();
-  // Passes until the finishes settle. In a pass every send takes as its
-  // ready time max(arrival of its chunk, current finish of the send before
-  // it on its receive port, or that port's busy time); every send-port run
-  // is then timed in closed form, the k-th send finishing at
-  // (k+1)c + max(F, max_{j<=k}(r_j - j c)): runs lie in ascending link order
-  // along the positions, so one block-wide prefix max over
-  // link << 33 | (r_j - j c + 2^32) serves all runs. Each thread owns a
-  // contiguous range of positions. Finishes start at zero, every update is
-  // monotone and bounded by the least schedule, so a pass that changes
-  // nothing has reached it (reads racing with writes of the same pass see
-  // either value, which keeps both properties).
-  uint64_t *red64 = (uint64_t *)(lds + a.o_fred64);
-  const int lane = tid & 63, wave = tid >> 6;
-  const uint32_t per = (tot + nt - 1) / nt;
-  const uint32_t x0 = min((uint32_t)tid * per, tot), x1 = min(x0 + per, tot);
-  // exclusive prefix max of this thread's aggregate over the block
-  auto block_carry = [&](uint64_t agg) {
-    const uint64_t incl = wave_scan_max64(agg);
-    if (lane == 63) red64[wave] = incl;
-    __syncthreads();
-    uint64_t run = dpp64<kWaveShr1>(incl);
-    const uint64_t wv = row_scan_max64(lane < nt / 64 ? red64[lane] : 0ull);
-    const uint32_t w = (uint32_t)__builtin_amdgcn_readfirstlane(wave);
-    if (w) run = max(run, readlane64(wv, w - 1));
-    return run;
-  };
-  constexpr int kReg = 4;  // positions per thread kept in registers
-  if (per <= kReg) {
-    // the fixed part of every owned position once: chunk, link, index in
-    // the run, cost, send-port busy time, ready time without the receive
-    // port's predecessor, and that predecessor (0xFFFF: none or a port
-    // without one, whose busy time is already in the ready time)
-    uint32_t pc[kReg], pl[kReg], pk[kReg], pcl[kReg], pF[kReg], pr0[kReg], prp[kReg];
+  // the send at the front of each owned run
+  uint32_t hcp[kPortSlots], hr0[kPortSlots];
 #pragma unroll
-    for (int q = 0; q < kReg; q++) {
-      const uint32_t x = x0 + q < x1 ? x0 + q : 0u;
-      pc[q] = sorted[x];
-      const uint32_t inf = pinf[x];
-      pl[q] = inf & 0xFFFFu;
-      pk[q] = inf >> 16;
-    }
+  for (int t = 0; t < kPortSlots; t++) {
+    hcp[t] = p[t] < e[t] ? wcp[p[t]] : 0u;
+    hr0[t] = p[t] < e[t] ? wr0[p[t]] : 0u;
+  }
+  const uint32_t spin_limit = 64u * (tot + 64u);
+  for (uint32_t idle = 0;;) {
+    bool left = false, moved = false;
 #pragma unroll
-    for (int q = 0; q < kReg; q++) {
-      pcl[q] = a.cost[pl[q]];
-      pF[q] = lfree[pl[q]];
-      const uint32_t c = pc[q], d = dl[c], pj = pd[c];
-      pr0[q] = ctime[c];
-      prp[q] = 0xFFFF;
-      if (d != 0xFFFF) {
-        if (pj == 0xFFFF) pr0[q] = max(pr0[q], lfree[d]);
-        else prp[q] = pj;
+    for (int t = 0; t < kPortSlots; t++) {
+      if (p[t] >= e[t]) continue;
+      const uint32_t pj = hcp[t] >> 16;
+      uint32_t r = hr0[t];
+      bool ready = true;
+      if (pj != 0xFFFFu) {
+        const uint32_t fp = lds_get(&fcur[pj]);
+        ready = fp != kUnsetF;
+        r = max(r, fp);
       }
-    }
-    for (int pass = 0;; pass++) {
-      uint64_t comp[kReg], agg = 0;
-#pragma unroll
-      for (int q = 0; q < kReg; q++) {
-        uint32_t r = pr0[q];
-        const uint32_t fp = lds_get(&fcur[prp[q] != 0xFFFF ? prp[q] : 0u]);
-        if (prp[q] != 0xFFFF) r = max(r, fp);
-        comp[q] = x0 + q < x1 ? ((uint64_t)pl[q] << 33) |
-                                    ((uint64_t)r + (1ull << 32) - (uint64_t)pk[q] * pcl[q])
-                              : 0ull;
-        agg = max(agg, comp[q]);
-      }
-      uint64_t run = block_carry(agg);
-      bool changed = false;
-#pragma unroll
-      for (int q = 0; q < kReg; q++) {
-        run = max(run, comp[q]);
-        const int64_t best =
-            max((int64_t)pF[q], (int64_t)(run & ((1ull << 33) - 1)) - (int64_t)(1ull << 32));
-        const uint32_t f = (uint32_t)((int64_t)(pk[q] + 1) * pcl[q] + best);
-        if (x0 + q < x1 && f != lds_get(&fcur[pc[q]])) {
-          lds_put(&fcur[pc[q]], f);
-          changed = true;
+      if (ready) {
+        const uint32_t f = max(r, F[t]) + cl[t];
+        lds_put(&fcur[hcp[t] & 0xFFFFu], f);
+        F[t] = f;
+        if (++p[t] < e[t]) {
+          hcp[t] = wcp[p[t]];
+          hr0[t] = wr0[p[t]];
         }
+        moved = true;
       }
-      if (!__syncthreads_or(changed)) break;
-      if (pass > C) {  // unreachable
-        *fault = true;
-        break;
-      }
+      left |= p[t] < e[t];
     }
-  } else {
-    for (int pass = 0;; pass++) {
-      uint64_t agg = 0;
-      for (uint32_t x = x0; x < x1; x++) {
-        const uint32_t c = sorted[x], inf = pinf[x];
-        const uint32_t l = inf & 0xFFFFu, k = inf >> 16;
-        uint32_t r = ctime[c];
-        if (dl[c] != 0xFFFF) r = max(r, pd[c] == 0xFFFF ? lfree[dl[c]] : lds_get(&fcur[pd[c]]));
-        agg = max(agg, ((uint64_t)l << 33) | ((uint64_t)r + (1ull << 32) - (uint64_t)k * a.cost[l]));
-      }
-      uint64_t run = block_carry(agg);
-      bool changed = false;
-      for (uint32_t x = x0; x < x1; x++) {
-        const uint32_t c = sorted[x], inf = pinf[x];
-        const uint32_t l = inf & 0xFFFFu, k = inf >> 16;
-        const uint32_t cl = a.cost[l];
-        uint32_t r = ctime[c];
-        if (dl[c] != 0xFFFF) r = max(r, pd[c] == 0xFFFF ? lfree[dl[c]] : lds_get(&fcur[pd[c]]));
-        run = max(run, ((uint64_t)l << 33) | ((uint64_t)r + (1ull << 32) - (uint64_t)k * cl));
-        const int64_t best =
-            max((int64_t)lfree[l], (int64_t)(run & ((1ull << 33) - 1)) - (int64_t)(1ull << 32));
-        const uint32_t f = (uint32_t)((int64_t)(k + 1) * cl + best);
-        if (f != lds_get(&fcur[c])) {
-          lds_put(&fcur[c], f);
-          changed = true;
-        }
-      }
-      if (!__syncthreads_or(changed)) break;
-      if (pass > C) {  // unreachable
-        *fault = true;
-        break;
-      }
+    if (__ballot(left) == 0) break;
+    idle = __ballot(moved) ? 0u : idle + 1u;
+    if (idle > spin_limit) {  // unreachable: the waits follow one order
+      *fault = true;
+      break;
     }
   }
+  __syncthreads();
   // arrivals and port free times after the level
   uint32_t mk = 0;
   for (uint32_t x = tid; x < tot; x += nt) {
@@ -501,7 +448,6 @@ int32_t path_layout(const taccl_plan &p, PathArgs &a) {
     a.o_fcur = take(4 * C);
     a.o_pd = take(2 * C);
     a.o_dl = take(2 * C);
-    a.o_fred64 = take(8 * (kPathPortThreads / 64));
   }
   a.lr_threads = (p.ports && p.max_lvl_sends > 4 * kPathThreads) ? kPathPortThreads : kPathThreads;
   a.lds_bytes = off;
@@ -949,8 +895,6 @@ int32_t path_fast_layout(const taccl_plan &p, PathArgs &a) {
   a.cbits = (int32_t)bits((uint32_t)C);
   a.lbits = (int32_t)bits((uint32_t)E);
   a.o_fred = take(4 * 2 * (kPathFastThreads / 64));  // sized for the largest block
-  a.o_fred64 = take(8 * (kPathFastThreads / 64));
-  a.o_fredf = take(4 * (kPathFastThreads / 64));
   a.lds_bytes = off;
   return off;
 }

@@ -91,8 +91,7 @@ struct PathArgs {
   int32_t ncls;
   const uint32_t *arec, *cpath, *cinfo, *cbkt;
   int32_t o_faux;
-  int32_t o_fcost, o_fcinfo, o_fcbkt, o_flcb, o_fctime, o_flfree, o_fbcnt, o_fepr, o_fsrt, o_fred,
-      o_fred64, o_fredf;
+  int32_t o_fcost, o_fcinfo, o_fcbkt, o_flcb, o_fctime, o_flfree, o_fbcnt, o_fepr, o_fsrt, o_fred;
   int32_t lds_bytes;
   int32_t cbits, lbits;  // chunk and link fields of a packed sorted send
   // contiguous transfers on links between nodes (contig != 0)
@@ -103,7 +102,7 @@ struct PathArgs {
   int32_t o_fmerge;
   // switch ports (LDS-record kernel): receive-port classes and state
   int32_t ports;
-  const uint16_t *hop_class2;
+  const uint16_t *hop_class2, *cls2_link;
   const uint32_t *lvl_cls2_begin, *llc2;
   int32_t o_ccnt2, o_ccur2, o_echunk2, o_eprio2, o_ecls2, o_sorted2, o_fcur, o_pd, o_dl;
   int32_t lr_threads;  // block size of the LDS-record kernel for this plan

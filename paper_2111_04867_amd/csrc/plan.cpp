@@ -406,6 +406,8 @@ static taccl_status_t build_levels(taccl_plan *p) {
     }
   };
   for (size_t i = 0; i < cv.size(); i++) p->cls_link[i] = (uint16_t)std::get<1>(cv[i]);
+  p->cls2_link.resize(cv2.size());
+  for (size_t i = 0; i < cv2.size(); i++) p->cls2_link[i] = (uint16_t)std::get<1>(cv2[i]);
   class_tables(cv, p->lvl_cls_begin, p->llc, p->max_lvl_cls);
   if (p->ports) class_tables(cv2, p->lvl_cls2_begin, p->llc2, p->max_lvl_cls2);
   // per hop: its send's class (first hop of a unit; 0xFFFF for the second

@@ -58,7 +58,7 @@ struct DeviceTables {
   const uint64_t *lbs = nullptr;
   const uint8_t *lmerge = nullptr;
   const uint16_t *lrev = nullptr;
-  const uint16_t *hop_class2 = nullptr;
+  const uint16_t *hop_class2 = nullptr, *cls2_link = nullptr;
   const uint32_t *lvl_cls2_begin = nullptr, *llc2 = nullptr;
   const uint16_t *hop_class = nullptr;
   const int8_t *path_lvl_hop = nullptr;
@@ -133,6 +133,7 @@ struct taccl_plan {
   std::vector<uint16_t> hop_class;     // [path_links.size()] class of each hop's send
   // switch ports: receive-port class of each switched send's first hop
   std::vector<uint16_t> hop_class2;
+  std::vector<uint16_t> cls2_link;  // [receive-port classes]: the downlink
   std::vector<uint32_t> lvl_cls2_begin, llc2;
   int32_t max_lvl_cls2 = 0;
   std::vector<int8_t> path_lvl_hop;    // [NPATH*nlev] hop at each level or -1
