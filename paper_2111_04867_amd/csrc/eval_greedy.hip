@@ -62,6 +62,10 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(8, 8))) void
   uint32_t *lnext = (uint32_t *)(lds + a.b_lnext);  // real order: next position
   uint32_t *red = (uint32_t *)(lds + a.b_red);      // [2][NW] window minima
   uint16_t *fpos = (uint16_t *)(lds + a.b_fpos);    // service position per slot
+  // the candidate's priorities of its routed hops, chunk after chunk (when
+  // the plan's sends fit: a.b_sprio >= 0), so each priority row is read from
+  // HBM once instead of hop by hop
+  uint32_t *sprio = (uint32_t *)(lds + (a.b_sprio >= 0 ? a.b_sprio : 0));
   for (int l = tid; l < E; l += NT) s_cost[l] = a.cost[l];
 
   for (int64_t i = blockIdx.x; i < a.n; i += gridDim.x) {
@@ -78,13 +82,14 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(8, 8))) void
     // served, time, and the current hop's link, key rank and priority
     // (one-word keys: the key's constant part, key rank | priority | chunk,
     // in place of the rank and the priority)
-    uint32_t qo[CPT], hops[CPT], cur[CPT], ct[CPT], cl[CPT], kr[CPT], pv[CPT];
+    uint32_t qo[CPT], hops[CPT], cur[CPT], ct[CPT], cl[CPT], kr[CPT], pv[CPT], po[CPT];
     uint64_t klo[CPT];
     bool bad = false;
     auto load_hop = [&](int j, int c) {
       const uint32_t h = a.mirror ? hops[j] - 1 - cur[j] : cur[j];
       cl[j] = a.path_links[qo[j] + h];
-      const uint32_t k = a.gkrank[qo[j] + h], pr = gpr[(uint32_t)c * H + h];
+      const uint32_t k = a.gkrank[qo[j] + h];
+      const uint32_t pr = a.b_sprio >= 0 ? sprio[po[j] + h] : gpr[(uint32_t)c * H + h];
       if (kPack) {
         klo[j] = ((uint64_t)k << a.kr_shift) | ((uint64_t)pr << a.chunk_bits) | (uint32_t)c;
       } else {
@@ -108,13 +113,34 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(8, 8))) void
             const uint32_t q = a.pair_base[sd] + k;
             qo[j] = a.path_off[q];
             hops[j] = a.path_off[q + 1] - qo[j];
-            load_hop(j, c);
           } else {
             bad = true;  // the pair is left unrouted
           }
         }
       }
     }
+    if (a.b_sprio >= 0) {
+      // chunk offsets: a block scan of the hop counts
+      uint32_t nh = 0;
+#pragma unroll
+      for (int j = 0; j < CPT; j++) nh += hops[j];
+      const uint32_t incl = wave_scan_add(nh);
+      if (lane == 63) red[wave] = incl;
+      __syncthreads();
+      uint32_t off = incl - nh;
+      for (int w = 0; w < wave; w++) off += red[w];
+#pragma unroll
+      for (int j = 0; j < CPT; j++) {
+        const int c = tid + NT * j;
+        po[j] = off;
+        for (uint32_t h = 0; h < hops[j]; h++) sprio[off + h] = gpr[(uint32_t)c * H + h];
+        off += hops[j];
+      }
+      __syncthreads();
+    }
+#pragma unroll
+    for (int j = 0; j < CPT; j++)
+      if (hops[j]) load_hop(j, tid + NT * j);
     __syncthreads();
 
     uint32_t mk = 0;
@@ -352,6 +378,9 @@ int32_t path_greedy_block_layout(const taccl_plan &p, PathGreedyArgs &a) {
   a.b_lnext = take(4 * E);
   a.b_red = take(4 * 2 * (kGreedyBlockThreads / 64));
   a.b_fpos = take(p.greedy == 2 ? 2 * a.nslots : 0);
+  // staged priorities while two blocks still fit a CU's 160 KB
+  a.b_sprio = -1;
+  if (off + 4 * p.max_sends <= 80 * 1024) a.b_sprio = take((int32_t)(4 * p.max_sends));
   a.block_bytes = off;
   return off;
 }

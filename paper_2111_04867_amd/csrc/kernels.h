@@ -133,7 +133,7 @@ struct PathGreedyArgs {
   // hop (plan table), chunks per thread and the LDS carve-up
   const uint32_t *gkrank;
   int32_t cpt, block_bytes;
-  int32_t b_cost, b_lfree, b_best1, b_best2, b_lserv, b_lnext, b_red, b_fpos;
+  int32_t b_cost, b_lfree, b_best1, b_best2, b_lserv, b_lnext, b_red, b_fpos, b_sprio;
   // one-word window keys: start - previous window start (clamped to
   // rel_max) << rel_shift | key rank << kr_shift | priority << chunk_bits |
   // chunk, when they fit 64 bits (pack != 0)
