@@ -1562,7 +1562,7 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_greedy_kernel(TreeArgs a
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   unsigned char *wl = lds + a.o_wave + wave * a.wave_bytes;
-  uint32_t *rt32 = (uint32_t *)wl;
+  uint32_t *rt32 = (uint32_t *)(wl + a.w_rt);
   uint32_t *dist = (uint32_t *)(wl + a.w_dist);
   uint16_t *anc = (uint16_t *)(wl + a.w_anc);
   uint32_t *gfin = (uint32_t *)(wl + a.w_gfin);  // per slot: finish, kNotYet before
@@ -1943,18 +1943,24 @@ int32_t tree_greedy_layout(const taccl_plan &p, TreeArgs &a) {
     w = align16(w + bytes);
     return o;
   };
-  a.w_rt = wtake(p.route_stride);
-  a.w_dist = wtake(4 * CV);
-  set_pj(a, V, CV);
+  // finish times, and for the push form (ReduceScatter, Allreduce, reverse
+  // path order) ready times and unscheduled inputs per send; the pull form
+  // never touches the latter two
+  const bool push = p.coll.kind == TACCL_REDUCESCATTER || p.coll.kind == TACCL_ALLREDUCE ||
+                    p.greedy == 2;
   a.w_gfin = wtake(4 * CV);
-  a.w_grdy = wtake(4 * CV);
-  a.w_gpend = wtake(4 * CV);
+  a.w_grdy = push ? wtake(4 * CV) : a.w_gfin;
+  a.w_gpend = push ? wtake(4 * CV) : a.w_gfin;
   a.w_gofs = wtake(4 * (E + 1));
-  // the ancestor arrays die with the trees, before the pending-send records
-  // are written
-  a.w_anc = w;
-  a.w_glist = wtake(std::max(16 * S, a.pj_rounds * align16(2 * CV)));
-  a.wave_bytes = w;
+  // the trees' arrays (one-hot routes, distances, ancestors) die before the
+  // pending-send records are written over them
+  set_pj(a, V, CV);
+  const int32_t u = w;
+  a.w_rt = u;
+  a.w_dist = u + align16(p.route_stride);
+  a.w_anc = a.w_dist + align16(4 * CV);
+  a.w_glist = u;
+  a.wave_bytes = std::max(a.w_anc + a.pj_rounds * align16(2 * CV), u + align16(16 * S));
   return a.o_wave + a.wave_bytes;
 }
 
