@@ -1275,7 +1275,8 @@ constexpr int kGreedyLinkSlots = 4;  // links per lane: at most 256 links
 // Several lanes of a window may push into the same send's ready time.
 struct LdsAtomics {
   __device__ static void max_into(uint32_t *p, uint32_t v) { atomicMax(p, v); }
-  __device__ static void decrement(uint32_t *p) { atomicSub(p, 1u); }
+  __device__ static uint32_t decrement(uint32_t *p) { return atomicSub(p, 1u); }
+  __device__ static uint32_t load(uint32_t *p) { return lds_get(p); }
 };
 
 template <bool kRS>
@@ -1652,6 +1653,15 @@ __global__ __launch_bounds__(kTreeMaxThreads) void tree_greedy_kernel(TreeArgs a
 #pragma unroll
       for (int j = 0; j < J; j++)
         if (pe[j] != ~0u && ps[j] != kNoPred) atomicAdd(&gpend[ps[j]], 1u);
+    }
+    if (kRS != mirror) {
+      // push form: a send without inputs is ready at 0
+      wave_sync();
+#pragma unroll
+      for (int j = 0; j < J; j++) {
+        const uint32_t sl = lane + 64 * j;
+        if (pe[j] != ~0u && gpend[sl] == 0) gfin[sl] = 0;
+      }
     }
     {
       // exclusive scan of the per-link counts (gofs[0] = 0)

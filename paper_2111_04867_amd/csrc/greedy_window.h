@@ -8,9 +8,12 @@
 // the mirrored lengths), priority, slot | other slot << 16} in
 // grec[base, base + len); the other slot is the send the chunk arrives by
 // (its finish, gfin[other], is the ready time; kGreedyNoPred: ready at 0)
-// or, for ReduceScatter (kRS), the send that carries the partial on (a
-// send is ready once gpend[slot], its unscheduled inputs, is 0, at
-// grdy[slot]). gfin[slot] is kGreedyNone while a send is pending.
+// or, in the push form (kRS: a send waits for all its inputs, as in a
+// ReduceScatter), the send it is an input of. In the pull form gfin[slot]
+// is kGreedyNone while a send is pending; in the push form it is
+// kGreedyNone until the send's last input is scheduled and then holds its
+// ready time (grdy[slot], the latest input finish; gpend[slot] counts the
+// inputs still unscheduled) until the send itself is scheduled.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -57,7 +60,7 @@ __host__ __device__ inline GreedyBest greedy_scan_link(const GreedyLink &lk, con
     for (int u = 0; u < 2; u++) {
       const uint32_t x = rc[u].w & 0xFFFFu, other = rc[u].w >> 16;
       if (kRS) {
-        r[u] = gpend[x] == 0 ? grdy[x] : kGreedyNone;
+        r[u] = gfin[x];
       } else {
         const uint32_t fo = gfin[other == kGreedyNoPred ? 0u : other];
         r[u] = other == kGreedyNoPred ? 0u : fo;
@@ -78,9 +81,10 @@ __host__ __device__ inline GreedyBest greedy_scan_link(const GreedyLink &lk, con
 }
 
 // Commit the winner b of a link (cost: the link's cost): its finish time,
-// the link's busy time and the running makespan; for ReduceScatter the
-// send that carries the partial on learns the finish through the Ops hooks
-// (max into grdy, one input fewer in gpend). The committed record is swapped
+// the link's busy time and the running makespan; in the push form the send
+// it is an input of learns the finish through the Ops hooks (max into grdy,
+// one input fewer in gpend; the input that takes the count to zero then
+// publishes the ready time in gfin). The committed record is swapped
 // to the end of the pending part, so a list ends in reverse service order.
 // Returns true if the record at the winner's index is not the winner (never
 // the case; reported as a fault).
@@ -97,7 +101,7 @@ __host__ __device__ inline bool greedy_commit(GreedyLink &lk, const GreedyBest &
     const uint32_t nxt = rc.w >> 16;
     if (nxt != kGreedyNoPred) {
       Ops::max_into(&grdy[nxt], f);
-      Ops::decrement(&gpend[nxt]);
+      if (Ops::decrement(&gpend[nxt]) == 1) gfin[nxt] = Ops::load(&grdy[nxt]);
     }
   }
   gfin[x] = f;

@@ -21,7 +21,8 @@ namespace {
 
 struct Plain {  // one lane at a time: plain updates
   static void max_into(uint32_t *p, uint32_t v) { *p = *p > v ? *p : v; }
-  static void decrement(uint32_t *p) { --*p; }
+  static uint32_t decrement(uint32_t *p) { return (*p)--; }
+  static uint32_t load(uint32_t *p) { return *p; }
 };
 
 bool read_u32(uint32_t *out, size_t n) { return fread(out, 4, n, stdin) == n; }
