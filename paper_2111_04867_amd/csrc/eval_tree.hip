@@ -68,6 +68,33 @@ __device__ __forceinline__ void wave_sync() {
 
 __device__ __forceinline__ uint32_t wave_max(uint32_t v) { return wave_reduce_max(v); }
 
+// The push-form hooks of the greedy window steps (greedy_window.h) in LDS;
+// several lanes of a window may push into the same send's ready time.
+struct LdsAtomics {
+  __device__ static void max_into(uint32_t *p, uint32_t v) { atomicMax(p, v); }
+  __device__ static uint32_t decrement(uint32_t *p) { return atomicSub(p, 1u); }
+  __device__ static uint32_t load(uint32_t *p) { return lds_get(p); }
+};
+
+// The general variant's per-link orders as greedy lists: chain[] entries
+// (slot | the slot on the chunk's other side of the send's source << 16)
+// with the Step-2 keys and priorities kept per slot.
+struct ChainView {
+  uint32_t *chain;
+  const uint64_t *key;
+  const uint32_t *prio;
+  __device__ uint4 get(uint32_t i) const {
+    const uint32_t ent = chain[i], s = ent & 0xFFFFu;
+    const uint64_t k = key[s];
+    return make_uint4((uint32_t)k, (uint32_t)(k >> 32), prio[s], ent);
+  }
+  __device__ void swap(uint32_t i, uint32_t j) const {
+    const uint32_t t = chain[i];
+    chain[i] = chain[j];
+    chain[j] = t;
+  }
+};
+
 __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v, int) { return wave_scan_add(v); }
 
 // n / V for n, V < 2^16 with a precomputed m = floor(2^32 / V) + 1
@@ -226,60 +253,52 @@ __device__ __forceinline__ bool any_schedule(const TreeArgs &a, bool rs, int lan
   if (a.greedy) {
     // plans have no zero-cost link, so c_min > 0 and every window serves
     const bool mirror = a.greedy == 2, push = rs != mirror;
-    // windows (as in the layered greedy kernel): W = the earliest start
-    // any ready send can take; a send not ready yet can only start c_min
-    // or more after W, so on every link the best ready send with start <
-    // W + c_min is the greedy's next there. Each link's pending sends are
-    // the front of its chain[] segment (count in lhead[]); a served send
-    // is swapped to the end of the pending part, so the segment ends up
-    // in reverse service order.
+    // windows (as in the record-based greedy kernels, with the same steps,
+    // greedy_window.h): W = the earliest start any ready send can take; a
+    // send not ready yet can only start c_min or more after W, so on every
+    // link the best ready send with start < W + c_min is the greedy's next
+    // there. Each link's pending sends are the front of its chain[] segment
+    // (count in lhead[]); a served send is swapped to the end of the
+    // pending part, so the segment ends up in reverse service order. In the
+    // push form a send's ready time appears in fin[] once its last input is
+    // served (a send without inputs is ready at 0).
+    const ChainView cv{chain, key, prio};
     for (int l = lane; l < E; l += 64) lhead[l] = lbase[l + 1] - lbase[l];
+    if (push)
+      for (int s = lane; s < CV; s += 64)
+        if (par[s] && pend[s] == 0) fin[s] = 0;
     wave_sync();
+    uint32_t gmk = 0;
     for (uint32_t round = 0;; round++) {
       uint32_t wmin = kNotYet;
       for (int l = lane; l < E; l += 64) {
-        const uint32_t b = lbase[l], n = lhead[l], F = lfree[l];
-        uint32_t cs = kNotYet, cq = 0, bp = ~0u, bs = ~0u;
-        uint64_t bk = ~0ull;
-        for (uint32_t q = 0; q < n; q++) {
-          const uint32_t ent = chain[b + q];
-          const uint32_t r = ready_of(ent, push);
-          if (r == kNotYet) continue;
-          const uint32_t sl = ent & 0xFFFFu, st = max(F, r);
-          const uint64_t k = key[sl];
-          const uint32_t p = prio[sl];
-          if (st < cs || (st == cs && (k < bk || (k == bk && (p < bp || (p == bp && sl < bs)))))) {
-            cs = st;
-            cq = q;
-            bk = k;
-            bp = p;
-            bs = sl;
-          }
-        }
-        gst[l] = cs;
-        gfirst[l] = cq;
-        wmin = min(wmin, cs);
+        const GreedyLink lk{lfree[l], lbase[l], lhead[l]};
+        const GreedyBest b =
+            push ? greedy_scan_link<true>(lk, cv, fin) : greedy_scan_link<false>(lk, cv, fin);
+        gst[l] = greedy_start(b);
+        gfirst[l] = b.w2;
+        wmin = min(wmin, gst[l]);
       }
       wmin = ~wave_reduce_max(~wmin);
       if (wmin == kNotYet) break;
       if (round > total) return true;  // unreachable: every window serves a send
       const uint64_t wend = (uint64_t)wmin + a.cmin;
       wave_sync();
+      bool lost = false;
       for (int l = lane; l < E; l += 64) {
         const uint32_t cs = gst[l];
         if (cs == kNotYet || (uint64_t)cs >= wend) continue;
-        const uint32_t b = lbase[l], n = lhead[l], cq = gfirst[l];
-        const uint32_t ent = chain[b + cq];
-        const uint32_t f = cs + s_cost[l];
-        publish(ent & 0xFFFFu, f, l, push);
-        lfree[l] = f;
-        if (!mirror) mk = max(mk, f);
-        chain[b + cq] = chain[b + n - 1];
-        chain[b + n - 1] = ent;
-        lhead[l] = n - 1;
+        GreedyLink lk{lfree[l], lbase[l], lhead[l]};
+        const GreedyBest b{(uint64_t)cs << 32, 0, gfirst[l]};
+        lost |= push ? greedy_commit<true, LdsAtomics>(lk, b, s_cost[l], cv, fin, rdy, pend, gmk)
+                     : greedy_commit<false, LdsAtomics>(lk, b, s_cost[l], cv, fin, rdy, pend, gmk);
+        lfree[l] = lk.free;
+        lhead[l] = lk.len;
       }
+      if (__ballot(lost)) return true;  // unreachable: the index is the winner's
       wave_sync();
     }
+    if (!mirror) mk = max(mk, gmk);
     bool left = false;  // a send that never became ready: unreachable
     for (int l = lane; l < E; l += 64) left |= lhead[l] != 0;
     if (__ballot(left)) return true;
@@ -1272,12 +1291,6 @@ constexpr int kGreedyLinkSlots = 4;  // links per lane: at most 256 links
 // fault if it ever differs. The scan of one link and the commit of its
 // winner are plain functions of one lane's data (greedy_window.h), which a
 // host build also runs.
-// Several lanes of a window may push into the same send's ready time.
-struct LdsAtomics {
-  __device__ static void max_into(uint32_t *p, uint32_t v) { atomicMax(p, v); }
-  __device__ static uint32_t decrement(uint32_t *p) { return atomicSub(p, 1u); }
-  __device__ static uint32_t load(uint32_t *p) { return lds_get(p); }
-};
 
 template <bool kRS>
 __device__ __forceinline__ void greedy_windows(int E, int lane, int nslots, uint32_t cmin,
@@ -1298,7 +1311,7 @@ __device__ __forceinline__ void greedy_windows(int E, int lane, int nslots, uint
     uint32_t wmin = kGreedyNone;
 #pragma unroll
     for (int t = 0; t < kGreedyLinkSlots; t++) {
-      best[t] = greedy_scan_link<kRS>(lk[t], grec, gfin, grdy, gpend);
+      best[t] = greedy_scan_link<kRS>(lk[t], RecArray<uint4>{grec}, gfin);
       wmin = min(wmin, greedy_start(best[t]));
     }
     wmin = ~wave_reduce_max(~wmin);
@@ -1313,7 +1326,8 @@ __device__ __forceinline__ void greedy_windows(int E, int lane, int nslots, uint
     for (int t = 0; t < kGreedyLinkSlots; t++) {
       const int l = lane + 64 * t;
       if (greedy_start(best[t]) != kGreedyNone && (uint64_t)greedy_start(best[t]) < wend)
-        fault |= greedy_commit<kRS, LdsAtomics>(lk[t], best[t], s_cost[l], grec, gfin, grdy, gpend,
+        fault |= greedy_commit<kRS, LdsAtomics>(lk[t], best[t], s_cost[l], RecArray<uint4>{grec},
+                                                gfin, grdy, gpend,
                                                 mk);
     }
     wave_sync();

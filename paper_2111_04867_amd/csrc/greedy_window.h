@@ -43,19 +43,33 @@ __host__ __device__ inline uint32_t greedy_start(const GreedyBest &b) {
   return b.w2 != kGreedyNone ? (uint32_t)(b.w0 >> 32) : kGreedyNone;
 }
 
+// Pending-send lists seen through a view: get(i) returns the record at list
+// position i ({key lo, key hi, priority, slot | other slot << 16}) and
+// swap(i, j) exchanges two positions. RecArray keeps the records
+// themselves; other layouts build them from their own arrays.
+template <class Rec>
+struct RecArray {
+  Rec *p;
+  __host__ __device__ Rec get(uint32_t i) const { return p[i]; }
+  __host__ __device__ void swap(uint32_t i, uint32_t j) const {
+    const Rec t = p[i];
+    p[i] = p[j];
+    p[j] = t;
+  }
+};
+
 // The best ready send among the link's pending records, two records a step
 // (their loads, then their ready times, then the comparisons).
-template <bool kRS, class Rec>
-__host__ __device__ inline GreedyBest greedy_scan_link(const GreedyLink &lk, const Rec *grec,
-                                                       const uint32_t *gfin, const uint32_t *grdy,
-                                                       const uint32_t *gpend) {
+template <bool kRS, class View>
+__host__ __device__ inline GreedyBest greedy_scan_link(const GreedyLink &lk, const View &grec,
+                                                       const uint32_t *gfin) {
   GreedyBest b{~0ull, ~0ull, kGreedyNone};
   for (uint32_t q0 = 0; q0 < lk.len; q0 += 2) {
-    Rec rc[2];
+    decltype(grec.get(0)) rc[2];
     uint32_t r[2];
     for (int u = 0; u < 2; u++) {
       const uint32_t q = q0 + u < lk.len ? q0 + u : lk.len - 1;
-      rc[u] = grec[lk.base + q];
+      rc[u] = grec.get(lk.base + q);
     }
     for (int u = 0; u < 2; u++) {
       const uint32_t x = rc[u].w & 0xFFFFu, other = rc[u].w >> 16;
@@ -88,12 +102,12 @@ __host__ __device__ inline GreedyBest greedy_scan_link(const GreedyLink &lk, con
 // to the end of the pending part, so a list ends in reverse service order.
 // Returns true if the record at the winner's index is not the winner (never
 // the case; reported as a fault).
-template <bool kRS, class Ops, class Rec>
+template <bool kRS, class Ops, class View>
 __host__ __device__ inline bool greedy_commit(GreedyLink &lk, const GreedyBest &b, uint32_t cost,
-                                              Rec *grec, uint32_t *gfin, uint32_t *grdy,
+                                              const View &grec, uint32_t *gfin, uint32_t *grdy,
                                               uint32_t *gpend, uint32_t &mk) {
   const uint32_t cs = (uint32_t)(b.w0 >> 32), cq = b.w2 & 0xFFFFu;
-  const Rec rc = grec[lk.base + cq];
+  const auto rc = grec.get(lk.base + cq);
   const uint32_t x = rc.w & 0xFFFFu;
   const bool lost = x != (b.w2 >> 16);
   const uint32_t f = cs + cost;
@@ -107,8 +121,7 @@ __host__ __device__ inline bool greedy_commit(GreedyLink &lk, const GreedyBest &
   gfin[x] = f;
   lk.free = f;
   mk = mk > f ? mk : f;
-  grec[lk.base + cq] = grec[lk.base + lk.len - 1];
-  grec[lk.base + lk.len - 1] = rc;
+  grec.swap(lk.base + cq, lk.base + lk.len - 1);
   lk.len--;
   return lost;
 }

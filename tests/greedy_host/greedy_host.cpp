@@ -56,10 +56,11 @@ int main() {
   uint32_t mk = 0;
   bool fault = false;
   std::vector<GreedyBest> best(lk.size());
+  const taccl::RecArray<uint4> view{grec.data()};
   for (uint32_t round = 0;; round++) {
     uint32_t wmin = kGreedyNone;
     for (size_t k = 0; k < lk.size(); k++) {
-      best[k] = taccl::greedy_scan_link<false>(lk[k], grec.data(), gfin.data(), nullptr, nullptr);
+      best[k] = taccl::greedy_scan_link<false>(lk[k], view, gfin.data());
       const uint32_t st = taccl::greedy_start(best[k]);
       wmin = st < wmin ? st : wmin;
     }
@@ -75,8 +76,7 @@ int main() {
         const uint32_t st = taccl::greedy_start(best[k]);
         if (st != kGreedyNone && (uint64_t)st < wend)
           fault |= taccl::greedy_commit<false, Plain>(lk[k], best[k], cost[lane + kLanes * t],
-                                                      grec.data(), gfin.data(), nullptr, nullptr,
-                                                      mk);
+                                                      view, gfin.data(), nullptr, nullptr, mk);
       }
   }
   if (fault) return 3;
