@@ -24,6 +24,8 @@ namespace taccl {
 
 namespace {
 
+constexpr uint32_t kNoOption = 0xFFFFFFFFu;  // a chunk without a send
+
 __device__ __forceinline__ uint32_t wave_max(uint32_t v) {
   for (int o = 32; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o));
   return v;
@@ -70,6 +72,22 @@ __device__ __forceinline__ void lds_put(uint32_t *p, uint32_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
+// Rank of entry me among the entries [b, e) of its class, four at a time
+// (the staging array has three spare entries past its end; entries past the
+// class never count).
+__device__ __forceinline__ uint32_t rank_in_class(const uint64_t *e64, uint32_t b, uint32_t e,
+                                                  uint64_t me) {
+  uint32_t rank = 0;
+  for (uint32_t y = b; y < e; y += 4) {
+    uint64_t m[4];
+#pragma unroll
+    for (int t = 0; t < 4; t++) m[t] = e64[y + t];
+#pragma unroll
+    for (int t = 0; t < 4; t++) rank += (uint32_t)((y + t < e) & (m[t] < me));
+  }
+  return rank;
+}
+
 // Switch ports, one level (App. B.3 switch constraints): a switched send
 // holds its send port (its class's link, already ordered in `sorted`) and
 // its receive port (the downlink), each port serving its sends in Step-2
@@ -86,14 +104,15 @@ __device__ uint32_t ports_level(const PathArgs &a, int L, const uint32_t *gpr, u
   extern __shared__ __align__(16) unsigned char lds[];
   uint32_t *ccnt2 = (uint32_t *)(lds + a.o_ccnt2);
   uint32_t *ccur2 = (uint32_t *)(lds + a.o_ccur2);
-  uint16_t *echunk2 = (uint16_t *)(lds + a.o_echunk2);
-  uint32_t *eprio2 = (uint32_t *)(lds + a.o_eprio2);
-  uint16_t *ecls2 = (uint16_t *)(lds + a.o_ecls2);
+  // the send order is sorted, so its class staging serves the receive-port
+  // order: priority << 32 | chunk per scattered send, and its class
+  uint64_t *e64 = (uint64_t *)(lds + a.o_e64);
+  uint16_t *ecls2 = (uint16_t *)(lds + a.o_ecls);
   uint16_t *sorted2 = (uint16_t *)(lds + a.o_sorted2);
   uint32_t *fcur = (uint32_t *)(lds + a.o_fcur);
   uint16_t *pd = (uint16_t *)(lds + a.o_pd);  // send before it on its receive port
   uint16_t *dl = (uint16_t *)(lds + a.o_dl);  // its receive port (downlink)
-  const uint8_t *rt = lds + a.o_rt;
+  const uint32_t *qc = (const uint32_t *)(lds + a.o_qc);
   const int tid = threadIdx.x, nt = blockDim.x;
   const int C = a.C, P = a.P, E = a.E, nlev = a.nlev;
   const uint32_t lo = a.lvl_cls_begin[L], lo2 = a.lvl_cls2_begin[L];
@@ -106,13 +125,8 @@ __device__ uint32_t ports_level(const PathArgs &a, int L, const uint32_t *gpr, u
   __syncthreads();
   // the chunk's send at this level: route option q, first hop h
   auto unit = [&](int c, uint32_t &q, int &h) {
-    const int pair = c / a.cpr;
-    const int s = pair / P, d = pair % P;
-    if (s == d) return false;
-    const int pp = s * P + d;
-    const int k = rt[c];
-    if (k >= a.npaths[pp]) return false;
-    q = a.pair_base[pp] + k;
+    q = qc[c];
+    if (q == kNoOption) return false;
     h = a.path_lvl_hop[(size_t)q * nlev + L];
     return h >= 0;
   };
@@ -134,22 +148,16 @@ __device__ uint32_t ports_level(const PathArgs &a, int L, const uint32_t *gpr, u
     const uint32_t k2 = a.hop_class2[a.path_off[q] + h];
     if (k2 == 0xFFFF) continue;
     const uint32_t slot = atomicAdd(&ccur2[k2 - lo2], 1u);
-    echunk2[slot] = (uint16_t)c;
+    e64[slot] = ((uint64_t)gpr[(size_t)c * a.H + h] << 32) | (uint32_t)c;
     ecls2[slot] = (uint16_t)(k2 - lo2);
-    eprio2[slot] = gpr[(size_t)c * a.H + h];
   }
   __syncthreads();
   const uint32_t tot2 = ccnt2[ncl2];
   for (uint32_t x = tid; x < tot2; x += nt) {
     const int k = ecls2[x];
-    const uint32_t b = ccnt2[k], e = ccnt2[k + 1];
-    const uint32_t px = eprio2[x], cx = echunk2[x];
-    uint32_t rank = 0;
-    for (uint32_t y = b; y < e; y++) {
-      const uint32_t py = eprio2[y], cy = echunk2[y];
-      rank += (py < px) || (py == px && cy < cx);
-    }
-    sorted2[b + rank] = (uint16_t)cx;
+    const uint32_t cx = (uint32_t)e64[x] & 0xFFFFu;
+    const uint32_t b = ccnt2[k];
+    sorted2[b + rank_in_class(e64, b, ccnt2[k + 1], e64[x])] = (uint16_t)cx;
     dl[cx] = a.cls2_link[lo2 + k];
   }
   __syncthreads();
@@ -175,7 +183,7 @@ __device__ uint32_t ports_level(const PathArgs &a, int L, const uint32_t *gpr, u
   // port << 16, and its ready time without that send (the receive port's
   // busy time folded in for the first send on a port); the send-order and
   // receive-port staging arrays are dead
-  uint32_t *wcp = eprio2, *wr0 = (uint32_t *)(lds + a.o_eprio);
+  uint32_t *wcp = (uint32_t *)e64, *wr0 = wcp + a.max_lvl;
   for (uint32_t x = tid; x < tot; x += nt) {
     const uint32_t c = sorted[x], d = dl[c];
     const uint32_t pj = d != 0xFFFFu ? (uint32_t)pd[c] : 0xFFFFu;
@@ -270,13 +278,16 @@ __device__ uint32_t ports_level(const PathArgs &a, int L, const uint32_t *gpr, u
 template <int NT>
 __global__ __launch_bounds__(NT) void path_eval_kernel(PathArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
-  uint8_t *rt = lds + a.o_rt;
+  // per chunk: its chosen route option (an index into the path tables), or
+  // kNoOption when it has no send (its own rank, or left unrouted)
+  uint32_t *qc = (uint32_t *)(lds + a.o_qc);
   uint32_t *ctime = (uint32_t *)(lds + a.o_ctime);  // chunk's arrival so far
   uint32_t *lfree = (uint32_t *)(lds + a.o_lfree);
   uint32_t *ccnt = (uint32_t *)(lds + a.o_ccnt);
   uint32_t *ccur = (uint32_t *)(lds + a.o_ccur);
-  uint16_t *echunk = (uint16_t *)(lds + a.o_echunk);
-  uint32_t *eprio = (uint32_t *)(lds + a.o_eprio);
+  // per scattered send: priority << 32 | chunk (ascending = the Step-2 tie
+  // order), and its class
+  uint64_t *e64 = (uint64_t *)(lds + a.o_e64);
   uint16_t *ecls = (uint16_t *)(lds + a.o_ecls);
   uint16_t *sorted = (uint16_t *)(lds + a.o_sorted);
   uint32_t *red = (uint32_t *)(lds + a.o_red);
@@ -289,12 +300,17 @@ __global__ __launch_bounds__(NT) void path_eval_kernel(PathArgs a) {
     const uint32_t *gpr = a.prio + (size_t)i * a.prio_stride;
     bool unrouted = false;
     for (int c = tid; c < C; c += nt) {
-      const uint8_t k = grt[c];
-      rt[c] = k;
+      const uint32_t k = grt[c];
       ctime[c] = 0;
       const int pair = c / a.cpr;
       const int s = pair / P, d = pair % P;
-      if (s != d && k >= a.npaths[s * P + d]) unrouted = true;
+      uint32_t q = kNoOption;
+      if (s != d) {
+        const int pp = s * P + d;
+        if (k < a.npaths[pp]) q = a.pair_base[pp] + k;
+        else unrouted = true;
+      }
+      qc[c] = q;
     }
     for (int l = tid; l < E; l += nt) lfree[l] = 0;
     const bool any_unrouted = __syncthreads_or(unrouted);
@@ -308,34 +324,25 @@ __global__ __launch_bounds__(NT) void path_eval_kernel(PathArgs a) {
       __syncthreads();
       // count the level's sends per class
       for (int c = tid; c < C; c += nt) {
-        const int pair = c / a.cpr;
-        const int s = pair / P, d = pair % P;
-        if (s == d) continue;
-        const int pp = s * P + d;
-        const int k = rt[c];
-        if (k >= a.npaths[pp]) continue;
-        const uint32_t q = a.pair_base[pp] + k;
+        const uint32_t q = qc[c];
+        if (q == kNoOption) continue;
         const int h = a.path_lvl_hop[(size_t)q * nlev + L];
+        const uint32_t po = a.path_off[q];
         if (h < 0) continue;
-        atomicAdd(&ccnt[a.hop_class[a.path_off[q] + h] - lo], 1u);
+        atomicAdd(&ccnt[a.hop_class[po + h] - lo], 1u);
       }
       __syncthreads();
       block_scan(ccnt, ccur, ncl, red);
       // scatter into classes (arbitrary order inside a class)
       for (int c = tid; c < C; c += nt) {
-        const int pair = c / a.cpr;
-        const int s = pair / P, d = pair % P;
-        if (s == d) continue;
-        const int pp = s * P + d;
-        const int k = rt[c];
-        if (k >= a.npaths[pp]) continue;
-        const uint32_t q = a.pair_base[pp] + k;
+        const uint32_t q = qc[c];
+        if (q == kNoOption) continue;
         const int h = a.path_lvl_hop[(size_t)q * nlev + L];
+        const uint32_t po = a.path_off[q];
         if (h < 0) continue;
-        const int cls = a.hop_class[a.path_off[q] + h] - lo;
+        const int cls = a.hop_class[po + h] - lo;
         const uint32_t slot = atomicAdd(&ccur[cls], 1u);
-        echunk[slot] = (uint16_t)c;
-        eprio[slot] = gpr[(size_t)c * a.H + h];
+        e64[slot] = ((uint64_t)gpr[(size_t)c * a.H + h] << 32) | (uint32_t)c;
         ecls[slot] = (uint16_t)cls;
       }
       __syncthreads();
@@ -343,14 +350,8 @@ __global__ __launch_bounds__(NT) void path_eval_kernel(PathArgs a) {
       const uint32_t tot = ccnt[ncl];
       for (uint32_t x = tid; x < tot; x += nt) {
         const int k = ecls[x];
-        const uint32_t b = ccnt[k], e = ccnt[k + 1];
-        const uint32_t px = eprio[x], cx = echunk[x];
-        uint32_t rank = 0;
-        for (uint32_t y = b; y < e; y++) {
-          const uint32_t py = eprio[y], cy = echunk[y];
-          rank += (py < px) || (py == px && cy < cx);
-        }
-        sorted[b + rank] = (uint16_t)cx;
+        const uint32_t b = ccnt[k];
+        sorted[b + rank_in_class(e64, b, ccnt[k + 1], e64[x])] = (uint16_t)e64[x];
       }
       __syncthreads();
       if (a.ports) {
@@ -427,23 +428,20 @@ int32_t path_layout(const taccl_plan &p, PathArgs &a) {
     off = align16(off + bytes);
     return o;
   };
-  a.o_rt = take(C);
+  a.o_qc = take(4 * C);
   a.o_ctime = take(4 * C);
   a.o_lfree = take(4 * E);
   a.o_ccnt = take(4 * (K + 1));
   a.o_ccur = take(4 * K);
-  a.o_echunk = take(2 * M);
-  a.o_eprio = take(4 * M);
+  a.o_e64 = take(8 * (M + 3));
   a.o_ecls = take(2 * M);
   a.o_sorted = take(2 * M);
+  a.max_lvl = M;
   a.o_red = take(4 * (kPathPortThreads / 64));
   if (p.ports) {  // receive-port order and per-chunk state
     const int32_t K2 = std::max(p.max_lvl_cls2, 1);
     a.o_ccnt2 = take(4 * (K2 + 1));
     a.o_ccur2 = take(4 * K2);
-    a.o_echunk2 = take(2 * M);
-    a.o_eprio2 = take(4 * M);
-    a.o_ecls2 = take(2 * M);
     a.o_sorted2 = take(2 * M);
     a.o_fcur = take(4 * C);
     a.o_pd = take(2 * C);

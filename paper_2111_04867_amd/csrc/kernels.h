@@ -86,7 +86,7 @@ struct PathArgs {
   uint32_t *makespan;
   uint8_t *valid;
   int64_t n;
-  int32_t o_rt, o_ctime, o_lfree, o_ccnt, o_ccur, o_echunk, o_eprio, o_ecls, o_sorted, o_red;
+  int32_t o_qc, o_ctime, o_lfree, o_ccnt, o_ccur, o_e64, o_ecls, o_sorted, o_red, max_lvl;
   // register-resident kernel
   int32_t ncls;
   const uint32_t *arec, *cpath, *cinfo, *cbkt;
@@ -104,7 +104,7 @@ struct PathArgs {
   int32_t ports;
   const uint16_t *hop_class2, *cls2_link;
   const uint32_t *lvl_cls2_begin, *llc2;
-  int32_t o_ccnt2, o_ccur2, o_echunk2, o_eprio2, o_ecls2, o_sorted2, o_fcur, o_pd, o_dl;
+  int32_t o_ccnt2, o_ccur2, o_sorted2, o_fcur, o_pd, o_dl;
   int32_t lr_threads;  // block size of the LDS-record kernel for this plan
 };
 
