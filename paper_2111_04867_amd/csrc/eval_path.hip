@@ -114,7 +114,7 @@ __device__ uint32_t ports_level(const PathArgs &a, int L, const uint32_t *gpr, u
   uint16_t *dl = (uint16_t *)(lds + a.o_dl);  // its receive port (downlink)
   const uint32_t *qc = (const uint32_t *)(lds + a.o_qc);
   const int tid = threadIdx.x, nt = blockDim.x;
-  const int C = a.C, P = a.P, E = a.E, nlev = a.nlev;
+  const int C = a.C, E = a.E, nlev = a.nlev;
   const uint32_t lo = a.lvl_cls_begin[L], lo2 = a.lvl_cls2_begin[L];
   const int ncl2 = (int)(a.lvl_cls2_begin[L + 1] - lo2);
   for (int j = tid; j <= ncl2; j += nt) ccnt2[j] = 0;
