@@ -79,7 +79,10 @@ def run(harness, w, ref, routes, prio, multicast):
     cmin = min(cost)
     blob = struct.pack(f"<4I{w.E}I{w.E + 1}I", w.E, nslots, cmin, len(flat), *cost, *gofs)
     blob += b"".join(struct.pack("<4I", *r) for r in flat)
-    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:abort_on_error=1",
+    # the harness carries its own sanitizer runtime: drop a preloaded one
+    # (the sanitizer leg of the CPU suite preloads clang's into this process)
+    env = {k: v for k, v in os.environ.items() if k != "LD_PRELOAD"}
+    env.update(ASAN_OPTIONS="detect_leaks=0:abort_on_error=1",
                UBSAN_OPTIONS="halt_on_error=1:print_stacktrace=1")
     out = subprocess.run([harness], input=blob, capture_output=True, env=env)
     assert out.returncode == 0, out.stderr.decode()[-2000:]
