@@ -192,6 +192,20 @@ def test_alltoall_block_kernel_two_word_keys(order):
 
 
 @pytest.mark.parametrize("order", [1, 2])
+def test_alltoall_block_kernel_unstaged_priorities(order):
+    """Two chunks per pair on the four-node plan: more sends than the block
+    kernel stages in LDS (it stages a candidate's priorities while two blocks
+    still fit a CU), so the priorities are read hop by hop."""
+    w = replace(cf.fournode64_a2a(n_candidates=4), chunks_per_rank=2)
+    w = cf.with_greedy(w) if order == 1 else cf.with_reverse_greedy(w)
+    plan, ref, opts = plans(w)
+    assert plan.num_chunks == 8192 and 4 * plan.info["max_sends"] > 80 * 1024
+    routes, prio = generate(w.seed + 15, 0, 4, opts, plan.prio_stride)
+    prio[:, ::7] = 3
+    check(plan, ref, routes, prio, f"fournode64 cpr=2 alltoall greedy order={order}")
+
+
+@pytest.mark.parametrize("order", [1, 2])
 def test_alltoall_block_kernel_eight_chunks_per_thread(order):
     """8192 chunks: the block kernel's largest shape (8 chunks per thread)."""
     edges = [(u, v, 700, 8) for u in range(64) for v in range(64) if u != v]
