@@ -251,14 +251,16 @@ taccl_status_t taccl_plan_upload(taccl_plan_t plan);
  * refuses plans whose worst case, the sum of all send costs over both
  * phases of an Allreduce, could reach it). A candidate whose evaluation
  * exceeded a bound the kernel relies on (a round limit of an iterative
- * schedule, a layer index past the plan's bound; none is reachable for a
- * plan that taccl_sketch_apply accepted) comes back as makespan ==
+ * schedule, a layer index past the plan's bound, a switch-port walk that
+ * stops making progress; none is reachable for a plan that
+ * taccl_sketch_apply accepted) comes back as makespan ==
  * TACCL_MAKESPAN_FAULT with valid == 0, so such an internal fault is never
  * mistaken for a bad candidate; taccl_count_faults counts them.
  * Errors (synchronous): INVALID_ARGUMENT for null pointers with n > 0,
  * n < 0 or a misaligned d_prio; UNSUPPORTED when a candidate's state does
- * not fit one block's LDS or an Alltoall greedy plan exceeds its limits;
- * HIP if the plan upload or the launch fails.
+ * not fit one block's LDS, an Alltoall greedy plan exceeds its limits, or a
+ * switch-port plan has more than four links per thread of its block; HIP if
+ * the plan upload or the launch fails.
  * Faults inside the kernel surface at the caller's next synchronisation.
  * n == 0 is a no-op.
  */
