@@ -5,9 +5,12 @@
 // arrange them. Built for the host only, under AddressSanitizer and
 // UndefinedBehaviorSanitizer.
 //
-// stdin (little-endian u32): E, nslots, cmin, n_records, cost[E],
-// gofs[E + 1], records[n_records][4]. stdout: makespan, then the finish
-// time of every slot (kGreedyNone for a slot without a send), one a line.
+// stdin (little-endian u32): E, nslots, cmin, n_records, push, cost[E],
+// gofs[E + 1], records[n_records][4]. push = 0: the pull form (a record's
+// other slot is the send the chunk arrives by); push = 1: the push form (a
+// send waits for every send whose other slot is its own, as in a
+// ReduceScatter). stdout: makespan, then the finish time of every slot
+// (kGreedyNone for a slot without a send), one a line.
 #include <cstdio>
 #include <vector>
 
@@ -30,9 +33,10 @@ bool read_u32(uint32_t *out, size_t n) { return fread(out, 4, n, stdin) == n; }
 }  // namespace
 
 int main() {
-  uint32_t hdr[4];
-  if (!read_u32(hdr, 4)) return 2;
+  uint32_t hdr[5];
+  if (!read_u32(hdr, 5)) return 2;
   const uint32_t E = hdr[0], nslots = hdr[1], cmin = hdr[2], nrec = hdr[3];
+  const bool push = hdr[4] != 0;
   constexpr int kLanes = 64, kSlots = 4;  // a wavefront, four links per lane
   if (E > (uint32_t)kLanes * kSlots || nslots > 65535) return 2;
   std::vector<uint32_t> cost(E), gofs(E + 1);
@@ -44,6 +48,23 @@ int main() {
     grec[r] = make_uint4(w[0], w[1], w[2], w[3]);
   }
   std::vector<uint32_t> gfin(nslots > 0 ? nslots : 1, kGreedyNone);
+  // push form: inputs per send, the latest input finish, and a send without
+  // inputs ready at 0
+  std::vector<uint32_t> gpend(gfin.size(), 0), grdy(gfin.size(), 0);
+  if (push) {
+    for (const uint4 &r : grec) {
+      const uint32_t other = r.w >> 16;
+      if (other != taccl::kGreedyNoPred) {
+        if (other >= nslots) return 2;
+        gpend[other]++;
+      }
+    }
+    for (const uint4 &r : grec) {
+      const uint32_t x = r.w & 0xFFFFu;
+      if (x >= nslots) return 2;
+      if (gpend[x] == 0) gfin[x] = 0;
+    }
+  }
   std::vector<GreedyLink> lk((size_t)kLanes * kSlots);
   for (int lane = 0; lane < kLanes; lane++)
     for (int t = 0; t < kSlots; t++) {
@@ -60,7 +81,8 @@ int main() {
   for (uint32_t round = 0;; round++) {
     uint32_t wmin = kGreedyNone;
     for (size_t k = 0; k < lk.size(); k++) {
-      best[k] = taccl::greedy_scan_link<false>(lk[k], view, gfin.data());
+      best[k] = push ? taccl::greedy_scan_link<true>(lk[k], view, gfin.data())
+                     : taccl::greedy_scan_link<false>(lk[k], view, gfin.data());
       const uint32_t st = taccl::greedy_start(best[k]);
       wmin = st < wmin ? st : wmin;
     }
@@ -75,8 +97,12 @@ int main() {
         const size_t k = (size_t)lane * kSlots + t;
         const uint32_t st = taccl::greedy_start(best[k]);
         if (st != kGreedyNone && (uint64_t)st < wend)
-          fault |= taccl::greedy_commit<false, Plain>(lk[k], best[k], cost[lane + kLanes * t],
-                                                      view, gfin.data(), nullptr, nullptr, mk);
+          fault |= push ? taccl::greedy_commit<true, Plain>(lk[k], best[k], cost[lane + kLanes * t],
+                                                            view, gfin.data(), grdy.data(),
+                                                            gpend.data(), mk)
+                        : taccl::greedy_commit<false, Plain>(lk[k], best[k],
+                                                             cost[lane + kLanes * t], view,
+                                                             gfin.data(), nullptr, nullptr, mk);
       }
   }
   if (fault) return 3;

@@ -44,8 +44,10 @@ def harness(tmp_path_factory):
     return exe
 
 
-def records(w, ref, sends, multicast):
-    """Per-link record lists as the greedy kernels build them."""
+def records(w, ref, sends, multicast, push=False):
+    """Per-link record lists as the greedy kernels build them (push: a
+    ReduceScatter, whose send out of v carries the partial on to the send
+    out of its parent u)."""
     P, V = w.P, w.V
     cpr = w.chunks_per_rank
     H = ref.max_hops
@@ -55,7 +57,11 @@ def records(w, ref, sends, multicast):
     n = len(sends["chunk"])
     for i in range(n):
         c, l, u, v = (int(sends[k][i]) for k in ("chunk", "link", "from", "to"))
-        if multicast:
+        if multicast and push:
+            o = c // cpr
+            slot = c * V + u
+            pred = NOPRED if v == o else c * V + v
+        elif multicast:
             o = c // cpr
             slot = c * V + v
             pred = NOPRED if u == o else c * V + u
@@ -72,12 +78,13 @@ def records(w, ref, sends, multicast):
     return nslots, gofs, flat, slot_of
 
 
-def run(harness, w, ref, routes, prio, multicast):
+def run(harness, w, ref, routes, prio, multicast, push=False):
     mk, ok, sends = ref.eval_detail(routes, prio)
-    nslots, gofs, flat, slot_of = records(w, ref, sends, multicast)
+    nslots, gofs, flat, slot_of = records(w, ref, sends, multicast, push)
     cost = [ref.link_cost(e) for e in range(w.E)]
     cmin = min(cost)
-    blob = struct.pack(f"<4I{w.E}I{w.E + 1}I", w.E, nslots, cmin, len(flat), *cost, *gofs)
+    blob = struct.pack(f"<5I{w.E}I{w.E + 1}I", w.E, nslots, cmin, len(flat), int(push), *cost,
+                       *gofs)
     blob += b"".join(struct.pack("<4I", *r) for r in flat)
     # the harness carries its own sanitizer runtime: drop a preloaded one
     # (the sanitizer leg of the CPU suite preloads clang's into this process)
@@ -94,18 +101,25 @@ def run(harness, w, ref, routes, prio, multicast):
     return mk
 
 
-@pytest.mark.parametrize("make,n,multicast", [
-    (lambda: cf.with_greedy(cf.cubemesh8_ag()), 40, True),
-    (lambda: cf.with_greedy(cf.twonode16_ag()), 6, True),
-    (lambda: cf.with_greedy(cf.full_ag(6, k=3, chunks_per_rank=2)), 20, True),
-    (lambda: cf.with_greedy(cf.switch16_a2a()), 4, False),
-    (lambda: cf.with_greedy(cf.full_a2a(5)), 20, False),
+def rs(w):
+    return cf.as_reduction(w, cf.REDUCESCATTER)
+
+
+@pytest.mark.parametrize("make,n,multicast,push", [
+    (lambda: cf.with_greedy(cf.cubemesh8_ag()), 40, True, False),
+    (lambda: cf.with_greedy(cf.twonode16_ag()), 6, True, False),
+    (lambda: cf.with_greedy(cf.full_ag(6, k=3, chunks_per_rank=2)), 20, True, False),
+    (lambda: cf.with_greedy(cf.switch16_a2a()), 4, False, False),
+    (lambda: cf.with_greedy(cf.full_a2a(5)), 20, False, False),
+    (lambda: cf.with_greedy(rs(cf.cubemesh8_ag())), 40, True, True),
+    (lambda: cf.with_greedy(rs(cf.twonode16_ag())), 6, True, True),
+    (lambda: cf.with_greedy(rs(cf.full_ag(6, k=3, chunks_per_rank=2))), 20, True, True),
 ])
-def test_window_steps_match_the_oracle(harness, make, n, multicast):
+def test_window_steps_match_the_oracle(harness, make, n, multicast, push):
     w = make()
     ref = OraclePlan.from_workload(w)
     assert ref.order == 1
     routes, prio = generate(w.seed + 41, 0, n, ref.route_options(), ref.prio_stride)
     prio[1::3] = 7  # equal priorities: the slot breaks the tie
-    spans = [run(harness, w, ref, routes[i], prio[i], multicast) for i in range(n)]
+    spans = [run(harness, w, ref, routes[i], prio[i], multicast, push) for i in range(n)]
     assert len(set(spans)) > 1 or n < 4
