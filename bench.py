@@ -228,6 +228,8 @@ def main():
     ap.add_argument("--no-all", action="store_true", help="skip the per-workload table")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run device-to-device copies of BYTES (counter calibration)")
+    ap.add_argument("--calibrate-read", type=int, default=0, metavar="BYTES",
+                    help="only run sums over BYTES of int32 (a second, read-only pattern)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("this evaluator runs on one GPU; candidates shard trivially across GPUs but no "
@@ -243,6 +245,14 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": args.calibrate_copy, "copies": args.steps}))
+        return
+    if args.calibrate_read:
+        src = torch.ones(args.calibrate_read // 4, dtype=torch.int32, device="cuda")
+        total = 0
+        for _ in range(args.steps):
+            total += int(src.sum().item())
+        print(json.dumps({"calibrate_read_bytes": args.calibrate_read, "sums": args.steps,
+                          "checksum": total}))
         return
     from workloads import (CONTIG_ORDER, GREEDY_LARGE_ORDER, GREEDY_ORDER, ORDER, PORTS_ORDER,
                            REDUCE_ORDER)
