@@ -57,12 +57,14 @@ __device__ __forceinline__ uint32_t div_m(uint32_t n, uint32_t mm) {
   return (uint32_t)(((uint64_t)n * mm) >> 32);
 }
 
-// The lane `Ctrl` selects through DPP, or v itself where there is none (an
-// out-of-row source or a row the mask leaves out), so max(v, dpp_or(v))
-// never mixes in a value from outside the pattern.
+// The larger of v and the value of the lane `Ctrl` selects through DPP; a
+// lane without one (an out-of-row source, or a row the mask leaves out)
+// keeps v (the DPP source reads as 0 there and every value is unsigned), so
+// no value from outside the pattern is mixed in. One v_max with a DPP
+// operand.
 template <int Ctrl, int RowMask = 0xf>
-__device__ __forceinline__ uint32_t dpp_or_self(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, Ctrl, RowMask, 0xf, false);
+__device__ __forceinline__ uint32_t max_dpp(uint32_t v) {
+  return max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, Ctrl, RowMask, 0xf, true));
 }
 
 // Route word j (route bytes of chunk j / PW) as one-hot option bytes:
@@ -464,19 +466,19 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
         {
           const bool c1 = kk >= 1;
           if (__ballot(c1)) {
-            const uint32_t t1 = max(v, dpp_or_self<kRowShr + 1>(v));
+            const uint32_t t1 = max_dpp<kRowShr + 1>(v);
             v = c1 ? t1 : v;
             const bool c2 = kk >= 2;
             if (__ballot(c2)) {
-              const uint32_t t2 = max(v, dpp_or_self<kRowShr + 2>(v));
+              const uint32_t t2 = max_dpp<kRowShr + 2>(v);
               v = c2 ? t2 : v;
               const bool c4 = kk >= 4;
               if (__ballot(c4)) {
-                const uint32_t t4 = max(v, dpp_or_self<kRowShr + 4>(v));
+                const uint32_t t4 = max_dpp<kRowShr + 4>(v);
                 v = c4 ? t4 : v;
                 const bool c8 = kk >= 8;
                 if (__ballot(c8)) {
-                  const uint32_t t8 = max(v, dpp_or_self<kRowShr + 8>(v));
+                  const uint32_t t8 = max_dpp<kRowShr + 8>(v);
                   v = c8 ? t8 : v;
                 }
               }
@@ -484,12 +486,12 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
             // runs that reach back across a row boundary
             const bool x15 = kk >= reach15;
             if (__ballot(x15)) {
-              const uint32_t t15 = max(v, dpp_or_self<kBcast15, 0xa>(v));
+              const uint32_t t15 = max_dpp<kBcast15, 0xa>(v);
               v = x15 ? t15 : v;
             }
             const bool x31 = kk >= reach31;
             if (__ballot(x31)) {
-              const uint32_t t31 = max(v, dpp_or_self<kBcast31, 0xc>(v));
+              const uint32_t t31 = max_dpp<kBcast31, 0xc>(v);
               v = x31 ? t31 : v;
             }
           }
