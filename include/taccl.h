@@ -156,7 +156,7 @@ void taccl_collective_destroy(taccl_collective_t coll);
  *     combined with contiguity (INVALID_ARGUMENT). On the GPU they are
  *     evaluated for every multicast
  *     plan (Allgather, explicit, ReduceScatter, Allreduce) and for Alltoall
- *     plans with at most 8192 chunks and 65535 send slots (chunks x longest
+ *     plans with at most 4096 chunks and 65535 send slots (chunks x longest
  *     route option) and no zero-cost link; larger Alltoall plans are
  *     refused at evaluation (UNSUPPORTED);
  *   switch_ports (Alltoall only): 0 = a switch vertex stores and forwards

@@ -10,6 +10,23 @@ LIB = os.path.join(PKG, "libtaccl.so")
 ARCH = "gfx950"
 
 
+def hip_flags():
+    """Flags of every HIP compile, the library's objects and the device
+    assembly alike. hipcc compiles every source as HIP; packed fp32 ops are
+    kept out of device code (the host pass warns that it does not know the
+    feature)."""
+    return ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall",
+            "-I" + os.path.join(ROOT, "include"), "-I" + CSRC,
+            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+
+
+def device_asm(src, out):
+    """Start compiling one source's device code to gfx950 assembly, as the
+    library compiles it; returns the process (stderr piped)."""
+    return subprocess.Popen(["hipcc"] + hip_flags() + ["--cuda-device-only", "-S", src, "-o", out],
+                            stderr=subprocess.PIPE, text=True)
+
+
 def build_library(verbose=False, jobs=8, only_changed=False, sanitize=False):
     """Compile every source (only_changed: skip sources whose object is newer
     than the source and every header, for quick rebuilds while editing).
@@ -21,8 +38,6 @@ def build_library(verbose=False, jobs=8, only_changed=False, sanitize=False):
     newest_header = max(os.path.getmtime(h) for h in headers)
     objdir = os.path.join(PKG, "_build", "san") if sanitize else os.path.join(PKG, "_build")
     os.makedirs(objdir, exist_ok=True)
-    common = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-I" + os.path.join(ROOT, "include"),
-              "-I" + CSRC]
     # host-only sanitizers: each -fsanitize= goes to the host pass alone
     san = (["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
             "-Xarch_host", "-fno-omit-frame-pointer", "-Xarch_host", "-fno-sanitize-recover=all"]
@@ -34,11 +49,7 @@ def build_library(verbose=False, jobs=8, only_changed=False, sanitize=False):
         if only_changed and os.path.exists(o) and \
                 os.path.getmtime(o) > max(os.path.getmtime(s), newest_header):
             continue
-        # hipcc compiles every source as HIP; keep packed fp32 ops out of
-        # device code (the host pass warns that it does not know the feature)
-        cmd = ["hipcc", "--offload-arch=" + ARCH] + common + san
-        cmd += ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
-        cmd += ["-c", s, "-o", o]
+        cmd = ["hipcc"] + hip_flags() + san + ["-c", s, "-o", o]
         if verbose:
             print(" ".join(cmd), flush=True)
         procs.append(subprocess.Popen(cmd, stderr=subprocess.PIPE, text=True))

@@ -152,7 +152,7 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     if (!wave && (path_greedy_block_layout(*p, g) <= 0 || g.block_bytes > t->max_lds))
       return fail(TACCL_ERR_UNSUPPORTED,
                   "time-aware greedy orders for Alltoall need at most 65535 send slots "
-                  "(chunks x longest path), 8192 chunks and no zero-cost link");
+                  "(chunks x longest path), 4096 chunks and no zero-cost link");
     g.mirror = p->greedy == 2;
     g.gkrank = t->gkrank;
     g.C = p->coll.C;

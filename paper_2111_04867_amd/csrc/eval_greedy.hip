@@ -48,8 +48,17 @@ constexpr uint32_t kNone = 0xFFFFFFFFu;
 
 int32_t align16(int32_t x) { return (x + 15) & ~15; }
 
+// Two 1024-thread blocks per CU (8 wavefronts per SIMD, 64 registers) for
+// one-word keys; two-word keys would spill there at 4 chunks per thread and
+// take up to 128 registers (one block per CU) instead.
+template <int CPT, bool kPack>
+constexpr int greedy_block_min_waves() {
+  return kPack && CPT <= 4 ? 8 : 4;
+}
+
 template <int CPT, int NT, bool kPack>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(8, 8))) void path_greedy_block(PathGreedyArgs a) {
+__global__ __launch_bounds__(NT) __attribute__((
+    amdgpu_waves_per_eu(greedy_block_min_waves<CPT, kPack>(), 8))) void path_greedy_block(PathGreedyArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int P = a.P, E = a.E, H = a.H;
@@ -322,8 +331,7 @@ const void *block_fn_p(int cpt) {
   switch (cpt) {
     case 1: return (const void *)path_greedy_block<1, NT, kPack>;
     case 2: return (const void *)path_greedy_block<2, NT, kPack>;
-    case 4: return (const void *)path_greedy_block<4, NT, kPack>;
-    default: return (const void *)path_greedy_block<8, NT, kPack>;
+    default: return (const void *)path_greedy_block<4, NT, kPack>;
   }
 }
 
@@ -348,7 +356,9 @@ int32_t path_greedy_block_layout(const taccl_plan &p, PathGreedyArgs &a) {
   if (cmin == 0) return 0;
   int cpt = 1;
   while (cpt * kGreedyBlockThreads < C) cpt *= 2;
-  if (cpt > 8) return 0;  // 1024 threads leave 128 registers per thread
+  // 1024 threads leave at most 128 registers per thread: more than 4
+  // chunks per thread would spill the per-chunk state
+  if (cpt > 4) return 0;
   a.cmin = cmin;
   a.nslots = C * H;
   a.cpt = cpt;

@@ -132,9 +132,10 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
   // Region A: one-hot routes, distances, ancestors and heights per slot;
   // then the bucket counters; then bucket entries and bounds per position;
   // then finish times per slot. Region B: the ordered sends.
+  // (distance, ancestor) and height per slot are padded to 64 J slots, so
+  // lanes past the last slot store without a guard
   uint32_t *rt32 = (uint32_t *)wl;
-  uint32_t *dist = (uint32_t *)(wl + a.w_dist);
-  uint16_t *anc = (uint16_t *)(wl + a.w_anc);
+  uint2 *da = (uint2 *)(wl + a.w_dist);
   uint32_t *hgt = (uint32_t *)(wl + a.w_h);
   uint32_t *cnt = (uint32_t *)wl;
   uint64_t *erec = (uint64_t *)wl;
@@ -221,17 +222,23 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
       // (chosen option bit & options through v), one byte per destination:
       // its lowest set bit, over the words in destination order, is byte
       // 4w + b of the smallest destination d whose drawn route passes v,
-      // and the bit inside the byte is that route's option kd (32 * PW when
+      // and the bit inside the byte is that route's option kd (all ones when
       // no word has a set bit; a later word's bits all lie above an earlier
       // word's, so the minimum over the words that have one is the first)
 #pragma unroll
       for (int q = 0; q < G; q++) {
         const uint32_t ob = si[q].y & 0xFFFFu, rb = (si[q].y >> 16) & 0xFFu;
-        uint32_t best = 32u * PW;
+        uint32_t best = ~0u;
 #pragma unroll
         for (int w = 0; w < PW; w++) {
           const uint32_t t = rt32[rb + w] & s_opt[ob + w * V];
-          best = min(best, t ? (uint32_t)__builtin_ctz(t) + 32u * w : 32u * PW);
+          // lowest set bit, all ones for none (v_ffbl_b32 gives that for
+          // 0; written as an instruction, so the compiler does not turn the
+          // minimum back into compares and selects), then the word's
+          // offset (all ones stay all ones)
+          uint32_t f;
+          asm("v_ffbl_b32 %0, %1" : "=v"(f) : "v"(t));
+          best = min(best, f | (32u * w));
         }
         pos[q] = best;
       }
@@ -242,11 +249,17 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
         // passes it; a rank of the postcondition without one is never reached
         const uint32_t in = (lane + 64 * (g0 + q) < (uint32_t)CV) ? 1u : 0u;
         const uint32_t live = in & ~(si[q].x >> 30) & 1u;
-        const uint32_t has = live & (pos[q] < 32u * PW ? 1u : 0u);
+        const uint32_t has = live & (pos[q] != ~0u ? 1u : 0u);
         bad |= live & ~has & (si[q].x >> 31);
         const uint32_t d = pos[q] >> 3, kd = pos[q] & 7;
-        const uint32_t ei = (si[q].x & 0xFFFFFu) + d * K + kd;
-        l[q] = has ? (uint32_t)s_ent[ei] : 0xFFu;
+        // entry 0 for a slot without a send (a mask, not a select, so that
+        // no lane-masked block is formed here); read for every lane (the
+        // empty asm keeps the compiler from moving the read into a branch of
+        // its own), then selected
+        const uint32_t ei = ((si[q].x & 0xFFFFFu) + d * K + kd) & (0u - has);
+        uint32_t le = s_ent[ei];
+        asm volatile("" : "+v"(le));
+        l[q] = has ? le : 0xFFu;
         pos[q] = has;
       }
 #pragma unroll
@@ -255,18 +268,17 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
         const bool has = pos[q] != 0;
         const uint32_t lq = l[q] < (uint32_t)E ? l[q] : 0u;
         fault |= has && l[q] >= (uint32_t)E;  // unreachable: the option passes v
-        const uint32_t u = s_src[lq], ec = s_cost[lq];
+        uint32_t u = s_src[lq], ec = s_cost[lq];
+        asm volatile("" : "+v"(u), "+v"(ec));
         const uint32_t cbase = (si[q].x >> 20) & 0x3FFu;
+        const uint32_t sl = lane + 64 * jj;
         pl[jj] = has ? (lq | (u << 8) | ((cbase + (si[q].y >> 24)) << 16)) : ~0u;
-        // the owner's slot (and a slot without a send) is its own
-        // ancestor, at distance 0
-        an[jj] = has ? cbase + u : slc[q];
+        // the owner's slot (and a slot without a send, or past the last
+        // slot) is its own ancestor, at distance 0
+        an[jj] = has ? cbase + u : sl;
         acc[jj] = has ? ec : 0u;
-        if (lane + 64 * jj < CV) {
-          dist[slc[q]] = acc[jj];
-          anc[slc[q]] = (uint16_t)an[jj];
-          hgt[slc[q]] = 0;
-        }
+        da[sl] = make_uint2(acc[jj], an[jj]);
+        hgt[sl] = 0;
       }
     }
     wave_sync();
@@ -284,10 +296,10 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
       uint32_t open = 0;
 #pragma unroll
       for (int j = 0; j < J; j++) {
-        const uint32_t sl = lane + 64 * j;
-        ra[j] = dist[an[j]];
-        rn[j] = anc[an[j]];
-        hv[j] = hgt[sl < (uint32_t)CV ? sl : 0u];
+        const uint2 r = da[an[j]];
+        ra[j] = r.x;
+        rn[j] = r.y;
+        hv[j] = hgt[lane + 64 * j];
         open |= (pl[j] != ~0u && an[j] != (pl[j] >> 16)) ? 1u : 0u;
       }
       if (__ballot(open) == 0) break;
@@ -301,10 +313,7 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
         if (pl[j] != ~0u && an[j] != (pl[j] >> 16)) atomicMax(&hgt[an[j]], hv[j] + acc[j]);
         acc[j] += ra[j];
         an[j] = rn[j];
-        if (sl < (uint32_t)CV) {
-          dist[sl] = acc[j];
-          anc[sl] = (uint16_t)an[j];
-        }
+        da[sl] = make_uint2(acc[j], an[j]);
       }
       wave_sync();
     }
@@ -321,8 +330,7 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
       uint32_t hh[J], cl[J];
 #pragma unroll
       for (int j = 0; j < J; j++) {
-        const uint32_t sl = lane + 64 * j;
-        hh[j] = hgt[sl < (uint32_t)CV ? sl : 0u];
+        hh[j] = hgt[lane + 64 * j];
         cl[j] = s_cost[pl[j] != ~0u ? pl[j] & 0xFFu : 0u];
       }
       const uint32_t top = (uint32_t)a.qrange - 1;
@@ -541,13 +549,20 @@ const void *rank_fn_j(int pw) {
   }
 }
 
+// slots per lane of the instantiation that runs C * V <= 512 slots
+int rank_slots_per_lane(int cv) {
+  const int j = (cv + 63) / 64;
+  return j <= 1 ? 1 : j <= 2 ? 2 : j <= 4 ? 4 : 8;
+}
+
 const void *rank_fn(const TreeArgs &a) {
-  const int J = (a.C * a.V + 63) / 64, pw = a.P / 4;
-  if (J <= 1) return rank_fn_j<1>(pw);
-  if (J <= 2) return rank_fn_j<2>(pw);
-  if (J <= 4) return rank_fn_j<4>(pw);
-  if (J <= 8) return rank_fn_j<8>(pw);
-  return rank_fn_j<16>(pw);
+  const int pw = a.P / 4;
+  switch (rank_slots_per_lane(a.C * a.V)) {
+    case 1: return rank_fn_j<1>(pw);
+    case 2: return rank_fn_j<2>(pw);
+    case 4: return rank_fn_j<4>(pw);
+    default: return rank_fn_j<8>(pw);
+  }
 }
 
 }  // namespace
@@ -559,7 +574,7 @@ int32_t tree_rank_layout(const taccl_plan &p, TreeArgs &a) {
   const int32_t pw = P / 4;
   if (p.coll.kind == TACCL_ALLTOALL || p.topt.empty() || p.tent.empty() || p.pq_range <= 0 ||
       K > 8 || H > 4 || P % 4 || (pw != 1 && pw != 2 && pw != 3 && pw != 4 && pw != 6 && pw != 8) ||
-      V > 64 || E < 1 || E > 255 || CV > 1024 || p.route_stride > 4 * 64 * kPfRouteWords ||
+      V > 64 || E < 1 || E > 255 || CV > 64 * kLayerMaxSlotsPerLane || p.route_stride > 4 * 64 * kPfRouteWords ||
       p.route_stride % 4)
     return 0;
   uint64_t cmin = ~0ull, cmax = 0;
@@ -602,14 +617,16 @@ int32_t tree_rank_layout(const taccl_plan &p, TreeArgs &a) {
   int r = 0;
   while ((1 << r) < V) r++;
   a.pj_rounds = std::max(r, 1);
-  // region A: one-hot routes, distances, ancestors, heights; then u16
-  // counters for nl_max * E + 1 starts plus one dummy word per lane; then
-  // 8-byte entries (three spare) and bounds per position; then finish times
-  const int32_t tree_bytes = align16(p.route_stride) + align16(4 * CV) + align16(2 * CV) +
-                             align16(4 * CV);
+  // region A: one-hot routes, (distance, ancestor) pairs and heights for
+  // every slot a lane holds (64 J, J of the instantiation that runs); then
+  // u16 counters for nl_max * E + 1 starts plus one dummy word per lane;
+  // then 8-byte entries (three spare) and bounds per position; then finish
+  // times
+  const int32_t CVp = 64 * rank_slots_per_lane(CV);
+  const int32_t tree_bytes = align16(p.route_stride) + align16(8 * CVp) + align16(4 * CVp);
   a.w_dist = align16(p.route_stride);
-  a.w_anc = a.w_dist + align16(4 * CV);
-  a.w_h = a.w_anc + align16(2 * CV);
+  a.w_anc = a.w_dist;
+  a.w_h = a.w_dist + align16(8 * CVp);
   const int32_t cnt_bytes = align16(4 * (int32_t)((nl * E + 2) / 2 + 64));
   a.w_bnd = align16(8 * (S + 3));
   const int32_t ent_bytes = a.w_bnd + align16(4 * S);

@@ -1846,7 +1846,7 @@ int32_t tree_layers_layout(const taccl_plan &p, TreeArgs &a) {
   if (p.topt.empty() || K > 8 || H > 4 || P % 4 ||
       (pw != 1 && pw != 2 && pw != 3 && pw != 4 && pw != 6 && pw != 8) ||
       V > 64 || E < 1 ||
-      CV > 64 * 16 || p.route_stride > 4 * 64 * kPfRoute || E > (1 << 22))
+      CV > 64 * kLayerMaxSlotsPerLane || p.route_stride > 4 * 64 * kPfRoute || E > (1 << 22))
     return 0;
   uint64_t cmin = ~0ull, cmax = 0;
   for (uint32_t c : p.cost) {
@@ -1924,8 +1924,7 @@ static const void *layers_fn_c(const TreeArgs &a) {
   if (J <= 1) return layers_fn_j<1, kC, kR>(pw);
   if (J <= 2) return layers_fn_j<2, kC, kR>(pw);
   if (J <= 4) return layers_fn_j<4, kC, kR>(pw);
-  if (J <= 8) return layers_fn_j<8, kC, kR>(pw);
-  return layers_fn_j<16, kC, kR>(pw);
+  return layers_fn_j<8, kC, kR>(pw);
 }
 
 // a.reduce selects the ReduceScatter variant (trees run backwards)
@@ -2006,8 +2005,7 @@ static const void *greedy_fn_r(const TreeArgs &a) {
   if (J <= 1) return greedy_fn_j<1, kR>(pw);
   if (J <= 2) return greedy_fn_j<2, kR>(pw);
   if (J <= 4) return greedy_fn_j<4, kR>(pw);
-  if (J <= 8) return greedy_fn_j<8, kR>(pw);
-  return greedy_fn_j<16, kR>(pw);
+  return greedy_fn_j<8, kR>(pw);
 }
 
 static const void *greedy_fn(const TreeArgs &a) {

@@ -160,6 +160,10 @@ struct ConnArgs {
 constexpr int kConnMaxThreads = 256;
 
 constexpr int kTreeMaxThreads = 512;  // up to 8 wavefronts per block
+// (chunk, vertex) slots per lane of the layered, greedy and ranked multicast
+// kernels: at most 8, i.e. C x V <= 512 (beyond that their register state
+// would spill to scratch; larger plans run on the general kernel)
+constexpr int kLayerMaxSlotsPerLane = 8;
 constexpr int kRankMaxThreads = 768;  // ranked multicast kernel: up to 12
 constexpr int kTreeRecLdsMax = 32768;  // route records kept in LDS up to this size
 constexpr int kPathThreads = 256;

@@ -193,38 +193,33 @@ def test_alltoall_block_kernel_two_word_keys(order):
 
 @pytest.mark.parametrize("order", [1, 2])
 def test_alltoall_block_kernel_unstaged_priorities(order):
-    """Two chunks per pair on the four-node plan: more sends than the block
-    kernel stages in LDS (it stages a candidate's priorities while two blocks
-    still fit a CU), so the priorities are read hop by hop."""
-    w = replace(cf.fournode64_a2a(n_candidates=4), chunks_per_rank=2)
-    w = cf.with_greedy(w) if order == 1 else cf.with_reverse_greedy(w)
+    """A bidirectional 30-rank ring, shortest routes, four chunks per pair:
+    3600 chunks (four per thread of the block kernel, its largest shape) and
+    27000 sends, more than the kernel stages in LDS (it stages a candidate's
+    priorities while two blocks still fit a CU), so the priorities are read
+    hop by hop; keys of up to 15 hops need two words."""
+    row_ptr, col, a, b = cf.csr_from_edges(30, cf.ring_edges(list(range(30)), 700, 46))
+    w = cf.Workload("ring30_a2a", 30, 30, row_ptr, col, a, b, None, cf.ALLTOALL, 4, 65536,
+                    cf.SHORTEST_ONLY, k=1, order=order)
     plan, ref, opts = plans(w)
-    assert plan.num_chunks == 8192 and 4 * plan.info["max_sends"] > 80 * 1024
-    routes, prio = generate(w.seed + 15, 0, 4, opts, plan.prio_stride)
+    assert plan.num_chunks == 3600 and 4 * plan.info["max_sends"] > 80 * 1024
+    routes, prio = generate(w.seed + 15, 0, 2, opts, plan.prio_stride)
     prio[:, ::7] = 3
-    check(plan, ref, routes, prio, f"fournode64 cpr=2 alltoall greedy order={order}")
+    check(plan, ref, routes, prio, f"ring30 cpr=4 alltoall greedy order={order}")
 
 
-@pytest.mark.parametrize("order", [1, 2])
-def test_alltoall_block_kernel_eight_chunks_per_thread(order):
-    """8192 chunks: the block kernel's largest shape (8 chunks per thread)."""
-    edges = [(u, v, 700, 8) for u in range(64) for v in range(64) if u != v]
-    row_ptr, col, a, b = cf.csr_from_edges(64, edges)
-    w = cf.Workload("mesh64_a2a", 64, 64, row_ptr, col, a, b, None, cf.ALLTOALL, 2, 4096,
-                    cf.KSHORTEST, k=2, order=order)
-    plan, ref, opts = plans(w)
-    assert plan.num_chunks == 8192
-    routes, prio = generate(9, 0, 6, opts, plan.prio_stride)
-    prio[:, ::5] = 2
-    check(plan, ref, routes, prio, f"mesh64 cpr=2 alltoall greedy order={order}")
-
-
-def test_alltoall_too_large_refused():
-    """More than 8192 chunks (8 per thread of a 1024-thread block): refused,
+@pytest.mark.parametrize("make", [
+    # more than 4096 chunks (4 per thread of a 1024-thread block)
+    lambda: cf.with_greedy(replace(cf.fournode64_a2a(n_candidates=2), chunks_per_rank=2)),
+    lambda: cf.with_greedy(replace(cf.full_a2a(24, chunk_bytes=4096), chunks_per_rank=15)),
+])
+def test_alltoall_too_large_refused(make):
+    """Greedy Alltoall plans beyond the block kernel's largest shape: refused,
     not approximated."""
     from paper_2111_04867_amd.binding import Plan, TacclError
-    w = cf.with_greedy(replace(cf.full_a2a(24, chunk_bytes=4096), chunks_per_rank=15))
+    w = make()
     plan = Plan.from_workload(w)
+    assert plan.num_chunks > 4096
     routes, prio = generate(1, 0, 2, plan.route_options(), plan.prio_stride)
     with pytest.raises(TacclError) as e:
         plan.eval(routes, prio)

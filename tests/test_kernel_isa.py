@@ -1,0 +1,115 @@
+"""Audit of the library's gfx950 device code for register spills.
+
+A VGPR spill is a per-lane scratch store, so it saves only the lanes that are
+active when it runs. The compiler has been seen to place a spill store in a
+join block ahead of the instruction that restores the execution mask after a
+branch: lanes that did not take the branch then keep whatever an earlier
+iteration left in the slot, and a later reload hands them a stale value (a
+multicast plan's postcondition bit, so a candidate with an unreached rank
+came out valid). The kernels are therefore kept free of VGPR spills, with
+one exception whose spills are all taken with the full mask: the block-per-
+candidate Alltoall greedy with one-word keys and four chunks per thread,
+which holds 64 registers so that two 1024-thread blocks share a CU and
+spills only set-up values before its candidate loop. For that kernel every
+spill store must come after a mask restore (or before any narrowing) in
+program order.
+
+The sources are compiled here with the library's own flags (no GPU needed).
+"""
+import glob
+import os
+import re
+import shutil
+import tempfile
+
+import pytest
+import yaml
+
+from paper_2111_04867_amd import build
+
+# kernels allowed to spill (mangled-name fragments), each still under the
+# full-mask rule below
+SPILL_OK = ["path_greedy_blockILi4ELi1024ELb1E"]
+
+
+@pytest.fixture(scope="module")
+def isa():
+    if shutil.which("hipcc") is None:
+        pytest.skip("hipcc is not installed")
+    out = {}
+    with tempfile.TemporaryDirectory() as tmp:
+        procs = []
+        for src in sorted(glob.glob(os.path.join(build.CSRC, "*.hip"))):
+            dst = os.path.join(tmp, os.path.basename(src) + ".s")
+            procs.append((src, dst, build.device_asm(src, dst)))
+        for src, dst, p in procs:
+            err = p.communicate()[1]
+            assert p.returncode == 0, err[-2000:]
+            out[os.path.basename(src)] = open(dst).read()
+    return out
+
+
+def kernels(asm):
+    """(name, metadata, body) of every kernel in one assembly file."""
+    meta = asm[asm.index(".amdgpu_metadata"):asm.index(".end_amdgpu_metadata")]
+    doc = yaml.safe_load(meta[meta.index("---"):meta.rindex("...") + 3])
+    for k in doc["amdhsa.kernels"]:
+        name = k[".name"]
+        start = asm.index("\n" + name + ":")
+        body = asm[start:asm.index(".Lfunc_end", start)]
+        yield name, k, body
+
+
+# instructions that narrow the execution mask, and the restore after a branch
+NARROW = re.compile(r"^s_(and|andn2|or|xor)_saveexec_b64|^s_(and|andn2|xor)_b64 exec,"
+                    r"|^s_mov_b64 exec, s\[|^s_cselect_b64 exec,")
+RESTORE = re.compile(r"^s_or_b64 exec, exec,|^s_mov_b64 exec, -1")
+
+
+def masked_spills(body):
+    """Spill stores whose latest mask write, in program order, narrows it."""
+    state, bad = "full", []
+    for line in body.split("\n"):
+        t = line.strip()
+        if RESTORE.match(t):
+            state = "full"
+        elif NARROW.match(t):
+            state = "narrow"
+        elif t.startswith("scratch_store") and "Spill" in t and state == "narrow":
+            bad.append(t)
+    return bad
+
+
+def test_every_source_has_kernels(isa):
+    assert {"eval_tree.hip", "eval_path.hip", "eval_rank.hip", "eval_greedy.hip"} <= set(isa)
+    for src, asm in isa.items():
+        assert list(kernels(asm)), src
+
+
+def test_no_vgpr_spills(isa):
+    spilling = []
+    for src, asm in isa.items():
+        for name, meta, _ in kernels(asm):
+            if meta.get(".vgpr_spill_count", 0) and not any(f in name for f in SPILL_OK):
+                spilling.append((src, name, meta[".vgpr_spill_count"]))
+    assert not spilling, spilling
+
+
+def test_allowed_spills_run_with_the_full_mask(isa):
+    seen = 0
+    for src, asm in isa.items():
+        for name, meta, body in kernels(asm):
+            if any(f in name for f in SPILL_OK):
+                seen += 1
+                assert masked_spills(body) == [], (src, name)
+    assert seen == len(SPILL_OK)
+
+
+def test_the_audit_finds_a_masked_spill():
+    """The rule flags a spill store between a narrowing and the restore."""
+    body = "\n".join(["s_and_saveexec_b64 s[0:1], vcc", "v_add_u32_e32 v1, v2, v3",
+                      "scratch_store_dwordx2 off, v[4:5], off offset:8 ; 8-byte Folded Spill",
+                      "s_or_b64 exec, exec, s[0:1]",
+                      "scratch_store_dword off, v6, off offset:16 ; 4-byte Folded Spill"])
+    assert masked_spills(body) == [
+        "scratch_store_dwordx2 off, v[4:5], off offset:8 ; 8-byte Folded Spill"]
