@@ -52,11 +52,6 @@ __device__ __forceinline__ void wave_sync() {
   asm volatile("" ::: "memory");
 }
 
-// n / m for n < 2^16 with mm = floor(2^32 / m) + 1
-__device__ __forceinline__ uint32_t div_m(uint32_t n, uint32_t mm) {
-  return (uint32_t)(((uint64_t)n * mm) >> 32);
-}
-
 // The larger of v and the value of the lane `Ctrl` selects through DPP; a
 // lane without one (an out-of-row source, or a row the mask leaves out)
 // keeps v (the DPP source reads as 0 there and every value is unsigned), so
@@ -92,7 +87,6 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
 
   uint32_t *s_cost = (uint32_t *)(lds + a.o_cost);
   uint8_t *s_src = lds + a.o_src;
-  uint8_t *s_own = lds + a.o_own;
   uint64_t *s_post = (uint64_t *)(lds + a.o_post);
   // option bytes of (o, v), word w, at (o * PW + w) * V + v plus a pad per
   // owner, so that the 16 lanes of a row (one chunk, consecutive vertices)
@@ -114,7 +108,6 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
   }
   for (int j = threadIdx.x; j < P * V * P * K; j += blockDim.x) s_ent[j] = a.ent[j];
   for (int j = threadIdx.x; j < C; j += blockDim.x) {
-    s_own[j] = a.owner8[j];
     s_post[j] = a.post_mask[j];
   }
   for (int j = threadIdx.x; j < CV; j += blockDim.x) {
@@ -130,8 +123,8 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   unsigned char *wl = lds + a.o_wave + wave * a.wave_bytes;
   // Region A: one-hot routes, distances, ancestors and heights per slot;
-  // then the bucket counters; then bucket entries and bounds per position;
-  // then finish times per slot. Region B: the ordered sends.
+  // then the bucket counters; then bucket entries, bounds and parent sends
+  // per position; then finish times per slot. Region B: the ordered sends.
   // (distance, ancestor) and height per slot are padded to 64 J slots, so
   // lanes past the last slot store without a guard
   uint32_t *rt32 = (uint32_t *)wl;
@@ -140,6 +133,7 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
   uint32_t *cnt = (uint32_t *)wl;
   uint64_t *erec = (uint64_t *)wl;
   uint32_t *bnd = (uint32_t *)(wl + a.w_bnd);
+  uint16_t *pjs = (uint16_t *)(wl + a.w_pj);  // parent send per position
   uint32_t *fin = (uint32_t *)wl;
   uint32_t *ord = (uint32_t *)(wl + a.w_ord2);
   uint32_t *info = (uint32_t *)(wl + a.w_info2);
@@ -203,9 +197,9 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
     wave_sync();
 
     // ---- trees: the hop into every reached (chunk, vertex) slot ------------
-    // pl: link | parent vertex << 8 | the owner's slot << 16 for a slot with
-    // a send, ~0 otherwise; an / acc: the slot's 2^k-th ancestor and the
-    // cost of the path up to it
+    // pl: link | parent vertex << 8 | owner vertex << 14 | the owner's slot
+    // << 20 for a slot with a send (V <= 64, C * V <= 1024), ~0 otherwise;
+    // an / acc: the slot's 2^k-th ancestor and the cost of the path up to it
     uint32_t pl[J], an[J], acc[J];
     uint32_t bad = 0, fault = 0;
 #pragma unroll
@@ -272,7 +266,8 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
         asm volatile("" : "+v"(u), "+v"(ec));
         const uint32_t cbase = (si[q].x >> 20) & 0x3FFu;
         const uint32_t sl = lane + 64 * jj;
-        pl[jj] = has ? (lq | (u << 8) | ((cbase + (si[q].y >> 24)) << 16)) : ~0u;
+        const uint32_t own = si[q].y >> 24;
+        pl[jj] = has ? (lq | (u << 8) | (own << 14) | ((cbase + own) << 20)) : ~0u;
         // the owner's slot (and a slot without a send, or past the last
         // slot) is its own ancestor, at distance 0
         an[jj] = has ? cbase + u : sl;
@@ -300,7 +295,7 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
         ra[j] = r.x;
         rn[j] = r.y;
         hv[j] = hgt[lane + 64 * j];
-        open |= (pl[j] != ~0u && an[j] != (pl[j] >> 16)) ? 1u : 0u;
+        open |= (pl[j] != ~0u && an[j] != (pl[j] >> 20)) ? 1u : 0u;
       }
       if (__ballot(open) == 0) break;
       wave_sync();
@@ -310,7 +305,7 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
         // no push into the owner's slot: it has no send and its height is
         // never read, and every chain ends there, so the pushes of a whole
         // chunk would queue on one LDS word
-        if (pl[j] != ~0u && an[j] != (pl[j] >> 16)) atomicMax(&hgt[an[j]], hv[j] + acc[j]);
+        if (pl[j] != ~0u && an[j] != (pl[j] >> 20)) atomicMax(&hgt[an[j]], hv[j] + acc[j]);
         acc[j] += ra[j];
         an[j] = rn[j];
         da[sl] = make_uint2(acc[j], an[j]);
@@ -323,7 +318,9 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
     // trav = dist(u) = dist(v) - cost, rem = cost + height(v); the key
     // orders (rem desc, trav asc, priority, slot); within a link every send
     // enters the same vertex, so slot order is chunk order
-    uint32_t bl[J];  // link | layer << 8, or ~0 for no send
+    // link | layer << 8 | parent send << 16 (the parent vertex's slot, kNone
+    // when the parent is the owner), or ~0 for no send
+    uint32_t bl[J];
     uint64_t key[J];
     uint64_t lm = 0;
     {
@@ -349,7 +346,9 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
             L = 0;
             fault = 1;
           }
-          bl[j] = (pl[j] & 0xFFu) | (L << 8);
+          const uint32_t u = (pl[j] >> 8) & 63u, own = (pl[j] >> 14) & 63u;
+          const uint32_t pjs_v = u == own ? kNone : (pl[j] >> 20) - own + u;
+          bl[j] = (pl[j] & 0xFFu) | (L << 8) | (pjs_v << 16);
           const uint32_t hi = ((top - rq) << 21) | (tq << 10) | (px[j] >> 22);
           const uint32_t lo = (px[j] << 10) | (uint32_t)(lane + 64 * j);
           key[j] = ((uint64_t)hi << 32) | lo;
@@ -416,6 +415,7 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
         const uint32_t pos = b0[k] + idx[k];
         erec[pos] = key[k];
         bnd[pos] = b0[k] | (b1[k] << 10) | ((bl[k] & 0xFFu) << 20);
+        pjs[pos] = (uint16_t)(bl[k] >> 16);
       }
     wave_sync();
 
@@ -423,11 +423,28 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
     // one lane per ordered position; the entry array has three spare
     // entries past its end, so four members load without clamping (entries
     // past the bucket never count)
+    // The next pass's entry, bounds and parent send are loaded while this
+    // pass ranks, so a pass waits only for its bucket's members.
     const uint32_t total = lst[nl];
+    uint64_t kx_n = 0;
+    uint32_t bd_n = 0, pj_n = 0;
+    if (total > 0) {
+      const uint32_t x0 = min((uint32_t)lane, total - 1u);
+      kx_n = erec[x0];
+      bd_n = bnd[x0];
+      pj_n = pjs[x0];
+    }
     for (uint32_t x = lane; x < total; x += 64) {
-      const uint64_t kx = erec[x];
-      const uint32_t bd = bnd[x];
+      const uint64_t kx = kx_n;
+      const uint32_t bd = bd_n, pred = pj_n;
+      {
+        const uint32_t xn = min(x + 64u, total - 1u);
+        kx_n = erec[xn];
+        bd_n = bnd[xn];
+        pj_n = pjs[xn];
+      }
       const uint32_t bs = bd & 0x3FFu, be = (bd >> 10) & 0x3FFu, l = bd >> 20;
+      const uint32_t sl = (uint32_t)kx & 0x3FFu;
       uint32_t rank = 0;
       for (uint32_t y = bs; y < be; y += 4) {
         uint64_t m[4];
@@ -436,10 +453,6 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
 #pragma unroll
         for (int t = 0; t < 4; t++) rank += (uint32_t)((y + t < be) & (m[t] < kx));
       }
-      const uint32_t sl = (uint32_t)kx & 0x3FFu;
-      const uint32_t c = div_m(sl, a.vmagic);
-      const uint32_t u = s_src[l];
-      const uint32_t pred = (u == s_own[c]) ? kNone : c * V + u;
       const uint32_t q = bs + rank;
       ord[q] = sl | (pred << 16);
       info[q] = l | (rank << 16) | ((uint32_t)(rank + 1 == be - bs) << 31);
@@ -453,19 +466,39 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
     // are buckets). kk = how many earlier sends of the lane's run lie in
     // this pass of 64 positions; the scan takes only the steps some lane
     // needs.
+    // The ordered sends of the next pass (the layer's next 64 positions, or
+    // the next layer's first) are loaded while the current pass is timed, so
+    // a pass waits for one round of LDS reads (ready time, cost, busy time);
+    // layer starts come from a register (lane ly holds layer ly's).
     uint32_t mk = 0;
+    const uint32_t lst_r = lane < nl ? lst[lane] : total;
+    auto layer_start = [&](int ly) -> uint32_t {
+      return ly < nl ? (uint32_t)__builtin_amdgcn_readlane((int)lst_r, ly) : total;
+    };
+    uint32_t e_n = 0, inf_n = 0;
+    auto prefetch = [&](uint32_t start) {  // positions past the end: the last one
+      const uint32_t q = min(start + (uint32_t)lane, total - 1u);
+      e_n = ord[q];
+      inf_n = info[q];
+    };
+    if (nl > 0) prefetch(0);
     for (int ly = 0; ly < nl; ly++) {
-      const uint32_t qs = lst[ly], qe = lst[ly + 1];
+      const uint32_t qs = layer_start(ly), qe = layer_start(ly + 1);
       uint32_t carry = 0;
       for (uint32_t base = qs; base < qe; base += 64) {
         const uint32_t q = base + lane;
         const bool ok = q < qe;
-        const uint32_t qq = ok ? q : qs;
-        const uint32_t e = ord[qq], inf = info[qq];
+        // a lane past the layer holds a valid send of a later one: its link
+        // and parent index valid reads, and it neither counts nor writes
+        const uint32_t e = e_n, inf = inf_n;
+        prefetch(min(base + 64u, qe));
         const uint32_t l = inf & 0xFFFFu, k = ok ? (inf >> 16) & 0x7FFFu : 0u;
         const uint32_t pj = e >> 16;
-        const uint32_t r0 = fin[pj == kNone ? 0u : pj];
-        const uint32_t c = s_cost[l], F = lfree[l];
+        uint32_t r0 = fin[pj == kNone ? 0u : pj];
+        uint32_t c = s_cost[l], F = lfree[l];
+        // all three reads issued together (the compiler would otherwise
+        // move the busy time's into the branch of a run's first send)
+        asm volatile("" : "+v"(r0), "+v"(c), "+v"(F));
         const uint32_t r = pj == kNone ? 0u : r0;
         const uint32_t kc = k * c;
         uint32_t v = k == 0 ? max(r, F) : (r > kc ? r - kc : 0u);
@@ -594,7 +627,6 @@ int32_t tree_rank_layout(const taccl_plan &p, TreeArgs &a) {
   a.qrange = p.pq_range;
   a.K = K;
   a.H = H;
-  a.vmagic = (uint32_t)((1ull << 32) / (uint64_t)V + 1);
   int32_t off = 0;
   auto take = [&](int32_t bytes) {
     const int32_t o = off;
@@ -603,7 +635,6 @@ int32_t tree_rank_layout(const taccl_plan &p, TreeArgs &a) {
   };
   a.o_cost = take(4 * E);
   a.o_src = take(E);
-  a.o_own = take(C);
   a.o_post = take(8 * C);
   // owner stride of the transposed option words: PW * V rounded up to 16
   // mod 32 (two owners' rows fall on different bank halves)
@@ -620,8 +651,8 @@ int32_t tree_rank_layout(const taccl_plan &p, TreeArgs &a) {
   // region A: one-hot routes, (distance, ancestor) pairs and heights for
   // every slot a lane holds (64 J, J of the instantiation that runs); then
   // u16 counters for nl_max * E + 1 starts plus one dummy word per lane;
-  // then 8-byte entries (three spare) and bounds per position; then finish
-  // times
+  // then 8-byte entries (three spare), bounds and u16 parent sends per
+  // position; then finish times
   const int32_t CVp = 64 * rank_slots_per_lane(CV);
   const int32_t tree_bytes = align16(p.route_stride) + align16(8 * CVp) + align16(4 * CVp);
   a.w_dist = align16(p.route_stride);
@@ -629,7 +660,8 @@ int32_t tree_rank_layout(const taccl_plan &p, TreeArgs &a) {
   a.w_h = a.w_dist + align16(8 * CVp);
   const int32_t cnt_bytes = align16(4 * (int32_t)((nl * E + 2) / 2 + 64));
   a.w_bnd = align16(8 * (S + 3));
-  const int32_t ent_bytes = a.w_bnd + align16(4 * S);
+  a.w_pj = a.w_bnd + align16(4 * S);
+  const int32_t ent_bytes = a.w_pj + align16(2 * S);
   const int32_t region_a = std::max({tree_bytes, cnt_bytes, ent_bytes, align16(4 * CV)});
   // region B: the ordered sends (slot | parent send, link | rank | last)
   a.w_ord2 = region_a;

@@ -61,12 +61,12 @@ struct TreeArgs {
   // order, and the per-link state of open contiguous transfers
   int32_t any, greedy, w_gst;
   // ranked variant: exact order-preserving codes of path lengths
-  // (code = (x * qmagic) >> 32 < qrange), the entering-link table and the
-  // per-slot heights
+  // (code = (x * qmagic) >> 32 < qrange), the entering-link table, the
+  // per-slot heights and the parent send of each bucket-sorted position
   uint64_t qmagic;
   int32_t qrange;
   const uint8_t *ent;
-  int32_t o_ent, w_h, o_slot, opt_ostride;
+  int32_t o_ent, w_h, o_slot, opt_ostride, w_pj;
 };
 
 // Alltoall evaluation: one block per candidate, level by level.
