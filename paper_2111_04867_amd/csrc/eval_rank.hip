@@ -401,11 +401,15 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
       }
     }
     wave_sync();
+    // a bucket's start and end: two neighbouring u16 counters, read as the
+    // two words that hold them (one LDS read of a word pair)
     uint32_t b0[J], b1[J];
 #pragma unroll
     for (int k = 0; k < J; k++) {
-      b0[k] = start_of(bb[k]);
-      b1[k] = start_of(bb[k] + 1);
+      const uint32_t w = bb[k] >> 1, x0 = cnt[w], x1 = cnt[w + 1];
+      const bool odd = (bb[k] & 1) != 0;
+      b0[k] = odd ? x0 >> 16 : x0 & 0xFFFFu;
+      b1[k] = odd ? x1 & 0xFFFFu : x0 >> 16;
     }
     for (int ly = lane; ly <= nl; ly += 64) lst[ly] = start_of((uint32_t)ly * E);
     wave_sync();  // the counters are dead from here on (entries overwrite them)
