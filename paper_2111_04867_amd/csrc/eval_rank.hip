@@ -250,7 +250,8 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
         // no lane-masked block is formed here); read for every lane (the
         // empty asm keeps the compiler from moving the read into a branch of
         // its own), then selected
-        const uint32_t ei = ((si[q].x & 0xFFFFFu) + d * K + kd) & (0u - has);
+        // 24-bit multiplies (d < 64, K <= 8) issue at the full VALU rate
+        const uint32_t ei = ((si[q].x & 0xFFFFFu) + __umul24(d, (uint32_t)K) + kd) & (0u - has);
         uint32_t le = s_ent[ei];
         asm volatile("" : "+v"(le));
         l[q] = has ? le : 0xFFu;
@@ -375,7 +376,7 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
       const bool has = bl[k] != ~0u;
       const uint32_t L = (bl[k] >> 8) & 63u;
       const uint32_t above = (uint32_t)__popcll((layers >> L) >> 1);
-      const uint32_t b = above * E + (bl[k] & 0xFFu);
+      const uint32_t b = __umul24(above, (uint32_t)E) + (bl[k] & 0xFFu);
       const uint32_t sh = (b & 1) << 4;
       const uint32_t old = atomicAdd(&cnt[has ? b >> 1 : (uint32_t)NW + lane], 1u << sh);
       bb[k] = has ? b : 0u;
@@ -504,7 +505,7 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
         // move the busy time's into the branch of a run's first send)
         asm volatile("" : "+v"(r0), "+v"(c), "+v"(F));
         const uint32_t r = pj == kNone ? 0u : r0;
-        const uint32_t kc = k * c;
+        const uint32_t kc = __umul24(k, c);  // k < 2^15, c < 2^24 (plan bound)
         uint32_t v = k == 0 ? max(r, F) : (r > kc ? r - kc : 0u);
         if (!ok) v = 0;
         const uint32_t kk = min(k, (uint32_t)lane);
@@ -619,7 +620,7 @@ int32_t tree_rank_layout(const taccl_plan &p, TreeArgs &a) {
     cmin = std::min<uint64_t>(cmin, c);
     cmax = std::max<uint64_t>(cmax, c);
   }
-  if (cmin == 0) return 0;
+  if (cmin == 0 || cmax >= (1u << 24)) return 0;  // link costs: 24-bit multiplies
   const uint64_t max_rem = (uint64_t)(V - 1) * cmax;
   if (max_rem >= (1ull << 32)) return 0;
   a.lmagic = ((1ull << 32) + cmin - 1) / cmin;  // ceil(2^32 / c_min)
