@@ -675,8 +675,16 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       block_excl_scan(bcnt, NB, red);
       const uint32_t tot = bcnt[NB];
       const uint32_t ept = (tot + NT - 1) / NT;  // <= CPT: a level has <= C sends
-      // pos / ept = (pos * em) >> 32 with em = floor((2^32 - 1) / ept) + 1 <= 2^32
-      const uint64_t em = ept ? 0xFFFFFFFFull / ept + 1 : 0;
+      // pos / ept for pos < 2^16 and ept <= 4 (the same for every thread):
+      // a shift, or (pos * 43691) >> 17 for 3 (exact below 2^17); 24-bit
+      // multiplies issue at the full VALU rate
+      const uint32_t esh = ept >= 4 ? 2u : ept >= 2 ? 1u : 0u;
+      auto div_ept = [&](uint32_t pos) -> uint32_t {
+        return ept == 3 ? __umul24(pos, 43691u) >> 17 : pos >> esh;
+      };
+      // the contiguity walker divides with one 64-bit multiply
+      // (y / ept = (y * em) >> 32, em = floor((2^32 - 1) / ept) + 1)
+      const uint64_t em = (kContig && ept) ? 0xFFFFFFFFull / ept + 1 : 0;
       // ---- C. scatter --------------------------------------------------------
       {
         uint32_t pos[CPT];
@@ -702,10 +710,18 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
         const uint32_t ax = aux[x];
         const uint32_t b = ax & 0xFFFFu, ci = s_cinfo[ax >> 16];
         const uint32_t b0 = bcnt[b], b1 = bcnt[b + 1], rs = bcnt[ci >> 16];
+        // four members a step (three spare entries past the array's end;
+        // entries past the bucket never count)
         uint32_t rank = 0;
-        for (uint32_t y = b0; y < b1; y++) rank += (uint32_t)(e64[y] < me);
+        for (uint32_t y = b0; y < b1; y += 4) {
+          uint64_t m[4];
+#pragma unroll
+          for (int u = 0; u < 4; u++) m[u] = e64[y + u];
+#pragma unroll
+          for (int u = 0; u < 4; u++) rank += (uint32_t)((y + u < b1) & (m[u] < me));
+        }
         const uint32_t pos = b0 + rank;
-        const uint32_t t = (uint32_t)(((uint64_t)pos * em) >> 32), q = pos - t * ept;
+        const uint32_t t = div_ept(pos), q = pos - __umul24(t, ept);
         pinfo[q * NT + t] = (uint32_t)me | ((ci & 0xFFFFu) << cb) | ((pos - rs) << kb);
       }
       __syncthreads();
@@ -734,7 +750,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       uint32_t prev = 0;
 #pragma unroll
       for (int q = 0; q < CPT; q++) {
-        const uint32_t k = pis[q] >> kb, kc = k * cs[q];
+        const uint32_t k = pis[q] >> kb, kc = __umul24(k, cs[q]);  // k < 2^16, c < 2^24
         const uint32_t av = k == 0 ? max(ct[q], lf[q]) : (ct[q] > kc ? ct[q] - kc : 0u);
         sv[q] = (k > 0 && q > 0) ? max(prev, av) : av;
         prev = sv[q];
@@ -835,7 +851,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
           const uint32_t cl = cs[q];
           // the run began before this thread's first position: k > q
           const uint32_t best = k > (uint32_t)q ? max(sv[q], cin) : sv[q];
-          const uint32_t f = (k + 1) * cl + best;
+          const uint32_t f = __umul24(k + 1, cl) + best;
           ctime[c] = f;
           mk = max(mk, f);
           const uint32_t nk = ((uint32_t)q + 1 < ept ? pis[q < CPT - 1 ? q + 1 : q] : nxt0) >> kb;
@@ -881,7 +897,7 @@ int32_t path_fast_layout(const taccl_plan &p, PathArgs &a) {
   // bucket counters, the level's total, and one dummy counter per lane of a
   // wavefront (slots without a send count there)
   a.o_fbcnt = take(4 * (p.max_lvl_nb + 1 + 64));
-  a.o_fepr = take(8 * M);
+  a.o_fepr = take(8 * (M + 3));
   a.o_faux = take(4 * M);
   a.o_fsrt = take(4 * path_fast_threads(p) * path_fast_cpt(p));
   // packed sorted sends: chunk, link and run index in one word
@@ -912,6 +928,10 @@ int path_fast_cpt(const taccl_plan &p) {
   if (2 * bits((uint32_t)p.coll.C) + bits((uint32_t)p.topo.E) > 32) return 0;
   // bucket and link fields are packed into 16 bits
   if (p.max_lvl_nb >= (1 << 16) || p.topo.E > (1 << 16)) return 0;
+  // sorted positions below 2^16 and link costs below 2^24 (24-bit multiplies)
+  if (p.max_lvl_sends > (1 << 16)) return 0;
+  for (uint32_t c : p.cost)
+    if (c >= (1u << 24)) return 0;
   const int nt = path_fast_threads(p);
   const int per = (p.coll.C + nt - 1) / nt;
   return per <= 1 ? 1 : per <= 2 ? 2 : per <= 4 ? 4 : 0;
