@@ -321,11 +321,11 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
       if (!layered) return launch_tree(x, tgrid, s);
       return greedy ? launch_tree_greedy(x, tgrid, s) : launch_tree_layers(x, tgrid, s);
     };
-    // Trees run forwards with the static order and one chunk per transfer
-    // (Allgather, explicit, the Allgather phase of an Allreduce): the ranked
-    // kernel, when the plan's path lengths have exact short codes
+    // Trees run forwards with the static order (Allgather, explicit, the
+    // Allgather phase of an Allreduce; contiguous transfers included): the
+    // ranked kernel, when the plan's path lengths have exact short codes
     TreeArgs ra = a;
-    const bool ranked = !p->contig && !greedy && a.routes_word_aligned && t->tent &&
+    const bool ranked = !greedy && a.routes_word_aligned && t->tent &&
                         tree_rank_layout(*p, ra) > 0 && tree_block_bytes(ra, 1) <= t->max_lds;
     ra.ent = t->tent;
     auto launch_ranked = [&](TreeArgs &x) {

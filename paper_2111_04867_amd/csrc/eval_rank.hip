@@ -1,7 +1,7 @@
 // Ranked multicast kernel for gfx950: Allgather and explicit multicast with
-// the static Step-2 order and one chunk per transfer (also the Allgather
-// phase of an Allreduce), for plans whose tree-path lengths take few
-// distinct values.
+// the static Step-2 order, one chunk per transfer or contiguous transfers on
+// links between nodes (Step 3, Sec. 4.1; also the Allgather phase of an
+// Allreduce), for plans whose tree-path lengths take few distinct values.
 //
 // One wavefront evaluates one candidate at a time (persistent blocks of
 // several wavefronts, the next candidate's routes and priorities streaming
@@ -33,6 +33,11 @@
 //      segmented prefix maximum over the layer's positions (DPP scans inside
 //      the wavefront with only the steps the longest run needs);
 //   6. postcondition (ballot) and makespan (wave maximum).
+// With contiguous transfers, a run on a link between nodes is walked by its
+// first lane instead: a send joins the open transfer when its remaining
+// length equals the previous send's and its chunk was ready when the
+// transfer started; a transfer of g sends takes alpha + ceil(beta bytes g /
+// 1000) and all its sends finish together.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -78,7 +83,7 @@ __device__ __forceinline__ uint32_t one_hot(uint32_t w, uint32_t j, const uint64
   return oh;
 }
 
-template <int J, int PW>
+template <int J, int PW, bool kC>
 __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int C = a.C, V = a.V, E = a.E, K = a.K;
@@ -87,6 +92,7 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
 
   uint32_t *s_cost = (uint32_t *)(lds + a.o_cost);
   uint8_t *s_src = lds + a.o_src;
+  uint8_t *s_merge = lds + a.o_merge;  // links that carry contiguous transfers
   uint64_t *s_post = (uint64_t *)(lds + a.o_post);
   // option bytes of (o, v), word w, at (o * PW + w) * V + v plus a pad per
   // owner, so that the 16 lanes of a row (one chunk, consecutive vertices)
@@ -101,6 +107,7 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
   for (int j = threadIdx.x; j < E; j += blockDim.x) {
     s_cost[j] = a.cost[j];
     s_src[j] = (uint8_t)a.lsrc[j];
+    if (kC) s_merge[j] = a.lmerge[j];
   }
   for (int j = threadIdx.x; j < P * V * PW; j += blockDim.x) {
     const int w = j % PW, ov = j / PW, o = ov / V, v = ov - o * V;
@@ -135,6 +142,7 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
   uint32_t *bnd = (uint32_t *)(wl + a.w_bnd);
   uint16_t *pjs = (uint16_t *)(wl + a.w_pj);  // parent send per position
   uint32_t *fin = (uint32_t *)wl;
+  uint32_t *rq = (uint32_t *)(wl + a.w_rq);  // ready times per position (contiguity)
   uint32_t *ord = (uint32_t *)(wl + a.w_ord2);
   uint32_t *info = (uint32_t *)(wl + a.w_info2);
   uint32_t *lfree = (uint32_t *)(wl + a.w_free);
@@ -450,17 +458,26 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
       }
       const uint32_t bs = bd & 0x3FFu, be = (bd >> 10) & 0x3FFu, l = bd >> 20;
       const uint32_t sl = (uint32_t)kx & 0x3FFu;
-      uint32_t rank = 0;
+      uint32_t rank = 0, same = 0;
       for (uint32_t y = bs; y < be; y += 4) {
         uint64_t m[4];
 #pragma unroll
         for (int t = 0; t < 4; t++) m[t] = erec[y + t];
 #pragma unroll
-        for (int t = 0; t < 4; t++) rank += (uint32_t)((y + t < be) & (m[t] < kx));
+        for (int t = 0; t < 4; t++) {
+          const uint32_t before = (uint32_t)((y + t < be) & (m[t] < kx));
+          rank += before;
+          // an earlier send of the bucket with the same remaining length
+          // (the code in the key's top 11 bits; equal lengths sort next to
+          // each other)
+          if (kC) same |= before & (uint32_t)((m[t] >> 53) == (kx >> 53));
+        }
       }
       const uint32_t q = bs + rank;
       ord[q] = sl | (pred << 16);
-      info[q] = l | (rank << 16) | ((uint32_t)(rank + 1 == be - bs) << 31);
+      // link | index in the run << 16 | same remaining length as the
+      // previous send << 30 | the run's last send << 31
+      info[q] = l | (rank << 16) | (same << 30) | ((uint32_t)(rank + 1 == be - bs) << 31);
     }
     wave_sync();
 
@@ -489,6 +506,15 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
     if (nl > 0) prefetch(0);
     for (int ly = 0; ly < nl; ly++) {
       const uint32_t qs = layer_start(ly), qe = layer_start(ly + 1);
+      if (kC) {
+        // ready times of the layer's sends, for the walkers below (parent
+        // sends lie in layers above)
+        for (uint32_t q = qs + lane; q < qe; q += 64) {
+          const uint32_t pj = ord[q] >> 16;
+          rq[q] = pj == kNone ? 0u : fin[pj];
+        }
+        wave_sync();
+      }
       uint32_t carry = 0;
       for (uint32_t base = qs; base < qe; base += 64) {
         const uint32_t q = base + lane;
@@ -497,7 +523,7 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
         // and parent index valid reads, and it neither counts nor writes
         const uint32_t e = e_n, inf = inf_n;
         prefetch(min(base + 64u, qe));
-        const uint32_t l = inf & 0xFFFFu, k = ok ? (inf >> 16) & 0x7FFFu : 0u;
+        const uint32_t l = inf & 0xFFFFu, k = ok ? (inf >> 16) & 0x3FFFu : 0u;
         const uint32_t pj = e >> 16;
         uint32_t r0 = fin[pj == kNone ? 0u : pj];
         uint32_t c = s_cost[l], F = lfree[l];
@@ -546,10 +572,42 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
         if (k > (uint32_t)lane) v = max(v, carry);
         carry = (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
         const uint32_t f = kc + c + v;
-        if (ok) {
+        const bool merge = kC && s_merge[l] != 0;
+        if (ok && !merge) {
           fin[e & 0xFFFFu] = f;
           mk = max(mk, f);
           if (inf >> 31) lfree[l] = f;  // the run's last send
+        }
+        if (kC && ok && merge && k == 0) {
+          // contiguous transfers: the run's first lane walks the run; a send
+          // joins the open transfer when its remaining length equals the
+          // previous send's and its chunk was ready when the transfer
+          // started, and a transfer of g sends takes alpha + ceil(beta
+          // bytes g / 1000)
+          const uint32_t al = a.lalpha[l];
+          const uint64_t bsz = a.lbs[l];
+          uint32_t Fw = F, gs = 0, gm = 0, g0 = q;
+          for (uint32_t j = q;; j++) {
+            const uint32_t ij = info[min(j, qe - 1u)];
+            const bool end = j >= qe || (j > q && ((ij >> 16) & 0x3FFFu) == 0);
+            const uint32_t rj = end ? 0u : rq[j];
+            const bool join = !end && gm > 0 && (ij >> 30 & 1u) && rj <= gs;
+            if (gm > 0 && !join) {  // close the open transfer
+              const uint32_t fw = gs + al + (uint32_t)((bsz * gm + 999) / 1000);
+              for (uint32_t t = g0; t < g0 + gm; t++) fin[ord[t] & 0xFFFFu] = fw;
+              Fw = fw;
+              mk = max(mk, fw);
+            }
+            if (end) break;
+            if (join) {
+              gm++;
+            } else {
+              gs = max(Fw, rj);
+              gm = 1;
+              g0 = j;
+            }
+          }
+          lfree[l] = Fw;
         }
       }
       wave_sync();
@@ -575,16 +633,21 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
 
 int32_t align16(int32_t x) { return (x + 15) & ~15; }
 
-template <int J>
-const void *rank_fn_j(int pw) {
+template <int J, bool kC>
+const void *rank_fn_jc(int pw) {
   switch (pw) {
-    case 1: return (const void *)tree_rank_kernel<J, 1>;
-    case 2: return (const void *)tree_rank_kernel<J, 2>;
-    case 3: return (const void *)tree_rank_kernel<J, 3>;
-    case 4: return (const void *)tree_rank_kernel<J, 4>;
-    case 6: return (const void *)tree_rank_kernel<J, 6>;
-    default: return (const void *)tree_rank_kernel<J, 8>;
+    case 1: return (const void *)tree_rank_kernel<J, 1, kC>;
+    case 2: return (const void *)tree_rank_kernel<J, 2, kC>;
+    case 3: return (const void *)tree_rank_kernel<J, 3, kC>;
+    case 4: return (const void *)tree_rank_kernel<J, 4, kC>;
+    case 6: return (const void *)tree_rank_kernel<J, 6, kC>;
+    default: return (const void *)tree_rank_kernel<J, 8, kC>;
   }
+}
+
+template <int J>
+const void *rank_fn_j(int pw, bool contig) {
+  return contig ? rank_fn_jc<J, true>(pw) : rank_fn_jc<J, false>(pw);
 }
 
 // slots per lane of the instantiation that runs C * V <= 512 slots
@@ -596,10 +659,10 @@ int rank_slots_per_lane(int cv) {
 const void *rank_fn(const TreeArgs &a) {
   const int pw = a.P / 4;
   switch (rank_slots_per_lane(a.C * a.V)) {
-    case 1: return rank_fn_j<1>(pw);
-    case 2: return rank_fn_j<2>(pw);
-    case 4: return rank_fn_j<4>(pw);
-    default: return rank_fn_j<8>(pw);
+    case 1: return rank_fn_j<1>(pw, a.contig != 0);
+    case 2: return rank_fn_j<2>(pw, a.contig != 0);
+    case 4: return rank_fn_j<4>(pw, a.contig != 0);
+    default: return rank_fn_j<8>(pw, a.contig != 0);
   }
 }
 
@@ -640,6 +703,7 @@ int32_t tree_rank_layout(const taccl_plan &p, TreeArgs &a) {
   };
   a.o_cost = take(4 * E);
   a.o_src = take(E);
+  a.o_merge = take(E);
   a.o_post = take(8 * C);
   // owner stride of the transposed option words: PW * V rounded up to 16
   // mod 32 (two owners' rows fall on different bank halves)
@@ -667,7 +731,10 @@ int32_t tree_rank_layout(const taccl_plan &p, TreeArgs &a) {
   a.w_bnd = align16(8 * (S + 3));
   a.w_pj = a.w_bnd + align16(4 * S);
   const int32_t ent_bytes = a.w_pj + align16(2 * S);
-  const int32_t region_a = std::max({tree_bytes, cnt_bytes, ent_bytes, align16(4 * CV)});
+  // finish times per slot, then (contiguous transfers) ready times per
+  // position
+  a.w_rq = align16(4 * CVp);
+  const int32_t region_a = std::max({tree_bytes, cnt_bytes, ent_bytes, a.w_rq + align16(4 * S)});
   // region B: the ordered sends (slot | parent send, link | rank | last)
   a.w_ord2 = region_a;
   a.w_info2 = a.w_ord2 + align16(4 * S);
