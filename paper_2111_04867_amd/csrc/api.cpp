@@ -321,13 +321,16 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
       if (!layered) return launch_tree(x, tgrid, s);
       return greedy ? launch_tree_greedy(x, tgrid, s) : launch_tree_layers(x, tgrid, s);
     };
-    // Trees run forwards with the static order (Allgather, explicit, the
-    // Allgather phase of an Allreduce; contiguous transfers included): the
-    // ranked kernel, when the plan's path lengths have exact short codes
+    // The static order on the ranked kernel, when the plan's path lengths
+    // have exact short codes: Allgather, explicit multicast and the
+    // Allgather phase of an Allreduce (contiguous transfers included), and
+    // the ReduceScatter (alone or as an Allreduce's first phase) when every
+    // route hop has a reverse link of equal cost and there is no contiguity
     TreeArgs ra = a;
     const bool ranked = !greedy && a.routes_word_aligned && t->tent &&
                         tree_rank_layout(*p, ra) > 0 && tree_block_bytes(ra, 1) <= t->max_lds;
     ra.ent = t->tent;
+    const bool ranked_rs = ranked && tree_rank_reverse_ok(*p);
     auto launch_ranked = [&](TreeArgs &x) {
       int best_w = 1, best_res = 0, best_bpc = 1;
       for (int w = 1; w <= kRankMaxThreads / 64; w++) {
@@ -355,7 +358,14 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
       // second, adding its makespan (same stream, so in order)
       a.reduce = 1;
       a.accumulate = 0;
-      e = launch(a);
+      if (ranked_rs) {
+        TreeArgs r = ra;
+        r.reduce = 1;
+        r.accumulate = 0;
+        e = launch_ranked(r);
+      } else {
+        e = launch(a);
+      }
       if (e == hipSuccess) {
         TreeArgs b = ranked ? ra : a;
         b.reduce = 0;
@@ -363,8 +373,8 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
         b.prio = d_prio + (size_t)p->coll.C * p->topo.V;
         e = ranked ? launch_ranked(b) : launch(b);
       }
-    } else if (kind != TACCL_REDUCESCATTER && ranked) {
-      ra.reduce = 0;
+    } else if (kind == TACCL_REDUCESCATTER ? ranked_rs : ranked) {
+      ra.reduce = kind == TACCL_REDUCESCATTER;
       ra.accumulate = 0;
       e = launch_ranked(ra);
     } else {

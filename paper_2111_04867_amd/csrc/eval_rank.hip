@@ -83,8 +83,14 @@ __device__ __forceinline__ uint32_t one_hot(uint32_t w, uint32_t j, const uint64
   return oh;
 }
 
-template <int J, int PW, bool kC>
+// kC: contiguous transfers; kR: ReduceScatter (the trees run backwards: a
+// send v -> u on the reverse of the link into v, costs of the reverse links,
+// remaining length = reversed distance from v to the owner, travelled
+// length = longest reversed path from below up to v; a send is ready when
+// every send into v has finished)
+template <int J, int PW, bool kC, bool kR>
 __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) {
+  static_assert(!(kC && kR), "contiguous transfers are not combined with ReduceScatter here");
   extern __shared__ __align__(16) unsigned char lds[];
   const int C = a.C, V = a.V, E = a.E, K = a.K;
   constexpr int P = 4 * PW;
@@ -105,7 +111,9 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
   uint2 *s_slot = (uint2 *)(lds + a.o_slot);
   const int OS = a.opt_ostride;
   for (int j = threadIdx.x; j < E; j += blockDim.x) {
-    s_cost[j] = a.cost[j];
+    // ReduceScatter: every link's entry holds its reverse's cost (a tree
+    // link always has a reverse, checked at plan time)
+    s_cost[j] = kR ? a.cost[a.lrev[j] != 0xFFFFu ? a.lrev[j] : j] : a.cost[j];
     s_src[j] = (uint8_t)a.lsrc[j];
     if (kC) s_merge[j] = a.lmerge[j];
   }
@@ -346,8 +354,8 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
         bl[j] = ~0u;
         key[j] = 0;
         if (pl[j] != ~0u) {
-          const uint32_t trav = acc[j] - cl[j];
-          const uint32_t rem = cl[j] + hh[j];
+          const uint32_t trav = kR ? hh[j] : acc[j] - cl[j];
+          const uint32_t rem = kR ? acc[j] : cl[j] + hh[j];
           uint32_t L = __umulhi(rem, lmag);
           const uint32_t rq = __umulhi(rem, qmag);
           const uint32_t tq = __umulhi(trav, qmag);
@@ -492,6 +500,10 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
     // the next layer's first) are loaded while the current pass is timed, so
     // a pass waits for one round of LDS reads (ready time, cost, busy time);
     // layer starts come from a register (lane ly holds layer ly's).
+    if (kR) {  // ready times start at 0 and are raised by the inputs
+      for (int j = lane; j < CV; j += 64) fin[j] = 0;
+      wave_sync();
+    }
     uint32_t mk = 0;
     const uint32_t lst_r = lane < nl ? lst[lane] : total;
     auto layer_start = [&](int ly) -> uint32_t {
@@ -525,12 +537,14 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
         prefetch(min(base + 64u, qe));
         const uint32_t l = inf & 0xFFFFu, k = ok ? (inf >> 16) & 0x3FFFu : 0u;
         const uint32_t pj = e >> 16;
-        uint32_t r0 = fin[pj == kNone ? 0u : pj];
+        // Allgather: the finish of the send that brings the chunk;
+        // ReduceScatter: the slot's own ready time, raised by its inputs
+        uint32_t r0 = fin[kR ? e & 0xFFFFu : (pj == kNone ? 0u : pj)];
         uint32_t c = s_cost[l], F = lfree[l];
         // all three reads issued together (the compiler would otherwise
         // move the busy time's into the branch of a run's first send)
         asm volatile("" : "+v"(r0), "+v"(c), "+v"(F));
-        const uint32_t r = pj == kNone ? 0u : r0;
+        const uint32_t r = (!kR && pj == kNone) ? 0u : r0;
         const uint32_t kc = __umul24(k, c);  // k < 2^15, c < 2^24 (plan bound)
         uint32_t v = k == 0 ? max(r, F) : (r > kc ? r - kc : 0u);
         if (!ok) v = 0;
@@ -574,7 +588,11 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
         const uint32_t f = kc + c + v;
         const bool merge = kC && s_merge[l] != 0;
         if (ok && !merge) {
-          fin[e & 0xFFFFu] = f;
+          if (kR) {  // the send out of u waits for this one
+            if (pj != kNone) atomicMax(&fin[pj], f);
+          } else {
+            fin[e & 0xFFFFu] = f;
+          }
           mk = max(mk, f);
           if (inf >> 31) lfree[l] = f;  // the run's last send
         }
@@ -633,21 +651,23 @@ __global__ __launch_bounds__(kRankMaxThreads) void tree_rank_kernel(TreeArgs a) 
 
 int32_t align16(int32_t x) { return (x + 15) & ~15; }
 
-template <int J, bool kC>
+template <int J, bool kC, bool kR>
 const void *rank_fn_jc(int pw) {
   switch (pw) {
-    case 1: return (const void *)tree_rank_kernel<J, 1, kC>;
-    case 2: return (const void *)tree_rank_kernel<J, 2, kC>;
-    case 3: return (const void *)tree_rank_kernel<J, 3, kC>;
-    case 4: return (const void *)tree_rank_kernel<J, 4, kC>;
-    case 6: return (const void *)tree_rank_kernel<J, 6, kC>;
-    default: return (const void *)tree_rank_kernel<J, 8, kC>;
+    case 1: return (const void *)tree_rank_kernel<J, 1, kC, kR>;
+    case 2: return (const void *)tree_rank_kernel<J, 2, kC, kR>;
+    case 3: return (const void *)tree_rank_kernel<J, 3, kC, kR>;
+    case 4: return (const void *)tree_rank_kernel<J, 4, kC, kR>;
+    case 6: return (const void *)tree_rank_kernel<J, 6, kC, kR>;
+    default: return (const void *)tree_rank_kernel<J, 8, kC, kR>;
   }
 }
 
+// ReduceScatter never runs with contiguous transfers here
 template <int J>
-const void *rank_fn_j(int pw, bool contig) {
-  return contig ? rank_fn_jc<J, true>(pw) : rank_fn_jc<J, false>(pw);
+const void *rank_fn_j(int pw, bool contig, bool reduce) {
+  if (reduce) return rank_fn_jc<J, false, true>(pw);
+  return contig ? rank_fn_jc<J, true, false>(pw) : rank_fn_jc<J, false, false>(pw);
 }
 
 // slots per lane of the instantiation that runs C * V <= 512 slots
@@ -659,10 +679,10 @@ int rank_slots_per_lane(int cv) {
 const void *rank_fn(const TreeArgs &a) {
   const int pw = a.P / 4;
   switch (rank_slots_per_lane(a.C * a.V)) {
-    case 1: return rank_fn_j<1>(pw, a.contig != 0);
-    case 2: return rank_fn_j<2>(pw, a.contig != 0);
-    case 4: return rank_fn_j<4>(pw, a.contig != 0);
-    default: return rank_fn_j<8>(pw, a.contig != 0);
+    case 1: return rank_fn_j<1>(pw, a.contig != 0, a.reduce != 0);
+    case 2: return rank_fn_j<2>(pw, a.contig != 0, a.reduce != 0);
+    case 4: return rank_fn_j<4>(pw, a.contig != 0, a.reduce != 0);
+    default: return rank_fn_j<8>(pw, a.contig != 0, a.reduce != 0);
   }
 }
 
@@ -747,6 +767,17 @@ int32_t tree_rank_layout(const taccl_plan &p, TreeArgs &a) {
   w = align16(w + 4 * 65);
   a.wave_bytes = w;
   return a.o_wave + a.wave_bytes;
+}
+
+bool tree_rank_reverse_ok(const taccl_plan &p) {
+  // the reverse of every route hop exists and costs the same, so reversed
+  // path sums are sums of the same costs and the path codes stay exact
+  if (p.contig || p.lrev.size() != (size_t)p.topo.E) return false;
+  for (uint16_t l : p.path_links) {
+    const uint16_t r = p.lrev[l];
+    if (r == 0xFFFFu || p.cost[r] != p.cost[l]) return false;
+  }
+  return true;
 }
 
 int tree_rank_blocks_per_cu(const TreeArgs &a) {

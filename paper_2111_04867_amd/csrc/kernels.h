@@ -180,6 +180,9 @@ int32_t tree_block_bytes(const TreeArgs &a, int waves);
 // fills the layout and returns the bytes of a one-wavefront block, or 0
 // when the plan does not meet its conditions.
 int32_t tree_rank_layout(const taccl_plan &p, TreeArgs &a);
+// the ranked kernel may run the plan's ReduceScatter (reverse links with
+// equal costs, no contiguity)
+bool tree_rank_reverse_ok(const taccl_plan &p);
 int tree_rank_blocks_per_cu(const TreeArgs &a);
 hipError_t launch_tree_rank(const TreeArgs &a, int grid, hipStream_t stream);
 // Layered multicast kernel: fills the layout and returns the bytes of a
