@@ -113,3 +113,24 @@ def test_plans_outside_the_layered_kernel(kind):
     routes, prio = generate(1, 0, 200, opts, plan.prio_stride)
     prio[::2, ::2] = 3
     check(plan, ref, routes, prio, f"full3 kind={kind}")
+
+
+@pytest.mark.parametrize("kind", [cf.REDUCESCATTER, cf.ALLREDUCE])
+@pytest.mark.parametrize("skew", [0, 30])
+def test_reverse_link_costs(kind, skew):
+    """Two fully connected quads joined rank by rank. With skew 0 every link's
+    reverse costs the same, so the ranked kernel runs the ReduceScatter; with
+    a skew the reverse links cost more (reversed path sums leave the set the
+    path codes cover) and the layered kernel runs it."""
+    edges = []
+    for u in range(8):
+        for v in range(8):
+            if u != v and (u // 4 == v // 4 or u % 4 == v % 4):
+                edges.append((u, v, 700, 46 + (skew if u < v else 0)))
+    row_ptr, col, a, b = cf.csr_from_edges(8, edges)
+    w = cf.Workload(f"quads8_skew{skew}", 8, 8, row_ptr, col, a, b, None, kind, 2, 65536,
+                    cf.KSHORTEST, k=3)
+    plan, ref, opts = plans(w)
+    routes, prio = generate(11 + skew, 0, 512, opts, plan.prio_stride)
+    prio[::3, ::5] = 7
+    check(plan, ref, routes, prio, f"quads8 skew={skew} kind={kind}")
