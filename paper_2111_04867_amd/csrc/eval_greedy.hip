@@ -100,7 +100,11 @@ __global__ __launch_bounds__(NT) __attribute__((
       const uint32_t k = a.gkrank[qo[j] + h];
       const uint32_t pr = a.b_sprio >= 0 ? sprio[po[j] + h] : gpr[(uint32_t)c * H + h];
       if (kPack) {
-        klo[j] = ((uint64_t)k << a.kr_shift) | ((uint64_t)pr << a.chunk_bits) | (uint32_t)c;
+        // k << kr_shift lies in the high word (kr_shift = chunk_bits + 32);
+        // the priority straddles the two words: 32-bit shifts only
+        const uint32_t cb = (uint32_t)a.chunk_bits;
+        const uint32_t hi = (k << (cb & 31u)) | (cb ? pr >> (32u - cb) : 0u);
+        klo[j] = ((uint64_t)hi << 32) | ((pr << (cb & 31u)) | (uint32_t)c);
       } else {
         kr[j] = k;
         pv[j] = pr;
@@ -177,8 +181,11 @@ __global__ __launch_bounds__(NT) __attribute__((
       for (int round = 0, buf = 0;; round++, buf ^= 1) {
         uint32_t st[CPT];
         uint32_t wmin = kNone;
+        // the relative start lies in the key's high word (rel_shift >= 32):
+        // a 32-bit shift there instead of a 64-bit one
+        const uint32_t rel_hi = (uint32_t)a.rel_shift - 32u;
         auto key_of = [&](int j) {
-          return klo[j] | ((uint64_t)min(st[j] - wp, a.rel_max) << a.rel_shift);
+          return klo[j] | ((uint64_t)(min(st[j] - wp, a.rel_max) << rel_hi) << 32);
         };
 #pragma unroll
         for (int j = 0; j < CPT; j++) {
@@ -199,10 +206,18 @@ __global__ __launch_bounds__(NT) __attribute__((
           break;
         }
         const uint64_t wend = (uint64_t)W + a.cmin;
+        // the link's minimum is this chunk's key exactly when its chunk
+        // field (the key's low bits; keys of one window differ in their
+        // chunk) is this chunk: the low word of the minimum suffices
+        const uint32_t cmask = (1u << a.chunk_bits) - 1u;
+        const uint32_t *best1w = (const uint32_t *)best1;
 #pragma unroll
-        for (int j = 0; j < CPT; j++)
-          if (st[j] != kNone && (uint64_t)st[j] < wend && best1[buf * bst + cl[j]] == key_of(j))
-            commit(j, tid + NT * j, st[j], cl[j]);
+        for (int j = 0; j < CPT; j++) {
+          const uint32_t c = tid + NT * j;
+          if (st[j] != kNone && (uint64_t)st[j] < wend &&
+              (best1w[2 * (buf * bst + cl[j])] & cmask) == c)
+            commit(j, (int)c, st[j], cl[j]);
+        }
         for (int l = tid; l < E; l += NT) best1[(buf ^ 1) * bst + l] = ~0ull;
         if (tid == 0) red[buf ^ 1] = kNone;
         wp = W;
