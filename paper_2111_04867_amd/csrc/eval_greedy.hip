@@ -164,11 +164,11 @@ __global__ __launch_bounds__(NT) __attribute__((
       ct[j] = f;
       lfree[l] = f;
       mk = max(mk, f);
-      if (a.mirror) {
+      if (a.mirror) {  // the reversed order needs each send's service position
         const uint32_t h = hops[j] - 1 - cur[j];
         fpos[(uint32_t)c * H + h] = (uint16_t)lserv[l];
+        lserv[l]++;
       }
-      lserv[l]++;
       if (++cur[j] < hops[j]) load_hop(j, c);
     };
     if (kPack) {
@@ -205,7 +205,7 @@ __global__ __launch_bounds__(NT) __attribute__((
           fault = true;
           break;
         }
-        const uint64_t wend = (uint64_t)W + a.cmin;
+        // a pending start is at least W: st - W < c_min is the window test
         // the link's minimum is this chunk's key exactly when its chunk
         // field (the key's low bits; keys of one window differ in their
         // chunk) is this chunk: the low word of the minimum suffices
@@ -214,7 +214,7 @@ __global__ __launch_bounds__(NT) __attribute__((
 #pragma unroll
         for (int j = 0; j < CPT; j++) {
           const uint32_t c = tid + NT * j;
-          if (st[j] != kNone && (uint64_t)st[j] < wend &&
+          if (st[j] != kNone && st[j] - W < a.cmin &&
               (best1w[2 * (buf * bst + cl[j])] & cmask) == c)
             commit(j, (int)c, st[j], cl[j]);
         }
