@@ -56,7 +56,8 @@ constexpr int greedy_block_min_waves() {
   return kPack && CPT <= 4 ? 8 : 4;
 }
 
-template <int CPT, int NT, bool kPack>
+// kStaged: the candidate's priorities are staged in LDS (a.b_sprio >= 0)
+template <int CPT, int NT, bool kPack, bool kStaged>
 __global__ __launch_bounds__(NT) __attribute__((
     amdgpu_waves_per_eu(greedy_block_min_waves<CPT, kPack>(), 8))) void path_greedy_block(PathGreedyArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
@@ -74,7 +75,7 @@ __global__ __launch_bounds__(NT) __attribute__((
   // the candidate's priorities of its routed hops, chunk after chunk (when
   // the plan's sends fit: a.b_sprio >= 0), so each priority row is read from
   // HBM once instead of hop by hop
-  uint32_t *sprio = (uint32_t *)(lds + (a.b_sprio >= 0 ? a.b_sprio : 0));
+  uint32_t *sprio = (uint32_t *)(lds + (kStaged ? a.b_sprio : 0));
   for (int l = tid; l < E; l += NT) s_cost[l] = a.cost[l];
 
   for (int64_t i = blockIdx.x; i < a.n; i += gridDim.x) {
@@ -98,7 +99,9 @@ __global__ __launch_bounds__(NT) __attribute__((
       const uint32_t h = a.mirror ? hops[j] - 1 - cur[j] : cur[j];
       cl[j] = a.path_links[qo[j] + h];
       const uint32_t k = a.gkrank[qo[j] + h];
-      const uint32_t pr = a.b_sprio >= 0 ? sprio[po[j] + h] : gpr[(uint32_t)c * H + h];
+      // a plain LDS read when staged (a run-time choice made this a generic
+      // load that waits for both memory counters)
+      const uint32_t pr = kStaged ? sprio[po[j] + h] : gpr[(uint32_t)c * H + h];
       if (kPack) {
         // k << kr_shift lies in the high word (kr_shift = chunk_bits + 32);
         // the priority straddles the two words: 32-bit shifts only
@@ -132,7 +135,7 @@ __global__ __launch_bounds__(NT) __attribute__((
         }
       }
     }
-    if (a.b_sprio >= 0) {
+    if (kStaged) {
       // chunk offsets: a block scan of the hop counts
       uint32_t nh = 0;
 #pragma unroll
@@ -341,18 +344,24 @@ __global__ __launch_bounds__(NT) __attribute__((
   }
 }
 
-template <int NT, bool kPack>
-const void *block_fn_p(int cpt) {
+template <int NT, bool kPack, bool kStaged>
+const void *block_fn_ps(int cpt) {
   switch (cpt) {
-    case 1: return (const void *)path_greedy_block<1, NT, kPack>;
-    case 2: return (const void *)path_greedy_block<2, NT, kPack>;
-    default: return (const void *)path_greedy_block<4, NT, kPack>;
+    case 1: return (const void *)path_greedy_block<1, NT, kPack, kStaged>;
+    case 2: return (const void *)path_greedy_block<2, NT, kPack, kStaged>;
+    default: return (const void *)path_greedy_block<4, NT, kPack, kStaged>;
   }
+}
+
+template <int NT, bool kPack>
+const void *block_fn_p(int cpt, bool staged) {
+  return staged ? block_fn_ps<NT, kPack, true>(cpt) : block_fn_ps<NT, kPack, false>(cpt);
 }
 
 template <int NT>
 const void *block_fn(const PathGreedyArgs &a) {
-  return a.pack ? block_fn_p<NT, true>(a.cpt) : block_fn_p<NT, false>(a.cpt);
+  const bool staged = a.b_sprio >= 0;
+  return a.pack ? block_fn_p<NT, true>(a.cpt, staged) : block_fn_p<NT, false>(a.cpt, staged);
 }
 
 int bits_for(uint64_t x) {  // bits to hold values 0..x
