@@ -469,14 +469,18 @@ hipError_t launch_path(const PathArgs &a, int grid, hipStream_t stream) {
 
 // ===========================================================================
 // Register-resident Alltoall kernel (paths of <= 6 hops, <= 8 levels,
-// <= 4096 chunks). One 512-thread block evaluates one candidate at a time.
-// Thread t owns chunks t, t+512, ...: their route option's record (hop count,
-// level and class of every hop) and the priorities of their hops are loaded
-// once into registers. Each level then takes O(1) work per send:
-//   A. count the level's sends per (class, top priority bits) bucket;
-//   B. block scan of the bucket counts (classes are ordered by link, then
-//      travelled cost, so a link's sends form one contiguous run);
-//   C. scatter the sends into their buckets;
+// <= 4096 chunks). One block of NT threads evaluates one candidate at a
+// time. Thread t owns chunks t, t+NT, ...: their route option's record (hop
+// count, level and class of every hop) and the priorities of their hops are
+// loaded once into registers. Per candidate:
+//   A. count every send of every level per (class, top priority bits)
+//      bucket (buckets are numbered level by level; within a level classes
+//      are ordered by link, then travelled cost, so a link's sends form one
+//      contiguous run);
+//   B. one block scan of all the bucket counts;
+// then per level, O(1) work per send:
+//   C. place the level's sends in their buckets (an atomic cursor per
+//      bucket: after the level a bucket's cursor is the next one's start);
 //   D. order the few sends that share a bucket by (priority, chunk);
 //   E. time every link's run at once: with link cost c, carried busy time F
 //      and ready times r_j of the run's sends in order, the k-th send
@@ -520,14 +524,19 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int C = a.C, E = a.E, H = a.H, nlev = a.nlev;
+  const uint32_t NBT = (uint32_t)a.nb_total;
 
   uint32_t *s_cost = (uint32_t *)(lds + a.o_fcost);
   uint32_t *s_cinfo = (uint32_t *)(lds + a.o_fcinfo);
   uint32_t *s_cbkt = (uint32_t *)(lds + a.o_fcbkt);
-  uint32_t *s_lcb = (uint32_t *)(lds + a.o_flcb);
+  uint32_t *s_lfb = (uint32_t *)(lds + a.o_flcb);    // [nlev+1] first bucket of a level
   uint32_t *ctime = (uint32_t *)(lds + a.o_fctime);  // a chunk's arrival so far
   uint32_t *lfree = (uint32_t *)(lds + a.o_flfree);  // [2][E]: busy time, next
-  uint32_t *bcnt = (uint32_t *)(lds + a.o_fbcnt);    // bucket counts, then starts
+  // bucket cursors over all levels: bst[0] = 0 and bst[b + 1] holds bucket
+  // b's count, then its start, then (once its level's sends are placed)
+  // its end, so bucket b spans [bst[b], bst[b + 1]) from then on; one dummy
+  // counter per lane follows at bst[NBT + 2 + lane]
+  uint32_t *bst = (uint32_t *)(lds + a.o_fbcnt);
   // bucket entries: priority << 32 | chunk (ascending = Step-2 tie order)
   uint64_t *e64 = (uint64_t *)(lds + a.o_fepr);
   // sorted sends, chunk | link << cb | index in its link run << (cb + lb),
@@ -547,7 +556,12 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
     s_cinfo[j] = a.cinfo[j];
     s_cbkt[j] = a.cbkt[j];
   }
-  for (int j = tid; j <= nlev; j += NT) s_lcb[j] = a.lvl_cls_begin[j];
+  for (int j = tid; j <= nlev; j += NT) {
+    // an empty level starts where the next one does
+    const uint32_t k = a.lvl_cls_begin[j];
+    s_lfb[j] = (j < nlev && k < (uint32_t)a.ncls) ? (a.cbkt[k] & 0xFFFFFFu) : NBT;
+  }
+  for (uint32_t j = tid; j < NBT + 2; j += NT) bst[j] = 0;
   __syncthreads();
 
   // The candidate's route choices, chunk tables and priorities (one batch
@@ -624,16 +638,30 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       lfree[l] = 0;
       lfree[E + l] = kUnset;
     }
+    // ---- A. every send of every level per bucket ----------------------------
+    // Straight-line code: a hop past the route counts on the lane's dummy
+    // counter, so the counter updates of all hops are in flight together.
+#pragma unroll
+    for (int j = 0; j < CPT; j++) {
+      const uint32_t hops = rw0[j] & 0xFF;
+#pragma unroll
+      for (int h = 0; h < kFastMaxHops; h++) {
+        if (h >= H) break;
+        const uint32_t cl = (rcl[j][h >> 1] >> (16 * (h & 1))) & 0xFFFFu;
+        const uint32_t cbk = s_cbkt[cl], bits = cbk >> 24;
+        const uint32_t b = (cbk & 0xFFFFFF) + (bits ? (pr[j][h] >> (32 - bits)) : 0u);
+        atomicAdd(&bst[(uint32_t)h < hops ? b + 1 : NBT + 2 + lane], 1u);
+      }
+    }
     const bool any_unrouted = __syncthreads_or(unrouted);
+    // ---- B. bucket starts ----------------------------------------------------
+    block_excl_scan(bst + 1, (int)NBT, red);
 
     uint32_t mk = 0;
     for (int L = 0; L < nlev; L++) {
-      const uint32_t lo = s_lcb[L];
-      const int ncl = (int)(s_lcb[L + 1] - lo);
-      // buckets of this level: after its last class's first bucket
-      const uint32_t lastb = s_cbkt[lo + ncl - 1];
-      const int NB = ncl ? (int)((lastb & 0xFFFFFF) + (1u << (lastb >> 24))) : 0;
-      for (int j = tid; j <= NB; j += NT) bcnt[j] = 0;
+      // this level's first position among all levels' sends (the end of the
+      // previous level's last bucket, untouched during this level)
+      const uint32_t lb0 = bst[s_lfb[L]];
       // busy times after the previous level (a link without a send there
       // keeps its time)
       for (int l = tid; l < E; l += NT) {
@@ -641,15 +669,10 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
         if (nx != kUnset) lfree[l] = nx;
         lfree[E + l] = kUnset;
       }
-      __syncthreads();
-
-      // ---- A. the level's sends per bucket ---------------------------------
-      // wa: bucket | first bucket of the send's link run << 16 (kUnset: no
-      // send at this level); wb: index in the bucket | link << 16
-      // Straight-line code (selects, and a per-lane dummy counter past the
-      // level's buckets for a slot without a send) so that the LDS loads and
-      // counter updates of all slots are in flight together.
-      uint32_t wa[CPT], wb[CPT], pl[CPT], cls[CPT];
+      // ---- C. place the level's sends ----------------------------------------
+      // Straight-line code (selects, and the lane's dummy counter for a slot
+      // without a send here) so that the LDS loads and cursor updates of all
+      // slots are in flight together.
 #pragma unroll
       for (int j = 0; j < CPT; j++) {
         const uint32_t h = (hmap[j] >> (3 * L)) & 7;  // 7: no hop at this level
@@ -660,20 +683,18 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
           if (h == (uint32_t)t) pv = pr[j][t];
         if (h >= 2) cw = rcl[j][1];
         if (h >= 4) cw = rcl[j][2];
-        cls[j] = act ? ((h & 1) ? (cw >> 16) : (cw & 0xFFFF)) : lo;
-        const uint32_t cbk = s_cbkt[cls[j]], ci = s_cinfo[cls[j]];
-        const uint32_t bits = cbk >> 24;
+        const uint32_t cl = (h & 1) ? (cw >> 16) : (cw & 0xFFFF);
+        const uint32_t cbk = s_cbkt[cl], bits = cbk >> 24;
         const uint32_t b = (cbk & 0xFFFFFF) + (bits ? (pv >> (32 - bits)) : 0u);
-        const uint32_t slot = atomicAdd(&bcnt[act ? b : (uint32_t)NB + 1 + lane], 1u);
-        pl[j] = pv;
-        wa[j] = act ? (b | ((ci >> 16) << 16)) : kUnset;
-        wb[j] = slot | ((ci & 0xFFFFu) << 16);
+        const uint32_t gp = atomicAdd(&bst[act ? b + 1 : NBT + 2 + lane], 1u);
+        if (act) {
+          e64[gp - lb0] = ((uint64_t)pv << 32) | (uint32_t)(tid + NT * j);
+          aux[gp - lb0] = b | (cl << 16);
+        }
       }
       if (L == nlev - 1) load_inputs(i + gridDim.x);  // this candidate's inputs are dead
       __syncthreads();
-      // ---- B. bucket starts --------------------------------------------------
-      block_excl_scan(bcnt, NB, red);
-      const uint32_t tot = bcnt[NB];
+      const uint32_t tot = bst[s_lfb[L + 1]] - lb0;
       const uint32_t ept = (tot + NT - 1) / NT;  // <= CPT: a level has <= C sends
       // pos / ept for pos < 2^16 and ept <= 4 (the same for every thread):
       // a shift, or (pos * 43691) >> 17 for 3 (exact below 2^17); 24-bit
@@ -685,20 +706,6 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       // the contiguity walker divides with one 64-bit multiply
       // (y / ept = (y * em) >> 32, em = floor((2^32 - 1) / ept) + 1)
       const uint64_t em = (kContig && ept) ? 0xFFFFFFFFull / ept + 1 : 0;
-      // ---- C. scatter --------------------------------------------------------
-      {
-        uint32_t pos[CPT];
-#pragma unroll
-        for (int j = 0; j < CPT; j++)
-          pos[j] = bcnt[wa[j] != kUnset ? wa[j] & 0xFFFFu : 0u] + (wb[j] & 0xFFFFu);
-#pragma unroll
-        for (int j = 0; j < CPT; j++)
-          if (wa[j] != kUnset) {
-            e64[pos[j]] = ((uint64_t)pl[j] << 32) | (uint32_t)(tid + NT * j);
-            aux[pos[j]] = (wa[j] & 0xFFFFu) | (cls[j] << 16);
-          }
-      }
-      __syncthreads();
       // ---- D. order inside buckets by (priority, chunk); record each send's
       //      link and its index in the link's run -------------------------
       // One lane per bucket-sorted position: neighbouring lanes hold
@@ -709,7 +716,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
         const uint64_t me = e64[x];
         const uint32_t ax = aux[x];
         const uint32_t b = ax & 0xFFFFu, ci = s_cinfo[ax >> 16];
-        const uint32_t b0 = bcnt[b], b1 = bcnt[b + 1], rs = bcnt[ci >> 16];
+        const uint32_t b0 = bst[b] - lb0, b1 = bst[b + 1] - lb0, rs = bst[ci >> 16] - lb0;
         // four members a step (three spare entries past the array's end;
         // entries past the bucket never count)
         uint32_t rank = 0;
@@ -871,6 +878,8 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       a.makespan[i] = m;
       a.valid[i] = (uint8_t)!any_unrouted;
     }
+    // the next candidate's bucket counters (the last level's ordering is done)
+    for (uint32_t j = tid; j <= NBT; j += NT) bst[j + 1] = 0;
     __syncthreads();
   }
 }
@@ -887,6 +896,7 @@ int32_t path_fast_layout(const taccl_plan &p, PathArgs &a) {
     return o;
   };
   a.ncls = p.ncls;
+  a.nb_total = p.nb_total;
   a.o_fcost = take(4 * E);
   a.o_fmerge = take(E);
   a.o_fcinfo = take(4 * std::max(p.ncls, 1));
@@ -894,9 +904,9 @@ int32_t path_fast_layout(const taccl_plan &p, PathArgs &a) {
   a.o_flcb = take(4 * (p.nlev + 1));
   a.o_fctime = take(4 * C);
   a.o_flfree = take(8 * E);
-  // bucket counters, the level's total, and one dummy counter per lane of a
-  // wavefront (slots without a send count there)
-  a.o_fbcnt = take(4 * (p.max_lvl_nb + 1 + 64));
+  // a zero, the bucket cursors of all levels, the total, and one dummy
+  // counter per lane of a wavefront (slots without a send count there)
+  a.o_fbcnt = take(4 * (p.nb_total + 2 + 64));
   a.o_fepr = take(8 * (M + 3));
   a.o_faux = take(4 * M);
   a.o_fsrt = take(4 * path_fast_threads(p) * path_fast_cpt(p));
@@ -927,7 +937,7 @@ int path_fast_cpt(const taccl_plan &p) {
   };
   if (2 * bits((uint32_t)p.coll.C) + bits((uint32_t)p.topo.E) > 32) return 0;
   // bucket and link fields are packed into 16 bits
-  if (p.max_lvl_nb >= (1 << 16) || p.topo.E > (1 << 16)) return 0;
+  if (p.nb_total > kFastMaxBuckets || p.topo.E > (1 << 16)) return 0;
   // sorted positions below 2^16 and link costs below 2^24 (24-bit multiplies)
   if (p.max_lvl_sends > (1 << 16)) return 0;
   for (uint32_t c : p.cost)

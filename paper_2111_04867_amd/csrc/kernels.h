@@ -88,7 +88,7 @@ struct PathArgs {
   int64_t n;
   int32_t o_qc, o_ctime, o_lfree, o_ccnt, o_ccur, o_e64, o_ecls, o_sorted, o_red, max_lvl;
   // register-resident kernel
-  int32_t ncls;
+  int32_t ncls, nb_total;
   const uint32_t *arec, *cpath, *cinfo, *cbkt;
   int32_t o_faux;
   int32_t o_fcost, o_fcinfo, o_fcbkt, o_flcb, o_fctime, o_flfree, o_fbcnt, o_fepr, o_fsrt, o_fred;

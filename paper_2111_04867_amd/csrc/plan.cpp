@@ -505,7 +505,9 @@ static taccl_status_t build_levels(taccl_plan *p) {
     }
     // priority sub-buckets per class, sized from the class's expected
     // membership under uniform route choice so a bucket holds 1-2 sends
-    // (any input stays exact: a crowded bucket is only slower to order)
+    // (any input stays exact: a crowded bucket is only slower to order),
+    // then halved all over until every level's buckets together fit the
+    // kernel's counters
     std::vector<double> expect(p->ncls, 0.0);
     for (int32_t s2 = 0; s2 < P; s2++)
       for (int32_t d2 = 0; d2 < P; d2++) {
@@ -518,17 +520,21 @@ static taccl_status_t build_levels(taccl_plan *p) {
             expect[p->hop_class[j]] += (double)cpr / np;
         }
       }
+    std::vector<int> cbits(p->ncls, 0);
+    for (int32_t k = 0; k < p->ncls; k++)
+      while (cbits[k] < 10 && (double)(2u << cbits[k]) <= expect[k]) cbits[k]++;
     p->cbkt.assign(p->ncls, 0);
-    p->max_lvl_nb = 1;
-    for (int32_t L = 0; L < p->nlev; L++) {
-      uint32_t nb = 0;
-      for (uint32_t k = p->lvl_cls_begin[L]; k < p->lvl_cls_begin[L + 1]; k++) {
-        int bits = 0;
-        while (bits < 10 && (double)(2u << bits) <= expect[k]) bits++;
-        p->cbkt[k] = nb | ((uint32_t)bits << 24);
-        nb += 1u << bits;
+    for (;;) {
+      // classes are numbered level by level, so one running count numbers
+      // every level's buckets in level order
+      uint64_t nb = 0;
+      for (int32_t k = 0; k < p->ncls; k++) {
+        p->cbkt[k] = (uint32_t)nb | ((uint32_t)cbits[k] << 24);
+        nb += 1u << cbits[k];
       }
-      p->max_lvl_nb = std::max<int32_t>(p->max_lvl_nb, (int32_t)nb);
+      p->nb_total = (int32_t)std::min<uint64_t>(nb, INT32_MAX);
+      if (nb <= (uint64_t)kFastMaxBuckets || p->ncls > kFastMaxBuckets) break;
+      for (int &b : cbits) b = std::max(b - 1, 0);
     }
     p->cinfo.assign(p->ncls, 0);
     for (int32_t L = 0; L < p->nlev; L++)

@@ -14,6 +14,9 @@ namespace taccl {
 // Limits of the register-resident Alltoall kernel.
 constexpr int kFastMaxHops = 6;
 constexpr int kFastMaxChunks = 4096;
+// priority sub-buckets of all levels together in the register-resident
+// Alltoall kernel (one LDS counter each)
+constexpr int kFastMaxBuckets = 16384;
 // chunk table entry of a pair that has no route option at all
 constexpr uint32_t kNoRoute = 0x00FFFFFFu;
 
@@ -143,13 +146,14 @@ struct taccl_plan {
   // register-resident Alltoall kernel: per route option {hops | level of
   // hop h << (8+3h), classes of hops 0..5 as u16 pairs}; per chunk its pair's
   // first option | option count << 24 (kNoRoute: the pair has no option);
-  // per class link | (first bucket of the same level and link,
-  // level-relative) << 16
+  // per class link | (first bucket of the same level and link) << 16
   bool path_fast = false;
   std::vector<uint32_t> arec, cpath, cinfo;
-  // per class: first priority sub-bucket (level-relative) | bits << 24
+  // per class: first priority sub-bucket | bits << 24. Buckets are numbered
+  // over all levels at once (level by level, class by class), nb_total of
+  // them.
   std::vector<uint32_t> cbkt;
-  int32_t max_lvl_nb = 0;
+  int32_t nb_total = 0;
   // Alltoall greedy orders: per hop (index into path_links) the rank of its
   // Step-2 key (remaining desc, travelled asc) among all hops of the plan,
   // with the lengths of the greedy's direction (mirrored in reverse path
