@@ -17,6 +17,8 @@
 // path always reaches its destination); the makespan is the latest finish.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "kernels.h"
 #include "wave.h"
 
@@ -739,24 +741,31 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       // values): a prefix maximum segmented by runs, which are contiguous
       // along the sorted positions. Thread tid owns sorted positions
       // [tid*ept, tid*ept + ept); every load is issued unmasked (stale
-      // entries are clamped to in-range indexes and never used).
-      const uint32_t x0 = (uint32_t)tid * ept;
-      uint32_t pis[CPT], ct[CPT], cs[CPT], lf[CPT];
+      // entries are clamped to in-range indexes and never used). Without
+      // contiguity the level's ept (the same for every thread) is a
+      // compile-time constant EP in each copy of the pass below; with it,
+      // one copy takes EP = CPT and the level's ept at run time (keeping the
+      // run walker in one copy).
+      auto time_level = [&](auto ep_c) {
+      constexpr int EP = decltype(ep_c)::value;
+      const uint32_t epr = kContig ? ept : (uint32_t)EP;
+      const uint32_t x0 = (uint32_t)tid * epr;
+      uint32_t pis[EP], ct[EP], cs[EP], lf[EP];
 #pragma unroll
-      for (int q = 0; q < CPT; q++) pis[q] = pinfo[q * NT + tid];
+      for (int q = 0; q < EP; q++) pis[q] = pinfo[q * NT + tid];
 #pragma unroll
-      for (int q = 0; q < CPT; q++) {
+      for (int q = 0; q < EP; q++) {
         const uint32_t l = min((pis[q] >> cb) & lmask, (uint32_t)E - 1);
         ct[q] = ctime[min(pis[q] & cmask, (uint32_t)C - 1)];
         cs[q] = s_cost[l];
         lf[q] = lfree[l];
       }
       // this thread's positions: segmented running maxima s[q]
-      const uint32_t nv = tot > x0 ? min(ept, tot - x0) : 0u;  // valid positions
-      uint32_t sv[CPT];
+      const uint32_t nv = tot > x0 ? min(epr, tot - x0) : 0u;  // valid positions
+      uint32_t sv[EP];
       uint32_t prev = 0;
 #pragma unroll
-      for (int q = 0; q < CPT; q++) {
+      for (int q = 0; q < EP; q++) {
         const uint32_t k = pis[q] >> kb, kc = __umul24(k, cs[q]);  // k < 2^16, c < 2^24
         const uint32_t av = k == 0 ? max(ct[q], lf[q]) : (ct[q] > kc ? ct[q] - kc : 0u);
         sv[q] = (k > 0 && q > 0) ? max(prev, av) : av;
@@ -766,10 +775,10 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       // whether it began before the thread's first position (then the
       // maximum of earlier threads of the same run joins in); a thread
       // without positions passes its predecessors' value on
-      const uint32_t kl = nv ? (pis[nv - 1 < CPT ? nv - 1 : 0] >> kb) : 0u;
+      const uint32_t kl = nv ? (pis[nv - 1 < EP ? nv - 1 : 0] >> kb) : 0u;
       uint32_t gv = 0, pass = nv == 0 ? 1u : (kl >= nv ? 1u : 0u);
 #pragma unroll
-      for (int q = 0; q < CPT; q++)
+      for (int q = 0; q < EP; q++)
         if ((uint32_t)q + 1 == nv) gv = sv[q];
       // inclusive scan of (value, pass) pairs over the lanes: a lane that
       // passes takes the maximum of the lanes before it, up to and
@@ -815,9 +824,9 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       // finish times
       const uint32_t nxt0 = (tid + 1 < NT) ? pinfo[tid + 1] : 0u;  // next thread's first
 #pragma unroll
-      for (int q = 0; q < CPT; q++) {
+      for (int q = 0; q < EP; q++) {
         const uint32_t x = x0 + q;
-        if ((uint32_t)q < ept && x < tot) {
+        if ((uint32_t)q < epr && x < tot) {
           const uint32_t c = pis[q] & cmask, l = (pis[q] >> cb) & lmask, k = pis[q] >> kb;
           if (kContig && s_merge[l]) {
             // contiguous transfers: the run's first position walks the run
@@ -861,8 +870,23 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
           const uint32_t f = __umul24(k + 1, cl) + best;
           ctime[c] = f;
           mk = max(mk, f);
-          const uint32_t nk = ((uint32_t)q + 1 < ept ? pis[q < CPT - 1 ? q + 1 : q] : nxt0) >> kb;
+          const uint32_t nk = ((uint32_t)q + 1 < epr ? pis[q < EP - 1 ? q + 1 : q] : nxt0) >> kb;
           if (x + 1 == tot || nk == 0) lfree[E + l] = f;  // last send of the link's run
+        }
+      }
+      };
+      if constexpr (kContig) {
+        time_level(std::integral_constant<int, CPT>{});
+      } else if (ept <= 1) {
+        time_level(std::integral_constant<int, 1>{});
+      } else if constexpr (CPT >= 2) {
+        if (ept == 2) {
+          time_level(std::integral_constant<int, 2>{});
+        } else if constexpr (CPT >= 4) {
+          if (ept == 3)
+            time_level(std::integral_constant<int, 3>{});
+          else
+            time_level(std::integral_constant<int, 4>{});
         }
       }
       __syncthreads();
