@@ -496,28 +496,48 @@ namespace {
 
 constexpr uint32_t kUnset = 0xFFFFFFFFu;
 
-// exclusive scan of cnt[0..n) in place, cnt[n] = total (all threads call)
-__device__ void block_excl_scan(uint32_t *cnt, int n, uint32_t *wsum) {
-  const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63, wave = tid >> 6;
-  const int per = (n + nt - 1) / nt;
-  const int b = min(tid * per, n), e = min(b + per, n);
+// Exclusive scan of cnt[0..n) in place with cnt[n] = total (all threads
+// call; cnt 16-byte aligned; cnt[n+1..n+3] are overwritten as well). Each
+// wavefront takes a contiguous range of 4-word groups and each lane one
+// group per round, so a round reads 1 KB of consecutive words: one pass
+// for the wavefront totals, one to write the prefixes.
+__device__ void block_excl_scan4(uint32_t *cnt, int n, uint32_t *wsum) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
+  const int ng = (n >> 2) + 1;  // groups up to and including index n
+  const int gpw = ((ng + nw - 1) / nw + 63) & ~63;
+  const int g0 = wave * gpw;
+  uint4 *c4 = (uint4 *)cnt;
+  auto group = [&](int g) {  // entries from index n on count as 0
+    uint4 x = g < ng ? c4[g] : make_uint4(0u, 0u, 0u, 0u);
+    const int e = 4 * g;
+    x.x = e < n ? x.x : 0u;
+    x.y = e + 1 < n ? x.y : 0u;
+    x.z = e + 2 < n ? x.z : 0u;
+    x.w = e + 3 < n ? x.w : 0u;
+    return x;
+  };
   uint32_t sum = 0;
-  for (int j = b; j < e; j++) sum += cnt[j];
-  const uint32_t incl = wave_scan_add(sum);
-  if (lane == 63) wsum[wave] = incl;
-  __syncthreads();
-  // offset of this wave: every wave scans the (at most 16) wave totals
-  // itself instead of summing them one by one
-  const uint32_t ws = row_scan_add(lane < (nt >> 6) ? wsum[lane] : 0u);
-  const uint32_t w = (uint32_t)__builtin_amdgcn_readfirstlane(wave);
-  const uint32_t off = w ? (uint32_t)__builtin_amdgcn_readlane((int)ws, w - 1) : 0u;
-  uint32_t run = off + incl - sum;
-  for (int j = b; j < e; j++) {
-    const uint32_t x = cnt[j];
-    cnt[j] = run;
-    run += x;
+  for (int r = 0; r < gpw; r += 64) {
+    const uint4 x = group(g0 + r + lane);
+    sum += x.x + x.y + x.z + x.w;
   }
-  if (tid == nt - 1) cnt[n] = off + incl;
+  const uint32_t wt = (uint32_t)__builtin_amdgcn_readlane((int)wave_scan_add(sum), 63);
+  if (lane == 0) wsum[wave] = wt;
+  __syncthreads();
+  const uint32_t ws = row_scan_add(lane < nw ? wsum[lane] : 0u);
+  const uint32_t w = (uint32_t)__builtin_amdgcn_readfirstlane(wave);
+  uint32_t run = w ? (uint32_t)__builtin_amdgcn_readlane((int)ws, w - 1) : 0u;
+  for (int r = 0; r < gpw; r += 64) {
+    const int g = g0 + r + lane;
+    const uint4 x = group(g);
+    const uint32_t gs = x.x + x.y + x.z + x.w;
+    const uint32_t inc = wave_scan_add(gs);
+    const uint32_t e0 = run + inc - gs;
+    // the group holding index n receives the total there (later entries
+    // count as 0)
+    if (g < ng) c4[g] = make_uint4(e0, e0 + x.x, e0 + x.x + x.y, e0 + x.x + x.y + x.z);
+    run += (uint32_t)__builtin_amdgcn_readlane((int)inc, 63);
+  }
   __syncthreads();
 }
 
@@ -537,8 +557,9 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
   // bucket cursors over all levels: bst[0] = 0 and bst[b + 1] holds bucket
   // b's count, then its start, then (once its level's sends are placed)
   // its end, so bucket b spans [bst[b], bst[b + 1]) from then on; one dummy
-  // counter per lane follows at bst[NBT + 2 + lane]
-  uint32_t *bst = (uint32_t *)(lds + a.o_fbcnt);
+  // counter per lane follows at bst[NBT + 2 + lane]. bst + 1 is 16-byte
+  // aligned for the scan.
+  uint32_t *bst = (uint32_t *)(lds + a.o_fbcnt) + 3;
   // bucket entries: priority << 32 | chunk (ascending = Step-2 tie order)
   uint64_t *e64 = (uint64_t *)(lds + a.o_fepr);
   // sorted sends, chunk | link << cb | index in its link run << (cb + lb),
@@ -657,7 +678,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
     }
     const bool any_unrouted = __syncthreads_or(unrouted);
     // ---- B. bucket starts ----------------------------------------------------
-    block_excl_scan(bst + 1, (int)NBT, red);
+    block_excl_scan4(bst + 1, (int)NBT, red);
 
     uint32_t mk = 0;
     for (int L = 0; L < nlev; L++) {
@@ -928,9 +949,10 @@ int32_t path_fast_layout(const taccl_plan &p, PathArgs &a) {
   a.o_flcb = take(4 * (p.nlev + 1));
   a.o_fctime = take(4 * C);
   a.o_flfree = take(8 * E);
-  // a zero, the bucket cursors of all levels, the total, and one dummy
-  // counter per lane of a wavefront (slots without a send count there)
-  a.o_fbcnt = take(4 * (p.nb_total + 2 + 64));
+  // three words of padding, a zero, the bucket cursors of all levels, the
+  // total, and one dummy counter per lane of a wavefront (slots without a
+  // send count there)
+  a.o_fbcnt = take(4 * (3 + p.nb_total + 2 + 64));
   a.o_fepr = take(8 * (M + 3));
   a.o_faux = take(4 * M);
   a.o_fsrt = take(4 * path_fast_threads(p) * path_fast_cpt(p));
