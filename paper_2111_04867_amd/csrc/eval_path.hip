@@ -560,12 +560,14 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
   // counter per lane follows at bst[NBT + 2 + lane]. bst + 1 is 16-byte
   // aligned for the scan.
   uint32_t *bst = (uint32_t *)(lds + a.o_fbcnt) + 3;
-  // bucket entries: priority << 32 | chunk (ascending = Step-2 tie order)
+  // bucket entries: priority << 32 | link << cb | chunk (ascending =
+  // Step-2 tie order: a bucket's sends share one link)
   uint64_t *e64 = (uint64_t *)(lds + a.o_fepr);
   // sorted sends, chunk | link << cb | index in its link run << (cb + lb),
   // stored transposed: position t*ept + q of thread t's range at q*NT + t
   uint32_t *pinfo = (uint32_t *)(lds + a.o_fsrt);
-  // per bucket-sorted position: its bucket | its class << 16
+  // per bucket-sorted position: its bucket | the first bucket of its link's
+  // run << 16
   uint32_t *aux = (uint32_t *)(lds + a.o_faux);
   const uint32_t cb = a.cbits, lb = a.lbits, kb = cb + lb;
   const uint32_t cmask = (1u << cb) - 1, lmask = (1u << lb) - 1;
@@ -707,12 +709,12 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
         if (h >= 2) cw = rcl[j][1];
         if (h >= 4) cw = rcl[j][2];
         const uint32_t cl = (h & 1) ? (cw >> 16) : (cw & 0xFFFF);
-        const uint32_t cbk = s_cbkt[cl], bits = cbk >> 24;
+        const uint32_t cbk = s_cbkt[cl], ci = s_cinfo[cl], bits = cbk >> 24;
         const uint32_t b = (cbk & 0xFFFFFF) + (bits ? (pv >> (32 - bits)) : 0u);
         const uint32_t gp = atomicAdd(&bst[act ? b + 1 : NBT + 2 + lane], 1u);
         if (act) {
-          e64[gp - lb0] = ((uint64_t)pv << 32) | (uint32_t)(tid + NT * j);
-          aux[gp - lb0] = b | (cl << 16);
+          e64[gp - lb0] = ((uint64_t)pv << 32) | (uint32_t)(tid + NT * j) | ((ci & 0xFFFFu) << cb);
+          aux[gp - lb0] = b | (ci & 0xFFFF0000u);
         }
       }
       if (L == nlev - 1) load_inputs(i + gridDim.x);  // this candidate's inputs are dead
@@ -738,8 +740,8 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       for (uint32_t x = (uint32_t)tid; x < tot; x += NT) {
         const uint64_t me = e64[x];
         const uint32_t ax = aux[x];
-        const uint32_t b = ax & 0xFFFFu, ci = s_cinfo[ax >> 16];
-        const uint32_t b0 = bst[b] - lb0, b1 = bst[b + 1] - lb0, rs = bst[ci >> 16] - lb0;
+        const uint32_t b = ax & 0xFFFFu;
+        const uint32_t b0 = bst[b] - lb0, b1 = bst[b + 1] - lb0, rs = bst[ax >> 16] - lb0;
         // four members a step (three spare entries past the array's end;
         // entries past the bucket never count)
         uint32_t rank = 0;
@@ -752,7 +754,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
         }
         const uint32_t pos = b0 + rank;
         const uint32_t t = div_ept(pos), q = pos - __umul24(t, ept);
-        pinfo[q * NT + t] = (uint32_t)me | ((ci & 0xFFFFu) << cb) | ((pos - rs) << kb);
+        pinfo[q * NT + t] = (uint32_t)me | ((pos - rs) << kb);
       }
       __syncthreads();
       // ---- E. finish times of every link run --------------------------------
