@@ -587,6 +587,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
     s_lfb[j] = (j < nlev && k < (uint32_t)a.ncls) ? (a.cbkt[k] & 0xFFFFFFu) : NBT;
   }
   for (uint32_t j = tid; j < NBT + 2; j += NT) bst[j] = 0;
+  for (int j = tid; j < NT * CPT; j += NT) pinfo[j] = 0;
   __syncthreads();
 
   // The candidate's route choices, chunk tables and priorities (one batch
@@ -763,8 +764,10 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       // and a_j = max(r_j - j c, 0) after it (F >= 0 dominates the clipped
       // values): a prefix maximum segmented by runs, which are contiguous
       // along the sorted positions. Thread tid owns sorted positions
-      // [tid*ept, tid*ept + ept); every load is issued unmasked (stale
-      // entries are clamped to in-range indexes and never used). Without
+      // [tid*ept, tid*ept + ept); every load is issued unmasked (an entry
+      // past the level's sends holds a send of an earlier level, or the
+      // zero it started with, so its indexes are in range; its values are
+      // never used). Without
       // contiguity the level's ept (the same for every thread) is a
       // compile-time constant EP in each copy of the pass below; with it,
       // one copy takes EP = CPT and the level's ept at run time (keeping the
@@ -778,8 +781,8 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       for (int q = 0; q < EP; q++) pis[q] = pinfo[q * NT + tid];
 #pragma unroll
       for (int q = 0; q < EP; q++) {
-        const uint32_t l = min((pis[q] >> cb) & lmask, (uint32_t)E - 1);
-        ct[q] = ctime[min(pis[q] & cmask, (uint32_t)C - 1)];
+        const uint32_t l = (pis[q] >> cb) & lmask;
+        ct[q] = ctime[pis[q] & cmask];
         cs[q] = s_cost[l];
         lf[q] = lfree[l];
       }
@@ -790,7 +793,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
 #pragma unroll
       for (int q = 0; q < EP; q++) {
         const uint32_t k = pis[q] >> kb, kc = __umul24(k, cs[q]);  // k < 2^16, c < 2^24
-        const uint32_t av = k == 0 ? max(ct[q], lf[q]) : (ct[q] > kc ? ct[q] - kc : 0u);
+        const uint32_t av = k == 0 ? max(ct[q], lf[q]) : __builtin_elementwise_sub_sat(ct[q], kc);
         sv[q] = (k > 0 && q > 0) ? max(prev, av) : av;
         prev = sv[q];
       }
