@@ -623,13 +623,14 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
     // ---- setup: owned chunks' records in registers -----------------------
     int tv = tid;
     asm volatile("" : "+v"(tv));
-    uint32_t rw0[CPT], rcl[CPT][3], hmap[CPT];
+    // rw0: hop count | level -> hop index << 8 (3 bits per level, 7 = none)
+    uint32_t rw0[CPT], rcl[CPT][3];
     bool unrouted = false;
     // second batch: the chosen route records
 #pragma unroll
     for (int j = 0; j < CPT; j++) {
       const int c = tv + NT * j;
-      rw0[j] = 0;
+      rw0[j] = 0xFFFFFFu << 8;
       rcl[j][0] = rcl[j][1] = rcl[j][2] = 0;
       if (c < C) {
         const uint32_t np = cp[j] >> 24;
@@ -647,18 +648,6 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
         }
         ctime[c] = 0;
       }
-    }
-#pragma unroll
-    for (int j = 0; j < CPT; j++) {
-      // level -> hop index (3 bits per level, 7 = none)
-      hmap[j] = 0xFFFFFFu;
-      const int hops = rw0[j] & 0xFF;
-#pragma unroll
-      for (int t = 0; t < kFastMaxHops; t++)
-        if (t < hops) {
-          const uint32_t lv = (rw0[j] >> (8 + 3 * t)) & 7;
-          hmap[j] = (hmap[j] & ~(7u << (3 * lv))) | ((uint32_t)t << (3 * lv));
-        }
     }
     for (int l = tid; l < E; l += NT) {
       lfree[l] = 0;
@@ -701,7 +690,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       // slots are in flight together.
 #pragma unroll
       for (int j = 0; j < CPT; j++) {
-        const uint32_t h = (hmap[j] >> (3 * L)) & 7;  // 7: no hop at this level
+        const uint32_t h = (rw0[j] >> (8 + 3 * L)) & 7;  // 7: no hop at this level
         const bool act = h < (uint32_t)kFastMaxHops;
         uint32_t cw = rcl[j][0], pv = pr[j][0];
 #pragma unroll

@@ -485,12 +485,14 @@ static taccl_status_t build_levels(taccl_plan *p) {
       uint32_t *r = &p->arec[q * 4];
       uint64_t rem = p->path_cost[q];
       int32_t h = 0;
+      uint32_t hm = 0xFFFFFFu;  // level -> hop, 3 bits per level (7: none)
       for (uint32_t j = p->path_off[q]; j < p->path_off[q + 1]; j++, h++) {
-        r[0] |= (uint32_t)level_of(rem) << (8 + 3 * h);
+        const uint32_t lv = (uint32_t)level_of(rem);
+        hm = (hm & ~(7u << (3 * lv))) | ((uint32_t)h << (3 * lv));
         r[1 + h / 2] |= (uint32_t)p->hop_class[j] << (16 * (h & 1));
         rem -= p->cost[p->path_links[j]];
       }
-      r[0] |= (uint32_t)h;
+      r[0] = (uint32_t)h | (hm << 8);
     }
     const int32_t C = p->coll.C, cpr = p->coll.cpr;
     p->cpath.assign(C, 0);

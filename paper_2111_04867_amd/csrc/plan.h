@@ -143,8 +143,9 @@ struct taccl_plan {
   std::vector<uint32_t> lvl_cls_begin; // [nlev+1]
   std::vector<uint32_t> llc;           // [nlev*E*2] class range of a link at a level
   std::vector<uint16_t> cls_link;      // [ncls]
-  // register-resident Alltoall kernel: per route option {hops | level of
-  // hop h << (8+3h), classes of hops 0..5 as u16 pairs}; per chunk its pair's
+  // register-resident Alltoall kernel: per route option {hops | the hop at
+  // each level (3 bits per level, 7: none) << 8, classes of hops 0..5 as u16
+  // pairs}; per chunk its pair's
   // first option | option count << 24 (kNoRoute: the pair has no option);
   // per class link | (first bucket of the same level and link) << 16
   bool path_fast = false;
