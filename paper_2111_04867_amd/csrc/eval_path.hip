@@ -612,9 +612,10 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       if (c < C) {
         kk[j] = grt[c];
         cp[j] = a.cpath[c];
+        // one address per chunk; the hops are immediate offsets from it
+        const uint32_t *row = gpr + __umul24((uint32_t)c, (uint32_t)H);
 #pragma unroll
-        for (int h = 0; h < kFastMaxHops; h++)
-          pr[j][h] = h < H ? gpr[(uint32_t)(c * H + h)] : 0u;
+        for (int h = 0; h < kFastMaxHops; h++) pr[j][h] = h < H ? row[h] : 0u;
       }
     }
   };
