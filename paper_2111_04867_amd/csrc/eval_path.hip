@@ -722,13 +722,31 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       // the contiguity walker divides with one 64-bit multiply
       // (y / ept = (y * em) >> 32, em = floor((2^32 - 1) / ept) + 1)
       const uint64_t em = (kContig && ept) ? 0xFFFFFFFFull / ept + 1 : 0;
+      // The level's ordering and timing passes. Without contiguity the
+      // level's ept (the same for every thread) is a compile-time constant
+      // EP in each copy of them below; with it, one copy takes EP = CPT and
+      // the level's ept at run time (keeping the run walker in one copy).
+      auto order_and_time = [&](auto ep_c) {
+      constexpr int EP = decltype(ep_c)::value;
+      const uint32_t epr = kContig ? ept : (uint32_t)EP;
       // ---- D. order inside buckets by (priority, chunk); record each send's
       //      link and its index in the link's run -------------------------
       // One lane per bucket-sorted position: neighbouring lanes hold
       // neighbouring buckets, so their members are read with few bank
       // conflicts, and a pass waits only for the largest bucket among its
       // 64 positions.
-      for (uint32_t x = (uint32_t)tid; x < tot; x += NT) {
+      auto div_e = [&](uint32_t pos) -> uint32_t {
+        if constexpr (kContig)
+          return div_ept(pos);
+        else if constexpr (EP == 3)
+          return __umul24(pos, 43691u) >> 17;
+        else
+          return pos >> (EP == 4 ? 2 : EP == 2 ? 1 : 0);
+      };
+#pragma unroll
+      for (int qq = 0; qq < EP; qq++) {
+        const uint32_t x = (uint32_t)tid + (uint32_t)(qq * NT);
+        if (x >= tot) break;
         const uint64_t me = e64[x];
         const uint32_t ax = aux[x];
         const uint32_t b = ax & 0xFFFFu;
@@ -744,7 +762,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
           for (int u = 0; u < 4; u++) rank += (uint32_t)((y + u < b1) & (m[u] < me));
         }
         const uint32_t pos = b0 + rank;
-        const uint32_t t = div_ept(pos), q = pos - __umul24(t, ept);
+        const uint32_t t = div_e(pos), q = pos - __umul24(t, epr);
         pinfo[q * NT + t] = (uint32_t)me | ((pos - rs) << kb);
       }
       __syncthreads();
@@ -757,14 +775,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       // [tid*ept, tid*ept + ept); every load is issued unmasked (an entry
       // past the level's sends holds a send of an earlier level, or the
       // zero it started with, so its indexes are in range; its values are
-      // never used). Without
-      // contiguity the level's ept (the same for every thread) is a
-      // compile-time constant EP in each copy of the pass below; with it,
-      // one copy takes EP = CPT and the level's ept at run time (keeping the
-      // run walker in one copy).
-      auto time_level = [&](auto ep_c) {
-      constexpr int EP = decltype(ep_c)::value;
-      const uint32_t epr = kContig ? ept : (uint32_t)EP;
+      // never used).
       const uint32_t x0 = (uint32_t)tid * epr;
       uint32_t pis[EP], ct[EP], cs[EP], lf[EP];
 #pragma unroll
@@ -892,17 +903,17 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       }
       };
       if constexpr (kContig) {
-        time_level(std::integral_constant<int, CPT>{});
+        order_and_time(std::integral_constant<int, CPT>{});
       } else if (ept <= 1) {
-        time_level(std::integral_constant<int, 1>{});
+        order_and_time(std::integral_constant<int, 1>{});
       } else if constexpr (CPT >= 2) {
         if (ept == 2) {
-          time_level(std::integral_constant<int, 2>{});
+          order_and_time(std::integral_constant<int, 2>{});
         } else if constexpr (CPT >= 4) {
           if (ept == 3)
-            time_level(std::integral_constant<int, 3>{});
+            order_and_time(std::integral_constant<int, 3>{});
           else
-            time_level(std::integral_constant<int, 4>{});
+            order_and_time(std::integral_constant<int, 4>{});
         }
       }
       __syncthreads();
