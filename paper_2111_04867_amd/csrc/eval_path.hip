@@ -496,6 +496,12 @@ namespace {
 
 constexpr uint32_t kUnset = 0xFFFFFFFFu;
 
+// The top `bits` bits of x (0 for bits = 0): one bit-field extract, whose
+// width 0 gives 0
+__device__ __forceinline__ uint32_t top_bits(uint32_t x, uint32_t bits) {
+  return __builtin_amdgcn_ubfe(x, 32u - bits, bits);
+}
+
 // Exclusive scan of cnt[0..n) in place with cnt[n] = total (all threads
 // call; cnt 16-byte aligned; cnt[n+1..n+3] are overwritten as well). Each
 // wavefront takes a contiguous range of 4-word groups and each lane one
@@ -665,7 +671,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
         if (h >= H) break;
         const uint32_t cl = (rcl[j][h >> 1] >> (16 * (h & 1))) & 0xFFFFu;
         const uint32_t cbk = s_cbkt[cl], bits = cbk >> 24;
-        const uint32_t b = (cbk & 0xFFFFFF) + (bits ? (pr[j][h] >> (32 - bits)) : 0u);
+        const uint32_t b = (cbk & 0xFFFFFF) + top_bits(pr[j][h], bits);
         atomicAdd(&bst[(uint32_t)h < hops ? b + 1 : NBT + 2 + lane], 1u);
       }
     }
@@ -701,7 +707,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
         if (h >= 4) cw = rcl[j][2];
         const uint32_t cl = (h & 1) ? (cw >> 16) : (cw & 0xFFFF);
         const uint32_t cbk = s_cbkt[cl], ci = s_cinfo[cl], bits = cbk >> 24;
-        const uint32_t b = (cbk & 0xFFFFFF) + (bits ? (pv >> (32 - bits)) : 0u);
+        const uint32_t b = (cbk & 0xFFFFFF) + top_bits(pv, bits);
         const uint32_t gp = atomicAdd(&bst[act ? b + 1 : NBT + 2 + lane], 1u);
         if (act) {
           e64[gp - lb0] = ((uint64_t)pv << 32) | (uint32_t)(tid + NT * j) | ((ci & 0xFFFFu) << cb);
@@ -930,7 +936,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       a.valid[i] = (uint8_t)!any_unrouted;
     }
     // the next candidate's bucket counters (the last level's ordering is done)
-    for (uint32_t j = tid; j <= NBT; j += NT) bst[j + 1] = 0;
+    for (uint32_t j = tid; j < (NBT + 4) / 4; j += NT) ((uint4 *)(bst + 1))[j] = make_uint4(0u, 0u, 0u, 0u);
     __syncthreads();
   }
 }
