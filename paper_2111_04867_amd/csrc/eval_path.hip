@@ -699,12 +699,26 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       for (int j = 0; j < CPT; j++) {
         const uint32_t h = (rw0[j] >> (8 + 3 * L)) & 7;  // 7: no hop at this level
         const bool act = h < (uint32_t)kFastMaxHops;
-        uint32_t cw = rcl[j][0], pv = pr[j][0];
+        // hop h's class and priority. With several chunks per thread: its
+        // pair of hops (h >> 1), then the half (h & 1), with three shared
+        // conditions; with one, a select per hop (measured faster there)
+        static_assert(kFastMaxHops == 6, "three pairs of hops");
+        uint32_t cw, pv;
+        if constexpr (CPT >= 2) {
+          const bool c2 = h >= 2, c4 = h >= 4, odd = (h & 1) != 0;
+          cw = c4 ? rcl[j][2] : c2 ? rcl[j][1] : rcl[j][0];
+          const uint32_t pe = c4 ? pr[j][4] : c2 ? pr[j][2] : pr[j][0];
+          const uint32_t po = c4 ? pr[j][5] : c2 ? pr[j][3] : pr[j][1];
+          pv = odd ? po : pe;
+        } else {
+          cw = rcl[j][0];
+          pv = pr[j][0];
 #pragma unroll
-        for (int t = 1; t < kFastMaxHops; t++)
-          if (h == (uint32_t)t) pv = pr[j][t];
-        if (h >= 2) cw = rcl[j][1];
-        if (h >= 4) cw = rcl[j][2];
+          for (int t = 1; t < kFastMaxHops; t++)
+            if (h == (uint32_t)t) pv = pr[j][t];
+          if (h >= 2) cw = rcl[j][1];
+          if (h >= 4) cw = rcl[j][2];
+        }
         const uint32_t cl = (h & 1) ? (cw >> 16) : (cw & 0xFFFF);
         const uint32_t cbk = s_cbkt[cl], ci = s_cinfo[cl], bits = cbk >> 24;
         const uint32_t b = (cbk & 0xFFFFFF) + top_bits(pv, bits);
