@@ -554,12 +554,13 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
   const int C = a.C, E = a.E, H = a.H, nlev = a.nlev;
   const uint32_t NBT = (uint32_t)a.nb_total;
 
-  uint32_t *s_cost = (uint32_t *)(lds + a.o_fcost);
+  // per link: {busy time, cost}, one 8-byte read in the timing pass
+  uint2 *lfc = (uint2 *)(lds + a.o_flfree);
+  uint32_t *lnext = (uint32_t *)(lds + a.o_fnext);  // busy time after this level
   uint32_t *s_cinfo = (uint32_t *)(lds + a.o_fcinfo);
   uint32_t *s_cbkt = (uint32_t *)(lds + a.o_fcbkt);
   uint32_t *s_lfb = (uint32_t *)(lds + a.o_flcb);    // [nlev+1] first bucket of a level
   uint32_t *ctime = (uint32_t *)(lds + a.o_fctime);  // a chunk's arrival so far
-  uint32_t *lfree = (uint32_t *)(lds + a.o_flfree);  // [2][E]: busy time, next
   // bucket cursors over all levels: bst[0] = 0 and bst[b + 1] holds bucket
   // b's count, then its start, then (once its level's sends are placed)
   // its end, so bucket b spans [bst[b], bst[b + 1]) from then on; one dummy
@@ -580,7 +581,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
   uint32_t *red = (uint32_t *)(lds + a.o_fred);      // [2][NT/64] scan scratch
   uint8_t *s_merge = lds + a.o_fmerge;  // links that carry contiguous transfers
   for (int j = tid; j < E; j += NT) {
-    s_cost[j] = a.cost[j];
+    lfc[j].y = a.cost[j];
     s_merge[j] = a.contig ? a.lmerge[j] : 0;
   }
   for (int j = tid; j < a.ncls; j += NT) {
@@ -657,8 +658,8 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       }
     }
     for (int l = tid; l < E; l += NT) {
-      lfree[l] = 0;
-      lfree[E + l] = kUnset;
+      lfc[l].x = 0;
+      lnext[l] = kUnset;
     }
     // ---- A. every send of every level per bucket ----------------------------
     // Straight-line code: a hop past the route counts on the lane's dummy
@@ -687,9 +688,9 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       // busy times after the previous level (a link without a send there
       // keeps its time)
       for (int l = tid; l < E; l += NT) {
-        const uint32_t nx = lfree[E + l];
-        if (nx != kUnset) lfree[l] = nx;
-        lfree[E + l] = kUnset;
+        const uint32_t nx = lnext[l];
+        if (nx != kUnset) lfc[l].x = nx;
+        lnext[l] = kUnset;
       }
       // ---- C. place the level's sends ----------------------------------------
       // Straight-line code (selects, and the lane's dummy counter for a slot
@@ -804,8 +805,9 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
       for (int q = 0; q < EP; q++) {
         const uint32_t l = (pis[q] >> cb) & lmask;
         ct[q] = ctime[pis[q] & cmask];
-        cs[q] = s_cost[l];
-        lf[q] = lfree[l];
+        const uint2 w = lfc[l];
+        cs[q] = w.y;
+        lf[q] = w.x;
       }
       // this thread's positions: segmented running maxima s[q]
       const uint32_t nv = tot > x0 ? min(epr, tot - x0) : 0u;  // valid positions
@@ -907,7 +909,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
                   g0 = y;
                 }
               }
-              lfree[E + l] = F;
+              lnext[l] = F;
             }
             continue;
           }
@@ -918,7 +920,7 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
           ctime[c] = f;
           mk = max(mk, f);
           const uint32_t nk = ((uint32_t)q + 1 < epr ? pis[q < EP - 1 ? q + 1 : q] : nxt0) >> kb;
-          if (x + 1 == tot || nk == 0) lfree[E + l] = f;  // last send of the link's run
+          if (x + 1 == tot || nk == 0) lnext[l] = f;  // last send of the link's run
         }
       }
       };
@@ -968,13 +970,13 @@ int32_t path_fast_layout(const taccl_plan &p, PathArgs &a) {
   };
   a.ncls = p.ncls;
   a.nb_total = p.nb_total;
-  a.o_fcost = take(4 * E);
+  a.o_fnext = take(4 * E);
   a.o_fmerge = take(E);
   a.o_fcinfo = take(4 * std::max(p.ncls, 1));
   a.o_fcbkt = take(4 * std::max(p.ncls, 1));
   a.o_flcb = take(4 * (p.nlev + 1));
   a.o_fctime = take(4 * C);
-  a.o_flfree = take(8 * E);
+  a.o_flfree = take(8 * E);  // {busy time, cost} per link
   // three words of padding, a zero, the bucket cursors of all levels, the
   // total, and one dummy counter per lane of a wavefront (slots without a
   // send count there)

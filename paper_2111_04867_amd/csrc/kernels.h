@@ -91,7 +91,7 @@ struct PathArgs {
   int32_t ncls, nb_total;
   const uint32_t *arec, *cpath, *cinfo, *cbkt;
   int32_t o_faux;
-  int32_t o_fcost, o_fcinfo, o_fcbkt, o_flcb, o_fctime, o_flfree, o_fbcnt, o_fepr, o_fsrt, o_fred;
+  int32_t o_fnext, o_fcinfo, o_fcbkt, o_flcb, o_fctime, o_flfree, o_fbcnt, o_fepr, o_fsrt, o_fred;
   int32_t lds_bytes;
   int32_t cbits, lbits;  // chunk and link fields of a packed sorted send
   // contiguous transfers on links between nodes (contig != 0)
