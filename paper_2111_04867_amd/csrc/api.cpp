@@ -235,6 +235,7 @@ taccl_status_t taccl_eval_batch(taccl_plan_t p, int64_t n, const uint8_t *d_rout
     a.cls2_link = t->cls2_link;
     a.arec = t->arec;
     a.cpath = t->cpath;
+    a.routes_words = (p->route_stride % 4 == 0) && (((uintptr_t)d_routes & 3) == 0);
     a.cinfo = t->cinfo;
     a.cbkt = t->cbkt;
     const int cpt = p->path_fast ? path_fast_cpt(*p) : 0;

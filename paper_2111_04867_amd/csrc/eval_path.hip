@@ -601,11 +601,23 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
   // of independent loads). The next candidate's batch is issued as soon as
   // the last level has taken what it needs from these registers, so its
   // HBM latency overlaps that level's ordering and timing.
+  // kk[j]: the chunk's route byte at bits 8 * (chunk & 3) (the aligned
+  // word that holds it, or the byte moved there)
   uint32_t pr[CPT][kFastMaxHops], kk[CPT], cp[CPT];
+  // Branch-free loads, so that no loaded value meets a select or a
+  // zero-extension before it is used and the batch stays in flight: past
+  // the batch the last candidate is read again, past the chunks the last
+  // chunk (never used); hops past the plan's longest route are skipped (a
+  // uniform branch) and keep stale values, which no route reads.
+#pragma unroll
+  for (int j = 0; j < CPT; j++)
+#pragma unroll
+    for (int h = 0; h < kFastMaxHops; h++) pr[j][h] = 0;
   auto load_inputs = [&](int64_t i) {
-    if (i >= a.n) return;
-    const uint8_t *grt = a.routes + (size_t)i * a.route_stride;
-    const uint32_t *gpr = a.prio + (size_t)i * a.prio_stride;
+    const int64_t ii = i < a.n ? i : a.n - 1;
+    const uint8_t *grt = a.routes + (size_t)ii * a.route_stride;
+    const uint32_t *grw = (const uint32_t *)grt;  // when routes_words
+    const uint32_t *gpr = a.prio + (size_t)ii * a.prio_stride;
     // the thread index is hidden from the optimiser, so per-chunk addresses
     // are recomputed instead of being hoisted out of the candidate loop and
     // spilled
@@ -613,17 +625,17 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
     asm volatile("" : "+v"(tv));
 #pragma unroll
     for (int j = 0; j < CPT; j++) {
-      const int c = tv + NT * j;
-      kk[j] = 0;
-      cp[j] = 0;
-      if (c < C) {
-        kk[j] = grt[c];
-        cp[j] = a.cpath[c];
-        // one address per chunk; the hops are immediate offsets from it
-        const uint32_t *row = gpr + __umul24((uint32_t)c, (uint32_t)H);
+      const uint32_t cc = (uint32_t)min(tv + NT * j, C - 1);
+      if (a.routes_words)
+        kk[j] = grw[cc >> 2];
+      else
+        kk[j] = (uint32_t)grt[cc] << (8 * (cc & 3));
+      cp[j] = a.cpath[cc];
+      // one address per chunk; the hops are immediate offsets from it
+      const uint32_t *row = gpr + __umul24(cc, (uint32_t)H);
 #pragma unroll
-        for (int h = 0; h < kFastMaxHops; h++) pr[j][h] = h < H ? row[h] : 0u;
-      }
+      for (int h = 0; h < kFastMaxHops; h++)
+        if (h < H) pr[j][h] = row[h];
     }
   };
   load_inputs(blockIdx.x);
@@ -634,28 +646,24 @@ __global__ __launch_bounds__(NT) void path_eval_fast(PathArgs a) {
     // rw0: hop count | level -> hop index << 8 (3 bits per level, 7 = none)
     uint32_t rw0[CPT], rcl[CPT][3];
     bool unrouted = false;
-    // second batch: the chosen route records
+    // second batch: the chosen route records, one unconditional load per
+    // chunk (record 0, without hops, for a chunk that has no route or no
+    // chunk at all)
 #pragma unroll
     for (int j = 0; j < CPT; j++) {
       const int c = tv + NT * j;
-      rw0[j] = 0xFFFFFFu << 8;
-      rcl[j][0] = rcl[j][1] = rcl[j][2] = 0;
-      if (c < C) {
-        const uint32_t np = cp[j] >> 24;
-        if (cp[j] == kNoRoute) unrouted = true;  // no route option at all: never delivered
-        if (np) {
-          if (kk[j] < np) {
-            const uint4 r = ((const uint4 *)a.arec)[(cp[j] & 0xFFFFFFu) + kk[j]];
-            rw0[j] = r.x;
-            rcl[j][0] = r.y;
-            rcl[j][1] = r.z;
-            rcl[j][2] = r.w;
-          } else {
-            unrouted = true;  // the pair is left unrouted
-          }
-        }
-        ctime[c] = 0;
-      }
+      const uint32_t np = cp[j] >> 24;
+      const bool live = c < C;
+      const uint32_t k = (kk[j] >> (8 * ((uint32_t)c & 3u))) & 0xFFu;  // the route choice
+      // no route option at all, or the pair left unrouted: never delivered
+      if (live && (cp[j] == kNoRoute || (np && k >= np))) unrouted = true;
+      const uint32_t rec = (live && k < np) ? (cp[j] & 0xFFFFFFu) + k : 0u;
+      const uint4 r = ((const uint4 *)a.arec)[rec];
+      rw0[j] = r.x;
+      rcl[j][0] = r.y;
+      rcl[j][1] = r.z;
+      rcl[j][2] = r.w;
+      if (live) ctime[c] = 0;
     }
     for (int l = tid; l < E; l += NT) {
       lfc[l].x = 0;
@@ -1009,7 +1017,7 @@ int path_fast_cpt(const taccl_plan &p) {
     while ((1ull << b) < n) b++;
     return b;
   };
-  if (2 * bits((uint32_t)p.coll.C) + bits((uint32_t)p.topo.E) > 32) return 0;
+  if (p.coll.C < 1 || 2 * bits((uint32_t)p.coll.C) + bits((uint32_t)p.topo.E) > 32) return 0;
   // bucket and link fields are packed into 16 bits
   if (p.nb_total > kFastMaxBuckets || p.topo.E > (1 << 16)) return 0;
   // sorted positions below 2^16 and link costs below 2^24 (24-bit multiplies)

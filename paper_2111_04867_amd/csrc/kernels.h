@@ -89,6 +89,9 @@ struct PathArgs {
   int32_t o_qc, o_ctime, o_lfree, o_ccnt, o_ccur, o_e64, o_ecls, o_sorted, o_red, max_lvl;
   // register-resident kernel
   int32_t ncls, nb_total;
+  // route_stride a multiple of 4 and the routes 4-byte aligned: a chunk's
+  // route byte is read with the aligned word that holds it
+  int32_t routes_words;
   const uint32_t *arec, *cpath, *cinfo, *cbkt;
   int32_t o_faux;
   int32_t o_fnext, o_fcinfo, o_fcbkt, o_flcb, o_fctime, o_flfree, o_fbcnt, o_fepr, o_fsrt, o_fred;

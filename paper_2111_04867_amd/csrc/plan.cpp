@@ -476,13 +476,16 @@ static taccl_status_t build_levels(taccl_plan *p) {
 
   // compact tables of the register-resident kernel (paths of <= 6 hops,
   // <= 8 levels, <= 2^24 route options)
-  p->path_fast = !p->ports && p->H <= kFastMaxHops && p->nlev <= 8 && npath < (1u << 24) &&
+  p->path_fast = !p->ports && p->H <= kFastMaxHops && p->nlev <= 8 && npath + 1 < kNoRoute &&
                  p->coll.C <= kFastMaxChunks;
   if (p->path_fast) {
-    p->arec.assign(npath * 4, 0);
+    // record 0 has no hops (what a chunk without a route loads); option q's
+    // record is record q + 1
+    p->arec.assign((npath + 1) * 4, 0);
+    p->arec[0] = 0xFFFFFFu << 8;
     for (size_t q = 0; q < npath; q++) {
       if (!used_path[q]) continue;
-      uint32_t *r = &p->arec[q * 4];
+      uint32_t *r = &p->arec[(q + 1) * 4];
       uint64_t rem = p->path_cost[q];
       int32_t h = 0;
       uint32_t hm = 0xFFFFFFu;  // level -> hop, 3 bits per level (7: none)
@@ -502,7 +505,7 @@ static taccl_status_t build_levels(taccl_plan *p) {
       const size_t pp = (size_t)s * P + d;
       // a pair without any route option can never be delivered: marked by
       // an all-ones option index and no options
-      p->cpath[ch] = p->npaths[pp] ? p->pair_base[pp] | ((uint32_t)p->npaths[pp] << 24)
+      p->cpath[ch] = p->npaths[pp] ? (p->pair_base[pp] + 1) | ((uint32_t)p->npaths[pp] << 24)
                                    : kNoRoute;
     }
     // priority sub-buckets per class, sized from the class's expected

@@ -145,8 +145,9 @@ struct taccl_plan {
   std::vector<uint16_t> cls_link;      // [ncls]
   // register-resident Alltoall kernel: per route option {hops | the hop at
   // each level (3 bits per level, 7: none) << 8, classes of hops 0..5 as u16
-  // pairs}; per chunk its pair's
-  // first option | option count << 24 (kNoRoute: the pair has no option);
+  // pairs}, option q at record q + 1 after an empty record 0; per chunk its
+  // pair's first record | option count << 24 (kNoRoute: the pair has no
+  // option);
   // per class link | (first bucket of the same level and link) << 16
   bool path_fast = false;
   std::vector<uint32_t> arec, cpath, cinfo;
