@@ -89,11 +89,10 @@ __global__ __launch_bounds__(NT) __attribute__((
       best2[l] = ~0ull;
     }
     // per chunk: first hop of its option in path_links, hop count, hops
-    // served, time, and the current hop's link, key rank and priority
-    // (one-word keys: the key's constant part, key rank | priority | chunk,
-    // in place of the rank and the priority)
+    // served, time, and the current hop's link, key rank and priority (kept
+    // as loaded: a one-word key is built from them when the next window
+    // needs it, so a commit does not wait for the next hop's loads)
     uint32_t qo[CPT], hops[CPT], cur[CPT], ct[CPT], cl[CPT], kr[CPT], pv[CPT], po[CPT];
-    uint64_t klo[CPT];
     bool bad = false;
     auto load_hop = [&](int j, int c) {
       const uint32_t h = a.mirror ? hops[j] - 1 - cur[j] : cur[j];
@@ -101,17 +100,8 @@ __global__ __launch_bounds__(NT) __attribute__((
       const uint32_t k = a.gkrank[qo[j] + h];
       // a plain LDS read when staged (a run-time choice made this a generic
       // load that waits for both memory counters)
-      const uint32_t pr = kStaged ? sprio[po[j] + h] : gpr[(uint32_t)c * H + h];
-      if (kPack) {
-        // k << kr_shift lies in the high word (kr_shift = chunk_bits + 32);
-        // the priority straddles the two words: 32-bit shifts only
-        const uint32_t cb = (uint32_t)a.chunk_bits;
-        const uint32_t hi = (k << (cb & 31u)) | (cb ? pr >> (32u - cb) : 0u);
-        klo[j] = ((uint64_t)hi << 32) | ((pr << (cb & 31u)) | (uint32_t)c);
-      } else {
-        kr[j] = k;
-        pv[j] = pr;
-      }
+      pv[j] = kStaged ? sprio[po[j] + h] : gpr[(uint32_t)c * H + h];
+      kr[j] = k;
     };
 #pragma unroll
     for (int j = 0; j < CPT; j++) {
@@ -184,11 +174,15 @@ __global__ __launch_bounds__(NT) __attribute__((
       for (int round = 0, buf = 0;; round++, buf ^= 1) {
         uint32_t st[CPT];
         uint32_t wmin = kNone;
-        // the relative start lies in the key's high word (rel_shift >= 32):
-        // a 32-bit shift there instead of a 64-bit one
-        const uint32_t rel_hi = (uint32_t)a.rel_shift - 32u;
+        // the relative start and the key rank lie in the key's high word
+        // (rel_shift, kr_shift >= 32) and the priority straddles the two
+        // words: 32-bit shifts only
+        const uint32_t rel_hi = (uint32_t)a.rel_shift - 32u, cb = (uint32_t)a.chunk_bits;
         auto key_of = [&](int j) {
-          return klo[j] | ((uint64_t)(min(st[j] - wp, a.rel_max) << rel_hi) << 32);
+          const uint32_t hi = (min(st[j] - wp, a.rel_max) << rel_hi) | (kr[j] << (cb & 31u)) |
+                              (cb ? pv[j] >> (32u - cb) : 0u);
+          const uint32_t lo = (pv[j] << (cb & 31u)) | (uint32_t)(tid + NT * j);
+          return ((uint64_t)hi << 32) | lo;
         };
 #pragma unroll
         for (int j = 0; j < CPT; j++) {
