@@ -473,8 +473,8 @@ hipError_t launch_path(const PathArgs &a, int grid, hipStream_t stream) {
 // Register-resident Alltoall kernel (paths of <= 6 hops, <= 8 levels,
 // <= 4096 chunks). One block of NT threads evaluates one candidate at a
 // time. Thread t owns chunks t, t+NT, ...: their route option's record (hop
-// count, level and class of every hop) and the priorities of their hops are
-// loaded once into registers. Per candidate:
+// count, the hop at each level, the class of every hop) and the priorities
+// of their hops are loaded once into registers. Per candidate:
 //   A. count every send of every level per (class, top priority bits)
 //      bucket (buckets are numbered level by level; within a level classes
 //      are ordered by link, then travelled cost, so a link's sends form one

@@ -475,7 +475,7 @@ static taccl_status_t build_levels(taccl_plan *p) {
   }
 
   // compact tables of the register-resident kernel (paths of <= 6 hops,
-  // <= 8 levels, <= 2^24 route options)
+  // <= 8 levels, fewer than 2^24 - 2 route options)
   p->path_fast = !p->ports && p->H <= kFastMaxHops && p->nlev <= 8 && npath + 1 < kNoRoute &&
                  p->coll.C <= kFastMaxChunks;
   if (p->path_fast) {
